@@ -1,0 +1,626 @@
+"""Plain fp64 CPU oracle of the GMC boundary operator.
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the
+benchmark's CPU-baseline leg may import this module.  The product path (the
+HIP library and its Python binding) never calls it, and it shares no code,
+table or helper with that path.
+
+It follows the paper ("Messages, Not Tokens: Grounded Coresets for Faithful
+VLM Compression") step by step, in its notation, in float64:
+
+  budget          Sec. 3.1 problem formulation; App. H "Batched complementary
+                  support" (totality rule)
+  message         Sec. 3.2; App. H Eq. cond-native-message,
+                  Eq. cond-mass-coordinate, Eq. cond-grounded-client
+  head weights    App. H Eq. cond-head-pattern, Eq. cond-head-weight
+  banks           Sec. 3.2; App. H Eq. cond-aux-clients, Eq. cond-coverage,
+                  Eq. cond-effective-bank-mass
+  selection       Sec. 3.3 Eq. coverage, Eq. responsibility;
+                  App. H Eq. cond-responsibility
+  certificates    Prop. 1 Eq. deployed-approximation; App. I
+                  Eq. cond-final-cert, Eq. cond-bank-mixture
+  assignment      Sec. 3.4; App. H Eq. cond-assignment,
+                  Eq. cond-population-gate
+  transport       Sec. 3.4 Eq. transport; App. H Eq. cond-transport,
+                  Eq. cond-grounded-energy
+  compaction      App. H "Index map and physical token accounting"
+
+Readings where the paper is silent are listed in ``READINGS`` and in the
+design notes; each is a named constant below.  Pins against the paper's
+identities, bounds, special cases and brute force live in tests/.
+
+Parity status: every function here is pinned by at least one test except the
+exact index choices of the batched responsibility heuristic on generic data,
+which the paper fixes only through its rules (no printed toy instance):
+for those, "parity unpinned" beyond the brute-force bounds, the b=1 greedy
+special case and the zero-gain fill order.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Optional
+
+import numpy as np
+
+__all__ = [
+    "GmcParams", "READINGS", "realized_budget", "row_features", "value_probe",
+    "mass_coordinate", "native_attention", "grounded_energy_rows",
+    "query_weights", "head_pattern_gram", "head_weights", "grounded_energy",
+    "appearance_bank", "appearance_bank_bounded", "spatial_coordinates",
+    "spatial_bank", "client_matrix", "coverage", "marginal_gains",
+    "responsibility_scores", "top_by_score", "select_support",
+    "assignment_gaps", "separability_gate", "ambiguity_gate",
+    "assign_population", "population_weights", "transport", "compact",
+    "gmc_single", "gmc", "prune_rounds",
+]
+
+
+@dataclasses.dataclass(frozen=True)
+class GmcParams:
+    """Frozen settings (App. H, Table cond-config) plus the readings below."""
+    probe_rank: int = 4
+    lambda_mass: float = 1.0
+    eps_mass: float = 1e-8
+    beta_msg: float = 1.0          # reading R1
+    beta_app: float = 0.5
+    beta_spa: float = 0.25
+    tau_v: float = 0.2
+    tau_s: float = 0.02
+    landmarks: int = 16
+    batch_b: int = 16
+    pool_mult: int = 4
+    tau_r: float = 0.1
+    resp_eps: float = 1e-30        # reading R9
+    spatial_w: float = 0.5
+    gate_t: float = 0.08
+    gate_p: float = 8.0
+    amb_margin: float = 0.05       # reading R5
+    amb_p: float = 8.0             # reading R5
+    g_form: str = "smooth"         # reading R5 ("smooth" | "hard")
+    pop_strength: float = 0.5
+    tau_j: float = 1.0             # reading R10
+    max_head_clusters: int = 4
+    disp_eps: float = 0.05
+    terminal_q_weight: float = 2.0
+    rms_eps: float = 1e-6          # reading R4
+    norm_eps: float = 1e-12        # reading R9
+    restore_eps: float = 1e-6      # reading R9
+    bounded_threshold_n: int = 4096  # reading R8
+    app_rank: int = 128
+    app_max_clients: int = 4096
+    batch_b_bounded: int = 512
+
+
+READINGS = {
+    "R1": "grounded (message) bank mass beta_msg = 1: current+history masses "
+          "0.5+0.5; with no history view supplied the current view carries both",
+    "R2": "grounded row (h,t) weight = beta_msg * omega_h * nu_t * a_(h,t); "
+          "reduces to beta/M * a_m for uniform omega and nu; nu_t is not used in "
+          "head patterns",
+    "R3": "native nonvisual softmax denominator enters as an optional per-(h,t) "
+          "log-sum-exp; P^G is invariant to it",
+    "R4": "value path folded into a per-head probe G_h [r][d]; x~ = RMSNorm(h) "
+          "with eps 1e-6 and unit gain",
+    "R5": "local ambiguity g_i = exp(-(delta_i/0.05)^8) (hard variant: "
+          "1[delta_i < 0.05])",
+    "R6": "spatial coordinates are grid-cell centres in [0,1]^2 from (h,w); "
+          "the temporal id is not a spatial coordinate but is kept in out_pos",
+    "R7": "one image per problem (I = 1); frames of one clip are one image",
+    "R8": "bounded appearance bank iff N > 4096, with b = 512",
+    "R9": "epsilons: responsibility 1e-30, normalisation 1e-12, RMS restore 1e-6",
+    "R10": "transport blend tau_j = 1 (appendix form R_j(c_j))",
+    "R11": "pool = top-min(4b, N-|S|) unselected tokens; last batch K-|S|",
+    "R12": "farthest-first picks min(4, active heads) centres; ties to the "
+           "earliest centre; empty clusters are dropped",
+    "R13": "ties in every ranking go to the lower source index",
+}
+
+
+# ----------------------------------------------------------------------------
+# Budget (Sec. 3.1 problem formulation; App. H totality rule)
+# ----------------------------------------------------------------------------
+def realized_budget(n: int, k_req: int, n_images: int = 1) -> int:
+    """K = min{N, max{K_r, I}}."""
+    return int(min(n, max(k_req, n_images)))
+
+
+# ----------------------------------------------------------------------------
+# Boundary features
+# ----------------------------------------------------------------------------
+def row_features(h: np.ndarray, p: GmcParams):
+    """Norms, unit directions x_i = h_i/max(||h_i||, eps) (App. H assignment),
+    RMS values, and the next block's RMSNorm x~_i (unit gain, reading R4)."""
+    h = np.asarray(h, dtype=np.float64)
+    norm = np.sqrt(np.sum(h * h, axis=1))
+    x = h / np.maximum(norm, p.norm_eps)[:, None]
+    ms = np.mean(h * h, axis=1)
+    rms = np.sqrt(ms)
+    xt = h / np.sqrt(ms + p.rms_eps)[:, None]
+    return norm, x, rms, xt
+
+
+def value_probe(xt: np.ndarray, probe: np.ndarray) -> np.ndarray:
+    """Z_h = (V_h O_h) P as one folded per-head map: Z[h][i][c] = x~_i . G[h][c]."""
+    return np.einsum("nd,hrd->hnr", xt, np.asarray(probe, np.float64))
+
+
+def mass_coordinate(z: np.ndarray, p: GmcParams) -> np.ndarray:
+    """sigma_h = sqrt(lambda_mass) max{||Z_h||_F / sqrt(N r), eps_mass}
+    (Eq. mass-coordinate / cond-mass-coordinate)."""
+    hq, n, r = z.shape
+    fro = np.sqrt(np.sum(z * z, axis=(1, 2)))
+    return math.sqrt(p.lambda_mass) * np.maximum(fro / math.sqrt(n * r), p.eps_mass)
+
+
+def native_attention(q: np.ndarray, k: np.ndarray, nonvis_lse: Optional[np.ndarray] = None):
+    """Visual-column slice of the native softmax (Eq. cond-native-message).
+
+    q [T][Hq][dh], k [N][Hkv][dh]; head h reads kv head floor(h*Hkv/Hq).
+    The denominator combines the visual logits with an optional nonvisual
+    log-sum-exp per (h,t) (reading R3).  Returns A [Hq][T][N].
+    """
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    t, hq, dh = q.shape
+    n, hkv, _ = k.shape
+    a = np.empty((hq, t, n))
+    for h in range(hq):
+        g = (h * hkv) // hq
+        s = q[:, h, :] @ k[:, g, :].T / math.sqrt(dh)          # [T][N]
+        mx = s.max(axis=1, keepdims=True)
+        lse = mx[:, 0] + np.log(np.sum(np.exp(s - mx), axis=1))
+        if nonvis_lse is not None:
+            lse = np.logaddexp(lse, np.asarray(nonvis_lse, np.float64)[h])
+        a[h] = np.exp(s - lse[:, None])
+    return a
+
+
+def grounded_energy_rows(a: np.ndarray, z: np.ndarray, sigma: np.ndarray):
+    """Atom norms e_(h,t,i) = ||u_i^(h,t)|| with u = A[t,i][Z_h[i]; sigma_h]
+    (Eq. grounded-client).  Returns e [Hq][T][N] and l [Hq][N] = ||w_h[i]||."""
+    ell = np.sqrt(np.sum(z * z, axis=2) + sigma[:, None] ** 2)   # [Hq][N]
+    e = a * ell[:, None, :]
+    return e, ell
+
+
+def query_weights(t: int, p: GmcParams) -> np.ndarray:
+    """nu_t: the terminal prompt query counts terminal_q_weight times the
+    others; normalised to sum one (App. H native message clients)."""
+    if t == 0:
+        return np.zeros(0)
+    w = np.ones(t)
+    w[-1] = p.terminal_q_weight
+    return w / w.sum()
+
+
+def head_pattern_gram(a: np.ndarray, z: np.ndarray, sigma: np.ndarray) -> np.ndarray:
+    """Gamma_hg = <vec U_h, vec U_g> = sum_(t,i) A_h A_g <w_h[i], w_g[i]>,
+    the Gram of the flattened per-head atoms (Eq. cond-head-pattern)."""
+    hq, t, n = a.shape
+    w = np.concatenate([z, np.broadcast_to(sigma[:, None, None], (hq, n, 1))], axis=2)
+    # the (t, i, c) sum grouped as sum_i <w_h[i], w_g[i]> * sum_t A_h[t,i] A_g[t,i]
+    aa = np.einsum("hti,gti->hgi", a, a)                          # [Hq][Hq][N]
+    ww = np.einsum("hic,gic->hgi", w, w)                          # [Hq][Hq][N]
+    return np.sum(aa * ww, axis=2)
+
+
+def head_weights(gram: np.ndarray, mean_atom_norm: np.ndarray, p: GmcParams):
+    """Farthest-first cosine head clustering and inverse-dispersion weights
+    (Eq. cond-head-pattern, Eq. cond-head-weight; reading R12).
+
+    gram: Gamma [Hq][Hq]; mean_atom_norm: average atom norm per head, which
+    sets the pre-normalisation pattern norm sqrt(beta Gamma_hh)/abar_h.
+    Returns (omega [Hq], centres list, cluster id per head (-1 inactive)).
+    """
+    hq = gram.shape[0]
+    diag = np.diag(gram).copy()
+    active = diag > 0
+    omega = np.zeros(hq)
+    assign = -np.ones(hq, dtype=np.int64)
+    n_active = int(active.sum())
+    if n_active == 0:
+        return omega, [], assign
+    nrm = np.sqrt(np.where(active, diag, 1.0))
+    cos = gram / nrm[:, None] / nrm[None, :]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        pre = np.where(active, np.sqrt(p.beta_msg * np.where(active, diag, 0.0))
+                       / np.where(mean_atom_norm > 0, mean_atom_norm, 1.0), -np.inf)
+    centres = [int(np.argmax(pre))]
+    n_c = min(p.max_head_clusters, n_active)
+    while len(centres) < n_c:
+        best, best_val = -1, np.inf
+        for hh in range(hq):
+            if not active[hh] or hh in centres:
+                continue
+            v = max(cos[hh, c] for c in centres)
+            if v < best_val:
+                best, best_val = hh, v
+        centres.append(best)
+    for hh in range(hq):
+        if not active[hh]:
+            continue
+        sims = [cos[hh, c] for c in centres]
+        assign[hh] = int(np.argmax(sims))          # first maximum: earliest centre
+    clusters = [np.flatnonzero(assign == c) for c in range(len(centres))]
+    clusters = [m for m in clusters if m.size > 0]
+    n_clusters = len(clusters)
+    for members in clusters:
+        sub = cos[np.ix_(members, members)]
+        mean_norm = math.sqrt(max(sub.sum(), 0.0))
+        disp = 1.0 - sub.sum(axis=1) / mean_norm        # d_h = 1 - u_h . mu_c
+        inv = 1.0 / (disp + p.disp_eps)
+        omega[members] = inv / inv.sum() / n_clusters
+    return omega, centres, assign
+
+
+def grounded_energy(e: np.ndarray, omega: np.ndarray, nu: np.ndarray):
+    """e_i = (sum_h omega_h ||r_i^(h,.)||^2)^(1/2), r = sqrt(nu_t) u, and
+    ebar_i = e_i / mean_j e_j with the uniform fallback ebar = 1
+    (Eq. cond-grounded-energy)."""
+    hq, t, n = e.shape
+    if t == 0:
+        return np.ones(n), np.zeros(n)
+    per_head = np.einsum("t,htn->hn", nu, e * e)
+    en = np.sqrt(np.einsum("h,hn->n", omega, per_head))
+    mean = en.mean()
+    if not mean > 0:
+        return np.ones(n), en
+    return en / mean, en
+
+
+# ----------------------------------------------------------------------------
+# Auxiliary banks (Eq. cond-aux-clients)
+# ----------------------------------------------------------------------------
+def _row_softmax(logits: np.ndarray) -> np.ndarray:
+    mx = logits.max(axis=1, keepdims=True)
+    ex = np.exp(logits - mx)
+    return ex / ex.sum(axis=1, keepdims=True)
+
+
+def appearance_bank(x: np.ndarray, p: GmcParams) -> np.ndarray:
+    """P^V_m(i) = softmax_i(x_m . x_i / tau_v), one client per token."""
+    return _row_softmax((x @ x.T) / p.tau_v)
+
+
+def appearance_bank_bounded(h: np.ndarray, proj: np.ndarray, p: GmcParams):
+    """Long-prefix bank: states projected by the fixed +-1 matrix, normalised,
+    and at most M_V uniformly spaced clients m_k = floor(k N / M_V)."""
+    n = h.shape[0]
+    y = np.asarray(h, np.float64) @ np.asarray(proj, np.float64).T
+    y = y / np.maximum(np.sqrt(np.sum(y * y, axis=1)), p.norm_eps)[:, None]
+    mv = min(p.app_max_clients, n)
+    clients = (np.arange(mv) * n) // mv
+    return _row_softmax((y[clients] @ y.T) / p.tau_v), clients
+
+
+def spatial_coordinates(pos: np.ndarray) -> np.ndarray:
+    """Original-grid (h, w) mapped to cell centres in [0,1]^2 (reading R6)."""
+    hh = pos[:, 1].astype(np.float64)
+    ww = pos[:, 2].astype(np.float64)
+    h0, w0 = hh.min(), ww.min()
+    gh, gw = hh.max() - h0 + 1.0, ww.max() - w0 + 1.0
+    return np.stack([(hh - h0 + 0.5) / gh, (ww - w0 + 0.5) / gw], axis=1)
+
+
+def spatial_bank(pos: np.ndarray, p: GmcParams) -> np.ndarray:
+    """P^S_ab(i) = softmax_i(-||p_i - l_ab||^2 / tau_s) around the L x L
+    landmarks l_ab = ((a+.5)/L, (b+.5)/L); row index a*L + b."""
+    pc = spatial_coordinates(pos)
+    grid = (np.arange(p.landmarks) + 0.5) / p.landmarks
+    la, lb = np.meshgrid(grid, grid, indexing="ij")
+    land = np.stack([la.ravel(), lb.ravel()], axis=1)
+    d2 = np.sum((land[:, None, :] - pc[None, :, :]) ** 2, axis=2)
+    return _row_softmax(-d2 / p.tau_s)
+
+
+# ----------------------------------------------------------------------------
+# Client matrix (Eq. cond-coverage) and coverage objective (Eq. coverage)
+# ----------------------------------------------------------------------------
+def client_matrix(pg: np.ndarray, active: np.ndarray, omega: np.ndarray, nu: np.ndarray,
+                  pv: np.ndarray, ps: np.ndarray, p: GmcParams):
+    """Stack the three banks into Cbar [M][N] with preweights.
+
+    Grounded row (h,t): beta_msg omega_h nu_t a_(h,t) P^G (reading R2);
+    appearance row: beta_app / M_V P^V; spatial row: beta_spa / M_S P^S.
+    Returns Cbar and the bank id of every row (0 grounded, 1 appearance,
+    2 spatial).
+    """
+    hq, t, n = pg.shape
+    rows, banks = [], []
+    if t > 0:
+        wg = p.beta_msg * omega[:, None] * nu[None, :] * active
+        rows.append((wg[:, :, None] * pg).reshape(hq * t, n))
+        banks.append(np.zeros(hq * t, dtype=np.int64))
+    rows.append(p.beta_app / pv.shape[0] * pv)
+    banks.append(np.ones(pv.shape[0], dtype=np.int64))
+    rows.append(p.beta_spa / ps.shape[0] * ps)
+    banks.append(np.full(ps.shape[0], 2, dtype=np.int64))
+    return np.concatenate(rows, axis=0), np.concatenate(banks)
+
+
+def coverage(cbar: np.ndarray, support) -> float:
+    """F(S) = sum_m max_(i in S) Cbar_mi, F(empty) = 0."""
+    s = np.asarray(list(support), dtype=np.int64)
+    if s.size == 0:
+        return 0.0
+    return float(cbar[:, s].max(axis=1).sum())
+
+
+def marginal_gains(cbar: np.ndarray, cov: np.ndarray) -> np.ndarray:
+    """u_i = sum_m [Cbar_mi - b_m]_+ with b_m the current coverage maxima."""
+    return np.maximum(cbar - cov[:, None], 0.0).sum(axis=0)
+
+
+def responsibility_scores(cbar: np.ndarray, cov: np.ndarray, pool: np.ndarray,
+                          p: GmcParams) -> np.ndarray:
+    """s_i = sum_m rho_mi R_mi over the pool, with rho the pool softmax of
+    R_mi / (tau_r max_(j in pool) R_mj + eps) (Eq. cond-responsibility)."""
+    r = np.maximum(cbar[:, pool] - cov[:, None], 0.0)          # [M][|pool|]
+    mu = r.max(axis=1, keepdims=True)
+    rho = _row_softmax(r / (p.tau_r * mu + p.resp_eps))
+    return np.sum(rho * r, axis=0)
+
+
+def top_by_score(score: np.ndarray, cand: np.ndarray, count: int) -> np.ndarray:
+    """The `count` candidates with the largest score; equal scores go to the
+    lower source index (reading R13).  Returned in rank order."""
+    cand = np.asarray(cand, dtype=np.int64)
+    order = np.lexsort((cand, -score))
+    return cand[order[:count]]
+
+
+def _cut_margin(sorted_vals: np.ndarray, count: int) -> float:
+    """Relative gap at a cut, (v_(count) - v_(count+1)) / v_(1); an exact
+    zero-zero cut is resolved by index and counts as infinite."""
+    if count >= sorted_vals.size or count == 0:
+        return math.inf
+    a, b = sorted_vals[count - 1], sorted_vals[count]
+    if a == 0.0 and b == 0.0:
+        return math.inf
+    top = sorted_vals[0]
+    return (a - b) / top if top > 0 else math.inf
+
+
+def select_support(cbar: np.ndarray, k: int, b: int, p: GmcParams, seed_set=()):
+    """Batched responsibility selection (Sec. 3.3; Eq. cond-responsibility).
+
+    Rounds until |S| = K: residual gains over unselected tokens, a pool of the
+    min(pool_mult*b, N-|S|) best gains, responsibility scores over the pool,
+    the min(b, K-|S|) best scores enter together, then the coverage maxima are
+    refreshed.  Zero-gain tokens then fill in source order automatically.
+
+    Returns dict with the support in selection order, per-round pools and
+    batches, the certificate factors q_t (Prop. 1) and the decision margins.
+    """
+    m, n = cbar.shape
+    cov = np.zeros(m)
+    chosen = np.zeros(n, dtype=bool)
+    order = []
+    for j in seed_set:
+        chosen[j] = True
+        order.append(int(j))
+        cov = np.maximum(cov, cbar[:, j])
+    f0 = float(cov.sum())
+    rounds = []
+    while len(order) < k:
+        cand = np.flatnonzero(~chosen)
+        u_all = marginal_gains(cbar, cov)
+        u = u_all[cand]
+        psize = min(p.pool_mult * b, cand.size)
+        pool = top_by_score(u, cand, psize)
+        u_sorted = np.sort(u)[::-1]
+        s = responsibility_scores(cbar, cov, pool, p)
+        bsize = min(b, k - len(order))
+        batch = top_by_score(s, pool, bsize)
+        s_sorted = np.sort(s)[::-1]
+        # certificate factor q_t = [F(S u B) - F(S)] / U_t, U_t = K largest u
+        u_top = float(u_sorted[:k].sum())
+        new_cov = np.maximum(cov, cbar[:, batch].max(axis=1))
+        gain = float(new_cov.sum() - cov.sum())
+        q = gain / u_top if u_top > 0 else 0.0
+        rounds.append(dict(pool=np.sort(pool), batch=batch, u=u_all.copy(),
+                           s=dict(zip(pool.tolist(), s.tolist())), q=q, gain=gain,
+                           u_top=u_top,
+                           pool_margin=_cut_margin(u_sorted, psize),
+                           batch_margin=_cut_margin(s_sorted, bsize)))
+        chosen[batch] = True
+        order.extend(int(j) for j in batch)
+        cov = new_cov
+    c_b = 1.0 - float(np.prod([1.0 - r["q"] for r in rounds])) if rounds else 0.0
+    return dict(order=np.array(order, dtype=np.int64), rounds=rounds, cov=cov,
+                f_s=float(cov.sum()), f0=f0, c_b=c_b)
+
+
+# ----------------------------------------------------------------------------
+# Population assignment (Sec. 3.4; Eq. cond-assignment, cond-population-gate)
+# ----------------------------------------------------------------------------
+def assignment_gaps(x: np.ndarray, support: np.ndarray):
+    """cos_ij = x_i . x_j for j in S and delta_i = best - second best
+    (delta = 0 when S has one member)."""
+    cos = x @ x[support].T                                      # [N][K]
+    if support.size < 2:
+        return cos, np.zeros(x.shape[0])
+    top2 = -np.sort(-cos, axis=1)[:, :2]
+    return cos, top2[:, 0] - top2[:, 1]
+
+
+def separability_gate(delta: np.ndarray, discarded: np.ndarray, p: GmcParams) -> float:
+    """s_x = 1 - exp[-(mean_(i discarded) delta_i / t)^p]; mean 0 when none."""
+    dbar = float(delta[discarded].mean()) if discarded.any() else 0.0
+    return 1.0 - math.exp(-((dbar / p.gate_t) ** p.gate_p)), dbar
+
+
+def ambiguity_gate(delta: np.ndarray, p: GmcParams) -> np.ndarray:
+    """Local ambiguity g_i from the selected-cosine gap (reading R5)."""
+    if p.g_form == "hard":
+        return (delta < p.amb_margin).astype(np.float64)
+    return np.exp(-((delta / p.amb_margin) ** p.amb_p))
+
+
+def assign_population(x: np.ndarray, pc: np.ndarray, support: np.ndarray, p: GmcParams):
+    """pi(i) = argmax_(j in S) cos_ij + 0.5 s_x g_i exp(-||p_i - p_j||^2/tau_s);
+    ties to the lower source index; selected tokens represent themselves."""
+    n = x.shape[0]
+    sup = np.sort(np.asarray(support, dtype=np.int64))
+    cos, delta = assignment_gaps(x, sup)
+    discarded = np.ones(n, dtype=bool)
+    discarded[sup] = False
+    sx, dbar = separability_gate(delta, discarded, p)
+    g = ambiguity_gate(delta, p)
+    d2 = np.sum((pc[:, None, :] - pc[sup][None, :, :]) ** 2, axis=2)
+    kappa = cos + p.spatial_w * sx * g[:, None] * np.exp(-d2 / p.tau_s)
+    pi = sup[np.argmax(kappa, axis=1)]                          # first max = lowest index
+    pi[sup] = sup
+    srt = -np.sort(-kappa, axis=1)
+    kmargin = srt[:, 0] - srt[:, 1] if sup.size > 1 else np.full(n, np.inf)
+    kmargin[sup] = np.inf
+    return dict(pi=pi, sx=sx, dbar=dbar, delta=delta, g=g, kappa_margin=kmargin,
+                cos=cos, kappa=kappa, support=sup)
+
+
+# ----------------------------------------------------------------------------
+# Transport (Sec. 3.4 Eq. transport; App. H Eq. cond-transport)
+# ----------------------------------------------------------------------------
+def population_weights(ebar: np.ndarray, sx: float, p: GmcParams) -> np.ndarray:
+    """m_i = (1 - alpha s_x) + alpha s_x ebar_i (Eq. cond-population-gate)."""
+    return (1.0 - p.pop_strength * sx) + p.pop_strength * sx * ebar
+
+
+def transport(h: np.ndarray, pi: np.ndarray, support: np.ndarray, m: np.ndarray, p: GmcParams):
+    """M_j, weighted centroid c_j, blend, and RMS restoration
+    R_j(u) = u rms(h_j) / (rms(u) + eps).  Returns per-support-member arrays
+    in ascending source order, plus the pre-restoration centroids."""
+    h = np.asarray(h, np.float64)
+    sup = np.sort(np.asarray(support, dtype=np.int64))
+    slot = -np.ones(h.shape[0], dtype=np.int64)
+    slot[sup] = np.arange(sup.size)
+    mass = np.zeros(sup.size)
+    acc = np.zeros((sup.size, h.shape[1]))
+    np.add.at(mass, slot[pi], m)
+    np.add.at(acc, slot[pi], m[:, None] * h)
+    cen = acc / mass[:, None]
+    v = (1.0 - p.tau_j) * h[sup] + p.tau_j * cen
+    rms_h = np.sqrt(np.mean(h[sup] ** 2, axis=1))
+    rms_v = np.sqrt(np.mean(v ** 2, axis=1))
+    out = v * (rms_h / (rms_v + p.restore_eps))[:, None]
+    return dict(support=sup, mass=mass, centroid=cen, out=out)
+
+
+def compact(support: np.ndarray, htilde: np.ndarray, pos: np.ndarray):
+    """Stable, order-preserving gather: ascending source indices, their
+    transported states, and their original (t,h,w) ids."""
+    sup = np.asarray(support, dtype=np.int64)
+    order = np.argsort(sup, kind="stable")
+    idx = sup[order]
+    return idx, htilde[order], pos[idx]
+
+
+# ----------------------------------------------------------------------------
+# The whole operator for one image (Algorithm 1, steps 2-6)
+# ----------------------------------------------------------------------------
+def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=None):
+    """Steps 2 of Algorithm 1: the three client banks and all message-side
+    quantities.  Returns a dict of intermediates."""
+    h = np.asarray(h, np.float64)
+    n = h.shape[0]
+    t = q.shape[0]
+    norm, x, rms, xt = row_features(h, p)
+    z = value_probe(xt, probe)
+    sigma = mass_coordinate(z, p)
+    hq = probe.shape[0]
+    nu = query_weights(t, p)
+    if t > 0:
+        a = native_attention(q, k, nonvis_lse)
+        e, ell = grounded_energy_rows(a, z, sigma)
+        zrow = e.sum(axis=2)                                     # [Hq][T]
+        active = zrow > 0
+        pg = np.where(active[:, :, None], e / np.where(active, zrow, 1.0)[:, :, None], 0.0)
+        gram = head_pattern_gram(a, z, sigma)
+        abar = e.reshape(hq, -1).mean(axis=1)
+        omega, centres, clus = head_weights(gram, abar, p)
+        ebar, en = grounded_energy(e, omega, nu)
+    else:
+        a = np.zeros((hq, 0, n))
+        e = np.zeros((hq, 0, n))
+        ell = None
+        pg = np.zeros((hq, 0, n))
+        active = np.zeros((hq, 0), dtype=bool)
+        gram = np.zeros((hq, hq))
+        omega, centres, clus = np.zeros(hq), [], -np.ones(hq, dtype=np.int64)
+        ebar, en = np.ones(n), np.zeros(n)
+    bounded = n > p.bounded_threshold_n
+    if bounded:
+        if app_proj is None:
+            raise ValueError("bounded appearance bank needs the projection matrix")
+        pv, app_clients = appearance_bank_bounded(h, app_proj, p)
+    else:
+        pv, app_clients = appearance_bank(x, p), np.arange(n)
+    ps = spatial_bank(pos, p)
+    cbar, banks = client_matrix(pg, active, omega, nu, pv, ps, p)
+    return dict(norm=norm, x=x, rms=rms, xt=xt, z=z, sigma=sigma, a=a, e=e, ell=ell,
+                pg=pg, active=active, gram=gram, omega=omega, centres=centres,
+                clusters=clus, nu=nu, ebar=ebar, energy=en, pv=pv, ps=ps,
+                app_clients=app_clients, cbar=cbar, banks=banks, bounded=bounded,
+                pc=spatial_coordinates(pos))
+
+
+def bank_saturation(cbar: np.ndarray, banks: np.ndarray, support) -> dict:
+    """Z_b = F_b(V), omega_b = Z_b / sum Z, c_b = F_b(S)/Z_b and the final
+    certificate F(S)/F(V) = sum_b omega_b c_b (Eq. cond-effective-bank-mass,
+    Eq. cond-bank-mixture)."""
+    sup = np.asarray(list(support), dtype=np.int64)
+    out = {}
+    zs = {}
+    for bnk in np.unique(banks):
+        rows = cbar[banks == bnk]
+        zb = float(rows.max(axis=1).sum())
+        fb = float(rows[:, sup].max(axis=1).sum()) if sup.size else 0.0
+        zs[int(bnk)] = (zb, fb)
+    tot = sum(v[0] for v in zs.values())
+    for bnk, (zb, fb) in zs.items():
+        out[bnk] = dict(z=zb, f=fb, omega=zb / tot if tot > 0 else 0.0,
+                        c=fb / zb if zb > 0 else 0.0)
+    return out
+
+
+def gmc_single(h, q, k, pos, probe, k_req: int, p: GmcParams = GmcParams(),
+               app_proj=None, nonvis_lse=None, keep_intermediates: bool = False):
+    """One problem end to end: budget, clients, selection, assignment,
+    transport and compaction.  Returns out_hidden (fp64, before the cast to
+    the residual dtype), out_pos, out_idx and diagnostics."""
+    h = np.asarray(h, np.float64)
+    n = h.shape[0]
+    kk = realized_budget(n, k_req)
+    if kk == n:
+        return dict(out_hidden=h.copy(), out_pos=np.asarray(pos).copy(),
+                    out_idx=np.arange(n, dtype=np.int64), identity=True, k=kk)
+    cl = build_clients(h, q, k, pos, probe, p, app_proj, nonvis_lse)
+    b = p.batch_b_bounded if cl["bounded"] else p.batch_b
+    sel = select_support(cl["cbar"], kk, b, p)
+    asg = assign_population(cl["x"], cl["pc"], sel["order"], p)
+    m = population_weights(cl["ebar"], asg["sx"], p)
+    tr = transport(h, asg["pi"], sel["order"], m, p)
+    idx, out_h, out_pos = compact(tr["support"], tr["out"], np.asarray(pos))
+    res = dict(out_hidden=out_h, out_pos=out_pos, out_idx=idx, identity=False, k=kk,
+               selection=sel, assignment=asg, m=m, transport=tr, b=b,
+               saturation=bank_saturation(cl["cbar"], cl["banks"], sel["order"]),
+               f_v=float(cl["cbar"].max(axis=1).sum()))
+    if keep_intermediates:
+        res["clients"] = cl
+    return res
+
+
+def gmc(hidden, text_q, vis_k, pos3d, probe, k_req: int, p: GmcParams = GmcParams(),
+        app_proj=None, nonvis_lse=None):
+    """Batched entry: independent problems, same shapes."""
+    return [gmc_single(hidden[i], text_q[i], vis_k[i], pos3d[i], probe, k_req, p, app_proj,
+                       None if nonvis_lse is None else nonvis_lse[i])
+            for i in range(hidden.shape[0])]
+
+
+def prune_rounds(k: int, n: int, p: GmcParams = GmcParams()) -> int:
+    """Number of selection rounds ceil(K / b) for the path N selects."""
+    b = p.batch_b_bounded if n > p.bounded_threshold_n else p.batch_b
+    kk = realized_budget(n, k)
+    return 0 if kk == n else -(-kk // b)
