@@ -1,0 +1,188 @@
+"""Throughput of the GMC boundary operator on one MI355X.
+
+A step is one gmc_prune call over one batch of synthetic boundary tensors
+(every stage: message clients, banks, all selection rounds, assignment,
+transport, compaction).  Inputs are resident in HBM before timing starts.
+Prints one JSON line:
+  value       = visual tokens pruned per second = B (N - K) / seconds per step
+  roofline    = dominant kernel's algorithmic bytes (or flops) per launch over
+                its average launch time, from hipEvents on the op stream in
+                a second pass over the same steps with stage timing on
+  cpu_baseline= the fp64 oracle timed on this host on a bounded sample
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0    # dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3
+
+METRIC = "visual tokens pruned/sec (GMC op, 1 GPU) at Qwen2.5-VL-7B shape; % roofline"
+
+WORKLOAD_TEXT = {
+    "qwen": "Qwen2.5-VL-7B boundary: N=1296 (36x36), T=64, d=3584, 28/4 heads, dh=128, K=256, "
+            "bf16 16-component Gaussian mixture",
+    "batch16": "16 x Qwen2.5-VL-7B boundary problems in one call (N=1296, T=64, K=256 each)",
+    "doc": "high-res document: N=4096 (64x64), T=128, d=3584, 28/4 heads, K=820, bf16",
+    "frames": "multi-frame: N=16384 (4x64x64), T=256, d=3584, 28/4 heads, K=2048, bf16, bounded bank",
+    "tiny": "tiny: N=256 (16x16), T=16, d=512, 8/2 heads, dh=64, K=64, fp32",
+}
+
+
+def kernel_work(stage: str, w, m_rows: int, nc: int):
+    """Algorithmic bytes or flops of one launch of a stage's kernel."""
+    n, k, b = w.n, w.k, w.batch
+    if stage == "gains":      # stream the client matrix once, write column partials
+        return "hbm", b * (4.0 * m_rows * n + 4.0 * nc * n + 8.0 * m_rows)
+    if stage == "appearance":  # N x N x d Gram
+        return "mfma", b * 2.0 * n * n * w.d
+    if stage == "transport":   # every member row once + the compact output
+        esz = 2 if w.dtype == "bf16" else 4
+        return "hbm", b * (esz * n * w.d + esz * k * w.d)
+    if stage == "logits":      # write the grounded client rows
+        return "hbm", b * 4.0 * w.hq * w.t * n
+    return None, None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="time budget of the oracle CPU baseline sample (0 disables)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the operator is single-GPU and this build has no "
+              "multi-GPU path (see the design notes on sharding by image)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_02134_amd import binding, synth
+    from tests.gpu_run import make_pruner, to_device
+
+    prob = synth.make_problem(args.workload)
+    w = prob.workload
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    hid = to_device(prob.hidden, w.dtype, torch)
+    q = to_device(prob.text_q, w.dtype, torch)
+    kk = to_device(prob.vis_k, w.dtype, torch)
+    pos = torch.from_numpy(prob.pos3d).cuda()
+    pr = make_pruner(prob, torch, max_k=w.k)
+    kr = binding.gmc_realized_k(w.n, w.k)
+    out_h = torch.empty((w.batch, kr, w.d), dtype=hid.dtype, device=dev)
+    out_p = torch.empty((w.batch, kr, 3), dtype=torch.int32, device=dev)
+    out_i = torch.empty((w.batch, kr), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    binding._check(binding.gmc_set_stream(stream.cuda_stream), "gmc_set_stream")
+    ptrs = (hid.data_ptr(), q.data_ptr(), kk.data_ptr(), pos.data_ptr())
+    outs = (out_h.data_ptr(), out_p.data_ptr(), out_i.data_ptr())
+
+    def step():
+        code = binding.lib().gmc_prune(*ptrs, w.n, w.t, w.k, *outs)
+        if code != 0:
+            raise binding.GmcError(code, "gmc_prune")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: K steps between events on the op stream
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / args.steps
+    pruned = w.batch * (w.n - kr)
+    value = pruned / (ms_step / 1e3)
+
+    # stage breakdown: the same K steps again with stage events on the stream
+    binding._check(binding.gmc_timing_enable(True), "gmc_timing_enable")
+    for _ in range(args.steps):
+        step()
+    stage_ms, stage_n = binding.gmc_timing_read()
+    binding._check(binding.gmc_timing_enable(False), "gmc_timing_enable")
+    stages = {name: {"ms_per_step": stage_ms[i] / args.steps,
+                     "launch_avg_us": (1e3 * stage_ms[i] / stage_n[i]) if stage_n[i] else None,
+                     "launches_per_step": stage_n[i] / args.steps}
+              for i, name in enumerate(binding.STAGE_NAMES)}
+
+    rounds, pool_cap, bcap, m_rows = binding.gmc_trace_dims(w.n, w.t, w.k)
+    nstrips = -(-w.n // 256)
+    nc = max(1, min(64, -(-1024 // (nstrips * w.batch)), -(-m_rows // 4)))
+    nc = -(-m_rows // (-(-m_rows // nc)))
+    single_kernel = ["gains", "appearance", "transport", "logits"]
+    dom = max(single_kernel, key=lambda s: stages[s]["ms_per_step"])
+    bound, work = kernel_work(dom, w, m_rows, nc)
+    avg_s = stages[dom]["launch_avg_us"] / 1e6
+    if bound == "hbm":
+        achieved, peak, unit = work / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = work / avg_s / 1e12
+        peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
+        unit = "TFLOP/s"
+    roofline = {"bound": bound, "kernel": dom, "achieved": achieved, "peak": peak, "unit": unit,
+                "frac": achieved / peak, "traffic": None,
+                "work_per_launch": work, "launch_avg_us": stages[dom]["launch_avg_us"]}
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(prob, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "batch": w.batch, "N": w.n, "T": w.t,
+                   "K": kr, "d": w.d, "heads": [w.hq, w.hkv], "head_dim": w.dh,
+                   "rounds": rounds, "client_rows": m_rows},
+        "roofline": roofline, "cpu_baseline": cpu, "stages": stages,
+    }
+    pr.close()
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(prob, budget_s: float):
+    """The oracle as it stands, on this host, on whole problems of the same
+    workload until the time budget is used (at least one problem)."""
+    from oracle import gmc_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    w = prob.workload
+    done, pruned, t0 = 0, 0, time.perf_counter()
+    while True:
+        b = done % w.batch
+        O.gmc_single(prob.hidden[b], prob.text_q[b], prob.vis_k[b], prob.pos3d[b], prob.probe, w.k,
+                     app_proj=prob.app_proj)
+        done += 1
+        pruned += w.n - min(w.n, max(w.k, 1))
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": pruned / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} whole {w.name} problem(s) (N={w.n}, K={w.k}) through the fp64 "
+                      f"oracle in {el:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,215 @@
+/*
+ * gmc.h - C-ABI of the MI355X (gfx950) GMC boundary operator library.
+ *
+ * GMC (Grounded Message Coreset pruning) compresses the N visual states of
+ * a vision-language decoder at a boundary layer p to K carriers:
+ *   1. native message clients from the text-query -> visual-key softmax
+ *      slice (Sec. 3.2; App. H Eq. cond-native-message, Eq.
+ *      cond-mass-coordinate, Eq. cond-grounded-client), with farthest-first
+ *      head clusters (Eq. cond-head-pattern, Eq. cond-head-weight);
+ *   2. appearance and spatial clients (Eq. cond-aux-clients) pre-weighted
+ *      into one facility-location objective (Eq. coverage, Eq. cond-coverage);
+ *   3. batched responsibility selection of K carriers (Eq. responsibility,
+ *      Eq. cond-responsibility), budget K = min{N, max{K_r, 1}}
+ *      (Sec. 3.1 problem formulation);
+ *   4. population assignment (Eq. cond-assignment, Eq.
+ *      cond-population-gate) and weighted-centroid transport with RMS
+ *      restoration (Eq. transport, Eq. cond-transport, Eq.
+ *      cond-grounded-energy);
+ *   5. physical compaction keeping each carrier's original (t,h,w) position
+ *      ids (App. H "Index map and physical token accounting").
+ *
+ * Conventions shared by every entry point:
+ *   - Tensor pointers are DEVICE pointers owned by the caller, unless stated.
+ *     The library keeps no reference to them after a call returns, except
+ *     value_probe / app_projection in gmc_config, which must stay valid until
+ *     gmc_free().
+ *   - Work is enqueued asynchronously on the stream set by gmc_set_stream
+ *     (default: the null stream).  Outputs are valid once that stream has
+ *     synchronised.  Host-side validation happens before anything is enqueued.
+ *   - Row-major layouts; "dtype" is the element type chosen in gmc_config
+ *     (float32 or bfloat16 stored as its 16-bit pattern).
+ *   - Return value 0 on success, a negative GMC_ERR_* code otherwise;
+ *     gmc_last_error() then describes the failure.  A failed call enqueues
+ *     nothing and leaves the outputs untouched.
+ *   - One library context per process; calls are serialised by an internal
+ *     mutex.  Calls that overlap on the device (several host threads on
+ *     different streams) are not supported: they share one workspace.
+ */
+#ifndef GMC_H
+#define GMC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GMC_OK 0
+#define GMC_ERR_ARG (-1)      /* null pointer, bad size, bad config value      */
+#define GMC_ERR_CAPACITY (-2) /* call exceeds the capacities given at init     */
+#define GMC_ERR_STATE (-3)    /* no context (gmc_init not called / failed)     */
+#define GMC_ERR_HIP (-4)      /* HIP runtime failure (no device, launch, OOM)  */
+
+#define GMC_F32 0
+#define GMC_BF16 1
+
+/* Number of float entries gmc_trace.stats receives per problem. */
+#define GMC_STATS 8
+/* stats layout: [0] s_x  [1] mean selected-cosine gap over discarded tokens
+ *               [2] F(S)  [3] F(V)  [4] realised K  [5] rounds  [6] M rows
+ *               [7] number of discarded tokens                              */
+
+/*
+ * gmc_config - model shape, capacities and the frozen settings.
+ * gmc_config_default() fills the settings of the paper's configuration table
+ * (App. H, Table cond-config) and the readings documented with the library;
+ * the caller then sets the shape, capacity and pointer fields.
+ */
+typedef struct gmc_config {
+  /* model shape */
+  int32_t d;            /* hidden size, multiple of 32                          */
+  int32_t n_q_heads;    /* Hq, 1..32                                             */
+  int32_t n_kv_heads;   /* Hkv, divides Hq; query head h reads kv head h*Hkv/Hq   */
+  int32_t head_dim;     /* dh, multiple of 32, <= 256                            */
+  int32_t probe_rank;   /* r, 1..8 (paper: 4)                                    */
+  int32_t dtype;        /* GMC_F32 or GMC_BF16 for hidden/text_q/vis_k/out      */
+  /* capacities: the workspace is sized once, in gmc_init, for these         */
+  int32_t max_batch;    /* problems per call (gmc_prune uses exactly this many) */
+  int32_t max_n;        /* visual tokens per problem, <= 32768                  */
+  int32_t max_t;        /* text queries per problem                             */
+  int32_t max_k;        /* realised budget per problem (0: max_n)               */
+  /* device inputs fixed for the context's lifetime (caller-owned)           */
+  const void* value_probe;    /* [Hq][r][d] dtype: per-head folded value path
+                                 G_h = (W^V_kv(h) O_h P)^T (Eq. cond-mass-
+                                 coordinate); required                       */
+  const void* app_projection; /* [app_rank][d] dtype, entries +-1: the fixed
+                                 Rademacher map of the bounded appearance bank
+                                 (App. H "Appearance and spatial clients");
+                                 required iff max_n > bounded_threshold_n     */
+  /* frozen settings (Table cond-config) */
+  float lambda_mass, eps_mass;          /* 1, 1e-8                            */
+  float beta_msg, beta_app, beta_spa;   /* 1, 0.5, 0.25                       */
+  float tau_v, tau_s;                   /* 0.2, 0.02                          */
+  int32_t landmarks;                    /* 16 (16 x 16 spatial clients)       */
+  int32_t batch_b, pool_mult;           /* 16, 4                              */
+  float tau_r, resp_eps;                /* 0.1, 1e-30                         */
+  float spatial_w, gate_t, gate_p;      /* 0.5, 0.08, 8                       */
+  float amb_margin, amb_p;              /* 0.05, 8                            */
+  int32_t g_form;                       /* 0 smooth exp(-(d/m)^p), 1 hard     */
+  float pop_strength, tau_j;            /* 0.5, 1                             */
+  int32_t max_head_clusters;            /* 4                                  */
+  float disp_eps, terminal_q_weight;    /* 0.05, 2                            */
+  float rms_eps, norm_eps, restore_eps; /* 1e-6, 1e-12, 1e-6                  */
+  int32_t bounded_threshold_n;          /* 4096: N above it uses the bounded bank */
+  int32_t app_rank, app_max_clients;    /* 128, 4096                          */
+  int32_t batch_b_bounded;              /* 512                                */
+} gmc_config;
+
+/*
+ * gmc_trace - optional device buffers the operator fills for inspection
+ * (tests, diagnostics).  Every pointer may be NULL.  Sizes come from
+ * gmc_trace_dims().  Problem p's block starts at p times the per-problem
+ * size.
+ */
+typedef struct gmc_trace {
+  int32_t* round_pool;  /* [B][rounds][pool_cap]: each round's candidate pool,
+                           ascending source index, -1 padded                  */
+  int32_t* round_batch; /* [B][rounds][batch_cap]: each round's batch,
+                           ascending source index, -1 padded                  */
+  int32_t* assign;      /* [B][N]: representative pi(i) (source index)        */
+  float* omega;         /* [B][Hq]: head weights omega_h                       */
+  float* ebar;          /* [B][N]: normalised grounded energy ebar_i           */
+  float* client;        /* [B][m_rows][N]: pre-weighted client matrix Cbar    */
+  float* stats;         /* [B][GMC_STATS]: see GMC_STATS                       */
+} gmc_trace;
+
+/* Fill *cfg with the frozen settings; shape/capacity/pointers are zeroed. */
+void gmc_config_default(gmc_config* cfg);
+
+/*
+ * gmc_init - validate *cfg, create the context and allocate its workspace
+ * (one device allocation sized from the capacities).  Replaces any existing
+ * context.  The config struct is copied; the two device pointers in it are
+ * borrowed.  Errors: GMC_ERR_ARG (bad field), GMC_ERR_HIP (no device, OOM).
+ */
+int gmc_init(const gmc_config* cfg);
+
+/* Use `stream` (a hipStream_t, or NULL for the null stream) for all
+ * subsequent work.  Errors: GMC_ERR_STATE. */
+int gmc_set_stream(void* stream);
+
+/*
+ * gmc_prune - run the operator on cfg.max_batch independent problems.
+ *   hidden     [B][N][d]        dtype   visual residual states h_i at boundary p
+ *   text_q     [B][T][Hq][dh]   dtype   text queries (post-norm, post-rotary)
+ *   vis_k      [B][N][Hkv][dh]  dtype   visual keys (post-norm, post-rotary)
+ *   pos3d      [B][N][3]        int32   original (t,h,w) multimodal position ids
+ *   N >= 1, T >= 0 (T = 0: no grounded clients, uniform energy), K = requested
+ *   budget K_r; the realised K = gmc_realized_k(N, K_r).
+ *   out_hidden [B][K][d]  dtype  transported carriers, ascending source order
+ *   out_pos    [B][K][3]  int32  the carriers' original position ids
+ *   out_idx    [B][K]     int32  the carriers' source indices, ascending
+ * K = N returns the inputs unchanged (identity).  Outputs must not overlap
+ * inputs.  Errors: GMC_ERR_ARG, GMC_ERR_CAPACITY, GMC_ERR_STATE, GMC_ERR_HIP.
+ */
+int gmc_prune(const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+              int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos,
+              int32_t* out_idx);
+
+/*
+ * gmc_prune_ex - gmc_prune with an explicit problem count 1 <= B <= max_batch
+ * and two optional extras:
+ *   nonvis_lse [B][Hq][T] float32 or NULL: log-sum-exp of each query's logits
+ *              over the preceding nonvisual keys, so the visual slice keeps the
+ *              native softmax denominator (Eq. cond-native-message); NULL
+ *              means visual keys only.
+ *   trace      host struct of optional device buffers (see gmc_trace), or NULL.
+ */
+int gmc_prune_ex(int64_t B, const void* hidden, const void* text_q, const void* vis_k,
+                 const int32_t* pos3d, int64_t N, int64_t T, int64_t K, void* out_hidden,
+                 int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse,
+                 const gmc_trace* trace);
+
+/* Realised budget K = min{N, max{K_r, 1}} (Sec. 3.1); 0 if N < 1. Host-only. */
+int64_t gmc_realized_k(int64_t N, int64_t K_req);
+
+/*
+ * Per-problem trace sizes for a call shape under the current context:
+ * selection rounds, pool capacity, batch capacity and client rows M.
+ * Errors: GMC_ERR_STATE, GMC_ERR_ARG.  Host-only.
+ */
+int gmc_trace_dims(int64_t N, int64_t T, int64_t K, int64_t* rounds, int64_t* pool_cap,
+                   int64_t* batch_cap, int64_t* m_rows);
+
+/*
+ * Stage timing for measurement.  While enabled, every subsequent call records
+ * hipEvents on the context stream around each stage's launches:
+ *   [0] row norms + value probe + mass coordinate   [1] message logits/softmax
+ *   [2] head-pattern Gram + head weights + energy  [3] appearance bank GEMM
+ *   [4] spatial bank + bank weights                [5] selection gains
+ *   [6] selection pool top-k                       [7] responsibility
+ *   [8] batch top-k                                [9] objective values
+ *   [10] assignment (cosines, gaps, gate, argmax)  [11] transport + compaction
+ * gmc_timing_read synchronises the stream, returns per-stage total
+ * milliseconds and span counts accumulated since the last read, and clears
+ * them.  Errors: GMC_ERR_STATE, GMC_ERR_ARG (n < GMC_TIMERS), GMC_ERR_HIP.
+ */
+#define GMC_TIMERS 12
+int gmc_timing_enable(int enable);
+int gmc_timing_read(double* total_ms, int64_t* spans, int32_t n);
+
+/* Bytes of device workspace the current context holds (0 without one). */
+int64_t gmc_workspace_bytes(void);
+
+/* Description of the last error on this process (static storage). */
+const char* gmc_last_error(void);
+
+/* Release the context and its workspace; safe to call repeatedly. */
+void gmc_free(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GMC_H */

@@ -1,0 +1,549 @@
+// C-ABI of the GMC boundary operator: context, validation, workspace plan and
+// the launch sequence of one call (Algorithm 1, steps 2-6):
+//   message clients -> appearance/spatial banks -> selection rounds ->
+//   assignment -> transport + compaction.
+// Nothing here synchronises the device; every launch goes to the context
+// stream.  The workspace is one allocation made in gmc_init.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "gmc.h"
+#include "gmc_internal.h"
+#include "gmc_kernels.h"
+
+using namespace gmc;
+
+namespace {
+
+struct Capacity {
+  int B, N, T, K, hq, hr, mv, m, ldE, nc_max, nc2_max, pool_cap, bmax, ldK, rank;
+  bool bounded_possible;
+};
+
+struct Context {
+  gmc_config cfg{};
+  Params pr{};
+  Capacity cap{};
+  Ws ws{};
+  void* mem = nullptr;
+  size_t bytes = 0;
+  hipStream_t stream = nullptr;
+  int device = 0;
+};
+
+std::mutex g_mu;
+Context* g_ctx = nullptr;
+char g_err[512] = "";
+
+// Stage timer: events recorded on the op stream around each stage's launches.
+struct Span {
+  int stage;
+  hipEvent_t a, b;
+};
+struct Timer {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<Span> spans;
+  hipEvent_t open[kNumStages] = {};
+  hipEvent_t take() {
+    if (used == pool.size()) {
+      hipEvent_t e = nullptr;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      pool.push_back(e);
+    }
+    return pool[used++];
+  }
+  void release() {
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+    pool.clear();
+    spans.clear();
+    used = 0;
+  }
+};
+Timer g_timer;
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+constexpr int kNcMax = 64;     // gains kernel row chunks
+constexpr int kNc2Max = 256;   // responsibility kernel row chunks
+constexpr int kGainsTargetBlocks = 1024;
+
+long long round_up(long long x, long long a) { return (x + a - 1) / a * a; }
+long long cdiv(long long x, long long a) { return (x + a - 1) / a; }
+
+int app_rows(const gmc_config& c, int n) {
+  return n > c.bounded_threshold_n ? std::min(c.app_max_clients, n) : n;
+}
+
+Params make_params(const gmc_config& c) {
+  Params p{};
+  p.lambda_mass = c.lambda_mass; p.eps_mass = c.eps_mass; p.beta_msg = c.beta_msg;
+  p.beta_app = c.beta_app; p.beta_spa = c.beta_spa; p.tau_v = c.tau_v; p.tau_s = c.tau_s;
+  p.tau_r = c.tau_r; p.resp_eps = c.resp_eps; p.spatial_w = c.spatial_w; p.gate_t = c.gate_t;
+  p.gate_p = c.gate_p; p.amb_margin = c.amb_margin; p.amb_p = c.amb_p; p.g_form = c.g_form;
+  p.pop_strength = c.pop_strength; p.tau_j = c.tau_j; p.max_head_clusters = c.max_head_clusters;
+  p.disp_eps = c.disp_eps; p.terminal_q_weight = c.terminal_q_weight; p.rms_eps = c.rms_eps;
+  p.norm_eps = c.norm_eps; p.restore_eps = c.restore_eps; p.pool_mult = c.pool_mult;
+  return p;
+}
+
+int validate_config(const gmc_config* c) {
+  if (!c) return fail(GMC_ERR_ARG, "gmc_init: cfg is NULL");
+  if (c->d <= 0 || c->d % 32 != 0) return fail(GMC_ERR_ARG, "d=%d must be a positive multiple of 32", c->d);
+  if (c->d > 256 * 8 * 8) return fail(GMC_ERR_ARG, "d=%d exceeds 16384", c->d);
+  if (c->n_q_heads < 1 || c->n_q_heads > kMaxHeads)
+    return fail(GMC_ERR_ARG, "n_q_heads=%d must be in [1, %d]", c->n_q_heads, kMaxHeads);
+  if (c->n_kv_heads < 1 || c->n_q_heads % c->n_kv_heads != 0)
+    return fail(GMC_ERR_ARG, "n_kv_heads=%d must divide n_q_heads=%d", c->n_kv_heads, c->n_q_heads);
+  if (c->head_dim < 32 || c->head_dim > 256 || c->head_dim % 32 != 0)
+    return fail(GMC_ERR_ARG, "head_dim=%d must be a multiple of 32 in [32, 256]", c->head_dim);
+  if (c->probe_rank < 1 || c->probe_rank > kMaxProbe)
+    return fail(GMC_ERR_ARG, "probe_rank=%d must be in [1, %d]", c->probe_rank, kMaxProbe);
+  if (c->dtype != GMC_F32 && c->dtype != GMC_BF16) return fail(GMC_ERR_ARG, "dtype=%d unknown", c->dtype);
+  if (c->max_batch < 1) return fail(GMC_ERR_ARG, "max_batch=%d must be >= 1", c->max_batch);
+  if (c->max_n < 1 || c->max_n > kMaxN) return fail(GMC_ERR_ARG, "max_n=%d must be in [1, %d]", c->max_n, kMaxN);
+  if (c->max_t < 0) return fail(GMC_ERR_ARG, "max_t=%d must be >= 0", c->max_t);
+  if (c->max_k < 0 || c->max_k > c->max_n) return fail(GMC_ERR_ARG, "max_k=%d must be in [0, max_n]", c->max_k);
+  if (!c->value_probe) return fail(GMC_ERR_ARG, "value_probe is NULL");
+  if (c->landmarks < 1 || c->landmarks > 64) return fail(GMC_ERR_ARG, "landmarks=%d out of [1, 64]", c->landmarks);
+  if (c->batch_b < 1 || c->batch_b_bounded < 1 || c->pool_mult < 1)
+    return fail(GMC_ERR_ARG, "batch sizes and pool_mult must be >= 1");
+  if (c->batch_b > 1024 || c->batch_b_bounded > 1024)
+    return fail(GMC_ERR_ARG, "batch sizes must be <= 1024");
+  if (static_cast<long long>(c->pool_mult) * std::max(c->batch_b, c->batch_b_bounded) > 2048)
+    return fail(GMC_ERR_ARG, "pool_mult * batch must be <= 2048");
+  if (c->max_head_clusters < 1) return fail(GMC_ERR_ARG, "max_head_clusters must be >= 1");
+  if (!(c->tau_v > 0 && c->tau_s > 0 && c->tau_r > 0 && c->gate_t > 0 && c->amb_margin > 0))
+    return fail(GMC_ERR_ARG, "temperatures and gate scales must be positive");
+  if (c->g_form != 0 && c->g_form != 1) return fail(GMC_ERR_ARG, "g_form=%d unknown", c->g_form);
+  if (c->bounded_threshold_n < 1) return fail(GMC_ERR_ARG, "bounded_threshold_n must be >= 1");
+  if (c->max_n > c->bounded_threshold_n) {
+    if (!c->app_projection) return fail(GMC_ERR_ARG, "app_projection is NULL but max_n exceeds the bounded threshold");
+    if (c->app_rank < 32 || c->app_rank % 32 != 0 || c->app_rank > 1024)
+      return fail(GMC_ERR_ARG, "app_rank=%d must be a multiple of 32 in [32, 1024]", c->app_rank);
+    if (c->app_max_clients < 1) return fail(GMC_ERR_ARG, "app_max_clients must be >= 1");
+  }
+  return GMC_OK;
+}
+
+// Workspace plan: per-problem strides from the capacities.
+struct Plan {
+  Capacity cap;
+  long long s_n, s_z, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
+      s_cov, s_sel, s_ord, s_part, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
+      s_pi, s_st, s_keys;
+};
+
+Plan make_plan(const gmc_config& c) {
+  Plan pl{};
+  Capacity& k = pl.cap;
+  k.B = c.max_batch;
+  k.N = c.max_n;
+  k.T = c.max_t;
+  k.K = c.max_k > 0 ? c.max_k : c.max_n;
+  k.hq = c.n_q_heads;
+  k.hr = c.n_q_heads * c.probe_rank;
+  k.bounded_possible = c.max_n > c.bounded_threshold_n;
+  k.mv = std::max(std::min(c.max_n, c.bounded_threshold_n),
+                  k.bounded_possible ? std::min(c.app_max_clients, c.max_n) : 0);
+  k.m = k.hq * k.T + k.mv + c.landmarks * c.landmarks;
+  k.ldE = static_cast<int>(round_up(k.N, 4));
+  k.nc_max = kNcMax;
+  k.nc2_max = kNc2Max;
+  k.bmax = std::max(c.batch_b, k.bounded_possible ? c.batch_b_bounded : 0);
+  k.pool_cap = c.pool_mult * k.bmax;
+  k.ldK = static_cast<int>(round_up(k.K, 4));
+  k.rank = k.bounded_possible ? c.app_rank : 0;
+  const long long npairs = static_cast<long long>(k.hq) * (k.hq + 1) / 2;
+  pl.s_n = k.N;
+  pl.s_z = static_cast<long long>(k.N) * k.hr;
+  pl.s_sig = kMaxHeads;
+  pl.s_ell = static_cast<long long>(k.hq) * k.N;
+  pl.s_E = static_cast<long long>(k.m) * k.ldE;
+  pl.s_m = k.m;
+  pl.s_apart = cdiv(k.N, 64) * k.mv;
+  pl.s_gpart = cdiv(k.N, kHeadTok) * npairs;
+  pl.s_e2 = static_cast<long long>(k.hq) * k.N;
+  pl.s_om = kMaxHeads;
+  pl.s_eb = k.N;
+  pl.s_pc = 2LL * k.N;
+  pl.s_bd = 4;
+  pl.s_y = static_cast<long long>(k.N) * k.rank;
+  pl.s_cl = k.mv;
+  pl.s_cov = 2LL * k.m;
+  pl.s_sel = k.N;
+  pl.s_ord = k.N;
+  pl.s_part = static_cast<long long>(k.nc_max) * k.ldE;
+  pl.s_pool = k.pool_cap;
+  pl.s_spart = std::max<long long>(static_cast<long long>(k.nc2_max) * k.pool_cap, 2 * cdiv(k.m, 256));
+  pl.s_bat = k.bmax;
+  pl.s_slot = k.N;
+  pl.s_sup = k.N;
+  pl.s_cos = static_cast<long long>(k.N) * k.ldK;
+  pl.s_del = k.N;
+  pl.s_dp = cdiv(k.N, 4) + 1;
+  pl.s_gate = 4;
+  pl.s_pi = k.N;
+  pl.s_st = kStats;
+  pl.s_keys = k.N;
+  return pl;
+}
+
+// Carve the allocation; returns total bytes when base is nullptr.
+size_t carve(const Plan& pl, char* base, Ws* ws) {
+  size_t off = 0;
+  const long long B = pl.cap.B;
+  auto take = [&](long long per_problem, size_t esz) -> char* {
+    off = round_up(off, 256);
+    char* p = base ? base + off : nullptr;
+    off += static_cast<size_t>(std::max<long long>(per_problem, 1) * B) * esz;
+    return p;
+  };
+#define F(name) ws->name = reinterpret_cast<float*>(take(pl.s_##name, 4)); ws->s_##name = pl.s_##name
+#define I(name) ws->name = reinterpret_cast<int*>(take(pl.s_##name, 4)); ws->s_##name = pl.s_##name
+  ws->n2 = reinterpret_cast<float*>(take(pl.s_n, 4)); ws->s_n = pl.s_n;
+  F(z); F(sig); F(ell); F(E);
+  ws->alpha = reinterpret_cast<float*>(take(pl.s_m, 4)); ws->s_m = pl.s_m;
+  ws->peak = reinterpret_cast<float*>(take(pl.s_m, 4));
+  ws->rowsum = reinterpret_cast<float*>(take(pl.s_m, 4));
+  ws->apart_sum = reinterpret_cast<float*>(take(pl.s_apart, 4));
+  ws->apart_max = reinterpret_cast<float*>(take(pl.s_apart, 4)); ws->s_apart = pl.s_apart;
+  F(gpart); F(e2);
+  ws->omega = reinterpret_cast<float*>(take(pl.s_om, 4)); ws->s_om = pl.s_om;
+  ws->ebar = reinterpret_cast<float*>(take(pl.s_eb, 4)); ws->s_eb = pl.s_eb;
+  F(pc);
+  ws->bounds = reinterpret_cast<float*>(take(pl.s_bd, 4)); ws->s_bd = pl.s_bd;
+  F(y);
+  ws->clients = reinterpret_cast<int*>(take(pl.s_cl, 4)); ws->s_cl = pl.s_cl;
+  F(cov);
+  I(sel);
+  ws->order = reinterpret_cast<int*>(take(pl.s_ord, 4)); ws->s_ord = pl.s_ord;
+  F(part); I(pool); F(spart);
+  ws->batch = reinterpret_cast<int*>(take(pl.s_bat, 4)); ws->s_bat = pl.s_bat;
+  I(slot); I(sup);
+  ws->cosb = reinterpret_cast<float*>(take(pl.s_cos, 4)); ws->s_cos = pl.s_cos;
+  ws->delta = reinterpret_cast<float*>(take(pl.s_del, 4)); ws->s_del = pl.s_del;
+  ws->dpart = reinterpret_cast<float*>(take(pl.s_dp, 4)); ws->s_dp = pl.s_dp;
+  ws->gate = reinterpret_cast<float*>(take(pl.s_gate, 4)); ws->s_gate = pl.s_gate;
+  I(pi);
+  ws->stats = reinterpret_cast<float*>(take(pl.s_st, 4)); ws->s_st = pl.s_st;
+  ws->keys = reinterpret_cast<uint32_t*>(take(pl.s_keys, 4)); ws->s_keys = pl.s_keys;
+#undef F
+#undef I
+  return round_up(off, 256);
+}
+
+}  // namespace
+
+namespace gmc {
+void timer_mark(int stage, bool begin, hipStream_t st) {
+  if (!g_timer.on || stage < 0 || stage >= kNumStages) return;
+  hipEvent_t e = g_timer.take();
+  if (!e) return;
+  (void)hipEventRecord(e, st);
+  if (begin) {
+    g_timer.open[stage] = e;
+  } else if (g_timer.open[stage]) {
+    g_timer.spans.push_back(Span{stage, g_timer.open[stage], e});
+    g_timer.open[stage] = nullptr;
+  }
+}
+}  // namespace gmc
+
+extern "C" {
+
+void gmc_config_default(gmc_config* c) {
+  if (!c) return;
+  std::memset(c, 0, sizeof(*c));
+  c->probe_rank = 4;
+  c->dtype = GMC_BF16;
+  c->max_batch = 1;
+  c->lambda_mass = 1.0f;
+  c->eps_mass = 1e-8f;
+  c->beta_msg = 1.0f;
+  c->beta_app = 0.5f;
+  c->beta_spa = 0.25f;
+  c->tau_v = 0.2f;
+  c->tau_s = 0.02f;
+  c->landmarks = 16;
+  c->batch_b = 16;
+  c->pool_mult = 4;
+  c->tau_r = 0.1f;
+  c->resp_eps = 1e-30f;
+  c->spatial_w = 0.5f;
+  c->gate_t = 0.08f;
+  c->gate_p = 8.0f;
+  c->amb_margin = 0.05f;
+  c->amb_p = 8.0f;
+  c->g_form = 0;
+  c->pop_strength = 0.5f;
+  c->tau_j = 1.0f;
+  c->max_head_clusters = 4;
+  c->disp_eps = 0.05f;
+  c->terminal_q_weight = 2.0f;
+  c->rms_eps = 1e-6f;
+  c->norm_eps = 1e-12f;
+  c->restore_eps = 1e-6f;
+  c->bounded_threshold_n = 4096;
+  c->app_rank = 128;
+  c->app_max_clients = 4096;
+  c->batch_b_bounded = 512;
+}
+
+void gmc_free(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_timer.on = false;
+  g_timer.release();
+  if (!g_ctx) return;
+  if (g_ctx->mem) {
+    (void)hipSetDevice(g_ctx->device);
+    (void)hipFree(g_ctx->mem);
+  }
+  delete g_ctx;
+  g_ctx = nullptr;
+}
+
+int gmc_init(const gmc_config* cfg) {
+  int rc = validate_config(cfg);
+  if (rc != GMC_OK) return rc;
+  gmc_free();
+  std::lock_guard<std::mutex> lk(g_mu);
+  Context* ctx = new Context();
+  ctx->cfg = *cfg;
+  if (ctx->cfg.max_k == 0) ctx->cfg.max_k = ctx->cfg.max_n;
+  ctx->pr = make_params(ctx->cfg);
+  Plan pl = make_plan(ctx->cfg);
+  ctx->cap = pl.cap;
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) {
+    delete ctx;
+    return fail(GMC_ERR_HIP, "gmc_init: no HIP device (%s)", hipGetErrorString(err));
+  }
+  ctx->device = dev;
+  Ws tmp{};
+  const size_t bytes = carve(pl, nullptr, &tmp);
+  err = hipMalloc(&ctx->mem, bytes);
+  if (err != hipSuccess) {
+    delete ctx;
+    return fail(GMC_ERR_HIP, "gmc_init: hipMalloc(%zu) failed (%s)", bytes, hipGetErrorString(err));
+  }
+  ctx->bytes = bytes;
+  carve(pl, static_cast<char*>(ctx->mem), &ctx->ws);
+  g_ctx = ctx;
+  return GMC_OK;
+}
+
+int gmc_set_stream(void* stream) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_set_stream: no context");
+  g_ctx->stream = static_cast<hipStream_t>(stream);
+  return GMC_OK;
+}
+
+int64_t gmc_realized_k(int64_t N, int64_t K_req) {
+  if (N < 1) return 0;
+  return std::min<int64_t>(N, std::max<int64_t>(K_req, 1));
+}
+
+int64_t gmc_workspace_bytes(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  return g_ctx ? static_cast<int64_t>(g_ctx->bytes) : 0;
+}
+
+const char* gmc_last_error(void) { return g_err; }
+
+int gmc_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_timing_enable: no context");
+  g_timer.on = enable != 0;
+  return GMC_OK;
+}
+
+int gmc_timing_read(double* total_ms, int64_t* spans, int32_t n) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_timing_read: no context");
+  if (!total_ms || !spans || n < kNumStages) return fail(GMC_ERR_ARG, "gmc_timing_read: need %d slots", kNumStages);
+  for (int i = 0; i < n; ++i) { total_ms[i] = 0.0; spans[i] = 0; }
+  hipError_t err = hipStreamSynchronize(g_ctx->stream);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "gmc_timing_read: %s", hipGetErrorString(err));
+  for (const Span& sp : g_timer.spans) {
+    float ms = 0.f;
+    err = hipEventElapsedTime(&ms, sp.a, sp.b);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "hipEventElapsedTime: %s", hipGetErrorString(err));
+    total_ms[sp.stage] += ms;
+    spans[sp.stage] += 1;
+  }
+  g_timer.spans.clear();
+  g_timer.used = 0;
+  for (int i = 0; i < kNumStages; ++i) g_timer.open[i] = nullptr;
+  return GMC_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Resolve the call shape; returns GMC_OK or an error code.
+int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req, Shape* out) {
+  const gmc_config& g = c.cfg;
+  if (B < 1) return fail(GMC_ERR_ARG, "batch=%lld must be >= 1", static_cast<long long>(B));
+  if (N < 1) return fail(GMC_ERR_ARG, "N=%lld must be >= 1", static_cast<long long>(N));
+  if (T < 0) return fail(GMC_ERR_ARG, "T=%lld must be >= 0", static_cast<long long>(T));
+  if (B > c.cap.B) return fail(GMC_ERR_CAPACITY, "batch=%lld exceeds max_batch=%d", static_cast<long long>(B), c.cap.B);
+  if (N > c.cap.N) return fail(GMC_ERR_CAPACITY, "N=%lld exceeds max_n=%d", static_cast<long long>(N), c.cap.N);
+  if (T > c.cap.T) return fail(GMC_ERR_CAPACITY, "T=%lld exceeds max_t=%d", static_cast<long long>(T), c.cap.T);
+  const int64_t K = gmc_realized_k(N, K_req);
+  Shape s{};
+  s.B = static_cast<int>(B);
+  s.N = static_cast<int>(N);
+  s.T = static_cast<int>(T);
+  s.K = static_cast<int>(K);
+  s.d = g.d;
+  s.hq = g.n_q_heads;
+  s.hkv = g.n_kv_heads;
+  s.hg = g.n_q_heads / g.n_kv_heads;
+  s.dh = g.head_dim;
+  s.r = g.probe_rank;
+  s.hr = s.hq * s.r;
+  s.dtype = g.dtype;
+  s.landmarks = g.landmarks;
+  if (K < N && K > c.cap.K)
+    return fail(GMC_ERR_CAPACITY, "realised K=%lld exceeds max_k=%d", static_cast<long long>(K), c.cap.K);
+  s.bounded = N > g.bounded_threshold_n ? 1 : 0;
+  s.app_rank = s.bounded ? g.app_rank : 0;
+  s.mg = s.hq * s.T;
+  s.mv = app_rows(g, s.N);
+  s.ms = g.landmarks * g.landmarks;
+  s.m = s.mg + s.mv + s.ms;
+  s.ldE = static_cast<int>(round_up(N, 4));
+  s.b = s.bounded ? g.batch_b_bounded : g.batch_b;
+  s.pool_cap = g.pool_mult * s.b;
+  s.rounds = (K < N) ? static_cast<int>(cdiv(K, s.b)) : 0;
+  s.ldK = static_cast<int>(round_up(K, 4));
+  s.nstrips = static_cast<int>(cdiv(N, kStripCols));
+  int nc = static_cast<int>(cdiv(kGainsTargetBlocks, static_cast<long long>(s.nstrips) * s.B));
+  nc = std::max(1, std::min({nc, kNcMax, static_cast<int>(cdiv(s.m, 4))}));
+  s.rc = static_cast<int>(cdiv(s.m, nc));
+  s.nc = static_cast<int>(cdiv(s.m, s.rc));
+  int nc2 = static_cast<int>(std::min<long long>(kNc2Max, cdiv(s.m, 32)));
+  nc2 = std::max(1, nc2);
+  s.rc2 = static_cast<int>(cdiv(s.m, nc2));
+  s.nc2 = static_cast<int>(cdiv(s.m, s.rc2));
+  s.n_app_cblk = static_cast<int>(cdiv(N, 64));
+  s.n_head_blk = static_cast<int>(cdiv(N, kHeadTok));
+  s.npairs = s.hq * (s.hq + 1) / 2;
+  *out = s;
+  return GMC_OK;
+}
+
+int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+        int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
+        const float* nonvis_lse, const gmc_trace* trace) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_prune: no context (call gmc_init first)");
+  Context& c = *g_ctx;
+  if (!hidden || !vis_k || !pos3d || !out_hidden || !out_pos || !out_idx)
+    return fail(GMC_ERR_ARG, "gmc_prune: null tensor pointer");
+  if (T > 0 && !text_q) return fail(GMC_ERR_ARG, "gmc_prune: text_q is NULL with T > 0");
+  Shape s;
+  int rc = make_shape(c, B, N, T, K, &s);
+  if (rc != GMC_OK) return rc;
+  const size_t esz = s.dtype == GMC_F32 ? 4 : 2;
+  // outputs must not overlap the inputs
+  auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
+    const char* x = static_cast<const char*>(a);
+    const char* y = static_cast<const char*>(b);
+    return x < y + nb && y < x + na;
+  };
+  const size_t n_hidden = esz * s.B * s.N * s.d, n_out = esz * s.B * s.K * s.d;
+  const size_t n_pos = 12ull * s.B * s.N, n_opos = 12ull * s.B * s.K, n_idx = 4ull * s.B * s.K;
+  const size_t n_q = esz * s.B * s.T * s.hq * s.dh, n_k = esz * s.B * s.N * s.hkv * s.dh;
+  const void* ins[4] = {hidden, text_q, vis_k, pos3d};
+  const size_t nins[4] = {n_hidden, text_q ? n_q : 0, n_k, n_pos};
+  const void* outs[3] = {out_hidden, out_pos, out_idx};
+  const size_t nouts[3] = {n_out, n_opos, n_idx};
+  for (int o = 0; o < 3; ++o) {
+    for (int i = 0; i < 4; ++i)
+      if (nins[i] && overlap(outs[o], nouts[o], ins[i], nins[i]))
+        return fail(GMC_ERR_ARG, "gmc_prune: output %d overlaps input %d", o, i);
+    for (int o2 = o + 1; o2 < 3; ++o2)
+      if (overlap(outs[o], nouts[o], outs[o2], nouts[o2]))
+        return fail(GMC_ERR_ARG, "gmc_prune: outputs %d and %d overlap", o, o2);
+  }
+  hipError_t err = hipSetDevice(c.device);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "hipSetDevice: %s", hipGetErrorString(err));
+  hipStream_t st = c.stream;
+  if (s.K == s.N) {
+    err = launch_identity(s, hidden, pos3d, out_hidden, out_pos, out_idx, st);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "identity copy: %s", hipGetErrorString(err));
+    return GMC_OK;
+  }
+  const gmc_trace tr = trace ? *trace : gmc_trace{};
+  err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega,
+                       tr.ebar, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
+  err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
+  err = launch_selection(s, c.pr, c.ws, tr.round_pool, tr.round_batch, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "selection kernels: %s", hipGetErrorString(err));
+  err = launch_assignment(s, c.pr, c.ws, hidden, tr.assign, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "assignment kernels: %s", hipGetErrorString(err));
+  err = launch_transport(s, c.pr, c.ws, hidden, pos3d, out_hidden, out_pos, out_idx, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "transport kernels: %s", hipGetErrorString(err));
+  if (tr.client || tr.stats) {
+    err = launch_trace_exports(s, c.ws, tr.client, tr.stats, st);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "trace exports: %s", hipGetErrorString(err));
+  }
+  return GMC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int gmc_prune(const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d, int64_t N,
+              int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx) {
+  int64_t B;
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_prune: no context (call gmc_init first)");
+    B = g_ctx->cfg.max_batch;
+  }
+  return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nullptr, nullptr);
+}
+
+int gmc_prune_ex(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+                 int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
+                 const float* nonvis_lse, const gmc_trace* trace) {
+  return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nonvis_lse, trace);
+}
+
+int gmc_trace_dims(int64_t N, int64_t T, int64_t K, int64_t* rounds, int64_t* pool_cap, int64_t* batch_cap,
+                   int64_t* m_rows) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_trace_dims: no context");
+  Shape s;
+  const int rc = make_shape(*g_ctx, 1, N, T, K, &s);
+  if (rc != GMC_OK) return rc;
+  if (rounds) *rounds = s.rounds;
+  if (pool_cap) *pool_cap = s.pool_cap;
+  if (batch_cap) *batch_cap = s.b;
+  if (m_rows) *m_rows = s.m;
+  return GMC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Shapes, settings and workspace layout shared by the host sequencer and the
+// kernels of the GMC operator.  Plain structs, passed to kernels by value.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gmc {
+
+constexpr int kMaxHeads = 32;     // Hq limit (head-pattern Gram kept in registers)
+constexpr int kMaxProbe = 8;      // probe rank limit
+constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
+constexpr int kHeadTok = 16;      // tokens per head-Gram block
+constexpr int kStripCols = 256;   // gains kernel: columns per wave strip (64 lanes x 4)
+constexpr int kStats = 8;
+
+// Call shape, resolved on the host for one gmc_prune call.
+struct Shape {
+  int B, N, T, K, d, hq, hkv, dh, r, hr;  // hr = hq * r
+  int hg;                                 // query heads per kv head
+  int mg, mv, ms, m;                      // client rows: grounded, appearance, spatial, total
+  int ldE;                                // client-matrix row stride (floats, multiple of 4)
+  int bounded;                            // 1: bounded appearance bank
+  int app_rank;
+  int b, pool_cap, rounds;                // selection batch, pool capacity, rounds
+  int ldK;                                // cosine buffer row stride (floats)
+  int nc;                                 // gains kernel row chunks
+  int rc;                                 // rows per gains chunk
+  int nstrips;                            // gains kernel column strips
+  int nc2, rc2;                           // responsibility kernel row chunks
+  int n_app_cblk;                         // column blocks of the appearance GEMM
+  int n_head_blk;                         // token blocks of the head-Gram kernel
+  int npairs;                             // head pairs h <= g
+  int landmarks;
+  int dtype;                              // 0 float32, 1 bfloat16
+};
+
+// Frozen settings (copied from gmc_config).
+struct Params {
+  float lambda_mass, eps_mass, beta_msg, beta_app, beta_spa, tau_v, tau_s;
+  float tau_r, resp_eps, spatial_w, gate_t, gate_p, amb_margin, amb_p;
+  int g_form;
+  float pop_strength, tau_j;
+  int max_head_clusters;
+  float disp_eps, terminal_q_weight, rms_eps, norm_eps, restore_eps;
+  int pool_mult;
+};
+
+// Workspace: every buffer is [max_batch][per-problem size]; s_* are the
+// per-problem strides in elements.
+struct Ws {
+  float* n2;       long long s_n;       // squared row norms            [N]
+  float* z;        long long s_z;       // probe coordinates Z          [N][hr]
+  float* sig;      long long s_sig;     // mass coordinate sigma_h      [hq]
+  float* ell;      long long s_ell;     // ||[Z_h[i]; sigma_h]||        [hq][N]
+  float* E;        long long s_E;       // client energies              [M][ldE]
+  float* alpha;    long long s_m;       // row pre-weights              [M]
+  float* peak;                          // max_i Cbar_mi                [M]
+  float* rowsum;                        // grounded row sums Z_(h,t)    [M]
+  float* apart_sum; float* apart_max; long long s_apart;  // appearance partials [cblk][mv]
+  float* gpart;    long long s_gpart;   // head-Gram partials           [blk][npairs]
+  float* e2;       long long s_e2;      // sum_t nu_t e^2               [hq][N]
+  float* omega;    long long s_om;      // head weights                 [kMaxHeads]
+  float* ebar;     long long s_eb;      // normalised energy            [N]
+  float* pc;       long long s_pc;      // spatial coordinates          [N][2]
+  float* bounds;   long long s_bd;      // grid origin/extent           [4]
+  float* y;        long long s_y;       // projected states (bounded)   [N][app_rank]
+  int* clients;    long long s_cl;      // bounded appearance clients   [mv]
+  float* cov;      long long s_cov;     // coverage maxima, ping-pong   [2][M]
+  int* sel;        long long s_sel;     // round that selected i, -1    [N]
+  int* order;      long long s_ord;     // support in selection order   [N]
+  float* part;     long long s_part;    // gains partials               [nc][ldE]
+  int* pool;       long long s_pool;    // current pool                 [pool_cap]
+  float* spart;    long long s_spart;   // responsibility partials      [nc2][pool_cap]
+  int* batch;      long long s_bat;     // last batch                   [b]
+  int* slot;       long long s_slot;    // rank of a selected token     [N]
+  int* sup;        long long s_sup;     // support, ascending           [N]
+  float* cosb;     long long s_cos;     // cos to support               [N][ldK]
+  float* delta;    long long s_del;     // selected-cosine gap          [N]
+  float* dpart;    long long s_dp;      // gap partial sums             [N/64+1]
+  float* gate;     long long s_gate;    // s_x, mean gap                [4]
+  int* pi;         long long s_pi;      // assignment                   [N]
+  float* stats;    long long s_st;      // diagnostics                  [kStats]
+  uint32_t* keys;  long long s_keys;    // top-k keys when N exceeds LDS [N]
+};
+
+}  // namespace gmc

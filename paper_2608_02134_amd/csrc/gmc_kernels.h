@@ -1,0 +1,52 @@
+// Host-side launchers of the GMC kernels (one per stage).  All enqueue on
+// `st` and never synchronise.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "gmc_internal.h"
+
+namespace gmc {
+
+// Stage ids of the measurement timer (see gmc_timing_enable in gmc.h).
+enum Stage {
+  kStProbe = 0, kStLogits, kStHeads, kStAppearance, kStSpatial, kStGains, kStPool, kStResp,
+  kStBatch, kStObjective, kStAssign, kStTransport, kNumStages
+};
+// Records a hipEvent on `st` opening (begin) or closing a stage span when
+// timing is enabled; a no-op otherwise.
+void timer_mark(int stage, bool begin, hipStream_t st);
+
+// Row norms, value probe, mass coordinate, native slice, head weights,
+// grounded row weights and normalised energy.
+hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
+                          const void* text_q, const void* vis_k, const void* probe,
+                          const float* nonvis_lse, float* trace_omega, float* trace_ebar,
+                          hipStream_t st);
+
+// Appearance (exact or bounded) and spatial banks with their row weights.
+hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
+                        const void* app_proj, const int32_t* pos3d, hipStream_t st);
+
+// All selection rounds, then the final coverage and objective values.
+hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
+                            int32_t* trace_batch, hipStream_t st);
+
+// Support list, selected-cosine gaps, separability gate, assignment.
+hipError_t launch_assignment(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
+                             int32_t* trace_assign, hipStream_t st);
+
+// Population weights, weighted centroids, RMS restoration, compaction.
+hipError_t launch_transport(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
+                            const int32_t* pos3d, void* out_hidden, int32_t* out_pos,
+                            int32_t* out_idx, hipStream_t st);
+
+// K = N: copy inputs to outputs.
+hipError_t launch_identity(const Shape& sh, const void* hidden, const int32_t* pos3d,
+                           void* out_hidden, int32_t* out_pos, int32_t* out_idx, hipStream_t st);
+
+// Debug exports: pre-weighted client matrix and per-problem statistics.
+hipError_t launch_trace_exports(const Shape& sh, const Ws& ws, float* trace_client,
+                                float* trace_stats, hipStream_t st);
+
+}  // namespace gmc

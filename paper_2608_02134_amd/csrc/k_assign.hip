@@ -1,0 +1,172 @@
+// Population assignment (Sec. 3.4; App. H Eq. cond-assignment, Eq.
+// cond-population-gate).
+//
+// cos_ij = h_i.h_j / (|h_i| |h_j|) for every token i and support member j
+// comes from an MFMA GEMM against the gathered support rows (normalised after
+// the contraction).  The gap delta_i (best - second best), the sample gate
+// s_x = 1 - exp(-(mean_discarded delta / t)^p) and the local ambiguity g_i
+// then decide kappa_ij = cos_ij + w s_x g_i exp(-|p_i - p_j|^2 / tau_s);
+// pi(i) = argmax_j kappa_ij with ties to the lower source index, and
+// selected tokens represent themselves.
+#include "gmc_device.h"
+#include "gmc_gemm.h"
+#include "gmc_internal.h"
+#include "gmc_kernels.h"
+
+namespace gmc {
+
+// Support in ascending source order and each selected token's slot.
+__global__ void __launch_bounds__(1024) support_kernel(Shape sh, Ws ws) {
+  __shared__ int scan[16];
+  const int p = blockIdx.x, tid = threadIdx.x;
+  const int* sel = ws.sel + p * ws.s_sel;
+  int* slot = ws.slot + p * ws.s_slot;
+  int* sup = ws.sup + p * ws.s_sup;
+  int base = 0;
+  for (int b0 = 0; b0 < sh.N; b0 += blockDim.x) {
+    const int i = b0 + tid;
+    const int f = (i < sh.N && sel[i] >= 0) ? 1 : 0;
+    int tot;
+    const int pos = base + block_exclusive_scan(f, scan, &tot);
+    if (i < sh.N) {
+      slot[i] = f ? pos : -1;
+      if (f) sup[pos] = i;
+    }
+    base += tot;
+  }
+}
+
+struct CosEpi {
+  Ws ws;
+  int ldK;
+  float norm_eps;
+  static constexpr bool kRowStats = false;
+  __device__ void store(int p, int r, int c, float acc) const {
+    const float* n2 = ws.n2 + p * ws.s_n;
+    const int j = ws.sup[p * ws.s_sup + c];
+    ws.cosb[p * ws.s_cos + static_cast<long long>(r) * ldK + c] =
+        acc / (fmaxf(sqrtf(n2[r]), norm_eps) * fmaxf(sqrtf(n2[j]), norm_eps));
+  }
+  __device__ float value(int, int, int, float) const { return 0.f; }
+  __device__ void row_stats(int, int, int, float, float) const {}
+};
+
+// delta_i = top1 - top2 of cos_i. over the support (0 when K = 1); one wave
+// per token; per-block sums of delta over discarded tokens.
+__global__ void __launch_bounds__(256) gap_kernel(Shape sh, Ws ws) {
+  __shared__ float red[4];
+  const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x * 4 + wave;
+  float contrib = 0.f;
+  if (i < sh.N) {
+    const float* c = ws.cosb + p * ws.s_cos + static_cast<long long>(i) * sh.ldK;
+    float t1 = -INFINITY, t2 = -INFINITY;
+    for (int j = lane; j < sh.K; j += 64) {
+      const float v = c[j];
+      if (v > t1) { t2 = t1; t1 = v; }
+      else if (v > t2) t2 = v;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float o1 = __shfl_xor(t1, o, kWave), o2 = __shfl_xor(t2, o, kWave);
+      const float n1 = fmaxf(t1, o1);
+      const float n2 = fmaxf(fminf(t1, o1), fmaxf(t2, o2));
+      t1 = n1;
+      t2 = n2;
+    }
+    const float delta = (sh.K >= 2) ? t1 - t2 : 0.f;
+    if (lane == 0) ws.delta[p * ws.s_del + i] = delta;
+    if (ws.sel[p * ws.s_sel + i] < 0) contrib = delta;
+  }
+  if (lane == 0) red[wave] = contrib;
+  __syncthreads();
+  if (threadIdx.x == 0) ws.dpart[p * ws.s_dp + blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+__global__ void gate_kernel(Shape sh, Params pr, Ws ws, int nblk) {
+  __shared__ float red[16];
+  const int p = blockIdx.x;
+  float s = 0.f;
+  for (int b = threadIdx.x; b < nblk; b += blockDim.x) s += ws.dpart[p * ws.s_dp + b];
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) {
+    const int nd = sh.N - sh.K;
+    const float dbar = nd > 0 ? s / static_cast<float>(nd) : 0.f;
+    const float sx = 1.f - expf(-powf(dbar / pr.gate_t, pr.gate_p));
+    ws.gate[p * ws.s_gate + 0] = sx;
+    ws.gate[p * ws.s_gate + 1] = dbar;
+    ws.stats[p * ws.s_st + 0] = sx;
+    ws.stats[p * ws.s_st + 1] = dbar;
+  }
+}
+
+// pi(i) = argmax_j kappa_ij; one wave per token.
+__global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, int32_t* trace_assign) {
+  const int p = blockIdx.y, lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= sh.N) return;
+  const int* sup = ws.sup + p * ws.s_sup;
+  int pi_i;
+  if (ws.sel[p * ws.s_sel + i] >= 0) {
+    pi_i = i;
+  } else {
+    const float sx = ws.gate[p * ws.s_gate];
+    const float delta = ws.delta[p * ws.s_del + i];
+    const float g = (pr.g_form == 1) ? (delta < pr.amb_margin ? 1.f : 0.f)
+                                     : expf(-powf(delta / pr.amb_margin, pr.amb_p));
+    const float w = pr.spatial_w * sx * g;
+    const float* c = ws.cosb + p * ws.s_cos + static_cast<long long>(i) * sh.ldK;
+    const float* pc = ws.pc + p * ws.s_pc;
+    const float py = pc[2 * i], px = pc[2 * i + 1];
+    const float inv_tau = 1.f / pr.tau_s;
+    float best = -INFINITY;
+    int bj = 0x7fffffff;
+    for (int j = lane; j < sh.K; j += 64) {
+      float k = c[j];
+      if (w > 0.f) {
+        const int sj = sup[j];
+        const float dy = py - pc[2 * sj], dx = px - pc[2 * sj + 1];
+        k += w * expf(-(dy * dy + dx * dx) * inv_tau);
+      }
+      if (k > best) { best = k; bj = j; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o, kWave);
+      const int oj = __shfl_xor(bj, o, kWave);
+      if (ob > best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+    }
+    pi_i = sup[(bj >= 0 && bj < sh.K) ? bj : 0];
+  }
+  if (lane == 0) {
+    ws.pi[p * ws.s_pi + i] = pi_i;
+    if (trace_assign) trace_assign[static_cast<long long>(p) * sh.N + i] = pi_i;
+  }
+}
+
+template <typename T>
+static hipError_t assign_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden_v,
+                              int32_t* trace_assign, hipStream_t st) {
+  timer_mark(kStAssign, true, st);
+  hipLaunchKernelGGL(support_kernel, dim3(sh.B), dim3(1024), 0, st, sh, ws);
+  const T* hidden = static_cast<const T*>(hidden_v);
+  RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
+  RowOperand<T> S{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, ws.sup, ws.s_sup, sh.K};
+  CosEpi epi{ws, sh.ldK, pr.norm_eps};
+  hipError_t err = launch_gemm_nt<T, 64, 64>(A, S, sh.d, sh.B, epi, st);
+  if (err != hipSuccess) return err;
+  const int nblk = (sh.N + 3) / 4;
+  hipLaunchKernelGGL(gap_kernel, dim3(nblk, sh.B), dim3(256), 0, st, sh, ws);
+  hipLaunchKernelGGL(gate_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, nblk);
+  hipLaunchKernelGGL(kappa_kernel, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws, trace_assign);
+  timer_mark(kStAssign, false, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_assignment(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
+                             int32_t* trace_assign, hipStream_t st) {
+  if (sh.dtype == 0) return assign_impl<float>(sh, pr, ws, hidden, trace_assign, st);
+  return assign_impl<bf16_t>(sh, pr, ws, hidden, trace_assign, st);
+}
+
+}  // namespace gmc

@@ -1,0 +1,189 @@
+// Population transport and physical compaction (Sec. 3.4 Eq. transport; App.
+// H Eq. cond-transport, Eq. cond-population-gate, and "Index map and physical
+// token accounting").
+//
+// One block per support member j (slot order = ascending source index):
+// members i with pi(i) = j are found by a ballot scan of pi in ascending
+// order and accumulated as m_i h_i in fp32 registers in that fixed order
+// (bitwise repeatable, no atomics).  Then c_j = acc / M_j, the blend
+// (1 - tau_j) h_j + tau_j c_j, RMS restoration to rms(h_j), one cast to the
+// residual dtype, and the compact write of the state, the original (t,h,w)
+// ids and the source index.  HBM traffic is one read of every member row.
+#include "gmc_device.h"
+#include "gmc_internal.h"
+#include "gmc_kernels.h"
+
+namespace gmc {
+
+template <typename T, int G>
+__global__ void __launch_bounds__(256)
+transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos3d, T* out_hidden,
+                 int32_t* out_pos, int32_t* out_idx) {
+  __shared__ unsigned long long masks[4];
+  __shared__ float red[16];
+  const int jj = blockIdx.x, p = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int j = ws.sup[p * ws.s_sup + jj];
+  const int* pi = ws.pi + p * ws.s_pi;
+  const float* eb = ws.ebar + p * ws.s_eb;
+  const float sx = ws.gate[p * ws.s_gate];
+  const float m0 = 1.f - pr.pop_strength * sx, m1 = pr.pop_strength * sx;
+  const T* H = hidden + static_cast<long long>(p) * sh.N * sh.d;
+  const int ngroups = sh.d / 8;
+  float acc[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
+  float mass = 0.f;
+  for (int i0 = 0; i0 < sh.N; i0 += 256) {
+    const int i = i0 + tid;
+    const bool member = i < sh.N && pi[i] == j;
+    const unsigned long long bal = __ballot(member);
+    __syncthreads();
+    if (lane == 0) masks[wave] = bal;
+    __syncthreads();
+    for (int w = 0; w < 4; ++w) {
+      unsigned long long mk = masks[w];
+      while (mk) {
+        const int b = __ffsll(static_cast<long long>(mk)) - 1;
+        mk &= mk - 1;
+        const int ii = i0 + w * 64 + b;
+        const float mi = m0 + m1 * eb[ii];
+        mass += mi;
+        const T* row = H + static_cast<long long>(ii) * sh.d;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const int grp = tid + g * 256;
+          if (grp < ngroups) {
+            const uint4 raw = ld16(row + grp * 8);
+            if constexpr (sizeof(T) == 2) {
+              const bf16_t* v = reinterpret_cast<const bf16_t*>(&raw);
+#pragma unroll
+              for (int e = 0; e < 8; ++e) acc[g][e] += mi * bf16_to_f32(v[e]);
+            } else {
+              const float* v = reinterpret_cast<const float*>(&raw);
+              const uint4 raw2 = ld16(row + grp * 8 + 4);
+              const float* v2 = reinterpret_cast<const float*>(&raw2);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) { acc[g][e] += mi * v[e]; acc[g][e + 4] += mi * v2[e]; }
+            }
+          }
+        }
+      }
+    }
+  }
+  // blend with the carrier's own state and restore its RMS
+  const T* hj = H + static_cast<long long>(j) * sh.d;
+  const float inv_mass = 1.f / mass;
+  float ss = 0.f;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int grp = tid + g * 256;
+    if (grp < ngroups) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float hv = to_f32<T>(hj[grp * 8 + e]);
+        const float v = (1.f - pr.tau_j) * hv + pr.tau_j * (acc[g][e] * inv_mass);
+        acc[g][e] = v;
+        ss += v * v;
+      }
+    }
+  }
+  ss = block_sum(ss, red);
+  const float rms_v = sqrtf(ss / static_cast<float>(sh.d));
+  const float rms_h = sqrtf(ws.n2[p * ws.s_n + j] / static_cast<float>(sh.d));
+  const float scale = rms_h / (rms_v + pr.restore_eps);
+  T* out = out_hidden + (static_cast<long long>(p) * sh.K + jj) * sh.d;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int grp = tid + g * 256;
+    if (grp < ngroups) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) out[grp * 8 + e] = from_f32<T>(acc[g][e] * scale);
+    }
+  }
+  if (tid < 3) {
+    out_pos[(static_cast<long long>(p) * sh.K + jj) * 3 + tid] =
+        pos3d[(static_cast<long long>(p) * sh.N + j) * 3 + tid];
+  }
+  if (tid == 0) out_idx[static_cast<long long>(p) * sh.K + jj] = j;
+}
+
+template <typename T>
+static hipError_t transport_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
+                                 const int32_t* pos3d, void* out_hidden, int32_t* out_pos,
+                                 int32_t* out_idx, hipStream_t st) {
+  const dim3 grid(sh.K, sh.B);
+  const int groups_per_thread = (sh.d / 8 + 255) / 256;
+  const T* h = static_cast<const T*>(hidden);
+  T* o = static_cast<T*>(out_hidden);
+  timer_mark(kStTransport, true, st);
+  if (groups_per_thread <= 1)
+    hipLaunchKernelGGL((transport_kernel<T, 1>), grid, dim3(256), 0, st, sh, pr, ws, h, pos3d, o, out_pos, out_idx);
+  else if (groups_per_thread <= 2)
+    hipLaunchKernelGGL((transport_kernel<T, 2>), grid, dim3(256), 0, st, sh, pr, ws, h, pos3d, o, out_pos, out_idx);
+  else if (groups_per_thread <= 4)
+    hipLaunchKernelGGL((transport_kernel<T, 4>), grid, dim3(256), 0, st, sh, pr, ws, h, pos3d, o, out_pos, out_idx);
+  else if (groups_per_thread <= 8)
+    hipLaunchKernelGGL((transport_kernel<T, 8>), grid, dim3(256), 0, st, sh, pr, ws, h, pos3d, o, out_pos, out_idx);
+  else
+    return hipErrorInvalidValue;
+  timer_mark(kStTransport, false, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_transport(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
+                            const int32_t* pos3d, void* out_hidden, int32_t* out_pos,
+                            int32_t* out_idx, hipStream_t st) {
+  if (sh.dtype == 0)
+    return transport_impl<float>(sh, pr, ws, hidden, pos3d, out_hidden, out_pos, out_idx, st);
+  return transport_impl<bf16_t>(sh, pr, ws, hidden, pos3d, out_hidden, out_pos, out_idx, st);
+}
+
+// ---------------------------------------------------------------------------
+// K = N identity and debug exports
+// ---------------------------------------------------------------------------
+__global__ void iota_kernel(int32_t* out_idx, int n, int batch) {
+  const long long total = static_cast<long long>(n) * batch;
+  for (long long x = blockIdx.x * static_cast<long long>(blockDim.x) + threadIdx.x; x < total;
+       x += static_cast<long long>(gridDim.x) * blockDim.x)
+    out_idx[x] = static_cast<int32_t>(x % n);
+}
+
+hipError_t launch_identity(const Shape& sh, const void* hidden, const int32_t* pos3d,
+                           void* out_hidden, int32_t* out_pos, int32_t* out_idx, hipStream_t st) {
+  const size_t esz = sh.dtype == 0 ? 4 : 2;
+  hipError_t err = hipMemcpyAsync(out_hidden, hidden, esz * sh.B * sh.N * sh.d, hipMemcpyDeviceToDevice, st);
+  if (err != hipSuccess) return err;
+  err = hipMemcpyAsync(out_pos, pos3d, sizeof(int32_t) * 3 * sh.B * sh.N, hipMemcpyDeviceToDevice, st);
+  if (err != hipSuccess) return err;
+  const long long total = static_cast<long long>(sh.B) * sh.N;
+  const int blocks = static_cast<int>(min(4096LL, (total + 255) / 256));
+  hipLaunchKernelGGL(iota_kernel, dim3(blocks), dim3(256), 0, st, out_idx, sh.N, sh.B);
+  return hipGetLastError();
+}
+
+__global__ void export_client_kernel(Shape sh, Ws ws, float* out) {
+  const int p = blockIdx.z, m = blockIdx.y;
+  const float a = ws.alpha[p * ws.s_m + m];
+  const float* E = ws.E + p * ws.s_E + static_cast<long long>(m) * sh.ldE;
+  float* o = out + (static_cast<long long>(p) * sh.m + m) * sh.N;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < sh.N; i += gridDim.x * blockDim.x) o[i] = a * E[i];
+}
+
+__global__ void export_stats_kernel(Shape sh, Ws ws, float* out) {
+  const int p = blockIdx.x;
+  if (threadIdx.x < kStats) out[p * kStats + threadIdx.x] = ws.stats[p * ws.s_st + threadIdx.x];
+}
+
+hipError_t launch_trace_exports(const Shape& sh, const Ws& ws, float* trace_client, float* trace_stats,
+                                hipStream_t st) {
+  if (trace_client)
+    hipLaunchKernelGGL(export_client_kernel, dim3((sh.N + 255) / 256, sh.m, sh.B), dim3(256), 0, st, sh,
+                       ws, trace_client);
+  if (trace_stats) hipLaunchKernelGGL(export_stats_kernel, dim3(sh.B), dim3(64), 0, st, sh, ws, trace_stats);
+  return hipGetLastError();
+}
+
+}  // namespace gmc

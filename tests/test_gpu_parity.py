@@ -1,0 +1,132 @@
+"""GPU parity: the HIP operator (through the C-ABI) against the fp64 oracle in
+follow mode, on seeded synthetic inputs of the five workloads (full size
+where the oracle finishes in seconds, shrunk but ragged otherwise) and on
+the method's edge cases."""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import gmc_oracle as O
+from paper_2608_02134_amd import synth
+
+from .parity import check_problem
+from .gpu_run import run
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+
+def _announce(name, prob):
+    w = prob.workload
+    print(f"\n[case] {name}: B={w.batch} N={w.n} T={w.t} d={w.d} K={prob.k} dtype={w.dtype}", flush=True)
+
+
+def _check_all(prob, outs, **kw):
+    w = prob.workload
+    reps = []
+    for b, g in enumerate(outs):
+        nv = kw.get("nonvis")
+        rep = check_problem(prob.hidden[b], prob.text_q[b], prob.vis_k[b], prob.pos3d[b], prob.probe,
+                            kw.get("k", prob.k), g, w.dtype, kw.get("params", O.GmcParams()),
+                            prob.app_proj, None if nv is None else nv[b])
+        reps.append(rep)
+        print(f"  problem {b}: {rep}", flush=True)
+    return reps
+
+
+CASES = {
+    "tiny": dict(name="tiny"),
+    "qwen_full": dict(name="qwen"),
+    "qwen_ragged": dict(name="qwen", grid=(1, 20, 21), t=24, k=83),
+    "doc_shrunk": dict(name="doc", grid=(1, 40, 40), t=32, k=320),
+    "batch_shrunk": dict(name="batch16", batch=3, grid=(1, 24, 24), t=16, k=96),
+    "frames_bounded": dict(name="frames", grid=(2, 48, 48), t=16, k=600),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_parity_follow_mode(case):
+    spec = dict(CASES[case])
+    name = spec.pop("name")
+    prob = synth.make_problem(name, **spec)
+    _announce(case, prob)
+    outs, pr = run(prob, torch)
+    try:
+        _check_all(prob, outs)
+    finally:
+        pr.close()
+
+
+def test_identity_when_budget_covers_all_tokens():
+    prob = synth.make_problem("qwen", grid=(1, 9, 9), t=8, k=81)
+    _announce("identity", prob)
+    for k in (81, 500):
+        outs, pr = run(prob, torch, k=k, trace=False)
+        pr.close()
+        g = outs[0]
+        assert np.array_equal(g["out_idx"], np.arange(81))
+        assert np.array_equal(g["out_pos"], prob.pos3d[0])
+        assert np.array_equal(g["out_hidden"], prob.hidden[0])
+
+
+@pytest.mark.parametrize("k", [1, 2, 17])
+def test_small_budgets(k):
+    prob = synth.make_problem("tiny", grid=(1, 7, 9), t=5, k=k)
+    _announce(f"budget{k}", prob)
+    outs, pr = run(prob, torch)
+    pr.close()
+    _check_all(prob, outs, k=k)
+
+
+def test_zero_and_one_text_queries():
+    for t in (0, 1):
+        prob = synth.make_problem("tiny", grid=(1, 11, 13), t=t, k=20)
+        _announce(f"T={t}", prob)
+        outs, pr = run(prob, torch)
+        pr.close()
+        _check_all(prob, outs)
+        if t == 0:
+            assert np.all(outs[0]["ebar"] == 1.0)
+
+
+def test_nonvisual_denominator():
+    prob = synth.make_problem("tiny", grid=(1, 12, 12), t=6, k=30)
+    nonvis = np.random.default_rng(5).standard_normal((1, prob.workload.hq, 6)).astype(np.float32) * 2
+    _announce("nonvis", prob)
+    outs, pr = run(prob, torch, nonvis=nonvis)
+    pr.close()
+    _check_all(prob, outs, nonvis=nonvis)
+
+
+def test_hard_ambiguity_gate():
+    prob = synth.make_problem("tiny", grid=(1, 12, 12), t=6, k=30)
+    _announce("hard gate", prob)
+    outs, pr = run(prob, torch, g_form=1)
+    pr.close()
+    _check_all(prob, outs, params=O.GmcParams(g_form="hard"))
+
+
+def test_bitwise_repeatable():
+    prob = synth.make_problem("qwen", grid=(1, 16, 16), t=16, k=50)
+    _announce("repeat", prob)
+    outs1, pr = run(prob, torch)
+    outs2, _ = run(prob, torch, pruner=pr)
+    pr.close()
+    for key in ("out_hidden", "out_idx", "out_pos", "assign", "client", "round_pool"):
+        assert np.array_equal(outs1[0][key], outs2[0][key]), key
+
+
+def test_capacity_and_argument_errors():
+    from paper_2608_02134_amd import binding
+    prob = synth.make_problem("tiny", grid=(1, 8, 8), t=4, k=10)
+    _announce("errors", prob)
+    outs, pr = run(prob, torch, trace=False)
+    big = synth.make_problem("tiny", grid=(1, 9, 9), t=4, k=10)
+    with pytest.raises(binding.GmcError) as ei:
+        run(big, torch, pruner=pr, trace=False)
+    assert ei.value.code == binding.GMC_ERR_CAPACITY
+    pr.close()
