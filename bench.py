@@ -39,11 +39,11 @@ WORKLOAD_TEXT = {
 }
 
 
-def kernel_work(stage: str, w, m_rows: int, nc: int):
+def kernel_work(stage: str, w, m_rows: int):
     """Algorithmic bytes or flops of one launch of a stage's kernel."""
     n, k, b = w.n, w.k, w.batch
-    if stage == "gains":      # stream the client matrix once, write column partials
-        return "hbm", b * (4.0 * m_rows * n + 4.0 * nc * n + 8.0 * m_rows)
+    if stage == "gains":      # the token-major client matrix once, row weights, coverage, gains
+        return "hbm", b * (4.0 * m_rows * n + 8.0 * m_rows + 4.0 * n)
     if stage == "appearance":  # N x N x d Gram
         return "mfma", b * 2.0 * n * n * w.d
     if stage == "transport":   # every member row once + the compact output
@@ -125,12 +125,9 @@ def main():
               for i, name in enumerate(binding.STAGE_NAMES)}
 
     rounds, pool_cap, bcap, m_rows = binding.gmc_trace_dims(w.n, w.t, w.k)
-    nstrips = -(-w.n // 256)
-    nc = max(1, min(64, -(-1024 // (nstrips * w.batch)), -(-m_rows // 4)))
-    nc = -(-m_rows // (-(-m_rows // nc)))
     single_kernel = ["gains", "appearance", "transport", "logits"]
     dom = max(single_kernel, key=lambda s: stages[s]["ms_per_step"])
-    bound, work = kernel_work(dom, w, m_rows, nc)
+    bound, work = kernel_work(dom, w, m_rows)
     avg_s = stages[dom]["launch_avg_us"] / 1e6
     if bound == "hbm":
         achieved, peak, unit = work / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"

@@ -68,7 +68,7 @@ extern "C" {
  */
 typedef struct gmc_config {
   /* model shape */
-  int32_t d;            /* hidden size, multiple of 32                          */
+  int32_t d;            /* hidden size, multiple of 64                          */
   int32_t n_q_heads;    /* Hq, 1..32                                             */
   int32_t n_kv_heads;   /* Hkv, divides Hq; query head h reads kv head h*Hkv/Hq   */
   int32_t head_dim;     /* dh, multiple of 32, <= 256                            */
@@ -187,10 +187,10 @@ int gmc_trace_dims(int64_t N, int64_t T, int64_t K, int64_t* rounds, int64_t* po
  * hipEvents on the context stream around each stage's launches:
  *   [0] row norms + value probe + mass coordinate   [1] message logits/softmax
  *   [2] head-pattern Gram + head weights + energy  [3] appearance bank GEMM
- *   [4] spatial bank + bank weights                [5] selection gains
- *   [6] selection pool top-k                       [7] responsibility
- *   [8] batch top-k                                [9] objective values
- *   [10] assignment (cosines, gaps, gate, argmax)  [11] transport + compaction
+ *   [4] spatial bank + bank weights                [5] coverage refresh
+ *   [6] singleton gains + candidate pool           [7] responsibility + batch
+ *   [8] final coverage + objective values          [9] assignment
+ *   [10] transport + compaction                    [11] per-call state reset
  * gmc_timing_read synchronises the stream, returns per-stage total
  * milliseconds and span counts accumulated since the last read, and clears
  * them.  Errors: GMC_ERR_STATE, GMC_ERR_ARG (n < GMC_TIMERS), GMC_ERR_HIP.

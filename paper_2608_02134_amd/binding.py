@@ -233,8 +233,8 @@ def gmc_timing_read():
 
 
 GMC_TIMERS = 12
-STAGE_NAMES = ["probe", "logits", "heads", "appearance", "spatial", "gains", "pool", "resp",
-               "batch", "objective", "assign", "transport"]
+STAGE_NAMES = ["probe", "logits", "heads", "appearance", "spatial", "cov", "gains", "resp",
+               "objective", "assign", "transport", "init"]
 SIGNATURES["gmc_timing_enable"] = (ctypes.c_int, [ctypes.c_int])
 SIGNATURES["gmc_timing_read"] = (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64),
                                                 ctypes.c_int32])

@@ -22,7 +22,7 @@ using namespace gmc;
 namespace {
 
 struct Capacity {
-  int B, N, T, K, hq, hr, mv, m, ldE, nc_max, nc2_max, pool_cap, bmax, ldK, rank;
+  int B, N, T, K, hq, hr, mv, m, ldM, pool_cap, bmax, ldK, rank;
   bool bounded_possible;
 };
 
@@ -77,9 +77,6 @@ int fail(int code, const char* fmt, ...) {
   return code;
 }
 
-constexpr int kNcMax = 64;     // gains kernel row chunks
-constexpr int kNc2Max = 256;   // responsibility kernel row chunks
-constexpr int kGainsTargetBlocks = 1024;
 
 long long round_up(long long x, long long a) { return (x + a - 1) / a * a; }
 long long cdiv(long long x, long long a) { return (x + a - 1) / a; }
@@ -102,7 +99,7 @@ Params make_params(const gmc_config& c) {
 
 int validate_config(const gmc_config* c) {
   if (!c) return fail(GMC_ERR_ARG, "gmc_init: cfg is NULL");
-  if (c->d <= 0 || c->d % 32 != 0) return fail(GMC_ERR_ARG, "d=%d must be a positive multiple of 32", c->d);
+  if (c->d <= 0 || c->d % 64 != 0) return fail(GMC_ERR_ARG, "d=%d must be a positive multiple of 64", c->d);
   if (c->d > 256 * 8 * 8) return fail(GMC_ERR_ARG, "d=%d exceeds 16384", c->d);
   if (c->n_q_heads < 1 || c->n_q_heads > kMaxHeads)
     return fail(GMC_ERR_ARG, "n_q_heads=%d must be in [1, %d]", c->n_q_heads, kMaxHeads);
@@ -132,8 +129,8 @@ int validate_config(const gmc_config* c) {
   if (c->bounded_threshold_n < 1) return fail(GMC_ERR_ARG, "bounded_threshold_n must be >= 1");
   if (c->max_n > c->bounded_threshold_n) {
     if (!c->app_projection) return fail(GMC_ERR_ARG, "app_projection is NULL but max_n exceeds the bounded threshold");
-    if (c->app_rank < 32 || c->app_rank % 32 != 0 || c->app_rank > 1024)
-      return fail(GMC_ERR_ARG, "app_rank=%d must be a multiple of 32 in [32, 1024]", c->app_rank);
+    if (c->app_rank < 64 || c->app_rank % 64 != 0 || c->app_rank > 1024)
+      return fail(GMC_ERR_ARG, "app_rank=%d must be a multiple of 64 in [64, 1024]", c->app_rank);
     if (c->app_max_clients < 1) return fail(GMC_ERR_ARG, "app_max_clients must be >= 1");
   }
   return GMC_OK;
@@ -143,8 +140,8 @@ int validate_config(const gmc_config* c) {
 struct Plan {
   Capacity cap;
   long long s_n, s_z, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
-      s_cov, s_sel, s_ord, s_part, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
-      s_pi, s_st, s_keys;
+      s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
+      s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat;
 };
 
 Plan make_plan(const gmc_config& c) {
@@ -160,9 +157,7 @@ Plan make_plan(const gmc_config& c) {
   k.mv = std::max(std::min(c.max_n, c.bounded_threshold_n),
                   k.bounded_possible ? std::min(c.app_max_clients, c.max_n) : 0);
   k.m = k.hq * k.T + k.mv + c.landmarks * c.landmarks;
-  k.ldE = static_cast<int>(round_up(k.N, 4));
-  k.nc_max = kNcMax;
-  k.nc2_max = kNc2Max;
+  k.ldM = static_cast<int>(round_up(k.m, 4));
   k.bmax = std::max(c.batch_b, k.bounded_possible ? c.batch_b_bounded : 0);
   k.pool_cap = c.pool_mult * k.bmax;
   k.ldK = static_cast<int>(round_up(k.K, 4));
@@ -172,8 +167,8 @@ Plan make_plan(const gmc_config& c) {
   pl.s_z = static_cast<long long>(k.N) * k.hr;
   pl.s_sig = kMaxHeads;
   pl.s_ell = static_cast<long long>(k.hq) * k.N;
-  pl.s_E = static_cast<long long>(k.m) * k.ldE;
-  pl.s_m = k.m;
+  pl.s_E = static_cast<long long>(k.N) * k.ldM;
+  pl.s_m = k.ldM;
   pl.s_apart = cdiv(k.N, 64) * k.mv;
   pl.s_gpart = cdiv(k.N, kHeadTok) * npairs;
   pl.s_e2 = static_cast<long long>(k.hq) * k.N;
@@ -183,12 +178,11 @@ Plan make_plan(const gmc_config& c) {
   pl.s_bd = 4;
   pl.s_y = static_cast<long long>(k.N) * k.rank;
   pl.s_cl = k.mv;
-  pl.s_cov = 2LL * k.m;
+  pl.s_cov = k.ldM;
   pl.s_sel = k.N;
   pl.s_ord = k.N;
-  pl.s_part = static_cast<long long>(k.nc_max) * k.ldE;
   pl.s_pool = k.pool_cap;
-  pl.s_spart = std::max<long long>(static_cast<long long>(k.nc2_max) * k.pool_cap, 2 * cdiv(k.m, 256));
+  pl.s_spart = 64 * cdiv(k.ldM, 256);
   pl.s_bat = k.bmax;
   pl.s_slot = k.N;
   pl.s_sup = k.N;
@@ -199,6 +193,10 @@ Plan make_plan(const gmc_config& c) {
   pl.s_pi = k.N;
   pl.s_st = kStats;
   pl.s_keys = k.N;
+  pl.s_u = k.N;
+  pl.s_cnt = kCounters;
+  pl.s_rstat = 3LL * k.ldM;
+  pl.s_lstat = static_cast<long long>(c.landmarks) * c.landmarks;
   return pl;
 }
 
@@ -231,7 +229,7 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   F(cov);
   I(sel);
   ws->order = reinterpret_cast<int*>(take(pl.s_ord, 4)); ws->s_ord = pl.s_ord;
-  F(part); I(pool); F(spart);
+  I(pool); F(spart);
   ws->batch = reinterpret_cast<int*>(take(pl.s_bat, 4)); ws->s_bat = pl.s_bat;
   I(slot); I(sup);
   ws->cosb = reinterpret_cast<float*>(take(pl.s_cos, 4)); ws->s_cos = pl.s_cos;
@@ -241,6 +239,9 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   I(pi);
   ws->stats = reinterpret_cast<float*>(take(pl.s_st, 4)); ws->s_st = pl.s_st;
   ws->keys = reinterpret_cast<uint32_t*>(take(pl.s_keys, 4)); ws->s_keys = pl.s_keys;
+  ws->u = reinterpret_cast<float*>(take(pl.s_u, 4)); ws->s_u = pl.s_u;
+  ws->cnt = reinterpret_cast<int*>(take(pl.s_cnt, 4)); ws->s_cnt = pl.s_cnt;
+  F(rstat); F(lstat);
 #undef F
 #undef I
   return round_up(off, 256);
@@ -343,6 +344,13 @@ int gmc_init(const gmc_config* cfg) {
   }
   ctx->bytes = bytes;
   carve(pl, static_cast<char*>(ctx->mem), &ctx->ws);
+  err = hipMemset(ctx->mem, 0, bytes);
+  if (err == hipSuccess) err = hipDeviceSynchronize();
+  if (err != hipSuccess) {
+    (void)hipFree(ctx->mem);
+    delete ctx;
+    return fail(GMC_ERR_HIP, "gmc_init: clearing the workspace failed (%s)", hipGetErrorString(err));
+  }
   g_ctx = ctx;
   return GMC_OK;
 }
@@ -429,20 +437,11 @@ int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req,
   s.mv = app_rows(g, s.N);
   s.ms = g.landmarks * g.landmarks;
   s.m = s.mg + s.mv + s.ms;
-  s.ldE = static_cast<int>(round_up(N, 4));
+  s.ldM = static_cast<int>(round_up(s.m, 4));
   s.b = s.bounded ? g.batch_b_bounded : g.batch_b;
   s.pool_cap = g.pool_mult * s.b;
   s.rounds = (K < N) ? static_cast<int>(cdiv(K, s.b)) : 0;
   s.ldK = static_cast<int>(round_up(K, 4));
-  s.nstrips = static_cast<int>(cdiv(N, kStripCols));
-  int nc = static_cast<int>(cdiv(kGainsTargetBlocks, static_cast<long long>(s.nstrips) * s.B));
-  nc = std::max(1, std::min({nc, kNcMax, static_cast<int>(cdiv(s.m, 4))}));
-  s.rc = static_cast<int>(cdiv(s.m, nc));
-  s.nc = static_cast<int>(cdiv(s.m, s.rc));
-  int nc2 = static_cast<int>(std::min<long long>(kNc2Max, cdiv(s.m, 32)));
-  nc2 = std::max(1, nc2);
-  s.rc2 = static_cast<int>(cdiv(s.m, nc2));
-  s.nc2 = static_cast<int>(cdiv(s.m, s.rc2));
   s.n_app_cblk = static_cast<int>(cdiv(N, 64));
   s.n_head_blk = static_cast<int>(cdiv(N, kHeadTok));
   s.npairs = s.hq * (s.hq + 1) / 2;
@@ -493,8 +492,9 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
     return GMC_OK;
   }
   const gmc_trace tr = trace ? *trace : gmc_trace{};
-  err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega,
-                       tr.ebar, st);
+  err = launch_call_init(s, c.ws, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "call init: %s", hipGetErrorString(err));
+  err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
   err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
@@ -504,8 +504,8 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "assignment kernels: %s", hipGetErrorString(err));
   err = launch_transport(s, c.pr, c.ws, hidden, pos3d, out_hidden, out_pos, out_idx, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "transport kernels: %s", hipGetErrorString(err));
-  if (tr.client || tr.stats) {
-    err = launch_trace_exports(s, c.ws, tr.client, tr.stats, st);
+  if (tr.client || tr.stats || tr.ebar) {
+    err = launch_trace_exports(s, c.ws, tr.client, tr.stats, tr.ebar, st);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "trace exports: %s", hipGetErrorString(err));
   }
   return GMC_OK;

@@ -173,6 +173,33 @@ __device__ __forceinline__ floatx4 mma(const Frag<float>& a, const Frag<float>& 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
 
+// Device-coherent hand-off between blocks of one kernel.  Data another block
+// reads in the same launch is written with agent-scope relaxed atomic stores
+// (write-through past the per-XCD L2) and read with agent-scope atomic loads,
+// so no L2 writeback/invalidate is needed; ordering against the completion
+// counter comes from waiting for this wave's stores before the block barrier.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Last-block detection: every wave waits until its device-coherent stores
+// have completed, then one counter increment per block; returns true in the
+// block that completes `total` arrivals (uniform across the block).
+__device__ __forceinline__ bool last_arrival(int* counter, int total, int* flag) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *flag = (__hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == total - 1) ? 1 : 0;
+  __syncthreads();
+  return *flag != 0;
+}
+
 // Order-preserving key of a non-negative float score (larger score -> larger
 // key); 0 is reserved for excluded candidates.
 __device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(fmaxf(s, 0.f)) + 1u; }

@@ -5,10 +5,12 @@
 // projected states, states x selected states).  Rows may be gathered through
 // an index list.  A block of 256 threads (4 waves, 2x2) computes a BM x BN
 // tile; each wave owns (BM/2) x (BN/2) as 16x16 MFMA tiles.  K advances in
-// steps of 32; the next global tile is prefetched into registers while the
-// current LDS tile feeds the MFMAs.  The epilogue functor sees every valid
-// output element and may also receive per-row sum/max over the block's
-// columns (for the softmax-style bank normalisers).
+// slabs of 64: global loads run two slabs ahead in two register stages,
+// the LDS tile is double-buffered, one barrier per slab.  Row indices are
+// clamped so every load is unconditional; out-of-range rows and columns are
+// masked in the epilogue.  The epilogue functor gets a per-row and a
+// per-column scale (loaded once per lane) and sees every valid element; it may
+// also receive per-row sum/max over the block's columns.
 #pragma once
 
 #include "gmc_device.h"
@@ -30,33 +32,28 @@ struct RowOperand {
 };
 
 constexpr int kGemmThreads = 256;
-constexpr int kBK = 32;
-
-template <typename T>
-struct GemmSmem {
-  // k-chunk pitch padded by 16 bytes to spread LDS banks between rows
-  static constexpr int kPitch = kBK + 16 / static_cast<int>(sizeof(T));
-};
+constexpr int kBK = 64;
 
 // Epilogue contract:
-//   __device__ void store(int p, int r, int c, float acc) const;
 //   static constexpr bool kRowStats;
-//   __device__ float value(int p, int r, int c, float acc) const;  // if kRowStats
+//   __device__ float row_scale(int p, int r) const;   // r valid
+//   __device__ float col_scale(int p, int c) const;   // c valid
+//   __device__ float value(int p, int r, int c, float acc_scaled) const;  // stores; returns value
 //   __device__ void row_stats(int p, int r, int cblk, float sum, float mx) const;
 template <typename T, int BM, int BN, class Epi>
 __global__ void __launch_bounds__(kGemmThreads)
 gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
-  constexpr int P = GemmSmem<T>::kPitch;
   constexpr int EPC = 16 / sizeof(T);                 // elements per 16-byte chunk
+  constexpr int P = kBK + EPC;                        // LDS row pitch (elements), 16 B pad
   constexpr int CPR = kBK / EPC;                      // chunks per tile row
-  constexpr int A_CHUNKS = BM * CPR / kGemmThreads;   // per thread
+  constexpr int A_CHUNKS = BM * CPR / kGemmThreads;   // per thread per slab
   constexpr int B_CHUNKS = BN * CPR / kGemmThreads;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 16, TN = WN / 16;
   static_assert(A_CHUNKS >= 1 && B_CHUNKS >= 1, "tile too small");
 
-  __shared__ __attribute__((aligned(16))) T As[BM * P];
-  __shared__ __attribute__((aligned(16))) T Bs[BN * P];
+  __shared__ __attribute__((aligned(16))) T As[2][BM * P];
+  __shared__ __attribute__((aligned(16))) T Bs[2][BN * P];
   __shared__ float red_sum[2][BM];
   __shared__ float red_max[2][BM];
 
@@ -70,30 +67,32 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
 #pragma unroll
   for (int i = 0; i < A_CHUNKS; ++i) {
     const int ch = tid + i * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
-    a_src[i] = (row0 + r < A.rows) ? A.row(p, row0 + r) + kc : nullptr;
+    a_src[i] = A.row(p, min(row0 + r, A.rows - 1)) + kc;
   }
 #pragma unroll
   for (int i = 0; i < B_CHUNKS; ++i) {
     const int ch = tid + i * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
-    b_src[i] = (col0 + r < B.rows) ? B.row(p, col0 + r) + kc : nullptr;
+    b_src[i] = B.row(p, min(col0 + r, B.rows - 1)) + kc;
   }
-  uint4 a_reg[A_CHUNKS], b_reg[B_CHUNKS];
-  auto load_global = [&](int k0) {
+  uint4 ra0[A_CHUNKS], rb0[B_CHUNKS], ra1[A_CHUNKS], rb1[B_CHUNKS];
+  const int nk = K / kBK;
+  auto load = [&](int kt, uint4* ra, uint4* rb) {
+    const int k0 = min(kt, nk - 1) * kBK;
 #pragma unroll
-    for (int i = 0; i < A_CHUNKS; ++i) a_reg[i] = a_src[i] ? ld16(a_src[i] + k0) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < A_CHUNKS; ++i) ra[i] = ld16(a_src[i] + k0);
 #pragma unroll
-    for (int i = 0; i < B_CHUNKS; ++i) b_reg[i] = b_src[i] ? ld16(b_src[i] + k0) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < B_CHUNKS; ++i) rb[i] = ld16(b_src[i] + k0);
   };
-  auto store_lds = [&]() {
+  auto store = [&](int buf, const uint4* ra, const uint4* rb) {
 #pragma unroll
     for (int i = 0; i < A_CHUNKS; ++i) {
       const int ch = tid + i * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
-      st16(&As[r * P + kc], a_reg[i]);
+      st16(&As[buf][r * P + kc], ra[i]);
     }
 #pragma unroll
     for (int i = 0; i < B_CHUNKS; ++i) {
       const int ch = tid + i * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
-      st16(&Bs[r * P + kc], b_reg[i]);
+      st16(&Bs[buf][r * P + kc], rb[i]);
     }
   };
 
@@ -103,51 +102,74 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = K / kBK;
-  load_global(0);
-  store_lds();
-  __syncthreads();
   const int fr = lane & 15, fk = (lane >> 4) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) load_global((kt + 1) * kBK);
-    Frag<T> fa[TM], fb[TN];
+  auto compute = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i) fa[i] = frag_load<T>(&As[(wr * WM + i * 16 + fr) * P + fk]);
+    for (int ks = 0; ks < kBK; ks += 32) {
+      Frag<T> fa[TM], fb[TN];
 #pragma unroll
-    for (int j = 0; j < TN; ++j) fb[j] = frag_load<T>(&Bs[(wc * WN + j * 16 + fr) * P + fk]);
+      for (int i = 0; i < TM; ++i) fa[i] = frag_load<T>(&As[buf][(wr * WM + i * 16 + fr) * P + ks + fk]);
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int j = 0; j < TN; ++j) fb[j] = frag_load<T>(&Bs[buf][(wc * WN + j * 16 + fr) * P + ks + fk]);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = mma(fa[i], fb[j], acc[i][j]);
-    __syncthreads();
-    if (kt + 1 < nk) {
-      store_lds();
-      __syncthreads();
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mma(fa[i], fb[j], acc[i][j]);
     }
+  };
+
+  // prologue: slab 0 in LDS buffer 0, slab 1 in flight in registers
+  load(0, ra0, rb0);
+  load(1, ra1, rb1);
+  store(0, ra0, rb0);
+  __syncthreads();
+  // steady state, unrolled by two so the register stages are static:
+  // compute slab kt from LDS while slab kt+2 loads; then slab kt+1 goes to LDS
+  for (int kt = 0; kt < nk; kt += 2) {
+    load(kt + 2, ra0, rb0);
+    compute(0);
+    store(1, ra1, rb1);      // past the last slab this stores a clamped copy, never read
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    load(kt + 3, ra1, rb1);
+    compute(1);
+    store(0, ra0, rb0);
+    __syncthreads();
   }
 
   // epilogue: lane holds column (lane&15), rows 4*(lane>>4)+e of each tile
   const int oc = lane & 15, orow = (lane >> 4) * 4;
-  if constexpr (Epi::kRowStats) {
-    float rs[TM][4], rm[TM][4];
+  float rsc[TM][4], csc[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) { rs[i][e] = 0.f; rm[i][e] = -INFINITY; }
+    for (int e = 0; e < 4; ++e)
+      rsc[i][e] = epi.row_scale(p, min(row0 + wr * WM + i * 16 + orow + e, A.rows - 1));
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+  for (int j = 0; j < TN; ++j) csc[j] = epi.col_scale(p, min(col0 + wc * WN + j * 16 + oc, B.rows - 1));
+
+  float rs[TM][4], rm[TM][4];
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = row0 + wr * WM + i * 16 + orow + e;
-          const int c = col0 + wc * WN + j * 16 + oc;
-          if (r < A.rows && c < B.rows) {
-            const float v = epi.value(p, r, c, acc[i][j][e]);
+    for (int e = 0; e < 4; ++e) { rs[i][e] = 0.f; rm[i][e] = -INFINITY; }
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = row0 + wr * WM + i * 16 + orow + e;
+        const int c = col0 + wc * WN + j * 16 + oc;
+        if (r < A.rows && c < B.rows) {
+          const float v = epi.value(p, r, c, acc[i][j][e] * rsc[i][e] * csc[j]);
+          if constexpr (Epi::kRowStats) {
             rs[i][e] += v;
             rm[i][e] = fmaxf(rm[i][e], v);
           }
         }
+      }
+  if constexpr (Epi::kRowStats) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -167,23 +189,13 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
         epi.row_stats(p, r, blockIdx.x, red_sum[0][rl] + red_sum[1][rl],
                       fmaxf(red_max[0][rl], red_max[1][rl]));
     }
-  } else {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = row0 + wr * WM + i * 16 + orow + e;
-          const int c = col0 + wc * WN + j * 16 + oc;
-          if (r < A.rows && c < B.rows) epi.store(p, r, c, acc[i][j][e]);
-        }
   }
 }
 
 template <typename T, int BM, int BN, class Epi>
 inline hipError_t launch_gemm_nt(const RowOperand<T>& A, const RowOperand<T>& B, int K, int batch,
                                  const Epi& epi, hipStream_t stream) {
+  if (K % kBK != 0) return hipErrorInvalidValue;
   dim3 grid((B.rows + BN - 1) / BN, (A.rows + BM - 1) / BM, batch);
   hipLaunchKernelGGL((gemm_nt_kernel<T, BM, BN, Epi>), grid, dim3(kGemmThreads), 0, stream, A, B, K,
                      epi);

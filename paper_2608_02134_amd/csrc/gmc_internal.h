@@ -11,23 +11,19 @@ constexpr int kMaxHeads = 32;     // Hq limit (head-pattern Gram kept in registe
 constexpr int kMaxProbe = 8;      // probe rank limit
 constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 16;      // tokens per head-Gram block
-constexpr int kStripCols = 256;   // gains kernel: columns per wave strip (64 lanes x 4)
 constexpr int kStats = 8;
+constexpr int kCounters = 8;      // completion counters per problem
 
 // Call shape, resolved on the host for one gmc_prune call.
 struct Shape {
   int B, N, T, K, d, hq, hkv, dh, r, hr;  // hr = hq * r
   int hg;                                 // query heads per kv head
   int mg, mv, ms, m;                      // client rows: grounded, appearance, spatial, total
-  int ldE;                                // client-matrix row stride (floats, multiple of 4)
+  int ldM;                                // token-major client matrix: floats per token (multiple of 4, >= m)
   int bounded;                            // 1: bounded appearance bank
   int app_rank;
   int b, pool_cap, rounds;                // selection batch, pool capacity, rounds
   int ldK;                                // cosine buffer row stride (floats)
-  int nc;                                 // gains kernel row chunks
-  int rc;                                 // rows per gains chunk
-  int nstrips;                            // gains kernel column strips
-  int nc2, rc2;                           // responsibility kernel row chunks
   int n_app_cblk;                         // column blocks of the appearance GEMM
   int n_head_blk;                         // token blocks of the head-Gram kernel
   int npairs;                             // head pairs h <= g
@@ -53,10 +49,10 @@ struct Ws {
   float* z;        long long s_z;       // probe coordinates Z          [N][hr]
   float* sig;      long long s_sig;     // mass coordinate sigma_h      [hq]
   float* ell;      long long s_ell;     // ||[Z_h[i]; sigma_h]||        [hq][N]
-  float* E;        long long s_E;       // client energies              [M][ldE]
-  float* alpha;    long long s_m;       // row pre-weights              [M]
-  float* peak;                          // max_i Cbar_mi                [M]
-  float* rowsum;                        // grounded row sums Z_(h,t)    [M]
+  float* E;        long long s_E;       // client energies, token-major [N][ldM]
+  float* alpha;    long long s_m;       // row pre-weights              [ldM]
+  float* peak;                          // max_i Cbar_mi                [ldM]
+  float* rowsum;                        // grounded row sums Z_(h,t)    [ldM]
   float* apart_sum; float* apart_max; long long s_apart;  // appearance partials [cblk][mv]
   float* gpart;    long long s_gpart;   // head-Gram partials           [blk][npairs]
   float* e2;       long long s_e2;      // sum_t nu_t e^2               [hq][N]
@@ -66,12 +62,11 @@ struct Ws {
   float* bounds;   long long s_bd;      // grid origin/extent           [4]
   float* y;        long long s_y;       // projected states (bounded)   [N][app_rank]
   int* clients;    long long s_cl;      // bounded appearance clients   [mv]
-  float* cov;      long long s_cov;     // coverage maxima, ping-pong   [2][M]
+  float* cov;      long long s_cov;     // coverage maxima b_m          [ldM]
   int* sel;        long long s_sel;     // round that selected i, -1    [N]
   int* order;      long long s_ord;     // support in selection order   [N]
-  float* part;     long long s_part;    // gains partials               [nc][ldE]
   int* pool;       long long s_pool;    // current pool                 [pool_cap]
-  float* spart;    long long s_spart;   // responsibility partials      [nc2][pool_cap]
+  float* spart;    long long s_spart;   // per-block score partials     [ceil(M/256)][64]
   int* batch;      long long s_bat;     // last batch                   [b]
   int* slot;       long long s_slot;    // rank of a selected token     [N]
   int* sup;        long long s_sup;     // support, ascending           [N]
@@ -82,6 +77,10 @@ struct Ws {
   int* pi;         long long s_pi;      // assignment                   [N]
   float* stats;    long long s_st;      // diagnostics                  [kStats]
   uint32_t* keys;  long long s_keys;    // top-k keys when N exceeds LDS [N]
+  float* u;        long long s_u;       // reduced singleton gains      [N]
+  int* cnt;        long long s_cnt;     // completion counters          [kCounters]
+  float* rstat;    long long s_rstat;   // large-pool row statistics    [3][ldM]
+  float* lstat;    long long s_lstat;   // landmark min distance        [L*L]
 };
 
 }  // namespace gmc

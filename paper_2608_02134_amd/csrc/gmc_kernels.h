@@ -10,8 +10,8 @@ namespace gmc {
 
 // Stage ids of the measurement timer (see gmc_timing_enable in gmc.h).
 enum Stage {
-  kStProbe = 0, kStLogits, kStHeads, kStAppearance, kStSpatial, kStGains, kStPool, kStResp,
-  kStBatch, kStObjective, kStAssign, kStTransport, kNumStages
+  kStProbe = 0, kStLogits, kStHeads, kStAppearance, kStSpatial, kStCov, kStGains, kStResp,
+  kStObjective, kStAssign, kStTransport, kStInit, kNumStages
 };
 // Records a hipEvent on `st` opening (begin) or closing a stage span when
 // timing is enabled; a no-op otherwise.
@@ -21,12 +21,15 @@ void timer_mark(int stage, bool begin, hipStream_t st);
 // grounded row weights and normalised energy.
 hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
                           const void* text_q, const void* vis_k, const void* probe,
-                          const float* nonvis_lse, float* trace_omega, float* trace_ebar,
+                          const float* nonvis_lse, float* trace_omega,
                           hipStream_t st);
 
 // Appearance (exact or bounded) and spatial banks with their row weights.
 hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
                         const void* app_proj, const int32_t* pos3d, hipStream_t st);
+
+// Per-call state: nothing selected, completion counters cleared.
+hipError_t launch_call_init(const Shape& sh, const Ws& ws, hipStream_t st);
 
 // All selection rounds, then the final coverage and objective values.
 hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
@@ -47,6 +50,6 @@ hipError_t launch_identity(const Shape& sh, const void* hidden, const int32_t* p
 
 // Debug exports: pre-weighted client matrix and per-problem statistics.
 hipError_t launch_trace_exports(const Shape& sh, const Ws& ws, float* trace_client,
-                                float* trace_stats, hipStream_t st);
+                                float* trace_stats, float* trace_ebar, hipStream_t st);
 
 }  // namespace gmc

@@ -41,13 +41,16 @@ struct CosEpi {
   int ldK;
   float norm_eps;
   static constexpr bool kRowStats = false;
-  __device__ void store(int p, int r, int c, float acc) const {
-    const float* n2 = ws.n2 + p * ws.s_n;
-    const int j = ws.sup[p * ws.s_sup + c];
-    ws.cosb[p * ws.s_cos + static_cast<long long>(r) * ldK + c] =
-        acc / (fmaxf(sqrtf(n2[r]), norm_eps) * fmaxf(sqrtf(n2[j]), norm_eps));
+  __device__ float row_scale(int p, int r) const {
+    return 1.f / fmaxf(sqrtf(ws.n2[p * ws.s_n + r]), norm_eps);
   }
-  __device__ float value(int, int, int, float) const { return 0.f; }
+  __device__ float col_scale(int p, int c) const {
+    return 1.f / fmaxf(sqrtf(ws.n2[p * ws.s_n + ws.sup[p * ws.s_sup + c]]), norm_eps);
+  }
+  __device__ float value(int p, int r, int c, float v) const {
+    ws.cosb[p * ws.s_cos + static_cast<long long>(r) * ldK + c] = v;
+    return v;
+  }
   __device__ void row_stats(int, int, int, float, float) const {}
 };
 

@@ -19,29 +19,29 @@ namespace gmc {
 
 struct AppearanceEpi {
   Ws ws;
-  int ldE;
+  int ldM;
   int row_off;   // first appearance row of the client matrix
   int exact;     // 1: normalise by row norms; 0: operands already unit
   float inv_tau, norm_eps;
   int ncblk;
   int mv;
-  const int* clients;  // bounded: client token of row r
   static constexpr bool kRowStats = true;
-  __device__ float value(int p, int r, int c, float acc) const {
-    float cs = acc;
-    if (exact) {
-      const float* n2 = ws.n2 + p * ws.s_n;
-      cs = acc / (fmaxf(sqrtf(n2[r]), norm_eps) * fmaxf(sqrtf(n2[c]), norm_eps));
-    }
+  // cos = h_m . h_i / (|h_m| |h_i|) on the exact bank (rows are client tokens)
+  __device__ float row_scale(int p, int r) const {
+    return exact ? 1.f / fmaxf(sqrtf(ws.n2[p * ws.s_n + r]), norm_eps) : 1.f;
+  }
+  __device__ float col_scale(int p, int c) const {
+    return exact ? 1.f / fmaxf(sqrtf(ws.n2[p * ws.s_n + c]), norm_eps) : 1.f;
+  }
+  __device__ float value(int p, int r, int c, float cs) const {
     const float v = expf((cs - 1.f) * inv_tau);
-    ws.E[p * ws.s_E + static_cast<long long>(row_off + r) * ldE + c] = v;
+    ws.E[p * ws.s_E + static_cast<long long>(c) * ldM + row_off + r] = v;
     return v;
   }
   __device__ void row_stats(int p, int r, int cblk, float s, float m) const {
     ws.apart_sum[p * ws.s_apart + static_cast<long long>(cblk) * mv + r] = s;
     ws.apart_max[p * ws.s_apart + static_cast<long long>(cblk) * mv + r] = m;
   }
-  __device__ void store(int, int, int, float) const {}
 };
 
 // Bounded bank: raw projection y = R h (fp32 out).
@@ -49,10 +49,12 @@ struct ProjEpi {
   Ws ws;
   int rank;
   static constexpr bool kRowStats = false;
-  __device__ void store(int p, int r, int c, float acc) const {
-    ws.y[p * ws.s_y + static_cast<long long>(r) * rank + c] = acc;
+  __device__ float row_scale(int, int) const { return 1.f; }
+  __device__ float col_scale(int, int) const { return 1.f; }
+  __device__ float value(int p, int r, int c, float v) const {
+    ws.y[p * ws.s_y + static_cast<long long>(r) * rank + c] = v;
+    return v;
   }
-  __device__ float value(int, int, int, float) const { return 0.f; }
   __device__ void row_stats(int, int, int, float, float) const {}
 };
 
@@ -84,6 +86,7 @@ __global__ void __launch_bounds__(256) appearance_alpha_kernel(Shape sh, Params 
   const float* ps = ws.apart_sum + p * ws.s_apart;
   const float* pm = ws.apart_max + p * ws.s_apart;
   float s = 0.f, m = 0.f;
+#pragma unroll 8
   for (int b = 0; b < sh.n_app_cblk; ++b) {
     s += ps[static_cast<long long>(b) * sh.mv + r];
     m = fmaxf(m, pm[static_cast<long long>(b) * sh.mv + r]);
@@ -117,9 +120,11 @@ __global__ void __launch_bounds__(256) spatial_coords_kernel(Shape sh, Ws ws, co
   }
 }
 
-// One block per landmark row: energies exp(-(d^2 - min d^2)/tau_s), row sum,
-// weight (beta_spa / L^2) / Z and peak (the row maximum is exactly 1).
-__global__ void __launch_bounds__(256) spatial_bank_kernel(Shape sh, Params pr, Ws ws) {
+// Spatial bank, landmark side: one block per landmark l_ab = ((a+.5)/L,
+// (b+.5)/L): the minimum squared distance to any token, the row sum of
+// exp(-(d^2 - min d^2)/tau_s), the weight (beta_spa / L^2) / Z and the peak
+// (the row maximum is exactly 1).
+__global__ void __launch_bounds__(256) spatial_stats_kernel(Shape sh, Params pr, Ws ws) {
   __shared__ float red[16];
   const int row = blockIdx.x, p = blockIdx.y;
   const int L = sh.landmarks;
@@ -132,21 +137,38 @@ __global__ void __launch_bounds__(256) spatial_bank_kernel(Shape sh, Params pr, 
     dmin = fminf(dmin, dy * dy + dx * dx);
   }
   dmin = block_min(dmin, red);
-  const int m = sh.mg + sh.mv + row;
-  float* E = ws.E + p * ws.s_E + static_cast<long long>(m) * sh.ldE;
   const float inv_tau = 1.f / pr.tau_s;
   float s = 0.f;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
     const float dy = pc[2 * i] - ly, dx = pc[2 * i + 1] - lx;
-    const float v = expf(-(dy * dy + dx * dx - dmin) * inv_tau);
-    E[i] = v;
-    s += v;
+    s += expf(-(dy * dy + dx * dx - dmin) * inv_tau);
   }
   s = block_sum(s, red);
   if (threadIdx.x == 0) {
+    const int m = sh.mg + sh.mv + row;
     const float a = pr.beta_spa / static_cast<float>(sh.ms) / s;
     ws.alpha[p * ws.s_m + m] = a;
     ws.peak[p * ws.s_m + m] = a;
+    ws.lstat[p * ws.s_lstat + row] = dmin;
+  }
+}
+
+// Spatial bank, token side: one wave per token writes its L^2 landmark
+// energies, contiguous in the token-major client matrix.
+__global__ void __launch_bounds__(256) spatial_write_kernel(Shape sh, Params pr, Ws ws) {
+  const int p = blockIdx.y, i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= sh.N) return;
+  const int L = sh.landmarks;
+  const float* pc = ws.pc + p * ws.s_pc;
+  const float py = pc[2 * i], px = pc[2 * i + 1];
+  const float inv_tau = 1.f / pr.tau_s;
+  const float* dmin = ws.lstat + p * ws.s_lstat;
+  float* E = ws.E + p * ws.s_E + static_cast<long long>(i) * sh.ldM + sh.mg + sh.mv;
+  for (int row = lane; row < sh.ms; row += 64) {
+    const float ly = (static_cast<float>(row / L) + 0.5f) / L;
+    const float lx = (static_cast<float>(row % L) + 0.5f) / L;
+    const float dy = py - ly, dx = px - lx;
+    E[row] = expf(-(dy * dy + dx * dx - dmin[row]) * inv_tau);
   }
 }
 
@@ -158,7 +180,7 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
   timer_mark(kStAppearance, true, st);
   if (!sh.bounded) {
     RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
-    AppearanceEpi epi{ws, sh.ldE, sh.mg, 1, 1.f / pr.tau_v, pr.norm_eps, sh.n_app_cblk, sh.mv, nullptr};
+    AppearanceEpi epi{ws, sh.ldM, sh.mg, 1, 1.f / pr.tau_v, pr.norm_eps, sh.n_app_cblk, sh.mv};
     err = launch_gemm_nt<T, 64, 64>(A, A, sh.d, sh.B, epi, st);
     if (err != hipSuccess) return err;
   } else {
@@ -171,7 +193,7 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
     hipLaunchKernelGGL(clients_kernel, dim3((sh.mv + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
     RowOperand<float> Yc{ws.y, sh.app_rank, ws.s_y, ws.clients, ws.s_cl, sh.mv};
     RowOperand<float> Y{ws.y, sh.app_rank, ws.s_y, nullptr, 0, sh.N};
-    AppearanceEpi epi{ws, sh.ldE, sh.mg, 0, 1.f / pr.tau_v, pr.norm_eps, sh.n_app_cblk, sh.mv, ws.clients};
+    AppearanceEpi epi{ws, sh.ldM, sh.mg, 0, 1.f / pr.tau_v, pr.norm_eps, sh.n_app_cblk, sh.mv};
     err = launch_gemm_nt<float, 64, 64>(Yc, Y, sh.app_rank, sh.B, epi, st);
     if (err != hipSuccess) return err;
   }
@@ -179,7 +201,8 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
   timer_mark(kStSpatial, true, st);
   hipLaunchKernelGGL(appearance_alpha_kernel, dim3((sh.mv + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws);
   hipLaunchKernelGGL(spatial_coords_kernel, dim3(sh.B), dim3(256), 0, st, sh, ws, pos3d);
-  hipLaunchKernelGGL(spatial_bank_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws);
+  hipLaunchKernelGGL(spatial_stats_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws);
+  hipLaunchKernelGGL(spatial_write_kernel, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws);
   timer_mark(kStSpatial, false, st);
   return hipGetLastError();
 }

@@ -22,6 +22,7 @@ __global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* 
   if (i >= sh.N) return;
   const T* row = hidden + (static_cast<long long>(p) * sh.N + i) * sh.d;
   float s = 0.f;
+#pragma unroll 4
   for (int k = lane * 8; k < sh.d; k += 64 * 8) {
     const uint4 raw = ld16(row + k);
     if constexpr (sizeof(T) == 2) {
@@ -48,13 +49,16 @@ struct ProbeEpi {
   Ws ws;
   int d;
   float rms_eps;
-  static constexpr bool kRowStats = false;
   int hr;
-  __device__ void store(int p, int r, int c, float acc) const {
-    const float ms = ws.n2[p * ws.s_n + r] / static_cast<float>(d);
-    ws.z[p * ws.s_z + static_cast<long long>(r) * hr + c] = acc * rsqrtf(ms + rms_eps);
+  static constexpr bool kRowStats = false;
+  __device__ float row_scale(int p, int r) const {
+    return rsqrtf(ws.n2[p * ws.s_n + r] / static_cast<float>(d) + rms_eps);
   }
-  __device__ float value(int, int, int, float) const { return 0.f; }
+  __device__ float col_scale(int, int) const { return 1.f; }
+  __device__ float value(int p, int r, int c, float v) const {
+    ws.z[p * ws.s_z + static_cast<long long>(r) * hr + c] = v;
+    return v;
+  }
   __device__ void row_stats(int, int, int, float, float) const {}
 };
 
@@ -125,26 +129,34 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   const int ntile = (sh.N + 15) / 16;
   const int orow = (lane >> 4) * 4, oc = lane & 15;
 
-  auto tile_logits = [&](int ct) -> floatx4 {
+  // key fragments of a column tile; the column is clamped so the loads are
+  // unconditional (out-of-range columns are masked by the callers), which
+  // lets the next tile's loads overlap the current tile's MFMAs
+  auto load_keys = [&](int ct, Frag<T>* kf) {
+    const int col = min(ct * 16 + fr, sh.N - 1);
+    const T* kr = kbase + col * kstride;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = frag_load<T>(kr + ks * 32 + fk);
+  };
+  auto tile_mma = [&](const Frag<T>* kf) -> floatx4 {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    const int col = ct * 16 + fr;
-    if (col < sh.N) {
-      const T* kr = kbase + col * kstride;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc = mma(qf[ks], frag_load<T>(kr + ks * 32 + fk), acc);
-    } else {
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc = mma(qf[ks], frag_zero<T>(), acc);
-    }
+    for (int ks = 0; ks < KS; ++ks) acc = mma(qf[ks], kf[ks], acc);
     return acc;
   };
+  const int last_tile = ntile - 1;
 
   // pass 1: online (max, sum exp) per row, lane-local over its columns
   float mx[4], sm[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) { mx[e] = -INFINITY; sm[e] = 0.f; }
+  Frag<T> kcur[KS], knext[KS];
+  load_keys(min(wave, last_tile), kcur);
   for (int ct = wave; ct < ntile; ct += 4) {
-    const floatx4 acc = tile_logits(ct);
+    load_keys(min(ct + 4, last_tile), knext);
+    const floatx4 acc = tile_mma(kcur);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kcur[ks] = knext[ks];
     if (ct * 16 + oc < sh.N) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -204,8 +216,12 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   }
   float* E = ws.E + p * ws.s_E;
   const float* ell = ws.ell + p * ws.s_ell;
+  load_keys(min(wave, last_tile), kcur);
   for (int ct = wave; ct < ntile; ct += 4) {
-    const floatx4 acc = tile_logits(ct);
+    load_keys(min(ct + 4, last_tile), knext);
+    const floatx4 acc = tile_mma(kcur);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kcur[ks] = knext[ks];
     const int col = ct * 16 + oc;
     if (col < sh.N) {
 #pragma unroll
@@ -213,7 +229,7 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
         if (!rvalid[e]) continue;
         const float a = expf(acc[e] * scale - D[e]);
         const float v = a * ell[static_cast<long long>(hrow[e]) * sh.N + col];
-        E[mrow[e] * sh.ldE + col] = v;
+        E[static_cast<long long>(col) * sh.ldM + mrow[e]] = v;
         rsum[e] += v;
         rmax[e] = fmaxf(rmax[e], v);
       }
@@ -273,11 +289,22 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
   for (int t0 = 0; t0 < T; t0 += kTC) {
     const int tc = min(kTC, T - t0);
     __syncthreads();
-    for (int x = tid; x < H * kTC * kHeadTok; x += 256) {
-      const int ii = x % kHeadTok, tt = (x / kHeadTok) % kTC, h = x / (kHeadTok * kTC);
-      float v = 0.f;
-      if (tt < tc && i0 + ii < sh.N) v = E[(static_cast<long long>(h) * T + t0 + tt) * sh.ldE + i0 + ii];
-      tileE[x] = v;
+    // unconditional (clamped) loads, masked afterwards, so they all issue together
+    constexpr int kPer = (kMaxHeads * kTC * kHeadTok) / 256;
+    float vals[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int x = tid + q * 256;
+      const int tt = x % kTC, h = (x / kTC) % kMaxHeads, ii = x / (kTC * kMaxHeads);
+      const int hc = min(h, H - 1), tc_ = min(tt, tc - 1), ic = min(i0 + ii, sh.N - 1);
+      vals[q] = E[static_cast<long long>(ic) * sh.ldM + hc * T + t0 + tc_];
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int x = tid + q * 256;
+      const int tt = x % kTC, h = (x / kTC) % kMaxHeads, ii = x / (kTC * kMaxHeads);
+      const bool ok = h < H && tt < tc && i0 + ii < sh.N;
+      tileE[(h * kTC + tt) * kHeadTok + ii] = ok ? vals[q] : 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -339,120 +366,125 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
 }
 
 // ---------------------------------------------------------------------------
-// Head clustering, head weights, grounded row weights and energy.
-// One block per problem.  Gamma is reduced from the per-block partials in a
-// fixed order; farthest-first clustering runs on one thread (Hq <= 32).
+// Head clustering, head weights and grounded row weights.  One block per
+// problem: Gamma is reduced from the per-block partials in block order
+// (many loads in flight per thread), then one wave runs farthest-first with
+// lane h owning head h (wave-wide argmax/argmin with lowest-index ties).
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega,
-                                                      float* trace_ebar) {
-  __shared__ float gam[kMaxHeads][kMaxHeads];
-  __shared__ float cosm[kMaxHeads][kMaxHeads];
-  __shared__ float abar[kMaxHeads];
+__device__ __forceinline__ void wave_argbest(float& v, int& idx, bool want_max) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(v, o, kWave);
+    const int oi = __shfl_xor(idx, o, kWave);
+    const bool better = want_max ? (ov > v || (ov == v && oi < idx)) : (ov < v || (ov == v && oi < idx));
+    if (better) { v = ov; idx = oi; }
+  }
+}
+
+__global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
+  __shared__ float gam[kMaxHeads][kMaxHeads + 1];
+  __shared__ float cosm[kMaxHeads][kMaxHeads + 1];
   __shared__ float om[kMaxHeads];
-  __shared__ float red[16];
+  __shared__ int asg[kMaxHeads];
   const int p = blockIdx.x, tid = threadIdx.x, H = sh.hq, T = sh.T;
   const float* gp = ws.gpart + p * ws.s_gpart;
+  const int nb = sh.n_head_blk;
   for (int q = tid; q < sh.npairs; q += blockDim.x) {
     int h = 0, rem = q;
     while (rem >= H - h) { rem -= H - h; ++h; }
     const int g = h + rem;
     float s = 0.f;
-    for (int b = 0; b < sh.n_head_blk; ++b) s += gp[static_cast<long long>(b) * sh.npairs + q];
+    int b = 0;
+    for (; b + 8 <= nb; b += 8) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = gp[static_cast<long long>(b + j) * sh.npairs + q];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    for (; b < nb; ++b) s += gp[static_cast<long long>(b) * sh.npairs + q];
     gam[h][g] = s;
     gam[g][h] = s;
   }
-  const float* rowsum = ws.rowsum + p * ws.s_m;
-  for (int h = tid; h < H; h += blockDim.x) {
-    float s = 0.f;
-    for (int t = 0; t < T; ++t) s += rowsum[h * T + t];
-    abar[h] = s / (static_cast<float>(T) * sh.N);
-  }
   __syncthreads();
-  if (tid == 0) {
-    bool active[kMaxHeads];
-    int n_active = 0;
-    float nrm[kMaxHeads];
-    for (int h = 0; h < H; ++h) {
-      active[h] = gam[h][h] > 0.f;
-      n_active += active[h];
-      nrm[h] = active[h] ? sqrtf(gam[h][h]) : 1.f;
-      om[h] = 0.f;
+  const float* rowsum = ws.rowsum + p * ws.s_m;
+  if (tid < 64) {
+    const int lane = tid, h = lane;
+    const bool valid = h < H;
+    // mean atom norm abar_h = sum_t Z_(h,t) / (T N) and activity
+    float abar = 0.f;
+    if (valid) {
+#pragma unroll 16
+      for (int t = 0; t < T; ++t) abar += rowsum[h * T + t];
+      abar /= static_cast<float>(T) * sh.N;
     }
-    for (int h = 0; h < H; ++h)
-      for (int g = 0; g < H; ++g) cosm[h][g] = gam[h][g] / (nrm[h] * nrm[g]);
+    const float ghh = valid ? gam[h][h] : 0.f;
+    const bool active = valid && ghh > 0.f;
+    const float nrm = active ? sqrtf(ghh) : 1.f;
+    if (valid)
+      for (int g = 0; g < H; ++g) {
+        const float gg = gam[g][g];
+        cosm[h][g] = gam[h][g] / (nrm * (gg > 0.f ? sqrtf(gg) : 1.f));
+      }
+    const int n_active = __popcll(__ballot(active));
+    float w_h = 0.f;
+    int cl = -1;
     if (n_active > 0) {
+      // first centre: largest pre-normalisation pattern sqrt(beta Gamma_hh) / abar_h
+      float v = active ? sqrtf(pr.beta_msg * ghh) / (abar > 0.f ? abar : 1.f) : -INFINITY;
+      int idx = active ? h : 0x7fffffff;
+      wave_argbest(v, idx, true);
       int centres[kMaxHeads];
       int nc = 0;
-      // first centre: largest pre-normalisation pattern sqrt(beta Gamma_hh) / abar_h
-      float best = -INFINITY;
-      int bi = -1;
-      for (int h = 0; h < H; ++h) {
-        if (!active[h]) continue;
-        const float v = sqrtf(pr.beta_msg * gam[h][h]) / (abar[h] > 0.f ? abar[h] : 1.f);
-        if (v > best) { best = v; bi = h; }
-      }
-      if (bi < 0) bi = 0;
-      centres[nc++] = bi;
+      centres[nc++] = idx;
+      bool is_c = h == idx;
+      float maxcos = valid ? cosm[h][idx] : -INFINITY;
       const int want = min(pr.max_head_clusters, n_active);
       while (nc < want) {
-        float bv = INFINITY;
-        int bh = -1;
-        for (int h = 0; h < H; ++h) {
-          if (!active[h]) continue;
-          bool is_c = false;
-          for (int c = 0; c < nc; ++c) is_c |= centres[c] == h;
-          if (is_c) continue;
-          float v = -INFINITY;
-          for (int c = 0; c < nc; ++c) v = fmaxf(v, cosm[h][centres[c]]);
-          if (v < bv) { bv = v; bh = h; }
-        }
-        if (bh < 0) break;
-        centres[nc++] = bh;
+        float cv = (active && !is_c) ? maxcos : INFINITY;
+        int ci = (active && !is_c) ? h : 0x7fffffff;
+        wave_argbest(cv, ci, false);
+        if (ci == 0x7fffffff) break;
+        centres[nc++] = ci;
+        is_c |= h == ci;
+        if (valid) maxcos = fmaxf(maxcos, cosm[h][ci]);
       }
-      int assign[kMaxHeads];
-      int count[kMaxHeads];
-      for (int c = 0; c < nc; ++c) count[c] = 0;
-      for (int h = 0; h < H; ++h) {
-        assign[h] = -1;
-        if (!active[h]) continue;
-        int bc = 0;
+      if (active) {
         float bv = cosm[h][centres[0]];
+        cl = 0;
         for (int c = 1; c < nc; ++c)
-          if (cosm[h][centres[c]] > bv) { bv = cosm[h][centres[c]]; bc = c; }
-        assign[h] = bc;
-        ++count[bc];
+          if (cosm[h][centres[c]] > bv) { bv = cosm[h][centres[c]]; cl = c; }
       }
+      if (valid) asg[h] = cl;
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      // clusters, dispersion d_h = 1 - u_h . mu_c and inverse-dispersion weights
       int n_clusters = 0;
-      for (int c = 0; c < nc; ++c) n_clusters += count[c] > 0;
+      for (int c = 0; c < nc; ++c) n_clusters += __ballot(cl == c) != 0ull;
+      float s_h = 0.f;
+      if (cl >= 0)
+        for (int g = 0; g < H; ++g)
+          if (asg[g] == cl) s_h += cosm[h][g];
+      float inv = 0.f;
       for (int c = 0; c < nc; ++c) {
-        if (count[c] == 0) continue;
-        float tot = 0.f;
-        for (int h = 0; h < H; ++h)
-          if (assign[h] == c)
-            for (int g = 0; g < H; ++g)
-              if (assign[g] == c) tot += cosm[h][g];
-        const float mean_norm = sqrtf(fmaxf(tot, 0.f));
-        float inv[kMaxHeads];
-        float isum = 0.f;
-        for (int h = 0; h < H; ++h) {
-          if (assign[h] != c) continue;
-          float s = 0.f;
-          for (int g = 0; g < H; ++g)
-            if (assign[g] == c) s += cosm[h][g];
-          const float disp = 1.f - s / mean_norm;
-          inv[h] = 1.f / (disp + pr.disp_eps);
-          isum += inv[h];
+        const float tot = wave_sum(cl == c ? s_h : 0.f);
+        if (cl == c) {
+          const float disp = 1.f - s_h / sqrtf(fmaxf(tot, 0.f));
+          inv = 1.f / (disp + pr.disp_eps);
         }
-        for (int h = 0; h < H; ++h)
-          if (assign[h] == c) om[h] = inv[h] / isum / static_cast<float>(n_clusters);
       }
+      for (int c = 0; c < nc; ++c) {
+        const float isum = wave_sum(cl == c ? inv : 0.f);
+        if (cl == c) w_h = inv / isum / static_cast<float>(n_clusters);
+      }
+    }
+    if (valid) {
+      om[h] = w_h;
+      ws.omega[p * ws.s_om + h] = w_h;
+      if (trace_omega) trace_omega[static_cast<long long>(p) * H + h] = w_h;
     }
   }
   __syncthreads();
-  for (int h = tid; h < H; h += blockDim.x) {
-    ws.omega[p * ws.s_om + h] = om[h];
-    if (trace_omega) trace_omega[static_cast<long long>(p) * H + h] = om[h];
-  }
   // grounded row weights beta_msg omega_h nu_t a_(h,t) / Z_(h,t)
   const float nu_o = 1.f / (T - 1 + pr.terminal_q_weight);
   for (int m = tid; m < sh.mg; m += blockDim.x) {
@@ -463,40 +495,54 @@ __global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws
     ws.alpha[p * ws.s_m + m] = a;
     ws.peak[p * ws.s_m + m] *= a;
   }
-  // e_i = sqrt(sum_h omega_h sum_t nu_t e^2); ebar = e / mean(e), fallback 1
-  const float* e2 = ws.e2 + p * ws.s_e2;
-  float local = 0.f;
-  for (int i = tid; i < sh.N; i += blockDim.x) {
+}
+
+// Grounded energy e_i = sqrt(sum_h omega_h sum_t nu_t e^2) for every token
+// (Eq. cond-grounded-energy) with per-block sums; the last block forms the
+// mean and stores 1/mean (0 selects the uniform fallback ebar = 1).
+__global__ void __launch_bounds__(256) energy_kernel(Shape sh, Ws ws) {
+  __shared__ float red[16];
+  __shared__ float om[kMaxHeads];
+  __shared__ int flag;
+  const int p = blockIdx.y, tid = threadIdx.x;
+  if (tid < sh.hq) om[tid] = ws.omega[p * ws.s_om + tid];
+  __syncthreads();
+  const int i = blockIdx.x * 256 + tid;
+  float e = 0.f;
+  if (i < sh.N) {
+    const float* e2 = ws.e2 + p * ws.s_e2;
     float s = 0.f;
-    for (int h = 0; h < H; ++h) s += om[h] * e2[static_cast<long long>(h) * sh.N + i];
-    local += sqrtf(s);
+#pragma unroll 8
+    for (int h = 0; h < sh.hq; ++h) s += om[h] * e2[static_cast<long long>(h) * sh.N + i];
+    e = sqrtf(s);
+    ws.ebar[p * ws.s_eb + i] = e;
   }
-  const float mean = block_sum(local, red) / static_cast<float>(sh.N);
-  float* eb = ws.ebar + p * ws.s_eb;
-  for (int i = tid; i < sh.N; i += blockDim.x) {
-    float v = 1.f;
-    if (mean > 0.f) {
-      float s = 0.f;
-      for (int h = 0; h < H; ++h) s += om[h] * e2[static_cast<long long>(h) * sh.N + i];
-      v = sqrtf(s) / mean;
-    }
-    eb[i] = v;
-    if (trace_ebar) trace_ebar[static_cast<long long>(p) * sh.N + i] = v;
+  const float bs = block_sum(e, red);
+  float* ep = ws.dpart + p * ws.s_dp;   // free until the assignment stage
+  if (tid == 0) st_dev(&ep[blockIdx.x], bs);
+  int* cnt = ws.cnt + p * ws.s_cnt + 3;
+  if (!last_arrival(cnt, gridDim.x, &flag)) return;
+  if (tid == 0) {
+    st_dev(cnt, 0);
+    float s = 0.f;
+    for (unsigned b = 0; b < gridDim.x; ++b) s += ld_dev(&ep[b]);
+    const float mean = s / static_cast<float>(sh.N);
+    ws.gate[p * ws.s_gate + 2] = (mean > 0.f) ? 1.f / mean : 0.f;
   }
 }
 
-// Empty grounded bank (T = 0): omega = 0, ebar = 1.
-__global__ void no_grounded_kernel(Shape sh, Ws ws, float* trace_omega, float* trace_ebar) {
+// Empty grounded bank (T = 0): omega = 0 and uniform energy ebar = 1.
+__global__ void no_grounded_kernel(Shape sh, Ws ws, float* trace_omega) {
   const int p = blockIdx.y;
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < sh.N; i += gridDim.x * blockDim.x) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < sh.N; i += gridDim.x * blockDim.x)
     ws.ebar[p * ws.s_eb + i] = 1.f;
-    if (trace_ebar) trace_ebar[static_cast<long long>(p) * sh.N + i] = 1.f;
-  }
-  if (blockIdx.x == 0)
+  if (blockIdx.x == 0) {
     for (int h = threadIdx.x; h < sh.hq; h += blockDim.x) {
       ws.omega[p * ws.s_om + h] = 0.f;
       if (trace_omega) trace_omega[static_cast<long long>(p) * sh.hq + h] = 0.f;
     }
+    if (threadIdx.x == 0) ws.gate[p * ws.s_gate + 2] = 1.f;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -505,7 +551,7 @@ __global__ void no_grounded_kernel(Shape sh, Ws ws, float* trace_omega, float* t
 template <typename T>
 static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden_v,
                                const void* text_q_v, const void* vis_k_v, const void* probe_v,
-                               const float* nonvis_lse, float* trace_omega, float* trace_ebar,
+                               const float* nonvis_lse, float* trace_omega,
                                hipStream_t st) {
   const T* hidden = static_cast<const T*>(hidden_v);
   timer_mark(kStProbe, true, st);
@@ -520,7 +566,7 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   if (sh.T == 0) {
     timer_mark(kStHeads, true, st);
     hipLaunchKernelGGL(no_grounded_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws,
-                       trace_omega, trace_ebar);
+                       trace_omega);
     timer_mark(kStHeads, false, st);
     return hipGetLastError();
   }
@@ -542,20 +588,19 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   timer_mark(kStLogits, false, st);
   timer_mark(kStHeads, true, st);
   hipLaunchKernelGGL(headgram_kernel, dim3(sh.n_head_blk, sh.B), dim3(256), 0, st, sh, pr, ws);
-  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, trace_omega, trace_ebar);
+  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, trace_omega);
+  hipLaunchKernelGGL(energy_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
   timer_mark(kStHeads, false, st);
   return hipGetLastError();
 }
 
 hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
                           const void* text_q, const void* vis_k, const void* probe,
-                          const float* nonvis_lse, float* trace_omega, float* trace_ebar,
+                          const float* nonvis_lse, float* trace_omega,
                           hipStream_t st) {
   if (sh.dtype == 0)
-    return message_impl<float>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega,
-                               trace_ebar, st);
-  return message_impl<bf16_t>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega,
-                              trace_ebar, st);
+    return message_impl<float>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, st);
+  return message_impl<bf16_t>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, st);
 }
 
 }  // namespace gmc

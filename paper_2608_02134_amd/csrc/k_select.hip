@@ -1,17 +1,24 @@
 // Batched responsibility selection (Sec. 3.3 Eq. coverage, Eq.
 // responsibility; App. H Eq. cond-responsibility and the totality rule).
 //
-// Client row m has weight alpha_m and energies E_m, so Cbar_mi = alpha_m E_mi
-// is formed on the fly; coverage maxima b_m live in a ping-pong pair.  One
-// round is four kernels:
-//   gains  - refresh b_m with the previous batch, then partial column sums of
-//            R_mi = [Cbar_mi - b_m]_+ over row chunks (float4 streaming)
-//   pool   - one block per problem: fixed-order sum of the partials, then a
-//            deterministic radix top-k of (gain desc, index asc) over the
-//            unselected tokens
-//   resp   - responsibility softmax of R over the pool per client row,
-//            partial column sums of rho R over row chunks
-//   batch  - one block per problem: top-b of the pool scores, mark them
+// The client energies are stored token-major, Et[i][m] (row stride ldM), and
+// Cbar_mi = alpha_m Et[i][m] is formed on the fly.  Token-major makes every
+// token's singleton gain u_i = sum_m [Cbar_mi - b_m]_+ one contiguous
+// reduction owned by a single wave, so no cross-block partial sums exist.
+// One round:
+//   cov   - b_m <- max(b_m, max_{j in previous batch} Cbar_mj), rows in parallel,
+//           batch columns split over blocks; in-place atomicMax on the bit
+//           pattern (non-negative floats order like their bits), so the
+//           result is independent of arrival order
+//   gains - u_i per token; the last block picks the pool, the min(4b, N-|S|)
+//           largest gains of unselected tokens (ties to the lower index)
+//   resp  - pool of at most 64: one lane per client row computes the
+//           responsibility softmax of R over the pool and its contributions
+//           rho R; a butterfly transpose-reduction sums them per pool token;
+//           the last block adds the block sums in order and picks the batch.
+//           Larger pools (bounded path): per-row max and softmax denominator
+//           first (rowstat), then one wave per pool token sums its column
+//           (colsum), the last block picks the batch.
 // Every reduction has a fixed order, so results are bitwise repeatable.
 // Zero-gain tokens key just above excluded ones, so once gains vanish the
 // lowest source indices fill the budget.
@@ -21,306 +28,454 @@
 
 namespace gmc {
 
-constexpr int kSubRows = 256;
+constexpr int kCpw = 2;                 // gains kernel: tokens per wave
+constexpr int kGainCols = 4 * kCpw;     // tokens per block
+constexpr int kLdsKeys = 12288;         // pool top-k keys live in LDS up to this N
 
-__global__ void __launch_bounds__(256) gains_kernel(Shape sh, Ws ws, int round, int prev_b) {
-  __shared__ float cov_s[kSubRows];
-  __shared__ float4 wsum[4][64];
-  const int p = blockIdx.y;
-  const int strip = blockIdx.x % sh.nstrips, chunk = blockIdx.x / sh.nstrips;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int r0 = chunk * sh.rc, r1 = min(sh.m, r0 + sh.rc);
-  const float* cov_in = ws.cov + p * ws.s_cov + (round & 1) * sh.m;
-  float* cov_out = ws.cov + p * ws.s_cov + ((round + 1) & 1) * sh.m;
-  const int* prev = ws.batch + p * ws.s_bat;
-  const float* E = ws.E + p * ws.s_E;
-  const float* alpha = ws.alpha + p * ws.s_m;
-  const int c0 = strip * kStripCols + lane * 4;
-  const bool col_ok = c0 < sh.N;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s0 = r0; s0 < r1; s0 += kSubRows) {
-    const int n = min(kSubRows, r1 - s0);
-    __syncthreads();
-    if (tid < n) {
-      const int m = s0 + tid;
-      const float a = alpha[m];
-      float c = (round == 0) ? 0.f : cov_in[m];
-      const float* Em = E + static_cast<long long>(m) * sh.ldE;
-      for (int j = 0; j < prev_b; ++j) c = fmaxf(c, a * Em[prev[j]]);
-      cov_s[tid] = c;
-      if (strip == 0) cov_out[m] = c;
-    }
-    __syncthreads();
-    if (col_ok) {
-      for (int rr = wave; rr < n; rr += 4) {
-        const int m = s0 + rr;
-        const float a = alpha[m], c = cov_s[rr];
-        const float4 v = *reinterpret_cast<const float4*>(E + static_cast<long long>(m) * sh.ldE + c0);
-        acc.x += fmaxf(a * v.x - c, 0.f);
-        acc.y += fmaxf(a * v.y - c, 0.f);
-        acc.z += fmaxf(a * v.z - c, 0.f);
-        acc.w += fmaxf(a * v.w - c, 0.f);
-      }
-    }
-  }
-  wsum[wave][lane] = acc;
-  __syncthreads();
-  if (wave == 0 && col_ok) {
-    float4 s = wsum[0][lane];
-    for (int w = 1; w < 4; ++w) {
-      const float4 t = wsum[w][lane];
-      s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
-    }
-    *reinterpret_cast<float4*>(ws.part + p * ws.s_part + static_cast<long long>(chunk) * sh.ldE + c0) = s;
-  }
-}
-
-// Deterministic block top-k over n keys held in LDS: the `count` largest
+// Deterministic top-k over n keys (256-thread block): the `count` largest
 // keys, equal keys resolved to the lower index.  Indices are written in
 // ascending order to out[0..count).  count must not exceed the number of
-// non-zero keys.  Uses radix selection of the threshold key (4 passes of
-// 8-bit digits) and ordered compaction in rounds of blockDim.x indices.
-__device__ void block_topk(const uint32_t* keys, int n, int count, int* out, int* hist, int* scan,
-                           int* bcast) {
-  const int tid = threadIdx.x, nt = blockDim.x;
+// non-zero keys.  Radix selection of the threshold key (4 passes of 8-bit
+// digits, parallel digit search), then one packed scan for the ordered
+// compaction (each thread owns a contiguous index segment).
+__device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, int* hist, int* scan,
+                              int* bc) {
+  const int tid = threadIdx.x;
   uint32_t prefix = 0, mask = 0;
   int remaining = count;
   for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int b = tid; b < 256; b += nt) hist[b] = 0;
+    hist[tid] = 0;
     __syncthreads();
-    for (int i = tid; i < n; i += nt) {
+    for (int i = tid; i < n; i += 256) {
       const uint32_t k = keys[i];
       if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
     }
     __syncthreads();
-    if (tid == 0) {
-      int cum = 0, d = 255;
-      for (; d > 0; --d) {
-        if (cum + hist[d] >= remaining) break;
-        cum += hist[d];
-      }
-      bcast[0] = d;
-      bcast[1] = remaining - cum;
+    const int d = 255 - tid;
+    const int v = hist[d];
+    int tot;
+    const int excl = block_exclusive_scan(v, scan, &tot);
+    if (excl < remaining && remaining <= excl + v) {
+      bc[0] = d;
+      bc[1] = remaining - excl;
     }
     __syncthreads();
-    prefix |= static_cast<uint32_t>(bcast[0]) << shift;
+    prefix |= static_cast<uint32_t>(bc[0]) << shift;
     mask |= 0xFFu << shift;
-    remaining = bcast[1];
+    remaining = bc[1];
     __syncthreads();
   }
   const uint32_t kth = prefix;
-  int eq_seen = 0, written = 0;
-  for (int b0 = 0; b0 < n; b0 += nt) {
-    const int i = b0 + tid;
-    const uint32_t k = (i < n) ? keys[i] : 0u;
-    const int is_eq = (i < n && k == kth) ? 1 : 0;
-    int eq_tot;
-    const int eq_before = eq_seen + block_exclusive_scan(is_eq, scan, &eq_tot);
-    const int take = (i < n) && (k > kth || (is_eq && eq_before < remaining));
-    int tot;
-    const int pos = written + block_exclusive_scan(take, scan, &tot);
-    if (take) out[pos] = i;
-    eq_seen += eq_tot;
-    written += tot;
+  const int seg = (n + 255) / 256;
+  const int i0 = min(n, tid * seg), i1 = min(n, i0 + seg);
+  int gt = 0, eq = 0;
+  for (int i = i0; i < i1; ++i) {
+    const uint32_t k = keys[i];
+    gt += k > kth;
+    eq += k == kth;
+  }
+  int tot;
+  const int pre = block_exclusive_scan(gt | (eq << 16), scan, &tot);
+  int gt_b = static_cast<int>(static_cast<unsigned>(pre) & 0xFFFFu);
+  int eq_b = static_cast<int>(static_cast<unsigned>(pre) >> 16);
+  for (int i = i0; i < i1; ++i) {
+    const uint32_t k = keys[i];
+    if (k > kth) {
+      out[gt_b + min(eq_b, remaining)] = i;
+      ++gt_b;
+    } else if (k == kth) {
+      if (eq_b < remaining) out[gt_b + eq_b] = i;
+      ++eq_b;
+    }
   }
   __syncthreads();
 }
 
-// Keys live in LDS when N fits (kLdsKeys), else in the workspace (L2).
-constexpr int kLdsKeys = 12288;
+// ---------------------------------------------------------------------------
+// coverage refresh with a batch
+// ---------------------------------------------------------------------------
+constexpr int kCovCols = 32;   // batch columns per block
 
+__global__ void __launch_bounds__(256) cov_kernel(Shape sh, Ws ws, int nb) {
+  const int p = blockIdx.z, m = blockIdx.x * 256 + threadIdx.x;
+  if (m >= sh.m) return;
+  const int j0 = blockIdx.y * kCovCols, j1 = min(nb, j0 + kCovCols);
+  const float a = ws.alpha[p * ws.s_m + m];
+  const int* bat = ws.batch + p * ws.s_bat;
+  const float* E = ws.E + p * ws.s_E + m;
+  float c = 0.f;
+  for (int j = j0; j < j1; ++j) c = fmaxf(c, a * E[static_cast<long long>(bat[j]) * sh.ldM]);
+  atomicMax(reinterpret_cast<unsigned*>(&ws.cov[p * ws.s_cov + m]), __float_as_uint(c));
+}
+
+// ---------------------------------------------------------------------------
+// singleton gains and the pool
+// ---------------------------------------------------------------------------
 template <bool kGlobalKeys>
-__global__ void __launch_bounds__(1024) pool_kernel(Shape sh, Ws ws, int round, int psize,
-                                                    int32_t* trace_pool) {
+__global__ void __launch_bounds__(256)
+gains_kernel(Shape sh, Ws ws, int round, int psize, int32_t* trace_pool) {
   extern __shared__ uint32_t keys_lds[];
-  __shared__ int hist[256], scan[16], bcast[2];
-  const int p = blockIdx.x, tid = threadIdx.x;
-  uint32_t* keys = kGlobalKeys ? ws.keys + p * ws.s_keys : keys_lds;
-  const float* part = ws.part + p * ws.s_part;
-  const int* sel = ws.sel + p * ws.s_sel;
-  for (int i = tid; i < sh.N; i += blockDim.x) {
-    float u = 0.f;
-    for (int c = 0; c < sh.nc; ++c) u += part[static_cast<long long>(c) * sh.ldE + i];
-    keys[i] = (sel[i] >= 0) ? 0u : score_key(u);
+  __shared__ int hist[256], scan[16], bc[2], flag;
+  const int p = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col0 = blockIdx.x * kGainCols + wave * kCpw;
+  const float* alpha = ws.alpha + p * ws.s_m;
+  const float* cov = ws.cov + p * ws.s_cov;
+  const float* E = ws.E + p * ws.s_E;
+  float* u = ws.u + p * ws.s_u;
+  float acc[kCpw];
+  const float* col[kCpw];
+#pragma unroll
+  for (int c = 0; c < kCpw; ++c) {
+    acc[c] = 0.f;
+    col[c] = E + static_cast<long long>(min(col0 + c, sh.N - 1)) * sh.ldM;
   }
+#pragma unroll 4
+  for (int m = lane * 4; m < sh.m; m += 256) {
+    const float4 a = *reinterpret_cast<const float4*>(alpha + m);
+    const float4 b = *reinterpret_cast<const float4*>(cov + m);
+#pragma unroll
+    for (int c = 0; c < kCpw; ++c) {
+      const float4 v = *reinterpret_cast<const float4*>(col[c] + m);
+      acc[c] += fmaxf(a.x * v.x - b.x, 0.f);
+      acc[c] += fmaxf(a.y * v.y - b.y, 0.f);
+      acc[c] += fmaxf(a.z * v.z - b.z, 0.f);
+      acc[c] += fmaxf(a.w * v.w - b.w, 0.f);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < kCpw; ++c) {
+    const float s = wave_sum(acc[c]);
+    if (lane == 0 && col0 + c < sh.N) st_dev(&u[col0 + c], s);
+  }
+
+  // tail: the pool, the psize largest gains among unselected tokens
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  if (!last_arrival(&cnt[0], gridDim.x, &flag)) return;
+  if (tid == 0) st_dev(&cnt[0], 0);
+  uint32_t* keys = kGlobalKeys ? ws.keys + p * ws.s_keys : keys_lds;
+  const int* sel = ws.sel + p * ws.s_sel;
+  for (int i = tid; i < sh.N; i += 256) keys[i] = (sel[i] >= 0) ? 0u : score_key(ld_dev(&u[i]));
   __syncthreads();
   int* pool = ws.pool + p * ws.s_pool;
-  block_topk(keys, sh.N, psize, pool, hist, scan, bcast);
+  block_topk256(keys, sh.N, psize, pool, hist, scan, bc);
   if (trace_pool) {
     int32_t* tp = trace_pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
-    for (int j = tid; j < sh.pool_cap; j += blockDim.x) tp[j] = (j < psize) ? pool[j] : -1;
+    for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool[j] : -1;
   }
 }
 
-template <int Q>
-__global__ void __launch_bounds__(256) resp_kernel(Shape sh, Params pr, Ws ws, int round, int psize) {
-  __shared__ int pool_s[64 * Q];
-  __shared__ float acc_s[4][64 * Q];
-  const int p = blockIdx.y, chunk = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int* pool = ws.pool + p * ws.s_pool;
-  for (int j = tid; j < 64 * Q; j += 256) pool_s[j] = (j < psize) ? pool[j] : 0;
-  __syncthreads();
-  const float* cov = ws.cov + p * ws.s_cov + ((round + 1) & 1) * sh.m;
-  const float* E = ws.E + p * ws.s_E;
-  const float* alpha = ws.alpha + p * ws.s_m;
-  float racc[Q];
-#pragma unroll
-  for (int q = 0; q < Q; ++q) racc[q] = 0.f;
-  const int r0 = chunk * sh.rc2, r1 = min(sh.m, r0 + sh.rc2);
-  for (int m = r0 + wave; m < r1; m += 4) {
-    const float a = alpha[m], c = cov[m];
-    const float* Em = E + static_cast<long long>(m) * sh.ldE;
-    float R[Q];
-    float mu = 0.f;
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int jj = lane + 64 * q;
-      R[q] = (jj < psize) ? fmaxf(a * Em[pool_s[jj]] - c, 0.f) : 0.f;
-      mu = fmaxf(mu, R[q]);
-    }
-    mu = wave_max(mu);
-    if (mu > 0.f) {
-      const float inv = 1.f / (pr.tau_r * mu + pr.resp_eps);
-      const float zmax = mu * inv;
-      float ex[Q];
-      float den = 0.f;
-#pragma unroll
-      for (int q = 0; q < Q; ++q) {
-        const int jj = lane + 64 * q;
-        ex[q] = (jj < psize) ? expf(R[q] * inv - zmax) : 0.f;
-        den += ex[q];
-      }
-      den = wave_sum(den);
-      const float rden = 1.f / den;
-#pragma unroll
-      for (int q = 0; q < Q; ++q) racc[q] += ex[q] * rden * R[q];
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < Q; ++q) acc_s[wave][lane + 64 * q] = racc[q];
-  __syncthreads();
-  float* sp = ws.spart + p * ws.s_spart + static_cast<long long>(chunk) * sh.pool_cap;
-  for (int j = tid; j < psize; j += 256) sp[j] = ((acc_s[0][j] + acc_s[1][j]) + acc_s[2][j]) + acc_s[3][j];
-}
-
-__global__ void __launch_bounds__(1024) batch_kernel(Shape sh, Ws ws, int round, int psize, int bsize,
-                                                     int sel_base, int32_t* trace_batch) {
-  extern __shared__ uint32_t keys[];
-  __shared__ int hist[256], scan[16], bcast[2];
-  __shared__ int chosen[1024];
-  const int p = blockIdx.x, tid = threadIdx.x;
-  const float* sp = ws.spart + p * ws.s_spart;
-  for (int j = tid; j < psize; j += blockDim.x) {
-    float s = 0.f;
-    for (int c = 0; c < sh.nc2; ++c) s += sp[static_cast<long long>(c) * sh.pool_cap + j];
-    keys[j] = score_key(s);
-  }
-  __syncthreads();
-  block_topk(keys, psize, bsize, chosen, hist, scan, bcast);
-  const int* pool = ws.pool + p * ws.s_pool;
+// Mark the batch (indices into the pool, ascending) and record it.
+__device__ void commit_batch(const Shape& sh, const Ws& ws, int p, int round, int bsize, int sel_base,
+                             const int* pool_s, const int* chosen, int32_t* trace_batch) {
   int* sel = ws.sel + p * ws.s_sel;
   int* order = ws.order + p * ws.s_ord;
   int* batch = ws.batch + p * ws.s_bat;
-  for (int k = tid; k < bsize; k += blockDim.x) {
-    const int i = pool[chosen[k]];
+  for (int k = threadIdx.x; k < bsize; k += blockDim.x) {
+    const int i = pool_s[chosen[k]];
     sel[i] = round;
     order[sel_base + k] = i;
     batch[k] = i;
   }
   if (trace_batch) {
     int32_t* tb = trace_batch + (static_cast<long long>(p) * sh.rounds + round) * sh.b;
-    for (int k = tid; k < sh.b; k += blockDim.x) tb[k] = (k < bsize) ? pool[chosen[k]] : -1;
+    for (int k = threadIdx.x; k < sh.b; k += blockDim.x) tb[k] = (k < bsize) ? pool_s[chosen[k]] : -1;
   }
 }
 
-// Initial state: nothing selected.
-__global__ void select_init_kernel(Shape sh, Ws ws) {
-  const int p = blockIdx.y;
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < sh.N; i += gridDim.x * blockDim.x)
-    ws.sel[p * ws.s_sel + i] = -1;
+// Wave-level top-b of at most 64 keys (lane = pool position, ascending
+// source index): rank by (key desc, position asc); chosen positions in
+// ascending order.  Called by one whole wave.
+__device__ void wave_topb(const uint32_t* keys, int psize, int bsize, int* chosen) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t k = (lane < psize) ? keys[lane] : 0u;
+  int rank = 0;
+  for (int t = 0; t < 64; ++t) {
+    const uint32_t kt = __shfl(k, t, kWave);
+    rank += (kt > k) || (kt == k && t < lane);
+  }
+  const bool take = lane < psize && rank < bsize;
+  const unsigned long long bal = __ballot(take);
+  const int pos = __popcll(bal & ((1ull << lane) - 1ull));
+  if (take) chosen[pos] = lane;
 }
 
-// Final coverage b_m(S) and per-block partial sums of F(S) and F(V).
-__global__ void __launch_bounds__(256) cov_final_kernel(Shape sh, Ws ws, int last_b) {
+// Butterfly transpose-reduction: lane l holds v[0..63] (one value per pool
+// position); afterwards v[0] in lane l is the sum over all 64 lanes of the
+// values for position l.  63 exchanges, fixed order.
+template <int O>
+__device__ __forceinline__ void transpose_reduce_step(float* v, int lane) {
+  const bool hi = (lane & O) != 0;
+#pragma unroll
+  for (int k = 0; k < O; ++k) {
+    const float send = hi ? v[k] : v[k + O];
+    const float keep = hi ? v[k + O] : v[k];
+    v[k] = keep + __shfl_xor(send, O, kWave);
+  }
+}
+__device__ __forceinline__ float transpose_reduce64(float* v, int lane) {
+  transpose_reduce_step<32>(v, lane);
+  transpose_reduce_step<16>(v, lane);
+  transpose_reduce_step<8>(v, lane);
+  transpose_reduce_step<4>(v, lane);
+  transpose_reduce_step<2>(v, lane);
+  transpose_reduce_step<1>(v, lane);
+  return v[0];
+}
+
+__global__ void __launch_bounds__(256)
+resp_small_kernel(Shape sh, Params pr, Ws ws, int round, int psize, int bsize, int sel_base,
+                  int32_t* trace_batch) {
+  __shared__ int pool_s[64];
+  __shared__ float wsum[4][64];
+  __shared__ uint32_t keys[64];
+  __shared__ int chosen[64];
+  __shared__ int flag;
+  const int p = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < 64) pool_s[tid] = (tid < psize) ? ws.pool[p * ws.s_pool + tid] : 0;
+  __syncthreads();
+  const int m = blockIdx.x * 256 + tid;
+  const bool row_ok = m < sh.m;
+  const int mc = row_ok ? m : 0;   // clamped: every load below is unconditional
+  const float* E = ws.E + p * ws.s_E + mc;
+  float v[64];
+  float mu = 0.f;
+  const float a = row_ok ? ws.alpha[p * ws.s_m + mc] : 0.f;
+  const float c = ws.cov[p * ws.s_cov + mc];
+#pragma unroll
+  for (int j = 0; j < 64; ++j) v[j] = E[static_cast<long long>(pool_s[j]) * sh.ldM];
+#pragma unroll
+  for (int j = 0; j < 64; ++j) {
+    const float r = (j < psize) ? fmaxf(a * v[j] - c, 0.f) : 0.f;
+    v[j] = r;
+    mu = fmaxf(mu, r);
+  }
+  if (mu > 0.f) {
+    const float inv = 1.f / (pr.tau_r * mu + pr.resp_eps);
+    const float zmax = mu * inv;
+    float den = 0.f;
+    float ex[64];
+#pragma unroll
+    for (int j = 0; j < 64; ++j) {
+      ex[j] = (j < psize) ? expf(v[j] * inv - zmax) : 0.f;
+      den += ex[j];
+    }
+    const float rden = 1.f / den;
+#pragma unroll
+    for (int j = 0; j < 64; ++j) v[j] = ex[j] * rden * v[j];
+  } else {
+#pragma unroll
+    for (int j = 0; j < 64; ++j) v[j] = 0.f;
+  }
+  wsum[wave][lane] = transpose_reduce64(v, lane);
+  __syncthreads();
+  float* sp = ws.spart + p * ws.s_spart;
+  if (tid < psize)
+    st_dev(&sp[static_cast<long long>(blockIdx.x) * 64 + tid], ((wsum[0][tid] + wsum[1][tid]) + wsum[2][tid]) + wsum[3][tid]);
+
+  // tail: block sums in block order, then the batch
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  if (!last_arrival(&cnt[1], gridDim.x, &flag)) return;
+  if (tid == 0) st_dev(&cnt[1], 0);
+  if (tid < psize) {
+    float s = 0.f;
+    const int nb = gridDim.x;
+    int b = 0;
+    for (; b + 8 <= nb; b += 8) {
+      float t[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) t[q] = ld_dev(&sp[static_cast<long long>(b + q) * 64 + tid]);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) s += t[q];
+    }
+    for (; b < nb; ++b) s += ld_dev(&sp[static_cast<long long>(b) * 64 + tid]);
+    keys[tid] = score_key(s);
+  }
+  __syncthreads();
+  if (wave == 0) wave_topb(keys, psize, bsize, chosen);
+  __syncthreads();
+  commit_batch(sh, ws, p, round, bsize, sel_base, pool_s, chosen, trace_batch);
+}
+
+// Large pools: per-row max mu_m and softmax denominator over the pool.
+// Block = 64 rows (lane = row) x 4 waves splitting the pool positions.
+__global__ void __launch_bounds__(256) rowstat_kernel(Shape sh, Params pr, Ws ws, int psize) {
+  __shared__ float part[4][64];
+  __shared__ float mu_s[64];
+  const int p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int m = blockIdx.x * 64 + lane;
+  const bool row_ok = m < sh.m;
+  const float a = row_ok ? ws.alpha[p * ws.s_m + m] : 0.f;
+  const float c = row_ok ? ws.cov[p * ws.s_cov + m] : 0.f;
+  const float* E = ws.E + p * ws.s_E + (row_ok ? m : 0);
+  const int* pool = ws.pool + p * ws.s_pool;
+  const int q = (psize + 3) / 4, j0 = wave * q, j1 = min(psize, j0 + q);
+  float mx = 0.f;
+#pragma unroll 8
+  for (int j = j0; j < j1; ++j) mx = fmaxf(mx, fmaxf(a * E[static_cast<long long>(pool[j]) * sh.ldM] - c, 0.f));
+  part[wave][lane] = mx;
+  __syncthreads();
+  if (wave == 0) mu_s[lane] = fmaxf(fmaxf(part[0][lane], part[1][lane]), fmaxf(part[2][lane], part[3][lane]));
+  __syncthreads();
+  const float mu = mu_s[lane];
+  const float inv = mu > 0.f ? 1.f / (pr.tau_r * mu + pr.resp_eps) : 0.f;
+  const float zmax = mu * inv;
+  float den = 0.f;
+  if (mu > 0.f)
+#pragma unroll 8
+    for (int j = j0; j < j1; ++j)
+      den += expf(fmaxf(a * E[static_cast<long long>(pool[j]) * sh.ldM] - c, 0.f) * inv - zmax);
+  __syncthreads();
+  part[wave][lane] = den;
+  __syncthreads();
+  if (wave == 0 && row_ok) {
+    const float d = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+    float* rs = ws.rstat + p * ws.s_rstat;
+    rs[m] = inv;
+    rs[sh.ldM + m] = zmax;
+    rs[2 * sh.ldM + m] = mu > 0.f ? 1.f / d : 0.f;
+  }
+}
+
+// Large pools: one wave per pool position sums rho R over all client rows;
+// the last block picks the batch.
+__global__ void __launch_bounds__(256)
+colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, int32_t* trace_batch) {
+  extern __shared__ uint32_t keys[];   // pool_cap words
+  __shared__ int hist[256], scan[16], bc[2], flag;
+  __shared__ int chosen[1024];
+  const int p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int jj = blockIdx.x * 4 + wave;
+  const int* pool = ws.pool + p * ws.s_pool;
+  const float* rs = ws.rstat + p * ws.s_rstat;
+  const float* alpha = ws.alpha + p * ws.s_m;
+  const float* cov = ws.cov + p * ws.s_cov;
+  float* sv = ws.u + p * ws.s_u;        // scores reuse the gains buffer
+  if (jj < psize) {
+    const float* col = ws.E + p * ws.s_E + static_cast<long long>(pool[jj]) * sh.ldM;
+    float acc = 0.f;
+    for (int m = lane * 4; m < sh.m; m += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(col + m);
+      const float4 a = *reinterpret_cast<const float4*>(alpha + m);
+      const float4 c = *reinterpret_cast<const float4*>(cov + m);
+      const float4 inv = *reinterpret_cast<const float4*>(rs + m);
+      const float4 zm = *reinterpret_cast<const float4*>(rs + sh.ldM + m);
+      const float4 rd = *reinterpret_cast<const float4*>(rs + 2 * sh.ldM + m);
+      float r;
+      r = fmaxf(a.x * v.x - c.x, 0.f); acc += expf(r * inv.x - zm.x) * rd.x * r;
+      r = fmaxf(a.y * v.y - c.y, 0.f); acc += expf(r * inv.y - zm.y) * rd.y * r;
+      r = fmaxf(a.z * v.z - c.z, 0.f); acc += expf(r * inv.z - zm.z) * rd.z * r;
+      r = fmaxf(a.w * v.w - c.w, 0.f); acc += expf(r * inv.w - zm.w) * rd.w * r;
+    }
+    const float s = wave_sum(acc);
+    if (lane == 0) st_dev(&sv[jj], s);
+  }
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  if (!last_arrival(&cnt[4], gridDim.x, &flag)) return;
+  if (tid == 0) st_dev(&cnt[4], 0);
+  for (int j = tid; j < psize; j += 256) keys[j] = score_key(ld_dev(&sv[j]));
+  __syncthreads();
+  block_topk256(keys, psize, bsize, chosen, hist, scan, bc);
+  commit_batch(sh, ws, p, round, bsize, sel_base, pool, chosen, trace_batch);
+}
+
+// Per-call state: nothing selected, coverage and row-weight padding zero,
+// completion counters cleared.
+__global__ void select_init_kernel(Shape sh, Ws ws) {
+  const int p = blockIdx.y;
+  const int x0 = blockIdx.x * blockDim.x + threadIdx.x, stride = gridDim.x * blockDim.x;
+  for (int i = x0; i < sh.N; i += stride) ws.sel[p * ws.s_sel + i] = -1;
+  for (int m = x0; m < sh.ldM; m += stride) {
+    ws.cov[p * ws.s_cov + m] = 0.f;
+    if (m >= sh.m) ws.alpha[p * ws.s_m + m] = 0.f;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < kCounters) ws.cnt[p * ws.s_cnt + threadIdx.x] = 0;
+}
+
+// F(S) = sum_m b_m(S) and F(V) = sum_m max_i Cbar_mi via per-block partials
+// reduced in order by the last block.
+__global__ void __launch_bounds__(256) objective_kernel(Shape sh, Ws ws) {
   __shared__ float red[16];
+  __shared__ int flag;
   const int p = blockIdx.y, m = blockIdx.x * 256 + threadIdx.x;
-  const float* cov_in = ws.cov + p * ws.s_cov + (sh.rounds & 1) * sh.m;
-  const int* prev = ws.batch + p * ws.s_bat;
   float c = 0.f, pk = 0.f;
   if (m < sh.m) {
-    const float a = ws.alpha[p * ws.s_m + m];
-    c = cov_in[m];
-    const float* Em = ws.E + p * ws.s_E + static_cast<long long>(m) * sh.ldE;
-    for (int j = 0; j < last_b; ++j) c = fmaxf(c, a * Em[prev[j]]);
+    c = ws.cov[p * ws.s_cov + m];
     pk = ws.peak[p * ws.s_m + m];
   }
   const float fs = block_sum(c, red);
   const float fv = block_sum(pk, red);
+  float* sp = ws.spart + p * ws.s_spart;
   if (threadIdx.x == 0) {
-    ws.spart[p * ws.s_spart + 2 * blockIdx.x] = fs;
-    ws.spart[p * ws.s_spart + 2 * blockIdx.x + 1] = fv;
+    st_dev(&sp[2 * blockIdx.x], fs);
+    st_dev(&sp[2 * blockIdx.x + 1], fv);
+  }
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  if (!last_arrival(&cnt[2], gridDim.x, &flag)) return;
+  if (threadIdx.x == 0) {
+    st_dev(&cnt[2], 0);
+    float a = 0.f, b = 0.f;
+    for (unsigned k = 0; k < gridDim.x; ++k) { a += ld_dev(&sp[2 * k]); b += ld_dev(&sp[2 * k + 1]); }
+    float* st = ws.stats + p * ws.s_st;
+    st[2] = a;
+    st[3] = b;
+    st[4] = static_cast<float>(sh.K);
+    st[5] = static_cast<float>(sh.rounds);
+    st[6] = static_cast<float>(sh.m);
+    st[7] = static_cast<float>(sh.N - sh.K);
   }
 }
 
-__global__ void objective_stats_kernel(Shape sh, Ws ws, int nblk) {
-  const int p = blockIdx.x;
-  if (threadIdx.x != 0) return;
-  float fs = 0.f, fv = 0.f;
-  for (int b = 0; b < nblk; ++b) {
-    fs += ws.spart[p * ws.s_spart + 2 * b];
-    fv += ws.spart[p * ws.s_spart + 2 * b + 1];
-  }
-  float* st = ws.stats + p * ws.s_st;
-  st[2] = fs;
-  st[3] = fv;
-  st[4] = static_cast<float>(sh.K);
-  st[5] = static_cast<float>(sh.rounds);
-  st[6] = static_cast<float>(sh.m);
-  st[7] = static_cast<float>(sh.N - sh.K);
+hipError_t launch_call_init(const Shape& sh, const Ws& ws, hipStream_t st) {
+  const int n = max(sh.N, sh.ldM);
+  hipLaunchKernelGGL(select_init_kernel, dim3((n + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
+  return hipGetLastError();
+}
+
+static void launch_cov(const Shape& sh, const Ws& ws, int nb, hipStream_t st) {
+  hipLaunchKernelGGL(cov_kernel, dim3((sh.m + 255) / 256, (nb + kCovCols - 1) / kCovCols, sh.B), dim3(256), 0,
+                     st, sh, ws, nb);
 }
 
 hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
                             int32_t* trace_batch, hipStream_t st) {
-  hipLaunchKernelGGL(select_init_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
-  const size_t pool_lds = static_cast<size_t>(sh.N) * sizeof(uint32_t);
-  const size_t batch_lds = static_cast<size_t>(sh.pool_cap) * sizeof(uint32_t);
+  const bool global_keys = sh.N > kLdsKeys;
+  const size_t key_lds = global_keys ? 0 : static_cast<size_t>(sh.N) * sizeof(uint32_t);
+  const bool small_pool = sh.pool_cap <= 64;
   int selected = 0;
   for (int r = 0; r < sh.rounds; ++r) {
     const int psize = min(sh.pool_cap, sh.N - selected);
     const int bsize = min(sh.b, sh.K - selected);
+    if (r > 0) {
+      timer_mark(kStCov, true, st);
+      launch_cov(sh, ws, sh.b, st);
+      timer_mark(kStCov, false, st);
+    }
+    const dim3 gg((sh.N + kGainCols - 1) / kGainCols, sh.B);
     timer_mark(kStGains, true, st);
-    hipLaunchKernelGGL(gains_kernel, dim3(sh.nstrips * sh.nc, sh.B), dim3(256), 0, st, sh, ws, r,
-                       r > 0 ? sh.b : 0);
-    timer_mark(kStGains, false, st);
-    timer_mark(kStPool, true, st);
-    if (sh.N <= kLdsKeys)
-      hipLaunchKernelGGL(pool_kernel<false>, dim3(sh.B), dim3(1024), pool_lds, st, sh, ws, r, psize, trace_pool);
+    if (global_keys)
+      hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, trace_pool);
     else
-      hipLaunchKernelGGL(pool_kernel<true>, dim3(sh.B), dim3(1024), 0, st, sh, ws, r, psize, trace_pool);
-    timer_mark(kStPool, false, st);
+      hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, trace_pool);
+    timer_mark(kStGains, false, st);
     timer_mark(kStResp, true, st);
-    const int q = (sh.pool_cap + 63) / 64;
-    const dim3 rg(sh.nc2, sh.B);
-    if (q <= 1) hipLaunchKernelGGL(resp_kernel<1>, rg, dim3(256), 0, st, sh, pr, ws, r, psize);
-    else if (q <= 2) hipLaunchKernelGGL(resp_kernel<2>, rg, dim3(256), 0, st, sh, pr, ws, r, psize);
-    else if (q <= 4) hipLaunchKernelGGL(resp_kernel<4>, rg, dim3(256), 0, st, sh, pr, ws, r, psize);
-    else if (q <= 8) hipLaunchKernelGGL(resp_kernel<8>, rg, dim3(256), 0, st, sh, pr, ws, r, psize);
-    else if (q <= 16) hipLaunchKernelGGL(resp_kernel<16>, rg, dim3(256), 0, st, sh, pr, ws, r, psize);
-    else if (q <= 32) hipLaunchKernelGGL(resp_kernel<32>, rg, dim3(256), 0, st, sh, pr, ws, r, psize);
-    else return hipErrorInvalidValue;
+    if (small_pool) {
+      hipLaunchKernelGGL(resp_small_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws, r,
+                         psize, bsize, selected, trace_batch);
+    } else {
+      hipLaunchKernelGGL(rowstat_kernel, dim3((sh.m + 63) / 64, sh.B), dim3(256), 0, st, sh, pr, ws, psize);
+      hipLaunchKernelGGL(colsum_kernel, dim3((psize + 3) / 4, sh.B), dim3(256),
+                         static_cast<size_t>(sh.pool_cap) * sizeof(uint32_t), st, sh, ws, r, psize, bsize,
+                         selected, trace_batch);
+    }
     timer_mark(kStResp, false, st);
-    timer_mark(kStBatch, true, st);
-    hipLaunchKernelGGL(batch_kernel, dim3(sh.B), dim3(1024), batch_lds, st, sh, ws, r, psize, bsize,
-                       selected, trace_batch);
-    timer_mark(kStBatch, false, st);
     selected += bsize;
   }
   const int last_b = sh.K - (sh.rounds - 1) * sh.b;
-  const int nblk = (sh.m + 255) / 256;
   timer_mark(kStObjective, true, st);
-  hipLaunchKernelGGL(cov_final_kernel, dim3(nblk, sh.B), dim3(256), 0, st, sh, ws, last_b);
-  hipLaunchKernelGGL(objective_stats_kernel, dim3(sh.B), dim3(64), 0, st, sh, ws, nblk);
+  launch_cov(sh, ws, last_b, st);
+  hipLaunchKernelGGL(objective_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
   timer_mark(kStObjective, false, st);
   return hipGetLastError();
 }

@@ -27,6 +27,7 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
   const int* pi = ws.pi + p * ws.s_pi;
   const float* eb = ws.ebar + p * ws.s_eb;
   const float sx = ws.gate[p * ws.s_gate];
+  const float inv_mean = ws.gate[p * ws.s_gate + 2];   // 0: uniform fallback ebar = 1
   const float m0 = 1.f - pr.pop_strength * sx, m1 = pr.pop_strength * sx;
   const T* H = hidden + static_cast<long long>(p) * sh.N * sh.d;
   const int ngroups = sh.d / 8;
@@ -49,7 +50,7 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
         const int b = __ffsll(static_cast<long long>(mk)) - 1;
         mk &= mk - 1;
         const int ii = i0 + w * 64 + b;
-        const float mi = m0 + m1 * eb[ii];
+        const float mi = m0 + m1 * (inv_mean > 0.f ? eb[ii] * inv_mean : 1.f);
         mass += mi;
         const T* row = H + static_cast<long long>(ii) * sh.d;
 #pragma unroll
@@ -167,9 +168,10 @@ hipError_t launch_identity(const Shape& sh, const void* hidden, const int32_t* p
 __global__ void export_client_kernel(Shape sh, Ws ws, float* out) {
   const int p = blockIdx.z, m = blockIdx.y;
   const float a = ws.alpha[p * ws.s_m + m];
-  const float* E = ws.E + p * ws.s_E + static_cast<long long>(m) * sh.ldE;
+  const float* E = ws.E + p * ws.s_E + m;
   float* o = out + (static_cast<long long>(p) * sh.m + m) * sh.N;
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < sh.N; i += gridDim.x * blockDim.x) o[i] = a * E[i];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < sh.N; i += gridDim.x * blockDim.x)
+    o[i] = a * E[static_cast<long long>(i) * sh.ldM];
 }
 
 __global__ void export_stats_kernel(Shape sh, Ws ws, float* out) {
@@ -177,8 +179,17 @@ __global__ void export_stats_kernel(Shape sh, Ws ws, float* out) {
   if (threadIdx.x < kStats) out[p * kStats + threadIdx.x] = ws.stats[p * ws.s_st + threadIdx.x];
 }
 
+__global__ void export_ebar_kernel(Shape sh, Ws ws, float* out) {
+  const int p = blockIdx.y;
+  const float inv_mean = ws.gate[p * ws.s_gate + 2];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < sh.N; i += gridDim.x * blockDim.x)
+    out[static_cast<long long>(p) * sh.N + i] = inv_mean > 0.f ? ws.ebar[p * ws.s_eb + i] * inv_mean : 1.f;
+}
+
 hipError_t launch_trace_exports(const Shape& sh, const Ws& ws, float* trace_client, float* trace_stats,
-                                hipStream_t st) {
+                                float* trace_ebar, hipStream_t st) {
+  if (trace_ebar)
+    hipLaunchKernelGGL(export_ebar_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws, trace_ebar);
   if (trace_client)
     hipLaunchKernelGGL(export_client_kernel, dim3((sh.N + 255) / 256, sh.m, sh.B), dim3(256), 0, st, sh,
                        ws, trace_client);

@@ -63,7 +63,7 @@ def _valid_cfg():
 
 
 @pytest.mark.parametrize("field,value", [
-    ("d", 0), ("d", 100), ("n_q_heads", 0), ("n_q_heads", 33), ("n_kv_heads", 3),
+    ("d", 0), ("d", 100), ("d", 96), ("n_q_heads", 0), ("n_q_heads", 33), ("n_kv_heads", 3),
     ("head_dim", 48), ("head_dim", 512), ("probe_rank", 0), ("probe_rank", 9), ("dtype", 7),
     ("max_batch", 0), ("max_n", 0), ("max_n", 40000), ("max_t", -1), ("max_k", 300),
     ("value_probe", None), ("tau_v", 0.0), ("g_form", 3), ("batch_b", 0), ("landmarks", 0),
