@@ -334,13 +334,34 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
   }
   // per-token pattern weights <w_h, w_g> / (l_h l_g)
   __syncthreads();
-  for (int x = tid; x < kHeadTok * sh.hr; x += 256) {
-    const int ii = x / sh.hr, c = x % sh.hr;
-    zt[x] = (i0 + ii < sh.N) ? ws.z[p * ws.s_z + static_cast<long long>(i0 + ii) * sh.hr + c] : 0.f;
-  }
-  for (int x = tid; x < H * kHeadTok; x += 256) {
-    const int h = x / kHeadTok, ii = x % kHeadTok;
-    lt[x] = (i0 + ii < sh.N) ? ws.ell[p * ws.s_ell + static_cast<long long>(h) * sh.N + i0 + ii] : 1.f;
+  {
+    // batched, clamped loads of the tokens' probe coordinates and atom norms
+    constexpr int kZ = kHeadTok * kMaxHeads * kMaxProbe / 256;
+    constexpr int kL = kMaxHeads * kHeadTok / 256;
+    float zv[kZ], lv[kL];
+    const int nz = kHeadTok * sh.hr;
+#pragma unroll
+    for (int q = 0; q < kZ; ++q) {
+      const int x = min(tid + q * 256, nz - 1);
+      const int ii = min(i0 + x / sh.hr, sh.N - 1), c = x % sh.hr;
+      zv[q] = ws.z[p * ws.s_z + static_cast<long long>(ii) * sh.hr + c];
+    }
+#pragma unroll
+    for (int q = 0; q < kL; ++q) {
+      const int x = tid + q * 256;
+      const int h = min(x / kHeadTok, H - 1), ii = min(i0 + x % kHeadTok, sh.N - 1);
+      lv[q] = ws.ell[p * ws.s_ell + static_cast<long long>(h) * sh.N + ii];
+    }
+#pragma unroll
+    for (int q = 0; q < kZ; ++q) {
+      const int x = tid + q * 256;
+      if (x < nz) zt[x] = (i0 + x / sh.hr < sh.N) ? zv[q] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < kL; ++q) {
+      const int x = tid + q * 256;
+      if (x < H * kHeadTok) lt[x] = (i0 + x % kHeadTok < sh.N) ? lv[q] : 1.f;
+    }
   }
   __syncthreads();
   const float* sig = ws.sig + p * ws.s_sig;
@@ -525,6 +546,7 @@ __global__ void __launch_bounds__(256) energy_kernel(Shape sh, Ws ws) {
   if (tid == 0) {
     st_dev(cnt, 0);
     float s = 0.f;
+#pragma unroll 8
     for (unsigned b = 0; b < gridDim.x; ++b) s += ld_dev(&ep[b]);
     const float mean = s / static_cast<float>(sh.N);
     ws.gate[p * ws.s_gate + 2] = (mean > 0.f) ? 1.f / mean : 0.f;

@@ -30,6 +30,8 @@ namespace gmc {
 
 constexpr int kCpw = 2;                 // gains kernel: tokens per wave
 constexpr int kGainCols = 4 * kCpw;     // tokens per block
+constexpr int kCpwF = 4;                // fused gains kernel: tokens per wave
+constexpr int kGainColsF = 4 * kCpwF;
 constexpr int kLdsKeys = 12288;         // pool top-k keys live in LDS up to this N
 
 // Deterministic top-k over n keys (256-thread block): the `count` largest
@@ -40,10 +42,36 @@ constexpr int kLdsKeys = 12288;         // pool top-k keys live in LDS up to thi
 // compaction (each thread owns a contiguous index segment).
 __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, int* hist, int* scan,
                               int* bc) {
-  const int tid = threadIdx.x;
-  uint32_t prefix = 0, mask = 0;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // bits shared by every key need no radix pass: AND / OR over all keys
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+  for (int i = tid; i < n; i += 256) {
+    const uint32_t k = keys[i];
+    kand &= k;
+    kor |= k;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kand &= static_cast<uint32_t>(__shfl_xor(static_cast<int>(kand), o, kWave));
+    kor |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(kor), o, kWave));
+  }
+  if (lane == 0) { scan[wave] = static_cast<int>(kand); scan[4 + wave] = static_cast<int>(kor); }
+  __syncthreads();
+  kand = static_cast<uint32_t>(scan[0]) & static_cast<uint32_t>(scan[1]) & static_cast<uint32_t>(scan[2]) &
+         static_cast<uint32_t>(scan[3]);
+  kor = static_cast<uint32_t>(scan[4]) | static_cast<uint32_t>(scan[5]) | static_cast<uint32_t>(scan[6]) |
+        static_cast<uint32_t>(scan[7]);
+  const uint32_t diff = kand ^ kor;                 // bits that vary between keys
+  uint32_t mask = 0, prefix = 0;
+  int top = 24;
+  while (top > 0 && ((diff >> top) & 0xFFu) == 0u) {
+    mask |= 0xFFu << top;
+    top -= 8;
+  }
+  prefix = kand & mask;
   int remaining = count;
-  for (int shift = 24; shift >= 0; shift -= 8) {
+  __syncthreads();
+  for (int shift = top; shift >= 0; shift -= 8) {
     hist[tid] = 0;
     __syncthreads();
     for (int i = tid; i < n; i += 256) {
@@ -51,19 +79,31 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
       if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
     }
     __syncthreads();
-    const int d = 255 - tid;
-    const int v = hist[d];
-    int tot;
-    const int excl = block_exclusive_scan(v, scan, &tot);
-    if (excl < remaining && remaining <= excl + v) {
-      bc[0] = d;
-      bc[1] = remaining - excl;
+    if (wave == 0) {
+      // wave 0 scans the 256 bins from the top digit down, 4 per lane
+      int v[4], loc = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { v[q] = hist[255 - (lane * 4 + q)]; loc += v[q]; }
+      int incl = loc;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += t;
+      }
+      int excl = incl - loc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (excl < remaining && remaining <= excl + v[q]) {
+          bc[0] = 255 - (lane * 4 + q);
+          bc[1] = remaining - excl;
+        }
+        excl += v[q];
+      }
     }
     __syncthreads();
     prefix |= static_cast<uint32_t>(bc[0]) << shift;
     mask |= 0xFFu << shift;
     remaining = bc[1];
-    __syncthreads();
   }
   const uint32_t kth = prefix;
   const int seg = (n + 255) / 256;
@@ -155,7 +195,23 @@ gains_kernel(Shape sh, Ws ws, int round, int psize, int32_t* trace_pool) {
   if (tid == 0) st_dev(&cnt[0], 0);
   uint32_t* keys = kGlobalKeys ? ws.keys + p * ws.s_keys : keys_lds;
   const int* sel = ws.sel + p * ws.s_sel;
-  for (int i = tid; i < sh.N; i += 256) keys[i] = (sel[i] >= 0) ? 0u : score_key(ld_dev(&u[i]));
+  // loads go to registers in batches first (keys may alias global memory, so
+  // interleaved stores would serialise them)
+  for (int base = 0; base < sh.N; base += 256 * 16) {
+    float g[16];
+    int sl[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int i = min(base + q * 256 + tid, sh.N - 1);
+      g[q] = ld_dev(&u[i]);
+      sl[q] = sel[i];
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int i = base + q * 256 + tid;
+      if (i < sh.N) keys[i] = (sl[q] >= 0) ? 0u : score_key(g[q]);
+    }
+  }
   __syncthreads();
   int* pool = ws.pool + p * ws.s_pool;
   block_topk256(keys, sh.N, psize, pool, hist, scan, bc);
@@ -223,14 +279,176 @@ __device__ __forceinline__ float transpose_reduce64(float* v, int lane) {
   return v[0];
 }
 
+// Batch of a small pool from the responsibility block sums (one whole wave):
+// scores summed in block order, top-b by (score desc, index asc).  Leaves
+// the pool in pool_s and the chosen source indices, ascending, in bidx.
+__device__ void small_batch(const Shape& sh, const Ws& ws, int p, int psize, int bsize, int nblk,
+                            int* pool_s, uint32_t* keys, int* chosen, int* bidx) {
+  const int lane = threadIdx.x & 63;
+  pool_s[lane] = (lane < psize) ? ws.pool[p * ws.s_pool + lane] : 0;
+  const float* sp = ws.spart + p * ws.s_spart;
+  float s = 0.f;
+  int b = 0;
+  for (; b + 8 <= nblk; b += 8) {
+    float t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t[q] = sp[static_cast<long long>(b + q) * 64 + lane];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += t[q];
+  }
+  for (; b < nblk; ++b) s += sp[static_cast<long long>(b) * 64 + lane];
+  keys[lane] = score_key(s);
+  __builtin_amdgcn_wave_barrier();
+  wave_topb(keys, psize, bsize, chosen);
+  __builtin_amdgcn_wave_barrier();
+  if (lane < bsize) bidx[lane] = pool_s[chosen[lane]];
+}
+
+// Small pools, fused round: (1) the previous round's batch from the
+// responsibility sums, recorded by block 0; (2) the coverage refresh
+// b_m <- max(b_m, max_{j in batch} Cbar_mj) for every row, into LDS (block 0
+// also stores it; a block that reads an already refreshed b_m recomputes the
+// same value, since max(b_new, Cbar_mB) = b_new); (3) singleton gains of the
+// block's tokens; (4) last block: the pool of this round, excluding the
+// selected set and the batch just chosen.
+template <bool kGlobalKeys>
 __global__ void __launch_bounds__(256)
-resp_small_kernel(Shape sh, Params pr, Ws ws, int round, int psize, int bsize, int sel_base,
-                  int32_t* trace_batch) {
+gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int prev_bsize, int prev_base,
+                   int32_t* trace_pool, int32_t* trace_batch) {
+  extern __shared__ float dyn[];      // refreshed coverage [ldM], then LDS keys [N]
+  __shared__ int hist[256], scan[16], bc[2], flag;
+  __shared__ int pool_s[64], chosen[64], bidx[64];
+  __shared__ uint32_t bkeys[64];
+  const int p = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float* bnew = dyn;
+  const float* alpha = ws.alpha + p * ws.s_m;
+  float* cov = ws.cov + p * ws.s_cov;
+  const float* E = ws.E + p * ws.s_E;
+  const int nb = round > 0 ? prev_bsize : 0;
+  if (round > 0) {
+    if (wave == 0) small_batch(sh, ws, p, prev_psize, prev_bsize, (sh.m + 255) / 256, pool_s, bkeys, chosen, bidx);
+    __syncthreads();
+    if (blockIdx.x == 0) commit_batch(sh, ws, p, round - 1, prev_bsize, prev_base, pool_s, chosen, trace_batch);
+    // two row chunks per trip, all their batch-column loads in flight together
+    for (int m0 = tid * 4; m0 < sh.m; m0 += 2048) {
+      float4 c[2], a[2], b[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int m = min(m0 + h * 1024, sh.ldM - 4);
+        a[h] = *reinterpret_cast<const float4*>(alpha + m);
+        b[h] = *reinterpret_cast<const float4*>(cov + m);
+        c[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      for (int k0 = 0; k0 < nb; k0 += 16) {
+        // indices past the batch repeat its last column: a maximum is unchanged
+        float4 v[2][16];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int q = 0; q < 16; ++q)
+            v[h][q] = *reinterpret_cast<const float4*>(
+                E + static_cast<long long>(bidx[min(k0 + q, nb - 1)]) * sh.ldM + min(m0 + h * 1024, sh.ldM - 4));
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            c[h].x = fmaxf(c[h].x, a[h].x * v[h][q].x); c[h].y = fmaxf(c[h].y, a[h].y * v[h][q].y);
+            c[h].z = fmaxf(c[h].z, a[h].z * v[h][q].z); c[h].w = fmaxf(c[h].w, a[h].w * v[h][q].w);
+          }
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int m = m0 + h * 1024;
+        if (m < sh.m) {
+          const float4 r = make_float4(fmaxf(b[h].x, c[h].x), fmaxf(b[h].y, c[h].y), fmaxf(b[h].z, c[h].z),
+                                       fmaxf(b[h].w, c[h].w));
+          *reinterpret_cast<float4*>(bnew + m) = r;
+          if (blockIdx.x == 0) *reinterpret_cast<float4*>(cov + m) = r;
+        }
+      }
+    }
+  } else {
+    for (int m = tid * 4; m < sh.m; m += 1024) *reinterpret_cast<float4*>(bnew + m) = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  __syncthreads();
+  const int col0 = blockIdx.x * kGainColsF + wave * kCpwF;
+  float* u = ws.u + p * ws.s_u;
+  float acc[kCpwF];
+  const float* col[kCpwF];
+#pragma unroll
+  for (int c = 0; c < kCpwF; ++c) {
+    acc[c] = 0.f;
+    col[c] = E + static_cast<long long>(min(col0 + c, sh.N - 1)) * sh.ldM;
+  }
+#pragma unroll 4
+  for (int m = lane * 4; m < sh.m; m += 256) {
+    const float4 a = *reinterpret_cast<const float4*>(alpha + m);
+    const float4 b = *reinterpret_cast<const float4*>(bnew + m);
+#pragma unroll
+    for (int c = 0; c < kCpwF; ++c) {
+      const float4 v = *reinterpret_cast<const float4*>(col[c] + m);
+      acc[c] += fmaxf(a.x * v.x - b.x, 0.f);
+      acc[c] += fmaxf(a.y * v.y - b.y, 0.f);
+      acc[c] += fmaxf(a.z * v.z - b.z, 0.f);
+      acc[c] += fmaxf(a.w * v.w - b.w, 0.f);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < kCpwF; ++c) {
+    const float s = wave_sum(acc[c]);
+    if (lane == 0 && col0 + c < sh.N) st_dev(&u[col0 + c], s);
+  }
+
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  if (!last_arrival(&cnt[0], gridDim.x, &flag)) return;
+  if (tid == 0) st_dev(&cnt[0], 0);
+  uint32_t* keys = kGlobalKeys ? ws.keys + p * ws.s_keys : reinterpret_cast<uint32_t*>(dyn + sh.ldM);
+  const int* sel = ws.sel + p * ws.s_sel;
+  for (int base = 0; base < sh.N; base += 256 * 16) {
+    float g[16];
+    int sl[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int i = min(base + q * 256 + tid, sh.N - 1);
+      g[q] = ld_dev(&u[i]);
+      sl[q] = sel[i];
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int i = base + q * 256 + tid;
+      if (i < sh.N) {
+        bool taken = sl[q] >= 0;
+        for (int k = 0; k < nb; ++k) taken |= bidx[k] == i;
+        keys[i] = taken ? 0u : score_key(g[q]);
+      }
+    }
+  }
+  __syncthreads();
+  int* pool = ws.pool + p * ws.s_pool;
+  block_topk256(keys, sh.N, psize, pool, hist, scan, bc);
+  if (trace_pool) {
+    int32_t* tp = trace_pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
+    for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool[j] : -1;
+  }
+}
+
+// Small pools, after the last round: its batch from the responsibility sums.
+__global__ void __launch_bounds__(64) final_batch_kernel(Shape sh, Ws ws, int round, int psize, int bsize,
+                                                         int sel_base, int32_t* trace_batch) {
+  __shared__ int pool_s[64], chosen[64], bidx[64];
+  __shared__ uint32_t keys[64];
+  const int p = blockIdx.x;
+  small_batch(sh, ws, p, psize, bsize, (sh.m + 255) / 256, pool_s, keys, chosen, bidx);
+  __syncthreads();
+  commit_batch(sh, ws, p, round, bsize, sel_base, pool_s, chosen, trace_batch);
+}
+
+// Pool of at most 64: per-block responsibility sums; the batch is picked by
+// the next kernel (the next round's gains, or the final batch kernel).
+__global__ void __launch_bounds__(256) resp_small_kernel(Shape sh, Params pr, Ws ws, int psize) {
   __shared__ int pool_s[64];
   __shared__ float wsum[4][64];
-  __shared__ uint32_t keys[64];
-  __shared__ int chosen[64];
-  __shared__ int flag;
   const int p = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid < 64) pool_s[tid] = (tid < psize) ? ws.pool[p * ws.s_pool + tid] : 0;
@@ -272,30 +490,7 @@ resp_small_kernel(Shape sh, Params pr, Ws ws, int round, int psize, int bsize, i
   __syncthreads();
   float* sp = ws.spart + p * ws.s_spart;
   if (tid < psize)
-    st_dev(&sp[static_cast<long long>(blockIdx.x) * 64 + tid], ((wsum[0][tid] + wsum[1][tid]) + wsum[2][tid]) + wsum[3][tid]);
-
-  // tail: block sums in block order, then the batch
-  int* cnt = ws.cnt + p * ws.s_cnt;
-  if (!last_arrival(&cnt[1], gridDim.x, &flag)) return;
-  if (tid == 0) st_dev(&cnt[1], 0);
-  if (tid < psize) {
-    float s = 0.f;
-    const int nb = gridDim.x;
-    int b = 0;
-    for (; b + 8 <= nb; b += 8) {
-      float t[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) t[q] = ld_dev(&sp[static_cast<long long>(b + q) * 64 + tid]);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) s += t[q];
-    }
-    for (; b < nb; ++b) s += ld_dev(&sp[static_cast<long long>(b) * 64 + tid]);
-    keys[tid] = score_key(s);
-  }
-  __syncthreads();
-  if (wave == 0) wave_topb(keys, psize, bsize, chosen);
-  __syncthreads();
-  commit_batch(sh, ws, p, round, bsize, sel_base, pool_s, chosen, trace_batch);
+    sp[static_cast<long long>(blockIdx.x) * 64 + tid] = ((wsum[0][tid] + wsum[1][tid]) + wsum[2][tid]) + wsum[3][tid];
 }
 
 // Large pools: per-row max mu_m and softmax denominator over the pool.
@@ -374,7 +569,14 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
   int* cnt = ws.cnt + p * ws.s_cnt;
   if (!last_arrival(&cnt[4], gridDim.x, &flag)) return;
   if (tid == 0) st_dev(&cnt[4], 0);
-  for (int j = tid; j < psize; j += 256) keys[j] = score_key(ld_dev(&sv[j]));
+  {
+    float g[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) g[q] = ld_dev(&sv[min(q * 256 + tid, psize - 1)]);
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (q * 256 + tid < psize) keys[q * 256 + tid] = score_key(g[q]);
+  }
   __syncthreads();
   block_topk256(keys, psize, bsize, chosen, hist, scan, bc);
   commit_batch(sh, ws, p, round, bsize, sel_base, pool, chosen, trace_batch);
@@ -416,6 +618,7 @@ __global__ void __launch_bounds__(256) objective_kernel(Shape sh, Ws ws) {
   if (threadIdx.x == 0) {
     st_dev(&cnt[2], 0);
     float a = 0.f, b = 0.f;
+#pragma unroll 8
     for (unsigned k = 0; k < gridDim.x; ++k) { a += ld_dev(&sp[2 * k]); b += ld_dev(&sp[2 * k + 1]); }
     float* st = ws.stats + p * ws.s_st;
     st[2] = a;
@@ -442,39 +645,70 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
                             int32_t* trace_batch, hipStream_t st) {
   const bool global_keys = sh.N > kLdsKeys;
   const size_t key_lds = global_keys ? 0 : static_cast<size_t>(sh.N) * sizeof(uint32_t);
-  const bool small_pool = sh.pool_cap <= 64;
-  int selected = 0;
+  const size_t fused_lds = static_cast<size_t>(sh.ldM) * sizeof(float) + key_lds;
+  // small pools fuse the batch pick and the coverage refresh into the gains
+  // kernel while the refreshed coverage fits in LDS next to the keys
+  // fused only while the call is latency-bound: every fused block re-reads
+  // the batch columns, which costs more than a launch once the client
+  // matrix is large
+  const long long cbar_bytes = 4LL * sh.B * sh.N * sh.m;
+  const bool fused = sh.pool_cap <= 64 && fused_lds <= 56 * 1024 && cbar_bytes <= (48LL << 20);
+  const dim3 gg((sh.N + kGainCols - 1) / kGainCols, sh.B);
+  const dim3 ggf((sh.N + kGainColsF - 1) / kGainColsF, sh.B);
+  int selected = 0, prev_psize = 0, prev_bsize = 0, prev_base = 0;
   for (int r = 0; r < sh.rounds; ++r) {
     const int psize = min(sh.pool_cap, sh.N - selected);
     const int bsize = min(sh.b, sh.K - selected);
-    if (r > 0) {
-      timer_mark(kStCov, true, st);
-      launch_cov(sh, ws, sh.b, st);
-      timer_mark(kStCov, false, st);
-    }
-    const dim3 gg((sh.N + kGainCols - 1) / kGainCols, sh.B);
-    timer_mark(kStGains, true, st);
-    if (global_keys)
-      hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, trace_pool);
-    else
-      hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, trace_pool);
-    timer_mark(kStGains, false, st);
-    timer_mark(kStResp, true, st);
-    if (small_pool) {
-      hipLaunchKernelGGL(resp_small_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws, r,
-                         psize, bsize, selected, trace_batch);
+    if (fused) {
+      timer_mark(kStGains, true, st);
+      if (global_keys)
+        hipLaunchKernelGGL(gains_fused_kernel<true>, ggf, dim3(256), fused_lds, st, sh, ws, r, psize,
+                           prev_psize, prev_bsize, prev_base, trace_pool, trace_batch);
+      else
+        hipLaunchKernelGGL(gains_fused_kernel<false>, ggf, dim3(256), fused_lds, st, sh, ws, r, psize,
+                           prev_psize, prev_bsize, prev_base, trace_pool, trace_batch);
+      timer_mark(kStGains, false, st);
+      timer_mark(kStResp, true, st);
+      hipLaunchKernelGGL(resp_small_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws,
+                         psize);
+      timer_mark(kStResp, false, st);
     } else {
-      hipLaunchKernelGGL(rowstat_kernel, dim3((sh.m + 63) / 64, sh.B), dim3(256), 0, st, sh, pr, ws, psize);
-      hipLaunchKernelGGL(colsum_kernel, dim3((psize + 3) / 4, sh.B), dim3(256),
-                         static_cast<size_t>(sh.pool_cap) * sizeof(uint32_t), st, sh, ws, r, psize, bsize,
-                         selected, trace_batch);
+      if (r > 0) {
+        timer_mark(kStCov, true, st);
+        launch_cov(sh, ws, sh.b, st);
+        timer_mark(kStCov, false, st);
+      }
+      timer_mark(kStGains, true, st);
+      if (global_keys)
+        hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, trace_pool);
+      else
+        hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, trace_pool);
+      timer_mark(kStGains, false, st);
+      timer_mark(kStResp, true, st);
+      if (sh.pool_cap <= 64)
+        hipLaunchKernelGGL(resp_small_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws,
+                           psize);
+      else {
+        hipLaunchKernelGGL(rowstat_kernel, dim3((sh.m + 63) / 64, sh.B), dim3(256), 0, st, sh, pr, ws, psize);
+        hipLaunchKernelGGL(colsum_kernel, dim3((psize + 3) / 4, sh.B), dim3(256),
+                           static_cast<size_t>(sh.pool_cap) * sizeof(uint32_t), st, sh, ws, r, psize, bsize,
+                           selected, trace_batch);
+      }
+      if (sh.pool_cap <= 64)
+        hipLaunchKernelGGL(final_batch_kernel, dim3(sh.B), dim3(64), 0, st, sh, ws, r, psize, bsize, selected,
+                           trace_batch);
+      timer_mark(kStResp, false, st);
     }
-    timer_mark(kStResp, false, st);
+    prev_psize = psize;
+    prev_bsize = bsize;
+    prev_base = selected;
     selected += bsize;
   }
-  const int last_b = sh.K - (sh.rounds - 1) * sh.b;
   timer_mark(kStObjective, true, st);
-  launch_cov(sh, ws, last_b, st);
+  if (fused)
+    hipLaunchKernelGGL(final_batch_kernel, dim3(sh.B), dim3(64), 0, st, sh, ws, sh.rounds - 1, prev_psize,
+                       prev_bsize, prev_base, trace_batch);
+  launch_cov(sh, ws, prev_bsize, st);
   hipLaunchKernelGGL(objective_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
   timer_mark(kStObjective, false, st);
   return hipGetLastError();

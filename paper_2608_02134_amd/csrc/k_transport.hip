@@ -19,7 +19,10 @@ template <typename T, int G>
 __global__ void __launch_bounds__(256)
 transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos3d, T* out_hidden,
                  int32_t* out_pos, int32_t* out_idx) {
+  constexpr int kMB = 8;                  // member rows loaded together
+  constexpr int CH = sizeof(T) == 2 ? 1 : 2;   // 16-byte chunks per 8-element group
   __shared__ unsigned long long masks[4];
+  __shared__ int members[256];
   __shared__ float red[16];
   const int jj = blockIdx.x, p = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -38,37 +41,52 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
   float mass = 0.f;
   for (int i0 = 0; i0 < sh.N; i0 += 256) {
+    // ordered member list of this chunk (ascending source index)
     const int i = i0 + tid;
     const bool member = i < sh.N && pi[i] == j;
     const unsigned long long bal = __ballot(member);
     __syncthreads();
     if (lane == 0) masks[wave] = bal;
     __syncthreads();
+    int before = 0, total = 0;
     for (int w = 0; w < 4; ++w) {
-      unsigned long long mk = masks[w];
-      while (mk) {
-        const int b = __ffsll(static_cast<long long>(mk)) - 1;
-        mk &= mk - 1;
-        const int ii = i0 + w * 64 + b;
-        const float mi = m0 + m1 * (inv_mean > 0.f ? eb[ii] * inv_mean : 1.f);
-        mass += mi;
+      const int c = __popcll(masks[w]);
+      if (w < wave) before += c;
+      total += c;
+    }
+    if (member) members[before + __popcll(bal & ((1ull << lane) - 1ull))] = i;
+    __syncthreads();
+    for (int b0 = 0; b0 < total; b0 += kMB) {
+      // all member rows of the batch are loaded before any accumulation
+      uint4 raw[kMB][G][CH];
+      float mi[kMB];
+#pragma unroll
+      for (int q = 0; q < kMB; ++q) {
+        const int ii = members[min(b0 + q, total - 1)];
+        mi[q] = m0 + m1 * (inv_mean > 0.f ? eb[ii] * inv_mean : 1.f);
         const T* row = H + static_cast<long long>(ii) * sh.d;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-          const int grp = tid + g * 256;
-          if (grp < ngroups) {
-            const uint4 raw = ld16(row + grp * 8);
-            if constexpr (sizeof(T) == 2) {
-              const bf16_t* v = reinterpret_cast<const bf16_t*>(&raw);
+          const int grp = min(tid + g * 256, ngroups - 1);
 #pragma unroll
-              for (int e = 0; e < 8; ++e) acc[g][e] += mi * bf16_to_f32(v[e]);
-            } else {
-              const float* v = reinterpret_cast<const float*>(&raw);
-              const uint4 raw2 = ld16(row + grp * 8 + 4);
-              const float* v2 = reinterpret_cast<const float*>(&raw2);
+          for (int c = 0; c < CH; ++c) raw[q][g][c] = ld16(row + grp * 8 + c * 4);
+        }
+      }
 #pragma unroll
-              for (int e = 0; e < 4; ++e) { acc[g][e] += mi * v[e]; acc[g][e + 4] += mi * v2[e]; }
-            }
+      for (int q = 0; q < kMB; ++q) {
+        if (b0 + q >= total) break;
+        mass += mi[q];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          if constexpr (sizeof(T) == 2) {
+            const bf16_t* v = reinterpret_cast<const bf16_t*>(&raw[q][g][0]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[g][e] += mi[q] * bf16_to_f32(v[e]);
+          } else {
+            const float* v = reinterpret_cast<const float*>(&raw[q][g][0]);
+            const float* v2 = reinterpret_cast<const float*>(&raw[q][g][1]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { acc[g][e] += mi[q] * v[e]; acc[g][e + 4] += mi[q] * v2[e]; }
           }
         }
       }
