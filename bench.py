@@ -13,6 +13,7 @@ Prints one JSON line:
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -39,11 +40,68 @@ WORKLOAD_TEXT = {
 }
 
 
-def kernel_work(stage: str, w, m_rows: int):
+# Sources whose change invalidates a stored PMC traffic measurement of the
+# selection kernels.
+TRAFFIC_SOURCES = ["paper_2608_02134_amd/csrc/k_select.hip", "paper_2608_02134_amd/csrc/gmc_device.h",
+                   "paper_2608_02134_amd/csrc/gmc_internal.h", "paper_2608_02134_amd/csrc/gmc_api.hip"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def source_hash(paths=TRAFFIC_SOURCES) -> str:
+    h = hashlib.sha256()
+    for rel in paths:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload: str, stage: str):
+    """HBM bytes per launch of the dominant kernel from the stored rocprofv3
+    FETCH_SIZE / WRITE_SIZE passes, scaled by the copy-kernel calibration;
+    None when absent or taken on different kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None, "no stored counter measurement"
+    ent = rec.get("workloads", {}).get(workload)
+    if not ent or ent.get("stage") != stage:
+        return None, "no stored counter measurement for this kernel"
+    if ent.get("source_hash") != source_hash():
+        return None, "kernel sources changed since the counters were taken"
+    cal = rec["copy_calibration"]
+    fetch = ent["fetch_kib_per_launch"] * 1024.0 * cal["fetch_factor"]
+    write = ent["write_kib_per_launch"] * 1024.0 * cal["write_factor"]
+    return fetch + write, (f"rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE on {ent['kernel']}, "
+                           f"scaled by a {cal['bytes'] / 2**20:.0f} MiB copy; see profiles/")
+
+
+def copy_calibration(mib: int, reps: int = 10):
+    """A plain device copy of known size (read `mib` MiB, write `mib` MiB), for
+    scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps,
+                      "kernel": "torch elementwise mul by 1 (read + write)"}), flush=True)
+
+
+def kernel_work(stage: str, w, m_rows: int, kr: int = 0, bsel: int = 16, pool_cap: int = 64):
     """Algorithmic bytes or flops of one launch of a stage's kernel."""
     n, k, b = w.n, w.k, w.batch
     if stage == "gains":      # the token-major client matrix once, row weights, coverage, gains
         return "hbm", b * (4.0 * m_rows * n + 8.0 * m_rows + 4.0 * n)
+    if stage == "select":     # every round in one launch: per round the client rows of the
+        total, sel = 0.0, 0  # unselected tokens (gains), of the pool (responsibilities) and of
+        while sel < kr:      # the batch (coverage), plus row weights and coverage once
+            ps, bs = min(pool_cap, n - sel), min(bsel, kr - sel)
+            total += 4.0 * m_rows * ((n - sel) + ps + bs) + 8.0 * m_rows + 4.0 * n
+            sel += bs
+        return "hbm", b * total
     if stage == "appearance":  # N x N x d Gram
         return "mfma", b * 2.0 * n * n * w.d
     if stage == "transport":   # every member row once + the compact output
@@ -62,11 +120,17 @@ def main():
     ap.add_argument("--workload", default="qwen", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="time budget of the oracle CPU baseline sample (0 disables)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the operator is single-GPU and this build has no "
               "multi-GPU path (see the design notes on sharding by image)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
 
     import torch
     from paper_2608_02134_amd import binding, synth
@@ -125,9 +189,9 @@ def main():
               for i, name in enumerate(binding.STAGE_NAMES)}
 
     rounds, pool_cap, bcap, m_rows = binding.gmc_trace_dims(w.n, w.t, w.k)
-    single_kernel = ["gains", "appearance", "transport", "logits"]
+    single_kernel = ["select", "gains", "appearance", "transport", "logits"]
     dom = max(single_kernel, key=lambda s: stages[s]["ms_per_step"])
-    bound, work = kernel_work(dom, w, m_rows)
+    bound, work = kernel_work(dom, w, m_rows, kr, bcap, pool_cap)
     avg_s = stages[dom]["launch_avg_us"] / 1e6
     if bound == "hbm":
         achieved, peak, unit = work / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
@@ -135,9 +199,11 @@ def main():
         achieved = work / avg_s / 1e12
         peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
         unit = "TFLOP/s"
+    traffic, traffic_note = stored_traffic(args.workload, dom)
     roofline = {"bound": bound, "kernel": dom, "achieved": achieved, "peak": peak, "unit": unit,
-                "frac": achieved / peak, "traffic": None,
-                "work_per_launch": work, "launch_avg_us": stages[dom]["launch_avg_us"]}
+                "frac": achieved / peak, "traffic": traffic, "traffic_note": traffic_note,
+                "work_per_launch": work, "launch_avg_us": stages[dom]["launch_avg_us"],
+                "source_hash": source_hash()}
 
     cpu = None
     if args.cpu_seconds > 0:

@@ -55,10 +55,12 @@ extern "C" {
 #define GMC_BF16 1
 
 /* Number of float entries gmc_trace.stats receives per problem. */
-#define GMC_STATS 8
+#define GMC_STATS 9
 /* stats layout: [0] s_x  [1] mean selected-cosine gap over discarded tokens
  *               [2] F(S)  [3] F(V)  [4] realised K  [5] rounds  [6] M rows
- *               [7] number of discarded tokens                              */
+ *               [7] number of discarded tokens
+ *               [8] device status: 0 ok; 1 = a grid barrier of the
+ *                   persistent selection timed out (results invalid)      */
 
 /*
  * gmc_config - model shape, capacities and the frozen settings.
@@ -191,11 +193,13 @@ int gmc_trace_dims(int64_t N, int64_t T, int64_t K, int64_t* rounds, int64_t* po
  *   [6] singleton gains + candidate pool           [7] responsibility + batch
  *   [8] final coverage + objective values          [9] assignment
  *   [10] transport + compaction                    [11] per-call state reset
+ *   [12] persistent selection (all rounds in one launch; stages 5-7 and the
+ *        final coverage are then empty)
  * gmc_timing_read synchronises the stream, returns per-stage total
  * milliseconds and span counts accumulated since the last read, and clears
  * them.  Errors: GMC_ERR_STATE, GMC_ERR_ARG (n < GMC_TIMERS), GMC_ERR_HIP.
  */
-#define GMC_TIMERS 12
+#define GMC_TIMERS 13
 int gmc_timing_enable(int enable);
 int gmc_timing_read(double* total_ms, int64_t* spans, int32_t n);
 

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libgmc.so")
 
 GMC_OK, GMC_ERR_ARG, GMC_ERR_CAPACITY, GMC_ERR_STATE, GMC_ERR_HIP = 0, -1, -2, -3, -4
 GMC_F32, GMC_BF16 = 0, 1
-GMC_STATS = 8
+GMC_STATS = 9
 
 _i32, _f32, _i64, _vp = ctypes.c_int32, ctypes.c_float, ctypes.c_int64, ctypes.c_void_p
 
@@ -232,9 +232,9 @@ def gmc_timing_read():
     return list(ms), list(cnt)
 
 
-GMC_TIMERS = 12
+GMC_TIMERS = 13
 STAGE_NAMES = ["probe", "logits", "heads", "appearance", "spatial", "cov", "gains", "resp",
-               "objective", "assign", "transport", "init"]
+               "objective", "assign", "transport", "init", "select"]
 SIGNATURES["gmc_timing_enable"] = (ctypes.c_int, [ctypes.c_int])
 SIGNATURES["gmc_timing_read"] = (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64),
                                                 ctypes.c_int32])

@@ -141,7 +141,7 @@ struct Plan {
   Capacity cap;
   long long s_n, s_z, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
       s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
-      s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat;
+      s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_tc;
 };
 
 Plan make_plan(const gmc_config& c) {
@@ -182,7 +182,7 @@ Plan make_plan(const gmc_config& c) {
   pl.s_sel = k.N;
   pl.s_ord = k.N;
   pl.s_pool = k.pool_cap;
-  pl.s_spart = 64 * cdiv(k.ldM, 256);
+  pl.s_spart = 2 * 64 * cdiv(k.ldM, 64);
   pl.s_bat = k.bmax;
   pl.s_slot = k.N;
   pl.s_sup = k.N;
@@ -197,6 +197,8 @@ Plan make_plan(const gmc_config& c) {
   pl.s_cnt = kCounters;
   pl.s_rstat = 3LL * k.ldM;
   pl.s_lstat = static_cast<long long>(c.landmarks) * c.landmarks;
+  pl.s_tu = 2LL * k.N;
+  pl.s_tc = 2LL * k.ldM;
   return pl;
 }
 
@@ -241,6 +243,8 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   ws->keys = reinterpret_cast<uint32_t*>(take(pl.s_keys, 4)); ws->s_keys = pl.s_keys;
   ws->u = reinterpret_cast<float*>(take(pl.s_u, 4)); ws->s_u = pl.s_u;
   ws->cnt = reinterpret_cast<int*>(take(pl.s_cnt, 4)); ws->s_cnt = pl.s_cnt;
+  ws->tu = reinterpret_cast<unsigned long long*>(take(pl.s_tu, 8)); ws->s_tu = pl.s_tu;
+  ws->tc = reinterpret_cast<unsigned long long*>(take(pl.s_tc, 8)); ws->s_tc = pl.s_tc;
   F(rstat); F(lstat);
 #undef F
 #undef I

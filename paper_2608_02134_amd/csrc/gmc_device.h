@@ -32,27 +32,56 @@ template <> __device__ __forceinline__ float from_f32<float>(float v) { return v
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
 
 // ---------------------------------------------------------------------------
-// wave64 reductions
+// wave64 scans and reductions on DPP row operations (gfx9 family):
+// row_shr:n moves values n lanes up inside each 16-lane row, row_bcast:15
+// and row_bcast:31 carry a row's last lane into the following rows.  Lanes
+// without a source keep `old` (the operation's identity).  A reduction is the
+// inclusive scan's last lane, read back as a wave-uniform value.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int dpp_i(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, kCtrl, kRowMask, 0xf, false);
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_f(float old, float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), kCtrl, kRowMask, 0xf,
+                                                    false));
 }
-__device__ __forceinline__ float wave_min(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, kWave));
+#define GMC_WAVE_SCAN(T, DPP, ID, OP)          \
+  v = OP(v, DPP<0x111, 0xf>(ID, v));           \
+  v = OP(v, DPP<0x112, 0xf>(ID, v));           \
+  v = OP(v, DPP<0x114, 0xf>(ID, v));           \
+  v = OP(v, DPP<0x118, 0xf>(ID, v));           \
+  v = OP(v, DPP<0x142, 0xa>(ID, v));           \
+  v = OP(v, DPP<0x143, 0xc>(ID, v));           \
   return v;
+
+__device__ __forceinline__ int op_add_i(int a, int b) { return a + b; }
+__device__ __forceinline__ float op_add_f(float a, float b) { return a + b; }
+__device__ __forceinline__ int op_and_i(int a, int b) { return a & b; }
+__device__ __forceinline__ int op_or_i(int a, int b) { return a | b; }
+
+// Inclusive prefix sums over the 64 lanes.
+__device__ __forceinline__ int wave_scan_add(int v) { GMC_WAVE_SCAN(int, dpp_i, 0, op_add_i) }
+__device__ __forceinline__ float wave_scan_addf(float v) { GMC_WAVE_SCAN(float, dpp_f, 0.f, op_add_f) }
+__device__ __forceinline__ float wave_scan_maxf(float v) { GMC_WAVE_SCAN(float, dpp_f, -INFINITY, fmaxf) }
+__device__ __forceinline__ float wave_scan_minf(float v) { GMC_WAVE_SCAN(float, dpp_f, INFINITY, fminf) }
+__device__ __forceinline__ int wave_scan_and(int v) { GMC_WAVE_SCAN(int, dpp_i, -1, op_and_i) }
+__device__ __forceinline__ int wave_scan_or(int v) { GMC_WAVE_SCAN(int, dpp_i, 0, op_or_i) }
+#undef GMC_WAVE_SCAN
+
+__device__ __forceinline__ float lane63(float v) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
-__device__ __forceinline__ int wave_sum_i(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+__device__ __forceinline__ float wave_sum(float v) { return lane63(wave_scan_addf(v)); }
+__device__ __forceinline__ float wave_max(float v) { return lane63(wave_scan_maxf(v)); }
+__device__ __forceinline__ float wave_min(float v) { return lane63(wave_scan_minf(v)); }
+__device__ __forceinline__ int wave_sum_i(int v) { return __builtin_amdgcn_readlane(wave_scan_add(v), 63); }
+__device__ __forceinline__ uint32_t wave_and_u(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(wave_scan_and(static_cast<int>(v)), 63));
+}
+__device__ __forceinline__ uint32_t wave_or_u(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(wave_scan_or(static_cast<int>(v)), 63));
 }
 // Reduce across the 16 lanes of one MFMA row group (lanes l with equal l/16).
 __device__ __forceinline__ float group16_sum(float v) {
@@ -104,12 +133,7 @@ __device__ __forceinline__ float block_min(float v, float* red) {
 // ints of LDS.
 __device__ __forceinline__ int block_exclusive_scan(int v, int* scan, int* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  int incl = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int t = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += t;
-  }
+  const int incl = wave_scan_add(v);
   __syncthreads();
   if (lane == 63) scan[w] = incl;
   __syncthreads();
@@ -186,6 +210,21 @@ __device__ __forceinline__ void st_dev(int* p, int v) {
 }
 __device__ __forceinline__ float ld_dev(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void st_dev64(unsigned long long* p, unsigned long long v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long ld_dev64(const unsigned long long* p) {
+  return __hip_atomic_load(const_cast<unsigned long long*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// A float with a 32-bit tag in the high word (one 8-byte atomic access).
+__device__ __forceinline__ unsigned long long tag_value(unsigned tag, float v) {
+  return (static_cast<unsigned long long>(tag) << 32) | __float_as_uint(v);
+}
+__device__ __forceinline__ unsigned tag_of(unsigned long long w) { return static_cast<unsigned>(w >> 32); }
+__device__ __forceinline__ float value_of(unsigned long long w) {
+  return __uint_as_float(static_cast<unsigned>(w & 0xFFFFFFFFull));
 }
 
 // Last-block detection: every wave waits until its device-coherent stores

@@ -11,7 +11,7 @@ constexpr int kMaxHeads = 32;     // Hq limit (head-pattern Gram kept in registe
 constexpr int kMaxProbe = 8;      // probe rank limit
 constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 16;      // tokens per head-Gram block
-constexpr int kStats = 8;
+constexpr int kStats = 9;
 constexpr int kCounters = 8;      // completion counters per problem
 
 // Call shape, resolved on the host for one gmc_prune call.
@@ -66,7 +66,7 @@ struct Ws {
   int* sel;        long long s_sel;     // round that selected i, -1    [N]
   int* order;      long long s_ord;     // support in selection order   [N]
   int* pool;       long long s_pool;    // current pool                 [pool_cap]
-  float* spart;    long long s_spart;   // per-block score partials     [ceil(M/256)][64]
+  float* spart;    long long s_spart;   // score partials per row chunk [2][ceil(M/64)][64]
   int* batch;      long long s_bat;     // last batch                   [b]
   int* slot;       long long s_slot;    // rank of a selected token     [N]
   int* sup;        long long s_sup;     // support, ascending           [N]
@@ -81,6 +81,10 @@ struct Ws {
   int* cnt;        long long s_cnt;     // completion counters          [kCounters]
   float* rstat;    long long s_rstat;   // large-pool row statistics    [3][ldM]
   float* lstat;    long long s_lstat;   // landmark min distance        [L*L]
+  // persistent selection: values tagged with (round + 1) in the high word,
+  // double-buffered by round parity; zeroed at the start of every call
+  unsigned long long* tu; long long s_tu;  // tagged gains               [2][N]
+  unsigned long long* tc; long long s_tc;  // tagged coverage            [2][ldM]
 };
 
 }  // namespace gmc

@@ -11,7 +11,7 @@ namespace gmc {
 // Stage ids of the measurement timer (see gmc_timing_enable in gmc.h).
 enum Stage {
   kStProbe = 0, kStLogits, kStHeads, kStAppearance, kStSpatial, kStCov, kStGains, kStResp,
-  kStObjective, kStAssign, kStTransport, kStInit, kNumStages
+  kStObjective, kStAssign, kStTransport, kStInit, kStSelect, kNumStages
 };
 // Records a hipEvent on `st` opening (begin) or closing a stage span when
 // timing is enabled; a no-op otherwise.

@@ -37,24 +37,24 @@ constexpr int kLdsKeys = 12288;         // pool top-k keys live in LDS up to thi
 // Deterministic top-k over n keys (256-thread block): the `count` largest
 // keys, equal keys resolved to the lower index.  Indices are written in
 // ascending order to out[0..count).  count must not exceed the number of
-// non-zero keys.  Radix selection of the threshold key (4 passes of 8-bit
-// digits, parallel digit search), then one packed scan for the ordered
+// non-zero keys.  Radix selection of the threshold key with 8-bit digits
+// (digits shared by every key are skipped; two histogram buffers, so each
+// pass needs two block barriers), then one packed scan for the ordered
 // compaction (each thread owns a contiguous index segment).
+// hist: 512 ints of LDS, scan: >= 16 ints, bc: 2 ints.
 __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, int* hist, int* scan,
                               int* bc) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // bits shared by every key need no radix pass: AND / OR over all keys
+  hist[tid] = 0;
+  hist[256 + tid] = 0;
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
   for (int i = tid; i < n; i += 256) {
     const uint32_t k = keys[i];
     kand &= k;
     kor |= k;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    kand &= static_cast<uint32_t>(__shfl_xor(static_cast<int>(kand), o, kWave));
-    kor |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(kor), o, kWave));
-  }
+  kand = wave_and_u(kand);
+  kor = wave_or_u(kor);
   if (lane == 0) { scan[wave] = static_cast<int>(kand); scan[4 + wave] = static_cast<int>(kor); }
   __syncthreads();
   kand = static_cast<uint32_t>(scan[0]) & static_cast<uint32_t>(scan[1]) & static_cast<uint32_t>(scan[2]) &
@@ -62,35 +62,28 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
   kor = static_cast<uint32_t>(scan[4]) | static_cast<uint32_t>(scan[5]) | static_cast<uint32_t>(scan[6]) |
         static_cast<uint32_t>(scan[7]);
   const uint32_t diff = kand ^ kor;                 // bits that vary between keys
-  uint32_t mask = 0, prefix = 0;
+  uint32_t mask = 0;
   int top = 24;
   while (top > 0 && ((diff >> top) & 0xFFu) == 0u) {
     mask |= 0xFFu << top;
     top -= 8;
   }
-  prefix = kand & mask;
-  int remaining = count;
-  __syncthreads();
-  for (int shift = top; shift >= 0; shift -= 8) {
-    hist[tid] = 0;
-    __syncthreads();
+  uint32_t prefix = kand & mask;
+  int remaining = count, buf = 0;
+  for (int shift = top; shift >= 0; shift -= 8, buf ^= 1) {
+    int* h = hist + buf * 256;
     for (int i = tid; i < n; i += 256) {
       const uint32_t k = keys[i];
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
+      if ((k & mask) == prefix) atomicAdd(&h[(k >> shift) & 255u], 1);
     }
+    hist[(buf ^ 1) * 256 + tid] = 0;   // read in the previous pass; used by the next one
     __syncthreads();
     if (wave == 0) {
       // wave 0 scans the 256 bins from the top digit down, 4 per lane
       int v[4], loc = 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) { v[q] = hist[255 - (lane * 4 + q)]; loc += v[q]; }
-      int incl = loc;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int t = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += t;
-      }
-      int excl = incl - loc;
+      for (int q = 0; q < 4; ++q) { v[q] = h[255 - (lane * 4 + q)]; loc += v[q]; }
+      int excl = wave_scan_add(loc) - loc;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if (excl < remaining && remaining <= excl + v[q]) {
@@ -131,6 +124,98 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
   __syncthreads();
 }
 
+// Register-resident variant of the same selection for small n: thread t
+// holds the keys of its contiguous index segment [t*seg, t*seg + seg) in
+// k[0..KPT) (0 past the segment).  Every wave scans the histogram itself, so
+// a radix pass needs one block barrier (three histogram buffers rotate).
+// hist: 768 ints of LDS, scan: >= 16 ints.
+template <int KPT>
+__device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, int* out, int* hist, int* scan) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  hist[tid] = 0;
+  hist[256 + tid] = 0;
+  hist[512 + tid] = 0;
+  // excluded (zero) keys are never selected: they take no part in the
+  // shared-digit test or the histograms
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    kand &= k[q] ? k[q] : 0xFFFFFFFFu;
+    kor |= k[q];
+  }
+  kand = wave_and_u(kand);
+  kor = wave_or_u(kor);
+  if (lane == 0) { scan[wave] = static_cast<int>(kand); scan[4 + wave] = static_cast<int>(kor); }
+  __syncthreads();
+  kand = static_cast<uint32_t>(scan[0]) & static_cast<uint32_t>(scan[1]) & static_cast<uint32_t>(scan[2]) &
+         static_cast<uint32_t>(scan[3]);
+  kor = static_cast<uint32_t>(scan[4]) | static_cast<uint32_t>(scan[5]) | static_cast<uint32_t>(scan[6]) |
+        static_cast<uint32_t>(scan[7]);
+  const uint32_t diff = kand ^ kor;
+  uint32_t mask = 0;
+  int top = 24;
+  while (top > 0 && ((diff >> top) & 0xFFu) == 0u) {
+    mask |= 0xFFu << top;
+    top -= 8;
+  }
+  uint32_t prefix = kand & mask;
+  int remaining = count, buf = 0;
+  for (int shift = top; shift >= 0; shift -= 8) {
+    int* h = hist + buf * 256;
+#pragma unroll
+    for (int q = 0; q < KPT; ++q)
+      if (k[q] != 0u && (k[q] & mask) == prefix) atomicAdd(&h[(k[q] >> shift) & 255u], 1);
+    const int nxt = buf == 2 ? 0 : buf + 1;
+    hist[nxt * 256 + tid] = 0;   // last read two passes ago
+    __syncthreads();
+    int v[4], loc = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) { v[q] = h[255 - (lane * 4 + q)]; loc += v[q]; }
+    const int incl = wave_scan_add(loc);
+    int excl = incl - loc;
+    const bool hit = excl < remaining && remaining <= incl;
+    int dig = 0, rem = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (excl < remaining && remaining <= excl + v[q]) {
+        dig = 255 - (lane * 4 + q);
+        rem = remaining - excl;
+      }
+      excl += v[q];
+    }
+    const int src = __ffsll(static_cast<unsigned long long>(__ballot(hit))) - 1;
+    dig = __builtin_amdgcn_readlane(dig, src);
+    rem = __builtin_amdgcn_readlane(rem, src);
+    prefix |= static_cast<uint32_t>(dig) << shift;
+    mask |= 0xFFu << shift;
+    remaining = rem;
+    buf = nxt;
+  }
+  const uint32_t kth = prefix;
+  int gt = 0, eq = 0;
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    gt += k[q] > kth;
+    eq += k[q] == kth;
+  }
+  int tot;
+  const int pre = block_exclusive_scan(gt | (eq << 16), scan, &tot);
+  int gt_b = static_cast<int>(static_cast<unsigned>(pre) & 0xFFFFu);
+  int eq_b = static_cast<int>(static_cast<unsigned>(pre) >> 16);
+  const int i0 = tid * seg;
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    if (k[q] > kth) {
+      out[gt_b + min(eq_b, remaining)] = i0 + q;
+      ++gt_b;
+    } else if (k[q] == kth) {
+      if (eq_b < remaining) out[gt_b + eq_b] = i0 + q;
+      ++eq_b;
+    }
+  }
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------------------
 // coverage refresh with a batch
 // ---------------------------------------------------------------------------
@@ -155,7 +240,7 @@ template <bool kGlobalKeys>
 __global__ void __launch_bounds__(256)
 gains_kernel(Shape sh, Ws ws, int round, int psize, int32_t* trace_pool) {
   extern __shared__ uint32_t keys_lds[];
-  __shared__ int hist[256], scan[16], bc[2], flag;
+  __shared__ int hist[512], scan[16], bc[2], flag;
   const int p = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col0 = blockIdx.x * kGainCols + wave * kCpw;
@@ -246,8 +331,9 @@ __device__ void wave_topb(const uint32_t* keys, int psize, int bsize, int* chose
   const int lane = threadIdx.x & 63;
   const uint32_t k = (lane < psize) ? keys[lane] : 0u;
   int rank = 0;
-  for (int t = 0; t < 64; ++t) {
-    const uint32_t kt = __shfl(k, t, kWave);
+#pragma unroll 16
+  for (int t = 0; t < psize; ++t) {
+    const uint32_t kt = keys[t];     // same address in every lane: an LDS broadcast
     rank += (kt > k) || (kt == k && t < lane);
   }
   const bool take = lane < psize && rank < bsize;
@@ -316,7 +402,7 @@ __global__ void __launch_bounds__(256)
 gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int prev_bsize, int prev_base,
                    int32_t* trace_pool, int32_t* trace_batch) {
   extern __shared__ float dyn[];      // refreshed coverage [ldM], then LDS keys [N]
-  __shared__ int hist[256], scan[16], bc[2], flag;
+  __shared__ int hist[512], scan[16], bc[2], flag;
   __shared__ int pool_s[64], chosen[64], bidx[64];
   __shared__ uint32_t bkeys[64];
   const int p = blockIdx.y;
@@ -476,7 +562,7 @@ __global__ void __launch_bounds__(256) resp_small_kernel(Shape sh, Params pr, Ws
     float ex[64];
 #pragma unroll
     for (int j = 0; j < 64; ++j) {
-      ex[j] = (j < psize) ? expf(v[j] * inv - zmax) : 0.f;
+      ex[j] = (j < psize) ? __expf(v[j] * inv - zmax) : 0.f;
       den += ex[j];
     }
     const float rden = 1.f / den;
@@ -520,7 +606,7 @@ __global__ void __launch_bounds__(256) rowstat_kernel(Shape sh, Params pr, Ws ws
   if (mu > 0.f)
 #pragma unroll 8
     for (int j = j0; j < j1; ++j)
-      den += expf(fmaxf(a * E[static_cast<long long>(pool[j]) * sh.ldM] - c, 0.f) * inv - zmax);
+      den += __expf(fmaxf(a * E[static_cast<long long>(pool[j]) * sh.ldM] - c, 0.f) * inv - zmax);
   __syncthreads();
   part[wave][lane] = den;
   __syncthreads();
@@ -538,7 +624,7 @@ __global__ void __launch_bounds__(256) rowstat_kernel(Shape sh, Params pr, Ws ws
 __global__ void __launch_bounds__(256)
 colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, int32_t* trace_batch) {
   extern __shared__ uint32_t keys[];   // pool_cap words
-  __shared__ int hist[256], scan[16], bc[2], flag;
+  __shared__ int hist[512], scan[16], bc[2], flag;
   __shared__ int chosen[1024];
   const int p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int jj = blockIdx.x * 4 + wave;
@@ -558,10 +644,10 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
       const float4 zm = *reinterpret_cast<const float4*>(rs + sh.ldM + m);
       const float4 rd = *reinterpret_cast<const float4*>(rs + 2 * sh.ldM + m);
       float r;
-      r = fmaxf(a.x * v.x - c.x, 0.f); acc += expf(r * inv.x - zm.x) * rd.x * r;
-      r = fmaxf(a.y * v.y - c.y, 0.f); acc += expf(r * inv.y - zm.y) * rd.y * r;
-      r = fmaxf(a.z * v.z - c.z, 0.f); acc += expf(r * inv.z - zm.z) * rd.z * r;
-      r = fmaxf(a.w * v.w - c.w, 0.f); acc += expf(r * inv.w - zm.w) * rd.w * r;
+      r = fmaxf(a.x * v.x - c.x, 0.f); acc += __expf(r * inv.x - zm.x) * rd.x * r;
+      r = fmaxf(a.y * v.y - c.y, 0.f); acc += __expf(r * inv.y - zm.y) * rd.y * r;
+      r = fmaxf(a.z * v.z - c.z, 0.f); acc += __expf(r * inv.z - zm.z) * rd.z * r;
+      r = fmaxf(a.w * v.w - c.w, 0.f); acc += __expf(r * inv.w - zm.w) * rd.w * r;
     }
     const float s = wave_sum(acc);
     if (lane == 0) st_dev(&sv[jj], s);
@@ -582,6 +668,322 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
   commit_batch(sh, ws, p, round, bsize, sel_base, pool, chosen, trace_batch);
 }
 
+// ---------------------------------------------------------------------------
+// Persistent selection: every round of a small-pool call in one cooperative
+// launch.  The grid is nblk blocks per problem (all co-resident).  A round:
+//   gains  - waves stream the client rows of unselected tokens (round robin
+//            over all waves of the problem) and publish u_i tagged with the
+//            round number
+//   pool   - every block waits for the tagged gains and picks the same pool
+//            (identical inputs, deterministic top-k)
+//   resp   - one wave per 64-row chunk: responsibility softmax over the pool,
+//            per-chunk sums per pool token -> global
+//   | grid barrier
+//   batch  - every block sums the chunk partials in chunk order and picks the
+//            same batch; block 0 records it
+//   cov    - one wave per chunk: b_m <- max(b_m, max_{j in batch} Cbar_mj),
+//            published tagged; every block waits for the tags and copies b
+//            into LDS
+// Tagged values and the chunk partials are double-buffered by round parity.
+// A buffer is rewritten two rounds later, and the grid barrier between keeps
+// every block within one round of the others, so no reader can see a value
+// of the wrong round.
+// Everything another block reads in the same launch goes through
+// device-coherent stores and loads.
+constexpr int kSpinLimit = 1 << 18;   // bounded barrier wait (a fraction of a second)
+constexpr int kCntBarrier = 5;         // arrivals at grid barriers (cumulative)
+constexpr int kCntStatus = 7;          // device status bits, 1 = barrier timeout
+
+// Grid barrier number k (1, 2, ...) over the nblk blocks of one problem:
+// arrivals accumulate (no reset inside the launch) and a block waits until
+// nblk * k have arrived.  The wait is
+// bounded: after kSpinLimit polls, or once any block of the problem has
+// recorded a timeout, the block records the timeout, stops waiting at this
+// and every later barrier, and runs to its end, so every wave always exits.
+__device__ __forceinline__ void grid_barrier(int* cnt, int nblk, int k, int* failed) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int old = __hip_atomic_fetch_add(&cnt[kCntBarrier], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old != nblk * k - 1 && !*failed) {
+      for (int spin = 0;; ++spin) {
+        if (__hip_atomic_load(&cnt[kCntBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nblk * k) break;
+        if (spin == kSpinLimit ||
+            ((spin & 63) == 63 &&
+             __hip_atomic_load(&cnt[kCntStatus], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
+          __hip_atomic_store(&cnt[kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          *failed = 1;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Marks the call failed (device status word) after a bounded wait.
+__device__ __forceinline__ void mark_timeout(int* cnt, int* failed) {
+  __hip_atomic_store(&cnt[kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  *failed = 1;
+}
+
+// Pool of the persistent selection with the keys in registers: thread t
+// takes the gains of its contiguous segment (taken tokens key 0), waiting
+// until each carries this round's tag.
+template <int KPT>
+__device__ __forceinline__ void pool_regs(const Shape& sh, const unsigned long long* tu, unsigned tag,
+                                          const unsigned char* taken, int psize, int* pool_s, int* hist, int* scan,
+                                          int* cnt, int* failed) {
+  const int seg = (sh.N + 255) / 256;
+  const int i0 = threadIdx.x * seg;
+  unsigned long long w[KPT];
+  bool need[KPT];
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    const int i = min(i0 + q, sh.N - 1);
+    need[q] = q < seg && i0 + q < sh.N && !taken[i];
+    w[q] = ld_dev64(&tu[i]);
+  }
+  for (int spin = 0;; ++spin) {
+    bool pend = false;
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) pend |= need[q] && tag_of(w[q]) != tag;
+    if (!pend || *failed) break;
+    if (spin == kSpinLimit) { mark_timeout(cnt, failed); break; }
+    __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+    for (int q = 0; q < KPT; ++q)
+      if (need[q] && tag_of(w[q]) != tag) w[q] = ld_dev64(&tu[min(i0 + q, sh.N - 1)]);
+  }
+  uint32_t k[KPT];
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) k[q] = need[q] ? score_key(value_of(w[q])) : 0u;
+  block_topk_regs<KPT>(k, seg, psize, pool_s, hist, scan);
+}
+
+__global__ void __launch_bounds__(256)
+select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_pool, int32_t* trace_batch) {
+  extern __shared__ float dyn[];
+  float* bl = dyn;                                                   // b_m       [ldM]
+  uint32_t* keys = reinterpret_cast<uint32_t*>(dyn + sh.ldM);        // pool keys [N]
+  unsigned char* taken = reinterpret_cast<unsigned char*>(keys + sh.N);  // selected flags [N]
+  __shared__ int hist[768], scan[16], bc[2], failed;
+  __shared__ int pool_s[64], chosen[64], bidx[64];
+  __shared__ uint32_t bkeys[64];
+  const int p = blockIdx.y, blk = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nwaves = nblk * 4, gw = blk * 4 + wave;
+  const int nchunk = (sh.m + 63) / 64;
+  const float* alpha = ws.alpha + p * ws.s_m;
+  float* cov = ws.cov + p * ws.s_cov;
+  const float* E = ws.E + p * ws.s_E;
+  unsigned long long* tu = ws.tu + p * ws.s_tu;
+  unsigned long long* tc = ws.tc + p * ws.s_tc;
+  float* sp = ws.spart + p * ws.s_spart;
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  for (int m = tid; m < sh.ldM; m += 256) bl[m] = 0.f;     // coverage is zero at call start
+  for (int i = tid; i < sh.N; i += 256) taken[i] = 0;
+  if (tid == 0) failed = 0;
+  __syncthreads();
+  int selected = 0;
+  for (int r = 0; r < sh.rounds; ++r) {
+    const int psize = min(sh.pool_cap, sh.N - selected);
+    const int bsize = min(sh.b, sh.K - selected);
+    const unsigned tag = static_cast<unsigned>(r + 1);
+    unsigned long long* tur = tu + (r & 1) * sh.N;
+    unsigned long long* tcr = tc + (r & 1) * sh.ldM;
+    float* spr = sp + (r & 1) * 64LL * nchunk;
+    // ---- singleton gains of unselected tokens, two tokens per wave pass,
+    //      published with this round's tag
+    for (int i0 = gw; i0 < sh.N; i0 += 2 * nwaves) {
+      const int i1 = i0 + nwaves;
+      const bool ok0 = taken[i0] == 0;
+      const bool ok1 = i1 < sh.N && taken[min(i1, sh.N - 1)] == 0;
+      if (!ok0 && !ok1) continue;
+      // a token that needs no gain re-reads the other one's row (cache hits)
+      const float* c0 = E + static_cast<long long>(ok0 ? i0 : i1) * sh.ldM;
+      const float* c1 = E + static_cast<long long>(ok1 ? i1 : i0) * sh.ldM;
+      float a0 = 0.f, a1 = 0.f;
+#pragma unroll 4
+      for (int m = lane * 4; m < sh.m; m += 256) {
+        const float4 a = *reinterpret_cast<const float4*>(alpha + m);
+        const float4 b = *reinterpret_cast<const float4*>(bl + m);
+        const float4 v0 = *reinterpret_cast<const float4*>(c0 + m);
+        const float4 v1 = *reinterpret_cast<const float4*>(c1 + m);
+        a0 += fmaxf(a.x * v0.x - b.x, 0.f); a0 += fmaxf(a.y * v0.y - b.y, 0.f);
+        a0 += fmaxf(a.z * v0.z - b.z, 0.f); a0 += fmaxf(a.w * v0.w - b.w, 0.f);
+        a1 += fmaxf(a.x * v1.x - b.x, 0.f); a1 += fmaxf(a.y * v1.y - b.y, 0.f);
+        a1 += fmaxf(a.z * v1.z - b.z, 0.f); a1 += fmaxf(a.w * v1.w - b.w, 0.f);
+      }
+      a0 = wave_sum(a0);
+      a1 = wave_sum(a1);
+      if (lane == 0) {
+        if (ok0) st_dev64(&tur[i0], tag_value(tag, a0));
+        if (ok1) st_dev64(&tur[i1], tag_value(tag, a1));
+      }
+    }
+
+    // ---- the pool, identical in every block (waits for this round's gains)
+    if (sh.N <= 256 * 8)
+      pool_regs<8>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
+    else if (sh.N <= 256 * 16)
+      pool_regs<16>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
+    else {
+      for (int base = 0; base < sh.N; base += 256 * 16) {
+        unsigned long long w[16];
+        bool need[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int i = base + q * 256 + tid;
+          need[q] = i < sh.N && !taken[min(i, sh.N - 1)];
+          w[q] = ld_dev64(&tur[min(i, sh.N - 1)]);
+        }
+        for (int spin = 0;; ++spin) {
+          bool pend = false;
+#pragma unroll
+          for (int q = 0; q < 16; ++q) pend |= need[q] && tag_of(w[q]) != tag;
+          if (!pend || failed) break;
+          if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int q = 0; q < 16; ++q)
+            if (need[q] && tag_of(w[q]) != tag) w[q] = ld_dev64(&tur[min(base + q * 256 + tid, sh.N - 1)]);
+        }
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int i = base + q * 256 + tid;
+          if (i < sh.N) keys[i] = need[q] ? score_key(value_of(w[q])) : 0u;
+        }
+      }
+      __syncthreads();
+      block_topk256(keys, sh.N, psize, pool_s, hist, scan, bc);
+    }
+    {
+      // clamp to valid rows (defensive) and pad past psize with a valid row, masked below
+      int pv = 0;
+      if (tid < 64) pv = min(max(pool_s[tid < psize ? tid : 0], 0), sh.N - 1);
+      __syncthreads();
+      if (tid < 64) pool_s[tid] = pv;
+      __syncthreads();
+    }
+    if (blk == 0 && trace_pool) {
+      int32_t* tp = trace_pool + (static_cast<long long>(p) * sh.rounds + r) * sh.pool_cap;
+      for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool_s[j] : -1;
+    }
+
+    // ---- responsibilities: one wave per 64-row chunk, lane = client row
+    for (int c = gw; c < nchunk; c += nwaves) {
+      const int m = c * 64 + lane;
+      const bool row_ok = m < sh.m;
+      const int mc = row_ok ? m : 0;
+      const float a = row_ok ? alpha[mc] : 0.f;
+      const float b = bl[mc];
+      float v[64];
+      float mu = 0.f;
+#pragma unroll
+      for (int j = 0; j < 64; ++j) v[j] = E[static_cast<long long>(pool_s[j]) * sh.ldM + mc];
+#pragma unroll
+      for (int j = 0; j < 64; ++j) {
+        const float rr = (j < psize) ? fmaxf(a * v[j] - b, 0.f) : 0.f;
+        v[j] = rr;
+        mu = fmaxf(mu, rr);
+      }
+      if (mu > 0.f) {
+        const float inv = 1.f / (pr.tau_r * mu + pr.resp_eps);
+        const float zmax = mu * inv;
+        float den = 0.f;
+        float ex[64];
+#pragma unroll
+        for (int j = 0; j < 64; ++j) {
+          ex[j] = (j < psize) ? __expf(v[j] * inv - zmax) : 0.f;
+          den += ex[j];
+        }
+        const float rden = 1.f / den;
+#pragma unroll
+        for (int j = 0; j < 64; ++j) v[j] = ex[j] * rden * v[j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < 64; ++j) v[j] = 0.f;
+      }
+      const float s = transpose_reduce64(v, lane);
+      st_dev(&spr[static_cast<long long>(c) * 64 + lane], s);
+    }
+    // the one grid barrier of the round: it also bounds how far any block
+    // can run ahead, which makes the double-buffered tagged values safe
+    grid_barrier(cnt, nblk, r + 1, &failed);
+
+    // ---- the batch, identical in every block
+    if (wave == 0) {
+      // chunk partials summed in chunk order; 32 loads in flight at a time
+      float s = 0.f;
+      for (int c0 = 0; c0 < nchunk; c0 += 32) {
+        float t[32];
+#pragma unroll
+        for (int q = 0; q < 32; ++q) t[q] = ld_dev(&spr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
+#pragma unroll
+        for (int q = 0; q < 32; ++q)
+          if (c0 + q < nchunk) s += t[q];
+      }
+      bkeys[lane] = score_key(s);
+      __builtin_amdgcn_wave_barrier();
+      wave_topb(bkeys, psize, bsize, chosen);
+      __builtin_amdgcn_wave_barrier();
+      if (lane < bsize) bidx[lane] = pool_s[chosen[lane]];
+    }
+    __syncthreads();
+    if (blk == 0) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, trace_batch);
+    if (tid < bsize) taken[bidx[tid]] = 1;
+    const bool last = r + 1 == sh.rounds;
+
+    // ---- coverage refresh with the batch: one wave per chunk, published
+    //      with this round's tag (the last round stores the plain values)
+    for (int c = gw; c < nchunk; c += nwaves) {
+      const int m = c * 64 + lane;
+      const int mc = min(m, sh.m - 1);
+      const float a = alpha[mc];
+      float cm = bl[mc];
+      for (int k0 = 0; k0 < bsize; k0 += 16) {
+        float v[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          v[q] = E[static_cast<long long>(bidx[min(k0 + q, bsize - 1)]) * sh.ldM + mc];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) cm = fmaxf(cm, a * v[q]);
+      }
+      if (m < sh.m) {
+        if (last)
+          cov[m] = cm;
+        else
+          st_dev64(&tcr[m], tag_value(tag, cm));
+      }
+    }
+    selected += bsize;
+    if (last) break;
+    // ---- every block copies the refreshed coverage into LDS (waits for the tags)
+    for (int m0 = 0; m0 < sh.m; m0 += 256 * 8) {
+      unsigned long long w[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) w[q] = ld_dev64(&tcr[min(m0 + q * 256 + tid, sh.m - 1)]);
+      for (int spin = 0;; ++spin) {
+        bool pend = false;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) pend |= tag_of(w[q]) != tag;
+        if (!pend || failed) break;
+        if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (tag_of(w[q]) != tag) w[q] = ld_dev64(&tcr[min(m0 + q * 256 + tid, sh.m - 1)]);
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (m0 + q * 256 + tid < sh.m) bl[m0 + q * 256 + tid] = value_of(w[q]);
+    }
+    __syncthreads();
+  }
+}
+
 // Per-call state: nothing selected, coverage and row-weight padding zero,
 // completion counters cleared.
 __global__ void select_init_kernel(Shape sh, Ws ws) {
@@ -591,6 +993,12 @@ __global__ void select_init_kernel(Shape sh, Ws ws) {
   for (int m = x0; m < sh.ldM; m += stride) {
     ws.cov[p * ws.s_cov + m] = 0.f;
     if (m >= sh.m) ws.alpha[p * ws.s_m + m] = 0.f;
+    ws.tc[p * ws.s_tc + m] = 0ull;
+    ws.tc[p * ws.s_tc + sh.ldM + m] = 0ull;
+  }
+  for (int i = x0; i < sh.N; i += stride) {
+    ws.tu[p * ws.s_tu + i] = 0ull;
+    ws.tu[p * ws.s_tu + sh.N + i] = 0ull;
   }
   if (blockIdx.x == 0 && threadIdx.x < kCounters) ws.cnt[p * ws.s_cnt + threadIdx.x] = 0;
 }
@@ -641,8 +1049,52 @@ static void launch_cov(const Shape& sh, const Ws& ws, int nb, hipStream_t st) {
                      st, sh, ws, nb);
 }
 
+// Blocks per problem for the persistent selection, or 0 when the call does
+// not qualify (large pools, keys beyond LDS, too little co-residency).
+static int persistent_blocks(const Shape& sh, size_t lds) {
+  if (sh.pool_cap > 64 || sh.N > kLdsKeys || lds > 64 * 1024) return 0;
+  static int coop = -1, n_cu = 0;
+  if (coop < 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      coop = 0;
+  }
+  if (!coop) return 0;
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(select_persistent_kernel),
+                                                   256, lds) != hipSuccess || per_cu < 1)
+    return 0;
+  // one CU per block; about two gain tokens per wave
+  const int cap = n_cu / sh.B;
+  const int want = max((sh.N + 7) / 8, ((sh.m + 63) / 64 + 3) / 4);
+  const int nblk = min(cap, want);
+  return nblk >= 1 ? nblk : 0;
+}
+
 hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
                             int32_t* trace_batch, hipStream_t st) {
+  {
+    const size_t lds = (static_cast<size_t>(sh.ldM) + static_cast<size_t>(sh.N)) * sizeof(float) +
+                       ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15));
+    int nblk = persistent_blocks(sh, lds);
+    if (nblk > 0) {
+      Shape a_sh = sh;
+      Params a_pr = pr;
+      Ws a_ws = ws;
+      void* args[] = {&a_sh, &a_pr, &a_ws, &nblk, &trace_pool, &trace_batch};
+      timer_mark(kStSelect, true, st);
+      hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(select_persistent_kernel),
+                                                dim3(nblk, sh.B), dim3(256), args, static_cast<unsigned>(lds), st);
+      timer_mark(kStSelect, false, st);
+      if (e != hipSuccess) return e;
+      timer_mark(kStObjective, true, st);
+      hipLaunchKernelGGL(objective_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
+      timer_mark(kStObjective, false, st);
+      return hipGetLastError();
+    }
+  }
   const bool global_keys = sh.N > kLdsKeys;
   const size_t key_lds = global_keys ? 0 : static_cast<size_t>(sh.N) * sizeof(uint32_t);
   const size_t fused_lds = static_cast<size_t>(sh.ldM) * sizeof(float) + key_lds;

@@ -194,7 +194,9 @@ __global__ void export_client_kernel(Shape sh, Ws ws, float* out) {
 
 __global__ void export_stats_kernel(Shape sh, Ws ws, float* out) {
   const int p = blockIdx.x;
-  if (threadIdx.x < kStats) out[p * kStats + threadIdx.x] = ws.stats[p * ws.s_st + threadIdx.x];
+  // the last entry is the device status word (completion-counter slot 7)
+  if (threadIdx.x < kStats - 1) out[p * kStats + threadIdx.x] = ws.stats[p * ws.s_st + threadIdx.x];
+  if (threadIdx.x == kStats - 1) out[p * kStats + threadIdx.x] = static_cast<float>(ws.cnt[p * ws.s_cnt + 7]);
 }
 
 __global__ void export_ebar_kernel(Shape sh, Ws ws, float* out) {

@@ -184,6 +184,7 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
         assert rep.bf16_ulp_frac > 0.99, f"only {rep.bf16_ulp_frac:.4f} of bf16 outputs within 1 ulp"
     if gpu.get("stats") is not None:
         st = gpu["stats"]
+        assert st[8] == 0, f"device status word {st[8]} (grid barrier timeout)"
         assert abs(st[0] - a["sx"]) < 1e-4 + 1e-3 * a["sx"], f"s_x {st[0]} vs {a['sx']}"
         fs = float(cov.sum())
         assert abs(st[2] - fs) <= 1e-4 * fs, f"F(S) {st[2]} vs {fs}"
