@@ -34,6 +34,10 @@ struct Context {
   void* mem = nullptr;
   size_t bytes = 0;
   hipStream_t stream = nullptr;
+  // internal side stream for the bank kernels (default priority) and the
+  // fork/join events that order it against the caller's stream
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   int device = 0;
 };
 
@@ -313,10 +317,14 @@ void gmc_free(void) {
   g_timer.on = false;
   g_timer.release();
   if (!g_ctx) return;
-  if (g_ctx->mem) {
-    (void)hipSetDevice(g_ctx->device);
-    (void)hipFree(g_ctx->mem);
+  (void)hipSetDevice(g_ctx->device);
+  if (g_ctx->side) {
+    (void)hipStreamSynchronize(g_ctx->side);
+    (void)hipStreamDestroy(g_ctx->side);
   }
+  if (g_ctx->fork) (void)hipEventDestroy(g_ctx->fork);
+  if (g_ctx->join) (void)hipEventDestroy(g_ctx->join);
+  if (g_ctx->mem) (void)hipFree(g_ctx->mem);
   delete g_ctx;
   g_ctx = nullptr;
 }
@@ -354,6 +362,16 @@ int gmc_init(const gmc_config* cfg) {
     (void)hipFree(ctx->mem);
     delete ctx;
     return fail(GMC_ERR_HIP, "gmc_init: clearing the workspace failed (%s)", hipGetErrorString(err));
+  }
+  err = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
+  if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->fork, hipEventDisableTiming);
+  if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->join, hipEventDisableTiming);
+  if (err != hipSuccess) {
+    if (ctx->side) (void)hipStreamDestroy(ctx->side);
+    if (ctx->fork) (void)hipEventDestroy(ctx->fork);
+    (void)hipFree(ctx->mem);
+    delete ctx;
+    return fail(GMC_ERR_HIP, "gmc_init: side stream or events (%s)", hipGetErrorString(err));
   }
   g_ctx = ctx;
   return GMC_OK;
@@ -498,10 +516,21 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   const gmc_trace tr = trace ? *trace : gmc_trace{};
   err = launch_call_init(s, c.ws, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "call init: %s", hipGetErrorString(err));
+  // row norms, then the bank kernels on the side stream while the message
+  // kernels run on the caller's stream (they write disjoint client rows)
+  err = launch_rownorm(s, c.ws, hidden, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "row norms: %s", hipGetErrorString(err));
+  err = hipEventRecord(c.fork, st);
+  if (err == hipSuccess) err = hipStreamWaitEvent(c.side, c.fork, 0);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
+  err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, c.side);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
+  err = hipEventRecord(c.join, c.side);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
-  err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, st);
-  if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
+  err = hipStreamWaitEvent(st, c.join, 0);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   err = launch_selection(s, c.pr, c.ws, tr.round_pool, tr.round_batch, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "selection kernels: %s", hipGetErrorString(err));
   err = launch_assignment(s, c.pr, c.ws, hidden, tr.assign, st);

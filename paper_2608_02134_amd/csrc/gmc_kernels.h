@@ -17,8 +17,11 @@ enum Stage {
 // timing is enabled; a no-op otherwise.
 void timer_mark(int stage, bool begin, hipStream_t st);
 
-// Row norms, value probe, mass coordinate, native slice, head weights,
-// grounded row weights and normalised energy.
+// Squared row norms of the visual states (every later stage reads them).
+hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, hipStream_t st);
+
+// Value probe, mass coordinate, native slice, head weights, grounded row
+// weights and normalised energy (after launch_rownorm).
 hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
                           const void* text_q, const void* vis_k, const void* probe,
                           const float* nonvis_lse, float* trace_omega,

@@ -1,9 +1,12 @@
 // Population assignment (Sec. 3.4; App. H Eq. cond-assignment, Eq.
 // cond-population-gate).
 //
-// cos_ij = h_i.h_j / (|h_i| |h_j|) for every token i and support member j
-// comes from an MFMA GEMM against the gathered support rows (normalised after
-// the contraction).  The gap delta_i (best - second best), the sample gate
+// cos_ij = h_i.h_j / (|h_i| |h_j|) for every token i and support member j.
+// With the exact appearance bank every pair's cosine is already stored as
+// E_V = exp((cos - 1) / tau_v) in the client matrix (client row j, token i),
+// so cos_ij = 1 + tau_v ln E_V is gathered from there; the bounded bank keeps
+// only projected cosines, so there an MFMA GEMM against the gathered support
+// rows (normalised after the contraction) computes them.  The gap delta_i (best - second best), the sample gate
 // s_x = 1 - exp(-(mean_discarded delta / t)^p) and the local ambiguity g_i
 // then decide kappa_ij = cos_ij + w s_x g_i exp(-|p_i - p_j|^2 / tau_s);
 // pi(i) = argmax_j kappa_ij with ties to the lower source index, and
@@ -54,20 +57,52 @@ struct CosEpi {
   __device__ void row_stats(int, int, int, float, float) const {}
 };
 
+// Cosine of token i to the support member in slot j: from the stored
+// appearance client value (exact bank) or from the GEMM output.
+template <bool kFromE>
+struct CosSource {
+  const float* row;   // E row of token i (kFromE) or cosb row of token i
+  int mg;
+  const int* sup;
+  float tau_v;
+  __device__ __forceinline__ float get(int j) const {
+    if constexpr (kFromE) return 1.f + tau_v * __logf(row[mg + sup[j]]);
+    else return row[j];
+  }
+};
+
+template <bool kFromE>
+__device__ __forceinline__ CosSource<kFromE> cos_source(const Shape& sh, const Params& pr, const Ws& ws, int p, int i) {
+  CosSource<kFromE> c;
+  c.row = kFromE ? ws.E + p * ws.s_E + static_cast<long long>(i) * sh.ldM
+                 : ws.cosb + p * ws.s_cos + static_cast<long long>(i) * sh.ldK;
+  c.mg = sh.mg;
+  c.sup = ws.sup + p * ws.s_sup;
+  c.tau_v = pr.tau_v;
+  return c;
+}
+
 // delta_i = top1 - top2 of cos_i. over the support (0 when K = 1); one wave
 // per token; per-block sums of delta over discarded tokens.
-__global__ void __launch_bounds__(256) gap_kernel(Shape sh, Ws ws) {
+template <bool kFromE>
+__global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
   __shared__ float red[4];
   const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = blockIdx.x * 4 + wave;
   float contrib = 0.f;
   if (i < sh.N) {
-    const float* c = ws.cosb + p * ws.s_cos + static_cast<long long>(i) * sh.ldK;
+    const CosSource<kFromE> cs = cos_source<kFromE>(sh, pr, ws, p, i);
     float t1 = -INFINITY, t2 = -INFINITY;
-    for (int j = lane; j < sh.K; j += 64) {
-      const float v = c[j];
-      if (v > t1) { t2 = t1; t1 = v; }
-      else if (v > t2) t2 = v;
+    for (int j0 = 0; j0 < sh.K; j0 += 64 * 8) {
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = cs.get(min(j0 + q * 64 + lane, sh.K - 1));
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (j0 + q * 64 + lane >= sh.K) continue;
+        if (v[q] > t1) { t2 = t1; t1 = v[q]; }
+        else if (v[q] > t2) t2 = v[q];
+      }
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -104,6 +139,7 @@ __global__ void gate_kernel(Shape sh, Params pr, Ws ws, int nblk) {
 }
 
 // pi(i) = argmax_j kappa_ij; one wave per token.
+template <bool kFromE>
 __global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, int32_t* trace_assign) {
   const int p = blockIdx.y, lane = threadIdx.x & 63;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -118,20 +154,30 @@ __global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, 
     const float g = (pr.g_form == 1) ? (delta < pr.amb_margin ? 1.f : 0.f)
                                      : expf(-powf(delta / pr.amb_margin, pr.amb_p));
     const float w = pr.spatial_w * sx * g;
-    const float* c = ws.cosb + p * ws.s_cos + static_cast<long long>(i) * sh.ldK;
+    const CosSource<kFromE> cs = cos_source<kFromE>(sh, pr, ws, p, i);
     const float* pc = ws.pc + p * ws.s_pc;
     const float py = pc[2 * i], px = pc[2 * i + 1];
     const float inv_tau = 1.f / pr.tau_s;
     float best = -INFINITY;
     int bj = 0x7fffffff;
-    for (int j = lane; j < sh.K; j += 64) {
-      float k = c[j];
-      if (w > 0.f) {
-        const int sj = sup[j];
-        const float dy = py - pc[2 * sj], dx = px - pc[2 * sj + 1];
-        k += w * expf(-(dy * dy + dx * dx) * inv_tau);
+    for (int j0 = 0; j0 < sh.K; j0 += 64 * 4) {
+      float kv[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = min(j0 + q * 64 + lane, sh.K - 1);
+        float k = cs.get(j);
+        if (w > 0.f) {
+          const int sj = sup[j];
+          const float dy = py - pc[2 * sj], dx = px - pc[2 * sj + 1];
+          k += w * expf(-(dy * dy + dx * dx) * inv_tau);
+        }
+        kv[q] = k;
       }
-      if (k > best) { best = k; bj = j; }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = j0 + q * 64 + lane;
+        if (j < sh.K && kv[q] > best) { best = kv[q]; bj = j; }
+      }
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -152,16 +198,23 @@ static hipError_t assign_impl(const Shape& sh, const Params& pr, const Ws& ws, c
                               int32_t* trace_assign, hipStream_t st) {
   timer_mark(kStAssign, true, st);
   hipLaunchKernelGGL(support_kernel, dim3(sh.B), dim3(1024), 0, st, sh, ws);
-  const T* hidden = static_cast<const T*>(hidden_v);
-  RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
-  RowOperand<T> S{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, ws.sup, ws.s_sup, sh.K};
-  CosEpi epi{ws, sh.ldK, pr.norm_eps};
-  hipError_t err = launch_gemm_nt<T, 64, 64>(A, S, sh.d, sh.B, epi, st);
-  if (err != hipSuccess) return err;
   const int nblk = (sh.N + 3) / 4;
-  hipLaunchKernelGGL(gap_kernel, dim3(nblk, sh.B), dim3(256), 0, st, sh, ws);
+  if (sh.bounded) {
+    const T* hidden = static_cast<const T*>(hidden_v);
+    RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
+    RowOperand<T> S{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, ws.sup, ws.s_sup, sh.K};
+    CosEpi epi{ws, sh.ldK, pr.norm_eps};
+    hipError_t err = launch_gemm_nt<T, 64, 64>(A, S, sh.d, sh.B, epi, st);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(gap_kernel<false>, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws);
+  } else {
+    hipLaunchKernelGGL(gap_kernel<true>, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws);
+  }
   hipLaunchKernelGGL(gate_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, nblk);
-  hipLaunchKernelGGL(kappa_kernel, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws, trace_assign);
+  if (sh.bounded)
+    hipLaunchKernelGGL(kappa_kernel<false>, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws, trace_assign);
+  else
+    hipLaunchKernelGGL(kappa_kernel<true>, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws, trace_assign);
   timer_mark(kStAssign, false, st);
   return hipGetLastError();
 }

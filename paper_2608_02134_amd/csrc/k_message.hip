@@ -150,19 +150,21 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   float mx[4], sm[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) { mx[e] = -INFINITY; sm[e] = 0.f; }
-  Frag<T> kcur[KS], knext[KS];
+  // three key tiles in flight per wave: the current one and the next two
+  Frag<T> kcur[KS], kn1[KS], kn2[KS];
   load_keys(min(wave, last_tile), kcur);
+  load_keys(min(wave + 4, last_tile), kn1);
   for (int ct = wave; ct < ntile; ct += 4) {
-    load_keys(min(ct + 4, last_tile), knext);
+    load_keys(min(ct + 8, last_tile), kn2);
     const floatx4 acc = tile_mma(kcur);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kcur[ks] = knext[ks];
+    for (int ks = 0; ks < KS; ++ks) { kcur[ks] = kn1[ks]; kn1[ks] = kn2[ks]; }
     if (ct * 16 + oc < sh.N) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float s = acc[e] * scale;
         const float nm = fmaxf(mx[e], s);
-        sm[e] = sm[e] * expf(mx[e] - nm) + expf(s - nm);
+        sm[e] = sm[e] * __expf(mx[e] - nm) + __expf(s - nm);
         mx[e] = nm;
       }
     }
@@ -216,19 +218,33 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   }
   float* E = ws.E + p * ws.s_E;
   const float* ell = ws.ell + p * ws.s_ell;
-  load_keys(min(wave, last_tile), kcur);
-  for (int ct = wave; ct < ntile; ct += 4) {
-    load_keys(min(ct + 4, last_tile), knext);
-    const floatx4 acc = tile_mma(kcur);
+  // atom norms l_h[col] of the lane's four rows travel with the key tiles
+  auto load_ell = [&](int ct, float* lv) {
+    const int col = min(ct * 16 + oc, sh.N - 1);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kcur[ks] = knext[ks];
+    for (int e = 0; e < 4; ++e) lv[e] = ell[static_cast<long long>(hrow[e]) * sh.N + col];
+  };
+  float lcur[4], ln1[4], ln2[4];
+  load_keys(min(wave, last_tile), kcur);
+  load_ell(min(wave, last_tile), lcur);
+  load_keys(min(wave + 4, last_tile), kn1);
+  load_ell(min(wave + 4, last_tile), ln1);
+  for (int ct = wave; ct < ntile; ct += 4) {
+    load_keys(min(ct + 8, last_tile), kn2);
+    load_ell(min(ct + 8, last_tile), ln2);
+    const floatx4 acc = tile_mma(kcur);
+    float lv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { lv[e] = lcur[e]; lcur[e] = ln1[e]; ln1[e] = ln2[e]; }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) { kcur[ks] = kn1[ks]; kn1[ks] = kn2[ks]; }
     const int col = ct * 16 + oc;
     if (col < sh.N) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (!rvalid[e]) continue;
-        const float a = expf(acc[e] * scale - D[e]);
-        const float v = a * ell[static_cast<long long>(hrow[e]) * sh.N + col];
+        const float a = __expf(acc[e] * scale - D[e]);
+        const float v = a * lv[e];
         E[static_cast<long long>(col) * sh.ldM + mrow[e]] = v;
         rsum[e] += v;
         rmax[e] = fmaxf(rmax[e], v);
@@ -257,132 +273,145 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
 }
 
 // ---------------------------------------------------------------------------
-// Head-pattern Gram Gamma_hg = sum_(t,i) A_h A_g <w_h[i], w_g[i]>
-//   = sum_i [<w_h,w_g>/(l_h l_g)](i) * sum_t e_h[t,i] e_g[t,i]
-// and e2[h][i] = sum_t nu_t e_h[t,i]^2.  One block per 16 tokens; the t axis
-// streams through LDS in chunks of 16; each thread owns (token, pair-slot).
+// Head-pattern Gram (Eq. cond-head-pattern)
+//   Gamma_hg = sum_(t,i) A_h A_g <w_h[i], w_g[i]>
+//            = sum_i W_i[h][g] * G_i[h][g],  G_i = X_i X_i^T,
+// with X_i[h][t] = e_(h,t,i) (the token's grounded atoms, one contiguous
+// slice of its client row) and W_i[h][g] = <w_h[i], w_g[i]> / (l_h[i] l_g[i]).
+// One wave per token at a time: X_i is staged in LDS in 64-column chunks
+// (heads padded to 32), G_i accumulates on fp32 MFMA (16x16x4 tiles (0,0),
+// (0,1), (1,1); the Gram is symmetric), W_i is applied in the epilogue and the
+// weighted tiles accumulate over the wave's tokens.  The diagonal gives
+// e2[h][i] = sum_t nu_t e_(h,t,i)^2 = nu G_hh + (nu_T - nu) X_i[h][T-1]^2.
+// The block's four waves are summed in wave order into one partial per pair.
 // ---------------------------------------------------------------------------
-constexpr int kTC = 16;
-constexpr int kPairsPerThread = (kMaxHeads * (kMaxHeads + 1) / 2 + 15) / 16;
+constexpr int kGramTC = 64;                 // t columns per LDS chunk
+constexpr int kGramPitch = kGramTC + 4;     // floats per staged head row
+constexpr int kGramTok = 4;                 // tokens per wave (kHeadTok per block)
+static_assert(kGramTok * 4 == kHeadTok, "one block covers kHeadTok tokens");
 
 __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws ws) {
-  __shared__ float tileE[kMaxHeads * kTC * kHeadTok];
-  __shared__ float zt[kHeadTok * kMaxHeads * kMaxProbe];
-  __shared__ float lt[kMaxHeads * kHeadTok];
-  __shared__ short pair_h[kMaxHeads * (kMaxHeads + 1) / 2], pair_g[kMaxHeads * (kMaxHeads + 1) / 2];
-  const int p = blockIdx.y, i0 = blockIdx.x * kHeadTok;
-  const int tid = threadIdx.x, il = tid & 15, slot = tid >> 4;
-  const int H = sh.hq, T = sh.T;
-  if (tid == 0) {
-    int q = 0;
-    for (int h = 0; h < H; ++h)
-      for (int g = h; g < H; ++g) { pair_h[q] = h; pair_g[q] = g; ++q; }
-  }
+  __shared__ __attribute__((aligned(16))) float xs[4][32 * kGramPitch];
+  __shared__ float zs[4][32 * (kMaxProbe + 2)];
+  const int p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int H = sh.hq, T = sh.T, r = sh.r, zw = r + 2;
+  const int fr = lane & 15, fk = lane >> 4;
   const float nu_o = 1.f / (T - 1 + pr.terminal_q_weight);
   const float nu_last = pr.terminal_q_weight * nu_o;
-  float acc[kPairsPerThread];
-#pragma unroll
-  for (int q = 0; q < kPairsPerThread; ++q) acc[q] = 0.f;
-  float e2a[2] = {0.f, 0.f};
+  float* X = xs[wave];
+  float* Z = zs[wave];
   const float* E = ws.E + p * ws.s_E;
-  const int i = i0 + il;
-  for (int t0 = 0; t0 < T; t0 += kTC) {
-    const int tc = min(kTC, T - t0);
-    __syncthreads();
-    // unconditional (clamped) loads, masked afterwards, so they all issue together
-    constexpr int kPer = (kMaxHeads * kTC * kHeadTok) / 256;
-    float vals[kPer];
-#pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const int x = tid + q * 256;
-      const int tt = x % kTC, h = (x / kTC) % kMaxHeads, ii = x / (kTC * kMaxHeads);
-      const int hc = min(h, H - 1), tc_ = min(tt, tc - 1), ic = min(i0 + ii, sh.N - 1);
-      vals[q] = E[static_cast<long long>(ic) * sh.ldM + hc * T + t0 + tc_];
-    }
-#pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const int x = tid + q * 256;
-      const int tt = x % kTC, h = (x / kTC) % kMaxHeads, ii = x / (kTC * kMaxHeads);
-      const bool ok = h < H && tt < tc && i0 + ii < sh.N;
-      tileE[(h * kTC + tt) * kHeadTok + ii] = ok ? vals[q] : 0.f;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < kPairsPerThread; ++q) {
-      const int pq = slot + 16 * q;
-      if (pq < sh.npairs) {
-        const float* eh = &tileE[pair_h[pq] * kTC * kHeadTok + il];
-        const float* eg = &tileE[pair_g[pq] * kTC * kHeadTok + il];
-        float s = 0.f;
-        for (int tt = 0; tt < tc; ++tt) s += eh[tt * kHeadTok] * eg[tt * kHeadTok];
-        acc[q] += s;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int h = slot + 16 * j;
-      if (h < H) {
-        const float* eh = &tileE[h * kTC * kHeadTok + il];
-        float s = 0.f;
-        for (int tt = 0; tt < tc; ++tt) {
-          const float nu = (t0 + tt == T - 1) ? nu_last : nu_o;
-          s += nu * eh[tt * kHeadTok] * eh[tt * kHeadTok];
-        }
-        e2a[j] += s;
-      }
-    }
-  }
-  // per-token pattern weights <w_h, w_g> / (l_h l_g)
-  __syncthreads();
-  {
-    // batched, clamped loads of the tokens' probe coordinates and atom norms
-    constexpr int kZ = kHeadTok * kMaxHeads * kMaxProbe / 256;
-    constexpr int kL = kMaxHeads * kHeadTok / 256;
-    float zv[kZ], lv[kL];
-    const int nz = kHeadTok * sh.hr;
-#pragma unroll
-    for (int q = 0; q < kZ; ++q) {
-      const int x = min(tid + q * 256, nz - 1);
-      const int ii = min(i0 + x / sh.hr, sh.N - 1), c = x % sh.hr;
-      zv[q] = ws.z[p * ws.s_z + static_cast<long long>(ii) * sh.hr + c];
-    }
-#pragma unroll
-    for (int q = 0; q < kL; ++q) {
-      const int x = tid + q * 256;
-      const int h = min(x / kHeadTok, H - 1), ii = min(i0 + x % kHeadTok, sh.N - 1);
-      lv[q] = ws.ell[p * ws.s_ell + static_cast<long long>(h) * sh.N + ii];
-    }
-#pragma unroll
-    for (int q = 0; q < kZ; ++q) {
-      const int x = tid + q * 256;
-      if (x < nz) zt[x] = (i0 + x / sh.hr < sh.N) ? zv[q] : 0.f;
-    }
-#pragma unroll
-    for (int q = 0; q < kL; ++q) {
-      const int x = tid + q * 256;
-      if (x < H * kHeadTok) lt[x] = (i0 + x % kHeadTok < sh.N) ? lv[q] : 1.f;
-    }
-  }
-  __syncthreads();
   const float* sig = ws.sig + p * ws.s_sig;
-  float* gp = ws.gpart + p * ws.s_gpart + static_cast<long long>(blockIdx.x) * sh.npairs;
+  const float* zp = ws.z + p * ws.s_z;
+  const float* ellp = ws.ell + p * ws.s_ell;
+  float* e2 = ws.e2 + p * ws.s_e2;
+  floatx4 acc[3];
 #pragma unroll
-  for (int q = 0; q < kPairsPerThread; ++q) {
-    const int pq = slot + 16 * q;
-    float v = 0.f;
-    if (pq < sh.npairs && i < sh.N) {
-      const int h = pair_h[pq], g = pair_g[pq];
-      float dot = sig[h] * sig[g];
-      for (int c = 0; c < sh.r; ++c) dot += zt[il * sh.hr + h * sh.r + c] * zt[il * sh.hr + g * sh.r + c];
-      v = acc[q] * dot / (lt[h * kHeadTok + il] * lt[g * kHeadTok + il]);
+  for (int tl = 0; tl < 3; ++tl) acc[tl] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int x = lane; x < 32 * kGramPitch; x += 64) X[x] = 0.f;   // padding heads stay zero
+  __builtin_amdgcn_wave_barrier();
+  for (int j = 0; j < kGramTok; ++j) {
+    const int i = blockIdx.x * kHeadTok + wave * kGramTok + j;
+    if (i >= sh.N) break;                                          // wave-uniform
+    const float* row = E + static_cast<long long>(i) * sh.ldM;
+    // weight data of this token: z_h[c] (c < r), sigma_h, l_h[i]
+    {
+      float zv[(32 * (kMaxProbe + 2) + 63) / 64];
+#pragma unroll
+      for (int q = 0; q < (32 * (kMaxProbe + 2) + 63) / 64; ++q) {
+        const int x = min(lane + 64 * q, 32 * zw - 1);
+        const int h = min(x / zw, H - 1), c = x % zw;
+        const float za = zp[static_cast<long long>(i) * sh.hr + h * r + min(c, r - 1)];
+        const float sa = sig[h];
+        const float la = ellp[static_cast<long long>(h) * sh.N + i];
+        zv[q] = c < r ? za : (c == r ? sa : la);
+      }
+#pragma unroll
+      for (int q = 0; q < (32 * (kMaxProbe + 2) + 63) / 64; ++q) {
+        const int x = lane + 64 * q;
+        if (x < 32 * zw) {
+          const bool pad = x / zw >= H;
+          Z[x] = pad ? ((x % zw) == r + 1 ? 1.f : 0.f) : zv[q];
+        }
+      }
     }
-    v = group16_sum(v);
-    if (il == 0 && pq < sh.npairs) gp[pq] = v;
-  }
+    floatx4 g[3];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int h = slot + 16 * j;
-    if (h < H && i < sh.N) ws.e2[p * ws.s_e2 + static_cast<long long>(h) * sh.N + i] = e2a[j];
+    for (int tl = 0; tl < 3; ++tl) g[tl] = floatx4{0.f, 0.f, 0.f, 0.f};
+    int t0 = 0;
+    for (; t0 < T; t0 += kGramTC) {
+      const int tc = min(kGramTC, T - t0);
+      __builtin_amdgcn_wave_barrier();
+      // stage X_i[h][t0 .. t0 + tc) (clamped loads, masked stores)
+      float v[32];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int h = min(k * 4 + fk, H - 1), c = min(fr * 4 + q, tc - 1);
+          v[k * 4 + q] = row[h * T + t0 + c];
+        }
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int h = k * 4 + fk, c = fr * 4 + q;
+          if (h < H) X[h * kGramPitch + c] = c < tc ? v[k * 4 + q] : 0.f;
+        }
+      __builtin_amdgcn_wave_barrier();
+      const int nk = (tc + 3) / 4;
+      for (int kk = 0; kk < nk; ++kk) {
+        const float a0 = X[fr * kGramPitch + 4 * kk + fk];
+        const float a1 = X[(16 + fr) * kGramPitch + 4 * kk + fk];
+        g[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, a0, g[0], 0, 0, 0);
+        g[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, a1, g[1], 0, 0, 0);
+        g[2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, a1, g[2], 0, 0, 0);
+      }
+    }
+    const int tl_last = (T - 1) - (t0 - kGramTC);   // column of t = T-1 in the last chunk
+    __builtin_amdgcn_wave_barrier();
+    // epilogue: lane holds G[16 hb + 4 fk + e][16 gb + fr]
+#pragma unroll
+    for (int tl = 0; tl < 3; ++tl) {
+      const int hb = tl == 2 ? 1 : 0, gb = tl == 0 ? 0 : 1;
+      const int gg = 16 * gb + fr;
+      float wg[kMaxProbe];
+#pragma unroll
+      for (int c = 0; c < kMaxProbe; ++c) wg[c] = c < r ? Z[gg * zw + c] : 0.f;
+      const float sg = Z[gg * zw + r], lg = Z[gg * zw + r + 1];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int hh = 16 * hb + 4 * fk + e;
+        float dot = Z[hh * zw + r] * sg;
+#pragma unroll
+        for (int c = 0; c < kMaxProbe; ++c)
+          if (c < r) dot += Z[hh * zw + c] * wg[c];
+        const float w = dot / (Z[hh * zw + r + 1] * lg);
+        acc[tl][e] += g[tl][e] * w;
+        if (tl != 1 && hh == gg && hh < H) {
+          const float xl = X[hh * kGramPitch + tl_last];
+          e2[static_cast<long long>(hh) * sh.N + i] = nu_o * g[tl][e] + (nu_last - nu_o) * xl * xl;
+        }
+      }
+    }
+  }
+  // the block's partial: waves summed in order, one value per pair h <= g
+  __syncthreads();
+  float* red = &xs[0][0];   // 4 waves x 768 floats, staging buffers are free now
+#pragma unroll
+  for (int tl = 0; tl < 3; ++tl)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) red[wave * 768 + tl * 256 + e * 64 + lane] = acc[tl][e];
+  __syncthreads();
+  float* gp = ws.gpart + p * ws.s_gpart + static_cast<long long>(blockIdx.x) * sh.npairs;
+  for (int x = tid; x < 768; x += 256) {
+    const int tl = x / 256, e = (x / 64) % 4, l = x % 64;
+    const int hb = tl == 2 ? 1 : 0, gb = tl == 0 ? 0 : 1;
+    const int hh = 16 * hb + 4 * (l >> 4) + e, gg = 16 * gb + (l & 15);
+    if (hh <= gg && gg < H) {
+      const float v = ((red[x] + red[768 + x]) + red[2 * 768 + x]) + red[3 * 768 + x];
+      gp[hh * H - hh * (hh - 1) / 2 + (gg - hh)] = v;
+    }
   }
 }
 
@@ -410,22 +439,34 @@ __global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws
   const int p = blockIdx.x, tid = threadIdx.x, H = sh.hq, T = sh.T;
   const float* gp = ws.gpart + p * ws.s_gpart;
   const int nb = sh.n_head_blk;
-  for (int q = tid; q < sh.npairs; q += blockDim.x) {
-    int h = 0, rem = q;
-    while (rem >= H - h) { rem -= H - h; ++h; }
-    const int g = h + rem;
-    float s = 0.f;
-    int b = 0;
-    for (; b + 8 <= nb; b += 8) {
-      float v[8];
+  // every thread sums two pair slots over the block partials in block order,
+  // 32 blocks of loads in flight per slot
+  {
+    float s0 = 0.f, s1 = 0.f;
+    const int q0 = min(tid, sh.npairs - 1), q1 = min(tid + 256, sh.npairs - 1);
+    for (int b0 = 0; b0 < nb; b0 += 32) {
+      float v0[32], v1[32];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = gp[static_cast<long long>(b + j) * sh.npairs + q];
+      for (int j = 0; j < 32; ++j) {
+        const long long b = min(b0 + j, nb - 1);
+        v0[j] = gp[b * sh.npairs + q0];
+        v1[j] = gp[b * sh.npairs + q1];
+      }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) s += v[j];
+      for (int j = 0; j < 32; ++j)
+        if (b0 + j < nb) { s0 += v0[j]; s1 += v1[j]; }
     }
-    for (; b < nb; ++b) s += gp[static_cast<long long>(b) * sh.npairs + q];
-    gam[h][g] = s;
-    gam[g][h] = s;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int q = tid + 256 * k;
+      if (q < sh.npairs) {
+        int h = 0, rem = q;
+        while (rem >= H - h) { rem -= H - h; ++h; }
+        const int g = h + rem;
+        gam[h][g] = k ? s1 : s0;
+        gam[g][h] = k ? s1 : s0;
+      }
+    }
   }
   __syncthreads();
   const float* rowsum = ws.rowsum + p * ws.s_m;
@@ -434,11 +475,15 @@ __global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws
     const bool valid = h < H;
     // mean atom norm abar_h = sum_t Z_(h,t) / (T N) and activity
     float abar = 0.f;
-    if (valid) {
-#pragma unroll 16
-      for (int t = 0; t < T; ++t) abar += rowsum[h * T + t];
-      abar /= static_cast<float>(T) * sh.N;
+    for (int t0 = 0; t0 < T; t0 += 64) {
+      float rv[64];
+#pragma unroll
+      for (int t = 0; t < 64; ++t) rv[t] = rowsum[min(h, H - 1) * T + min(t0 + t, T - 1)];
+#pragma unroll
+      for (int t = 0; t < 64; ++t)
+        if (t0 + t < T) abar += rv[t];
     }
+    abar = valid ? abar / (static_cast<float>(T) * sh.N) : 0.f;
     const float ghh = valid ? gam[h][h] : 0.f;
     const bool active = valid && ghh > 0.f;
     const float nrm = active ? sqrtf(ghh) : 1.f;
@@ -508,13 +553,25 @@ __global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws
   __syncthreads();
   // grounded row weights beta_msg omega_h nu_t a_(h,t) / Z_(h,t)
   const float nu_o = 1.f / (T - 1 + pr.terminal_q_weight);
-  for (int m = tid; m < sh.mg; m += blockDim.x) {
-    const int h = m / T, t = m % T;
-    const float nu = (t == T - 1) ? pr.terminal_q_weight * nu_o : nu_o;
-    const float z = rowsum[m];
-    const float a = (z > 0.f) ? pr.beta_msg * om[h] * nu / z : 0.f;
-    ws.alpha[p * ws.s_m + m] = a;
-    ws.peak[p * ws.s_m + m] *= a;
+  for (int m0 = 0; m0 < sh.mg; m0 += 256 * 8) {
+    float zv[8], pv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int m = min(m0 + k * 256 + tid, sh.mg - 1);
+      zv[k] = rowsum[m];
+      pv[k] = ws.peak[p * ws.s_m + m];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int m = m0 + k * 256 + tid;
+      if (m < sh.mg) {
+        const int h = m / T, t = m % T;
+        const float nu = (t == T - 1) ? pr.terminal_q_weight * nu_o : nu_o;
+        const float a = (zv[k] > 0.f) ? pr.beta_msg * om[h] * nu / zv[k] : 0.f;
+        ws.alpha[p * ws.s_m + m] = a;
+        ws.peak[p * ws.s_m + m] = pv[k] * a;
+      }
+    }
   }
 }
 
@@ -577,7 +634,6 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
                                hipStream_t st) {
   const T* hidden = static_cast<const T*>(hidden_v);
   timer_mark(kStProbe, true, st);
-  hipLaunchKernelGGL(rownorm_kernel<T>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, ws, hidden);
   RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
   RowOperand<T> Bp{static_cast<const T*>(probe_v), sh.d, 0, nullptr, 0, sh.hr};
   ProbeEpi pe{ws, sh.d, pr.rms_eps, sh.hr};
@@ -613,6 +669,18 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, trace_omega);
   hipLaunchKernelGGL(energy_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
   timer_mark(kStHeads, false, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, hipStream_t st) {
+  timer_mark(kStInit, true, st);
+  if (sh.dtype == 0)
+    hipLaunchKernelGGL(rownorm_kernel<float>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, ws,
+                       static_cast<const float*>(hidden));
+  else
+    hipLaunchKernelGGL(rownorm_kernel<bf16_t>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, ws,
+                       static_cast<const bf16_t*>(hidden));
+  timer_mark(kStInit, false, st);
   return hipGetLastError();
 }
 
