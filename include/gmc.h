@@ -186,13 +186,15 @@ int gmc_trace_dims(int64_t N, int64_t T, int64_t K, int64_t* rounds, int64_t* po
 
 /*
  * Stage timing for measurement.  While enabled, every subsequent call records
- * hipEvents on the context stream around each stage's launches:
+ * hipEvents on the context stream around each stage's launches, and all
+ * stages run on that one stream (normally the bank kernels overlap the
+ * message kernels on an internal stream), so each span times one stage:
  *   [0] row norms + value probe + mass coordinate   [1] message logits/softmax
  *   [2] head-pattern Gram + head weights + energy  [3] appearance bank GEMM
  *   [4] spatial bank + bank weights                [5] coverage refresh
  *   [6] singleton gains + candidate pool           [7] responsibility + batch
  *   [8] final coverage + objective values          [9] assignment
- *   [10] transport + compaction                    [11] per-call state reset
+ *   [10] transport + compaction                    [11] per-call reset + row norms
  *   [12] persistent selection (all rounds in one launch; stages 5-7 and the
  *        final coverage are then empty)
  * gmc_timing_read synchronises the stream, returns per-stage total

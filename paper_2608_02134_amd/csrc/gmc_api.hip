@@ -517,20 +517,30 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   err = launch_call_init(s, c.ws, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "call init: %s", hipGetErrorString(err));
   // row norms, then the bank kernels on the side stream while the message
-  // kernels run on the caller's stream (they write disjoint client rows)
+  // kernels run on the caller's stream (they write disjoint client rows).
+  // With stage timing on, everything stays on one stream so each stage's
+  // span measures that stage alone.
   err = launch_rownorm(s, c.ws, hidden, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "row norms: %s", hipGetErrorString(err));
-  err = hipEventRecord(c.fork, st);
-  if (err == hipSuccess) err = hipStreamWaitEvent(c.side, c.fork, 0);
-  if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
-  err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, c.side);
+  const bool fork = !g_timer.on;
+  hipStream_t bank_st = fork ? c.side : st;
+  if (fork) {
+    err = hipEventRecord(c.fork, st);
+    if (err == hipSuccess) err = hipStreamWaitEvent(c.side, c.fork, 0);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
+  }
+  err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, bank_st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
-  err = hipEventRecord(c.join, c.side);
-  if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
+  if (fork) {
+    err = hipEventRecord(c.join, c.side);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
+  }
   err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
-  err = hipStreamWaitEvent(st, c.join, 0);
-  if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
+  if (fork) {
+    err = hipStreamWaitEvent(st, c.join, 0);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
+  }
   err = launch_selection(s, c.pr, c.ws, tr.round_pool, tr.round_batch, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "selection kernels: %s", hipGetErrorString(err));
   err = launch_assignment(s, c.pr, c.ws, hidden, tr.assign, st);

@@ -330,10 +330,18 @@ __device__ void commit_batch(const Shape& sh, const Ws& ws, int p, int round, in
 __device__ void wave_topb(const uint32_t* keys, int psize, int bsize, int* chosen) {
   const int lane = threadIdx.x & 63;
   const uint32_t k = (lane < psize) ? keys[lane] : 0u;
+  // all 64 keys in registers (16-byte LDS broadcasts), positions past psize
+  // key 0 and never outrank a member
+  uint32_t kk[64];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    const uint4 q = reinterpret_cast<const uint4*>(keys)[t];
+    kk[4 * t] = q.x; kk[4 * t + 1] = q.y; kk[4 * t + 2] = q.z; kk[4 * t + 3] = q.w;
+  }
   int rank = 0;
-#pragma unroll 16
-  for (int t = 0; t < psize; ++t) {
-    const uint32_t kt = keys[t];     // same address in every lane: an LDS broadcast
+#pragma unroll
+  for (int t = 0; t < 64; ++t) {
+    const uint32_t kt = t < psize ? kk[t] : 0u;
     rank += (kt > k) || (kt == k && t < lane);
   }
   const bool take = lane < psize && rank < bsize;
@@ -404,7 +412,7 @@ gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int pr
   extern __shared__ float dyn[];      // refreshed coverage [ldM], then LDS keys [N]
   __shared__ int hist[512], scan[16], bc[2], flag;
   __shared__ int pool_s[64], chosen[64], bidx[64];
-  __shared__ uint32_t bkeys[64];
+  __shared__ __attribute__((aligned(16))) uint32_t bkeys[64];
   const int p = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   float* bnew = dyn;
@@ -523,7 +531,7 @@ gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int pr
 __global__ void __launch_bounds__(64) final_batch_kernel(Shape sh, Ws ws, int round, int psize, int bsize,
                                                          int sel_base, int32_t* trace_batch) {
   __shared__ int pool_s[64], chosen[64], bidx[64];
-  __shared__ uint32_t keys[64];
+  __shared__ __attribute__((aligned(16))) uint32_t keys[64];
   const int p = blockIdx.x;
   small_batch(sh, ws, p, psize, bsize, (sh.m + 255) / 256, pool_s, keys, chosen, bidx);
   __syncthreads();
@@ -676,11 +684,12 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 //            round number
 //   pool   - every block waits for the tagged gains and picks the same pool
 //            (identical inputs, deterministic top-k)
-//   resp   - one wave per 64-row chunk: responsibility softmax over the pool,
-//            per-chunk sums per pool token -> global
+//   resp   - one block per 64-row chunk, its waves splitting the pool:
+//            responsibility softmax over the pool, per-chunk sums per pool
+//            token -> global
 //   | grid barrier
 //   batch  - every block sums the chunk partials in chunk order and picks the
-//            same batch; block 0 records it
+//            same batch; the last block records it
 //   cov    - one wave per chunk: b_m <- max(b_m, max_{j in batch} Cbar_mj),
 //            published tagged; every block waits for the tags and copies b
 //            into LDS
@@ -770,7 +779,8 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
   unsigned char* taken = reinterpret_cast<unsigned char*>(keys + sh.N);  // selected flags [N]
   __shared__ int hist[768], scan[16], bc[2], failed;
   __shared__ int pool_s[64], chosen[64], bidx[64];
-  __shared__ uint32_t bkeys[64];
+  __shared__ __attribute__((aligned(16))) uint32_t bkeys[64];
+  __shared__ float rmu[4][64], rden_s[4][64];
   const int p = blockIdx.y, blk = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nwaves = nblk * 4, gw = blk * 4 + wave;
@@ -867,47 +877,59 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       if (tid < 64) pool_s[tid] = pv;
       __syncthreads();
     }
-    if (blk == 0 && trace_pool) {
+    if (blk == nblk - 1 && trace_pool) {
       int32_t* tp = trace_pool + (static_cast<long long>(p) * sh.rounds + r) * sh.pool_cap;
       for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool_s[j] : -1;
     }
 
-    // ---- responsibilities: one wave per 64-row chunk, lane = client row
-    for (int c = gw; c < nchunk; c += nwaves) {
+    // ---- responsibilities: one block per 64-row chunk (lane = client row),
+    //      its four waves split the pool positions 16 apiece
+    for (int c = blk; c < nchunk; c += nblk) {
       const int m = c * 64 + lane;
       const bool row_ok = m < sh.m;
       const int mc = row_ok ? m : 0;
       const float a = row_ok ? alpha[mc] : 0.f;
       const float b = bl[mc];
-      float v[64];
+      const int j0 = wave * 16;
+      float v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v[j] = E[static_cast<long long>(pool_s[j0 + j]) * sh.ldM + mc];
       float mu = 0.f;
 #pragma unroll
-      for (int j = 0; j < 64; ++j) v[j] = E[static_cast<long long>(pool_s[j]) * sh.ldM + mc];
-#pragma unroll
-      for (int j = 0; j < 64; ++j) {
-        const float rr = (j < psize) ? fmaxf(a * v[j] - b, 0.f) : 0.f;
+      for (int j = 0; j < 16; ++j) {
+        const float rr = (j0 + j < psize) ? fmaxf(a * v[j] - b, 0.f) : 0.f;
         v[j] = rr;
         mu = fmaxf(mu, rr);
       }
-      if (mu > 0.f) {
-        const float inv = 1.f / (pr.tau_r * mu + pr.resp_eps);
-        const float zmax = mu * inv;
-        float den = 0.f;
-        float ex[64];
+      rmu[wave][lane] = mu;
+      __syncthreads();
+      mu = fmaxf(fmaxf(rmu[0][lane], rmu[1][lane]), fmaxf(rmu[2][lane], rmu[3][lane]));
+      const float inv = mu > 0.f ? 1.f / (pr.tau_r * mu + pr.resp_eps) : 0.f;
+      const float zmax = mu * inv;
+      float den = 0.f;
 #pragma unroll
-        for (int j = 0; j < 64; ++j) {
-          ex[j] = (j < psize) ? __expf(v[j] * inv - zmax) : 0.f;
-          den += ex[j];
-        }
-        const float rden = 1.f / den;
-#pragma unroll
-        for (int j = 0; j < 64; ++j) v[j] = ex[j] * rden * v[j];
-      } else {
-#pragma unroll
-        for (int j = 0; j < 64; ++j) v[j] = 0.f;
+      for (int j = 0; j < 16; ++j) {
+        const float ex = (j0 + j < psize) ? __expf(v[j] * inv - zmax) : 0.f;
+        den += ex;
+        v[j] *= ex;    // rho numerator times R; scaled by 1/den below
       }
-      const float s = transpose_reduce64(v, lane);
-      st_dev(&spr[static_cast<long long>(c) * 64 + lane], s);
+      rden_s[wave][lane] = den;
+      __syncthreads();
+      den = ((rden_s[0][lane] + rden_s[1][lane]) + rden_s[2][lane]) + rden_s[3][lane];
+      const float rden = mu > 0.f ? 1.f / den : 0.f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v[j] *= rden;
+      // sum over the 64 rows per pool position: butterfly inside 16-lane
+      // groups, then across the four groups
+      transpose_reduce_step<8>(v, lane);
+      transpose_reduce_step<4>(v, lane);
+      transpose_reduce_step<2>(v, lane);
+      transpose_reduce_step<1>(v, lane);
+      float tot = v[0];
+      tot += __shfl_xor(tot, 16, kWave);
+      tot += __shfl_xor(tot, 32, kWave);
+      if (lane < 16) st_dev(&spr[static_cast<long long>(c) * 64 + j0 + lane], tot);
+      __syncthreads();   // rmu / rden_s are reused by the next chunk
     }
     // the one grid barrier of the round: it also bounds how far any block
     // can run ahead, which makes the double-buffered tagged values safe
@@ -915,14 +937,14 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
 
     // ---- the batch, identical in every block
     if (wave == 0) {
-      // chunk partials summed in chunk order; 32 loads in flight at a time
+      // chunk partials summed in chunk order; up to 64 loads in flight
       float s = 0.f;
-      for (int c0 = 0; c0 < nchunk; c0 += 32) {
-        float t[32];
+      for (int c0 = 0; c0 < nchunk; c0 += 64) {
+        float t[64];
 #pragma unroll
-        for (int q = 0; q < 32; ++q) t[q] = ld_dev(&spr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
+        for (int q = 0; q < 64; ++q) t[q] = ld_dev(&spr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
 #pragma unroll
-        for (int q = 0; q < 32; ++q)
+        for (int q = 0; q < 64; ++q)
           if (c0 + q < nchunk) s += t[q];
       }
       bkeys[lane] = score_key(s);
@@ -932,7 +954,9 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       if (lane < bsize) bidx[lane] = pool_s[chosen[lane]];
     }
     __syncthreads();
-    if (blk == 0) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, trace_batch);
+    // the last block records the batch: it owns no row chunk, so the
+    // global stores stay off the coverage refresh's path
+    if (blk == nblk - 1) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, trace_batch);
     if (tid < bsize) taken[bidx[tid]] = 1;
     const bool last = r + 1 == sh.rounds;
 
