@@ -677,8 +677,8 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 }
 
 // ---------------------------------------------------------------------------
-// Persistent selection: every round of a small-pool call in one cooperative
-// launch.  The grid is nblk blocks per problem (all co-resident).  A round:
+// Persistent selection: every round of a small-pool call in one launch.  The
+// grid is nblk blocks per problem, sized to be co-resident.  A round:
 //   gains  - waves stream the client rows of unselected tokens (round robin
 //            over all waves of the problem) and publish u_i tagged with the
 //            round number
@@ -1074,18 +1074,23 @@ static void launch_cov(const Shape& sh, const Ws& ws, int nb, hipStream_t st) {
 }
 
 // Blocks per problem for the persistent selection, or 0 when the call does
-// not qualify (large pools, keys beyond LDS, too little co-residency).
+// not qualify (large pools, keys beyond LDS).  The grid never exceeds what
+// the device holds at once (one block per CU, checked against the kernel's
+// occupancy), so on a device not shared with other work every block is
+// resident from the start.  The launch is an ordinary one: a cooperative
+// launch costs a cross-queue synchronisation on each side of the kernel, and
+// the bounded barrier waits already turn a block that never becomes resident
+// (a device saturated by foreign work) into a reported timeout rather than a
+// hang.
 static int persistent_blocks(const Shape& sh, size_t lds) {
-  if (sh.pool_cap > 64 || sh.N > kLdsKeys || lds > 64 * 1024) return 0;
-  static int coop = -1, n_cu = 0;
-  if (coop < 0) {
+  static int n_cu = -1;
+  if (n_cu < 0) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess ||
         hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      coop = 0;
+      n_cu = 0;
   }
-  if (!coop) return 0;
+  if (n_cu <= 0 || sh.pool_cap > 64 || sh.N > kLdsKeys || lds > 64 * 1024) return 0;
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(select_persistent_kernel),
                                                    256, lds) != hipSuccess || per_cu < 1)
@@ -1104,14 +1109,11 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
                        ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15));
     int nblk = persistent_blocks(sh, lds);
     if (nblk > 0) {
-      Shape a_sh = sh;
-      Params a_pr = pr;
-      Ws a_ws = ws;
-      void* args[] = {&a_sh, &a_pr, &a_ws, &nblk, &trace_pool, &trace_batch};
       timer_mark(kStSelect, true, st);
-      hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(select_persistent_kernel),
-                                                dim3(nblk, sh.B), dim3(256), args, static_cast<unsigned>(lds), st);
+      hipLaunchKernelGGL(select_persistent_kernel, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws, nblk,
+                         trace_pool, trace_batch);
       timer_mark(kStSelect, false, st);
+      const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       timer_mark(kStObjective, true, st);
       hipLaunchKernelGGL(objective_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
