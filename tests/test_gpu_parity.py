@@ -1,7 +1,7 @@
 """GPU parity: the HIP operator (through the C-ABI) against the fp64 oracle in
-follow mode, on seeded synthetic inputs of the five workloads (full size
-where the oracle finishes in seconds, shrunk but ragged otherwise) and on
-the method's edge cases."""
+follow mode, on seeded synthetic inputs of the five workloads (each at full
+size, plus shrunk and ragged variants that span several tiles with partial
+tails) and on the method's edge cases."""
 import sys
 
 import numpy as np
@@ -45,6 +45,12 @@ CASES = {
     "doc_shrunk": dict(name="doc", grid=(1, 40, 40), t=32, k=320),
     "batch_shrunk": dict(name="batch16", batch=3, grid=(1, 24, 24), t=16, k=96),
     "frames_bounded": dict(name="frames", grid=(2, 48, 48), t=16, k=600),
+    # the benchmarked shapes at full size, in the launch configuration the
+    # benchmark times (document: 16 pool keys per thread; 16 images: 16 blocks
+    # per problem)
+    "doc_full": dict(name="doc"),
+    "batch16_full": dict(name="batch16"),
+    "frames_full": dict(name="frames"),
 }
 
 
