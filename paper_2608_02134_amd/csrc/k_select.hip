@@ -324,30 +324,40 @@ __device__ void commit_batch(const Shape& sh, const Ws& ws, int p, int round, in
   }
 }
 
+// Ballot-based selection inside one wave.  Keys are held in lanes (KPT per
+// lane); the count of keys >= c is a sum of ballot popcounts, so the
+// count-th largest key value is found by a 32-step bitwise search with no
+// LDS traffic: the largest v with at least `count` keys >= v.
+template <int KPT>
+__device__ __forceinline__ int wave_count_ge(const uint32_t (&k)[KPT], uint32_t c) {
+  int n = 0;
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) n += __popcll(__ballot(k[q] >= c));
+  return n;
+}
+template <int KPT>
+__device__ __forceinline__ uint32_t wave_kth(const uint32_t (&k)[KPT], int count) {
+  uint32_t prefix = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    if (wave_count_ge<KPT>(k, cand) >= count) prefix = cand;
+  }
+  return prefix;
+}
+
 // Wave-level top-b of at most 64 keys (lane = pool position, ascending
 // source index): rank by (key desc, position asc); chosen positions in
 // ascending order.  Called by one whole wave.
 __device__ void wave_topb(const uint32_t* keys, int psize, int bsize, int* chosen) {
   const int lane = threadIdx.x & 63;
-  const uint32_t k = (lane < psize) ? keys[lane] : 0u;
-  // all 64 keys in registers (16-byte LDS broadcasts), positions past psize
-  // key 0 and never outrank a member
-  uint32_t kk[64];
-#pragma unroll
-  for (int t = 0; t < 16; ++t) {
-    const uint4 q = reinterpret_cast<const uint4*>(keys)[t];
-    kk[4 * t] = q.x; kk[4 * t + 1] = q.y; kk[4 * t + 2] = q.z; kk[4 * t + 3] = q.w;
-  }
-  int rank = 0;
-#pragma unroll
-  for (int t = 0; t < 64; ++t) {
-    const uint32_t kt = t < psize ? kk[t] : 0u;
-    rank += (kt > k) || (kt == k && t < lane);
-  }
-  const bool take = lane < psize && rank < bsize;
-  const unsigned long long bal = __ballot(take);
-  const int pos = __popcll(bal & ((1ull << lane) - 1ull));
-  if (take) chosen[pos] = lane;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  const uint32_t k[1] = {(lane < psize) ? keys[lane] : 0u};
+  const uint32_t kth = wave_kth<1>(k, bsize);
+  const int quota = bsize - __popcll(__ballot(k[0] > kth));
+  const unsigned long long eqm = __ballot(lane < psize && k[0] == kth);
+  const bool take = lane < psize && (k[0] > kth || (k[0] == kth && __popcll(eqm & below) < quota));
+  const unsigned long long tm = __ballot(take);
+  if (take) chosen[__popcll(tm & below)] = lane;
 }
 
 // Butterfly transpose-reduction: lane l holds v[0..63] (one value per pool
