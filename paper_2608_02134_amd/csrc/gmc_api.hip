@@ -143,7 +143,7 @@ int validate_config(const gmc_config* c) {
 // Workspace plan: per-problem strides from the capacities.
 struct Plan {
   Capacity cap;
-  long long s_n, s_z, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
+  long long s_n, s_z, s_zp, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
       s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
       s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_tc;
 };
@@ -169,6 +169,7 @@ Plan make_plan(const gmc_config& c) {
   const long long npairs = static_cast<long long>(k.hq) * (k.hq + 1) / 2;
   pl.s_n = k.N;
   pl.s_z = static_cast<long long>(k.N) * k.hr;
+  pl.s_zp = kProbeSplit * pl.s_z;
   pl.s_sig = kMaxHeads;
   pl.s_ell = static_cast<long long>(k.hq) * k.N;
   pl.s_E = static_cast<long long>(k.N) * k.ldM;
@@ -219,7 +220,7 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
 #define F(name) ws->name = reinterpret_cast<float*>(take(pl.s_##name, 4)); ws->s_##name = pl.s_##name
 #define I(name) ws->name = reinterpret_cast<int*>(take(pl.s_##name, 4)); ws->s_##name = pl.s_##name
   ws->n2 = reinterpret_cast<float*>(take(pl.s_n, 4)); ws->s_n = pl.s_n;
-  F(z); F(sig); F(ell); F(E);
+  F(z); F(zp); F(sig); F(ell); F(E);
   ws->alpha = reinterpret_cast<float*>(take(pl.s_m, 4)); ws->s_m = pl.s_m;
   ws->peak = reinterpret_cast<float*>(take(pl.s_m, 4));
   ws->rowsum = reinterpret_cast<float*>(take(pl.s_m, 4));
@@ -541,9 +542,10 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
     err = hipStreamWaitEvent(st, c.join, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }
-  err = launch_selection(s, c.pr, c.ws, tr.round_pool, tr.round_batch, st);
+  bool support_ready = false;
+  err = launch_selection(s, c.pr, c.ws, tr.round_pool, tr.round_batch, st, &support_ready);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "selection kernels: %s", hipGetErrorString(err));
-  err = launch_assignment(s, c.pr, c.ws, hidden, tr.assign, st);
+  err = launch_assignment(s, c.pr, c.ws, hidden, support_ready, tr.assign, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "assignment kernels: %s", hipGetErrorString(err));
   err = launch_transport(s, c.pr, c.ws, hidden, pos3d, out_hidden, out_pos, out_idx, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "transport kernels: %s", hipGetErrorString(err));

@@ -34,7 +34,7 @@ struct RowOperand {
 constexpr int kGemmThreads = 256;
 constexpr int kBK = 64;
 
-// Epilogue contract:
+// Epilogue contract (p is the problem index, or problem * ksplit + split):
 //   static constexpr bool kRowStats;
 //   __device__ float row_scale(int p, int r) const;   // r valid
 //   __device__ float col_scale(int p, int c) const;   // c valid
@@ -42,7 +42,7 @@ constexpr int kBK = 64;
 //   __device__ void row_stats(int p, int r, int cblk, float sum, float mx) const;
 template <typename T, int BM, int BN, class Epi>
 __global__ void __launch_bounds__(kGemmThreads)
-gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
+gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, int ksplit, Epi epi) {
   constexpr int EPC = 16 / sizeof(T);                 // elements per 16-byte chunk
   constexpr int P = kBK + EPC;                        // LDS row pitch (elements), 16 B pad
   constexpr int CPR = kBK / EPC;                      // chunks per tile row
@@ -57,7 +57,10 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
   __shared__ float red_sum[2][BM];
   __shared__ float red_max[2][BM];
 
-  const int p = blockIdx.z;
+  // blockIdx.z = problem * ksplit + split: split s covers K columns
+  // [s*K, (s+1)*K) (K is the per-split length); the epilogue sees the
+  // combined index, so a split-K epilogue can keep its partial sums apart
+  const int pe = blockIdx.z, p = pe / ksplit, ks0 = (pe % ksplit) * K;
   const int row0 = blockIdx.y * BM, col0 = blockIdx.x * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;
@@ -67,12 +70,12 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
 #pragma unroll
   for (int i = 0; i < A_CHUNKS; ++i) {
     const int ch = tid + i * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
-    a_src[i] = A.row(p, min(row0 + r, A.rows - 1)) + kc;
+    a_src[i] = A.row(p, min(row0 + r, A.rows - 1)) + ks0 + kc;
   }
 #pragma unroll
   for (int i = 0; i < B_CHUNKS; ++i) {
     const int ch = tid + i * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
-    b_src[i] = B.row(p, min(col0 + r, B.rows - 1)) + kc;
+    b_src[i] = B.row(p, min(col0 + r, B.rows - 1)) + ks0 + kc;
   }
   uint4 ra0[A_CHUNKS], rb0[B_CHUNKS], ra1[A_CHUNKS], rb1[B_CHUNKS];
   const int nk = K / kBK;
@@ -144,9 +147,9 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      rsc[i][e] = epi.row_scale(p, min(row0 + wr * WM + i * 16 + orow + e, A.rows - 1));
+      rsc[i][e] = epi.row_scale(pe, min(row0 + wr * WM + i * 16 + orow + e, A.rows - 1));
 #pragma unroll
-  for (int j = 0; j < TN; ++j) csc[j] = epi.col_scale(p, min(col0 + wc * WN + j * 16 + oc, B.rows - 1));
+  for (int j = 0; j < TN; ++j) csc[j] = epi.col_scale(pe, min(col0 + wc * WN + j * 16 + oc, B.rows - 1));
 
   float rs[TM][4], rm[TM][4];
 #pragma unroll
@@ -162,7 +165,7 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
         const int r = row0 + wr * WM + i * 16 + orow + e;
         const int c = col0 + wc * WN + j * 16 + oc;
         if (r < A.rows && c < B.rows) {
-          const float v = epi.value(p, r, c, acc[i][j][e] * rsc[i][e] * csc[j]);
+          const float v = epi.value(pe, r, c, acc[i][j][e] * rsc[i][e] * csc[j]);
           if constexpr (Epi::kRowStats) {
             rs[i][e] += v;
             rm[i][e] = fmaxf(rm[i][e], v);
@@ -186,19 +189,21 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, Epi epi) {
     for (int rl = tid; rl < BM; rl += kGemmThreads) {
       const int r = row0 + rl;
       if (r < A.rows)
-        epi.row_stats(p, r, blockIdx.x, red_sum[0][rl] + red_sum[1][rl],
+        epi.row_stats(pe, r, blockIdx.x, red_sum[0][rl] + red_sum[1][rl],
                       fmaxf(red_max[0][rl], red_max[1][rl]));
     }
   }
 }
 
+// K must divide into ksplit slices that are multiples of 64; with ksplit > 1
+// the epilogue's problem index is problem * ksplit + split.
 template <typename T, int BM, int BN, class Epi>
 inline hipError_t launch_gemm_nt(const RowOperand<T>& A, const RowOperand<T>& B, int K, int batch,
-                                 const Epi& epi, hipStream_t stream) {
-  if (K % kBK != 0) return hipErrorInvalidValue;
-  dim3 grid((B.rows + BN - 1) / BN, (A.rows + BM - 1) / BM, batch);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, BM, BN, Epi>), grid, dim3(kGemmThreads), 0, stream, A, B, K,
-                     epi);
+                                 const Epi& epi, hipStream_t stream, int ksplit = 1) {
+  if (ksplit < 1 || K % (kBK * ksplit) != 0) return hipErrorInvalidValue;
+  dim3 grid((B.rows + BN - 1) / BN, (A.rows + BM - 1) / BM, batch * ksplit);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, BM, BN, Epi>), grid, dim3(kGemmThreads), 0, stream, A, B, K / ksplit,
+                     ksplit, epi);
   return hipGetLastError();
 }
 

@@ -13,6 +13,7 @@ constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 16;      // tokens per head-Gram block
 constexpr int kStats = 9;
 constexpr int kCounters = 8;      // completion counters per problem
+constexpr int kProbeSplit = 4;    // K splits of the value-probe GEMM (d a multiple of 256)
 
 // Call shape, resolved on the host for one gmc_prune call.
 struct Shape {
@@ -47,8 +48,9 @@ struct Params {
 struct Ws {
   float* n2;       long long s_n;       // squared row norms            [N]
   float* z;        long long s_z;       // probe coordinates Z          [N][hr]
+  float* zp;       long long s_zp;      // split-K probe partials       [kProbeSplit][N][hr]
   float* sig;      long long s_sig;     // mass coordinate sigma_h      [hq]
-  float* ell;      long long s_ell;     // ||[Z_h[i]; sigma_h]||        [hq][N]
+  float* ell;      long long s_ell;     // ||Z_h[i]||^2; the atom norm is sqrt(ell + sigma_h^2)  [hq][N]
   float* E;        long long s_E;       // client energies, token-major [N][ldM]
   float* alpha;    long long s_m;       // row pre-weights              [ldM]
   float* peak;                          // max_i Cbar_mi                [ldM]

@@ -35,12 +35,13 @@ hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const v
 hipError_t launch_call_init(const Shape& sh, const Ws& ws, hipStream_t st);
 
 // All selection rounds, then the final coverage and objective values.
+// *support_ready reports that the support list and slots were written too.
 hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
-                            int32_t* trace_batch, hipStream_t st);
+                            int32_t* trace_batch, hipStream_t st, bool* support_ready);
 
 // Support list, selected-cosine gaps, separability gate, assignment.
 hipError_t launch_assignment(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
-                             int32_t* trace_assign, hipStream_t st);
+                             bool support_ready, int32_t* trace_assign, hipStream_t st);
 
 // Population weights, weighted centroids, RMS restoration, compaction.
 hipError_t launch_transport(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,

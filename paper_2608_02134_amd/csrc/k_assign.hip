@@ -83,10 +83,14 @@ __device__ __forceinline__ CosSource<kFromE> cos_source(const Shape& sh, const P
 }
 
 // delta_i = top1 - top2 of cos_i. over the support (0 when K = 1); one wave
-// per token; per-block sums of delta over discarded tokens.
+// per token; per-block sums of delta over discarded tokens, reduced in block
+// order by the last block, which sets s_x = 1 - exp(-(mean delta / t)^p).
+constexpr int kCntGap = 6;   // completion counter of the gap kernel
+
 template <bool kFromE>
 __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
-  __shared__ float red[4];
+  __shared__ float red[4], bred[16];
+  __shared__ int flag;
   const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = blockIdx.x * 4 + wave;
   float contrib = 0.f;
@@ -118,15 +122,15 @@ __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
   }
   if (lane == 0) red[wave] = contrib;
   __syncthreads();
-  if (threadIdx.x == 0) ws.dpart[p * ws.s_dp + blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
-}
-
-__global__ void gate_kernel(Shape sh, Params pr, Ws ws, int nblk) {
-  __shared__ float red[16];
-  const int p = blockIdx.x;
+  float* dp = ws.dpart + p * ws.s_dp;
+  if (threadIdx.x == 0) st_dev(&dp[blockIdx.x], ((red[0] + red[1]) + red[2]) + red[3]);
+  // the last block: mean gap over discarded tokens and the separability gate
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  if (!last_arrival(&cnt[kCntGap], gridDim.x, &flag)) return;
+  if (threadIdx.x == 0) st_dev(&cnt[kCntGap], 0);
   float s = 0.f;
-  for (int b = threadIdx.x; b < nblk; b += blockDim.x) s += ws.dpart[p * ws.s_dp + b];
-  s = block_sum(s, red);
+  for (unsigned b = threadIdx.x; b < gridDim.x; b += blockDim.x) s += ld_dev(&dp[b]);
+  s = block_sum(s, bred);
   if (threadIdx.x == 0) {
     const int nd = sh.N - sh.K;
     const float dbar = nd > 0 ? s / static_cast<float>(nd) : 0.f;
@@ -195,9 +199,9 @@ __global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, 
 
 template <typename T>
 static hipError_t assign_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden_v,
-                              int32_t* trace_assign, hipStream_t st) {
+                              bool support_ready, int32_t* trace_assign, hipStream_t st) {
   timer_mark(kStAssign, true, st);
-  hipLaunchKernelGGL(support_kernel, dim3(sh.B), dim3(1024), 0, st, sh, ws);
+  if (!support_ready) hipLaunchKernelGGL(support_kernel, dim3(sh.B), dim3(1024), 0, st, sh, ws);
   const int nblk = (sh.N + 3) / 4;
   if (sh.bounded) {
     const T* hidden = static_cast<const T*>(hidden_v);
@@ -210,7 +214,6 @@ static hipError_t assign_impl(const Shape& sh, const Params& pr, const Ws& ws, c
   } else {
     hipLaunchKernelGGL(gap_kernel<true>, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws);
   }
-  hipLaunchKernelGGL(gate_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, nblk);
   if (sh.bounded)
     hipLaunchKernelGGL(kappa_kernel<false>, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws, trace_assign);
   else
@@ -220,9 +223,9 @@ static hipError_t assign_impl(const Shape& sh, const Params& pr, const Ws& ws, c
 }
 
 hipError_t launch_assignment(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
-                             int32_t* trace_assign, hipStream_t st) {
-  if (sh.dtype == 0) return assign_impl<float>(sh, pr, ws, hidden, trace_assign, st);
-  return assign_impl<bf16_t>(sh, pr, ws, hidden, trace_assign, st);
+                             bool support_ready, int32_t* trace_assign, hipStream_t st) {
+  if (sh.dtype == 0) return assign_impl<float>(sh, pr, ws, hidden, support_ready, trace_assign, st);
+  return assign_impl<bf16_t>(sh, pr, ws, hidden, support_ready, trace_assign, st);
 }
 
 }  // namespace gmc

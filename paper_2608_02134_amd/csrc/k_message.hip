@@ -45,46 +45,77 @@ __global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* 
 
 // Probe GEMM epilogue: Z[i][c] = (h_i . G_c) / sqrt(mean h_i^2 + eps), the
 // folded value path applied to the next block's RMSNorm of h_i.
-struct ProbeEpi {
+// Value probe partials: split s of problem p (combined index p * S + s)
+// writes its K-slice of x_i . G[h][c] (the RMS scale is applied after the
+// splits are summed).
+struct ProbeSplitEpi {
   Ws ws;
-  int d;
-  float rms_eps;
   int hr;
+  long long slot;    // N * hr floats per (problem, split)
   static constexpr bool kRowStats = false;
-  __device__ float row_scale(int p, int r) const {
-    return rsqrtf(ws.n2[p * ws.s_n + r] / static_cast<float>(d) + rms_eps);
-  }
+  __device__ float row_scale(int, int) const { return 1.f; }
   __device__ float col_scale(int, int) const { return 1.f; }
-  __device__ float value(int p, int r, int c, float v) const {
-    ws.z[p * ws.s_z + static_cast<long long>(r) * hr + c] = v;
+  __device__ float value(int pe, int r, int c, float v) const {
+    ws.zp[static_cast<long long>(pe) * slot + static_cast<long long>(r) * hr + c] = v;
     return v;
   }
   __device__ void row_stats(int, int, int, float, float) const {}
 };
 
-// sigma_h = sqrt(lambda) max(||Z_h||_F / sqrt(N r), eps) and
-// l_h[i] = ||[Z_h[i]; sigma_h]||.  One block per (head, problem).
-__global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws ws) {
-  __shared__ float red[16];
-  const int h = blockIdx.x, p = blockIdx.y;
-  const float* z = ws.z + p * ws.s_z;
-  float acc = 0.f;
-  for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
-    const float* zi = z + static_cast<long long>(i) * sh.hr + h * sh.r;
-    float s = 0.f;
-    for (int c = 0; c < sh.r; ++c) s += zi[c] * zi[c];
-    acc += s;
+// Z_h[i] = rms(h_i)^-1 sum_s partial_s (the next block's RMSNorm, unit gain)
+// and q_h[i] = ||Z_h[i]||^2, stored in place of the atom norm: consumers form
+// l_h[i] = ||[Z_h[i]; sigma_h]|| = sqrt(q_h[i] + sigma_h^2).  One wave per
+// (head, 64 tokens), lane = token; per-(block, head) sums of q feed
+// sigma_h = sqrt(lambda) max(sqrt(sum q / (N r)), eps), formed by the last
+// block in block order.
+__global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws ws, int ksplit) {
+  __shared__ int flag;
+  const int p = blockIdx.z, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = blockIdx.y * 4 + wave;
+  const int i = blockIdx.x * 64 + lane;
+  float* part = ws.gpart + p * ws.s_gpart;          // free until the head-pattern Gram
+  if (h < sh.hq) {
+    const int ic = min(i, sh.N - 1);
+    const float* zp = ws.zp + static_cast<long long>(p) * ksplit * sh.N * sh.hr +
+                      static_cast<long long>(ic) * sh.hr + h * sh.r;
+    const long long sstride = static_cast<long long>(sh.N) * sh.hr;
+    float v[kProbeSplit][kMaxProbe];
+#pragma unroll
+    for (int s = 0; s < kProbeSplit; ++s)
+#pragma unroll
+      for (int c = 0; c < kMaxProbe; ++c)
+        v[s][c] = (s < ksplit && c < sh.r) ? zp[s * sstride + c] : 0.f;
+    const float rs = rsqrtf(ws.n2[p * ws.s_n + ic] / static_cast<float>(sh.d) + pr.rms_eps);
+    float q = 0.f;
+    float* z = ws.z + p * ws.s_z + static_cast<long long>(ic) * sh.hr + h * sh.r;
+#pragma unroll
+    for (int c = 0; c < kMaxProbe; ++c) {
+      if (c < sh.r) {
+        const float zc = (((v[0][c] + v[1][c]) + v[2][c]) + v[3][c]) * rs;
+        q += zc * zc;
+        if (i < sh.N) z[c] = zc;
+      }
+    }
+    if (i < sh.N) ws.ell[p * ws.s_ell + static_cast<long long>(h) * sh.N + i] = q;
+    const float bq = wave_sum(i < sh.N ? q : 0.f);
+    if (lane == 0) st_dev(&part[blockIdx.x * sh.hq + h], bq);
   }
-  const float fro2 = block_sum(acc, red);
-  const float mean2 = fro2 / (static_cast<float>(sh.N) * sh.r);
-  const float sig = sqrtf(pr.lambda_mass) * fmaxf(sqrtf(mean2), pr.eps_mass);
-  if (threadIdx.x == 0) ws.sig[p * ws.s_sig + h] = sig;
-  float* ell = ws.ell + p * ws.s_ell + static_cast<long long>(h) * sh.N;
-  for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
-    const float* zi = z + static_cast<long long>(i) * sh.hr + h * sh.r;
-    float s = 0.f;
-    for (int c = 0; c < sh.r; ++c) s += zi[c] * zi[c];
-    ell[i] = sqrtf(s + sig * sig);
+  int* cnt = ws.cnt + p * ws.s_cnt;
+  if (!last_arrival(&cnt[1], gridDim.x * gridDim.y, &flag)) return;
+  if (threadIdx.x == 0) st_dev(&cnt[1], 0);
+  if (threadIdx.x < sh.hq) {
+    const int hh = threadIdx.x;
+    float sum = 0.f;
+    for (unsigned b0 = 0; b0 < gridDim.x; b0 += 16) {
+      float t[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) t[k] = ld_dev(&part[min(b0 + k, gridDim.x - 1) * sh.hq + hh]);
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if (b0 + k < gridDim.x) sum += t[k];
+    }
+    const float mean2 = sum / (static_cast<float>(sh.N) * sh.r);
+    ws.sig[p * ws.s_sig + hh] = sqrtf(pr.lambda_mass) * fmaxf(sqrtf(mean2), pr.eps_mass);
   }
 }
 
@@ -97,11 +128,17 @@ __global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws 
 // log-sum-exp, write e to the grounded client rows, and reduce row sums and
 // row maxima.  Nothing but e ever reaches HBM.
 // ---------------------------------------------------------------------------
+// Waves per logits block, each on its own key tiles (fewer where the fp32
+// fragments of a wide head would not fit the registers of eight waves).
 template <typename T, int DH>
-__global__ void __launch_bounds__(256)
+constexpr int logit_waves() { return (sizeof(T) == 4 && DH >= 224) ? 4 : 8; }
+
+template <typename T, int DH>
+__global__ void __launch_bounds__((64 * logit_waves<T, DH>()))
 logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* nonvis_lse) {
   constexpr int KS = DH / 32;
-  __shared__ float sm_m[4][16], sm_s[4][16];
+  constexpr int kLogitWaves = logit_waves<T, DH>();
+  __shared__ float sm_m[kLogitWaves][16], sm_s[kLogitWaves][16];
   __shared__ float sm_D[16];
   const int p = blockIdx.z, g = blockIdx.y;
   const int rows_g = sh.hg * sh.T;
@@ -153,9 +190,9 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   // three key tiles in flight per wave: the current one and the next two
   Frag<T> kcur[KS], kn1[KS], kn2[KS];
   load_keys(min(wave, last_tile), kcur);
-  load_keys(min(wave + 4, last_tile), kn1);
-  for (int ct = wave; ct < ntile; ct += 4) {
-    load_keys(min(ct + 8, last_tile), kn2);
+  load_keys(min(wave + kLogitWaves, last_tile), kn1);
+  for (int ct = wave; ct < ntile; ct += kLogitWaves) {
+    load_keys(min(ct + 2 * kLogitWaves, last_tile), kn2);
     const floatx4 acc = tile_mma(kcur);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) { kcur[ks] = kn1[ks]; kn1[ks] = kn2[ks]; }
@@ -185,9 +222,9 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   if (threadIdx.x < 16) {
     const int r = threadIdx.x;
     float m = -INFINITY;
-    for (int w = 0; w < 4; ++w) m = fmaxf(m, sm_m[w][r]);
+    for (int w = 0; w < kLogitWaves; ++w) m = fmaxf(m, sm_m[w][r]);
     float s = 0.f;
-    for (int w = 0; w < 4; ++w) s += (sm_m[w][r] == -INFINITY) ? 0.f : sm_s[w][r] * expf(sm_m[w][r] - m);
+    for (int w = 0; w < kLogitWaves; ++w) s += (sm_m[w][r] == -INFINITY) ? 0.f : sm_s[w][r] * expf(sm_m[w][r] - m);
     float D = m + logf(s);
     const int rr = rb + r;
     if (nonvis_lse && rr < rows_g) {
@@ -224,14 +261,20 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
 #pragma unroll
     for (int e = 0; e < 4; ++e) lv[e] = ell[static_cast<long long>(hrow[e]) * sh.N + col];
   };
+  float sig2[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float sg = ws.sig[p * ws.s_sig + hrow[e]];
+    sig2[e] = sg * sg;
+  }
   float lcur[4], ln1[4], ln2[4];
   load_keys(min(wave, last_tile), kcur);
   load_ell(min(wave, last_tile), lcur);
-  load_keys(min(wave + 4, last_tile), kn1);
-  load_ell(min(wave + 4, last_tile), ln1);
-  for (int ct = wave; ct < ntile; ct += 4) {
-    load_keys(min(ct + 8, last_tile), kn2);
-    load_ell(min(ct + 8, last_tile), ln2);
+  load_keys(min(wave + kLogitWaves, last_tile), kn1);
+  load_ell(min(wave + kLogitWaves, last_tile), ln1);
+  for (int ct = wave; ct < ntile; ct += kLogitWaves) {
+    load_keys(min(ct + 2 * kLogitWaves, last_tile), kn2);
+    load_ell(min(ct + 2 * kLogitWaves, last_tile), ln2);
     const floatx4 acc = tile_mma(kcur);
     float lv[4];
 #pragma unroll
@@ -244,7 +287,7 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
       for (int e = 0; e < 4; ++e) {
         if (!rvalid[e]) continue;
         const float a = __expf(acc[e] * scale - D[e]);
-        const float v = a * lv[e];
+        const float v = a * sqrtf(lv[e] + sig2[e]);   // atom norm l_h[col]
         E[static_cast<long long>(col) * sh.ldM + mrow[e]] = v;
         rsum[e] += v;
         rmax[e] = fmaxf(rmax[e], v);
@@ -264,7 +307,7 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
     if (rr < rows_g) {
       const int h = g * sh.hg + rr / sh.T, t = rr % sh.T;
       float s = 0.f, m = 0.f;
-      for (int w = 0; w < 4; ++w) { s += sm_s[w][r]; m = fmaxf(m, sm_m[w][r]); }
+      for (int w = 0; w < kLogitWaves; ++w) { s += sm_s[w][r]; m = fmaxf(m, sm_m[w][r]); }
       const long long mi = static_cast<long long>(h) * sh.T + t;
       ws.rowsum[p * ws.s_m + mi] = s;
       ws.peak[p * ws.s_m + mi] = m;   // max_i e; scaled by the row weight later
@@ -290,51 +333,74 @@ constexpr int kGramPitch = kGramTC + 4;     // floats per staged head row
 constexpr int kGramTok = 4;                 // tokens per wave (kHeadTok per block)
 static_assert(kGramTok * 4 == kHeadTok, "one block covers kHeadTok tokens");
 
+template <int R>
 __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws ws) {
+  constexpr int U = R + 1;                     // [Z_h[i]; sigma_h] / l_h[i]
   __shared__ __attribute__((aligned(16))) float xs[4][32 * kGramPitch];
-  __shared__ float zs[4][32 * (kMaxProbe + 2)];
+  __shared__ float us[4][32 * U];
   const int p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int H = sh.hq, T = sh.T, r = sh.r, zw = r + 2;
+  const int H = sh.hq, T = sh.T;
   const int fr = lane & 15, fk = lane >> 4;
   const float nu_o = 1.f / (T - 1 + pr.terminal_q_weight);
   const float nu_last = pr.terminal_q_weight * nu_o;
   float* X = xs[wave];
-  float* Z = zs[wave];
+  float* Uv = us[wave];
   const float* E = ws.E + p * ws.s_E;
   const float* sig = ws.sig + p * ws.s_sig;
   const float* zp = ws.z + p * ws.s_z;
-  const float* ellp = ws.ell + p * ws.s_ell;
+  const float* qp = ws.ell + p * ws.s_ell;     // ||Z_h[i]||^2
   float* e2 = ws.e2 + p * ws.s_e2;
   floatx4 acc[3];
 #pragma unroll
   for (int tl = 0; tl < 3; ++tl) acc[tl] = floatx4{0.f, 0.f, 0.f, 0.f};
-  for (int x = lane; x < 32 * kGramPitch; x += 64) X[x] = 0.f;   // padding heads stay zero
-  __builtin_amdgcn_wave_barrier();
-  for (int j = 0; j < kGramTok; ++j) {
-    const int i = blockIdx.x * kHeadTok + wave * kGramTok + j;
-    if (i >= sh.N) break;                                          // wave-uniform
-    const float* row = E + static_cast<long long>(i) * sh.ldM;
-    // weight data of this token: z_h[c] (c < r), sigma_h, l_h[i]
-    {
-      float zv[(32 * (kMaxProbe + 2) + 63) / 64];
+  // lane h < 32 owns head h's normalised vector; the first chunk of the next
+  // token and its vector load while the current token is computed
+  const int hl = min(lane, H - 1);
+  const float sg = sig[hl];
+  float vx[32], uz[R], uq;
+  auto load_token = [&](int i, int t0) {
+    const float* row = E + static_cast<long long>(min(i, sh.N - 1)) * sh.ldM;
+    const int tc = min(kGramTC, T - t0);
 #pragma unroll
-      for (int q = 0; q < (32 * (kMaxProbe + 2) + 63) / 64; ++q) {
-        const int x = min(lane + 64 * q, 32 * zw - 1);
-        const int h = min(x / zw, H - 1), c = x % zw;
-        const float za = zp[static_cast<long long>(i) * sh.hr + h * r + min(c, r - 1)];
-        const float sa = sig[h];
-        const float la = ellp[static_cast<long long>(h) * sh.N + i];
-        zv[q] = c < r ? za : (c == r ? sa : la);
-      }
+    for (int k = 0; k < 8; ++k)
 #pragma unroll
-      for (int q = 0; q < (32 * (kMaxProbe + 2) + 63) / 64; ++q) {
-        const int x = lane + 64 * q;
-        if (x < 32 * zw) {
-          const bool pad = x / zw >= H;
-          Z[x] = pad ? ((x % zw) == r + 1 ? 1.f : 0.f) : zv[q];
-        }
+      for (int q = 0; q < 4; ++q) {
+        const int h = min(k * 4 + fk, H - 1), c = min(fr * 4 + q, tc - 1);
+        vx[k * 4 + q] = row[h * T + t0 + c];
       }
+  };
+  auto load_vec = [&](int i) {
+    const int ic = min(i, sh.N - 1);
+#pragma unroll
+    for (int c = 0; c < R; ++c) uz[c] = zp[static_cast<long long>(ic) * sh.hr + hl * R + c];
+    uq = qp[static_cast<long long>(hl) * sh.N + ic];
+  };
+  auto store_chunk = [&](int tc) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int h = k * 4 + fk, c = fr * 4 + q;
+        X[h * kGramPitch + c] = (h < H && c < tc) ? vx[k * 4 + q] : 0.f;
+      }
+  };
+  auto store_vec = [&]() {
+    if (lane < 32) {
+      const bool ok = lane < H;
+      const float inv_l = ok ? rsqrtf(uq + sg * sg) : 0.f;     // 1 / l_h[i]
+#pragma unroll
+      for (int c = 0; c < R; ++c) Uv[lane * U + c] = uz[c] * inv_l;
+      Uv[lane * U + R] = sg * inv_l;
     }
+  };
+  const int tok0 = blockIdx.x * kHeadTok + wave * kGramTok;
+  load_token(tok0, 0);
+  load_vec(tok0);
+  for (int j = 0; j < kGramTok; ++j) {
+    const int i = tok0 + j;
+    if (i >= sh.N) break;                                          // wave-uniform
+    __builtin_amdgcn_wave_barrier();
+    store_vec();
     floatx4 g[3];
 #pragma unroll
     for (int tl = 0; tl < 3; ++tl) g[tl] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -342,22 +408,8 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
     for (; t0 < T; t0 += kGramTC) {
       const int tc = min(kGramTC, T - t0);
       __builtin_amdgcn_wave_barrier();
-      // stage X_i[h][t0 .. t0 + tc) (clamped loads, masked stores)
-      float v[32];
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int h = min(k * 4 + fk, H - 1), c = min(fr * 4 + q, tc - 1);
-          v[k * 4 + q] = row[h * T + t0 + c];
-        }
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int h = k * 4 + fk, c = fr * 4 + q;
-          if (h < H) X[h * kGramPitch + c] = c < tc ? v[k * 4 + q] : 0.f;
-        }
+      if (t0 > 0) load_token(i, t0);                               // later chunks of a long T
+      store_chunk(tc);
       __builtin_amdgcn_wave_barrier();
       const int nk = (tc + 3) / 4;
       for (int kk = 0; kk < nk; ++kk) {
@@ -369,24 +421,26 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
       }
     }
     const int tl_last = (T - 1) - (t0 - kGramTC);   // column of t = T-1 in the last chunk
+    if (j + 1 < kGramTok) {                          // next token's loads overlap the epilogue
+      load_token(i + 1, 0);
+      load_vec(i + 1);
+    }
     __builtin_amdgcn_wave_barrier();
-    // epilogue: lane holds G[16 hb + 4 fk + e][16 gb + fr]
+    // epilogue: lane holds G[16 hb + 4 fk + e][16 gb + fr]; weight
+    // W[h][g] = u_h . u_g with u = [Z; sigma] / l
 #pragma unroll
     for (int tl = 0; tl < 3; ++tl) {
       const int hb = tl == 2 ? 1 : 0, gb = tl == 0 ? 0 : 1;
       const int gg = 16 * gb + fr;
-      float wg[kMaxProbe];
+      float ug[U];
 #pragma unroll
-      for (int c = 0; c < kMaxProbe; ++c) wg[c] = c < r ? Z[gg * zw + c] : 0.f;
-      const float sg = Z[gg * zw + r], lg = Z[gg * zw + r + 1];
+      for (int c = 0; c < U; ++c) ug[c] = Uv[gg * U + c];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int hh = 16 * hb + 4 * fk + e;
-        float dot = Z[hh * zw + r] * sg;
+        float w = 0.f;
 #pragma unroll
-        for (int c = 0; c < kMaxProbe; ++c)
-          if (c < r) dot += Z[hh * zw + c] * wg[c];
-        const float w = dot / (Z[hh * zw + r + 1] * lg);
+        for (int c = 0; c < U; ++c) w += Uv[hh * U + c] * ug[c];
         acc[tl][e] += g[tl][e] * w;
         if (tl != 1 && hh == gg && hh < H) {
           const float xl = X[hh * kGramPitch + tl_last];
@@ -636,10 +690,13 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   timer_mark(kStProbe, true, st);
   RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
   RowOperand<T> Bp{static_cast<const T*>(probe_v), sh.d, 0, nullptr, 0, sh.hr};
-  ProbeEpi pe{ws, sh.d, pr.rms_eps, sh.hr};
-  hipError_t err = launch_gemm_nt<T, 64, 64>(A, Bp, sh.d, sh.B, pe, st);
+  // split the d-long contraction so four times as many blocks stream hidden
+  const int ksplit = (sh.d % (64 * kProbeSplit) == 0) ? kProbeSplit : 1;
+  ProbeSplitEpi pe{ws, sh.hr, static_cast<long long>(sh.N) * sh.hr};
+  hipError_t err = launch_gemm_nt<T, 64, 64>(A, Bp, sh.d, sh.B, pe, st, ksplit);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(sigma_ell_kernel, dim3(sh.hq, sh.B), dim3(256), 0, st, sh, pr, ws);
+  hipLaunchKernelGGL(sigma_ell_kernel, dim3((sh.N + 63) / 64, (sh.hq + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws,
+                     ksplit);
   timer_mark(kStProbe, false, st);
   if (sh.T == 0) {
     timer_mark(kStHeads, true, st);
@@ -653,19 +710,26 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   const T* k = static_cast<const T*>(vis_k_v);
   timer_mark(kStLogits, true, st);
   switch (sh.dh) {
-    case 32: hipLaunchKernelGGL((logits_kernel<T, 32>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 64: hipLaunchKernelGGL((logits_kernel<T, 64>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 96: hipLaunchKernelGGL((logits_kernel<T, 96>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 128: hipLaunchKernelGGL((logits_kernel<T, 128>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 160: hipLaunchKernelGGL((logits_kernel<T, 160>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 192: hipLaunchKernelGGL((logits_kernel<T, 192>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 224: hipLaunchKernelGGL((logits_kernel<T, 224>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 256: hipLaunchKernelGGL((logits_kernel<T, 256>), lg, dim3(256), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 32: hipLaunchKernelGGL((logits_kernel<T, 32>), lg, dim3(64 * logit_waves<T, 32>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 64: hipLaunchKernelGGL((logits_kernel<T, 64>), lg, dim3(64 * logit_waves<T, 64>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 96: hipLaunchKernelGGL((logits_kernel<T, 96>), lg, dim3(64 * logit_waves<T, 96>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 128: hipLaunchKernelGGL((logits_kernel<T, 128>), lg, dim3(64 * logit_waves<T, 128>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 160: hipLaunchKernelGGL((logits_kernel<T, 160>), lg, dim3(64 * logit_waves<T, 160>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 192: hipLaunchKernelGGL((logits_kernel<T, 192>), lg, dim3(64 * logit_waves<T, 192>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 224: hipLaunchKernelGGL((logits_kernel<T, 224>), lg, dim3(64 * logit_waves<T, 224>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+    case 256: hipLaunchKernelGGL((logits_kernel<T, 256>), lg, dim3(64 * logit_waves<T, 256>()), 0, st, sh, ws, q, k, nonvis_lse); break;
     default: return hipErrorInvalidValue;
   }
   timer_mark(kStLogits, false, st);
   timer_mark(kStHeads, true, st);
-  hipLaunchKernelGGL(headgram_kernel, dim3(sh.n_head_blk, sh.B), dim3(256), 0, st, sh, pr, ws);
+  switch (sh.r) {
+#define GMC_HEADGRAM(R) \
+    case R: hipLaunchKernelGGL(headgram_kernel<R>, dim3(sh.n_head_blk, sh.B), dim3(256), 0, st, sh, pr, ws); break;
+    GMC_HEADGRAM(1) GMC_HEADGRAM(2) GMC_HEADGRAM(3) GMC_HEADGRAM(4)
+    GMC_HEADGRAM(5) GMC_HEADGRAM(6) GMC_HEADGRAM(7) GMC_HEADGRAM(8)
+#undef GMC_HEADGRAM
+    default: return hipErrorInvalidValue;
+  }
   hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, trace_omega);
   hipLaunchKernelGGL(energy_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
   timer_mark(kStHeads, false, st);

@@ -703,6 +703,9 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 //   cov    - one wave per chunk: b_m <- max(b_m, max_{j in batch} Cbar_mj),
 //            published tagged; every block waits for the tags and copies b
 //            into LDS
+// After the last round the last block writes the support list (ascending,
+// with each token's slot) and, after a final barrier, F(S) and F(V) from the
+// chunks' shares.
 // Tagged values and the chunk partials are double-buffered by round parity.
 // A buffer is rewritten two rounds later, and the grid barrier between keeps
 // every block within one round of the others, so no reader can see a value
@@ -739,6 +742,13 @@ __device__ __forceinline__ void grid_barrier(int* cnt, int nblk, int k, int* fai
     }
   }
   __syncthreads();
+}
+
+// Arrival at grid barrier k without waiting (for blocks with no later work).
+__device__ __forceinline__ void grid_arrive(int* cnt) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(&cnt[kCntBarrier], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Marks the call failed (device status word) after a bounded wait.
@@ -801,6 +811,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
   unsigned long long* tu = ws.tu + p * ws.s_tu;
   unsigned long long* tc = ws.tc + p * ws.s_tc;
   float* sp = ws.spart + p * ws.s_spart;
+  float* obj = ws.rstat + p * ws.s_rstat;   // per-chunk objective shares [2 * nchunk]
   int* cnt = ws.cnt + p * ws.s_cnt;
   for (int m = tid; m < sh.ldM; m += 256) bl[m] = 0.f;     // coverage is zero at call start
   for (int i = tid; i < sh.N; i += 256) taken[i] = 0;
@@ -991,9 +1002,57 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
         else
           st_dev64(&tcr[m], tag_value(tag, cm));
       }
+      if (last) {
+        // this chunk's share of F(S) = sum_m b_m and F(V) = sum_m max_i Cbar_mi
+        const float fs = wave_sum(m < sh.m ? cm : 0.f);
+        const float fv = wave_sum(m < sh.m ? ws.peak[p * ws.s_m + mc] : 0.f);
+        if (lane == 0) {
+          st_dev(&obj[2 * c], fs);
+          st_dev(&obj[2 * c + 1], fv);
+        }
+      }
     }
     selected += bsize;
-    if (last) break;
+    if (last) {
+      if (blk != nblk - 1) {
+        grid_arrive(cnt);
+        break;
+      }
+      // the last block: support list in ascending source order with each
+      // token's slot, then (after every chunk's share has arrived) the
+      // objective values in chunk order
+      int* sup = ws.sup + p * ws.s_sup;
+      int* slot = ws.slot + p * ws.s_slot;
+      __syncthreads();   // the last batch's flags are visible to every thread
+      int base = 0;
+      for (int b0 = 0; b0 < sh.N; b0 += 256) {
+        const int i = b0 + tid;
+        const int f = (i < sh.N && taken[i]) ? 1 : 0;
+        int tot;
+        const int pos = base + block_exclusive_scan(f, scan, &tot);
+        if (i < sh.N) {
+          slot[i] = f ? pos : -1;
+          if (f) sup[pos] = i;
+        }
+        base += tot;
+      }
+      grid_barrier(cnt, nblk, sh.rounds + 1, &failed);
+      if (tid == 0) {
+        float a = 0.f, b2 = 0.f;
+        for (int c = 0; c < nchunk; ++c) {
+          a += ld_dev(&obj[2 * c]);
+          b2 += ld_dev(&obj[2 * c + 1]);
+        }
+        float* st = ws.stats + p * ws.s_st;
+        st[2] = a;
+        st[3] = b2;
+        st[4] = static_cast<float>(sh.K);
+        st[5] = static_cast<float>(sh.rounds);
+        st[6] = static_cast<float>(sh.m);
+        st[7] = static_cast<float>(sh.N - sh.K);
+      }
+      break;
+    }
     // ---- every block copies the refreshed coverage into LDS (waits for the tags)
     for (int m0 = 0; m0 < sh.m; m0 += 256 * 8) {
       unsigned long long w[8];
@@ -1113,7 +1172,8 @@ static int persistent_blocks(const Shape& sh, size_t lds) {
 }
 
 hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
-                            int32_t* trace_batch, hipStream_t st) {
+                            int32_t* trace_batch, hipStream_t st, bool* support_ready) {
+  *support_ready = false;
   {
     const size_t lds = (static_cast<size_t>(sh.ldM) + static_cast<size_t>(sh.N)) * sizeof(float) +
                        ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15));
@@ -1123,11 +1183,7 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
       hipLaunchKernelGGL(select_persistent_kernel, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws, nblk,
                          trace_pool, trace_batch);
       timer_mark(kStSelect, false, st);
-      const hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-      timer_mark(kStObjective, true, st);
-      hipLaunchKernelGGL(objective_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
-      timer_mark(kStObjective, false, st);
+      *support_ready = true;
       return hipGetLastError();
     }
   }
