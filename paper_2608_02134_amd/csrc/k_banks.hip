@@ -2,8 +2,9 @@
 // Eq. cond-coverage, Eq. cond-effective-bank-mass).
 //
 // Exact bank (N <= threshold): E_V[m][i] = exp((cos_mi - 1) / tau_v) from an
-// MFMA Gram of the raw states, normalised after the contraction
-// (cos = h_m.h_i / (|h_m| |h_i|)) so the MFMA operands are the exact inputs.
+// MFMA Gram of the raw states (upper-triangle tiles only, mirrored in the
+// epilogue), normalised after the contraction (cos = h_m.h_i / (|h_m| |h_i|))
+// so the MFMA operands are the exact inputs.
 // The row maximum of x_m.x_i is the self term 1, so no max pass is needed.
 // Bounded bank: states projected by the fixed +-1 map, normalised, and
 // M_V <= 4096 uniformly spaced clients; the same Gibbs epilogue on the fp32
@@ -43,6 +44,173 @@ struct AppearanceEpi {
     ws.apart_max[p * ws.s_apart + static_cast<long long>(cblk) * mv + r] = m;
   }
 };
+
+// Exact bank on the symmetric Gram: only tiles (I, J) with I <= J of the
+// 64 x 64 tiling are computed; each writes E_V for (client r in I, token c in
+// J) and, off the diagonal, the mirror (client c, token r), with the row
+// statistics of both orientations (client r over column block J; client c
+// over column block I), so the N x N bank costs half the contraction.
+// Same operand pipeline as the generic MFMA GEMM (two register stages, double
+// LDS buffer), 256 threads in a 2 x 2 wave grid of 32 x 32 sub-tiles.
+template <typename T>
+__global__ void __launch_bounds__(kGemmThreads)
+gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps) {
+  constexpr int BM = 64, EPC = 16 / sizeof(T), P = kBK + EPC, CPR = kBK / EPC;
+  constexpr int CH = BM * CPR / kGemmThreads;   // chunks per thread per slab (A and B each)
+  constexpr int WM = 32, TM = 2;
+  __shared__ __attribute__((aligned(16))) T As[2][BM * P];
+  __shared__ __attribute__((aligned(16))) T Bs[2][BM * P];
+  __shared__ float rs_sum[2][BM], rs_max[2][BM], cs_sum[2][BM], cs_max[2][BM];
+  const int p = blockIdx.y;
+  // upper-triangle tile (I, J), I <= J, from the linear block index
+  const int nt = (sh.N + BM - 1) / BM;
+  int I = 0, rem = blockIdx.x;
+  while (rem >= nt - I) { rem -= nt - I; ++I; }
+  const int J = I + rem;
+  const int row0 = I * BM, col0 = J * BM;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  const T* base = hidden + static_cast<long long>(p) * sh.N * sh.d;
+  const T* a_src[CH];
+  const T* b_src[CH];
+#pragma unroll
+  for (int q = 0; q < CH; ++q) {
+    const int ch = tid + q * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
+    a_src[q] = base + static_cast<long long>(min(row0 + r, sh.N - 1)) * sh.d + kc;
+    b_src[q] = base + static_cast<long long>(min(col0 + r, sh.N - 1)) * sh.d + kc;
+  }
+  uint4 ra0[CH], rb0[CH], ra1[CH], rb1[CH];
+  const int nk = sh.d / kBK;
+  auto load = [&](int kt, uint4* ra, uint4* rb) {
+    const int k0 = min(kt, nk - 1) * kBK;
+#pragma unroll
+    for (int q = 0; q < CH; ++q) { ra[q] = ld16(a_src[q] + k0); rb[q] = ld16(b_src[q] + k0); }
+  };
+  auto store = [&](int buf, const uint4* ra, const uint4* rb) {
+#pragma unroll
+    for (int q = 0; q < CH; ++q) {
+      const int ch = tid + q * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
+      st16(&As[buf][r * P + kc], ra[q]);
+      st16(&Bs[buf][r * P + kc], rb[q]);
+    }
+  };
+  floatx4 acc[TM][TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int fr = lane & 15, fk = (lane >> 4) * 8;
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int ks = 0; ks < kBK; ks += 32) {
+      Frag<T> fa[TM], fb[TM];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) fa[i] = frag_load<T>(&As[buf][(wr * WM + i * 16 + fr) * P + ks + fk]);
+#pragma unroll
+      for (int j = 0; j < TM; ++j) fb[j] = frag_load<T>(&Bs[buf][(wc * WM + j * 16 + fr) * P + ks + fk]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j) acc[i][j] = mma(fa[i], fb[j], acc[i][j]);
+    }
+  };
+  load(0, ra0, rb0);
+  load(1, ra1, rb1);
+  store(0, ra0, rb0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    load(kt + 2, ra0, rb0);
+    compute(0);
+    store(1, ra1, rb1);
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    load(kt + 3, ra1, rb1);
+    compute(1);
+    store(0, ra0, rb0);
+    __syncthreads();
+  }
+
+  // epilogue: lane holds column (lane & 15), rows 4 (lane >> 4) + e of each
+  // 16 x 16 tile; cos = acc / (|h_r| |h_c|), v = exp((cos - 1) / tau_v)
+  const int oc = lane & 15, orow = (lane >> 4) * 4;
+  const float* n2 = ws.n2 + p * ws.s_n;
+  float rsc[TM][4], csc[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      rsc[i][e] = 1.f / fmaxf(sqrtf(n2[min(row0 + wr * WM + i * 16 + orow + e, sh.N - 1)]), norm_eps);
+#pragma unroll
+  for (int j = 0; j < TM; ++j) csc[j] = 1.f / fmaxf(sqrtf(n2[min(col0 + wc * WM + j * 16 + oc, sh.N - 1)]), norm_eps);
+  float* E = ws.E + p * ws.s_E;
+  const bool diag = I == J;
+  float rsum[TM][4], rmax[TM][4], csum[TM], cmax[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { rsum[i][e] = 0.f; rmax[i][e] = 0.f; }
+#pragma unroll
+  for (int j = 0; j < TM; ++j) { csum[j] = 0.f; cmax[j] = 0.f; }
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = row0 + wr * WM + i * 16 + orow + e;
+        const int c = col0 + wc * WM + j * 16 + oc;
+        if (r < sh.N && c < sh.N) {
+          const float v = expf((acc[i][j][e] * rsc[i][e] * csc[j] - 1.f) * inv_tau);
+          E[static_cast<long long>(c) * sh.ldM + sh.mg + r] = v;           // client r, token c
+          rsum[i][e] += v;
+          rmax[i][e] = fmaxf(rmax[i][e], v);
+          if (!diag) {
+            E[static_cast<long long>(r) * sh.ldM + sh.mg + c] = v;         // client c, token r
+            csum[j] += v;
+            cmax[j] = fmaxf(cmax[j], v);
+          }
+        }
+      }
+  // client r: sum / max over the tile's columns (16 lanes of a row group,
+  // then the two column waves); client c: over the tile's rows (4 rows per
+  // lane, the 4 row groups, the two row tiles, then the two row waves)
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float sv = rsum[i][e], mv = rmax[i][e];
+      sv = group16_sum(sv);
+      mv = group16_max(mv);
+      if (oc == 0) { rs_sum[wc][wr * WM + i * 16 + orow + e] = sv; rs_max[wc][wr * WM + i * 16 + orow + e] = mv; }
+    }
+  if (!diag) {
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      float sv = csum[j], mv = cmax[j];
+      sv += __shfl_xor(sv, 16, kWave);
+      mv = fmaxf(mv, __shfl_xor(mv, 16, kWave));
+      sv += __shfl_xor(sv, 32, kWave);
+      mv = fmaxf(mv, __shfl_xor(mv, 32, kWave));
+      if (lane < 16) { cs_sum[wr][wc * WM + j * 16 + oc] = sv; cs_max[wr][wc * WM + j * 16 + oc] = mv; }
+    }
+  }
+  __syncthreads();
+  float* ps = ws.apart_sum + p * ws.s_apart;
+  float* pm = ws.apart_max + p * ws.s_apart;
+  if (tid < BM) {
+    const int r = row0 + tid;
+    if (r < sh.N) {
+      ps[static_cast<long long>(J) * sh.mv + r] = rs_sum[0][tid] + rs_sum[1][tid];
+      pm[static_cast<long long>(J) * sh.mv + r] = fmaxf(rs_max[0][tid], rs_max[1][tid]);
+    }
+  } else if (!diag && tid < 2 * BM) {
+    const int cl = tid - BM, c = col0 + cl;
+    if (c < sh.N) {
+      ps[static_cast<long long>(I) * sh.mv + c] = cs_sum[0][cl] + cs_sum[1][cl];
+      pm[static_cast<long long>(I) * sh.mv + c] = fmaxf(cs_max[0][cl], cs_max[1][cl]);
+    }
+  }
+}
 
 // Bounded bank: raw projection y = R h (fp32 out).
 struct ProjEpi {
@@ -179,10 +347,9 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
   hipError_t err;
   timer_mark(kStAppearance, true, st);
   if (!sh.bounded) {
-    RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
-    AppearanceEpi epi{ws, sh.ldM, sh.mg, 1, 1.f / pr.tau_v, pr.norm_eps, sh.n_app_cblk, sh.mv};
-    err = launch_gemm_nt<T, 64, 64>(A, A, sh.d, sh.B, epi, st);
-    if (err != hipSuccess) return err;
+    const int nt = (sh.N + 63) / 64;
+    hipLaunchKernelGGL(gram_sym_kernel<T>, dim3(nt * (nt + 1) / 2, sh.B), dim3(kGemmThreads), 0, st, sh, ws,
+                       hidden, 1.f / pr.tau_v, pr.norm_eps);
   } else {
     RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
     RowOperand<T> R{static_cast<const T*>(proj_v), sh.d, 0, nullptr, 0, sh.app_rank};

@@ -794,9 +794,11 @@ __device__ __forceinline__ void pool_regs(const Shape& sh, const unsigned long l
 __global__ void __launch_bounds__(256)
 select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_pool, int32_t* trace_batch) {
   extern __shared__ float dyn[];
-  float* bl = dyn;                                                   // b_m       [ldM]
-  uint32_t* keys = reinterpret_cast<uint32_t*>(dyn + sh.ldM);        // pool keys [N]
-  unsigned char* taken = reinterpret_cast<unsigned char*>(keys + sh.N);  // selected flags [N]
+  // LDS: b_m [ldM] | selected flags [N, padded to 16 bytes] | pool keys [N]
+  //      (only when N exceeds the register top-k)
+  float* bl = dyn;
+  unsigned char* taken = reinterpret_cast<unsigned char*>(dyn + sh.ldM);
+  uint32_t* keys = reinterpret_cast<uint32_t*>(taken + ((sh.N + 15) & ~15));
   __shared__ int hist[768], scan[16], bc[2], failed;
   __shared__ int pool_s[64], chosen[64], bidx[64];
   __shared__ __attribute__((aligned(16))) uint32_t bkeys[64];
@@ -1152,14 +1154,22 @@ static void launch_cov(const Shape& sh, const Ws& ws, int nb, hipStream_t st) {
 // (a device saturated by foreign work) into a reported timeout rather than a
 // hang.
 static int persistent_blocks(const Shape& sh, size_t lds) {
-  static int n_cu = -1;
+  static int n_cu = -1, lds_max = 0, lds_set = 64 * 1024;
   if (n_cu < 0) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
       n_cu = 0;
   }
-  if (n_cu <= 0 || sh.pool_cap > 64 || sh.N > kLdsKeys || lds > 64 * 1024) return 0;
+  if (n_cu <= 0 || sh.pool_cap > 64 || sh.N > kLdsKeys || lds > static_cast<size_t>(lds_max)) return 0;
+  if (static_cast<int>(lds) > lds_set) {
+    // dynamic LDS above 64 KB has to be granted to the kernel first
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(select_persistent_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)) != hipSuccess)
+      return 0;
+    lds_set = static_cast<int>(lds);
+  }
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(select_persistent_kernel),
                                                    256, lds) != hipSuccess || per_cu < 1)
@@ -1175,8 +1185,9 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
                             int32_t* trace_batch, hipStream_t st, bool* support_ready) {
   *support_ready = false;
   {
-    const size_t lds = (static_cast<size_t>(sh.ldM) + static_cast<size_t>(sh.N)) * sizeof(float) +
-                       ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15));
+    const size_t lds = static_cast<size_t>(sh.ldM) * sizeof(float) +
+                       ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15)) +
+                       (sh.N > 256 * 16 ? static_cast<size_t>(sh.N) * sizeof(uint32_t) : 0);
     int nblk = persistent_blocks(sh, lds);
     if (nblk > 0) {
       timer_mark(kStSelect, true, st);
