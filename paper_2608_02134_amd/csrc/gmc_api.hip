@@ -145,7 +145,7 @@ struct Plan {
   Capacity cap;
   long long s_n, s_z, s_zp, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
       s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
-      s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_tc;
+      s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_ts, s_tc;
 };
 
 Plan make_plan(const gmc_config& c) {
@@ -203,7 +203,8 @@ Plan make_plan(const gmc_config& c) {
   pl.s_rstat = 3LL * k.ldM;
   pl.s_lstat = static_cast<long long>(c.landmarks) * c.landmarks;
   pl.s_tu = 2LL * k.N;
-  pl.s_tc = 2LL * k.ldM;
+  pl.s_ts = 2 * 64 * cdiv(k.ldM, 64);
+  pl.s_tc = 2LL * (k.ldM + kMaxPersist);
   return pl;
 }
 
@@ -249,6 +250,7 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   ws->u = reinterpret_cast<float*>(take(pl.s_u, 4)); ws->s_u = pl.s_u;
   ws->cnt = reinterpret_cast<int*>(take(pl.s_cnt, 4)); ws->s_cnt = pl.s_cnt;
   ws->tu = reinterpret_cast<unsigned long long*>(take(pl.s_tu, 8)); ws->s_tu = pl.s_tu;
+  ws->ts = reinterpret_cast<unsigned long long*>(take(pl.s_ts, 8)); ws->s_ts = pl.s_ts;
   ws->tc = reinterpret_cast<unsigned long long*>(take(pl.s_tc, 8)); ws->s_tc = pl.s_tc;
   F(rstat); F(lstat);
 #undef F

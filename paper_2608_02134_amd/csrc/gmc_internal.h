@@ -13,6 +13,7 @@ constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 16;      // tokens per head-Gram block
 constexpr int kStats = 9;
 constexpr int kCounters = 8;      // completion counters per problem
+constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection
 constexpr int kProbeSplit = 4;    // K splits of the value-probe GEMM (d a multiple of 256)
 
 // Call shape, resolved on the host for one gmc_prune call.
@@ -86,7 +87,8 @@ struct Ws {
   // persistent selection: values tagged with (round + 1) in the high word,
   // double-buffered by round parity; zeroed at the start of every call
   unsigned long long* tu; long long s_tu;  // tagged gains               [2][N]
-  unsigned long long* tc; long long s_tc;  // tagged coverage            [2][ldM]
+  unsigned long long* ts; long long s_ts;  // tagged score partials     [2][ceil(M/64)][64]
+  unsigned long long* tc; long long s_tc;  // tagged coverage + heartbeats [2][ldM + kMaxPersist]
 };
 
 }  // namespace gmc

@@ -688,7 +688,8 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 
 // ---------------------------------------------------------------------------
 // Persistent selection: every round of a small-pool call in one launch.  The
-// grid is nblk blocks per problem, sized to be co-resident.  A round:
+// grid is nblk blocks per problem, sized to be co-resident; every block keeps
+// its own copy of the coverage b_m and of the row weights in LDS.  A round:
 //   gains  - waves stream the client rows of unselected tokens (round robin
 //            over all waves of the problem) and publish u_i tagged with the
 //            round number
@@ -696,65 +697,43 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 //            (identical inputs, deterministic top-k)
 //   resp   - one block per 64-row chunk, its waves splitting the pool:
 //            responsibility softmax over the pool, per-chunk sums per pool
-//            token -> global
-//   | grid barrier
-//   batch  - every block sums the chunk partials in chunk order and picks the
-//            same batch; the last block records it
-//   cov    - one wave per chunk: b_m <- max(b_m, max_{j in batch} Cbar_mj),
-//            published tagged; every block waits for the tags and copies b
-//            into LDS
-// After the last round the last block writes the support list (ascending,
-// with each token's slot) and, after a final barrier, F(S) and F(V) from the
-// chunks' shares.
-// Tagged values and the chunk partials are double-buffered by round parity.
-// A buffer is rewritten two rounds later, and the grid barrier between keeps
-// every block within one round of the others, so no reader can see a value
-// of the wrong round.
-// Everything another block reads in the same launch goes through
-// device-coherent stores and loads.
-constexpr int kSpinLimit = 1 << 18;   // bounded barrier wait (a fraction of a second)
-constexpr int kCntBarrier = 5;         // arrivals at grid barriers (cumulative)
-constexpr int kCntStatus = 7;          // device status bits, 1 = barrier timeout
-
-// Grid barrier number k (1, 2, ...) over the nblk blocks of one problem:
-// arrivals accumulate (no reset inside the launch) and a block waits until
-// nblk * k have arrived.  The wait is
-// bounded: after kSpinLimit polls, or once any block of the problem has
-// recorded a timeout, the block records the timeout, stops waiting at this
-// and every later barrier, and runs to its end, so every wave always exits.
-__device__ __forceinline__ void grid_barrier(int* cnt, int nblk, int k, int* failed) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int old = __hip_atomic_fetch_add(&cnt[kCntBarrier], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (old != nblk * k - 1 && !*failed) {
-      for (int spin = 0;; ++spin) {
-        if (__hip_atomic_load(&cnt[kCntBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nblk * k) break;
-        if (spin == kSpinLimit ||
-            ((spin & 63) == 63 &&
-             __hip_atomic_load(&cnt[kCntStatus], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
-          __hip_atomic_store(&cnt[kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          *failed = 1;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-    }
-  }
-  __syncthreads();
-}
-
-// Arrival at grid barrier k without waiting (for blocks with no later work).
-__device__ __forceinline__ void grid_arrive(int* cnt) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(&cnt[kCntBarrier], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+//            token, published tagged
+//   batch  - every block waits for the tagged chunk sums, adds them in chunk
+//            order and picks the same batch; the last block records it
+//   cov    - one wave per 64-row chunk: b_m <- max(b_m, max_{j in batch}
+//            Cbar_mj), published tagged; every block waits for the tags and
+//            copies b into LDS
+// In the last round only the last block continues after the batch: it
+// refreshes its own coverage copy, writes the coverage, F(S) and F(V), and
+// the support list (ascending, with each token's slot).
+//
+// Tagged values are double-buffered by round parity, so a buffer is rewritten
+// two rounds after the round that read it.  Along with its coverage rows each
+// block publishes a tagged heartbeat (after it has read everything of the
+// round except the coverage), and the coverage hand-off waits for every
+// block's heartbeat as well as for the rows.  A block therefore starts round
+// r + 1 only after every block has finished its reads of round r - 1 and
+// earlier, so no value is overwritten before all its readers are done; the
+// ordering rides on a poll that happens anyway, with no barrier and no
+// same-address atomics.  Every wait is
+// bounded: after kSpinLimit polls, or once this block has recorded a timeout,
+// the block records the timeout (device status word) and stops waiting, so
+// every wave always exits.
+constexpr int kSpinLimit = 1 << 18;   // bounded waits (a fraction of a second)
+constexpr int kCntStatus = 7;          // device status bits, 1 = wait timeout
 
 // Marks the call failed (device status word) after a bounded wait.
 __device__ __forceinline__ void mark_timeout(int* cnt, int* failed) {
   __hip_atomic_store(&cnt[kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   *failed = 1;
+}
+
+// Entry i of the coverage hand-off poll: rows [0, m), then the heartbeats at
+// [ldM, ldM + nblk); the padding rows [m, ldM) are never written and poll
+// row m - 1 instead.
+__device__ __forceinline__ int stage_index(int i, const Shape& sh, int nst) {
+  i = min(i, nst - 1);
+  return (i >= sh.m && i < sh.ldM) ? sh.m - 1 : i;
 }
 
 // Pool of the persistent selection with the keys in registers: thread t
@@ -794,28 +773,33 @@ __device__ __forceinline__ void pool_regs(const Shape& sh, const unsigned long l
 __global__ void __launch_bounds__(256)
 select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_pool, int32_t* trace_batch) {
   extern __shared__ float dyn[];
-  // LDS: b_m [ldM] | selected flags [N, padded to 16 bytes] | pool keys [N]
-  //      (only when N exceeds the register top-k)
+  // LDS: b_m [ldM] | alpha_m [ldM] | selected flags [N, padded to 16 bytes] |
+  //      pool keys [N] (only when N exceeds the register top-k)
   float* bl = dyn;
-  unsigned char* taken = reinterpret_cast<unsigned char*>(dyn + sh.ldM);
+  float* al = dyn + sh.ldM;
+  unsigned char* taken = reinterpret_cast<unsigned char*>(dyn + 2 * sh.ldM);
   uint32_t* keys = reinterpret_cast<uint32_t*>(taken + ((sh.N + 15) & ~15));
   __shared__ int hist[768], scan[16], bc[2], failed;
   __shared__ int pool_s[64], chosen[64], bidx[64];
   __shared__ __attribute__((aligned(16))) uint32_t bkeys[64];
-  __shared__ float rmu[4][64], rden_s[4][64];
+  __shared__ float rmu[4][64], rden_s[4][64], red[16];
   const int p = blockIdx.y, blk = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nwaves = nblk * 4, gw = blk * 4 + wave;
   const int nchunk = (sh.m + 63) / 64;
-  const float* alpha = ws.alpha + p * ws.s_m;
-  float* cov = ws.cov + p * ws.s_cov;
   const float* E = ws.E + p * ws.s_E;
   unsigned long long* tu = ws.tu + p * ws.s_tu;
+  unsigned long long* ts = ws.ts + p * ws.s_ts;
   unsigned long long* tc = ws.tc + p * ws.s_tc;
-  float* sp = ws.spart + p * ws.s_spart;
-  float* obj = ws.rstat + p * ws.s_rstat;   // per-chunk objective shares [2 * nchunk]
+  const float* alpha_g = ws.alpha + p * ws.s_m;
   int* cnt = ws.cnt + p * ws.s_cnt;
-  for (int m = tid; m < sh.ldM; m += 256) bl[m] = 0.f;     // coverage is zero at call start
+  {
+    const float* alpha = ws.alpha + p * ws.s_m;
+    for (int m = tid; m < sh.ldM; m += 256) {
+      bl[m] = 0.f;   // coverage is zero at call start
+      al[m] = alpha[m];
+    }
+  }
   for (int i = tid; i < sh.N; i += 256) taken[i] = 0;
   if (tid == 0) failed = 0;
   __syncthreads();
@@ -825,10 +809,10 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     const int bsize = min(sh.b, sh.K - selected);
     const unsigned tag = static_cast<unsigned>(r + 1);
     unsigned long long* tur = tu + (r & 1) * sh.N;
-    unsigned long long* tcr = tc + (r & 1) * sh.ldM;
-    float* spr = sp + (r & 1) * 64LL * nchunk;
-    // ---- singleton gains of unselected tokens, two tokens per wave pass,
-    //      published with this round's tag
+    unsigned long long* tsr = ts + (r & 1) * 64LL * nchunk;
+
+    // ---- singleton gains of unselected tokens, two tokens per wave pass with
+    //      all their row loads in flight, published with this round's tag
     for (int i0 = gw; i0 < sh.N; i0 += 2 * nwaves) {
       const int i1 = i0 + nwaves;
       const bool ok0 = taken[i0] == 0;
@@ -840,7 +824,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       float a0 = 0.f, a1 = 0.f;
 #pragma unroll 4
       for (int m = lane * 4; m < sh.m; m += 256) {
-        const float4 a = *reinterpret_cast<const float4*>(alpha + m);
+        const float4 a = *reinterpret_cast<const float4*>(alpha_g + m);
         const float4 b = *reinterpret_cast<const float4*>(bl + m);
         const float4 v0 = *reinterpret_cast<const float4*>(c0 + m);
         const float4 v1 = *reinterpret_cast<const float4*>(c1 + m);
@@ -906,12 +890,13 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     }
 
     // ---- responsibilities: one block per 64-row chunk (lane = client row),
-    //      its four waves split the pool positions 16 apiece
+    //      its four waves split the pool positions 16 apiece; the per-chunk
+    //      sums are published with this round's tag
     for (int c = blk; c < nchunk; c += nblk) {
       const int m = c * 64 + lane;
       const bool row_ok = m < sh.m;
       const int mc = row_ok ? m : 0;
-      const float a = row_ok ? alpha[mc] : 0.f;
+      const float a = row_ok ? al[mc] : 0.f;
       const float b = bl[mc];
       const int j0 = wave * 16;
       float v[16];
@@ -951,24 +936,32 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       float tot = v[0];
       tot += __shfl_xor(tot, 16, kWave);
       tot += __shfl_xor(tot, 32, kWave);
-      if (lane < 16) st_dev(&spr[static_cast<long long>(c) * 64 + j0 + lane], tot);
+      if (lane < 16) st_dev64(&tsr[static_cast<long long>(c) * 64 + j0 + lane], tag_value(tag, tot));
       __syncthreads();   // rmu / rden_s are reused by the next chunk
     }
-    // the one grid barrier of the round: it also bounds how far any block
-    // can run ahead, which makes the double-buffered tagged values safe
-    grid_barrier(cnt, nblk, r + 1, &failed);
 
-    // ---- the batch, identical in every block
+    // ---- the batch, identical in every block: wave 0 waits for every
+    //      chunk's tagged sums (64 loads in flight) and adds them in chunk order
     if (wave == 0) {
-      // chunk partials summed in chunk order; up to 64 loads in flight
       float s = 0.f;
       for (int c0 = 0; c0 < nchunk; c0 += 64) {
-        float t[64];
+        unsigned long long w[64];
 #pragma unroll
-        for (int q = 0; q < 64; ++q) t[q] = ld_dev(&spr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
+        for (int q = 0; q < 64; ++q) w[q] = ld_dev64(&tsr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
+        for (int spin = 0;; ++spin) {
+          bool pend = false;
+#pragma unroll
+          for (int q = 0; q < 64; ++q) pend |= tag_of(w[q]) != tag;
+          if (!pend || failed) break;
+          if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int q = 0; q < 64; ++q)
+            if (tag_of(w[q]) != tag) w[q] = ld_dev64(&tsr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
+        }
 #pragma unroll
         for (int q = 0; q < 64; ++q)
-          if (c0 + q < nchunk) s += t[q];
+          if (c0 + q < nchunk) s += value_of(w[q]);
       }
       bkeys[lane] = score_key(s);
       __builtin_amdgcn_wave_barrier();
@@ -977,55 +970,111 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       if (lane < bsize) bidx[lane] = pool_s[chosen[lane]];
     }
     __syncthreads();
-    // the last block records the batch: it owns no row chunk, so the
-    // global stores stay off the coverage refresh's path
-    if (blk == nblk - 1) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, trace_batch);
-    if (tid < bsize) taken[bidx[tid]] = 1;
     const bool last = r + 1 == sh.rounds;
+    // the last block records the batch (and alone finishes the last round)
+    if (blk == nblk - 1) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, trace_batch);
+    else if (last) break;
+    if (tid < bsize) taken[bidx[tid]] = 1;
+    if (!last) {
+      // ---- coverage refresh with the batch: one wave per 64-row chunk,
+      //      published with this round's tag
+      unsigned long long* tcr = tc + (r & 1) * (sh.ldM + kMaxPersist);
+      for (int c = gw; c < nchunk; c += nwaves) {
+        const int m = c * 64 + lane;
+        const int mc = min(m, sh.m - 1);
+        const float a = al[mc];
+        float cm = bl[mc];
+        for (int k0 = 0; k0 < bsize; k0 += 16) {
+          float v[16];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) v[q] = E[static_cast<long long>(bidx[min(k0 + q, bsize - 1)]) * sh.ldM + mc];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) cm = fmaxf(cm, a * v[q]);
+        }
+        if (m < sh.m) st_dev64(&tcr[m], tag_value(tag, cm));
+      }
+      // this block's heartbeat: it has read everything of earlier rounds
+      if (tid == 0) st_dev64(&tcr[sh.ldM + blk], tag_value(tag, 0.f));
+      // ---- every block copies the refreshed coverage into LDS, waiting for
+      //      the tags and for every block's heartbeat
+      const int nst = sh.ldM + nblk;
+      for (int m0 = 0; m0 < nst; m0 += 256 * 8) {
+        unsigned long long w[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) w[q] = ld_dev64(&tcr[stage_index(m0 + q * 256 + tid, sh, nst)]);
+        for (int spin = 0;; ++spin) {
+          bool pend = false;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) pend |= tag_of(w[q]) != tag;
+          if (!pend || failed) break;
+          if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (tag_of(w[q]) != tag) w[q] = ld_dev64(&tcr[stage_index(m0 + q * 256 + tid, sh, nst)]);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (m0 + q * 256 + tid < sh.m) bl[m0 + q * 256 + tid] = value_of(w[q]);
+      }
+      __syncthreads();
+      selected += bsize;
+      continue;
+    }
 
-    // ---- coverage refresh with the batch: one wave per chunk, published
-    //      with this round's tag (the last round stores the plain values)
-    for (int c = gw; c < nchunk; c += nwaves) {
-      const int m = c * 64 + lane;
-      const int mc = min(m, sh.m - 1);
-      const float a = alpha[mc];
-      float cm = bl[mc];
+    // ---- the last round (last block only): coverage refresh of the LDS copy
+    //      with two row groups per trip, 16 batch rows each, all loads in flight
+    for (int m0 = tid * 4; m0 < sh.m; m0 += 2048) {
+      float4 c[2];
+      c[0] = c[1] = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int k0 = 0; k0 < bsize; k0 += 16) {
-        float v[16];
+        // indices past the batch repeat its last row: a maximum is unchanged
+        float4 v[2][16];
 #pragma unroll
-        for (int q = 0; q < 16; ++q)
-          v[q] = E[static_cast<long long>(bidx[min(k0 + q, bsize - 1)]) * sh.ldM + mc];
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) cm = fmaxf(cm, a * v[q]);
+          for (int q = 0; q < 16; ++q)
+            v[h][q] = *reinterpret_cast<const float4*>(E + static_cast<long long>(bidx[min(k0 + q, bsize - 1)]) * sh.ldM +
+                                                       min(m0 + h * 1024, sh.ldM - 4));
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            c[h].x = fmaxf(c[h].x, v[h][q].x); c[h].y = fmaxf(c[h].y, v[h][q].y);
+            c[h].z = fmaxf(c[h].z, v[h][q].z); c[h].w = fmaxf(c[h].w, v[h][q].w);
+          }
       }
-      if (m < sh.m) {
-        if (last)
-          cov[m] = cm;
-        else
-          st_dev64(&tcr[m], tag_value(tag, cm));
-      }
-      if (last) {
-        // this chunk's share of F(S) = sum_m b_m and F(V) = sum_m max_i Cbar_mi
-        const float fs = wave_sum(m < sh.m ? cm : 0.f);
-        const float fv = wave_sum(m < sh.m ? ws.peak[p * ws.s_m + mc] : 0.f);
-        if (lane == 0) {
-          st_dev(&obj[2 * c], fs);
-          st_dev(&obj[2 * c + 1], fv);
+      // alpha_m >= 0, so alpha_m max_j Et[j][m] = max_j Cbar_mj exactly
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int m = m0 + h * 1024;
+        if (m < sh.m) {
+          const float4 a = *reinterpret_cast<const float4*>(al + m);
+          float4 b = *reinterpret_cast<const float4*>(bl + m);
+          b.x = fmaxf(b.x, a.x * c[h].x); b.y = fmaxf(b.y, a.y * c[h].y);
+          b.z = fmaxf(b.z, a.z * c[h].z); b.w = fmaxf(b.w, a.w * c[h].w);
+          *reinterpret_cast<float4*>(bl + m) = b;
         }
       }
     }
     selected += bsize;
+    __syncthreads();
     if (last) {
-      if (blk != nblk - 1) {
-        grid_arrive(cnt);
-        break;
+      // the last block: the coverage, F(S) = sum_m b_m and F(V) = sum_m
+      // max_i Cbar_mi, then the support list in ascending source order with
+      // each token's slot
+      float* cov = ws.cov + p * ws.s_cov;
+      const float* peak = ws.peak + p * ws.s_m;
+      float fs = 0.f, fv = 0.f;
+      for (int m = tid; m < sh.m; m += 256) {
+        cov[m] = bl[m];
+        fs += bl[m];
+        fv += peak[m];
       }
-      // the last block: support list in ascending source order with each
-      // token's slot, then (after every chunk's share has arrived) the
-      // objective values in chunk order
+      fs = block_sum(fs, red);
+      fv = block_sum(fv, red);
       int* sup = ws.sup + p * ws.s_sup;
       int* slot = ws.slot + p * ws.s_slot;
-      __syncthreads();   // the last batch's flags are visible to every thread
       int base = 0;
       for (int b0 = 0; b0 < sh.N; b0 += 256) {
         const int i = b0 + tid;
@@ -1038,16 +1087,10 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
         }
         base += tot;
       }
-      grid_barrier(cnt, nblk, sh.rounds + 1, &failed);
       if (tid == 0) {
-        float a = 0.f, b2 = 0.f;
-        for (int c = 0; c < nchunk; ++c) {
-          a += ld_dev(&obj[2 * c]);
-          b2 += ld_dev(&obj[2 * c + 1]);
-        }
         float* st = ws.stats + p * ws.s_st;
-        st[2] = a;
-        st[3] = b2;
+        st[2] = fs;
+        st[3] = fv;
         st[4] = static_cast<float>(sh.K);
         st[5] = static_cast<float>(sh.rounds);
         st[6] = static_cast<float>(sh.m);
@@ -1055,27 +1098,6 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       }
       break;
     }
-    // ---- every block copies the refreshed coverage into LDS (waits for the tags)
-    for (int m0 = 0; m0 < sh.m; m0 += 256 * 8) {
-      unsigned long long w[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) w[q] = ld_dev64(&tcr[min(m0 + q * 256 + tid, sh.m - 1)]);
-      for (int spin = 0;; ++spin) {
-        bool pend = false;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) pend |= tag_of(w[q]) != tag;
-        if (!pend || failed) break;
-        if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
-        __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-        for (int q = 0; q < 8; ++q)
-          if (tag_of(w[q]) != tag) w[q] = ld_dev64(&tcr[min(m0 + q * 256 + tid, sh.m - 1)]);
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        if (m0 + q * 256 + tid < sh.m) bl[m0 + q * 256 + tid] = value_of(w[q]);
-    }
-    __syncthreads();
   }
 }
 
@@ -1088,9 +1110,9 @@ __global__ void select_init_kernel(Shape sh, Ws ws) {
   for (int m = x0; m < sh.ldM; m += stride) {
     ws.cov[p * ws.s_cov + m] = 0.f;
     if (m >= sh.m) ws.alpha[p * ws.s_m + m] = 0.f;
-    ws.tc[p * ws.s_tc + m] = 0ull;
-    ws.tc[p * ws.s_tc + sh.ldM + m] = 0ull;
   }
+  for (int j = x0; j < 128 * ((sh.m + 63) / 64); j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
+  for (int j = x0; j < 2 * (sh.ldM + kMaxPersist); j += stride) ws.tc[p * ws.s_tc + j] = 0ull;
   for (int i = x0; i < sh.N; i += stride) {
     ws.tu[p * ws.s_tu + i] = 0ull;
     ws.tu[p * ws.s_tu + sh.N + i] = 0ull;
@@ -1177,7 +1199,7 @@ static int persistent_blocks(const Shape& sh, size_t lds) {
   // one CU per block; about two gain tokens per wave
   const int cap = n_cu / sh.B;
   const int want = max((sh.N + 7) / 8, ((sh.m + 63) / 64 + 3) / 4);
-  const int nblk = min(cap, want);
+  const int nblk = min(min(cap, want), kMaxPersist);
   return nblk >= 1 ? nblk : 0;
 }
 
@@ -1185,7 +1207,7 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
                             int32_t* trace_batch, hipStream_t st, bool* support_ready) {
   *support_ready = false;
   {
-    const size_t lds = static_cast<size_t>(sh.ldM) * sizeof(float) +
+    const size_t lds = 2 * static_cast<size_t>(sh.ldM) * sizeof(float) +
                        ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15)) +
                        (sh.N > 256 * 16 ? static_cast<size_t>(sh.N) * sizeof(uint32_t) : 0);
     int nblk = persistent_blocks(sh, lds);
