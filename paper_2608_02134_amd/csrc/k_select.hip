@@ -126,17 +126,23 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
 
 // Register-resident variant of the same selection for small n: thread t
 // holds the keys of its contiguous index segment [t*seg, t*seg + seg) in
-// k[0..KPT) (0 past the segment).  Every wave scans the histogram itself, so
-// a radix pass needs one block barrier (three histogram buffers rotate).
+// k[0..KPT) (0 past the segment; zero keys are excluded).  The radix windows
+// start at the highest bit in which the non-zero keys differ, so the first
+// histogram spreads the keys over up to 256 bins.  Once the bin holding the
+// threshold has at most 64 keys, its keys are gathered into LDS and every
+// wave finishes the threshold with a bitwise ballot search over them (no
+// further histogram passes or block barriers).  Every wave scans the
+// histograms itself, so a radix pass needs one block barrier (three
+// histogram buffers rotate).
 // hist: 768 ints of LDS, scan: >= 16 ints.
 template <int KPT>
 __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, int* out, int* hist, int* scan) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned long long below = (1ull << lane) - 1ull;
   hist[tid] = 0;
   hist[256 + tid] = 0;
   hist[512 + tid] = 0;
-  // excluded (zero) keys are never selected: they take no part in the
-  // shared-digit test or the histograms
+  if (tid == 0) scan[8] = 0;
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
 #pragma unroll
   for (int q = 0; q < KPT; ++q) {
@@ -152,19 +158,19 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
   kor = static_cast<uint32_t>(scan[4]) | static_cast<uint32_t>(scan[5]) | static_cast<uint32_t>(scan[6]) |
         static_cast<uint32_t>(scan[7]);
   const uint32_t diff = kand ^ kor;
-  uint32_t mask = 0;
-  int top = 24;
-  while (top > 0 && ((diff >> top) & 0xFFu) == 0u) {
-    mask |= 0xFFu << top;
-    top -= 8;
-  }
+  // bits [hi, 32) are shared by every non-zero key; with no differing bit
+  // every non-zero key equals kand
+  int hi = diff ? 32 - __clz(diff) : 0;
+  uint32_t mask = hi >= 32 ? 0u : ~((1u << hi) - 1u);
   uint32_t prefix = kand & mask;
   int remaining = count, buf = 0;
-  for (int shift = top; shift >= 0; shift -= 8) {
+  while (hi > 0) {
+    const int lo = max(hi - 8, 0);
+    const uint32_t wmask = ((1u << (hi - lo)) - 1u) << lo;
     int* h = hist + buf * 256;
 #pragma unroll
     for (int q = 0; q < KPT; ++q)
-      if (k[q] != 0u && (k[q] & mask) == prefix) atomicAdd(&h[(k[q] >> shift) & 255u], 1);
+      if (k[q] != 0u && (k[q] & mask) == prefix) atomicAdd(&h[(k[q] & wmask) >> lo], 1);
     const int nxt = buf == 2 ? 0 : buf + 1;
     hist[nxt * 256 + tid] = 0;   // last read two passes ago
     __syncthreads();
@@ -174,21 +180,56 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
     const int incl = wave_scan_add(loc);
     int excl = incl - loc;
     const bool hit = excl < remaining && remaining <= incl;
-    int dig = 0, rem = 0;
+    int dig = 0, rem = 0, inbin = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (excl < remaining && remaining <= excl + v[q]) {
         dig = 255 - (lane * 4 + q);
         rem = remaining - excl;
+        inbin = v[q];
       }
       excl += v[q];
     }
     const int src = __ffsll(static_cast<unsigned long long>(__ballot(hit))) - 1;
     dig = __builtin_amdgcn_readlane(dig, src);
     rem = __builtin_amdgcn_readlane(rem, src);
-    prefix |= static_cast<uint32_t>(dig) << shift;
-    mask |= 0xFFu << shift;
+    inbin = __builtin_amdgcn_readlane(inbin, src);
+    prefix |= static_cast<uint32_t>(dig) << lo;
+    mask |= wmask;
     remaining = rem;
+    hi = lo;
+    if (hi > 0 && inbin <= 64) {
+      // gather the threshold bin's keys into the third buffer (free: last
+      // read before the barrier above), one LDS atomic per wave
+      uint32_t* cand = reinterpret_cast<uint32_t*>(hist + (3 - buf - nxt) * 256);
+      unsigned long long bm[KPT];
+      int tot = 0;
+#pragma unroll
+      for (int q = 0; q < KPT; ++q) {
+        bm[q] = __ballot(k[q] != 0u && (k[q] & mask) == prefix);
+        tot += __popcll(bm[q]);
+      }
+      int base = 0;
+      if (lane == 0 && tot > 0) base = atomicAdd(&scan[8], tot);
+      base = __builtin_amdgcn_readlane(base, 0);
+#pragma unroll
+      for (int q = 0; q < KPT; ++q) {
+        if ((bm[q] >> lane) & 1ull) cand[base + __popcll(bm[q] & below)] = k[q];
+        base += __popcll(bm[q]);
+      }
+      __syncthreads();
+      // the remaining-th largest key of the bin, bit by bit below lo
+      const bool has = lane < inbin;
+      const uint32_t c = has ? cand[lane] : 0u;
+      uint32_t t = prefix;
+      for (int bit = hi - 1; bit >= 0; --bit) {
+        const uint32_t trial = t | (1u << bit);
+        if (__popcll(__ballot(has && c >= trial)) >= remaining) t = trial;
+      }
+      remaining -= __popcll(__ballot(has && c > t));
+      prefix = t;
+      hi = 0;
+    }
     buf = nxt;
   }
   const uint32_t kth = prefix;
@@ -940,29 +981,37 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       __syncthreads();   // rmu / rden_s are reused by the next chunk
     }
 
-    // ---- the batch, identical in every block: wave 0 waits for every
-    //      chunk's tagged sums (64 loads in flight) and adds them in chunk order
-    if (wave == 0) {
+    // ---- the batch, identical in every block: each wave waits for the
+    //      tagged sums of a quarter of the chunks (16 loads in flight) and
+    //      adds them in chunk order; the quarters are added in wave order
+    {
+      const int per = (nchunk + 3) / 4;
+      const int c_end = min(nchunk, (wave + 1) * per);
       float s = 0.f;
-      for (int c0 = 0; c0 < nchunk; c0 += 64) {
-        unsigned long long w[64];
+      for (int c0 = wave * per; c0 < c_end; c0 += 16) {
+        unsigned long long w[16];
 #pragma unroll
-        for (int q = 0; q < 64; ++q) w[q] = ld_dev64(&tsr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
+        for (int q = 0; q < 16; ++q) w[q] = ld_dev64(&tsr[static_cast<long long>(min(c0 + q, c_end - 1)) * 64 + lane]);
         for (int spin = 0;; ++spin) {
           bool pend = false;
 #pragma unroll
-          for (int q = 0; q < 64; ++q) pend |= tag_of(w[q]) != tag;
+          for (int q = 0; q < 16; ++q) pend |= tag_of(w[q]) != tag;
           if (!pend || failed) break;
           if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
           __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-          for (int q = 0; q < 64; ++q)
-            if (tag_of(w[q]) != tag) w[q] = ld_dev64(&tsr[static_cast<long long>(min(c0 + q, nchunk - 1)) * 64 + lane]);
+          for (int q = 0; q < 16; ++q)
+            if (tag_of(w[q]) != tag) w[q] = ld_dev64(&tsr[static_cast<long long>(min(c0 + q, c_end - 1)) * 64 + lane]);
         }
 #pragma unroll
-        for (int q = 0; q < 64; ++q)
-          if (c0 + q < nchunk) s += value_of(w[q]);
+        for (int q = 0; q < 16; ++q)
+          if (c0 + q < c_end) s += value_of(w[q]);
       }
+      rmu[wave][lane] = s;   // free: the responsibility loop ended with a barrier
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const float s = ((rmu[0][lane] + rmu[1][lane]) + rmu[2][lane]) + rmu[3][lane];
       bkeys[lane] = score_key(s);
       __builtin_amdgcn_wave_barrier();
       wave_topb(bkeys, psize, bsize, chosen);
@@ -998,23 +1047,23 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       // ---- every block copies the refreshed coverage into LDS, waiting for
       //      the tags and for every block's heartbeat
       const int nst = sh.ldM + nblk;
-      for (int m0 = 0; m0 < nst; m0 += 256 * 8) {
-        unsigned long long w[8];
+      for (int m0 = 0; m0 < nst; m0 += 256 * 16) {
+        unsigned long long w[16];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) w[q] = ld_dev64(&tcr[stage_index(m0 + q * 256 + tid, sh, nst)]);
+        for (int q = 0; q < 16; ++q) w[q] = ld_dev64(&tcr[stage_index(m0 + q * 256 + tid, sh, nst)]);
         for (int spin = 0;; ++spin) {
           bool pend = false;
 #pragma unroll
-          for (int q = 0; q < 8; ++q) pend |= tag_of(w[q]) != tag;
+          for (int q = 0; q < 16; ++q) pend |= tag_of(w[q]) != tag;
           if (!pend || failed) break;
           if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
           __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-          for (int q = 0; q < 8; ++q)
+          for (int q = 0; q < 16; ++q)
             if (tag_of(w[q]) != tag) w[q] = ld_dev64(&tcr[stage_index(m0 + q * 256 + tid, sh, nst)]);
         }
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
+        for (int q = 0; q < 16; ++q)
           if (m0 + q * 256 + tid < sh.m) bl[m0 + q * 256 + tid] = value_of(w[q]);
       }
       __syncthreads();
