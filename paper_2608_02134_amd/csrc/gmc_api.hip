@@ -145,7 +145,7 @@ struct Plan {
   Capacity cap;
   long long s_n, s_z, s_zp, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
       s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
-      s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_ts, s_tc;
+      s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_ts, s_tc, s_lpart, s_lcnt;
 };
 
 Plan make_plan(const gmc_config& c) {
@@ -170,6 +170,8 @@ Plan make_plan(const gmc_config& c) {
   pl.s_n = k.N;
   pl.s_z = static_cast<long long>(k.N) * k.hr;
   pl.s_zp = kProbeSplit * pl.s_z;
+  pl.s_lpart = 4LL * kLogitSplit * k.hq * std::max(k.T, 1);
+  pl.s_lcnt = cdiv(static_cast<long long>(c.n_q_heads / c.n_kv_heads) * std::max(k.T, 1), 16) * c.n_kv_heads;
   pl.s_sig = kMaxHeads;
   pl.s_ell = static_cast<long long>(k.hq) * k.N;
   pl.s_E = static_cast<long long>(k.N) * k.ldM;
@@ -221,7 +223,7 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
 #define F(name) ws->name = reinterpret_cast<float*>(take(pl.s_##name, 4)); ws->s_##name = pl.s_##name
 #define I(name) ws->name = reinterpret_cast<int*>(take(pl.s_##name, 4)); ws->s_##name = pl.s_##name
   ws->n2 = reinterpret_cast<float*>(take(pl.s_n, 4)); ws->s_n = pl.s_n;
-  F(z); F(zp); F(sig); F(ell); F(E);
+  F(z); F(zp); F(lpart); I(lcnt); F(sig); F(ell); F(E);
   ws->alpha = reinterpret_cast<float*>(take(pl.s_m, 4)); ws->s_m = pl.s_m;
   ws->peak = reinterpret_cast<float*>(take(pl.s_m, 4));
   ws->rowsum = reinterpret_cast<float*>(take(pl.s_m, 4));
@@ -469,6 +471,15 @@ int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req,
   s.ldK = static_cast<int>(round_up(K, 4));
   s.n_app_cblk = static_cast<int>(cdiv(N, 64));
   s.n_head_blk = static_cast<int>(cdiv(N, kHeadTok));
+  {
+    // split the logit columns until about two blocks per CU of a 256-CU part
+    // are busy, keeping at least eight tiles (one per wave) per range
+    const long long blocks = cdiv(static_cast<long long>(s.hg) * s.T, 16) * s.hkv * s.B;
+    const long long ntile = cdiv(N, 16);
+    long long ls = blocks > 0 ? 512 / blocks : 1;
+    ls = std::min<long long>(ls, ntile / 8);
+    s.lsplit = static_cast<int>(std::max<long long>(1, std::min<long long>(ls, kLogitSplit)));
+  }
   s.npairs = s.hq * (s.hq + 1) / 2;
   *out = s;
   return GMC_OK;

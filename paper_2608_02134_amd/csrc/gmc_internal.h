@@ -14,6 +14,7 @@ constexpr int kHeadTok = 16;      // tokens per head-Gram block
 constexpr int kStats = 9;
 constexpr int kCounters = 8;      // completion counters per problem
 constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection
+constexpr int kLogitSplit = 8;    // column ranges of the message-logit kernels (at most)
 constexpr int kProbeSplit = 4;    // K splits of the value-probe GEMM (d a multiple of 256)
 
 // Call shape, resolved on the host for one gmc_prune call.
@@ -28,6 +29,7 @@ struct Shape {
   int ldK;                                // cosine buffer row stride (floats)
   int n_app_cblk;                         // column blocks of the appearance GEMM
   int n_head_blk;                         // token blocks of the head-Gram kernel
+  int lsplit;                             // column ranges of the message-logit kernels
   int npairs;                             // head pairs h <= g
   int landmarks;
   int dtype;                              // 0 float32, 1 bfloat16
@@ -50,6 +52,8 @@ struct Ws {
   float* n2;       long long s_n;       // squared row norms            [N]
   float* z;        long long s_z;       // probe coordinates Z          [N][hr]
   float* zp;       long long s_zp;      // split-K probe partials       [kProbeSplit][N][hr]
+  float* lpart;    long long s_lpart;   // message-logit range partials  [4][kLogitSplit][mg]
+  int* lcnt;       long long s_lcnt;    // range arrivals per logit row tile [ceil(hg T/16) hkv]
   float* sig;      long long s_sig;     // mass coordinate sigma_h      [hq]
   float* ell;      long long s_ell;     // ||Z_h[i]||^2; the atom norm is sqrt(ell + sigma_h^2)  [hq][N]
   float* E;        long long s_E;       // client energies, token-major [N][ldM]

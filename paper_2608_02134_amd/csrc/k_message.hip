@@ -121,35 +121,59 @@ __global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws 
 
 // ---------------------------------------------------------------------------
 // Native message slice and grounded energies.
-// Block = 16 rows (h,t) of one kv group x all N visual columns; the 4 waves
-// split the 16-column tiles.  Pass 1: online max / sum-exp of the logits
-// q.k/sqrt(dh).  Pass 2: recompute the logits (cheaper than storing them),
-// e = exp(s - D) * l_h[i] with D the (optionally nonvisual-extended)
-// log-sum-exp, write e to the grounded client rows, and reduce row sums and
-// row maxima.  Nothing but e ever reaches HBM.
+// A block covers 16 rows (h,t) of one kv group and one of lsplit column
+// ranges; its waves take the 16-column tiles of the range in turn.  Two
+// kernels: logits_lse_kernel reduces the online max / sum-exp of the logits
+// q.k/sqrt(dh) over the block's columns into per-range partials;
+// logits_kernel combines the partials into the log-sum-exp D (optionally
+// extended by the nonvisual part), recomputes the logits (cheaper than
+// storing them), writes e = exp(s - D) l_h[i] to the grounded client rows and
+// leaves per-range row sums and row maxima.  Nothing but e reaches HBM.
+// Splitting the columns over blocks puts every CU to work on the key stream.
 // ---------------------------------------------------------------------------
 // Waves per logits block, each on its own key tiles (fewer where the fp32
 // fragments of a wide head would not fit the registers of eight waves).
 template <typename T, int DH>
 constexpr int logit_waves() { return (sizeof(T) == 4 && DH >= 224) ? 4 : 8; }
 
+// Tiles per wave and chunk: every load of a chunk is issued before its first
+// MFMA, so a chunk costs one memory latency and no load is in flight across
+// the chunk loop's back edge (where the compiler would wait for everything).
 template <typename T, int DH>
-__global__ void __launch_bounds__((64 * logit_waves<T, DH>()))
-logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* nonvis_lse) {
-  constexpr int KS = DH / 32;
-  constexpr int kLogitWaves = logit_waves<T, DH>();
-  __shared__ float sm_m[kLogitWaves][16], sm_s[kLogitWaves][16];
-  __shared__ float sm_D[16];
-  const int p = blockIdx.z, g = blockIdx.y;
-  const int rows_g = sh.hg * sh.T;
-  const int rb = blockIdx.x * 16;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int fr = lane & 15, fk = (lane >> 4) * 8;
-  const float scale = rsqrtf(static_cast<float>(DH));
+constexpr int logit_chunk() {
+  constexpr int KS = DH / 32, FR = static_cast<int>(sizeof(Frag<T>) / 4);
+  constexpr int budget = logit_waves<T, DH>() == 4 ? 192 : 96;   // registers for key tiles
+  return budget / (KS * FR) < 1 ? 1 : (budget / (KS * FR) > 6 ? 6 : budget / (KS * FR));
+}
 
-  // A operand: query row rb + fr of this group
+// Shared set-up of both logits kernels: block coordinates, the query
+// fragments (A operand, row rb + fr), key addressing and the column range.
+template <typename T, int DH>
+struct LogitBlock {
+  static constexpr int KS = DH / 32;
+  int p, g, rb, split, rows_g, t_beg, t_end;
+  int lane, wave, fr, fk, orow, oc;
+  float scale;
+  const T* kbase;
+  long long kstride;
   Frag<T> qf[KS];
-  {
+
+  __device__ LogitBlock(const Shape& sh, const T* text_q, const T* vis_k) {
+    p = blockIdx.z;
+    g = blockIdx.y;
+    rb = (blockIdx.x / sh.lsplit) * 16;
+    split = blockIdx.x % sh.lsplit;
+    rows_g = sh.hg * sh.T;
+    lane = threadIdx.x & 63;
+    wave = threadIdx.x >> 6;
+    fr = lane & 15;
+    fk = (lane >> 4) * 8;
+    orow = (lane >> 4) * 4;
+    oc = lane & 15;
+    scale = rsqrtf(static_cast<float>(DH));
+    const int ntile = (sh.N + 15) / 16, tps = (ntile + sh.lsplit - 1) / sh.lsplit;
+    t_beg = min(ntile, split * tps);
+    t_end = min(ntile, t_beg + tps);
     const int rr = rb + fr;
     if (rr < rows_g) {
       const int h = g * sh.hg + rr / sh.T, t = rr % sh.T;
@@ -160,159 +184,229 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) qf[ks] = frag_zero<T>();
     }
+    kbase = vis_k + static_cast<long long>(p) * sh.N * sh.hkv * DH + g * DH;
+    kstride = static_cast<long long>(sh.hkv) * DH;
   }
-  const T* kbase = vis_k + static_cast<long long>(p) * sh.N * sh.hkv * DH + g * DH;
-  const long long kstride = static_cast<long long>(sh.hkv) * DH;
-  const int ntile = (sh.N + 15) / 16;
-  const int orow = (lane >> 4) * 4, oc = lane & 15;
-
   // key fragments of a column tile; the column is clamped so the loads are
-  // unconditional (out-of-range columns are masked by the callers), which
-  // lets the next tile's loads overlap the current tile's MFMAs
-  auto load_keys = [&](int ct, Frag<T>* kf) {
+  // unconditional (out-of-range columns are masked by the callers)
+  __device__ void load_keys(const Shape& sh, int ct, Frag<T>* kf) const {
     const int col = min(ct * 16 + fr, sh.N - 1);
     const T* kr = kbase + col * kstride;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) kf[ks] = frag_load<T>(kr + ks * 32 + fk);
-  };
-  auto tile_mma = [&](const Frag<T>* kf) -> floatx4 {
+  }
+  __device__ floatx4 tile_mma(const Frag<T>* kf) const {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) acc = mma(qf[ks], kf[ks], acc);
     return acc;
-  };
-  const int last_tile = ntile - 1;
+  }
+  // grounded client row of block row r (valid rows only)
+  __device__ long long mrow(const Shape& sh, int r) const {
+    const int rr = rb + r;
+    return static_cast<long long>(g * sh.hg + rr / sh.T) * sh.T + rr % sh.T;
+  }
+};
 
-  // pass 1: online (max, sum exp) per row, lane-local over its columns
+template <typename T, int DH>
+__global__ void __launch_bounds__((64 * logit_waves<T, DH>()))
+logits_lse_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k) {
+  constexpr int W = logit_waves<T, DH>(), MT = logit_chunk<T, DH>(), KS = DH / 32;
+  __shared__ float sm_m[W][16], sm_s[W][16];
+  const LogitBlock<T, DH> lb(sh, text_q, vis_k);
+  // online (max, sum exp) per row, lane-local over its columns
   float mx[4], sm[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) { mx[e] = -INFINITY; sm[e] = 0.f; }
-  // three key tiles in flight per wave: the current one and the next two
-  Frag<T> kcur[KS], kn1[KS], kn2[KS];
-  load_keys(min(wave, last_tile), kcur);
-  load_keys(min(wave + kLogitWaves, last_tile), kn1);
-  for (int ct = wave; ct < ntile; ct += kLogitWaves) {
-    load_keys(min(ct + 2 * kLogitWaves, last_tile), kn2);
-    const floatx4 acc = tile_mma(kcur);
+  for (int c0 = lb.t_beg + lb.wave; c0 < lb.t_end; c0 += MT * W) {
+    Frag<T> kf[MT][KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) { kcur[ks] = kn1[ks]; kn1[ks] = kn2[ks]; }
-    if (ct * 16 + oc < sh.N) {
+    for (int j = 0; j < MT; ++j)
+      if (c0 + j * W < lb.t_end) lb.load_keys(sh, c0 + j * W, kf[j]);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float s = acc[e] * scale;
-        const float nm = fmaxf(mx[e], s);
-        sm[e] = sm[e] * __expf(mx[e] - nm) + __expf(s - nm);
-        mx[e] = nm;
+    for (int j = 0; j < MT; ++j) {
+      const int ct = c0 + j * W;
+      if (ct < lb.t_end) {
+        const floatx4 acc = lb.tile_mma(kf[j]);
+        if (ct * 16 + lb.oc < sh.N) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float s = acc[e] * lb.scale;
+            const float nm = fmaxf(mx[e], s);
+            sm[e] = sm[e] * __expf(mx[e] - nm) + __expf(s - nm);
+            mx[e] = nm;
+          }
+        }
       }
     }
   }
-  // merge across the 16 lanes of a row group, then across waves
+  // merge across the 16 lanes of a row group (maximum first, then each
+  // lane's sum rescaled once and added), then across waves
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) {
-      const float om = __shfl_xor(mx[e], o, kWave), os = __shfl_xor(sm[e], o, kWave);
-      const float nm = fmaxf(mx[e], om);
-      sm[e] = (nm == -INFINITY) ? 0.f : sm[e] * expf(mx[e] - nm) + os * expf(om - nm);
-      mx[e] = nm;
-    }
-    if (oc == 0) { sm_m[wave][orow + e] = mx[e]; sm_s[wave][orow + e] = sm[e]; }
+    const float m = group16_max(mx[e]);
+    const float sc = (mx[e] == -INFINITY) ? 0.f : sm[e] * __expf(mx[e] - m);
+    const float t = group16_sum(sc);
+    if (lb.oc == 0) { sm_m[lb.wave][lb.orow + e] = m; sm_s[lb.wave][lb.orow + e] = t; }
   }
   __syncthreads();
   if (threadIdx.x < 16) {
     const int r = threadIdx.x;
-    float m = -INFINITY;
-    for (int w = 0; w < kLogitWaves; ++w) m = fmaxf(m, sm_m[w][r]);
-    float s = 0.f;
-    for (int w = 0; w < kLogitWaves; ++w) s += (sm_m[w][r] == -INFINITY) ? 0.f : sm_s[w][r] * expf(sm_m[w][r] - m);
-    float D = m + logf(s);
-    const int rr = rb + r;
-    if (nonvis_lse && rr < rows_g) {
-      const int h = g * sh.hg + rr / sh.T, t = rr % sh.T;
-      const float nv = nonvis_lse[(static_cast<long long>(p) * sh.hq + h) * sh.T + t];
-      const float hi = fmaxf(D, nv), lo = fminf(D, nv);
-      D = (hi == -INFINITY) ? hi : hi + log1pf(expf(lo - hi));
+    if (lb.rb + r < lb.rows_g) {
+      float m = -INFINITY;
+      for (int w = 0; w < W; ++w) m = fmaxf(m, sm_m[w][r]);
+      float s = 0.f;
+      for (int w = 0; w < W; ++w) s += (sm_m[w][r] == -INFINITY) ? 0.f : sm_s[w][r] * __expf(sm_m[w][r] - m);
+      float* part = ws.lpart + lb.p * ws.s_lpart;
+      const long long mi = lb.mrow(sh, r);
+      part[static_cast<long long>(lb.split) * sh.mg + mi] = m;
+      part[static_cast<long long>(kLogitSplit + lb.split) * sh.mg + mi] = s;
+    }
+  }
+}
+
+template <typename T, int DH>
+__global__ void __launch_bounds__((64 * logit_waves<T, DH>()))
+logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* nonvis_lse) {
+  constexpr int W = logit_waves<T, DH>(), MT = logit_chunk<T, DH>(), KS = DH / 32;
+  __shared__ float sm_m[W][16], sm_s[W][16];
+  __shared__ float sm_D[16];
+  const LogitBlock<T, DH> lb(sh, text_q, vis_k);
+  float* part = ws.lpart + lb.p * ws.s_lpart;
+  if (threadIdx.x < 16) {
+    // the row's log-sum-exp from the per-range partials, in range order
+    const int r = threadIdx.x, rr = lb.rb + r;
+    float D = 0.f;
+    if (rr < lb.rows_g) {
+      const long long mi = lb.mrow(sh, r);
+      float m = -INFINITY;
+      for (int s = 0; s < sh.lsplit; ++s) m = fmaxf(m, part[static_cast<long long>(s) * sh.mg + mi]);
+      float sum = 0.f;
+      for (int s = 0; s < sh.lsplit; ++s) {
+        const float ms = part[static_cast<long long>(s) * sh.mg + mi];
+        sum += (ms == -INFINITY) ? 0.f : part[static_cast<long long>(kLogitSplit + s) * sh.mg + mi] * expf(ms - m);
+      }
+      D = m + logf(sum);
+      if (nonvis_lse) {
+        const int h = lb.g * sh.hg + rr / sh.T, t = rr % sh.T;
+        const float nv = nonvis_lse[(static_cast<long long>(lb.p) * sh.hq + h) * sh.T + t];
+        const float hi = fmaxf(D, nv), lo = fminf(D, nv);
+        D = (hi == -INFINITY) ? hi : hi + log1pf(expf(lo - hi));
+      }
     }
     sm_D[r] = D;
   }
   __syncthreads();
 
-  // pass 2: write e = A * l and reduce row sums / maxima
-  float D[4], rsum[4], rmax[4];
+  // e = A * l, written to the grounded client rows; row sums / maxima
+  float D[4], rsum[4], rmax[4], sig2[4];
   int hrow[4];
   long long mrow[4];
   bool rvalid[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const int rr = rb + orow + e;
-    rvalid[e] = rr < rows_g;
-    const int h = g * sh.hg + (rvalid[e] ? rr / sh.T : 0), t = rvalid[e] ? rr % sh.T : 0;
-    hrow[e] = h;
-    mrow[e] = static_cast<long long>(h) * sh.T + t;
-    D[e] = sm_D[orow + e];
+    const int rr = lb.rb + lb.orow + e;
+    rvalid[e] = rr < lb.rows_g;
+    hrow[e] = lb.g * sh.hg + (rvalid[e] ? rr / sh.T : 0);
+    mrow[e] = rvalid[e] ? lb.mrow(sh, lb.orow + e) : 0;
+    D[e] = sm_D[lb.orow + e];
     rsum[e] = 0.f;
     rmax[e] = 0.f;
-  }
-  float* E = ws.E + p * ws.s_E;
-  const float* ell = ws.ell + p * ws.s_ell;
-  // atom norms l_h[col] of the lane's four rows travel with the key tiles
-  auto load_ell = [&](int ct, float* lv) {
-    const int col = min(ct * 16 + oc, sh.N - 1);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) lv[e] = ell[static_cast<long long>(hrow[e]) * sh.N + col];
-  };
-  float sig2[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const float sg = ws.sig[p * ws.s_sig + hrow[e]];
+    const float sg = ws.sig[lb.p * ws.s_sig + hrow[e]];
     sig2[e] = sg * sg;
   }
-  float lcur[4], ln1[4], ln2[4];
-  load_keys(min(wave, last_tile), kcur);
-  load_ell(min(wave, last_tile), lcur);
-  load_keys(min(wave + kLogitWaves, last_tile), kn1);
-  load_ell(min(wave + kLogitWaves, last_tile), ln1);
-  for (int ct = wave; ct < ntile; ct += kLogitWaves) {
-    load_keys(min(ct + 2 * kLogitWaves, last_tile), kn2);
-    load_ell(min(ct + 2 * kLogitWaves, last_tile), ln2);
-    const floatx4 acc = tile_mma(kcur);
-    float lv[4];
+  // with T a multiple of 16 the 16 rows of a block are one head's
+  // consecutive queries: a lane's four rows are four consecutive client rows
+  // (one 16-byte store per tile) and share the atom norm l_h[col]
+  const bool vec = (sh.T & 15) == 0;
+  float* E = ws.E + lb.p * ws.s_E;
+  const float* ell = ws.ell + lb.p * ws.s_ell;
+  for (int c0 = lb.t_beg + lb.wave; c0 < lb.t_end; c0 += MT * W) {
+    Frag<T> kf[MT][KS];
+    float lv[MT][4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) { lv[e] = lcur[e]; lcur[e] = ln1[e]; ln1[e] = ln2[e]; }
+    for (int j = 0; j < MT; ++j) {
+      const int ct = c0 + j * W;
+      if (ct >= lb.t_end) continue;
+      lb.load_keys(sh, ct, kf[j]);
+      const int col = min(ct * 16 + lb.oc, sh.N - 1);
+      if (vec) {
+        lv[j][0] = ell[static_cast<long long>(hrow[0]) * sh.N + col];
+      } else {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) { kcur[ks] = kn1[ks]; kn1[ks] = kn2[ks]; }
-    const int col = ct * 16 + oc;
-    if (col < sh.N) {
+        for (int e = 0; e < 4; ++e) lv[j][e] = ell[static_cast<long long>(hrow[e]) * sh.N + col];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      const int ct = c0 + j * W;
+      if (ct >= lb.t_end) continue;
+      const floatx4 acc = lb.tile_mma(kf[j]);
+      const int col = ct * 16 + lb.oc;
+      if (col >= sh.N) continue;
+      float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        if (!rvalid[e]) continue;
-        const float a = __expf(acc[e] * scale - D[e]);
-        const float v = a * sqrtf(lv[e] + sig2[e]);   // atom norm l_h[col]
-        E[static_cast<long long>(col) * sh.ldM + mrow[e]] = v;
-        rsum[e] += v;
-        rmax[e] = fmaxf(rmax[e], v);
+        const float a = __expf(acc[e] * lb.scale - D[e]);
+        v[e] = a * sqrtf((vec ? lv[j][0] : lv[j][e]) + sig2[e]);   // atom norm l_h[col]
+      }
+      if (vec) {
+        *reinterpret_cast<float4*>(E + static_cast<long long>(col) * sh.ldM + mrow[0]) =
+            make_float4(v[0], v[1], v[2], v[3]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          rsum[e] += v[e];
+          rmax[e] = fmaxf(rmax[e], v[e]);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (!rvalid[e]) continue;
+          E[static_cast<long long>(col) * sh.ldM + mrow[e]] = v[e];
+          rsum[e] += v[e];
+          rmax[e] = fmaxf(rmax[e], v[e]);
+        }
       }
     }
   }
-  __syncthreads();
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const float s = group16_sum(rsum[e]);
     const float m = group16_max(rmax[e]);
-    if (oc == 0) { sm_s[wave][orow + e] = s; sm_m[wave][orow + e] = m; }
+    if (lb.oc == 0) { sm_s[lb.wave][lb.orow + e] = s; sm_m[lb.wave][lb.orow + e] = m; }
   }
   __syncthreads();
-  if (threadIdx.x < 16) {
-    const int r = threadIdx.x, rr = rb + r;
-    if (rr < rows_g) {
-      const int h = g * sh.hg + rr / sh.T, t = rr % sh.T;
-      float s = 0.f, m = 0.f;
-      for (int w = 0; w < kLogitWaves; ++w) { s += sm_s[w][r]; m = fmaxf(m, sm_m[w][r]); }
-      const long long mi = static_cast<long long>(h) * sh.T + t;
-      ws.rowsum[p * ws.s_m + mi] = s;
-      ws.peak[p * ws.s_m + mi] = m;   // max_i e; scaled by the row weight later
+  const int r = threadIdx.x;
+  const bool row = r < 16 && lb.rb + r < lb.rows_g;
+  const long long mi = row ? lb.mrow(sh, r) : 0;
+  float s = 0.f, m = 0.f;
+  if (row)
+    for (int w = 0; w < W; ++w) { s += sm_s[w][r]; m = fmaxf(m, sm_m[w][r]); }
+  if (sh.lsplit == 1) {
+    if (row) {
+      ws.rowsum[lb.p * ws.s_m + mi] = s;
+      ws.peak[lb.p * ws.s_m + mi] = m;   // max_i e; scaled by the row weight later
     }
+    return;
   }
+  // the last of the row tile's ranges adds the range partials in range order
+  if (row) {
+    st_dev(&part[static_cast<long long>(2 * kLogitSplit + lb.split) * sh.mg + mi], s);
+    st_dev(&part[static_cast<long long>(3 * kLogitSplit + lb.split) * sh.mg + mi], m);
+  }
+  __shared__ int flag;
+  int* cnt = ws.lcnt + lb.p * ws.s_lcnt + (blockIdx.x / sh.lsplit) * sh.hkv + lb.g;
+  if (!last_arrival(cnt, sh.lsplit, &flag)) return;
+  if (row) {
+    float ts = 0.f, tm = 0.f;
+    for (int q = 0; q < sh.lsplit; ++q) {
+      ts += ld_dev(&part[static_cast<long long>(2 * kLogitSplit + q) * sh.mg + mi]);
+      tm = fmaxf(tm, ld_dev(&part[static_cast<long long>(3 * kLogitSplit + q) * sh.mg + mi]));
+    }
+    ws.rowsum[lb.p * ws.s_m + mi] = ts;
+    ws.peak[lb.p * ws.s_m + mi] = tm;
+  }
+  if (threadIdx.x == 0) st_dev(cnt, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -705,19 +799,20 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
     timer_mark(kStHeads, false, st);
     return hipGetLastError();
   }
-  const dim3 lg((sh.hg * sh.T + 15) / 16, sh.hkv, sh.B);
+  const dim3 lg((sh.hg * sh.T + 15) / 16 * sh.lsplit, sh.hkv, sh.B);
   const T* q = static_cast<const T*>(text_q_v);
   const T* k = static_cast<const T*>(vis_k_v);
   timer_mark(kStLogits, true, st);
   switch (sh.dh) {
-    case 32: hipLaunchKernelGGL((logits_kernel<T, 32>), lg, dim3(64 * logit_waves<T, 32>()), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 64: hipLaunchKernelGGL((logits_kernel<T, 64>), lg, dim3(64 * logit_waves<T, 64>()), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 96: hipLaunchKernelGGL((logits_kernel<T, 96>), lg, dim3(64 * logit_waves<T, 96>()), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 128: hipLaunchKernelGGL((logits_kernel<T, 128>), lg, dim3(64 * logit_waves<T, 128>()), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 160: hipLaunchKernelGGL((logits_kernel<T, 160>), lg, dim3(64 * logit_waves<T, 160>()), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 192: hipLaunchKernelGGL((logits_kernel<T, 192>), lg, dim3(64 * logit_waves<T, 192>()), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 224: hipLaunchKernelGGL((logits_kernel<T, 224>), lg, dim3(64 * logit_waves<T, 224>()), 0, st, sh, ws, q, k, nonvis_lse); break;
-    case 256: hipLaunchKernelGGL((logits_kernel<T, 256>), lg, dim3(64 * logit_waves<T, 256>()), 0, st, sh, ws, q, k, nonvis_lse); break;
+#define GMC_LOGITS(DH)                                                                                         \
+    case DH:                                                                                                   \
+      hipLaunchKernelGGL((logits_lse_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, ws, q, k); \
+      hipLaunchKernelGGL((logits_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, ws, q, k,       \
+                         nonvis_lse);                                                                          \
+      break;
+    GMC_LOGITS(32) GMC_LOGITS(64) GMC_LOGITS(96) GMC_LOGITS(128)
+    GMC_LOGITS(160) GMC_LOGITS(192) GMC_LOGITS(224) GMC_LOGITS(256)
+#undef GMC_LOGITS
     default: return hipErrorInvalidValue;
   }
   timer_mark(kStLogits, false, st);

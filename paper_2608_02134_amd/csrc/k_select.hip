@@ -1162,6 +1162,7 @@ __global__ void select_init_kernel(Shape sh, Ws ws) {
   }
   for (int j = x0; j < 128 * ((sh.m + 63) / 64); j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
   for (int j = x0; j < 2 * (sh.ldM + kMaxPersist); j += stride) ws.tc[p * ws.s_tc + j] = 0ull;
+  for (int j = x0; j < (sh.hg * sh.T + 15) / 16 * sh.hkv; j += stride) ws.lcnt[p * ws.s_lcnt + j] = 0;
   for (int i = x0; i < sh.N; i += stride) {
     ws.tu[p * ws.s_tu + i] = 0ull;
     ws.tu[p * ws.s_tu + sh.N + i] = 0ull;
