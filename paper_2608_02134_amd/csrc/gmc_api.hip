@@ -528,9 +528,7 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
     return GMC_OK;
   }
   const gmc_trace tr = trace ? *trace : gmc_trace{};
-  err = launch_call_init(s, c.ws, st);
-  if (err != hipSuccess) return fail(GMC_ERR_HIP, "call init: %s", hipGetErrorString(err));
-  // row norms, then the bank kernels on the side stream while the message
+  // per-call reset and row norms (one kernel), then the bank kernels on the side stream while the message
   // kernels run on the caller's stream (they write disjoint client rows).
   // With stage timing on, everything stays on one stream so each stage's
   // span measures that stage alone.

@@ -196,6 +196,33 @@ __device__ __forceinline__ floatx4 mma(const Frag<float>& a, const Frag<float>& 
 // 16-byte global<->LDS chunk copies (8 bf16 or 4 floats).
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+// Eight consecutive elements (16-byte aligned) as fp32, and back.
+template <typename T> __device__ __forceinline__ void load8_f32(const T* p, float* v);
+template <> __device__ __forceinline__ void load8_f32<bf16_t>(const bf16_t* p, float* v) {
+  const uint4 raw = ld16(p);
+  const bf16_t* b = reinterpret_cast<const bf16_t*>(&raw);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = bf16_to_f32(b[e]);
+}
+template <> __device__ __forceinline__ void load8_f32<float>(const float* p, float* v) {
+  const uint4 r0 = ld16(p), r1 = ld16(p + 4);
+  const float* a = reinterpret_cast<const float*>(&r0);
+  const float* b = reinterpret_cast<const float*>(&r1);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) { v[e] = a[e]; v[e + 4] = b[e]; }
+}
+template <typename T> __device__ __forceinline__ void store8_f32(T* p, const float* v);
+template <> __device__ __forceinline__ void store8_f32<bf16_t>(bf16_t* p, const float* v) {
+  uint4 raw;
+  bf16_t* b = reinterpret_cast<bf16_t*>(&raw);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) b[e] = f32_to_bf16(v[e]);
+  st16(p, raw);
+}
+template <> __device__ __forceinline__ void store8_f32<float>(float* p, const float* v) {
+  st16(p, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])));
+  st16(p + 4, make_uint4(__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]), __float_as_uint(v[7])));
+}
 
 // Device-coherent hand-off between blocks of one kernel.  Data another block
 // reads in the same launch is written with agent-scope relaxed atomic stores

@@ -79,8 +79,8 @@ struct Ws {
   int* sup;        long long s_sup;     // support, ascending           [N]
   float* cosb;     long long s_cos;     // cos to support               [N][ldK]
   float* delta;    long long s_del;     // selected-cosine gap          [N]
-  float* dpart;    long long s_dp;      // gap partial sums             [N/64+1]
   float* gate;     long long s_gate;    // s_x, mean gap                [4]
+  float* dpart;    long long s_dp;      // per-block energy partials    [N/4+1]
   int* pi;         long long s_pi;      // assignment                   [N]
   float* stats;    long long s_st;      // diagnostics                  [kStats]
   uint32_t* keys;  long long s_keys;    // top-k keys when N exceeds LDS [N]
@@ -94,5 +94,26 @@ struct Ws {
   unsigned long long* ts; long long s_ts;  // tagged score partials     [2][ceil(M/64)][64]
   unsigned long long* tc; long long s_tc;  // tagged coverage + heartbeats [2][ldM + kMaxPersist]
 };
+
+#ifdef __HIPCC__
+// Per-call state of problem p, over a grid-stride range (x0, stride): nothing
+// selected, coverage and row-weight padding zero, tagged hand-off buffers and
+// completion counters cleared.  Runs inside the first kernel of a call.
+__device__ __forceinline__ void call_init_range(const Shape& sh, const Ws& ws, int p, int x0, int stride) {
+  for (int i = x0; i < sh.N; i += stride) {
+    ws.sel[p * ws.s_sel + i] = -1;
+    ws.tu[p * ws.s_tu + i] = 0ull;
+    ws.tu[p * ws.s_tu + sh.N + i] = 0ull;
+  }
+  for (int m = x0; m < sh.ldM; m += stride) {
+    ws.cov[p * ws.s_cov + m] = 0.f;
+    if (m >= sh.m) ws.alpha[p * ws.s_m + m] = 0.f;
+  }
+  for (int j = x0; j < 128 * ((sh.m + 63) / 64); j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
+  for (int j = x0; j < 2 * (sh.ldM + kMaxPersist); j += stride) ws.tc[p * ws.s_tc + j] = 0ull;
+  for (int j = x0; j < (sh.hg * sh.T + 15) / 16 * sh.hkv; j += stride) ws.lcnt[p * ws.s_lcnt + j] = 0;
+  if (x0 < kCounters) ws.cnt[p * ws.s_cnt + x0] = 0;
+}
+#endif
 
 }  // namespace gmc

@@ -32,7 +32,6 @@ hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const v
                         const void* app_proj, const int32_t* pos3d, hipStream_t st);
 
 // Per-call state: nothing selected, completion counters cleared.
-hipError_t launch_call_init(const Shape& sh, const Ws& ws, hipStream_t st);
 
 // All selection rounds, then the final coverage and objective values.
 // *support_ready reports that the support list and slots were written too.

@@ -83,17 +83,12 @@ __device__ __forceinline__ CosSource<kFromE> cos_source(const Shape& sh, const P
 }
 
 // delta_i = top1 - top2 of cos_i. over the support (0 when K = 1); one wave
-// per token; per-block sums of delta over discarded tokens, reduced in block
-// order by the last block, which sets s_x = 1 - exp(-(mean delta / t)^p).
-constexpr int kCntGap = 6;   // completion counter of the gap kernel
+// per token.
 
 template <bool kFromE>
 __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
-  __shared__ float red[4], bred[16];
-  __shared__ int flag;
   const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = blockIdx.x * 4 + wave;
-  float contrib = 0.f;
   if (i < sh.N) {
     const CosSource<kFromE> cs = cos_source<kFromE>(sh, pr, ws, p, i);
     float t1 = -INFINITY, t2 = -INFINITY;
@@ -118,42 +113,55 @@ __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
     }
     const float delta = (sh.K >= 2) ? t1 - t2 : 0.f;
     if (lane == 0) ws.delta[p * ws.s_del + i] = delta;
-    if (ws.sel[p * ws.s_sel + i] < 0) contrib = delta;
   }
-  if (lane == 0) red[wave] = contrib;
-  __syncthreads();
-  float* dp = ws.dpart + p * ws.s_dp;
-  if (threadIdx.x == 0) st_dev(&dp[blockIdx.x], ((red[0] + red[1]) + red[2]) + red[3]);
-  // the last block: mean gap over discarded tokens and the separability gate
-  int* cnt = ws.cnt + p * ws.s_cnt;
-  if (!last_arrival(&cnt[kCntGap], gridDim.x, &flag)) return;
-  if (threadIdx.x == 0) st_dev(&cnt[kCntGap], 0);
+}
+
+// The separability gate s_x = 1 - exp(-(mean delta / t)^p) over the discarded
+// tokens, formed by every block from all the gaps (a fixed summation order,
+// so every block holds the same value); block 0 records it.
+__device__ float separability_gate(const Shape& sh, const Params& pr, const Ws& ws, int p, float* red) {
+  const float* delta = ws.delta + p * ws.s_del;
+  const int* sel = ws.sel + p * ws.s_sel;
   float s = 0.f;
-  for (unsigned b = threadIdx.x; b < gridDim.x; b += blockDim.x) s += ld_dev(&dp[b]);
-  s = block_sum(s, bred);
-  if (threadIdx.x == 0) {
-    const int nd = sh.N - sh.K;
-    const float dbar = nd > 0 ? s / static_cast<float>(nd) : 0.f;
-    const float sx = 1.f - expf(-powf(dbar / pr.gate_t, pr.gate_p));
+  for (int i0 = 0; i0 < sh.N; i0 += 256 * 8) {
+    float dv[8];
+    int sv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = min(i0 + q * 256 + static_cast<int>(threadIdx.x), sh.N - 1);
+      dv[q] = delta[i];
+      sv[q] = sel[i];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (i0 + q * 256 + static_cast<int>(threadIdx.x) < sh.N && sv[q] < 0) s += dv[q];
+  }
+  s = block_sum(s, red);
+  const int nd = sh.N - sh.K;
+  const float dbar = nd > 0 ? s / static_cast<float>(nd) : 0.f;
+  const float sx = 1.f - expf(-powf(dbar / pr.gate_t, pr.gate_p));
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
     ws.gate[p * ws.s_gate + 0] = sx;
     ws.gate[p * ws.s_gate + 1] = dbar;
     ws.stats[p * ws.s_st + 0] = sx;
     ws.stats[p * ws.s_st + 1] = dbar;
   }
+  return sx;
 }
 
 // pi(i) = argmax_j kappa_ij; one wave per token.
 template <bool kFromE>
 __global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, int32_t* trace_assign) {
+  __shared__ float red[16];
   const int p = blockIdx.y, lane = threadIdx.x & 63;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const float sx = separability_gate(sh, pr, ws, p, red);
   if (i >= sh.N) return;
   const int* sup = ws.sup + p * ws.s_sup;
   int pi_i;
   if (ws.sel[p * ws.s_sel + i] >= 0) {
     pi_i = i;
   } else {
-    const float sx = ws.gate[p * ws.s_gate];
     const float delta = ws.delta[p * ws.s_del + i];
     const float g = (pr.g_form == 1) ? (delta < pr.amb_margin ? 1.f : 0.f)
                                      : expf(-powf(delta / pr.amb_margin, pr.amb_p));

@@ -13,11 +13,14 @@
 namespace gmc {
 
 // ---------------------------------------------------------------------------
-// Squared row norms of the hidden states: one wave per token.
+// Squared row norms of the hidden states (one wave per token); the same
+// kernel resets the per-call state, being the first of every call.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* hidden) {
   const int p = blockIdx.y;
+  // the call's first kernel also resets the per-call state
+  call_init_range(sh, ws, p, blockIdx.x * 256 + threadIdx.x, gridDim.x * 256);
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= sh.N) return;
   const T* row = hidden + (static_cast<long long>(p) * sh.N + i) * sh.d;
@@ -65,11 +68,28 @@ struct ProbeSplitEpi {
 // Z_h[i] = rms(h_i)^-1 sum_s partial_s (the next block's RMSNorm, unit gain)
 // and q_h[i] = ||Z_h[i]||^2, stored in place of the atom norm: consumers form
 // l_h[i] = ||[Z_h[i]; sigma_h]|| = sqrt(q_h[i] + sigma_h^2).  One wave per
-// (head, 64 tokens), lane = token; per-(block, head) sums of q feed
-// sigma_h = sqrt(lambda) max(sqrt(sum q / (N r)), eps), formed by the last
-// block in block order.
+// (head, 64 tokens), lane = token; per-(block, head) sums of q are left for
+// sigma_h = sqrt(lambda) max(sqrt(sum q / (N r)), eps), which the first
+// block of the next kernel forms (sigma_from_partials).
+// sigma_h from the per-(token block, head) sums of q, in token-block order.
+__device__ void sigma_from_partials(const Shape& sh, const Params& pr, const Ws& ws, int p) {
+  if (threadIdx.x >= sh.hq) return;
+  const int hh = threadIdx.x, nb = (sh.N + 63) / 64;
+  const float* part = ws.gpart + p * ws.s_gpart;
+  float sum = 0.f;
+  for (int b0 = 0; b0 < nb; b0 += 16) {
+    float t[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) t[k] = part[min(b0 + k, nb - 1) * sh.hq + hh];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (b0 + k < nb) sum += t[k];
+  }
+  const float mean2 = sum / (static_cast<float>(sh.N) * sh.r);
+  ws.sig[p * ws.s_sig + hh] = sqrtf(pr.lambda_mass) * fmaxf(sqrtf(mean2), pr.eps_mass);
+}
+
 __global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws ws, int ksplit) {
-  __shared__ int flag;
   const int p = blockIdx.z, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int h = blockIdx.y * 4 + wave;
   const int i = blockIdx.x * 64 + lane;
@@ -98,24 +118,7 @@ __global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws 
     }
     if (i < sh.N) ws.ell[p * ws.s_ell + static_cast<long long>(h) * sh.N + i] = q;
     const float bq = wave_sum(i < sh.N ? q : 0.f);
-    if (lane == 0) st_dev(&part[blockIdx.x * sh.hq + h], bq);
-  }
-  int* cnt = ws.cnt + p * ws.s_cnt;
-  if (!last_arrival(&cnt[1], gridDim.x * gridDim.y, &flag)) return;
-  if (threadIdx.x == 0) st_dev(&cnt[1], 0);
-  if (threadIdx.x < sh.hq) {
-    const int hh = threadIdx.x;
-    float sum = 0.f;
-    for (unsigned b0 = 0; b0 < gridDim.x; b0 += 16) {
-      float t[16];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) t[k] = ld_dev(&part[min(b0 + k, gridDim.x - 1) * sh.hq + hh]);
-#pragma unroll
-      for (int k = 0; k < 16; ++k)
-        if (b0 + k < gridDim.x) sum += t[k];
-    }
-    const float mean2 = sum / (static_cast<float>(sh.N) * sh.r);
-    ws.sig[p * ws.s_sig + hh] = sqrtf(pr.lambda_mass) * fmaxf(sqrtf(mean2), pr.eps_mass);
+    if (lane == 0) part[blockIdx.x * sh.hq + h] = bq;
   }
 }
 
@@ -210,7 +213,7 @@ struct LogitBlock {
 
 template <typename T, int DH>
 __global__ void __launch_bounds__((64 * logit_waves<T, DH>()))
-logits_lse_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k) {
+logits_lse_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k) {
   constexpr int W = logit_waves<T, DH>(), MT = logit_chunk<T, DH>(), KS = DH / 32;
   __shared__ float sm_m[W][16], sm_s[W][16];
   const LogitBlock<T, DH> lb(sh, text_q, vis_k);
@@ -263,6 +266,9 @@ logits_lse_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k) {
       part[static_cast<long long>(kLogitSplit + lb.split) * sh.mg + mi] = s;
     }
   }
+  // one spare job for the problem's first block: the mass coordinates, needed
+  // from the next kernel on
+  if (blockIdx.x == 0 && blockIdx.y == 0) sigma_from_partials(sh, pr, ws, lb.p);
 }
 
 template <typename T, int DH>
@@ -744,7 +750,7 @@ __global__ void __launch_bounds__(256) energy_kernel(Shape sh, Ws ws) {
     ws.ebar[p * ws.s_eb + i] = e;
   }
   const float bs = block_sum(e, red);
-  float* ep = ws.dpart + p * ws.s_dp;   // free until the assignment stage
+  float* ep = ws.dpart + p * ws.s_dp;
   if (tid == 0) st_dev(&ep[blockIdx.x], bs);
   int* cnt = ws.cnt + p * ws.s_cnt + 3;
   if (!last_arrival(cnt, gridDim.x, &flag)) return;
@@ -806,7 +812,7 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   switch (sh.dh) {
 #define GMC_LOGITS(DH)                                                                                         \
     case DH:                                                                                                   \
-      hipLaunchKernelGGL((logits_lse_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, ws, q, k); \
+      hipLaunchKernelGGL((logits_lse_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, pr, ws, q, k); \
       hipLaunchKernelGGL((logits_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, ws, q, k,       \
                          nonvis_lse);                                                                          \
       break;

@@ -1150,26 +1150,6 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
   }
 }
 
-// Per-call state: nothing selected, coverage and row-weight padding zero,
-// completion counters cleared.
-__global__ void select_init_kernel(Shape sh, Ws ws) {
-  const int p = blockIdx.y;
-  const int x0 = blockIdx.x * blockDim.x + threadIdx.x, stride = gridDim.x * blockDim.x;
-  for (int i = x0; i < sh.N; i += stride) ws.sel[p * ws.s_sel + i] = -1;
-  for (int m = x0; m < sh.ldM; m += stride) {
-    ws.cov[p * ws.s_cov + m] = 0.f;
-    if (m >= sh.m) ws.alpha[p * ws.s_m + m] = 0.f;
-  }
-  for (int j = x0; j < 128 * ((sh.m + 63) / 64); j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
-  for (int j = x0; j < 2 * (sh.ldM + kMaxPersist); j += stride) ws.tc[p * ws.s_tc + j] = 0ull;
-  for (int j = x0; j < (sh.hg * sh.T + 15) / 16 * sh.hkv; j += stride) ws.lcnt[p * ws.s_lcnt + j] = 0;
-  for (int i = x0; i < sh.N; i += stride) {
-    ws.tu[p * ws.s_tu + i] = 0ull;
-    ws.tu[p * ws.s_tu + sh.N + i] = 0ull;
-  }
-  if (blockIdx.x == 0 && threadIdx.x < kCounters) ws.cnt[p * ws.s_cnt + threadIdx.x] = 0;
-}
-
 // F(S) = sum_m b_m(S) and F(V) = sum_m max_i Cbar_mi via per-block partials
 // reduced in order by the last block.
 __global__ void __launch_bounds__(256) objective_kernel(Shape sh, Ws ws) {
@@ -1205,11 +1185,6 @@ __global__ void __launch_bounds__(256) objective_kernel(Shape sh, Ws ws) {
   }
 }
 
-hipError_t launch_call_init(const Shape& sh, const Ws& ws, hipStream_t st) {
-  const int n = max(sh.N, sh.ldM);
-  hipLaunchKernelGGL(select_init_kernel, dim3((n + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
-  return hipGetLastError();
-}
 
 static void launch_cov(const Shape& sh, const Ws& ws, int nb, hipStream_t st) {
   hipLaunchKernelGGL(cov_kernel, dim3((sh.m + 255) / 256, (nb + kCovCols - 1) / kCovCols, sh.B), dim3(256), 0,

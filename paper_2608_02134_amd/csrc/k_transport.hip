@@ -19,13 +19,16 @@ template <typename T, int G>
 __global__ void __launch_bounds__(256)
 transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos3d, T* out_hidden,
                  int32_t* out_pos, int32_t* out_idx) {
-  constexpr int kMB = 8;                  // member rows loaded together
   constexpr int CH = sizeof(T) == 2 ? 1 : 2;   // 16-byte chunks per 8-element group
-  __shared__ unsigned long long masks[4];
-  __shared__ int members[256];
+  // member rows loaded together (about 128 registers of row data)
+  constexpr int kMB = 128 / (G * CH * 4) < 1 ? 1 : (128 / (G * CH * 4) > 8 ? 8 : 128 / (G * CH * 4));
+  constexpr int kPiQ = 8;                 // assignment entries per thread and pass
+  __shared__ unsigned long long masks[kPiQ][4];
+  __shared__ int members[kPiQ * 256];
   __shared__ float red[16];
   const int jj = blockIdx.x, p = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned long long below = (1ull << lane) - 1ull;
   const int j = ws.sup[p * ws.s_sup + jj];
   const int* pi = ws.pi + p * ws.s_pi;
   const float* eb = ws.ebar + p * ws.s_eb;
@@ -40,21 +43,32 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
   float mass = 0.f;
-  for (int i0 = 0; i0 < sh.N; i0 += 256) {
-    // ordered member list of this chunk (ascending source index)
-    const int i = i0 + tid;
-    const bool member = i < sh.N && pi[i] == j;
-    const unsigned long long bal = __ballot(member);
-    __syncthreads();
-    if (lane == 0) masks[wave] = bal;
-    __syncthreads();
-    int before = 0, total = 0;
-    for (int w = 0; w < 4; ++w) {
-      const int c = __popcll(masks[w]);
-      if (w < wave) before += c;
-      total += c;
+  for (int base = 0; base < sh.N; base += kPiQ * 256) {
+    // the ordered member list of this pass (ascending source index): every
+    // assignment load in flight, one ballot per 256 tokens
+    int pv[kPiQ];
+#pragma unroll
+    for (int q = 0; q < kPiQ; ++q) {
+      const int i = base + q * 256 + tid;
+      pv[q] = i < sh.N ? pi[i] : -1;
     }
-    if (member) members[before + __popcll(bal & ((1ull << lane) - 1ull))] = i;
+    unsigned long long bal[kPiQ];
+#pragma unroll
+    for (int q = 0; q < kPiQ; ++q) bal[q] = __ballot(pv[q] == j);
+    __syncthreads();   // the previous pass is done with masks and members
+    if (lane == 0)
+#pragma unroll
+      for (int q = 0; q < kPiQ; ++q) masks[q][wave] = bal[q];
+    __syncthreads();
+    int total = 0;
+#pragma unroll
+    for (int q = 0; q < kPiQ; ++q)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int c = __popcll(masks[q][w]);
+        if (w == wave && ((bal[q] >> lane) & 1ull)) members[total + __popcll(bal[q] & below)] = base + q * 256 + tid;
+        total += c;
+      }
     __syncthreads();
     for (int b0 = 0; b0 < total; b0 += kMB) {
       // all member rows of the batch are loaded before any accumulation
@@ -62,7 +76,8 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
       float mi[kMB];
 #pragma unroll
       for (int q = 0; q < kMB; ++q) {
-        const int ii = members[min(b0 + q, total - 1)];
+        if (b0 + q >= total) break;
+        const int ii = members[b0 + q];
         mi[q] = m0 + m1 * (inv_mean > 0.f ? eb[ii] * inv_mean : 1.f);
         const T* row = H + static_cast<long long>(ii) * sh.d;
 #pragma unroll
@@ -100,10 +115,11 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
   for (int g = 0; g < G; ++g) {
     const int grp = tid + g * 256;
     if (grp < ngroups) {
+      float hv[8];
+      load8_f32<T>(hj + grp * 8, hv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float hv = to_f32<T>(hj[grp * 8 + e]);
-        const float v = (1.f - pr.tau_j) * hv + pr.tau_j * (acc[g][e] * inv_mass);
+        const float v = (1.f - pr.tau_j) * hv[e] + pr.tau_j * (acc[g][e] * inv_mass);
         acc[g][e] = v;
         ss += v * v;
       }
@@ -118,8 +134,10 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
   for (int g = 0; g < G; ++g) {
     const int grp = tid + g * 256;
     if (grp < ngroups) {
+      float v[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) out[grp * 8 + e] = from_f32<T>(acc[g][e] * scale);
+      for (int e = 0; e < 8; ++e) v[e] = acc[g][e] * scale;
+      store8_f32<T>(out + grp * 8, v);
     }
   }
   if (tid < 3) {
