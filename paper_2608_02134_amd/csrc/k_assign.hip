@@ -82,8 +82,10 @@ __device__ __forceinline__ CosSource<kFromE> cos_source(const Shape& sh, const P
   return c;
 }
 
-// delta_i = top1 - top2 of cos_i. over the support (0 when K = 1); one wave
-// per token.
+// delta_i = top1 - top2 of cos_i. over the support (0 when K = 1), and the
+// token's grounded energy e_i = sqrt(sum_h omega_h sum_t nu_t e^2) (Eq.
+// cond-grounded-energy; the head-pattern kernel left sum_t nu_t e^2 per head);
+// one wave per token.
 
 template <bool kFromE>
 __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
@@ -113,30 +115,48 @@ __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
     }
     const float delta = (sh.K >= 2) ? t1 - t2 : 0.f;
     if (lane == 0) ws.delta[p * ws.s_del + i] = delta;
+    if (sh.T > 0) {
+      // lane h holds head h (at most kMaxHeads of them)
+      const float w = lane < sh.hq ? ws.omega[p * ws.s_om + lane] * ws.e2[p * ws.s_e2 + static_cast<long long>(lane) * sh.N + i] : 0.f;
+      const float e = sqrtf(wave_sum(w));
+      if (lane == 0) ws.ebar[p * ws.s_eb + i] = e;
+    }
   }
 }
 
 // The separability gate s_x = 1 - exp(-(mean delta / t)^p) over the discarded
-// tokens, formed by every block from all the gaps (a fixed summation order,
-// so every block holds the same value); block 0 records it.
+// tokens and 1 / mean e (the population weights' normaliser; 0 selects the
+// uniform fallback ebar = 1), formed by every block from all tokens (a fixed
+// summation order, so every block holds the same values); block 0 records
+// them.
 __device__ float separability_gate(const Shape& sh, const Params& pr, const Ws& ws, int p, float* red) {
   const float* delta = ws.delta + p * ws.s_del;
+  const float* eb = ws.ebar + p * ws.s_eb;
   const int* sel = ws.sel + p * ws.s_sel;
-  float s = 0.f;
+  float s = 0.f, se = 0.f;
   for (int i0 = 0; i0 < sh.N; i0 += 256 * 8) {
-    float dv[8];
+    float dv[8], ev[8];
     int sv[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const int i = min(i0 + q * 256 + static_cast<int>(threadIdx.x), sh.N - 1);
       dv[q] = delta[i];
+      ev[q] = eb[i];
       sv[q] = sel[i];
     }
 #pragma unroll
     for (int q = 0; q < 8; ++q)
-      if (i0 + q * 256 + static_cast<int>(threadIdx.x) < sh.N && sv[q] < 0) s += dv[q];
+      if (i0 + q * 256 + static_cast<int>(threadIdx.x) < sh.N) {
+        if (sv[q] < 0) s += dv[q];
+        se += ev[q];
+      }
   }
   s = block_sum(s, red);
+  se = block_sum(se, red);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const float mean = se / static_cast<float>(sh.N);
+    ws.gate[p * ws.s_gate + 2] = mean > 0.f ? 1.f / mean : 0.f;
+  }
   const int nd = sh.N - sh.K;
   const float dbar = nd > 0 ? s / static_cast<float>(nd) : 0.f;
   const float sx = 1.f - expf(-powf(dbar / pr.gate_t, pr.gate_p));

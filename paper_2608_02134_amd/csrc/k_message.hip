@@ -557,14 +557,16 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
 #pragma unroll
     for (int e = 0; e < 4; ++e) red[wave * 768 + tl * 256 + e * 64 + lane] = acc[tl][e];
   __syncthreads();
-  float* gp = ws.gpart + p * ws.s_gpart + static_cast<long long>(blockIdx.x) * sh.npairs;
+  // pair-major partials, rows padded to a multiple of four blocks
+  const long long nbp = (sh.n_head_blk + 3) & ~3;
+  float* gp = ws.gpart + p * ws.s_gpart + blockIdx.x;
   for (int x = tid; x < 768; x += 256) {
     const int tl = x / 256, e = (x / 64) % 4, l = x % 64;
     const int hb = tl == 2 ? 1 : 0, gb = tl == 0 ? 0 : 1;
     const int hh = 16 * hb + 4 * (l >> 4) + e, gg = 16 * gb + (l & 15);
     if (hh <= gg && gg < H) {
       const float v = ((red[x] + red[768 + x]) + red[2 * 768 + x]) + red[3 * 768 + x];
-      gp[hh * H - hh * (hh - 1) / 2 + (gg - hh)] = v;
+      gp[(hh * H - hh * (hh - 1) / 2 + (gg - hh)) * nbp] = v;
     }
   }
 }
@@ -585,67 +587,91 @@ __device__ __forceinline__ void wave_argbest(float& v, int& idx, bool want_max) 
   }
 }
 
-__global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
+// One block per problem, so occupancy is irrelevant: the register budget goes
+// to keeping every independent load in flight.
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2)))
+cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
+  constexpr int kGB = 32;        // float4 partial loads in flight per pair slot
+  constexpr int kRW = 4;         // grounded rows per thread and pass of the row weights
   __shared__ float gam[kMaxHeads][kMaxHeads + 1];
   __shared__ float cosm[kMaxHeads][kMaxHeads + 1];
   __shared__ float om[kMaxHeads];
   __shared__ int asg[kMaxHeads];
   const int p = blockIdx.x, tid = threadIdx.x, H = sh.hq, T = sh.T;
   const float* gp = ws.gpart + p * ws.s_gpart;
-  const int nb = sh.n_head_blk;
-  // every thread sums two pair slots over the block partials in block order,
-  // 32 blocks of loads in flight per slot
-  {
-    float s0 = 0.f, s1 = 0.f;
-    const int q0 = min(tid, sh.npairs - 1), q1 = min(tid + 256, sh.npairs - 1);
-    for (int b0 = 0; b0 < nb; b0 += 32) {
-      float v0[32], v1[32];
-#pragma unroll
-      for (int j = 0; j < 32; ++j) {
-        const long long b = min(b0 + j, nb - 1);
-        v0[j] = gp[b * sh.npairs + q0];
-        v1[j] = gp[b * sh.npairs + q1];
-      }
-#pragma unroll
-      for (int j = 0; j < 32; ++j)
-        if (b0 + j < nb) { s0 += v0[j]; s1 += v1[j]; }
-    }
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int q = tid + 256 * k;
-      if (q < sh.npairs) {
-        int h = 0, rem = q;
-        while (rem >= H - h) { rem -= H - h; ++h; }
-        const int g = h + rem;
-        gam[h][g] = k ? s1 : s0;
-        gam[g][h] = k ? s1 : s0;
-      }
-    }
-  }
-  __syncthreads();
   const float* rowsum = ws.rowsum + p * ws.s_m;
-  if (tid < 64) {
-    const int lane = tid, h = lane;
-    const bool valid = h < H;
-    // mean atom norm abar_h = sum_t Z_(h,t) / (T N) and activity
-    float abar = 0.f;
-    for (int t0 = 0; t0 < T; t0 += 64) {
-      float rv[64];
+  const int nb = sh.n_head_blk, nbp = (nb + 3) & ~3;
+  // loads that do not depend on Gamma go out first: the first pass of the
+  // grounded row weights (row sums and maxima) and, in wave 0, the per-head
+  // row sums of the mean atom norm
+  float zv0[kRW], pv0[kRW];
 #pragma unroll
-      for (int t = 0; t < 64; ++t) rv[t] = rowsum[min(h, H - 1) * T + min(t0 + t, T - 1)];
+  for (int k = 0; k < kRW; ++k) {
+    const int m = min(k * 512 + tid, sh.mg - 1);
+    zv0[k] = rowsum[m];
+    pv0[k] = ws.peak[p * ws.s_m + m];
+  }
+  // (the first 64 queries of a head are loaded now and added after Gamma)
+  float rv[64];
+  if (tid < 64) {
+    const int h = min(tid, H - 1);
+#pragma unroll
+    for (int t = 0; t < 64; ++t) rv[t] = rowsum[h * T + min(t, T - 1)];
+  }
+  // Gamma: one thread per pair slot sums its block partials (contiguous,
+  // pair-major) in block order
+  for (int q = tid; q < sh.npairs; q += 512) {
+    const float* row = gp + static_cast<long long>(q) * nbp;
+    float s = 0.f;
+    for (int b0 = 0; b0 < nb; b0 += 4 * kGB) {
+      float4 v[kGB];
+#pragma unroll
+      for (int j = 0; j < kGB; ++j) v[j] = *reinterpret_cast<const float4*>(row + min(b0 + 4 * j, nbp - 4));
+      __builtin_amdgcn_sched_barrier(0);   // every load issued before the first add
+#pragma unroll
+      for (int j = 0; j < kGB; ++j) {
+        const int b = b0 + 4 * j;
+        if (b < nb) s += v[j].x;
+        if (b + 1 < nb) s += v[j].y;
+        if (b + 2 < nb) s += v[j].z;
+        if (b + 3 < nb) s += v[j].w;
+      }
+    }
+    int h = 0, rem = q;
+    while (rem >= H - h) { rem -= H - h; ++h; }
+    const int g = h + rem;
+    gam[h][g] = s;
+    gam[g][h] = s;
+  }
+  float abar = 0.f;
+  if (tid < 64) {
+    const int h = min(tid, H - 1);
+#pragma unroll
+    for (int t = 0; t < 64; ++t)
+      if (t < T) abar += rv[t];
+    for (int t0 = 64; t0 < T; t0 += 64) {
+#pragma unroll
+      for (int t = 0; t < 64; ++t) rv[t] = rowsum[h * T + min(t0 + t, T - 1)];
 #pragma unroll
       for (int t = 0; t < 64; ++t)
         if (t0 + t < T) abar += rv[t];
     }
+  }
+  __syncthreads();
+  // cosines of the head patterns, all threads
+  for (int x = tid; x < H * H; x += 512) {
+    const int h = x / H, g = x % H;
+    const float hh = gam[h][h], gg = gam[g][g];
+    cosm[h][g] = gam[h][g] / ((hh > 0.f ? sqrtf(hh) : 1.f) * (gg > 0.f ? sqrtf(gg) : 1.f));
+  }
+  __syncthreads();
+  if (tid < 64) {
+    const int lane = tid, h = lane;
+    const bool valid = h < H;
+    // mean atom norm abar_h = sum_t Z_(h,t) / (T N) and activity
     abar = valid ? abar / (static_cast<float>(T) * sh.N) : 0.f;
     const float ghh = valid ? gam[h][h] : 0.f;
     const bool active = valid && ghh > 0.f;
-    const float nrm = active ? sqrtf(ghh) : 1.f;
-    if (valid)
-      for (int g = 0; g < H; ++g) {
-        const float gg = gam[g][g];
-        cosm[h][g] = gam[h][g] / (nrm * (gg > 0.f ? sqrtf(gg) : 1.f));
-      }
     const int n_active = __popcll(__ballot(active));
     float w_h = 0.f;
     int cl = -1;
@@ -707,17 +733,22 @@ __global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws
   __syncthreads();
   // grounded row weights beta_msg omega_h nu_t a_(h,t) / Z_(h,t)
   const float nu_o = 1.f / (T - 1 + pr.terminal_q_weight);
-  for (int m0 = 0; m0 < sh.mg; m0 += 256 * 8) {
-    float zv[8], pv[8];
+  for (int m0 = 0; m0 < sh.mg; m0 += 512 * kRW) {
+    float zv[kRW], pv[kRW];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int m = min(m0 + k * 256 + tid, sh.mg - 1);
-      zv[k] = rowsum[m];
-      pv[k] = ws.peak[p * ws.s_m + m];
+    for (int k = 0; k < kRW; ++k) {
+      if (m0 == 0) {
+        zv[k] = zv0[k];
+        pv[k] = pv0[k];
+      } else {
+        const int m = min(m0 + k * 512 + tid, sh.mg - 1);
+        zv[k] = rowsum[m];
+        pv[k] = ws.peak[p * ws.s_m + m];
+      }
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int m = m0 + k * 256 + tid;
+    for (int k = 0; k < kRW; ++k) {
+      const int m = m0 + k * 512 + tid;
       if (m < sh.mg) {
         const int h = m / T, t = m % T;
         const float nu = (t == T - 1) ? pr.terminal_q_weight * nu_o : nu_o;
@@ -726,41 +757,6 @@ __global__ void __launch_bounds__(256) cluster_kernel(Shape sh, Params pr, Ws ws
         ws.peak[p * ws.s_m + m] = pv[k] * a;
       }
     }
-  }
-}
-
-// Grounded energy e_i = sqrt(sum_h omega_h sum_t nu_t e^2) for every token
-// (Eq. cond-grounded-energy) with per-block sums; the last block forms the
-// mean and stores 1/mean (0 selects the uniform fallback ebar = 1).
-__global__ void __launch_bounds__(256) energy_kernel(Shape sh, Ws ws) {
-  __shared__ float red[16];
-  __shared__ float om[kMaxHeads];
-  __shared__ int flag;
-  const int p = blockIdx.y, tid = threadIdx.x;
-  if (tid < sh.hq) om[tid] = ws.omega[p * ws.s_om + tid];
-  __syncthreads();
-  const int i = blockIdx.x * 256 + tid;
-  float e = 0.f;
-  if (i < sh.N) {
-    const float* e2 = ws.e2 + p * ws.s_e2;
-    float s = 0.f;
-#pragma unroll 8
-    for (int h = 0; h < sh.hq; ++h) s += om[h] * e2[static_cast<long long>(h) * sh.N + i];
-    e = sqrtf(s);
-    ws.ebar[p * ws.s_eb + i] = e;
-  }
-  const float bs = block_sum(e, red);
-  float* ep = ws.dpart + p * ws.s_dp;
-  if (tid == 0) st_dev(&ep[blockIdx.x], bs);
-  int* cnt = ws.cnt + p * ws.s_cnt + 3;
-  if (!last_arrival(cnt, gridDim.x, &flag)) return;
-  if (tid == 0) {
-    st_dev(cnt, 0);
-    float s = 0.f;
-#pragma unroll 8
-    for (unsigned b = 0; b < gridDim.x; ++b) s += ld_dev(&ep[b]);
-    const float mean = s / static_cast<float>(sh.N);
-    ws.gate[p * ws.s_gate + 2] = (mean > 0.f) ? 1.f / mean : 0.f;
   }
 }
 
@@ -774,7 +770,6 @@ __global__ void no_grounded_kernel(Shape sh, Ws ws, float* trace_omega) {
       ws.omega[p * ws.s_om + h] = 0.f;
       if (trace_omega) trace_omega[static_cast<long long>(p) * sh.hq + h] = 0.f;
     }
-    if (threadIdx.x == 0) ws.gate[p * ws.s_gate + 2] = 1.f;
   }
 }
 
@@ -831,8 +826,7 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
 #undef GMC_HEADGRAM
     default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(256), 0, st, sh, pr, ws, trace_omega);
-  hipLaunchKernelGGL(energy_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
+  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(512), 0, st, sh, pr, ws, trace_omega);
   timer_mark(kStHeads, false, st);
   return hipGetLastError();
 }
