@@ -5,8 +5,9 @@
 // projected states, states x selected states).  Rows may be gathered through
 // an index list.  A block of 256 threads (4 waves, 2x2) computes a BM x BN
 // tile; each wave owns (BM/2) x (BN/2) as 16x16 MFMA tiles.  K advances in
-// slabs of 64: global loads run two slabs ahead in two register stages,
-// the LDS tile is double-buffered, one barrier per slab.  Row indices are
+// slabs of 64: global loads run kStages slabs ahead in register stages (so a
+// slab's loads have kStages - 1 slabs of MFMA work to arrive), the LDS tile is
+// double-buffered, one barrier per slab.  Row indices are
 // clamped so every load is unconditional; out-of-range rows and columns are
 // masked in the epilogue.  The epilogue functor gets a per-row and a
 // per-column scale (loaded once per lane) and sees every valid element; it may
@@ -33,6 +34,10 @@ struct RowOperand {
 
 constexpr int kGemmThreads = 256;
 constexpr int kBK = 64;
+// register stages of the slab pipeline: eight 16-byte chunks per thread and
+// stage cost 32 registers, so fp32 operands (twice the chunks) get half
+template <typename T>
+constexpr int gemm_stages() { return sizeof(T) == 2 ? 8 : 4; }
 
 // Epilogue contract (p is the problem index, or problem * ksplit + split):
 //   static constexpr bool kRowStats;
@@ -77,7 +82,8 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, int ksplit, Epi epi) {
     const int ch = tid + i * kGemmThreads, r = ch / CPR, kc = (ch % CPR) * EPC;
     b_src[i] = B.row(p, min(col0 + r, B.rows - 1)) + ks0 + kc;
   }
-  uint4 ra0[A_CHUNKS], rb0[B_CHUNKS], ra1[A_CHUNKS], rb1[B_CHUNKS];
+  constexpr int S = gemm_stages<T>();
+  uint4 ra[S][A_CHUNKS], rb[S][B_CHUNKS];
   const int nk = K / kBK;
   auto load = [&](int kt, uint4* ra, uint4* rb) {
     const int k0 = min(kt, nk - 1) * kBK;
@@ -121,23 +127,24 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, int ksplit, Epi epi) {
     }
   };
 
-  // prologue: slab 0 in LDS buffer 0, slab 1 in flight in registers
-  load(0, ra0, rb0);
-  load(1, ra1, rb1);
-  store(0, ra0, rb0);
+  // prologue: slabs 0..S-1 in flight, slab 0 in LDS buffer 0
+#pragma unroll
+  for (int s = 0; s < S; ++s) load(s, ra[s], rb[s]);
+  store(0, ra[0], rb[0]);
   __syncthreads();
-  // steady state, unrolled by two so the register stages are static:
-  // compute slab kt from LDS while slab kt+2 loads; then slab kt+1 goes to LDS
-  for (int kt = 0; kt < nk; kt += 2) {
-    load(kt + 2, ra0, rb0);
-    compute(0);
-    store(1, ra1, rb1);      // past the last slab this stores a clamped copy, never read
-    __syncthreads();
-    if (kt + 1 >= nk) break;
-    load(kt + 3, ra1, rb1);
-    compute(1);
-    store(0, ra0, rb0);
-    __syncthreads();
+  // steady state, unrolled by S so the register stages are static: step s
+  // computes slab kt+s from LDS buffer s&1, refills its now free stage with
+  // slab kt+s+S and moves slab kt+s+1 into the other buffer (past the last
+  // slab these are clamped copies, never read)
+  for (int kt = 0; kt < nk; kt += S) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      if (kt + s >= nk) break;
+      load(kt + s + S, ra[s], rb[s]);
+      compute(s & 1);
+      store((s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
+      __syncthreads();
+    }
   }
 
   // epilogue: lane holds column (lane&15), rows 4*(lane>>4)+e of each tile

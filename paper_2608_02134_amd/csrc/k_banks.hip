@@ -79,7 +79,8 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
     a_src[q] = base + static_cast<long long>(min(row0 + r, sh.N - 1)) * sh.d + kc;
     b_src[q] = base + static_cast<long long>(min(col0 + r, sh.N - 1)) * sh.d + kc;
   }
-  uint4 ra0[CH], rb0[CH], ra1[CH], rb1[CH];
+  constexpr int S = gemm_stages<T>();
+  uint4 ra[S][CH], rb[S][CH];
   const int nk = sh.d / kBK;
   auto load = [&](int kt, uint4* ra, uint4* rb) {
     const int k0 = min(kt, nk - 1) * kBK;
@@ -114,20 +115,20 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
         for (int j = 0; j < TM; ++j) acc[i][j] = mma(fa[i], fb[j], acc[i][j]);
     }
   };
-  load(0, ra0, rb0);
-  load(1, ra1, rb1);
-  store(0, ra0, rb0);
+  // the GEMM core's slab pipeline: S register stages, double-buffered LDS
+#pragma unroll
+  for (int s = 0; s < S; ++s) load(s, ra[s], rb[s]);
+  store(0, ra[0], rb[0]);
   __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    load(kt + 2, ra0, rb0);
-    compute(0);
-    store(1, ra1, rb1);
-    __syncthreads();
-    if (kt + 1 >= nk) break;
-    load(kt + 3, ra1, rb1);
-    compute(1);
-    store(0, ra0, rb0);
-    __syncthreads();
+  for (int kt = 0; kt < nk; kt += S) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      if (kt + s >= nk) break;
+      load(kt + s + S, ra[s], rb[s]);
+      compute(s & 1);
+      store((s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
+      __syncthreads();
+    }
   }
 
   // epilogue: lane holds column (lane & 15), rows 4 (lane >> 4) + e of each

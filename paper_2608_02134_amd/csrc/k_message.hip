@@ -161,11 +161,11 @@ struct LogitBlock {
   long long kstride;
   Frag<T> qf[KS];
 
-  __device__ LogitBlock(const Shape& sh, const T* text_q, const T* vis_k) {
+  __device__ LogitBlock(const Shape& sh, const T* text_q, const T* vis_k, int lsplit) {
     p = blockIdx.z;
     g = blockIdx.y;
-    rb = (blockIdx.x / sh.lsplit) * 16;
-    split = blockIdx.x % sh.lsplit;
+    rb = (blockIdx.x / lsplit) * 16;
+    split = blockIdx.x % lsplit;
     rows_g = sh.hg * sh.T;
     lane = threadIdx.x & 63;
     wave = threadIdx.x >> 6;
@@ -174,7 +174,7 @@ struct LogitBlock {
     orow = (lane >> 4) * 4;
     oc = lane & 15;
     scale = rsqrtf(static_cast<float>(DH));
-    const int ntile = (sh.N + 15) / 16, tps = (ntile + sh.lsplit - 1) / sh.lsplit;
+    const int ntile = (sh.N + 15) / 16, tps = (ntile + lsplit - 1) / lsplit;
     t_beg = min(ntile, split * tps);
     t_end = min(ntile, t_beg + tps);
     const int rr = rb + fr;
@@ -216,7 +216,7 @@ __global__ void __launch_bounds__((64 * logit_waves<T, DH>()))
 logits_lse_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k) {
   constexpr int W = logit_waves<T, DH>(), MT = logit_chunk<T, DH>(), KS = DH / 32;
   __shared__ float sm_m[W][16], sm_s[W][16];
-  const LogitBlock<T, DH> lb(sh, text_q, vis_k);
+  const LogitBlock<T, DH> lb(sh, text_q, vis_k, sh.lsplit);
   // online (max, sum exp) per row, lane-local over its columns
   float mx[4], sm[4];
 #pragma unroll
@@ -277,7 +277,7 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   constexpr int W = logit_waves<T, DH>(), MT = logit_chunk<T, DH>(), KS = DH / 32;
   __shared__ float sm_m[W][16], sm_s[W][16];
   __shared__ float sm_D[16];
-  const LogitBlock<T, DH> lb(sh, text_q, vis_k);
+  const LogitBlock<T, DH> lb(sh, text_q, vis_k, sh.lsplit);
   float* part = ws.lpart + lb.p * ws.s_lpart;
   if (threadIdx.x < 16) {
     // the row's log-sum-exp from the per-range partials, in range order
@@ -413,6 +413,180 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
     ws.peak[lb.p * ws.s_m + mi] = tm;
   }
   if (threadIdx.x == 0) st_dev(cnt, 0);
+}
+
+// Small N: a block keeps its 16 rows' logits over every column in registers
+// (at most MAXT tiles per wave), so the keys are read once, the log-sum-exp is
+// reduced inside the block, and e is written with 16-byte stores; the mass
+// coordinates of the block's heads are formed from the probe partials first.
+constexpr int kLogitRegTiles = 12;   // tiles per wave held in registers
+// configurations whose query and key fragments leave room for the tiles
+template <typename T, int DH>
+constexpr bool logit_reg_ok() {
+  return logit_waves<T, DH>() == 8 && (DH / 32) * static_cast<int>(sizeof(Frag<T>) / 4) <= 32;
+}
+
+template <typename T, int DH, int MAXT>
+__global__ void __launch_bounds__(512)
+logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, const float* nonvis_lse) {
+  constexpr int W = 8, MT = logit_chunk<T, DH>(), KS = DH / 32;
+  __shared__ float sm_m[W][16], sm_s[W][16], sm_D[16], sm_sig[16];
+  const LogitBlock<T, DH> lb(sh, text_q, vis_k, 1);
+  const int ntile = (sh.N + 15) / 16;
+  // sigma of each block row's head, in token-block order
+  if (threadIdx.x < 16) {
+    const int rr = lb.rb + threadIdx.x;
+    const int h = lb.g * sh.hg + (rr < lb.rows_g ? rr / sh.T : 0);
+    const float* part = ws.gpart + lb.p * ws.s_gpart;
+    const int nb = (sh.N + 63) / 64;
+    float sum = 0.f;
+    for (int b0 = 0; b0 < nb; b0 += 16) {
+      float t[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) t[k] = part[min(b0 + k, nb - 1) * sh.hq + h];
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if (b0 + k < nb) sum += t[k];
+    }
+    const float mean2 = sum / (static_cast<float>(sh.N) * sh.r);
+    sm_sig[threadIdx.x] = sqrtf(pr.lambda_mass) * fmaxf(sqrtf(mean2), pr.eps_mass);
+  }
+  // the head-pattern kernel needs every head's sigma
+  if (blockIdx.x == 0 && blockIdx.y == 0) sigma_from_partials(sh, pr, ws, lb.p);
+
+  int hrow[4];
+  long long mrow[4];
+  bool rvalid[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int rr = lb.rb + lb.orow + e;
+    rvalid[e] = rr < lb.rows_g;
+    hrow[e] = lb.g * sh.hg + (rvalid[e] ? rr / sh.T : 0);
+    mrow[e] = rvalid[e] ? lb.mrow(sh, lb.orow + e) : 0;
+  }
+  const bool vec = (sh.T & 15) == 0;
+  const float* ell = ws.ell + lb.p * ws.s_ell;
+  // logits s = q.k / sqrt(dh) of the wave's tiles wave, wave + W, ...:
+  // chunks of MT tiles, every load of a chunk before its MFMAs
+  floatx4 sv[MAXT];
+  float lv[MAXT][4];
+#pragma unroll
+  for (int c = 0; c < MAXT; c += MT) {
+    Frag<T> kf[MT][KS];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      const int t = c + j, ct = lb.wave + t * W;
+      if (t < MAXT && ct < ntile) {
+        lb.load_keys(sh, ct, kf[j]);
+        const int col = min(ct * 16 + lb.oc, sh.N - 1);
+        if (vec) {
+          lv[t][0] = ell[static_cast<long long>(hrow[0]) * sh.N + col];
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) lv[t][e] = ell[static_cast<long long>(hrow[e]) * sh.N + col];
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      const int t = c + j, ct = lb.wave + t * W;
+      if (t < MAXT) {
+        const bool ok = ct < ntile && ct * 16 + lb.oc < sh.N;
+        const floatx4 acc = ct < ntile ? lb.tile_mma(kf[j]) : floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sv[t][e] = ok ? acc[e] * lb.scale : -INFINITY;
+      }
+    }
+  }
+  // log-sum-exp per row: lane, 16-lane group (maximum first), waves
+  float mx[4], sm[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) m = fmaxf(m, sv[t][e]);
+    float z = 0.f;
+    if (m != -INFINITY)
+#pragma unroll
+      for (int t = 0; t < MAXT; ++t) z += __expf(sv[t][e] - m);
+    const float gm = group16_max(m);
+    const float gz = group16_sum(m == -INFINITY ? 0.f : z * __expf(m - gm));
+    mx[e] = gm;
+    sm[e] = gz;
+    if (lb.oc == 0) { sm_m[lb.wave][lb.orow + e] = gm; sm_s[lb.wave][lb.orow + e] = gz; }
+  }
+  __syncthreads();
+  if (threadIdx.x < 16) {
+    const int r = threadIdx.x, rr = lb.rb + r;
+    float D = 0.f;
+    if (rr < lb.rows_g) {
+      float m = -INFINITY;
+      for (int w = 0; w < W; ++w) m = fmaxf(m, sm_m[w][r]);
+      float z = 0.f;
+      for (int w = 0; w < W; ++w) z += (sm_m[w][r] == -INFINITY) ? 0.f : sm_s[w][r] * __expf(sm_m[w][r] - m);
+      D = m + logf(z);
+      if (nonvis_lse) {
+        const int h = lb.g * sh.hg + rr / sh.T, t = rr % sh.T;
+        const float nv = nonvis_lse[(static_cast<long long>(lb.p) * sh.hq + h) * sh.T + t];
+        const float hi = fmaxf(D, nv), lo = fminf(D, nv);
+        D = (hi == -INFINITY) ? hi : hi + log1pf(expf(lo - hi));
+      }
+    }
+    sm_D[r] = D;
+  }
+  __syncthreads();
+  // e = A * l_h[col], written to the grounded client rows; row sums / maxima
+  float D[4], sig2[4], rsum[4], rmax[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    D[e] = sm_D[lb.orow + e];
+    const float sg = sm_sig[lb.orow + e];
+    sig2[e] = sg * sg;
+    rsum[e] = 0.f;
+    rmax[e] = 0.f;
+  }
+  float* E = ws.E + lb.p * ws.s_E;
+#pragma unroll
+  for (int t = 0; t < MAXT; ++t) {
+    const int ct = lb.wave + t * W, col = ct * 16 + lb.oc;
+    if (ct >= ntile || col >= sh.N) continue;
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = __expf(sv[t][e] - D[e]) * sqrtf((vec ? lv[t][0] : lv[t][e]) + sig2[e]);
+    if (vec) {
+      *reinterpret_cast<float4*>(E + static_cast<long long>(col) * sh.ldM + mrow[0]) = make_float4(v[0], v[1], v[2], v[3]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        rsum[e] += v[e];
+        rmax[e] = fmaxf(rmax[e], v[e]);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (!rvalid[e]) continue;
+        E[static_cast<long long>(col) * sh.ldM + mrow[e]] = v[e];
+        rsum[e] += v[e];
+        rmax[e] = fmaxf(rmax[e], v[e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float s2 = group16_sum(rsum[e]);
+    const float m2 = group16_max(rmax[e]);
+    if (lb.oc == 0) { sm_s[lb.wave][lb.orow + e] = s2; sm_m[lb.wave][lb.orow + e] = m2; }
+  }
+  __syncthreads();
+  if (threadIdx.x < 16) {
+    const int r = threadIdx.x;
+    if (lb.rb + r < lb.rows_g) {
+      float s2 = 0.f, m2 = 0.f;
+      for (int w = 0; w < W; ++w) { s2 += sm_s[w][r]; m2 = fmaxf(m2, sm_m[w][r]); }
+      const long long mi = lb.mrow(sh, r);
+      ws.rowsum[lb.p * ws.s_m + mi] = s2;
+      ws.peak[lb.p * ws.s_m + mi] = m2;   // max_i e; scaled by the row weight later
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -801,12 +975,22 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
     return hipGetLastError();
   }
   const dim3 lg((sh.hg * sh.T + 15) / 16 * sh.lsplit, sh.hkv, sh.B);
+  const dim3 lr((sh.hg * sh.T + 15) / 16, sh.hkv, sh.B);
+  // every tile of a block's rows fits the registers of its eight waves
+  const bool reg = (sh.N + 15) / 16 <= 8 * kLogitRegTiles;
   const T* q = static_cast<const T*>(text_q_v);
   const T* k = static_cast<const T*>(vis_k_v);
   timer_mark(kStLogits, true, st);
   switch (sh.dh) {
 #define GMC_LOGITS(DH)                                                                                         \
     case DH:                                                                                                   \
+      if constexpr (logit_reg_ok<T, DH>()) {                                                                  \
+        if (reg) {                                                                                             \
+          hipLaunchKernelGGL((logits_reg_kernel<T, DH, kLogitRegTiles>), lr, dim3(512), 0, st, sh, pr, ws, q, k, \
+                             nonvis_lse);                                                                      \
+          break;                                                                                               \
+        }                                                                                                      \
+      }                                                                                                        \
       hipLaunchKernelGGL((logits_lse_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, pr, ws, q, k); \
       hipLaunchKernelGGL((logits_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, ws, q, k,       \
                          nonvis_lse);                                                                          \
