@@ -177,7 +177,7 @@ Plan make_plan(const gmc_config& c) {
   pl.s_E = static_cast<long long>(k.N) * k.ldM;
   pl.s_m = k.ldM;
   pl.s_apart = cdiv(k.N, 64) * k.mv;
-  pl.s_gpart = round_up(cdiv(k.N, kHeadTok), 4) * npairs;
+  pl.s_gpart = cdiv(k.N, kHeadTok) * round_up(npairs, 4);
   pl.s_e2 = static_cast<long long>(k.hq) * k.N;
   pl.s_om = kMaxHeads;
   pl.s_eb = k.N;

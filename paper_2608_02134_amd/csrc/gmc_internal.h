@@ -10,7 +10,7 @@ namespace gmc {
 constexpr int kMaxHeads = 32;     // Hq limit (head-pattern Gram kept in registers)
 constexpr int kMaxProbe = 8;      // probe rank limit
 constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
-constexpr int kHeadTok = 16;      // tokens per head-Gram block
+constexpr int kHeadTok = 8;       // tokens per head-Gram block (two per wave)
 constexpr int kStats = 9;
 constexpr int kCounters = 8;      // completion counters per problem
 constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection

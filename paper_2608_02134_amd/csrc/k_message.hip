@@ -604,7 +604,7 @@ logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, c
 // ---------------------------------------------------------------------------
 constexpr int kGramTC = 64;                 // t columns per LDS chunk
 constexpr int kGramPitch = kGramTC + 4;     // floats per staged head row
-constexpr int kGramTok = 4;                 // tokens per wave (kHeadTok per block)
+constexpr int kGramTok = 2;                 // tokens per wave (kHeadTok per block)
 static_assert(kGramTok * 4 == kHeadTok, "one block covers kHeadTok tokens");
 
 template <int R>
@@ -731,16 +731,16 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
 #pragma unroll
     for (int e = 0; e < 4; ++e) red[wave * 768 + tl * 256 + e * 64 + lane] = acc[tl][e];
   __syncthreads();
-  // pair-major partials, rows padded to a multiple of four blocks
-  const long long nbp = (sh.n_head_blk + 3) & ~3;
-  float* gp = ws.gpart + p * ws.s_gpart + blockIdx.x;
+  // block-major partials, pairs padded to a multiple of four
+  const long long npp = (sh.npairs + 3) & ~3;
+  float* gp = ws.gpart + p * ws.s_gpart + blockIdx.x * npp;
   for (int x = tid; x < 768; x += 256) {
     const int tl = x / 256, e = (x / 64) % 4, l = x % 64;
     const int hb = tl == 2 ? 1 : 0, gb = tl == 0 ? 0 : 1;
     const int hh = 16 * hb + 4 * (l >> 4) + e, gg = 16 * gb + (l & 15);
     if (hh <= gg && gg < H) {
       const float v = ((red[x] + red[768 + x]) + red[2 * 768 + x]) + red[3 * 768 + x];
-      gp[(hh * H - hh * (hh - 1) / 2 + (gg - hh)) * nbp] = v;
+      gp[hh * H - hh * (hh - 1) / 2 + (gg - hh)] = v;
     }
   }
 }
@@ -761,57 +761,75 @@ __device__ __forceinline__ void wave_argbest(float& v, int& idx, bool want_max) 
   }
 }
 
-// One block per problem, so occupancy is irrelevant: the register budget goes
-// to keeping every independent load in flight.
-__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2)))
+// One block per problem (occupancy is irrelevant, so the register budget goes
+// to loads in flight).  Every load goes out first and coalesced: the Gram
+// partials as float4 quads of pairs over groups of blocks, the grounded row
+// sums as float4 runs of queries, the first pass of the row weights; partial
+// sums are combined through LDS in a fixed order.
+constexpr int kClusterThreads = 512;
+constexpr int kClusterGB = 36;   // block partial quads in flight per thread
+
+__global__ void __launch_bounds__(kClusterThreads) __attribute__((amdgpu_waves_per_eu(1, 2)))
 cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
-  constexpr int kGB = 32;        // float4 partial loads in flight per pair slot
-  constexpr int kRW = 4;         // grounded rows per thread and pass of the row weights
+  constexpr int NT = kClusterThreads, kRW = 4;
   __shared__ float gam[kMaxHeads][kMaxHeads + 1];
   __shared__ float cosm[kMaxHeads][kMaxHeads + 1];
+  __shared__ float4 gq[NT];
+  __shared__ float hs[4 * NT];
   __shared__ float om[kMaxHeads];
   __shared__ int asg[kMaxHeads];
   const int p = blockIdx.x, tid = threadIdx.x, H = sh.hq, T = sh.T;
   const float* gp = ws.gpart + p * ws.s_gpart;
   const float* rowsum = ws.rowsum + p * ws.s_m;
-  const int nb = sh.n_head_blk, nbp = (nb + 3) & ~3;
-  // loads that do not depend on Gamma go out first: the first pass of the
-  // grounded row weights (row sums and maxima) and, in wave 0, the per-head
-  // row sums of the mean atom norm
+  const int nb = sh.n_head_blk, npp = (sh.npairs + 3) & ~3, nq = npp / 4;
+  // the first pass of the grounded row weights
   float zv0[kRW], pv0[kRW];
 #pragma unroll
   for (int k = 0; k < kRW; ++k) {
-    const int m = min(k * 512 + tid, sh.mg - 1);
+    const int m = min(k * NT + tid, sh.mg - 1);
     zv0[k] = rowsum[m];
     pv0[k] = ws.peak[p * ws.s_m + m];
   }
-  // (the first 64 queries of a head are loaded now and added after Gamma)
-  float rv[64];
-  if (tid < 64) {
-    const int h = min(tid, H - 1);
+  // grounded row sums in runs of four queries of one head (T a multiple of 4
+  // and at most 4 NT runs; otherwise each head's lane adds its rows below)
+  const bool runs = (T & 3) == 0 && sh.mg <= 16 * NT;
+  float4 rq[4];
 #pragma unroll
-    for (int t = 0; t < 64; ++t) rv[t] = rowsum[h * T + min(t, T - 1)];
+  for (int k = 0; k < 4; ++k) {
+    const int x = k * NT + tid;
+    rq[k] = (runs && 4 * x < sh.mg) ? *reinterpret_cast<const float4*>(rowsum + 4 * x) : float4{0.f, 0.f, 0.f, 0.f};
   }
-  // Gamma: one thread per pair slot sums its block partials (contiguous,
-  // pair-major) in block order
-  for (int q = tid; q < sh.npairs; q += 512) {
-    const float* row = gp + static_cast<long long>(q) * nbp;
-    float s = 0.f;
-    for (int b0 = 0; b0 < nb; b0 += 4 * kGB) {
-      float4 v[kGB];
+  // Gamma: thread (quad qq of pairs, block group bg) adds its groups' quads in
+  // block order; the groups are added in order below
+  const int ngrp = max(1, NT / nq);
+  const int qq = tid % nq, bg = tid / nq;
+  const int bper = (nb + ngrp - 1) / ngrp;
+  const int b_beg = bg * bper, b_end = min(nb, b_beg + bper);
+  float4 gs = {0.f, 0.f, 0.f, 0.f};
+  if (bg < ngrp) {
+    for (int b0 = b_beg; b0 < b_end; b0 += kClusterGB) {
+      float4 v[kClusterGB];
 #pragma unroll
-      for (int j = 0; j < kGB; ++j) v[j] = *reinterpret_cast<const float4*>(row + min(b0 + 4 * j, nbp - 4));
+      for (int j = 0; j < kClusterGB; ++j)
+        v[j] = *reinterpret_cast<const float4*>(gp + static_cast<long long>(min(b0 + j, b_end - 1)) * npp + 4 * qq);
       __builtin_amdgcn_sched_barrier(0);   // every load issued before the first add
 #pragma unroll
-      for (int j = 0; j < kGB; ++j) {
-        const int b = b0 + 4 * j;
-        if (b < nb) s += v[j].x;
-        if (b + 1 < nb) s += v[j].y;
-        if (b + 2 < nb) s += v[j].z;
-        if (b + 3 < nb) s += v[j].w;
-      }
+      for (int j = 0; j < kClusterGB; ++j)
+        if (b0 + j < b_end) { gs.x += v[j].x; gs.y += v[j].y; gs.z += v[j].z; gs.w += v[j].w; }
     }
-    int h = 0, rem = q;
+  }
+  gq[tid] = gs;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) hs[k * NT + tid] = (rq[k].x + rq[k].y) + (rq[k].z + rq[k].w);
+  __syncthreads();
+  for (int x = tid; x < sh.npairs; x += NT) {
+    const int q4 = x >> 2, c = x & 3;
+    float s = 0.f;
+    for (int g2 = 0; g2 < ngrp; ++g2) {
+      const float4 v = gq[g2 * nq + q4];
+      s += c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
+    }
+    int h = 0, rem = x;
     while (rem >= H - h) { rem -= H - h; ++h; }
     const int g = h + rem;
     gam[h][g] = s;
@@ -819,21 +837,17 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
   }
   float abar = 0.f;
   if (tid < 64) {
+    // mean atom norm abar_h = sum_t Z_(h,t) / (T N)
     const int h = min(tid, H - 1);
-#pragma unroll
-    for (int t = 0; t < 64; ++t)
-      if (t < T) abar += rv[t];
-    for (int t0 = 64; t0 < T; t0 += 64) {
-#pragma unroll
-      for (int t = 0; t < 64; ++t) rv[t] = rowsum[h * T + min(t0 + t, T - 1)];
-#pragma unroll
-      for (int t = 0; t < 64; ++t)
-        if (t0 + t < T) abar += rv[t];
+    if (runs) {
+      for (int x = h * (T / 4); x < (h + 1) * (T / 4); ++x) abar += hs[x];
+    } else {
+      for (int t = 0; t < T; ++t) abar += rowsum[h * T + t];
     }
   }
   __syncthreads();
   // cosines of the head patterns, all threads
-  for (int x = tid; x < H * H; x += 512) {
+  for (int x = tid; x < H * H; x += NT) {
     const int h = x / H, g = x % H;
     const float hh = gam[h][h], gg = gam[g][g];
     cosm[h][g] = gam[h][g] / ((hh > 0.f ? sqrtf(hh) : 1.f) * (gg > 0.f ? sqrtf(gg) : 1.f));
@@ -842,7 +856,6 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
   if (tid < 64) {
     const int lane = tid, h = lane;
     const bool valid = h < H;
-    // mean atom norm abar_h = sum_t Z_(h,t) / (T N) and activity
     abar = valid ? abar / (static_cast<float>(T) * sh.N) : 0.f;
     const float ghh = valid ? gam[h][h] : 0.f;
     const bool active = valid && ghh > 0.f;
@@ -883,8 +896,9 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
       for (int c = 0; c < nc; ++c) n_clusters += __ballot(cl == c) != 0ull;
       float s_h = 0.f;
       if (cl >= 0)
-        for (int g = 0; g < H; ++g)
-          if (asg[g] == cl) s_h += cosm[h][g];
+#pragma unroll
+        for (int g = 0; g < kMaxHeads; ++g)
+          if (g < H && asg[g] == cl) s_h += cosm[h][g];
       float inv = 0.f;
       for (int c = 0; c < nc; ++c) {
         const float tot = wave_sum(cl == c ? s_h : 0.f);
@@ -907,7 +921,7 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
   __syncthreads();
   // grounded row weights beta_msg omega_h nu_t a_(h,t) / Z_(h,t)
   const float nu_o = 1.f / (T - 1 + pr.terminal_q_weight);
-  for (int m0 = 0; m0 < sh.mg; m0 += 512 * kRW) {
+  for (int m0 = 0; m0 < sh.mg; m0 += NT * kRW) {
     float zv[kRW], pv[kRW];
 #pragma unroll
     for (int k = 0; k < kRW; ++k) {
@@ -915,14 +929,14 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
         zv[k] = zv0[k];
         pv[k] = pv0[k];
       } else {
-        const int m = min(m0 + k * 512 + tid, sh.mg - 1);
+        const int m = min(m0 + k * NT + tid, sh.mg - 1);
         zv[k] = rowsum[m];
         pv[k] = ws.peak[p * ws.s_m + m];
       }
     }
 #pragma unroll
     for (int k = 0; k < kRW; ++k) {
-      const int m = m0 + k * 512 + tid;
+      const int m = m0 + k * NT + tid;
       if (m < sh.mg) {
         const int h = m / T, t = m % T;
         const float nu = (t == T - 1) ? pr.terminal_q_weight * nu_o : nu_o;
@@ -1010,7 +1024,7 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
 #undef GMC_HEADGRAM
     default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(512), 0, st, sh, pr, ws, trace_omega);
+  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(kClusterThreads), 0, st, sh, pr, ws, trace_omega);
   timer_mark(kStHeads, false, st);
   return hipGetLastError();
 }
