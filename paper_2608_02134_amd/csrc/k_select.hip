@@ -129,9 +129,9 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
 // k[0..KPT) (0 past the segment; zero keys are excluded).  The radix windows
 // start at the highest bit in which the non-zero keys differ, so the first
 // histogram spreads the keys over up to 256 bins.  Once the bin holding the
-// threshold has at most 64 keys, its keys are gathered into LDS and every
-// wave finishes the threshold with a bitwise ballot search over them (no
-// further histogram passes or block barriers).  Every wave scans the
+// threshold has at most 64 keys, its keys are gathered into LDS, one per
+// lane, and every wave ranks them by counting (no further histogram passes or
+// block barriers).  Every wave scans the
 // histograms itself, so a radix pass needs one block barrier (three
 // histogram buffers rotate).
 // hist: 768 ints of LDS, scan: >= 16 ints.
@@ -218,14 +218,19 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
         base += __popcll(bm[q]);
       }
       __syncthreads();
-      // the remaining-th largest key of the bin, bit by bit below lo
+      // the remaining-th largest key of the bin: every lane counts the bin's
+      // keys above and at its own; the lane whose counts bracket the rank
+      // holds it
       const bool has = lane < inbin;
       const uint32_t c = has ? cand[lane] : 0u;
-      uint32_t t = prefix;
-      for (int bit = hi - 1; bit >= 0; --bit) {
-        const uint32_t trial = t | (1u << bit);
-        if (__popcll(__ballot(has && c >= trial)) >= remaining) t = trial;
+      int gt = 0, ge = 0;
+      for (int j = 0; j < inbin; ++j) {
+        const uint32_t cj = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(c), j));
+        gt += cj > c;
+        ge += cj >= c;
       }
+      const int src = __ffsll(static_cast<unsigned long long>(__ballot(has && gt < remaining && remaining <= ge))) - 1;
+      const uint32_t t = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(c), src));
       remaining -= __popcll(__ballot(has && c > t));
       prefix = t;
       hi = 0;
