@@ -45,6 +45,9 @@ CASES = {
     "doc_shrunk": dict(name="doc", grid=(1, 40, 40), t=32, k=320),
     "batch_shrunk": dict(name="batch16", batch=3, grid=(1, 24, 24), t=16, k=96),
     "frames_bounded": dict(name="frames", grid=(2, 48, 48), t=16, k=600),
+    # fp32 above the register-held logits limit (N > 1536): the column-range
+    # logits kernels, with a query count that is not a multiple of 16
+    "tiny_ranges": dict(name="tiny", grid=(1, 40, 40), t=7, k=200),
     # the benchmarked shapes at full size, in the launch configuration the
     # benchmark times (document: 16 pool keys per thread; 16 images: 16 blocks
     # per problem)
