@@ -816,6 +816,14 @@ __device__ __forceinline__ void pool_regs(const Shape& sh, const unsigned long l
   block_topk_regs<KPT>(k, seg, psize, pool_s, hist, scan);
 }
 
+// RES: block b owns tokens [8 b, 8 b + 8) (N <= 8 blocks, M <= 256 kResJ) and
+// keeps their weighted client rows alpha_m E[i][m] (Cbar, the product rounded
+// once) in registers for the whole call, wave w holding the rows
+// m = 64 (w + 4 j) + lane, j < kResJ, of all eight tokens; a round's gains
+// then read only the coverage.  Otherwise each wave streams the rows of
+// its tokens (gw, gw + waves, ...) from the caches every round.
+constexpr int kResJ = 14;
+template <bool RES>
 __global__ void __launch_bounds__(256)
 select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_pool, int32_t* trace_batch) {
   extern __shared__ float dyn[];
@@ -848,6 +856,22 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
   }
   for (int i = tid; i < sh.N; i += 256) taken[i] = 0;
   if (tid == 0) failed = 0;
+  float er[RES ? 8 : 1][RES ? kResJ : 1];
+  if constexpr (RES) {
+    // rows past M and tokens past N hold zeros (clamped loads, then select)
+#pragma unroll
+    for (int j = 0; j < kResJ; ++j) {
+      const int m = 64 * (wave + 4 * j) + lane;
+      const int mc = min(m, sh.m - 1);
+      const float a = alpha_g[mc];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int t = blk * 8 + s;
+        const float v = E[static_cast<long long>(min(t, sh.N - 1)) * sh.ldM + mc];
+        er[s][j] = (m < sh.m && t < sh.N) ? a * v : 0.f;
+      }
+    }
+  }
   __syncthreads();
   int selected = 0;
   for (int r = 0; r < sh.rounds; ++r) {
@@ -858,7 +882,36 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     unsigned long long* tsr = ts + (r & 1) * 64LL * nchunk;
 
     // ---- singleton gains of unselected tokens, two tokens per wave pass with
-    //      all their row loads in flight, published with this round's tag
+    //      all their row loads in flight (or the block's rows held in registers),
+    //      published with this round's tag
+    if constexpr (RES) {
+      // per lane: the partial gains of the eight tokens over its rows
+      // (b_m >= 0, so rows past M add zero); then summed over the lanes and
+      // the four waves, in that order
+      float acc[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) acc[s] = 0.f;
+#pragma unroll
+      for (int j = 0; j < kResJ; ++j) {
+        const float b = bl[min(64 * (wave + 4 * j) + lane, sh.ldM - 1)];
+#pragma unroll
+        for (int s = 0; s < 8; ++s) acc[s] += fmaxf(er[s][j] - b, 0.f);
+      }
+      transpose_reduce_step<4>(acc, lane);
+      transpose_reduce_step<2>(acc, lane);
+      transpose_reduce_step<1>(acc, lane);
+      float g = acc[0];             // token lane & 7, summed over 8 lanes
+      g += __shfl_xor(g, 8, kWave);
+      g += __shfl_xor(g, 16, kWave);
+      g += __shfl_xor(g, 32, kWave);
+      if (lane < 8) rmu[wave][lane] = g;
+      __syncthreads();
+      if (tid < 8) {
+        const int t = blk * 8 + tid;
+        if (t < sh.N && !taken[t])
+          st_dev64(&tur[t], tag_value(tag, ((rmu[0][tid] + rmu[1][tid]) + rmu[2][tid]) + rmu[3][tid]));
+      }
+    } else
     for (int i0 = gw; i0 < sh.N; i0 += 2 * nwaves) {
       const int i1 = i0 + nwaves;
       const bool ok0 = taken[i0] == 0;
@@ -888,7 +941,9 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     }
 
     // ---- the pool, identical in every block (waits for this round's gains)
-    if (sh.N <= 256 * 8)
+    if constexpr (RES)
+      pool_regs<8>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
+    else if (sh.N <= 256 * 8)
       pool_regs<8>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
     else if (sh.N <= 256 * 16)
       pool_regs<16>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
@@ -1205,8 +1260,13 @@ static void launch_cov(const Shape& sh, const Ws& ws, int nb, hipStream_t st) {
 // the bounded barrier waits already turn a block that never becomes resident
 // (a device saturated by foreign work) into a reported timeout rather than a
 // hang.
-static int persistent_blocks(const Shape& sh, size_t lds) {
-  static int n_cu = -1, lds_max = 0, lds_set = 64 * 1024;
+static const void* persistent_fn(int res) {
+  return res ? reinterpret_cast<const void*>(select_persistent_kernel<true>)
+             : reinterpret_cast<const void*>(select_persistent_kernel<false>);
+}
+
+static int persistent_blocks(const Shape& sh, size_t lds, int res) {
+  static int n_cu = -1, lds_max = 0, lds_set[2] = {64 * 1024, 64 * 1024};
   if (n_cu < 0) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -1215,16 +1275,16 @@ static int persistent_blocks(const Shape& sh, size_t lds) {
       n_cu = 0;
   }
   if (n_cu <= 0 || sh.pool_cap > 64 || sh.N > kLdsKeys || lds > static_cast<size_t>(lds_max)) return 0;
-  if (static_cast<int>(lds) > lds_set) {
+  const int v = res ? 1 : 0;
+  if (static_cast<int>(lds) > lds_set[v]) {
     // dynamic LDS above 64 KB has to be granted to the kernel first
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(select_persistent_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)) != hipSuccess)
+    if (hipFuncSetAttribute(persistent_fn(res), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            static_cast<int>(lds)) != hipSuccess)
       return 0;
-    lds_set = static_cast<int>(lds);
+    lds_set[v] = static_cast<int>(lds);
   }
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(select_persistent_kernel),
-                                                   256, lds) != hipSuccess || per_cu < 1)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(res), 256, lds) != hipSuccess || per_cu < 1)
     return 0;
   // one CU per block; about two gain tokens per wave
   const int cap = n_cu / sh.B;
@@ -1240,11 +1300,19 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
     const size_t lds = 2 * static_cast<size_t>(sh.ldM) * sizeof(float) +
                        ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15)) +
                        (sh.N > 256 * 16 ? static_cast<size_t>(sh.N) * sizeof(uint32_t) : 0);
-    int nblk = persistent_blocks(sh, lds);
+    int nblk = persistent_blocks(sh, lds, 0);
+    // the blocks' client rows held in registers when each block owns at
+    // most eight tokens and the rows are short enough
+    const bool resident = nblk > 0 && sh.N <= 8 * nblk && sh.m <= 256 * kResJ &&
+                          persistent_blocks(sh, lds, 1) == nblk;
     if (nblk > 0) {
       timer_mark(kStSelect, true, st);
-      hipLaunchKernelGGL(select_persistent_kernel, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws, nblk,
-                         trace_pool, trace_batch);
+      if (resident)
+        hipLaunchKernelGGL(select_persistent_kernel<true>, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws,
+                           nblk, trace_pool, trace_batch);
+      else
+        hipLaunchKernelGGL(select_persistent_kernel<false>, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws, nblk,
+                           trace_pool, trace_batch);
       timer_mark(kStSelect, false, st);
       *support_ready = true;
       return hipGetLastError();
