@@ -130,10 +130,11 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
 // start at the highest bit in which the non-zero keys differ, so the first
 // histogram spreads the keys over up to 256 bins.  Once the bin holding the
 // threshold has at most 64 keys, its keys are gathered into LDS, one per
-// lane, and every wave ranks them by counting (no further histogram passes or
-// block barriers).  Every wave scans the
+// lane, and every wave finds the threshold among them bit by bit with ballots
+// (no further histogram passes or block barriers).  Every wave scans the
 // histograms itself, so a radix pass needs one block barrier (three
-// histogram buffers rotate).
+// histogram buffers rotate).  The selected indices are written to out[0,
+// count) in ascending index order and out[count, 64) is filled with index 0.
 // hist: 768 ints of LDS, scan: >= 16 ints.
 template <int KPT>
 __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, int* out, int* hist, int* scan) {
@@ -218,21 +219,30 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
         base += __popcll(bm[q]);
       }
       __syncthreads();
-      // the remaining-th largest key of the bin: every lane counts the bin's
-      // keys above and at its own; the lane whose counts bracket the rank
-      // holds it
+      // the remaining-th largest key of the bin, one bit at a time below hi:
+      // of the keys still matching the prefix, those with the bit set are
+      // all taken when there are fewer than remaining of them.  Once every
+      // key still matching is taken, the selection is exactly the keys >=
+      // prefix (its lower bits zero): kth = prefix, all keys equal to it.
       const bool has = lane < inbin;
       const uint32_t c = has ? cand[lane] : 0u;
-      int gt = 0, ge = 0;
-      for (int j = 0; j < inbin; ++j) {
-        const uint32_t cj = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(c), j));
-        gt += cj > c;
-        ge += cj >= c;
+      unsigned long long alive = static_cast<unsigned long long>(__ballot(has));
+      for (int b = hi - 1;; --b) {
+        if (__popcll(alive) == remaining) {
+          remaining = __popcll(alive & static_cast<unsigned long long>(__ballot(c == prefix)));
+          break;
+        }
+        if (b < 0) break;
+        const unsigned long long ones = alive & static_cast<unsigned long long>(__ballot((c >> b) & 1u));
+        const int n1 = __popcll(ones);
+        if (n1 >= remaining) {
+          alive = ones;
+          prefix |= 1u << b;
+        } else {
+          remaining -= n1;
+          alive &= ~ones;
+        }
       }
-      const int src = __ffsll(static_cast<unsigned long long>(__ballot(has && gt < remaining && remaining <= ge))) - 1;
-      const uint32_t t = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(c), src));
-      remaining -= __popcll(__ballot(has && c > t));
-      prefix = t;
       hi = 0;
     }
     buf = nxt;
@@ -244,8 +254,14 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
     gt += k[q] > kth;
     eq += k[q] == kth;
   }
-  int tot;
-  const int pre = block_exclusive_scan(gt | (eq << 16), scan, &tot);
+  // exclusive prefix of (gt, eq) over threads: wave scans, then the wave
+  // totals (scan[12..15], untouched earlier in the call) after one barrier
+  const int v = gt | (eq << 16);
+  const int incl = wave_scan_add(v);
+  if (lane == 63) scan[12 + wave] = incl;
+  __syncthreads();
+  int pre = incl - v;
+  for (int w = 0; w < wave; ++w) pre += scan[12 + w];
   int gt_b = static_cast<int>(static_cast<unsigned>(pre) & 0xFFFFu);
   int eq_b = static_cast<int>(static_cast<unsigned>(pre) >> 16);
   const int i0 = tid * seg;
@@ -259,6 +275,7 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
       ++eq_b;
     }
   }
+  if (tid >= count && tid < 64) out[tid] = 0;
   __syncthreads();
 }
 
@@ -941,9 +958,12 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     }
 
     // ---- the pool, identical in every block (waits for this round's gains)
-    if constexpr (RES)
-      pool_regs<8>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
-    else if (sh.N <= 256 * 8)
+    if constexpr (RES) {
+      if (sh.N <= 256 * 6)
+        pool_regs<6>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
+      else
+        pool_regs<8>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
+    } else if (sh.N <= 256 * 8)
       pool_regs<8>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
     else if (sh.N <= 256 * 16)
       pool_regs<16>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
@@ -977,8 +997,9 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       __syncthreads();
       block_topk256(keys, sh.N, psize, pool_s, hist, scan, bc);
     }
-    {
-      // clamp to valid rows (defensive) and pad past psize with a valid row, masked below
+    if constexpr (!RES) {
+      // clamp to valid rows (defensive) and pad past psize with a valid row,
+      // masked below (the register top-k pads with row 0 itself)
       int pv = 0;
       if (tid < 64) pv = min(max(pool_s[tid < psize ? tid : 0], 0), sh.N - 1);
       __syncthreads();
