@@ -749,17 +749,9 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
 // Head clustering, head weights and grounded row weights.  One block per
 // problem: Gamma is reduced from the per-block partials in block order
 // (many loads in flight per thread), then one wave runs farthest-first with
-// lane h owning head h (wave-wide argmax/argmin with lowest-index ties).
+// lane h owning head h: wave-wide max / min (DPP scans), the lowest lane
+// holding the best value by ballot.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void wave_argbest(float& v, int& idx, bool want_max) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(v, o, kWave);
-    const int oi = __shfl_xor(idx, o, kWave);
-    const bool better = want_max ? (ov > v || (ov == v && oi < idx)) : (ov < v || (ov == v && oi < idx));
-    if (better) { v = ov; idx = oi; }
-  }
-}
 
 // One block per problem (occupancy is irrelevant, so the register budget goes
 // to loads in flight).  Every load goes out first and coalesced: the Gram
@@ -822,18 +814,19 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
 #pragma unroll
   for (int k = 0; k < 4; ++k) hs[k * NT + tid] = (rq[k].x + rq[k].y) + (rq[k].z + rq[k].w);
   __syncthreads();
-  for (int x = tid; x < sh.npairs; x += NT) {
-    const int q4 = x >> 2, c = x & 3;
-    float s = 0.f;
-    for (int g2 = 0; g2 < ngrp; ++g2) {
-      const float4 v = gq[g2 * nq + q4];
-      s += c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
+  for (int hg = tid; hg < kMaxHeads * kMaxHeads; hg += NT) {
+    const int h = hg / kMaxHeads, g = hg % kMaxHeads;
+    if (h <= g && g < H) {
+      const int x = h * H - h * (h - 1) / 2 + (g - h);   // pair (h, g) in row-major upper order
+      const int q4 = x >> 2, c = x & 3;
+      float s = 0.f;
+      for (int g2 = 0; g2 < ngrp; ++g2) {
+        const float4 v = gq[g2 * nq + q4];
+        s += c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
+      }
+      gam[h][g] = s;
+      gam[g][h] = s;
     }
-    int h = 0, rem = x;
-    while (rem >= H - h) { rem -= H - h; ++h; }
-    const int g = h + rem;
-    gam[h][g] = s;
-    gam[g][h] = s;
   }
   float abar = 0.f;
   if (tid < 64) {
@@ -864,30 +857,31 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
     int cl = -1;
     if (n_active > 0) {
       // first centre: largest pre-normalisation pattern sqrt(beta Gamma_hh) / abar_h
-      float v = active ? sqrtf(pr.beta_msg * ghh) / (abar > 0.f ? abar : 1.f) : -INFINITY;
-      int idx = active ? h : 0x7fffffff;
-      wave_argbest(v, idx, true);
-      int centres[kMaxHeads];
-      int nc = 0;
-      centres[nc++] = idx;
+      const float v = active ? sqrtf(pr.beta_msg * ghh) / (abar > 0.f ? abar : 1.f) : -INFINITY;
+      const float vbest = wave_max(v);
+      const int idx = __ffsll(static_cast<unsigned long long>(__ballot(active && v == vbest))) - 1;
+      int nc = 1;
       bool is_c = h == idx;
       float maxcos = valid ? cosm[h][idx] : -INFINITY;
+      // each head's nearest centre so far (ties to the earlier centre)
+      float bv = maxcos;
+      int best = 0;
       const int want = min(pr.max_head_clusters, n_active);
       while (nc < want) {
-        float cv = (active && !is_c) ? maxcos : INFINITY;
-        int ci = (active && !is_c) ? h : 0x7fffffff;
-        wave_argbest(cv, ci, false);
-        if (ci == 0x7fffffff) break;
-        centres[nc++] = ci;
+        // next centre: the active non-centre head least similar to every centre
+        const bool cand = active && !is_c;
+        const float cv = cand ? maxcos : INFINITY;
+        const float cbest = wave_min(cv);
+        const unsigned long long cm = static_cast<unsigned long long>(__ballot(cand && cv == cbest));
+        if (cm == 0ull) break;
+        const int ci = __ffsll(cm) - 1;
+        const float cc = valid ? cosm[h][ci] : -INFINITY;
+        if (cc > bv) { bv = cc; best = nc; }
+        ++nc;
         is_c |= h == ci;
-        if (valid) maxcos = fmaxf(maxcos, cosm[h][ci]);
+        maxcos = fmaxf(maxcos, cc);
       }
-      if (active) {
-        float bv = cosm[h][centres[0]];
-        cl = 0;
-        for (int c = 1; c < nc; ++c)
-          if (cosm[h][centres[c]] > bv) { bv = cosm[h][centres[c]]; cl = c; }
-      }
+      if (active) cl = best;
       if (valid) asg[h] = cl;
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
