@@ -404,11 +404,18 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   int* cnt = ws.lcnt + lb.p * ws.s_lcnt + (blockIdx.x / sh.lsplit) * sh.hkv + lb.g;
   if (!last_arrival(cnt, sh.lsplit, &flag)) return;
   if (row) {
-    float ts = 0.f, tm = 0.f;
-    for (int q = 0; q < sh.lsplit; ++q) {
-      ts += ld_dev(&part[static_cast<long long>(2 * kLogitSplit + q) * sh.mg + mi]);
-      tm = fmaxf(tm, ld_dev(&part[static_cast<long long>(3 * kLogitSplit + q) * sh.mg + mi]));
+    // every load in flight first, then the sums in range order
+    float vs[kLogitSplit], vm[kLogitSplit];
+#pragma unroll
+    for (int q = 0; q < kLogitSplit; ++q) {
+      const int qc = min(q, sh.lsplit - 1);
+      vs[q] = ld_dev(&part[static_cast<long long>(2 * kLogitSplit + qc) * sh.mg + mi]);
+      vm[q] = ld_dev(&part[static_cast<long long>(3 * kLogitSplit + qc) * sh.mg + mi]);
     }
+    float ts = 0.f, tm = 0.f;
+#pragma unroll
+    for (int q = 0; q < kLogitSplit; ++q)
+      if (q < sh.lsplit) { ts += vs[q]; tm = fmaxf(tm, vm[q]); }
     ws.rowsum[lb.p * ws.s_m + mi] = ts;
     ws.peak[lb.p * ws.s_m + mi] = tm;
   }
@@ -774,6 +781,21 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
   const float* gp = ws.gpart + p * ws.s_gpart;
   const float* rowsum = ws.rowsum + p * ws.s_m;
   const int nb = sh.n_head_blk, npp = (sh.npairs + 3) & ~3, nq = npp / 4;
+  // Gamma: thread (quad qq of pairs, block group bg) adds its groups' quads in
+  // block order; the groups are added in order below.  The first batch of
+  // quads goes out before the row-sum loads, and every load of the first
+  // batch before the first add.
+  const int ngrp = max(1, NT / nq);
+  const int qq = tid % nq, bg = tid / nq;
+  const int bper = (nb + ngrp - 1) / ngrp;
+  const int b_beg = bg * bper, b_end = min(nb, b_beg + bper);
+  const bool gthr = bg < ngrp && b_beg < b_end;
+  float4 v[kClusterGB];
+  if (gthr) {
+#pragma unroll
+    for (int j = 0; j < kClusterGB; ++j)
+      v[j] = *reinterpret_cast<const float4*>(gp + static_cast<long long>(min(b_beg + j, b_end - 1)) * npp + 4 * qq);
+  }
   // the first pass of the grounded row weights
   float zv0[kRW], pv0[kRW];
 #pragma unroll
@@ -791,20 +813,17 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
     const int x = k * NT + tid;
     rq[k] = (runs && 4 * x < sh.mg) ? *reinterpret_cast<const float4*>(rowsum + 4 * x) : float4{0.f, 0.f, 0.f, 0.f};
   }
-  // Gamma: thread (quad qq of pairs, block group bg) adds its groups' quads in
-  // block order; the groups are added in order below
-  const int ngrp = max(1, NT / nq);
-  const int qq = tid % nq, bg = tid / nq;
-  const int bper = (nb + ngrp - 1) / ngrp;
-  const int b_beg = bg * bper, b_end = min(nb, b_beg + bper);
+  __builtin_amdgcn_sched_barrier(0);
   float4 gs = {0.f, 0.f, 0.f, 0.f};
-  if (bg < ngrp) {
-    for (int b0 = b_beg; b0 < b_end; b0 += kClusterGB) {
-      float4 v[kClusterGB];
+  if (gthr) {
+#pragma unroll
+    for (int j = 0; j < kClusterGB; ++j)
+      if (b_beg + j < b_end) { gs.x += v[j].x; gs.y += v[j].y; gs.z += v[j].z; gs.w += v[j].w; }
+    for (int b0 = b_beg + kClusterGB; b0 < b_end; b0 += kClusterGB) {
 #pragma unroll
       for (int j = 0; j < kClusterGB; ++j)
         v[j] = *reinterpret_cast<const float4*>(gp + static_cast<long long>(min(b0 + j, b_end - 1)) * npp + 4 * qq);
-      __builtin_amdgcn_sched_barrier(0);   // every load issued before the first add
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < kClusterGB; ++j)
         if (b0 + j < b_end) { gs.x += v[j].x; gs.y += v[j].y; gs.z += v[j].z; gs.w += v[j].w; }
@@ -819,11 +838,9 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
     if (h <= g && g < H) {
       const int x = h * H - h * (h - 1) / 2 + (g - h);   // pair (h, g) in row-major upper order
       const int q4 = x >> 2, c = x & 3;
+      const float* gqf = reinterpret_cast<const float*>(gq);
       float s = 0.f;
-      for (int g2 = 0; g2 < ngrp; ++g2) {
-        const float4 v = gq[g2 * nq + q4];
-        s += c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
-      }
+      for (int g2 = 0; g2 < ngrp; ++g2) s += gqf[4 * (g2 * nq + q4) + c];
       gam[h][g] = s;
       gam[g][h] = s;
     }
@@ -888,11 +905,12 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
       // clusters, dispersion d_h = 1 - u_h . mu_c and inverse-dispersion weights
       int n_clusters = 0;
       for (int c = 0; c < nc; ++c) n_clusters += __ballot(cl == c) != 0ull;
+      // members of the head's cluster (adding zeros for the others leaves
+      // the sum unchanged)
       float s_h = 0.f;
-      if (cl >= 0)
 #pragma unroll
-        for (int g = 0; g < kMaxHeads; ++g)
-          if (g < H && asg[g] == cl) s_h += cosm[h][g];
+      for (int g = 0; g < kMaxHeads; ++g) s_h += (g < H && asg[g] == cl) ? cosm[h][g] : 0.f;
+      if (cl < 0) s_h = 0.f;
       float inv = 0.f;
       for (int c = 0; c < nc; ++c) {
         const float tot = wave_sum(cl == c ? s_h : 0.f);
