@@ -59,8 +59,9 @@ extern "C" {
 /* stats layout: [0] s_x  [1] mean selected-cosine gap over discarded tokens
  *               [2] F(S)  [3] F(V)  [4] realised K  [5] rounds  [6] M rows
  *               [7] number of discarded tokens
- *               [8] device status: 0 ok; 1 = a grid barrier of the
- *                   persistent selection timed out (results invalid)      */
+ *               [8] device status: 0 ok; 1 = a bounded device wait (a
+ *                   hand-off of the persistent selection, or the wait for
+ *                   the bank kernels) timed out (results invalid)         */
 
 /*
  * gmc_config - model shape, capacities and the frozen settings.

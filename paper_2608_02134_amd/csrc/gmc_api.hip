@@ -543,13 +543,23 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   }
   err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, bank_st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
-  if (fork) {
+  // join: with text queries the last message kernel (one block per problem)
+  // waits on a device flag that the side stream raises after its last bank
+  // kernel, which costs less than an event wait on the caller's stream;
+  // without text queries, an event
+  int* bank_flag = c.ws.cnt + kCntBankFlag;   // cleared by the row-norm kernel
+  const bool flag_join = fork && s.T > 0;
+  if (flag_join) {
+    err = launch_bank_signal(bank_flag, c.side);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
+  } else if (fork) {
     err = hipEventRecord(c.join, c.side);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }
-  err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega, st);
+  err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega,
+                       flag_join ? bank_flag : nullptr, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
-  if (fork) {
+  if (fork && !flag_join) {
     err = hipStreamWaitEvent(st, c.join, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }

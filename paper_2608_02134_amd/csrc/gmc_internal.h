@@ -13,6 +13,9 @@ constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 8;       // tokens per head-Gram block (two per wave)
 constexpr int kStats = 9;
 constexpr int kCounters = 8;      // completion counters per problem
+constexpr int kCntBankFlag = 6;   // slot of problem 0: the bank kernels of the call have finished
+constexpr int kCntStatus = 7;     // device status bits, 1 = a bounded device wait timed out
+constexpr int kBankSpinLimit = 1 << 18;   // polls of the bank flag before the wait gives up
 constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection
 constexpr int kLogitSplit = 8;    // column ranges of the message-logit kernels (at most)
 constexpr int kProbeSplit = 4;    // K splits of the value-probe GEMM (d a multiple of 256)

@@ -21,11 +21,15 @@ void timer_mark(int stage, bool begin, hipStream_t st);
 hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, hipStream_t st);
 
 // Value probe, mass coordinate, native slice, head weights, grounded row
-// weights and normalised energy (after launch_rownorm).
+// weights and normalised energy (after launch_rownorm).  With bank_flag set
+// (T > 0), the last kernel also waits until the flag reads 1.
 hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
                           const void* text_q, const void* vis_k, const void* probe,
-                          const float* nonvis_lse, float* trace_omega,
+                          const float* nonvis_lse, float* trace_omega, const int* bank_flag,
                           hipStream_t st);
+
+// Sets *flag = 1 once the work before it on st has finished.
+hipError_t launch_bank_signal(int* flag, hipStream_t st);
 
 // Appearance (exact or bounded) and spatial banks with their row weights.
 hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,

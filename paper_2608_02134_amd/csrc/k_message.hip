@@ -760,6 +760,11 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
 // holding the best value by ballot.
 // ---------------------------------------------------------------------------
 
+// Raised by the side stream once every bank kernel of the call has finished.
+__global__ void bank_signal_kernel(int* flag) {
+  if (threadIdx.x == 0) __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // One block per problem (occupancy is irrelevant, so the register budget goes
 // to loads in flight).  Every load goes out first and coalesced: the Gram
 // partials as float4 quads of pairs over groups of blocks, the grounded row
@@ -769,7 +774,7 @@ constexpr int kClusterThreads = 512;
 constexpr int kClusterGB = 36;   // block partial quads in flight per thread
 
 __global__ void __launch_bounds__(kClusterThreads) __attribute__((amdgpu_waves_per_eu(1, 2)))
-cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
+cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_flag) {
   constexpr int NT = kClusterThreads, kRW = 4;
   __shared__ float gam[kMaxHeads][kMaxHeads + 1];
   __shared__ float cosm[kMaxHeads][kMaxHeads + 1];
@@ -958,6 +963,18 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega) {
       }
     }
   }
+  // the bank kernels run on another stream; the kernel after this one reads
+  // their client rows, so this one ends only once the side stream has raised
+  // bank_flag (one thread per block waits; every wait is bounded)
+  if (bank_flag && tid == 0) {
+    for (int spin = 0; __hip_atomic_load(bank_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 1; ++spin) {
+      if (spin == kBankSpinLimit) {
+        __hip_atomic_store(&ws.cnt[p * ws.s_cnt + kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
 }
 
 // Empty grounded bank (T = 0): omega = 0 and uniform energy ebar = 1.
@@ -979,7 +996,7 @@ __global__ void no_grounded_kernel(Shape sh, Ws ws, float* trace_omega) {
 template <typename T>
 static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden_v,
                                const void* text_q_v, const void* vis_k_v, const void* probe_v,
-                               const float* nonvis_lse, float* trace_omega,
+                               const float* nonvis_lse, float* trace_omega, const int* bank_flag,
                                hipStream_t st) {
   const T* hidden = static_cast<const T*>(hidden_v);
   timer_mark(kStProbe, true, st);
@@ -1036,7 +1053,7 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
 #undef GMC_HEADGRAM
     default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(kClusterThreads), 0, st, sh, pr, ws, trace_omega);
+  hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(kClusterThreads), 0, st, sh, pr, ws, trace_omega, bank_flag);
   timer_mark(kStHeads, false, st);
   return hipGetLastError();
 }
@@ -1055,11 +1072,16 @@ hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, hip
 
 hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
                           const void* text_q, const void* vis_k, const void* probe,
-                          const float* nonvis_lse, float* trace_omega,
+                          const float* nonvis_lse, float* trace_omega, const int* bank_flag,
                           hipStream_t st) {
   if (sh.dtype == 0)
-    return message_impl<float>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, st);
-  return message_impl<bf16_t>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, st);
+    return message_impl<float>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, bank_flag, st);
+  return message_impl<bf16_t>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, bank_flag, st);
+}
+
+hipError_t launch_bank_signal(int* flag, hipStream_t st) {
+  hipLaunchKernelGGL(bank_signal_kernel, dim3(1), dim3(64), 0, st, flag);
+  return hipGetLastError();
 }
 
 }  // namespace gmc

@@ -783,7 +783,6 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 // the block records the timeout (device status word) and stops waiting, so
 // every wave always exits.
 constexpr int kSpinLimit = 1 << 18;   // bounded waits (a fraction of a second)
-constexpr int kCntStatus = 7;          // device status bits, 1 = wait timeout
 
 // Marks the call failed (device status word) after a bounded wait.
 __device__ __forceinline__ void mark_timeout(int* cnt, int* failed) {
