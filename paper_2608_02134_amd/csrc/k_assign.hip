@@ -92,6 +92,10 @@ __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
   const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = blockIdx.x * 4 + wave;
   if (i < sh.N) {
+    // the energy inputs go out with the first cosine loads
+    const float w = (sh.T > 0 && lane < sh.hq)
+                        ? ws.omega[p * ws.s_om + lane] * ws.e2[p * ws.s_e2 + static_cast<long long>(lane) * sh.N + i]
+                        : 0.f;
     const CosSource<kFromE> cs = cos_source<kFromE>(sh, pr, ws, p, i);
     float t1 = -INFINITY, t2 = -INFINITY;
     for (int j0 = 0; j0 < sh.K; j0 += 64 * 8) {
@@ -117,7 +121,6 @@ __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
     if (lane == 0) ws.delta[p * ws.s_del + i] = delta;
     if (sh.T > 0) {
       // lane h holds head h (at most kMaxHeads of them)
-      const float w = lane < sh.hq ? ws.omega[p * ws.s_om + lane] * ws.e2[p * ws.s_e2 + static_cast<long long>(lane) * sh.N + i] : 0.f;
       const float e = sqrtf(wave_sum(w));
       if (lane == 0) ws.ebar[p * ws.s_eb + i] = e;
     }
@@ -175,20 +178,33 @@ __global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, 
   __shared__ float red[16];
   const int p = blockIdx.y, lane = threadIdx.x & 63;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int ic = min(i, sh.N - 1);
+  const int* sup = ws.sup + p * ws.s_sup;
+  const float* pc = ws.pc + p * ws.s_pc;
+  const CosSource<kFromE> cs = cos_source<kFromE>(sh, pr, ws, p, ic);
+  // the token's own loads and its first support batch (cosines and spatial
+  // coordinates) go out before the gate's block reductions
+  const bool selected = ws.sel[p * ws.s_sel + ic] >= 0;
+  const float delta = ws.delta[p * ws.s_del + ic];
+  const float py = pc[2 * ic], px = pc[2 * ic + 1];
+  float c0[4], y0[4], x0[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int j = min(q * 64 + lane, sh.K - 1);
+    const int sj = sup[j];
+    c0[q] = cs.get(j);
+    y0[q] = pc[2 * sj];
+    x0[q] = pc[2 * sj + 1];
+  }
   const float sx = separability_gate(sh, pr, ws, p, red);
   if (i >= sh.N) return;
-  const int* sup = ws.sup + p * ws.s_sup;
   int pi_i;
-  if (ws.sel[p * ws.s_sel + i] >= 0) {
+  if (selected) {
     pi_i = i;
   } else {
-    const float delta = ws.delta[p * ws.s_del + i];
     const float g = (pr.g_form == 1) ? (delta < pr.amb_margin ? 1.f : 0.f)
                                      : expf(-powf(delta / pr.amb_margin, pr.amb_p));
     const float w = pr.spatial_w * sx * g;
-    const CosSource<kFromE> cs = cos_source<kFromE>(sh, pr, ws, p, i);
-    const float* pc = ws.pc + p * ws.s_pc;
-    const float py = pc[2 * i], px = pc[2 * i + 1];
     const float inv_tau = 1.f / pr.tau_s;
     float best = -INFINITY;
     int bj = 0x7fffffff;
@@ -197,10 +213,15 @@ __global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, 
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int j = min(j0 + q * 64 + lane, sh.K - 1);
-        float k = cs.get(j);
-        if (w > 0.f) {
+        float k, sy, sxx;
+        if (j0 == 0) {
+          k = c0[q]; sy = y0[q]; sxx = x0[q];
+        } else {
           const int sj = sup[j];
-          const float dy = py - pc[2 * sj], dx = px - pc[2 * sj + 1];
+          k = cs.get(j); sy = pc[2 * sj]; sxx = pc[2 * sj + 1];
+        }
+        if (w > 0.f) {
+          const float dy = py - sy, dx = px - sxx;
           k += w * expf(-(dy * dy + dx * dx) * inv_tau);
         }
         kv[q] = k;

@@ -37,6 +37,16 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
   const float m0 = 1.f - pr.pop_strength * sx, m1 = pr.pop_strength * sx;
   const T* H = hidden + static_cast<long long>(p) * sh.N * sh.d;
   const int ngroups = sh.d / 8;
+  // the carrier's own row and norm go out first (they need only j)
+  const T* hj = H + static_cast<long long>(j) * sh.d;
+  uint4 own[G][CH];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int grp = min(tid + g * 256, ngroups - 1);
+#pragma unroll
+    for (int c = 0; c < CH; ++c) own[g][c] = ld16(hj + grp * 8 + c * 4);
+  }
+  const float n2j = ws.n2[p * ws.s_n + j];
   float acc[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g)
@@ -108,7 +118,6 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
     }
   }
   // blend with the carrier's own state and restore its RMS
-  const T* hj = H + static_cast<long long>(j) * sh.d;
   const float inv_mass = 1.f / mass;
   float ss = 0.f;
 #pragma unroll
@@ -116,7 +125,16 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
     const int grp = tid + g * 256;
     if (grp < ngroups) {
       float hv[8];
-      load8_f32<T>(hj + grp * 8, hv);
+      if constexpr (sizeof(T) == 2) {
+        const bf16_t* v = reinterpret_cast<const bf16_t*>(&own[g][0]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) hv[e] = bf16_to_f32(v[e]);
+      } else {
+        const float* v = reinterpret_cast<const float*>(&own[g][0]);
+        const float* v2 = reinterpret_cast<const float*>(&own[g][1]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { hv[e] = v[e]; hv[e + 4] = v2[e]; }
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float v = (1.f - pr.tau_j) * hv[e] + pr.tau_j * (acc[g][e] * inv_mass);
@@ -127,7 +145,7 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
   }
   ss = block_sum(ss, red);
   const float rms_v = sqrtf(ss / static_cast<float>(sh.d));
-  const float rms_h = sqrtf(ws.n2[p * ws.s_n + j] / static_cast<float>(sh.d));
+  const float rms_h = sqrtf(n2j / static_cast<float>(sh.d));
   const float scale = rms_h / (rms_v + pr.restore_eps);
   T* out = out_hidden + (static_cast<long long>(p) * sh.K + jj) * sh.d;
 #pragma unroll
