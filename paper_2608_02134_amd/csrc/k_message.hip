@@ -440,26 +440,22 @@ logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, c
   __shared__ float sm_m[W][16], sm_s[W][16], sm_D[16], sm_sig[16];
   const LogitBlock<T, DH> lb(sh, text_q, vis_k, 1);
   const int ntile = (sh.N + 15) / 16;
-  // sigma of each block row's head, in token-block order
-  if (threadIdx.x < 16) {
+  // sigma of each block row's head (threads 0..15) and, in block (0, 0), of
+  // every head for the head-pattern kernel (threads 64 + h): the partials of
+  // the token blocks (at most 1536 / 64 on this path) go out now and are
+  // added, in token-block order, after the logits
+  constexpr int kSigB = 16 * 8 * MAXT / 64;
+  const int nb = (sh.N + 63) / 64;
+  const bool own_sig = threadIdx.x < 16;
+  const bool all_sig = blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x >= 64 && threadIdx.x < 64 + sh.hq;
+  float sg_t[kSigB];
+  if (own_sig || all_sig) {
     const int rr = lb.rb + threadIdx.x;
-    const int h = lb.g * sh.hg + (rr < lb.rows_g ? rr / sh.T : 0);
+    const int h = own_sig ? lb.g * sh.hg + (rr < lb.rows_g ? rr / sh.T : 0) : static_cast<int>(threadIdx.x) - 64;
     const float* part = ws.gpart + lb.p * ws.s_gpart;
-    const int nb = (sh.N + 63) / 64;
-    float sum = 0.f;
-    for (int b0 = 0; b0 < nb; b0 += 16) {
-      float t[16];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) t[k] = part[min(b0 + k, nb - 1) * sh.hq + h];
-#pragma unroll
-      for (int k = 0; k < 16; ++k)
-        if (b0 + k < nb) sum += t[k];
-    }
-    const float mean2 = sum / (static_cast<float>(sh.N) * sh.r);
-    sm_sig[threadIdx.x] = sqrtf(pr.lambda_mass) * fmaxf(sqrtf(mean2), pr.eps_mass);
+    for (int k = 0; k < kSigB; ++k) sg_t[k] = part[min(k, nb - 1) * sh.hq + h];
   }
-  // the head-pattern kernel needs every head's sigma
-  if (blockIdx.x == 0 && blockIdx.y == 0) sigma_from_partials(sh, pr, ws, lb.p);
 
   int hrow[4];
   long long mrow[4];
@@ -504,6 +500,16 @@ logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, c
         for (int e = 0; e < 4; ++e) sv[t][e] = ok ? acc[e] * lb.scale : -INFINITY;
       }
     }
+  }
+  if (own_sig || all_sig) {
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < kSigB; ++k)
+      if (k < nb) sum += sg_t[k];
+    const float mean2 = sum / (static_cast<float>(sh.N) * sh.r);
+    const float sg = sqrtf(pr.lambda_mass) * fmaxf(sqrtf(mean2), pr.eps_mass);
+    if (own_sig) sm_sig[threadIdx.x] = sg;
+    else ws.sig[lb.p * ws.s_sig + threadIdx.x - 64] = sg;
   }
   // log-sum-exp per row: lane, 16-lane group (maximum first), waves
   float mx[4], sm[4];
