@@ -83,15 +83,22 @@ __device__ __forceinline__ uint32_t wave_and_u(uint32_t v) {
 __device__ __forceinline__ uint32_t wave_or_u(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_readlane(wave_scan_or(static_cast<int>(v)), 63));
 }
-// Reduce across the 16 lanes of one MFMA row group (lanes l with equal l/16).
+// Reduce across the 16 lanes of one MFMA row group (lanes l with equal l/16)
+// with DPP moves: two quad butterflies, then rotations by 4 and 8 inside the
+// 16-lane row.  Every lane receives the reduction; for sums the association
+// differs between the row's quads, so callers take one fixed lane's value.
 __device__ __forceinline__ float group16_sum(float v) {
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  v += dpp_f<0xB1, 0xf>(0.f, v);    // quad_perm [1, 0, 3, 2]
+  v += dpp_f<0x4E, 0xf>(0.f, v);    // quad_perm [2, 3, 0, 1]
+  v += dpp_f<0x124, 0xf>(0.f, v);   // row_ror:4
+  v += dpp_f<0x128, 0xf>(0.f, v);   // row_ror:8
   return v;
 }
 __device__ __forceinline__ float group16_max(float v) {
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  v = fmaxf(v, dpp_f<0xB1, 0xf>(v, v));
+  v = fmaxf(v, dpp_f<0x4E, 0xf>(v, v));
+  v = fmaxf(v, dpp_f<0x124, 0xf>(v, v));
+  v = fmaxf(v, dpp_f<0x128, 0xf>(v, v));
   return v;
 }
 
