@@ -83,6 +83,19 @@ __device__ __forceinline__ uint32_t wave_and_u(uint32_t v) {
 __device__ __forceinline__ uint32_t wave_or_u(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_readlane(wave_scan_or(static_cast<int>(v)), 63));
 }
+// The value of lane l ^ O (O < 16) by DPP moves, no LDS round trip: quad
+// permutations for 1 and 2; 4 and 8 compose a quad reversal (l ^ 3) or a row
+// mirror (l ^ 15) with a half-row mirror (l ^ 7).
+template <int O>
+__device__ __forceinline__ float xor_lane(float v) {
+  static_assert(O == 1 || O == 2 || O == 4 || O == 8, "DPP lane exchange inside a 16-lane row");
+  if constexpr (O == 1) return dpp_f<0xB1, 0xf>(v, v);
+  if constexpr (O == 2) return dpp_f<0x4E, 0xf>(v, v);
+  if constexpr (O == 4) return dpp_f<0x141, 0xf>(v, dpp_f<0x1B, 0xf>(v, v));
+  if constexpr (O == 8) return dpp_f<0x141, 0xf>(v, dpp_f<0x140, 0xf>(v, v));
+  return v;
+}
+
 // Reduce across the 16 lanes of one MFMA row group (lanes l with equal l/16)
 // with DPP moves: two quad butterflies, then rotations by 4 and 8 inside the
 // 16-lane row.  Every lane receives the reduction; for sums the association

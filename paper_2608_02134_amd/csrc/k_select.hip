@@ -433,7 +433,8 @@ __device__ __forceinline__ void transpose_reduce_step(float* v, int lane) {
   for (int k = 0; k < O; ++k) {
     const float send = hi ? v[k] : v[k + O];
     const float keep = hi ? v[k + O] : v[k];
-    v[k] = keep + __shfl_xor(send, O, kWave);
+    if constexpr (O < 16) v[k] = keep + xor_lane<O>(send);
+    else v[k] = keep + __shfl_xor(send, O, kWave);
   }
 }
 __device__ __forceinline__ float transpose_reduce64(float* v, int lane) {
@@ -917,7 +918,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       transpose_reduce_step<2>(acc, lane);
       transpose_reduce_step<1>(acc, lane);
       float g = acc[0];             // token lane & 7, summed over 8 lanes
-      g += __shfl_xor(g, 8, kWave);
+      g += xor_lane<8>(g);
       g += __shfl_xor(g, 16, kWave);
       g += __shfl_xor(g, 32, kWave);
       if (lane < 8) rmu[wave][lane] = g;
