@@ -88,12 +88,38 @@ __device__ __forceinline__ uint32_t wave_or_u(uint32_t v) {
 // mirror (l ^ 15) with a half-row mirror (l ^ 7).
 template <int O>
 __device__ __forceinline__ float xor_lane(float v) {
-  static_assert(O == 1 || O == 2 || O == 4 || O == 8, "DPP lane exchange inside a 16-lane row");
+  static_assert(O == 1 || O == 2 || O == 4 || O == 8 || O == 16 || O == 32, "lane exchange by a power of two");
   if constexpr (O == 1) return dpp_f<0xB1, 0xf>(v, v);
   if constexpr (O == 2) return dpp_f<0x4E, 0xf>(v, v);
   if constexpr (O == 4) return dpp_f<0x141, 0xf>(v, dpp_f<0x1B, 0xf>(v, v));
   if constexpr (O == 8) return dpp_f<0x141, 0xf>(v, dpp_f<0x140, 0xf>(v, v));
+  // 16 and 32: a permlane swap of two copies leaves the lane's own value in
+  // one result and its partner's in the other, by the lane's half
+  if constexpr (O == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(((threadIdx.x >> 4) & 1) ? r[0] : r[1]);
+  }
+  if constexpr (O == 32) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(((threadIdx.x >> 5) & 1) ? r[0] : r[1]);
+  }
   return v;
+}
+template <int O>
+__device__ __forceinline__ int xor_lane_i(int v) {
+  return __float_as_int(xor_lane<O>(__int_as_float(v)));
+}
+
+// v[l] + v[l ^ 16] and v[l] + v[l ^ 32] in every lane: a permlane swap of two
+// copies of v puts the partner's value beside the lane's own (the order of
+// the two terms differs between halves; the sum does not).
+__device__ __forceinline__ float add_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float add_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // Reduce across the 16 lanes of one MFMA row group (lanes l with equal l/16)

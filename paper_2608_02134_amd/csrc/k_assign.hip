@@ -87,6 +87,23 @@ __device__ __forceinline__ CosSource<kFromE> cos_source(const Shape& sh, const P
 // cond-grounded-energy; the head-pattern kernel left sum_t nu_t e^2 per head);
 // one wave per token.
 
+// One butterfly step of a wave-wide (largest, second largest) pair.
+template <int O>
+__device__ __forceinline__ void top2_step(float& t1, float& t2) {
+  const float o1 = xor_lane<O>(t1), o2 = xor_lane<O>(t2);
+  const float n1 = fmaxf(t1, o1);
+  const float n2 = fmaxf(fminf(t1, o1), fmaxf(t2, o2));
+  t1 = n1;
+  t2 = n2;
+}
+// One butterfly step of a wave-wide argmax (ties to the lower index).
+template <int O>
+__device__ __forceinline__ void argmax_step(float& best, int& bj) {
+  const float ob = xor_lane<O>(best);
+  const int oj = xor_lane_i<O>(bj);
+  if (ob > best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+}
+
 template <bool kFromE>
 __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
   const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -109,14 +126,12 @@ __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
         else if (v[q] > t2) t2 = v[q];
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float o1 = __shfl_xor(t1, o, kWave), o2 = __shfl_xor(t2, o, kWave);
-      const float n1 = fmaxf(t1, o1);
-      const float n2 = fmaxf(fminf(t1, o1), fmaxf(t2, o2));
-      t1 = n1;
-      t2 = n2;
-    }
+    top2_step<32>(t1, t2);
+    top2_step<16>(t1, t2);
+    top2_step<8>(t1, t2);
+    top2_step<4>(t1, t2);
+    top2_step<2>(t1, t2);
+    top2_step<1>(t1, t2);
     const float delta = (sh.K >= 2) ? t1 - t2 : 0.f;
     if (lane == 0) ws.delta[p * ws.s_del + i] = delta;
     if (sh.T > 0) {
@@ -232,12 +247,12 @@ __global__ void __launch_bounds__(256) kappa_kernel(Shape sh, Params pr, Ws ws, 
         if (j < sh.K && kv[q] > best) { best = kv[q]; bj = j; }
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ob = __shfl_xor(best, o, kWave);
-      const int oj = __shfl_xor(bj, o, kWave);
-      if (ob > best || (ob == best && oj < bj)) { best = ob; bj = oj; }
-    }
+    argmax_step<32>(best, bj);
+    argmax_step<16>(best, bj);
+    argmax_step<8>(best, bj);
+    argmax_step<4>(best, bj);
+    argmax_step<2>(best, bj);
+    argmax_step<1>(best, bj);
     pi_i = sup[(bj >= 0 && bj < sh.K) ? bj : 0];
   }
   if (lane == 0) {

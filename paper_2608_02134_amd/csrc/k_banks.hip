@@ -188,10 +188,10 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       float sv = csum[j], mv = cmax[j];
-      sv += __shfl_xor(sv, 16, kWave);
-      mv = fmaxf(mv, __shfl_xor(mv, 16, kWave));
-      sv += __shfl_xor(sv, 32, kWave);
-      mv = fmaxf(mv, __shfl_xor(mv, 32, kWave));
+      sv = add_xor16(sv);
+      mv = fmaxf(mv, xor_lane<16>(mv));
+      sv = add_xor32(sv);
+      mv = fmaxf(mv, xor_lane<32>(mv));
       if (lane < 16) { cs_sum[wr][wc * WM + j * 16 + oc] = sv; cs_max[wr][wc * WM + j * 16 + oc] = mv; }
     }
   }

@@ -919,8 +919,8 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       transpose_reduce_step<1>(acc, lane);
       float g = acc[0];             // token lane & 7, summed over 8 lanes
       g += xor_lane<8>(g);
-      g += __shfl_xor(g, 16, kWave);
-      g += __shfl_xor(g, 32, kWave);
+      g = add_xor16(g);
+      g = add_xor32(g);
       if (lane < 8) rmu[wave][lane] = g;
       __syncthreads();
       if (tid < 8) {
@@ -1056,8 +1056,8 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       transpose_reduce_step<2>(v, lane);
       transpose_reduce_step<1>(v, lane);
       float tot = v[0];
-      tot += __shfl_xor(tot, 16, kWave);
-      tot += __shfl_xor(tot, 32, kWave);
+      tot = add_xor16(tot);
+      tot = add_xor32(tot);
       if (lane < 16) st_dev64(&tsr[static_cast<long long>(c) * 64 + j0 + lane], tag_value(tag, tot));
       __syncthreads();   // rmu / rden_s are reused by the next chunk
     }
