@@ -1106,9 +1106,33 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     else if (last) break;
     if (tid < bsize) taken[bidx[tid]] = 1;
     if (!last) {
-      // ---- coverage refresh with the batch: one wave per 64-row chunk,
-      //      published with this round's tag
+      // ---- coverage refresh with the batch, published with this round's
+      //      tag: with one chunk per block, by the chunk's responsibility
+      //      block (its pool columns, the batch among them, were just read
+      //      here, so the loads hit this XCD's L2), wave w taking batch
+      //      entries w, w + 4, ...; otherwise one wave per 64-row chunk
       unsigned long long* tcr = tc + (r & 1) * (sh.ldM + kMaxPersist);
+      if (nchunk <= nblk && bsize <= 16) {
+        if (blk < nchunk) {
+          const int m = blk * 64 + lane;
+          const int mc = min(m, sh.m - 1);
+          const float a = al[mc];
+          // the pool holds at most 64 = 4 b entries here, so b <= 16: four
+          // batch entries per wave
+          float v[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            v[q] = E[static_cast<long long>(bidx[min(wave + 4 * q, bsize - 1)]) * sh.ldM + mc];
+          float cm = bl[mc];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (wave + 4 * q < bsize) cm = fmaxf(cm, a * v[q]);
+          rmu[wave][lane] = cm;   // free: last read before the barrier after the batch
+          __syncthreads();
+          if (wave == 0 && m < sh.m)
+            st_dev64(&tcr[m], tag_value(tag, fmaxf(fmaxf(rmu[0][lane], rmu[1][lane]), fmaxf(rmu[2][lane], rmu[3][lane]))));
+        }
+      } else
       for (int c = gw; c < nchunk; c += nwaves) {
         const int m = c * 64 + lane;
         const int mc = min(m, sh.m - 1);
