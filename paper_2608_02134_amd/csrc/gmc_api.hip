@@ -34,10 +34,13 @@ struct Context {
   void* mem = nullptr;
   size_t bytes = 0;
   hipStream_t stream = nullptr;
-  // internal side stream for the bank kernels (default priority) and the
-  // fork/join events that order it against the caller's stream
+  // internal side stream for the bank kernels (default priority); it starts
+  // each call behind a device gate on the row-norm blocks' call tags (one
+  // image) or an event, and joins the caller's stream through a device flag
+  // (an event without text queries)
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
+  int call_tag = 0;   // last call number handed to the row-norm blocks
   int device = 0;
 };
 
@@ -144,7 +147,7 @@ int validate_config(const gmc_config* c) {
 struct Plan {
   Capacity cap;
   long long s_n, s_z, s_zp, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
-      s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_dp, s_gate,
+      s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_ftag, s_gate,
       s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_ts, s_tc, s_lpart, s_lcnt;
 };
 
@@ -195,7 +198,7 @@ Plan make_plan(const gmc_config& c) {
   pl.s_sup = k.N;
   pl.s_cos = static_cast<long long>(k.N) * k.ldK;
   pl.s_del = k.N;
-  pl.s_dp = cdiv(k.N, 4) + 1;
+  pl.s_ftag = cdiv(k.N, 4);
   pl.s_gate = 4;
   pl.s_pi = k.N;
   pl.s_st = kStats;
@@ -244,7 +247,7 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   I(slot); I(sup);
   ws->cosb = reinterpret_cast<float*>(take(pl.s_cos, 4)); ws->s_cos = pl.s_cos;
   ws->delta = reinterpret_cast<float*>(take(pl.s_del, 4)); ws->s_del = pl.s_del;
-  ws->dpart = reinterpret_cast<float*>(take(pl.s_dp, 4)); ws->s_dp = pl.s_dp;
+  I(ftag);
   ws->gate = reinterpret_cast<float*>(take(pl.s_gate, 4)); ws->s_gate = pl.s_gate;
   I(pi);
   ws->stats = reinterpret_cast<float*>(take(pl.s_st, 4)); ws->s_st = pl.s_st;
@@ -532,11 +535,26 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   // kernels run on the caller's stream (they write disjoint client rows).
   // With stage timing on, everything stays on one stream so each stage's
   // span measures that stage alone.
-  err = launch_rownorm(s, c.ws, hidden, st);
-  if (err != hipSuccess) return fail(GMC_ERR_HIP, "row norms: %s", hipGetErrorString(err));
   const bool fork = !g_timer.on;
+  // one image: the fork is a one-block gate on the side stream that waits for
+  // this call's row-norm blocks (no event record on the caller's stream, whose
+  // next kernel would wait for the command processor to process it).  The
+  // gate of the next call may already wait while this call's selection runs,
+  // so with several images, whose persistent selection takes every CU, an
+  // event is used instead.
+  const bool gate = fork && s.B == 1;
+  int call_tag = 0;
+  if (gate) {
+    c.call_tag = c.call_tag == 0x7fffffff ? 1 : c.call_tag + 1;
+    call_tag = c.call_tag;
+  }
+  err = launch_rownorm(s, c.ws, hidden, call_tag, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "row norms: %s", hipGetErrorString(err));
   hipStream_t bank_st = fork ? c.side : st;
-  if (fork) {
+  if (gate) {
+    err = launch_bank_gate(s, c.ws, call_tag, c.side);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
+  } else if (fork) {
     err = hipEventRecord(c.fork, st);
     if (err == hipSuccess) err = hipStreamWaitEvent(c.side, c.fork, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));

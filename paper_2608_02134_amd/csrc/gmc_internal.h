@@ -83,7 +83,7 @@ struct Ws {
   float* cosb;     long long s_cos;     // cos to support               [N][ldK]
   float* delta;    long long s_del;     // selected-cosine gap          [N]
   float* gate;     long long s_gate;    // s_x, mean gap                [4]
-  float* dpart;    long long s_dp;      // per-block energy partials    [N/4+1]
+  int* ftag;       long long s_ftag;    // row-norm blocks done: call number [ceil(N/4)]
   int* pi;         long long s_pi;      // assignment                   [N]
   float* stats;    long long s_st;      // diagnostics                  [kStats]
   uint32_t* keys;  long long s_keys;    // top-k keys when N exceeds LDS [N]
@@ -115,7 +115,8 @@ __device__ __forceinline__ void call_init_range(const Shape& sh, const Ws& ws, i
   for (int j = x0; j < 128 * ((sh.m + 63) / 64); j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
   for (int j = x0; j < 2 * (sh.ldM + kMaxPersist); j += stride) ws.tc[p * ws.s_tc + j] = 0ull;
   for (int j = x0; j < (sh.hg * sh.T + 15) / 16 * sh.hkv; j += stride) ws.lcnt[p * ws.s_lcnt + j] = 0;
-  if (x0 < kCounters) ws.cnt[p * ws.s_cnt + x0] = 0;
+  // written through: the bank stream raises its flag in these words
+  if (x0 < kCounters) __hip_atomic_store(&ws.cnt[p * ws.s_cnt + x0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 #endif
 

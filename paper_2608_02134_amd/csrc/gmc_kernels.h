@@ -18,7 +18,11 @@ enum Stage {
 void timer_mark(int stage, bool begin, hipStream_t st);
 
 // Squared row norms of the visual states (every later stage reads them).
-hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, hipStream_t st);
+// call_tag != 0: every block also tags itself done with it for the gate.
+hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, int call_tag, hipStream_t st);
+
+// One block that returns once every row-norm block carries call_tag.
+hipError_t launch_bank_gate(const Shape& sh, const Ws& ws, int call_tag, hipStream_t st);
 
 // Value probe, mass coordinate, native slice, head weights, grounded row
 // weights and normalised energy (after launch_rownorm).  With bank_flag set

@@ -17,12 +17,12 @@ namespace gmc {
 // kernel resets the per-call state, being the first of every call.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* hidden) {
+__global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* hidden, int call_tag) {
   const int p = blockIdx.y;
   // the call's first kernel also resets the per-call state
   call_init_range(sh, ws, p, blockIdx.x * 256 + threadIdx.x, gridDim.x * 256);
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (i >= sh.N) return;
+  if (i < sh.N) {
   const T* row = hidden + (static_cast<long long>(p) * sh.N + i) * sh.d;
   float s = 0.f;
 #pragma unroll 4
@@ -43,7 +43,54 @@ __global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* 
     }
   }
   s = wave_sum(s);
-  if (lane == 0) ws.n2[p * ws.s_n + i] = s;
+  // written through: the bank stream reads the norms without a kernel
+  // boundary in between
+  if (lane == 0) __hip_atomic_store(&ws.n2[p * ws.s_n + i], s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  if (call_tag != 0) {
+    // this block is done (its written-through stores have completed): tag it
+    // with the call number for the bank stream's gate
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0)
+      __hip_atomic_store(&ws.ftag[p * ws.s_ftag + blockIdx.x], call_tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// The bank stream's first kernel: one block waits until every row-norm block
+// of the call has tagged itself (bounded), so the bank kernels that follow on
+// that stream see the norms and the per-call reset, and start only after the
+// caller's stream has finished the previous call.
+__global__ void __launch_bounds__(256) bank_gate_kernel(Shape sh, Ws ws, int call_tag) {
+  const int nb = (sh.N + 3) / 4, total = nb * sh.B;
+  for (int x0 = 0; x0 < total; x0 += 256 * 8) {
+    int v[8];
+    bool need[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int x = x0 + q * 256 + static_cast<int>(threadIdx.x);
+      need[q] = x < total;
+      const int xc = min(x, total - 1), p = xc / nb, b = xc % nb;
+      v[q] = __hip_atomic_load(&ws.ftag[p * ws.s_ftag + b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    for (int spin = 0;; ++spin) {
+      bool pend = false;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) pend |= need[q] && v[q] != call_tag;
+      if (!pend) break;
+      if (spin == kBankSpinLimit) {
+        __hip_atomic_store(&ws.cnt[kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(8);   // a light poll: it may wait through a whole selection
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (!need[q] || v[q] == call_tag) continue;
+        const int x = x0 + q * 256 + static_cast<int>(threadIdx.x), p = x / nb, b = x % nb;
+        v[q] = __hip_atomic_load(&ws.ftag[p * ws.s_ftag + b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
 }
 
 // Probe GEMM epilogue: Z[i][c] = (h_i . G_c) / sqrt(mean h_i^2 + eps), the
@@ -1064,15 +1111,20 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   return hipGetLastError();
 }
 
-hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, hipStream_t st) {
+hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, int call_tag, hipStream_t st) {
   timer_mark(kStInit, true, st);
   if (sh.dtype == 0)
     hipLaunchKernelGGL(rownorm_kernel<float>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, ws,
-                       static_cast<const float*>(hidden));
+                       static_cast<const float*>(hidden), call_tag);
   else
     hipLaunchKernelGGL(rownorm_kernel<bf16_t>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, ws,
-                       static_cast<const bf16_t*>(hidden));
+                       static_cast<const bf16_t*>(hidden), call_tag);
   timer_mark(kStInit, false, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_bank_gate(const Shape& sh, const Ws& ws, int call_tag, hipStream_t st) {
+  hipLaunchKernelGGL(bank_gate_kernel, dim3(1), dim3(256), 0, st, sh, ws, call_tag);
   return hipGetLastError();
 }
 

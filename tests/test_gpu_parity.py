@@ -129,6 +129,35 @@ def test_bitwise_repeatable():
         assert np.array_equal(outs1[0][key], outs2[0][key]), key
 
 
+@pytest.mark.parametrize("name", ["qwen", "batch16"])
+def test_back_to_back_calls(name):
+    """Calls queued without synchronisation (the next call's bank stream may
+    start while this call's selection runs) give the synchronised call's
+    outputs bit for bit, with the device status clear."""
+    from .gpu_run import from_device, to_device
+    spec = dict(name=name) if name == "qwen" else dict(name=name, batch=4)
+    prob = synth.make_problem(**spec)
+    _announce(f"back-to-back {name}", prob)
+    ref, pr = run(prob, torch)
+    w = prob.workload
+    hid = to_device(prob.hidden, w.dtype, torch)
+    q = to_device(prob.text_q, w.dtype, torch)
+    kk = to_device(prob.vis_k, w.dtype, torch)
+    pos = torch.from_numpy(prob.pos3d).cuda()
+    try:
+        for _ in range(6):
+            pr.prune(hid, q, kk, pos, prob.k, trace=False)
+        res = pr.prune(hid, q, kk, pos, prob.k, trace=True)
+        torch.cuda.synchronize()
+        for b in range(w.batch):
+            assert np.array_equal(res[2][b].cpu().numpy(), ref[b]["out_idx"])
+            assert np.array_equal(res[1][b].cpu().numpy(), ref[b]["out_pos"])
+            assert np.array_equal(from_device(res[0][b], torch), ref[b]["out_hidden"])
+            assert res[3]["stats"][b][8].item() == 0.0
+    finally:
+        pr.close()
+
+
 def test_capacity_and_argument_errors():
     from paper_2608_02134_amd import binding
     prob = synth.make_problem("tiny", grid=(1, 8, 8), t=4, k=10)
