@@ -120,15 +120,27 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
   for (int s = 0; s < S; ++s) load(s, ra[s], rb[s]);
   store(0, ra[0], rb[0]);
   __syncthreads();
-  for (int kt = 0; kt < nk; kt += S) {
+  // The main loop runs whole groups of S steps with no exit inside the
+  // group, so every path into its head has the same loads in flight and the
+  // compiler's wait counts stay exact (an exit inside the unrolled group
+  // merges those paths and forces a wait for every load at the head).  The
+  // last nk % S slabs are already loaded: the tail only computes and stores.
+  const int nk_main = nk - nk % S;
+  for (int kt = 0; kt < nk_main; kt += S) {
 #pragma unroll
     for (int s = 0; s < S; ++s) {
-      if (kt + s >= nk) break;
       load(kt + s + S, ra[s], rb[s]);
       compute(s & 1);
       store((s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
       __syncthreads();
     }
+  }
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s) {
+    if (nk_main + s >= nk) break;
+    compute(s & 1);
+    store((s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
+    __syncthreads();
   }
 
   // epilogue: lane holds column (lane & 15), rows 4 (lane >> 4) + e of each
