@@ -107,6 +107,13 @@ typedef struct gmc_config {
   int32_t bounded_threshold_n;          /* 4096: N above it uses the bounded bank */
   int32_t app_rank, app_max_clients;    /* 128, 4096                          */
   int32_t batch_b_bounded;              /* 512                                */
+  /* optional device input fixed for the context's lifetime (caller-owned)  */
+  const float* value_probe_bias; /* [Hq][r] fp32 or NULL (zero): the value
+                                    projection's bias carried through the same
+                                    folded path, b_h = b^V_kv(h) O_h P, for
+                                    models whose V projection has a bias; then
+                                    Z_h[i] = x~_i G_h + b_h (Eq. cond-mass-
+                                    coordinate with V = x~ W^V + b^V)        */
 } gmc_config;
 
 /*

@@ -101,7 +101,8 @@ READINGS = {
     "R3": "native nonvisual softmax denominator enters as an optional per-(h,t) "
           "log-sum-exp; P^G is invariant to it",
     "R4": "value path folded into a per-head probe G_h [r][d]; x~ = RMSNorm(h) "
-          "with eps 1e-6 and unit gain",
+          "with eps 1e-6 and unit gain; an optional value bias folds into "
+          "b_h = b^V O_h P added to Z_h[i]",
     "R5": "local ambiguity g_i = exp(-(delta_i/0.05)^8) (hard variant: "
           "1[delta_i < 0.05])",
     "R6": "spatial coordinates are grid-cell centres in [0,1]^2 from (h,w); "
@@ -140,9 +141,13 @@ def row_features(h: np.ndarray, p: GmcParams):
     return norm, x, rms, xt
 
 
-def value_probe(xt: np.ndarray, probe: np.ndarray) -> np.ndarray:
-    """Z_h = (V_h O_h) P as one folded per-head map: Z[h][i][c] = x~_i . G[h][c]."""
-    return np.einsum("nd,hrd->hnr", xt, np.asarray(probe, np.float64))
+def value_probe(xt: np.ndarray, probe: np.ndarray, bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """Z_h = (V_h O_h) P as one folded per-head map: Z[h][i][c] = x~_i . G[h][c]
+    (+ b[h][c] = (b^V O_h P)[c] when the value projection has a bias b^V)."""
+    z = np.einsum("nd,hrd->hnr", xt, np.asarray(probe, np.float64))
+    if bias is not None:
+        z = z + np.asarray(bias, np.float64)[:, None, :]
+    return z
 
 
 def mass_coordinate(z: np.ndarray, p: GmcParams) -> np.ndarray:
@@ -519,14 +524,14 @@ def compact(support: np.ndarray, htilde: np.ndarray, pos: np.ndarray):
 # ----------------------------------------------------------------------------
 # The whole operator for one image (Algorithm 1, steps 2-6)
 # ----------------------------------------------------------------------------
-def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=None):
+def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=None, probe_bias=None):
     """Steps 2 of Algorithm 1: the three client banks and all message-side
     quantities.  Returns a dict of intermediates."""
     h = np.asarray(h, np.float64)
     n = h.shape[0]
     t = q.shape[0]
     norm, x, rms, xt = row_features(h, p)
-    z = value_probe(xt, probe)
+    z = value_probe(xt, probe, probe_bias)
     sigma = mass_coordinate(z, p)
     hq = probe.shape[0]
     nu = query_weights(t, p)
@@ -585,7 +590,7 @@ def bank_saturation(cbar: np.ndarray, banks: np.ndarray, support) -> dict:
 
 
 def gmc_single(h, q, k, pos, probe, k_req: int, p: GmcParams = GmcParams(),
-               app_proj=None, nonvis_lse=None, keep_intermediates: bool = False):
+               app_proj=None, nonvis_lse=None, keep_intermediates: bool = False, probe_bias=None):
     """One problem end to end: budget, clients, selection, assignment,
     transport and compaction.  Returns out_hidden (fp64, before the cast to
     the residual dtype), out_pos, out_idx and diagnostics."""
@@ -595,7 +600,7 @@ def gmc_single(h, q, k, pos, probe, k_req: int, p: GmcParams = GmcParams(),
     if kk == n:
         return dict(out_hidden=h.copy(), out_pos=np.asarray(pos).copy(),
                     out_idx=np.arange(n, dtype=np.int64), identity=True, k=kk)
-    cl = build_clients(h, q, k, pos, probe, p, app_proj, nonvis_lse)
+    cl = build_clients(h, q, k, pos, probe, p, app_proj, nonvis_lse, probe_bias)
     b = p.batch_b_bounded if cl["bounded"] else p.batch_b
     sel = select_support(cl["cbar"], kk, b, p)
     asg = assign_population(cl["x"], cl["pc"], sel["order"], p)
@@ -612,10 +617,10 @@ def gmc_single(h, q, k, pos, probe, k_req: int, p: GmcParams = GmcParams(),
 
 
 def gmc(hidden, text_q, vis_k, pos3d, probe, k_req: int, p: GmcParams = GmcParams(),
-        app_proj=None, nonvis_lse=None):
+        app_proj=None, nonvis_lse=None, probe_bias=None):
     """Batched entry: independent problems, same shapes."""
     return [gmc_single(hidden[i], text_q[i], vis_k[i], pos3d[i], probe, k_req, p, app_proj,
-                       None if nonvis_lse is None else nonvis_lse[i])
+                       None if nonvis_lse is None else nonvis_lse[i], probe_bias=probe_bias)
             for i in range(hidden.shape[0])]
 
 

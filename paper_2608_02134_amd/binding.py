@@ -43,6 +43,7 @@ class GmcConfig(ctypes.Structure):
         ("bounded_threshold_n", _i32),
         ("app_rank", _i32), ("app_max_clients", _i32),
         ("batch_b_bounded", _i32),
+        ("value_probe_bias", _vp),
     ]
 
 
@@ -153,13 +154,14 @@ class Pruner:
     """Owns one library context for a model shape and capacity.
 
     ``probe`` [Hq][r][d] and ``app_projection`` [app_rank][d] are device
-    tensors in the operator dtype; the wrapper keeps them alive.  ``prune``
+    tensors in the operator dtype, ``probe_bias`` [Hq][r] an optional fp32
+    device tensor; the wrapper keeps them alive.  ``prune``
     allocates outputs with torch and calls gmc_prune_ex on torch's current
     stream.
     """
 
     def __init__(self, *, d, n_q_heads, n_kv_heads, head_dim, probe, dtype, max_batch, max_n,
-                 max_t, max_k=0, app_projection=None, **overrides):
+                 max_t, max_k=0, app_projection=None, probe_bias=None, **overrides):
         import torch
         self.torch = torch
         cfg = gmc_config_default()
@@ -173,6 +175,11 @@ class Pruner:
         self.app_projection = None if app_projection is None else app_projection.contiguous()
         cfg.value_probe = self.probe.data_ptr()
         cfg.app_projection = 0 if self.app_projection is None else self.app_projection.data_ptr()
+        self.probe_bias = None if probe_bias is None else probe_bias.contiguous()
+        if self.probe_bias is not None and (self.probe_bias.dtype != torch.float32 or
+                                            tuple(self.probe_bias.shape) != (n_q_heads, cfg.probe_rank)):
+            raise ValueError("probe_bias must be a float32 [n_q_heads][probe_rank] tensor")
+        cfg.value_probe_bias = 0 if self.probe_bias is None else self.probe_bias.data_ptr()
         self.cfg = cfg
         self.dtype = dtype
         _check(gmc_init(cfg), "gmc_init")

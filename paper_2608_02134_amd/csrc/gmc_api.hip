@@ -101,6 +101,7 @@ Params make_params(const gmc_config& c) {
   p.pop_strength = c.pop_strength; p.tau_j = c.tau_j; p.max_head_clusters = c.max_head_clusters;
   p.disp_eps = c.disp_eps; p.terminal_q_weight = c.terminal_q_weight; p.rms_eps = c.rms_eps;
   p.norm_eps = c.norm_eps; p.restore_eps = c.restore_eps; p.pool_mult = c.pool_mult;
+  p.probe_bias = c.value_probe_bias;
   return p;
 }
 

@@ -47,6 +47,7 @@ struct Params {
   int max_head_clusters;
   float disp_eps, terminal_q_weight, rms_eps, norm_eps, restore_eps;
   int pool_mult;
+  const float* probe_bias;   // [hq][r] or null: b_h added to Z_h[i]
 };
 
 // Workspace: every buffer is [max_batch][per-problem size]; s_* are the

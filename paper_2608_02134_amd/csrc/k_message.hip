@@ -113,7 +113,7 @@ struct ProbeSplitEpi {
 };
 
 // Z_h[i] = rms(h_i)^-1 sum_s partial_s (the next block's RMSNorm, unit gain)
-// and q_h[i] = ||Z_h[i]||^2, stored in place of the atom norm: consumers form
+// plus the folded value bias b_h when one is configured, and q_h[i] = ||Z_h[i]||^2, stored in place of the atom norm: consumers form
 // l_h[i] = ||[Z_h[i]; sigma_h]|| = sqrt(q_h[i] + sigma_h^2).  One wave per
 // (head, 64 tokens), lane = token; per-(block, head) sums of q are left for
 // sigma_h = sqrt(lambda) max(sqrt(sum q / (N r)), eps), which the first
@@ -158,7 +158,8 @@ __global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws 
 #pragma unroll
     for (int c = 0; c < kMaxProbe; ++c) {
       if (c < sh.r) {
-        const float zc = (((v[0][c] + v[1][c]) + v[2][c]) + v[3][c]) * rs;
+        const float zs = (((v[0][c] + v[1][c]) + v[2][c]) + v[3][c]) * rs;
+        const float zc = pr.probe_bias ? zs + pr.probe_bias[h * sh.r + c] : zs;
         q += zc * zc;
         if (i < sh.N) z[c] = zc;
       }

@@ -18,14 +18,15 @@ def from_device(t, torch) -> np.ndarray:
     return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
 
 
-def make_pruner(prob: synth.Problem, torch, max_k=0, **overrides):
+def make_pruner(prob: synth.Problem, torch, max_k=0, probe_bias=None, **overrides):
     w = prob.workload
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     probe = to_device(prob.probe, w.dtype, torch)
     proj = None if prob.app_proj is None else to_device(prob.app_proj, w.dtype, torch)
+    bias = None if probe_bias is None else torch.from_numpy(np.ascontiguousarray(probe_bias, np.float32)).cuda()
     return binding.Pruner(d=w.d, n_q_heads=w.hq, n_kv_heads=w.hkv, head_dim=w.dh, probe=probe,
                           dtype=tdt, max_batch=w.batch, max_n=w.n, max_t=max(w.t, 1),
-                          max_k=max_k, app_projection=proj, **overrides)
+                          max_k=max_k, app_projection=proj, probe_bias=bias, **overrides)
 
 
 def run(prob: synth.Problem, torch, k=None, trace=True, nonvis=None, pruner=None, **overrides):

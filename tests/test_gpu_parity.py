@@ -119,6 +119,27 @@ def test_hard_ambiguity_gate():
     _check_all(prob, outs, params=O.GmcParams(g_form="hard"))
 
 
+def test_value_probe_bias():
+    # the folded value bias b_h shifts every Z_h[i]; scaled like Z itself so
+    # it moves sigma, the atom norms and the head weights
+    prob = synth.make_problem("qwen", grid=(1, 20, 21), t=24, k=83)
+    w = prob.workload
+    _, _, _, xt = O.row_features(prob.hidden[0], O.GmcParams())
+    zs = float(np.std(O.value_probe(xt, prob.probe)))
+    bias = (np.random.default_rng(11).standard_normal((w.hq, prob.probe.shape[1])) * zs).astype(np.float32)
+    _announce("probe bias", prob)
+    outs, pr = run(prob, torch, probe_bias=bias)
+    pr.close()
+    g = outs[0]
+    rep = check_problem(prob.hidden[0], prob.text_q[0], prob.vis_k[0], prob.pos3d[0], prob.probe,
+                        prob.k, g, w.dtype, O.GmcParams(), prob.app_proj, None, bias)
+    print(f"  problem 0: {rep}", flush=True)
+    # not vacuous: without the bias the oracle's head weights differ
+    cl0 = O.build_clients(prob.hidden[0], prob.text_q[0], prob.vis_k[0], prob.pos3d[0], prob.probe,
+                          O.GmcParams())
+    assert np.max(np.abs(cl0["omega"] - g["omega"])) > 1e-3
+
+
 def test_bitwise_repeatable():
     prob = synth.make_problem("qwen", grid=(1, 16, 16), t=16, k=50)
     _announce("repeat", prob)

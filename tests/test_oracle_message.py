@@ -141,6 +141,30 @@ def test_mass_coordinate_of_identical_tokens():
         assert sig[hh] == pytest.approx(np.linalg.norm(z0) / 2.0, rel=1e-12)
 
 
+def test_folded_value_probe_with_bias():
+    # Z_h = (V_h O_h) P with V = x~ W^V + b^V, computed step by step, equals
+    # the folded map x~ G_h + b_h with G_h = (W^V O_h P)^T and b_h = b^V O_h P
+    rng = np.random.default_rng(21)
+    n, d, dh, r, hq = 7, 24, 8, 4, 3
+    h = rng.standard_normal((n, d))
+    wv = rng.standard_normal((hq, d, dh))
+    bv = rng.standard_normal((hq, dh))
+    o = rng.standard_normal((hq, dh, d))
+    pr, _ = np.linalg.qr(rng.standard_normal((d, r)))
+    _, _, _, xt = O.row_features(h, P)
+    g = np.zeros((hq, r, d))
+    bias = np.zeros((hq, r))
+    ref = np.zeros((hq, n, r))
+    for hh in range(hq):
+        v = xt @ wv[hh] + bv[hh]
+        ref[hh] = (v @ o[hh]) @ pr
+        g[hh] = (wv[hh] @ o[hh] @ pr).T
+        bias[hh] = bv[hh] @ o[hh] @ pr
+    np.testing.assert_allclose(O.value_probe(xt, g, bias), ref, rtol=1e-10, atol=1e-10)
+    # without the bias term the folded map misses exactly b_h on every token
+    np.testing.assert_allclose(O.value_probe(xt, g), ref - bias[:, None, :], rtol=1e-10, atol=1e-10)
+
+
 def test_rmsnorm_features():
     # x~ = h / sqrt(mean h^2 + eps): mean square ms/(ms+eps); x is unit
     h, *_ = _small(9)
