@@ -55,13 +55,16 @@ extern "C" {
 #define GMC_BF16 1
 
 /* Number of float entries gmc_trace.stats receives per problem. */
-#define GMC_STATS 9
+#define GMC_STATS 15
 /* stats layout: [0] s_x  [1] mean selected-cosine gap over discarded tokens
  *               [2] F(S)  [3] F(V)  [4] realised K  [5] rounds  [6] M rows
  *               [7] number of discarded tokens
  *               [8] device status: 0 ok; 1 = a bounded device wait (a
  *                   hand-off of the persistent selection, or the wait for
- *                   the bank kernels) timed out (results invalid)         */
+ *                   the bank kernels) timed out (results invalid)
+ *               [9..11]  F_b(S) of the grounded, appearance, spatial bank
+ *               [12..14] F_b(V) of the same banks; omega_b = F_b(V)/F(V)
+ *                   and c_b = F_b(S)/F_b(V) (Eq. cond-bank-mixture)       */
 
 /*
  * gmc_config - model shape, capacities and the frozen settings.

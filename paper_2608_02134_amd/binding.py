@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libgmc.so")
 
 GMC_OK, GMC_ERR_ARG, GMC_ERR_CAPACITY, GMC_ERR_STATE, GMC_ERR_HIP = 0, -1, -2, -3, -4
 GMC_F32, GMC_BF16 = 0, 1
-GMC_STATS = 9
+GMC_STATS = 15
 
 _i32, _f32, _i64, _vp = ctypes.c_int32, ctypes.c_float, ctypes.c_int64, ctypes.c_void_p
 

@@ -11,7 +11,7 @@ constexpr int kMaxHeads = 32;     // Hq limit (head-pattern Gram kept in registe
 constexpr int kMaxProbe = 8;      // probe rank limit
 constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 8;       // tokens per head-Gram block (two per wave)
-constexpr int kStats = 9;
+constexpr int kStats = 15;
 constexpr int kCounters = 8;      // completion counters per problem
 constexpr int kCntBankFlag = 6;   // slot of problem 0: the bank kernels of the call have finished
 constexpr int kCntStatus = 7;     // device status bits, 1 = a bounded device wait timed out

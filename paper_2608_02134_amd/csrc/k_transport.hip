@@ -228,11 +228,33 @@ __global__ void export_client_kernel(Shape sh, Ws ws, float* out) {
     o[i] = a * E[static_cast<long long>(i) * sh.ldM];
 }
 
+// One wave per problem: the selection's statistics, the device status word
+// (completion-counter slot 7) and the per-bank objectives F_b(S) = sum of the
+// final coverage b_m and F_b(V) = sum of max_i Cbar_mi over the bank's rows
+// (grounded, appearance, spatial), from which omega_b = F_b(V) / F(V) and the
+// saturation c_b = F_b(S) / F_b(V) follow (Eq. cond-bank-mixture).
 __global__ void export_stats_kernel(Shape sh, Ws ws, float* out) {
-  const int p = blockIdx.x;
-  // the last entry is the device status word (completion-counter slot 7)
-  if (threadIdx.x < kStats - 1) out[p * kStats + threadIdx.x] = ws.stats[p * ws.s_st + threadIdx.x];
-  if (threadIdx.x == kStats - 1) out[p * kStats + threadIdx.x] = static_cast<float>(ws.cnt[p * ws.s_cnt + 7]);
+  const int p = blockIdx.x, t = threadIdx.x;
+  float* o = out + p * kStats;
+  if (t < 8) o[t] = ws.stats[p * ws.s_st + t];
+  if (t == 8) o[8] = static_cast<float>(ws.cnt[p * ws.s_cnt + 7]);
+  const float* cov = ws.cov + p * ws.s_cov;
+  const float* peak = ws.peak + p * ws.s_m;
+  const int lo[3] = {0, sh.mg, sh.mg + sh.mv}, hi[3] = {sh.mg, sh.mg + sh.mv, sh.m};
+#pragma unroll
+  for (int b = 0; b < 3; ++b) {
+    float fs = 0.f, fv = 0.f;
+    for (int m = lo[b] + t; m < hi[b]; m += 64) {
+      fs += cov[m];
+      fv += peak[m];
+    }
+    fs = wave_sum(fs);
+    fv = wave_sum(fv);
+    if (t == 0) {
+      o[9 + b] = fs;
+      o[12 + b] = fv;
+    }
+  }
 }
 
 __global__ void export_ebar_kernel(Shape sh, Ws ws, float* out) {

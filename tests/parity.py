@@ -190,6 +190,14 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
         assert abs(st[2] - fs) <= 1e-4 * fs, f"F(S) {st[2]} vs {fs}"
         fv = float(cbar.max(axis=1).sum())
         assert abs(st[3] - fv) <= 1e-4 * fv, f"F(V) {st[3]} vs {fv}"
+        # per-bank objectives (grounded, appearance, spatial): omega_b and
+        # the saturation c_b of the bank mixture follow from them
+        for bank in (0, 1, 2):
+            rows = cl["banks"] == bank
+            fsb = float(cov[rows].sum()) if rows.any() else 0.0
+            fvb = float(cbar[rows].max(axis=1).sum()) if rows.any() else 0.0
+            assert abs(st[9 + bank] - fsb) <= 1e-4 * fs, f"F_{bank}(S) {st[9 + bank]} vs {fsb}"
+            assert abs(st[12 + bank] - fvb) <= 1e-4 * fv, f"F_{bank}(V) {st[12 + bank]} vs {fvb}"
     free = O.select_support(cbar, kk, b, p)
     rep.identical_to_free_oracle = bool(np.array_equal(np.sort(free["order"]), support))
     if rep.pool_near_ties == 0 and rep.batch_near_ties == 0:

@@ -47,6 +47,16 @@ def test_config_layout_round_trips_defaults(lib):
     assert c.bounded_threshold_n == 4096 and c.app_rank == 128
     assert c.app_max_clients == 4096 and c.batch_b_bounded == 512  # last field: layout intact
     assert c.value_probe is None and c.app_projection is None
+    assert c.value_probe_bias is None   # appended last: optional, zero by default
+
+
+def test_header_constants_match_binding():
+    src = open(HEADER).read()
+    consts = dict((k, int(v)) for k, v in re.findall(r"#define\s+(GMC_[A-Z0-9_]+)\s+\(?(-?\d+)\)?", src))
+    assert consts["GMC_STATS"] == B.GMC_STATS
+    assert (consts["GMC_OK"], consts["GMC_ERR_ARG"], consts["GMC_ERR_CAPACITY"], consts["GMC_ERR_STATE"],
+            consts["GMC_ERR_HIP"]) == (B.GMC_OK, B.GMC_ERR_ARG, B.GMC_ERR_CAPACITY, B.GMC_ERR_STATE, B.GMC_ERR_HIP)
+    assert (consts["GMC_F32"], consts["GMC_BF16"]) == (B.GMC_F32, B.GMC_BF16)
 
 
 @pytest.mark.parametrize("n,k,want", [(10, 20, 10), (10, 0, 1), (10, -4, 1), (10, 3, 3), (0, 5, 0)])
