@@ -52,7 +52,8 @@ __all__ = [
     "responsibility_scores", "top_by_score", "select_support",
     "assignment_gaps", "separability_gate", "ambiguity_gate",
     "assign_population", "population_weights", "transport", "compact",
-    "gmc_single", "gmc", "prune_rounds",
+    "gmc_single", "gmc", "prune_rounds", "index_map", "compact_sequence",
+    "gather_cache",
 ]
 
 
@@ -519,6 +520,47 @@ def compact(support: np.ndarray, htilde: np.ndarray, pos: np.ndarray):
     order = np.argsort(sup, kind="stable")
     idx = sup[order]
     return idx, htilde[order], pos[idx]
+
+
+# ----------------------------------------------------------------------------
+# Sequence compaction after pruning (App. H "Index map and physical token
+# accounting"; the cached deployment gathers prefix K/V by the same indices)
+# ----------------------------------------------------------------------------
+def index_map(seq_len: int, vis_start: int, n: int, kept_visual):
+    """iota over the original positions of a sequence whose visual tokens sit
+    at [vis_start, vis_start + n): the visual positions not kept are deleted
+    and every retained position keeps its order.  Returns iota (new position,
+    -1 for a deleted one) and keep (the retained original positions, i.e. the
+    inverse map), walking the sequence once."""
+    kept = {vis_start + int(j) for j in kept_visual}
+    iota = np.full(seq_len, -1, dtype=np.int64)
+    keep = []
+    for i in range(seq_len):
+        if vis_start <= i < vis_start + n and i not in kept:
+            continue
+        iota[i] = len(keep)
+        keep.append(i)
+    return iota, np.asarray(keep, dtype=np.int64)
+
+
+def compact_sequence(seq_rows, vis_rows, seq_pos, vis_start: int, n: int, kept_visual):
+    """The boundary sequence after compaction: text positions keep their
+    states, the retained visual token j receives its transported state (row k
+    of vis_rows for the k-th kept token, ascending), and every retained
+    position keeps its original position ids.  Returns iota, keep, the rows
+    and the position ids."""
+    seq_rows = np.asarray(seq_rows)
+    iota, keep = index_map(seq_rows.shape[0], vis_start, n, kept_visual)
+    out = seq_rows[keep].copy()
+    for k, j in enumerate(np.asarray(kept_visual, dtype=np.int64)):
+        out[iota[vis_start + j]] = np.asarray(vis_rows)[k]
+    return iota, keep, out, np.asarray(seq_pos)[keep]
+
+
+def gather_cache(cache, keep):
+    """Prefix-layer cache rows gathered at the retained original positions
+    (axis -2 is the sequence axis)."""
+    return np.take(np.asarray(cache), np.asarray(keep, dtype=np.int64), axis=-2)
 
 
 # ----------------------------------------------------------------------------
