@@ -216,6 +216,56 @@ int gmc_trace_dims(int64_t N, int64_t T, int64_t K, int64_t* rounds, int64_t* po
 int gmc_timing_enable(int enable);
 int gmc_timing_read(double* total_ms, int64_t* spans, int32_t n);
 
+/*
+ * Sequence compaction after pruning (App. H "Index map and physical token
+ * accounting"; the cached deployment gathers prompt K/V of the prefix layers
+ * at the retained sequence indices).  B sequences of L positions each hold
+ * their N visual tokens at [vis_start, vis_start + N); out_idx [B][K] int32
+ * (device) holds the K retained visual tokens of each, strictly ascending in
+ * [0, N), as gmc_prune returns them.  The compacted length is
+ * L2 = L - N + K, and position i maps to iota(i): unchanged before the visual
+ * span, vis_start + k for the k-th retained visual token, i - (N - K) after
+ * the span, -1 for a deleted visual position (order preserving).
+ *
+ * gmc_compact_sequence - for every sequence: (all device pointers, [B] leading)
+ *   iota     [B][L]   int32 out, or NULL: the map above
+ *   keep     [B][L2]  int32 out, or NULL: the retained original positions
+ *            (the inverse map), the index list gmc_gather_rows takes
+ *   seq_rows [B][L][row_bytes] in, out_rows [B][L2][row_bytes] out, vis_rows
+ *            [B][K][row_bytes] in (the transported states, e.g. gmc_prune's
+ *            out_hidden), all NULL or all set: text positions keep their
+ *            row, the k-th retained visual position receives vis_rows row k
+ *   seq_pos  [B][L][3] int32 in, out_pos [B][L2][3] int32 out, both NULL or
+ *            both set: every retained position keeps its original ids
+ * row_bytes is a positive multiple of 16, rows 16-byte aligned; 0 <= vis_start,
+ * vis_start + N <= L, 1 <= K <= N.  out_idx entries that are not strictly
+ * ascending in [0, N) give unspecified (but in-bounds) results.  Outputs
+ * must not overlap inputs.  Runs on the context stream; needs a context (the
+ * workspace is not used).  Errors: GMC_ERR_ARG, GMC_ERR_STATE, GMC_ERR_HIP.
+ */
+int gmc_compact_sequence(int64_t B, int64_t L, int64_t vis_start, int64_t N, int64_t K,
+                         const int32_t* out_idx, int32_t* iota, int32_t* keep, const void* seq_rows,
+                         const void* vis_rows, void* out_rows, int64_t row_bytes, const int32_t* seq_pos,
+                         int32_t* out_pos);
+
+/*
+ * gmc_gather_rows - gather the rows of n_tensors caches at retained original
+ * positions: dst[t][s][j] = src[t][s][keep[s / seqs_per_keep][j]] for every
+ * tensor t < n_tensors, sequence s < n_seq and j < L2, rows of row_bytes
+ * bytes.  src and dst are host arrays of n_tensors device pointers, each
+ * tensor laid out [n_seq][L][row_bytes] (source) and [n_seq][L2][row_bytes]
+ * (destination); seqs_per_keep consecutive sequences share one keep list
+ * (keep [n_seq / seqs_per_keep][L2] int32, device, entries in [0, L)), e.g.
+ * the heads of a head-major [B][Hkv][L][dh] cache with seqs_per_keep = Hkv,
+ * or 1 for a token-major [B][L][Hkv * dh] cache.  1 <= n_tensors <= 64,
+ * n_seq a multiple of seqs_per_keep, row_bytes a positive multiple of 16,
+ * rows 16-byte aligned.  Keep entries outside [0, L) are clamped.  Runs on
+ * the context stream.  Errors: GMC_ERR_ARG, GMC_ERR_STATE, GMC_ERR_HIP.
+ */
+#define GMC_MAX_GATHER_TENSORS 64
+int gmc_gather_rows(int64_t n_tensors, const void* const* src, void* const* dst, int64_t n_seq,
+                    int64_t seqs_per_keep, int64_t L, int64_t L2, int64_t row_bytes, const int32_t* keep);
+
 /* Bytes of device workspace the current context holds (0 without one). */
 int64_t gmc_workspace_bytes(void);
 

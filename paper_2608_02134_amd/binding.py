@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libgmc.so")
 GMC_OK, GMC_ERR_ARG, GMC_ERR_CAPACITY, GMC_ERR_STATE, GMC_ERR_HIP = 0, -1, -2, -3, -4
 GMC_F32, GMC_BF16 = 0, 1
 GMC_STATS = 15
+GMC_MAX_GATHER_TENSORS = 64
 
 _i32, _f32, _i64, _vp = ctypes.c_int32, ctypes.c_float, ctypes.c_int64, ctypes.c_void_p
 
@@ -64,6 +65,10 @@ SIGNATURES = {
     "gmc_realized_k": (_i64, [_i64, _i64]),
     "gmc_trace_dims": (ctypes.c_int, [_i64, _i64, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
                                       ctypes.POINTER(_i64), ctypes.POINTER(_i64)]),
+    "gmc_compact_sequence": (ctypes.c_int, [_i64, _i64, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i64,
+                                            _vp, _vp]),
+    "gmc_gather_rows": (ctypes.c_int, [_i64, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i64, _i64, _i64, _i64,
+                                       _i64, _vp]),
     "gmc_workspace_bytes": (_i64, []),
     "gmc_last_error": (ctypes.c_char_p, []),
     "gmc_free": (None, []),
@@ -135,6 +140,64 @@ def gmc_trace_dims(n: int, t: int, k: int):
     code = lib().gmc_trace_dims(n, t, k, *[ctypes.byref(v) for v in vals])
     _check(code, "gmc_trace_dims")
     return tuple(int(v.value) for v in vals)
+
+
+def gmc_compact_sequence(b, seq_len, vis_start, n, k, out_idx, iota, keep, seq_rows, vis_rows, out_rows,
+                         row_bytes, seq_pos, out_pos) -> int:
+    return lib().gmc_compact_sequence(b, seq_len, vis_start, n, k, out_idx, iota, keep, seq_rows, vis_rows,
+                                      out_rows, row_bytes, seq_pos, out_pos)
+
+
+def gmc_gather_rows(src_ptrs, dst_ptrs, n_seq, seqs_per_keep, seq_len, seq_len2, row_bytes, keep) -> int:
+    n = len(src_ptrs)
+    src = (_vp * max(n, 1))(*src_ptrs)
+    dst = (_vp * max(len(dst_ptrs), 1))(*dst_ptrs)
+    return lib().gmc_gather_rows(n, src, dst, n_seq, seqs_per_keep, seq_len, seq_len2, row_bytes, keep)
+
+
+def compact_sequence(out_idx, vis_start, n, seq_rows=None, vis_rows=None, seq_pos=None, seq_len=None):
+    """Tensor-level sequence compaction on torch's current stream (argument
+    marshalling only): out_idx [B][K] int32 device; seq_rows [B][L][...] and
+    vis_rows [B][K][...] of one dtype; seq_pos [B][L][3] int32.  Returns
+    (iota [B][L], keep [B][L2], out_rows or None, out_pos or None)."""
+    import torch
+    b, k = out_idx.shape
+    if seq_len is None:
+        seq_len = seq_rows.shape[1] if seq_rows is not None else seq_pos.shape[1]
+    l2 = seq_len - n + k
+    dev = out_idx.device
+    iota = torch.empty((b, seq_len), dtype=torch.int32, device=dev)
+    keep = torch.empty((b, l2), dtype=torch.int32, device=dev)
+    out_rows = out_pos = None
+    row_bytes = 0
+    if seq_rows is not None:
+        out_rows = torch.empty((b, l2) + tuple(seq_rows.shape[2:]), dtype=seq_rows.dtype, device=dev)
+        row_bytes = seq_rows[0, 0].numel() * seq_rows.element_size()
+    if seq_pos is not None:
+        out_pos = torch.empty((b, l2, 3), dtype=torch.int32, device=dev)
+    _check(gmc_set_stream(torch.cuda.current_stream(dev).cuda_stream), "gmc_set_stream")
+    ptr = (lambda t: None if t is None else t.data_ptr())
+    _check(gmc_compact_sequence(b, seq_len, vis_start, n, k, out_idx.data_ptr(), iota.data_ptr(), keep.data_ptr(),
+                                ptr(seq_rows), ptr(vis_rows), ptr(out_rows), row_bytes, ptr(seq_pos), ptr(out_pos)),
+           "gmc_compact_sequence")
+    return iota, keep, out_rows, out_pos
+
+
+def gather_rows(caches, keep, seqs_per_keep=1):
+    """Tensor-level row gather on torch's current stream: each cache is
+    [n_seq][L][...] (contiguous), keep [n_seq / seqs_per_keep][L2] int32;
+    returns the gathered [n_seq][L2][...] caches."""
+    import torch
+    n_seq, seq_len = caches[0].shape[:2]
+    l2 = keep.shape[1]
+    outs = [torch.empty((n_seq, l2) + tuple(c.shape[2:]), dtype=c.dtype, device=c.device) for c in caches]
+    row_bytes = caches[0][0, 0].numel() * caches[0].element_size()
+    _check(gmc_set_stream(torch.cuda.current_stream(caches[0].device).cuda_stream), "gmc_set_stream")
+    for i in range(0, len(caches), GMC_MAX_GATHER_TENSORS):
+        part = slice(i, i + GMC_MAX_GATHER_TENSORS)
+        _check(gmc_gather_rows([c.data_ptr() for c in caches[part]], [o.data_ptr() for o in outs[part]], n_seq,
+                               seqs_per_keep, seq_len, l2, row_bytes, keep.data_ptr()), "gmc_gather_rows")
+    return outs
 
 
 def gmc_workspace_bytes() -> int:

@@ -398,6 +398,65 @@ int64_t gmc_realized_k(int64_t N, int64_t K_req) {
   return std::min<int64_t>(N, std::max<int64_t>(K_req, 1));
 }
 
+int gmc_compact_sequence(int64_t B, int64_t L, int64_t vis_start, int64_t N, int64_t K, const int32_t* out_idx,
+                         int32_t* iota, int32_t* keep, const void* seq_rows, const void* vis_rows, void* out_rows,
+                         int64_t row_bytes, const int32_t* seq_pos, int32_t* out_pos) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_compact_sequence: no context (call gmc_init first)");
+  if (B < 1 || L < 1 || N < 1 || K < 1 || K > N || vis_start < 0 || vis_start + N > L || L > (1LL << 30))
+    return fail(GMC_ERR_ARG, "gmc_compact_sequence: need B, L >= 1, 1 <= K <= N, 0 <= vis_start, vis_start + N <= L "
+                "(B=%lld L=%lld vis_start=%lld N=%lld K=%lld)", static_cast<long long>(B), static_cast<long long>(L),
+                static_cast<long long>(vis_start), static_cast<long long>(N), static_cast<long long>(K));
+  if (!out_idx) return fail(GMC_ERR_ARG, "gmc_compact_sequence: out_idx is NULL");
+  const int rows_set = (seq_rows != nullptr) + (vis_rows != nullptr) + (out_rows != nullptr);
+  if (rows_set != 0 && rows_set != 3)
+    return fail(GMC_ERR_ARG, "gmc_compact_sequence: seq_rows, vis_rows and out_rows must be all NULL or all set");
+  if (rows_set == 3 && (row_bytes < 16 || row_bytes % 16 != 0 || row_bytes > (1LL << 24)))
+    return fail(GMC_ERR_ARG, "gmc_compact_sequence: row_bytes=%lld must be a positive multiple of 16",
+                static_cast<long long>(row_bytes));
+  if ((seq_pos == nullptr) != (out_pos == nullptr))
+    return fail(GMC_ERR_ARG, "gmc_compact_sequence: seq_pos and out_pos must be both NULL or both set");
+  auto misaligned = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) != 0; };
+  if (rows_set == 3 && (misaligned(seq_rows) || misaligned(vis_rows) || misaligned(out_rows)))
+    return fail(GMC_ERR_ARG, "gmc_compact_sequence: rows must be 16-byte aligned");
+  hipError_t err = hipSetDevice(g_ctx->device);
+  if (err == hipSuccess)
+    err = launch_compact_sequence(static_cast<int>(B), static_cast<int>(L), static_cast<int>(vis_start),
+                                  static_cast<int>(N), static_cast<int>(K), out_idx, iota, keep, seq_rows, vis_rows,
+                                  out_rows, rows_set == 3 ? static_cast<int>(row_bytes / 16) : 0, seq_pos, out_pos,
+                                  g_ctx->stream);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "gmc_compact_sequence: %s", hipGetErrorString(err));
+  return GMC_OK;
+}
+
+int gmc_gather_rows(int64_t n_tensors, const void* const* src, void* const* dst, int64_t n_seq,
+                    int64_t seqs_per_keep, int64_t L, int64_t L2, int64_t row_bytes, const int32_t* keep) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_gather_rows: no context (call gmc_init first)");
+  if (n_tensors < 1 || n_tensors > kMaxGather)
+    return fail(GMC_ERR_ARG, "gmc_gather_rows: n_tensors=%lld out of [1, %d]", static_cast<long long>(n_tensors),
+                kMaxGather);
+  if (!src || !dst || !keep) return fail(GMC_ERR_ARG, "gmc_gather_rows: null pointer");
+  if (n_seq < 1 || seqs_per_keep < 1 || n_seq % seqs_per_keep != 0 || L < 1 || L2 < 1 || L > (1LL << 30) ||
+      L2 > (1LL << 30) || n_seq > (1LL << 30))
+    return fail(GMC_ERR_ARG, "gmc_gather_rows: need n_seq a positive multiple of seqs_per_keep, L, L2 >= 1");
+  if (row_bytes < 16 || row_bytes % 16 != 0 || row_bytes > (1LL << 24))
+    return fail(GMC_ERR_ARG, "gmc_gather_rows: row_bytes=%lld must be a positive multiple of 16",
+                static_cast<long long>(row_bytes));
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    if (!src[t] || !dst[t]) return fail(GMC_ERR_ARG, "gmc_gather_rows: tensor %lld is NULL", static_cast<long long>(t));
+    if ((reinterpret_cast<uintptr_t>(src[t]) | reinterpret_cast<uintptr_t>(dst[t])) & 15u)
+      return fail(GMC_ERR_ARG, "gmc_gather_rows: tensor %lld is not 16-byte aligned", static_cast<long long>(t));
+  }
+  hipError_t err = hipSetDevice(g_ctx->device);
+  if (err == hipSuccess)
+    err = launch_gather_rows(static_cast<int>(n_tensors), src, dst, static_cast<int>(n_seq),
+                             static_cast<int>(seqs_per_keep), static_cast<int>(L), static_cast<int>(L2),
+                             static_cast<int>(row_bytes / 16), keep, g_ctx->stream);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "gmc_gather_rows: %s", hipGetErrorString(err));
+  return GMC_OK;
+}
+
 int64_t gmc_workspace_bytes(void) {
   std::lock_guard<std::mutex> lk(g_mu);
   return g_ctx ? static_cast<int64_t>(g_ctx->bytes) : 0;

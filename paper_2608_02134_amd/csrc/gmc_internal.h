@@ -17,6 +17,7 @@ constexpr int kCntBankFlag = 6;   // slot of problem 0: the bank kernels of the 
 constexpr int kCntStatus = 7;     // device status bits, 1 = a bounded device wait timed out
 constexpr int kBankSpinLimit = 1 << 18;   // polls of the bank flag before the wait gives up
 constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection
+constexpr int kMaxGather = 64;    // tensors per row-gather launch (GMC_MAX_GATHER_TENSORS)
 constexpr int kLogitSplit = 8;    // column ranges of the message-logit kernels (at most)
 constexpr int kProbeSplit = 4;    // K splits of the value-probe GEMM (d a multiple of 256)
 

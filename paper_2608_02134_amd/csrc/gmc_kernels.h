@@ -39,8 +39,6 @@ hipError_t launch_bank_signal(int* flag, hipStream_t st);
 hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
                         const void* app_proj, const int32_t* pos3d, hipStream_t st);
 
-// Per-call state: nothing selected, completion counters cleared.
-
 // All selection rounds, then the final coverage and objective values.
 // *support_ready reports that the support list and slots were written too.
 hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
@@ -58,6 +56,16 @@ hipError_t launch_transport(const Shape& sh, const Params& pr, const Ws& ws, con
 // K = N: copy inputs to outputs.
 hipError_t launch_identity(const Shape& sh, const void* hidden, const int32_t* pos3d,
                            void* out_hidden, int32_t* out_pos, int32_t* out_idx, hipStream_t st);
+
+// Sequence compaction after pruning: index map, inverse map, boundary rows
+// and position ids (row_chunks = row bytes / 16; NULL outputs are skipped).
+hipError_t launch_compact_sequence(int B, int L, int v0, int N, int K, const int32_t* out_idx, int32_t* iota,
+                                   int32_t* keep, const void* seq_rows, const void* vis_rows, void* out_rows,
+                                   int row_chunks, const int32_t* seq_pos, int32_t* out_pos, hipStream_t st);
+
+// Row gather of up to kMaxGather tensors at the retained positions.
+hipError_t launch_gather_rows(int n_tensors, const void* const* src, void* const* dst, int n_seq, int spk, int L,
+                              int L2, int row_chunks, const int32_t* keep, hipStream_t st);
 
 // Debug exports: pre-weighted client matrix and per-problem statistics.
 hipError_t launch_trace_exports(const Shape& sh, const Ws& ws, float* trace_client,

@@ -57,6 +57,7 @@ def test_header_constants_match_binding():
     assert (consts["GMC_OK"], consts["GMC_ERR_ARG"], consts["GMC_ERR_CAPACITY"], consts["GMC_ERR_STATE"],
             consts["GMC_ERR_HIP"]) == (B.GMC_OK, B.GMC_ERR_ARG, B.GMC_ERR_CAPACITY, B.GMC_ERR_STATE, B.GMC_ERR_HIP)
     assert (consts["GMC_F32"], consts["GMC_BF16"]) == (B.GMC_F32, B.GMC_BF16)
+    assert consts["GMC_MAX_GATHER_TENSORS"] == B.GMC_MAX_GATHER_TENSORS
 
 
 @pytest.mark.parametrize("n,k,want", [(10, 20, 10), (10, 0, 1), (10, -4, 1), (10, 3, 3), (0, 5, 0)])
@@ -106,6 +107,9 @@ def test_calls_without_context(lib):
     assert B.gmc_workspace_bytes() == 0
     with pytest.raises(B.GmcError):
         B.gmc_trace_dims(10, 1, 2)
+    assert B.gmc_compact_sequence(1, 10, 2, 4, 2, 0x1000, None, None, None, None, None, 0, None,
+                                  None) == B.GMC_ERR_STATE
+    assert B.gmc_gather_rows([0x1000], [0x2000], 1, 1, 10, 8, 16, 0x3000) == B.GMC_ERR_STATE
 
 
 def test_init_without_device_reports_hip_error(lib):
