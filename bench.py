@@ -122,6 +122,9 @@ def main():
                     help="time budget of the oracle CPU baseline sample (0 disables)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration) and exit")
+    ap.add_argument("--op", default="prune", choices=["prune", "compact"],
+                    help="prune: the operator (default line); compact: sequence compaction and "
+                         "prefix K/V gather after pruning")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the operator is single-GPU and this build has no "
@@ -130,6 +133,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.op == "compact":
+        bench_compaction(args)
         return
 
     import torch
@@ -217,6 +223,106 @@ def main():
                    "K": kr, "d": w.d, "heads": [w.hq, w.hkv], "head_dim": w.dh,
                    "rounds": rounds, "client_rows": m_rows},
         "roofline": roofline, "cpu_baseline": cpu, "stages": stages,
+    }
+    pr.close()
+    print(json.dumps(line), flush=True)
+
+
+# Sequence compaction after pruning at the Qwen2.5-VL-7B shape: 16 prompts of
+# 15 system + 1296 visual + 64 question positions, K = 256 retained, the
+# boundary states (d = 3584) and the prompt K/V of 16 prefix layers (token
+# major, 4 kv heads x 128, bf16) gathered at the retained positions.
+COMPACT = dict(batch=16, before=15, n=1296, after=64, k=256, d=3584, layers=16, hkv=4, dh=128)
+COMPACT_METRIC = "bytes moved / s (sequence compaction + prefix K/V gather after pruning, 1 GPU)"
+
+
+def bench_compaction(args):
+    import torch
+    from paper_2608_02134_amd import binding, synth
+    from tests.gpu_run import make_pruner
+    c = COMPACT
+    b, n, k = c["batch"], c["n"], c["k"]
+    seq = c["before"] + n + c["after"]
+    l2 = seq - n + k
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    pr = make_pruner(synth.make_problem("tiny", grid=(1, 8, 8), t=4, k=16), torch)   # a context
+    g = torch.Generator(device=dev).manual_seed(7)
+    kept = torch.stack([torch.randperm(n, generator=g, device=dev)[:k].sort().values for _ in range(b)])
+    kept = kept.to(torch.int32).contiguous()
+    rows = torch.randn((b, seq, c["d"]), generator=g, device=dev).to(torch.bfloat16)
+    vis = torch.randn((b, k, c["d"]), generator=g, device=dev).to(torch.bfloat16)
+    pos = torch.randint(0, 1000, (b, seq, 3), generator=g, device=dev, dtype=torch.int32)
+    caches = [torch.randn((b, seq, c["hkv"] * c["dh"]), generator=g, device=dev).to(torch.bfloat16)
+              for _ in range(2 * c["layers"])]
+    iota = torch.empty((b, seq), dtype=torch.int32, device=dev)
+    keep = torch.empty((b, l2), dtype=torch.int32, device=dev)
+    out_rows = torch.empty((b, l2, c["d"]), dtype=torch.bfloat16, device=dev)
+    out_pos = torch.empty((b, l2, 3), dtype=torch.int32, device=dev)
+    outs = [torch.empty((b, l2, c["hkv"] * c["dh"]), dtype=torch.bfloat16, device=dev) for _ in caches]
+    row_bytes, kv_bytes = c["d"] * 2, c["hkv"] * c["dh"] * 2
+    stream = torch.cuda.current_stream(dev)
+    binding._check(binding.gmc_set_stream(stream.cuda_stream), "gmc_set_stream")
+    src = [t.data_ptr() for t in caches]
+    dst = [t.data_ptr() for t in outs]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    gather_ms = []
+
+    def step(timed=False):
+        binding._check(binding.gmc_compact_sequence(b, seq, c["before"], n, k, kept.data_ptr(), iota.data_ptr(),
+                                                    keep.data_ptr(), rows.data_ptr(), vis.data_ptr(),
+                                                    out_rows.data_ptr(), row_bytes, pos.data_ptr(),
+                                                    out_pos.data_ptr()), "gmc_compact_sequence")
+        if timed:
+            ev[0].record(stream)
+        binding._check(binding.gmc_gather_rows(src, dst, b, 1, seq, l2, kv_bytes, keep.data_ptr()), "gmc_gather_rows")
+        if timed:
+            ev[1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    # the gather kernel alone: events around its launch on the op stream
+    for _ in range(args.steps):
+        step(timed=True)
+        torch.cuda.synchronize()
+        gather_ms.append(ev[0].elapsed_time(ev[1]))
+    gather_s = sum(gather_ms) / len(gather_ms) / 1e3
+    gather_work = 2.0 * len(caches) * b * l2 * kv_bytes + 4.0 * b * l2          # rows read + written, keep
+    seq_work = 2.0 * b * l2 * (row_bytes + 12) + 4.0 * b * (seq + l2 + k)     # rows, ids, maps, out_idx
+    work = gather_work + seq_work
+    # CPU baseline: the oracle's gather of the same caches on the host, one
+    # prompt at a time until about two seconds are used
+    from oracle import gmc_oracle as O
+    host = [t[0].view(torch.int16).cpu().numpy() for t in caches]
+    hkeep = keep[0].cpu().numpy()
+    n_done, tc0 = 0, time.perf_counter()
+    while time.perf_counter() - tc0 < 2.0 or n_done == 0:
+        for h in host:
+            O.gather_cache(h, hkeep)
+        n_done += 1
+    cpu_s = (time.perf_counter() - tc0) / n_done
+    line = {
+        "metric": COMPACT_METRIC, "value": work / (ms_step / 1e3) / 1e9, "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "sequence compaction after pruning, Qwen2.5-VL-7B shape: 16 prompts of 15 + 1296 "
+                               "visual + 64 positions, K = 256, boundary states d = 3584 and prompt K/V of 16 "
+                               "prefix layers (token-major, 4 x 128, bf16)",
+                   "batch": b, "L": seq, "L2": l2, "N": n, "K": k, "tensors": len(caches)},
+        "roofline": {"bound": "hbm", "kernel": "gather_rows_kernel", "achieved": gather_work / gather_s / 1e9,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gather_work / gather_s / 1e9 / HBM_PEAK_GBS,
+                     "traffic": None, "work_per_launch": gather_work, "launch_avg_us": gather_s * 1e6},
+        "cpu_baseline": {"value": 2.0 * len(caches) * l2 * kv_bytes / cpu_s / 1e9, "unit": "GB/s", "cores": 1,
+                         "kind": "oracle", "sample": f"the oracle's gather of one prompt's {len(caches)} caches, "
+                                                     f"{n_done} times ({cpu_s * 1e3:.1f} ms each)"},
     }
     pr.close()
     print(json.dumps(line), flush=True)

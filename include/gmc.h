@@ -258,7 +258,7 @@ int gmc_compact_sequence(int64_t B, int64_t L, int64_t vis_start, int64_t N, int
  * (keep [n_seq / seqs_per_keep][L2] int32, device, entries in [0, L)), e.g.
  * the heads of a head-major [B][Hkv][L][dh] cache with seqs_per_keep = Hkv,
  * or 1 for a token-major [B][L][Hkv * dh] cache.  1 <= n_tensors <= 64,
- * n_seq a multiple of seqs_per_keep, row_bytes a positive multiple of 16,
+ * 1 <= n_seq <= 65535 a multiple of seqs_per_keep, row_bytes a positive multiple of 16,
  * rows 16-byte aligned.  Keep entries outside [0, L) are clamped.  Runs on
  * the context stream.  Errors: GMC_ERR_ARG, GMC_ERR_STATE, GMC_ERR_HIP.
  */

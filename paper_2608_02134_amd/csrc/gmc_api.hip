@@ -438,11 +438,13 @@ int gmc_gather_rows(int64_t n_tensors, const void* const* src, void* const* dst,
                 kMaxGather);
   if (!src || !dst || !keep) return fail(GMC_ERR_ARG, "gmc_gather_rows: null pointer");
   if (n_seq < 1 || seqs_per_keep < 1 || n_seq % seqs_per_keep != 0 || L < 1 || L2 < 1 || L > (1LL << 30) ||
-      L2 > (1LL << 30) || n_seq > (1LL << 30))
-    return fail(GMC_ERR_ARG, "gmc_gather_rows: need n_seq a positive multiple of seqs_per_keep, L, L2 >= 1");
+      L2 > (1LL << 30) || n_seq > 65535)
+    return fail(GMC_ERR_ARG, "gmc_gather_rows: need n_seq in [1, 65535] a multiple of seqs_per_keep, L, L2 >= 1");
   if (row_bytes < 16 || row_bytes % 16 != 0 || row_bytes > (1LL << 24))
     return fail(GMC_ERR_ARG, "gmc_gather_rows: row_bytes=%lld must be a positive multiple of 16",
                 static_cast<long long>(row_bytes));
+  if (n_seq * L2 * (row_bytes / 16) >= (1LL << 31))
+    return fail(GMC_ERR_ARG, "gmc_gather_rows: a destination tensor above 32 GiB; split the call");
   for (int64_t t = 0; t < n_tensors; ++t) {
     if (!src[t] || !dst[t]) return fail(GMC_ERR_ARG, "gmc_gather_rows: tensor %lld is NULL", static_cast<long long>(t));
     if ((reinterpret_cast<uintptr_t>(src[t]) | reinterpret_cast<uintptr_t>(dst[t])) & 15u)

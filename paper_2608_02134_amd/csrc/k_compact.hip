@@ -68,31 +68,33 @@ struct GatherTable {
 };
 
 // blockIdx.y = tensor; threads stride over the tensor's (sequence, row,
-// 16-byte chunk) space, four chunks in flight per thread.
+// 16-byte chunk) space, kGatherDepth chunks in flight per thread (32-bit
+// indices: the host keeps a tensor below 2^31 chunks).
+constexpr int kGatherDepth = 4;
 __global__ void __launch_bounds__(256)
 gather_rows_kernel(GatherTable tab, int n_seq, int spk, int L, int L2, int row_chunks,
                    const int32_t* __restrict__ keep) {
   const uint4* src = tab.src[blockIdx.y];
   uint4* dst = tab.dst[blockIdx.y];
-  const long long total = static_cast<long long>(n_seq) * L2 * row_chunks;
-  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long base = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x; base < total;
-       base += 4 * stride) {
-    uint4 v[4];
-    long long to[4];
+  const unsigned total = static_cast<unsigned>(n_seq) * L2 * row_chunks;
+  const unsigned stride = gridDim.x * blockDim.x;
+  const unsigned rc = row_chunks, l2 = L2;
+  for (unsigned base = blockIdx.x * blockDim.x + threadIdx.x; base < total; base += kGatherDepth * stride) {
+    uint4 v[kGatherDepth];
+    unsigned to[kGatherDepth];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const long long q = min(base + u * stride, total - 1);
-      const int c = static_cast<int>(q % row_chunks);
-      const long long r = q / row_chunks;         // s * L2 + j
-      const int j = static_cast<int>(r % L2);
-      const int s = static_cast<int>(r / L2);
+    for (int u = 0; u < kGatherDepth; ++u) {
+      const unsigned q = min(base + u * stride, total - 1);
+      const unsigned r = q / rc;                 // s * L2 + j
+      const unsigned c = q - r * rc;
+      const unsigned s = r / l2;
+      const unsigned j = r - s * l2;
       const int from = min(max(keep[static_cast<long long>(s / spk) * L2 + j], 0), L - 1);
       v[u] = src[(static_cast<long long>(s) * L + from) * row_chunks + c];
-      to[u] = r * row_chunks + c;
+      to[u] = q;
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < kGatherDepth; ++u)
       if (base + u * stride < total) dst[to[u]] = v[u];
   }
 }
@@ -115,10 +117,10 @@ hipError_t launch_gather_rows(int n_tensors, const void* const* src, void* const
     tab.dst[t] = static_cast<uint4*>(dst[t]);
   }
   const long long total = static_cast<long long>(n_seq) * L2 * row_chunks;
-  // about eight resident blocks per CU over all tensors, four chunks per
-  // thread and trip
-  const long long want = (total + 4LL * 256 - 1) / (4LL * 256);
-  const long long cap = std::max<long long>(1, 2048 / n_tensors);
+  // about eight resident blocks per CU over all tensors, kGatherDepth chunks
+  // per thread and trip
+  const long long want = (total + 1LL * kGatherDepth * 256 - 1) / (1LL * kGatherDepth * 256);
+  const long long cap = std::max<long long>(1, 32768 / n_tensors);
   const int gx = static_cast<int>(std::max<long long>(1, std::min(want, cap)));
   hipLaunchKernelGGL(gather_rows_kernel, dim3(gx, n_tensors), dim3(256), 0, st, tab, n_seq, spk, L, L2, row_chunks,
                      keep);
