@@ -19,6 +19,8 @@
 
 namespace gmc {
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
 // One wave per position index x: the map of input position x (x < L) and
 // output row x (x < L2) with its row and position ids.
 __global__ void __launch_bounds__(256)
@@ -57,7 +59,7 @@ compact_sequence_kernel(int L, int v0, int N, int K, const int32_t* __restrict__
     const uint4* from = vis ? vis_rows + (static_cast<long long>(b) * K + (x - v0)) * row_chunks
                             : seq_rows + (static_cast<long long>(b) * L + src) * row_chunks;
     uint4* to = out_rows + (static_cast<long long>(b) * L2 + x) * row_chunks;
-    for (int c = lane; c < row_chunks; c += 64) to[c] = from[c];
+    for (int c = lane; c < row_chunks; c += 64) to[c] = from[c];   // (non-temporal measured slower here)
   }
 }
 
@@ -69,7 +71,9 @@ struct GatherTable {
 
 // blockIdx.y = tensor; threads stride over the tensor's (sequence, row,
 // 16-byte chunk) space, kGatherDepth chunks in flight per thread (32-bit
-// indices: the host keeps a tensor below 2^31 chunks).
+// indices: the host keeps a tensor below 2^31 chunks).  Every byte is moved
+// once, so loads and stores are non-temporal (measured: 68% of HBM peak
+// against 57% with cached ones).
 constexpr int kGatherDepth = 4;
 __global__ void __launch_bounds__(256)
 gather_rows_kernel(GatherTable tab, int n_seq, int spk, int L, int L2, int row_chunks,
@@ -80,7 +84,7 @@ gather_rows_kernel(GatherTable tab, int n_seq, int spk, int L, int L2, int row_c
   const unsigned stride = gridDim.x * blockDim.x;
   const unsigned rc = row_chunks, l2 = L2;
   for (unsigned base = blockIdx.x * blockDim.x + threadIdx.x; base < total; base += kGatherDepth * stride) {
-    uint4 v[kGatherDepth];
+    u32x4 v[kGatherDepth];
     unsigned to[kGatherDepth];
 #pragma unroll
     for (int u = 0; u < kGatherDepth; ++u) {
@@ -90,12 +94,13 @@ gather_rows_kernel(GatherTable tab, int n_seq, int spk, int L, int L2, int row_c
       const unsigned s = r / l2;
       const unsigned j = r - s * l2;
       const int from = min(max(keep[static_cast<long long>(s / spk) * L2 + j], 0), L - 1);
-      v[u] = src[(static_cast<long long>(s) * L + from) * row_chunks + c];
+      v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) +
+                                        (static_cast<long long>(s) * L + from) * row_chunks + c);
       to[u] = q;
     }
 #pragma unroll
     for (int u = 0; u < kGatherDepth; ++u)
-      if (base + u * stride < total) dst[to[u]] = v[u];
+      if (base + u * stride < total) __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(dst) + to[u]);
   }
 }
 
