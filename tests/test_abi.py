@@ -122,3 +122,18 @@ def test_init_without_device_reports_hip_error(lib):
         pytest.skip("a device is present")
     assert B.gmc_init(_valid_cfg()) == B.GMC_ERR_HIP
     assert "device" in B.gmc_last_error()
+
+
+def test_header_is_plain_c(tmp_path):
+    # the boundary header must stay a C header (no C++ or HIP types)
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use.c"
+    src.write_text('#include "gmc.h"\nint main(void) { gmc_config c; gmc_trace t; gmc_config_default(&c);\n'
+                   '  (void)t; return gmc_realized_k(4, 2) == 2 ? 0 : 1; }\n')
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only",
+                        "-I", os.path.dirname(HEADER), str(src)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
