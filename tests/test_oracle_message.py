@@ -261,3 +261,63 @@ def test_energy_single_head_single_query_closed_form():
     assert c["omega"][0] == pytest.approx(1.0)
     e = c["a"][0, 0] * c["ell"][0]
     np.testing.assert_allclose(c["ebar"], e / e.mean(), rtol=1e-12)
+
+
+def test_energy_two_heads_two_queries_hand_computed():
+    # Eq. cond-grounded-energy with unequal head weights and T = 2 queries
+    # (nu = (1/3, 2/3): the terminal query counts twice).  Atom norms:
+    # head 0 has 1 at (t=0, i=0), head 1 has 2 at (t=1, i=1), all else 0.
+    #   e_0^2 = omega_0 nu_0 1^2 = 1/4 * 1/3 * 1 = 1/12
+    #   e_1^2 = omega_1 nu_1 2^2 = 3/4 * 2/3 * 4 = 2
+    # so ebar = 2 (sqrt(1/12), sqrt(2)) / (sqrt(1/12) + sqrt(2))
+    #         = (2, 2 sqrt(24)) / (1 + sqrt(24)).
+    e = np.zeros((2, 2, 2))
+    e[0, 0, 0] = 1.0
+    e[1, 1, 1] = 2.0
+    omega = np.array([0.25, 0.75])
+    nu = O.query_weights(2, P)
+    np.testing.assert_allclose(nu, [1 / 3, 2 / 3], rtol=1e-15)
+    ebar, en = O.grounded_energy(e, omega, nu)
+    np.testing.assert_allclose(en, [math.sqrt(1 / 12), math.sqrt(2)], rtol=1e-14)
+    r = math.sqrt(24)
+    np.testing.assert_allclose(ebar, [2 / (1 + r), 2 * r / (1 + r)], rtol=1e-14)
+
+
+def test_energy_weights_heads_not_uniformly():
+    # the same token energy from two heads: a head with weight 3/4 counts
+    # three times a head with weight 1/4 (e^2 is linear in omega):
+    # token 0 draws 1 from head 0, token 1 draws 1 from head 1, one query,
+    # so e = (sqrt(1/4), sqrt(3/4)) and ebar = 2 (1, sqrt 3) / (1 + sqrt 3).
+    e = np.zeros((2, 1, 2))
+    e[0, 0, 0] = 1.0
+    e[1, 0, 1] = 1.0
+    ebar, en = O.grounded_energy(e, np.array([0.25, 0.75]), O.query_weights(1, P))
+    np.testing.assert_allclose(en, [0.5, math.sqrt(0.75)], rtol=1e-14)
+    s3 = math.sqrt(3)
+    np.testing.assert_allclose(ebar, [2 / (1 + s3), 2 * s3 / (1 + s3)], rtol=1e-14)
+
+
+def test_head_weights_first_centre_is_largest_pre_normalisation_pattern():
+    # Eq. cond-head-pattern: the first farthest-first centre is the head with
+    # the largest sqrt(beta Gamma_hh) / abar_h (the pattern after scaling the
+    # atoms to unit average norm), not the largest raw Gram diagonal.
+    # Four unit directions in a plane at 0, 50, 95 and 150 degrees; raw norms
+    # (2, 1.5, 1, 1), mean atom norms (2, 1, 1, 1): the largest raw pattern is
+    # head 0, the largest normalised one is head 1 (1.5 vs 1).
+    #   first centre head 1 -> farthest is head 3 (100 deg); head 0 (50 deg
+    #   from 1, 150 from 3) and head 2 (45 from 1, 55 from 3) join head 1:
+    #   clusters {0, 1, 2} and {3}, so omega_3 = 1/2.
+    #   (first centre head 0 would give centres 0, 3 and clusters {0, 1},
+    #   {2, 3}, omega_3 < 1/2.)
+    ang = np.radians([0.0, 50.0, 95.0, 150.0])
+    norms = np.array([2.0, 1.5, 1.0, 1.0])
+    u = norms[:, None] * np.stack([np.cos(ang), np.sin(ang)], axis=1)
+    abar = np.array([2.0, 1.0, 1.0, 1.0])
+    p2 = O.GmcParams(max_head_clusters=2)
+    omega, centres, assign = O.head_weights(_gram_from_patterns(u), abar, p2)
+    assert centres == [1, 3]
+    assert assign.tolist() == [0, 0, 0, 1]
+    assert omega[3] == pytest.approx(0.5, rel=1e-14)
+    assert omega[:3].sum() == pytest.approx(0.5, rel=1e-14)
+    # head 1 sits nearest the cluster mean, so it gets the largest share
+    assert np.argmax(omega[:3]) == 1

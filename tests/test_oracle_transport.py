@@ -226,3 +226,39 @@ def test_compact_sorts_support_and_gathers_positions():
     assert idx.tolist() == [2, 5, 7]
     assert out_h[:, 0].tolist() == [2.0, 5.0, 7.0]
     assert np.array_equal(out_pos, pos[[2, 5, 7]])
+
+
+def test_ambiguity_gate_values():
+    # reading R5 of Eq. cond-population-gate: g = exp(-(delta / 0.05)^8);
+    # at the margin itself g = 1/e, at zero 1, at twice the margin e^-256
+    d = np.array([0.0, 0.05, 0.1, 0.025])
+    g = O.ambiguity_gate(d, P)
+    assert g[0] == 1.0
+    assert g[1] == pytest.approx(math.exp(-1.0), rel=1e-12)
+    assert g[2] == pytest.approx(math.exp(-256.0), rel=1e-9)
+    assert g[3] == pytest.approx(math.exp(-(0.5 ** 8)), rel=1e-12)
+    # hard form: 1[delta < 0.05], so the margin itself is already unambiguous
+    hard = O.GmcParams(g_form="hard")
+    gh = O.ambiguity_gate(np.array([0.0, 0.0499999, 0.05, 0.0500001, 0.3]), hard)
+    assert gh.tolist() == [1.0, 1.0, 0.0, 0.0, 0.0]
+
+
+def test_kappa_hand_computed():
+    # Eq. cond-assignment: kappa_ij = cos_ij + 0.5 s_x g_i exp(-||p_i - p_j||^2 / 0.02).
+    # Carriers 0 = e1 and 1 = e2; discarded 2 = (e1 + e2)/sqrt 2 (gap 0, g = 1),
+    # 3 = e1 and 4 = e2 (gap 1, g = exp(-20^8) = 0).  Mean gap 2/3, so
+    # s_x = 1 - exp(-(25/3)^8) = 1 in double precision.  Token 2 sits 0.1 from
+    # carrier 0 and 0.2 from carrier 1:
+    #   kappa_20 = 1/sqrt 2 + 0.5 exp(-0.01/0.02) = 1/sqrt 2 + 0.5 e^-0.5
+    #   kappa_21 = 1/sqrt 2 + 0.5 exp(-0.04/0.02) = 1/sqrt 2 + 0.5 e^-2
+    r = 1 / math.sqrt(2)
+    x = np.array([[1.0, 0.0], [0.0, 1.0], [r, r], [1.0, 0.0], [0.0, 1.0]])
+    pc = np.array([[0.5, 0.6], [0.5, 0.3], [0.5, 0.5], [0.9, 0.9], [0.1, 0.1]])
+    a = O.assign_population(x, pc, np.array([0, 1]), P)
+    assert a["sx"] == 1.0
+    assert a["dbar"] == pytest.approx(2 / 3, rel=1e-15)
+    np.testing.assert_allclose(a["kappa"][2], [r + 0.5 * math.exp(-0.5), r + 0.5 * math.exp(-2.0)],
+                               rtol=1e-14)
+    np.testing.assert_allclose(a["kappa"][3], [1.0, 0.0], atol=1e-15)
+    np.testing.assert_allclose(a["kappa"][4], [0.0, 1.0], atol=1e-15)
+    assert a["pi"].tolist() == [0, 1, 0, 0, 1]
