@@ -140,7 +140,7 @@ def main():
 
     import torch
     from paper_2608_02134_amd import binding, synth
-    from tests.gpu_run import make_pruner, to_device
+    from paper_2608_02134_amd.binding import make_pruner, to_device
 
     prob = synth.make_problem(args.workload)
     w = prob.workload
@@ -180,6 +180,12 @@ def main():
     torch.cuda.synchronize()
     ms_total = t0.elapsed_time(t1)
     ms_step = ms_total / args.steps
+    # the device status of the timed calls (sticky bits: any timed-out
+    # device wait or non-finite value in any of them) invalidates the run
+    code, diag = binding.gmc_get_diag(0)
+    if code != binding.GMC_OK:
+        print(f"timed calls failed on the device: {binding.gmc_last_error()}", file=sys.stderr)
+        sys.exit(3)
     pruned = w.batch * (w.n - kr)
     value = pruned / (ms_step / 1e3)
 
@@ -189,6 +195,10 @@ def main():
         step()
     stage_ms, stage_n = binding.gmc_timing_read()
     binding._check(binding.gmc_timing_enable(False), "gmc_timing_enable")
+    code, _ = binding.gmc_get_diag(0)
+    if code != binding.GMC_OK:
+        print(f"stage-timed calls failed on the device: {binding.gmc_last_error()}", file=sys.stderr)
+        sys.exit(3)
     stages = {name: {"ms_per_step": stage_ms[i] / args.steps,
                      "launch_avg_us": (1e3 * stage_ms[i] / stage_n[i]) if stage_n[i] else None,
                      "launches_per_step": stage_n[i] / args.steps}
@@ -239,7 +249,7 @@ COMPACT_METRIC = "bytes moved / s (sequence compaction + prefix K/V gather after
 def bench_compaction(args):
     import torch
     from paper_2608_02134_amd import binding, synth
-    from tests.gpu_run import make_pruner
+    from paper_2608_02134_amd.binding import make_pruner
     c = COMPACT
     b, n, k = c["batch"], c["n"], c["k"]
     seq = c["before"] + n + c["after"]
@@ -328,29 +338,58 @@ def bench_compaction(args):
     print(json.dumps(line), flush=True)
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(prob, budget_s: float):
     """The oracle as it stands, on this host, on whole problems of the same
-    workload until the time budget is used (at least one problem)."""
+    workload: three runs with the BLAS pool at its default width (the median
+    is `value`) and one single-thread run, each of at least one problem and
+    about a fifth of the time budget."""
     from oracle import gmc_oracle as O
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
+        threadpool_limits = None
         cores = os.cpu_count()
     w = prob.workload
-    done, pruned, t0 = 0, 0, time.perf_counter()
-    while True:
-        b = done % w.batch
-        O.gmc_single(prob.hidden[b], prob.text_q[b], prob.vis_k[b], prob.pos3d[b], prob.probe, w.k,
-                     app_proj=prob.app_proj)
-        done += 1
-        pruned += w.n - min(w.n, max(w.k, 1))
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    el = time.perf_counter() - t0
-    return {"value": pruned / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} whole {w.name} problem(s) (N={w.n}, K={w.k}) through the fp64 "
-                      f"oracle in {el:.1f} s"}
+    per_problem = w.n - min(w.n, max(w.k, 1))
+
+    def run(seconds):
+        done, t0 = 0, time.perf_counter()
+        while True:
+            b = done % w.batch
+            O.gmc_single(prob.hidden[b], prob.text_q[b], prob.vis_k[b], prob.pos3d[b], prob.probe, w.k,
+                         app_proj=prob.app_proj)
+            done += 1
+            if time.perf_counter() - t0 >= seconds:
+                break
+        el = time.perf_counter() - t0
+        return done * per_problem / el, done, el
+
+    part = budget_s / 5.0
+    runs = [run(part) for _ in range(3)]
+    rates = sorted(r[0] for r in runs)
+    single = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            single = run(part)
+    return {"value": rates[1], "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu_model": _cpu_model(), "runs": [r[0] for r in runs],
+            "single_thread_value": None if single is None else single[0],
+            "sample": (f"median of 3 runs of whole {w.name} problems (N={w.n}, K={w.k}) through the fp64 "
+                       f"oracle, {sum(r[1] for r in runs)} problems in {sum(r[2] for r in runs):.1f} s on "
+                       f"{cores} BLAS threads" +
+                       ("" if single is None else f"; single thread: {single[1]} problem(s) in {single[2]:.1f} s"))}
 
 
 if __name__ == "__main__":

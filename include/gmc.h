@@ -33,8 +33,9 @@
  *     gmc_last_error() then describes the failure.  A failed call enqueues
  *     nothing and leaves the outputs untouched.
  *   - One library context per process; calls are serialised by an internal
- *     mutex.  Calls that overlap on the device (several host threads on
- *     different streams) are not supported: they share one workspace.
+ *     mutex and share one workspace.  Consecutive pruning calls are ordered
+ *     on the device even when gmc_set_stream changed the stream in between
+ *     (the new stream first waits for the previous call's stream).
  */
 #ifndef GMC_H
 #define GMC_H
@@ -50,6 +51,17 @@ extern "C" {
 #define GMC_ERR_CAPACITY (-2) /* call exceeds the capacities given at init     */
 #define GMC_ERR_STATE (-3)    /* no context (gmc_init not called / failed)     */
 #define GMC_ERR_HIP (-4)      /* HIP runtime failure (no device, launch, OOM)  */
+#define GMC_ERR_DEVICE (-5)   /* gmc_get_diag: a bounded device wait of an
+                                 earlier call timed out (its results are invalid) */
+#define GMC_ERR_NONFINITE (-6) /* gmc_get_diag, debug mode: an earlier call met a
+                                  non-finite value (App. J numerical checks)    */
+
+/* Device status bits (sticky: set by the kernels of any call, cleared only by
+ * gmc_get_diag, which reports and clears them).                              */
+#define GMC_STATUS_SELECT_TIMEOUT 1u /* a hand-off wait of the persistent selection */
+#define GMC_STATUS_BANK_TIMEOUT 2u   /* the bank stream's start gate or its join     */
+#define GMC_STATUS_NONFINITE 4u      /* debug mode: a non-finite client energy, row
+                                        weight or output value                      */
 
 #define GMC_F32 0
 #define GMC_BF16 1
@@ -59,9 +71,10 @@ extern "C" {
 /* stats layout: [0] s_x  [1] mean selected-cosine gap over discarded tokens
  *               [2] F(S)  [3] F(V)  [4] realised K  [5] rounds  [6] M rows
  *               [7] number of discarded tokens
- *               [8] device status: 0 ok; 1 = a bounded device wait (a
- *                   hand-off of the persistent selection, or the wait for
- *                   the bank kernels) timed out (results invalid)
+ *               [8] device status bits (GMC_STATUS_*), sticky until
+ *                   gmc_get_diag clears them: nonzero means a bounded device
+ *                   wait timed out or (debug mode) a non-finite value was met;
+ *                   the results of that call are invalid
  *               [9..11]  F_b(S) of the grounded, appearance, spatial bank
  *               [12..14] F_b(V) of the same banks; omega_b = F_b(V)/F(V)
  *                   and c_b = F_b(S)/F_b(V) (Eq. cond-bank-mixture)       */
@@ -135,6 +148,13 @@ typedef struct gmc_trace {
   float* ebar;          /* [B][N]: normalised grounded energy ebar_i           */
   float* client;        /* [B][m_rows][N]: pre-weighted client matrix Cbar    */
   float* stats;         /* [B][GMC_STATS]: see GMC_STATS                       */
+  float* round_gains;   /* [B][rounds][N]: each round's singleton gains
+                           u_i = sum_m [Cbar_mi - b_m(S_t)]_+ as the selection
+                           computed them (Eq. cond-responsibility), 0 for tokens
+                           selected in earlier rounds                         */
+  float* round_scores;  /* [B][rounds][pool_cap]: each round's responsibility
+                           scores s_i of the pool, in round_pool's order
+                           (ascending source index), 0 padded                 */
 } gmc_trace;
 
 /* Fill *cfg with the frozen settings; shape/capacity/pointers are zeroed. */
@@ -183,6 +203,65 @@ int gmc_prune_ex(int64_t B, const void* hidden, const void* text_q, const void* 
                  const int32_t* pos3d, int64_t N, int64_t T, int64_t K, void* out_hidden,
                  int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse,
                  const gmc_trace* trace);
+
+/*
+ * Diagnostics (Prop. 1 Eq. deployed-approximation; App. I Eq. cond-final-cert,
+ * Eq. cond-bank-mixture; App. J numerical checks).
+ *
+ * gmc_set_diag - flags for subsequent calls (0 by default):
+ *   GMC_DIAG_CERT    log the deployed batched-solver certificate of every
+ *                    selection round of the call: U_t = the sum of the K
+ *                    largest remaining singleton gains, the round's coverage
+ *                    gain F(S_t u B_t) - F(S_t), q_t = gain / U_t (0 when
+ *                    U_t = 0), c_B = 1 - prod_t (1 - q_t), and the decision
+ *                    margins (relative pool and batch cut gaps).  Computed on
+ *                    the device from the selection's own gains and scores,
+ *                    for calls of at most GMC_CERT_MAX_ROUNDS rounds (and the
+ *                    context's round capacity); extra kernels, no effect on
+ *                    the outputs.
+ *   GMC_DIAG_FINITE  scan the client matrix, row weights and outputs of
+ *                    every call for non-finite values (sets
+ *                    GMC_STATUS_NONFINITE).
+ * Errors: GMC_ERR_STATE, GMC_ERR_ARG (unknown flag).
+ */
+#define GMC_DIAG_CERT 1
+#define GMC_DIAG_FINITE 2
+#define GMC_CERT_MAX_ROUNDS 64
+int gmc_set_diag(int32_t flags);
+
+/*
+ * gmc_diag - host-side diagnostics of the last pruning call (one problem).
+ * The per-round arrays are caller-owned HOST arrays of max_rounds entries,
+ * or NULL; entries past `rounds` are left untouched.
+ */
+typedef struct gmc_diag {
+  uint32_t status;        /* OR of every problem's device status bits (GMC_STATUS_*) */
+  int32_t identity;       /* 1: the last call returned its inputs (K = N)            */
+  int32_t has_certificate;/* 1: the per-round certificate below was computed         */
+  int32_t k, rounds, m_rows, n_discarded;
+  float s_x, dbar;        /* separability gate, mean selected-cosine gap             */
+  float f_s, f_v;         /* F(S), F(V)                                              */
+  float f_bank_s[3], f_bank_v[3]; /* F_b(S), F_b(V): grounded, appearance, spatial   */
+  float c_b;              /* 1 - prod_t (1 - q_t)  (Prop. 1)                         */
+  int32_t max_rounds;     /* capacity of the arrays below                            */
+  float* u_top;           /* [rounds] U_t                                            */
+  float* gain;            /* [rounds] F(S_t u B_t) - F(S_t)                          */
+  float* q;               /* [rounds] q_t                                            */
+  float* pool_margin;     /* [rounds] (u_(p) - u_(p+1)) / u_(1), p = pool size;
+                             INFINITY when the cut is between exact zeros or the
+                             pool takes every remaining token                     */
+  float* batch_margin;    /* [rounds] (s_(b) - s_(b+1)) / s_(1), b = batch size   */
+} gmc_diag;
+
+/*
+ * gmc_get_diag - synchronise the context's streams, fill *out for problem
+ * `problem` (0 <= problem < B) of the last gmc_prune / gmc_prune_ex call,
+ * then clear the device status bits.  Returns GMC_ERR_DEVICE when a
+ * timeout bit was set, GMC_ERR_NONFINITE when the non-finite bit was set
+ * (out is filled in both cases), GMC_ERR_STATE without a context or a
+ * call, GMC_ERR_ARG for a bad problem index or NULL out, GMC_ERR_HIP.
+ */
+int gmc_get_diag(int64_t problem, gmc_diag* out);
 
 /* Realised budget K = min{N, max{K_r, 1}} (Sec. 3.1); 0 if N < 1. Host-only. */
 int64_t gmc_realized_k(int64_t N, int64_t K_req);

@@ -10,10 +10,16 @@ import ctypes
 import os
 from typing import Optional
 
+import numpy as np
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libgmc.so")
 
 GMC_OK, GMC_ERR_ARG, GMC_ERR_CAPACITY, GMC_ERR_STATE, GMC_ERR_HIP = 0, -1, -2, -3, -4
+GMC_ERR_DEVICE, GMC_ERR_NONFINITE = -5, -6
+GMC_STATUS_SELECT_TIMEOUT, GMC_STATUS_BANK_TIMEOUT, GMC_STATUS_NONFINITE = 1, 2, 4
+GMC_DIAG_CERT, GMC_DIAG_FINITE = 1, 2
+GMC_CERT_MAX_ROUNDS = 64
 GMC_F32, GMC_BF16 = 0, 1
 GMC_STATS = 15
 GMC_MAX_GATHER_TENSORS = 64
@@ -51,7 +57,20 @@ class GmcConfig(ctypes.Structure):
 class GmcTrace(ctypes.Structure):
     """Mirror of ``gmc_trace``: optional device output pointers."""
     _fields_ = [("round_pool", _vp), ("round_batch", _vp), ("assign", _vp), ("omega", _vp),
-                ("ebar", _vp), ("client", _vp), ("stats", _vp)]
+                ("ebar", _vp), ("client", _vp), ("stats", _vp), ("round_gains", _vp),
+                ("round_scores", _vp)]
+
+
+class GmcDiag(ctypes.Structure):
+    """Mirror of ``gmc_diag``: host-side diagnostics of the last call."""
+    _fields_ = [("status", ctypes.c_uint32), ("identity", _i32), ("has_certificate", _i32),
+                ("k", _i32), ("rounds", _i32), ("m_rows", _i32), ("n_discarded", _i32),
+                ("s_x", _f32), ("dbar", _f32), ("f_s", _f32), ("f_v", _f32),
+                ("f_bank_s", _f32 * 3), ("f_bank_v", _f32 * 3), ("c_b", _f32),
+                ("max_rounds", _i32),
+                ("u_top", ctypes.POINTER(_f32)), ("gain", ctypes.POINTER(_f32)),
+                ("q", ctypes.POINTER(_f32)), ("pool_margin", ctypes.POINTER(_f32)),
+                ("batch_margin", ctypes.POINTER(_f32))]
 
 
 # name -> (restype, argtypes) of every symbol include/gmc.h declares
@@ -69,6 +88,8 @@ SIGNATURES = {
                                             _vp, _vp]),
     "gmc_gather_rows": (ctypes.c_int, [_i64, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i64, _i64, _i64, _i64,
                                        _i64, _vp]),
+    "gmc_set_diag": (ctypes.c_int, [_i32]),
+    "gmc_get_diag": (ctypes.c_int, [_i64, ctypes.POINTER(GmcDiag)]),
     "gmc_workspace_bytes": (_i64, []),
     "gmc_last_error": (ctypes.c_char_p, []),
     "gmc_free": (None, []),
@@ -155,6 +176,104 @@ def gmc_gather_rows(src_ptrs, dst_ptrs, n_seq, seqs_per_keep, seq_len, seq_len2,
     return lib().gmc_gather_rows(n, src, dst, n_seq, seqs_per_keep, seq_len, seq_len2, row_bytes, keep)
 
 
+def check_prune_inputs(cfg: GmcConfig, dtype, hidden, text_q, vis_k, pos3d, nonvis_lse=None):
+    """Shapes, dtypes and devices of a pruning call's tensors against the
+    context's configuration (the library itself sees raw pointers only).
+    Returns (B, N, T); raises ValueError."""
+    import torch
+    if hidden.dim() != 3 or hidden.shape[2] != cfg.d:
+        raise ValueError(f"hidden must be [B][N][{cfg.d}], got {tuple(hidden.shape)}")
+    b, n, _ = hidden.shape
+    hd = cfg.n_q_heads * cfg.head_dim
+    if text_q.dim() < 3 or text_q.shape[0] != b or int(np.prod(text_q.shape[2:])) != hd:
+        raise ValueError(f"text_q must be [B][T][{cfg.n_q_heads}][{cfg.head_dim}] (or [B][T][Hq*dh]), "
+                         f"got {tuple(text_q.shape)}")
+    t = text_q.shape[1]
+    if vis_k.dim() < 3 or vis_k.shape[0] != b or vis_k.shape[1] != n or \
+            int(np.prod(vis_k.shape[2:])) != cfg.n_kv_heads * cfg.head_dim:
+        raise ValueError(f"vis_k must be [B][N][{cfg.n_kv_heads}][{cfg.head_dim}] (or [B][N][Hkv*dh]), "
+                         f"got {tuple(vis_k.shape)}")
+    if tuple(pos3d.shape) != (b, n, 3) or pos3d.dtype != torch.int32:
+        raise ValueError(f"pos3d must be int32 [B][N][3] = ({b}, {n}, 3), got {pos3d.dtype} {tuple(pos3d.shape)}")
+    for name, x in (("hidden", hidden), ("text_q", text_q), ("vis_k", vis_k)):
+        if x.dtype != dtype:
+            raise ValueError(f"{name} has dtype {x.dtype}, the context computes in {dtype}")
+    tensors = [("hidden", hidden), ("text_q", text_q), ("vis_k", vis_k), ("pos3d", pos3d)]
+    if nonvis_lse is not None:
+        if nonvis_lse.dtype != torch.float32 or tuple(nonvis_lse.shape) != (b, cfg.n_q_heads, t):
+            raise ValueError(f"nonvis_lse must be float32 [B][Hq][T] = ({b}, {cfg.n_q_heads}, {t}), "
+                             f"got {nonvis_lse.dtype} {tuple(nonvis_lse.shape)}")
+        tensors.append(("nonvis_lse", nonvis_lse))
+    for name, x in tensors:
+        if not x.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    dev = hidden.device
+    for name, x in tensors:
+        if x.device.type != "cuda" or x.device != dev:
+            raise ValueError(f"{name} must be on the GPU, on hidden's device; got {x.device}")
+    return b, n, t
+
+
+def check_gather_inputs(caches, keep, seqs_per_keep):
+    """Every cache contiguous with the same [n_seq][L] leading shape and row
+    bytes, on keep's device; keep int32 [n_seq / seqs_per_keep][L2].  Raises
+    ValueError."""
+    import torch
+    if not caches:
+        raise ValueError("gather_rows needs at least one cache")
+    c0 = caches[0]
+    if c0.dim() < 2:
+        raise ValueError("caches must be [n_seq][L][...]")
+    n_seq, seq_len = c0.shape[:2]
+    row_bytes = (c0.numel() // max(n_seq * seq_len, 1)) * c0.element_size()
+    for i, c in enumerate(caches):
+        if c.dim() < 2 or tuple(c.shape[:2]) != (n_seq, seq_len):
+            raise ValueError(f"cache {i} has leading shape {tuple(c.shape[:2])}, expected {(n_seq, seq_len)}")
+        if (c.numel() // max(n_seq * seq_len, 1)) * c.element_size() != row_bytes:
+            raise ValueError(f"cache {i} rows are not {row_bytes} bytes")
+        if not c.is_contiguous():
+            raise ValueError(f"cache {i} must be contiguous")
+    if keep.dtype != torch.int32 or keep.dim() != 2 or not keep.is_contiguous():
+        raise ValueError("keep must be a contiguous int32 [n_seq / seqs_per_keep][L2] tensor")
+    if seqs_per_keep < 1 or keep.shape[0] * seqs_per_keep != n_seq:
+        raise ValueError(f"keep has {keep.shape[0]} lists; {n_seq} sequences need {n_seq} / seqs_per_keep")
+    for i, c in enumerate(caches):
+        if c.device.type != "cuda" or c.device != keep.device:
+            raise ValueError(f"cache {i} must be on the GPU, on keep's device; got {c.device}")
+    return n_seq, seq_len, row_bytes
+
+
+def check_compact_inputs(out_idx, n, seq_rows, vis_rows, seq_pos, seq_len):
+    """out_idx int32 [B][K]; seq_rows [B][L][...] and vis_rows [B][K][...] of one
+    dtype and row size; seq_pos int32 [B][L][3]; all on out_idx's device.
+    Raises ValueError."""
+    import torch
+    if out_idx.dtype != torch.int32 or out_idx.dim() != 2 or not out_idx.is_contiguous():
+        raise ValueError("out_idx must be a contiguous int32 [B][K] tensor")
+    b, k = out_idx.shape
+    if not 1 <= k <= n:
+        raise ValueError(f"need 1 <= K <= N, got K={k}, N={n}")
+    tensors = [("out_idx", out_idx)]
+    if (seq_rows is None) != (vis_rows is None):
+        raise ValueError("seq_rows and vis_rows must be given together")
+    if seq_rows is not None:
+        if seq_rows.shape[0] != b or seq_rows.shape[1] != seq_len or vis_rows.shape[0] != b or vis_rows.shape[1] != k:
+            raise ValueError(f"seq_rows must be [B][L][...] and vis_rows [B][K][...] with B={b}, L={seq_len}, K={k}")
+        if seq_rows.dtype != vis_rows.dtype or seq_rows[0, 0].numel() != vis_rows[0, 0].numel():
+            raise ValueError("seq_rows and vis_rows must share dtype and row size")
+        tensors += [("seq_rows", seq_rows), ("vis_rows", vis_rows)]
+    if seq_pos is not None:
+        if seq_pos.dtype != torch.int32 or tuple(seq_pos.shape) != (b, seq_len, 3):
+            raise ValueError(f"seq_pos must be int32 [B][L][3] = ({b}, {seq_len}, 3)")
+        tensors.append(("seq_pos", seq_pos))
+    for name, x in tensors:
+        if not x.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    for name, x in tensors:
+        if x.device.type != "cuda" or x.device != out_idx.device:
+            raise ValueError(f"{name} must be on the GPU, on out_idx's device; got {x.device}")
+
+
 def compact_sequence(out_idx, vis_start, n, seq_rows=None, vis_rows=None, seq_pos=None, seq_len=None):
     """Tensor-level sequence compaction on torch's current stream (argument
     marshalling only): out_idx [B][K] int32 device; seq_rows [B][L][...] and
@@ -164,6 +283,7 @@ def compact_sequence(out_idx, vis_start, n, seq_rows=None, vis_rows=None, seq_po
     b, k = out_idx.shape
     if seq_len is None:
         seq_len = seq_rows.shape[1] if seq_rows is not None else seq_pos.shape[1]
+    check_compact_inputs(out_idx, n, seq_rows, vis_rows, seq_pos, seq_len)
     l2 = seq_len - n + k
     dev = out_idx.device
     iota = torch.empty((b, seq_len), dtype=torch.int32, device=dev)
@@ -188,16 +308,38 @@ def gather_rows(caches, keep, seqs_per_keep=1):
     [n_seq][L][...] (contiguous), keep [n_seq / seqs_per_keep][L2] int32;
     returns the gathered [n_seq][L2][...] caches."""
     import torch
-    n_seq, seq_len = caches[0].shape[:2]
+    n_seq, seq_len, row_bytes = check_gather_inputs(caches, keep, seqs_per_keep)
     l2 = keep.shape[1]
     outs = [torch.empty((n_seq, l2) + tuple(c.shape[2:]), dtype=c.dtype, device=c.device) for c in caches]
-    row_bytes = caches[0][0, 0].numel() * caches[0].element_size()
     _check(gmc_set_stream(torch.cuda.current_stream(caches[0].device).cuda_stream), "gmc_set_stream")
     for i in range(0, len(caches), GMC_MAX_GATHER_TENSORS):
         part = slice(i, i + GMC_MAX_GATHER_TENSORS)
         _check(gmc_gather_rows([c.data_ptr() for c in caches[part]], [o.data_ptr() for o in outs[part]], n_seq,
                                seqs_per_keep, seq_len, l2, row_bytes, keep.data_ptr()), "gmc_gather_rows")
     return outs
+
+
+def gmc_set_diag(flags: int) -> int:
+    return lib().gmc_set_diag(flags)
+
+
+def gmc_get_diag(problem: int = 0, max_rounds: int = GMC_CERT_MAX_ROUNDS):
+    """Diagnostics of the last pruning call for one problem (synchronises).
+    Returns (code, dict); the per-round arrays hold `rounds` entries."""
+    arrs = {k: (_f32 * max(max_rounds, 1))() for k in ("u_top", "gain", "q", "pool_margin", "batch_margin")}
+    d = GmcDiag()
+    d.max_rounds = max_rounds
+    for k, a in arrs.items():
+        setattr(d, k, ctypes.cast(a, ctypes.POINTER(_f32)))
+    code = lib().gmc_get_diag(problem, ctypes.byref(d))
+    out = {k: getattr(d, k) for k in ("status", "identity", "has_certificate", "k", "rounds", "m_rows",
+                                       "n_discarded", "s_x", "dbar", "f_s", "f_v", "c_b")}
+    out["f_bank_s"] = list(d.f_bank_s)
+    out["f_bank_v"] = list(d.f_bank_v)
+    nr = min(d.rounds, max_rounds) if d.has_certificate else 0
+    for k, a in arrs.items():
+        out[k] = [a[i] for i in range(nr)]
+    return code, out
 
 
 def gmc_workspace_bytes() -> int:
@@ -252,11 +394,8 @@ class Pruner:
 
     def prune(self, hidden, text_q, vis_k, pos3d, k, nonvis_lse=None, trace: bool = False):
         torch = self.torch
-        b, n, d = hidden.shape
-        t = text_q.shape[1]
-        for x in (hidden, text_q, vis_k, pos3d):
-            if not x.is_contiguous():
-                raise ValueError("inputs must be contiguous")
+        b, n, t = check_prune_inputs(self.cfg, self.dtype, hidden, text_q, vis_k, pos3d, nonvis_lse)
+        d = hidden.shape[2]
         kk = gmc_realized_k(n, k)
         dev = hidden.device
         out_h = torch.empty((b, kk, d), dtype=hidden.dtype, device=dev)
@@ -266,17 +405,20 @@ class Pruner:
         if trace:
             rounds, pool_cap, bcap, m_rows = gmc_trace_dims(n, t, k)
             hq = self.cfg.n_q_heads
+            r1 = max(rounds, 1)
             bufs = dict(
-                round_pool=torch.full((b, max(rounds, 1), pool_cap), -1, dtype=torch.int32, device=dev),
-                round_batch=torch.full((b, max(rounds, 1), bcap), -1, dtype=torch.int32, device=dev),
+                round_pool=torch.full((b, r1, pool_cap), -1, dtype=torch.int32, device=dev),
+                round_batch=torch.full((b, r1, bcap), -1, dtype=torch.int32, device=dev),
                 assign=torch.full((b, n), -1, dtype=torch.int32, device=dev),
                 omega=torch.zeros((b, hq), dtype=torch.float32, device=dev),
                 ebar=torch.zeros((b, n), dtype=torch.float32, device=dev),
                 client=torch.zeros((b, m_rows, n), dtype=torch.float32, device=dev),
-                stats=torch.zeros((b, GMC_STATS), dtype=torch.float32, device=dev))
+                stats=torch.zeros((b, GMC_STATS), dtype=torch.float32, device=dev),
+                round_gains=torch.full((b, r1, n), -1.0, dtype=torch.float32, device=dev),
+                round_scores=torch.full((b, r1, pool_cap), -1.0, dtype=torch.float32, device=dev))
             tr = GmcTrace(**{key: v.data_ptr() for key, v in bufs.items()})
         _check(gmc_set_stream(torch.cuda.current_stream(dev).cuda_stream), "gmc_set_stream")
-        nv = None if nonvis_lse is None else nonvis_lse.contiguous().data_ptr()
+        nv = None if nonvis_lse is None else nonvis_lse.data_ptr()
         code = gmc_prune_ex(b, hidden.data_ptr(), text_q.data_ptr() if t > 0 else None,
                             vis_k.data_ptr(), pos3d.data_ptr(), n, t, k, out_h.data_ptr(),
                             out_p.data_ptr(), out_i.data_ptr(), nv, tr)
@@ -284,6 +426,13 @@ class Pruner:
         if trace:
             return out_h, out_p, out_i, bufs
         return out_h, out_p, out_i
+
+    def set_diag(self, flags: int):
+        _check(gmc_set_diag(flags), "gmc_set_diag")
+
+    def diag(self, problem: int = 0):
+        """(code, dict) of gmc_get_diag for the last call (synchronises)."""
+        return gmc_get_diag(problem)
 
     def close(self):
         gmc_free()
@@ -308,3 +457,31 @@ STAGE_NAMES = ["probe", "logits", "heads", "appearance", "spatial", "cov", "gain
 SIGNATURES["gmc_timing_enable"] = (ctypes.c_int, [ctypes.c_int])
 SIGNATURES["gmc_timing_read"] = (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64),
                                                 ctypes.c_int32])
+
+
+# --- host <-> device marshalling of seeded workloads --------------------------
+def to_device(a, dtype: str, torch):
+    """A float32 numpy array holding exact values of `dtype` ("f32" or
+    "bf16") as a contiguous device tensor of that dtype."""
+    from . import synth
+    if dtype == "bf16":
+        bits = synth.bf16_bits(a).view(np.int16)
+        return torch.from_numpy(np.ascontiguousarray(bits)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def from_device(t, torch) -> np.ndarray:
+    return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+
+def make_pruner(prob, torch, max_k=0, probe_bias=None, **overrides) -> Pruner:
+    """A Pruner sized for a seeded workload (synth.Problem): its shape, dtype,
+    batch and token capacity, probe and bounded-bank projection."""
+    w = prob.workload
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    probe = to_device(prob.probe, w.dtype, torch)
+    proj = None if prob.app_proj is None else to_device(prob.app_proj, w.dtype, torch)
+    bias = None if probe_bias is None else torch.from_numpy(np.ascontiguousarray(probe_bias, np.float32)).cuda()
+    return Pruner(d=w.d, n_q_heads=w.hq, n_kv_heads=w.hkv, head_dim=w.dh, probe=probe, dtype=tdt,
+                  max_batch=w.batch, max_n=w.n, max_t=max(w.t, 1), max_k=max_k, app_projection=proj,
+                  probe_bias=bias, **overrides)

@@ -16,6 +16,7 @@
 #include "gmc.h"
 #include "gmc_internal.h"
 #include "gmc_kernels.h"
+#include "gmc_path.h"
 
 using namespace gmc;
 
@@ -23,6 +24,7 @@ namespace {
 
 struct Capacity {
   int B, N, T, K, hq, hr, mv, m, ldM, pool_cap, bmax, ldK, rank;
+  int cert_rounds;   // selection rounds the certificate buffers hold
   bool bounded_possible;
 };
 
@@ -42,6 +44,13 @@ struct Context {
   hipEvent_t fork = nullptr, join = nullptr;
   int call_tag = 0;   // last call number handed to the row-norm blocks
   int device = 0;
+  int diag = 0;       // GMC_DIAG_* flags for the next calls
+  // the last pruning call: its stream (a call on another stream waits for it
+  // through `xfer`), its shape and what it recorded
+  hipStream_t last_stream = nullptr;
+  hipEvent_t xfer = nullptr;
+  bool has_call = false, last_identity = false, last_cert = false;
+  Shape last{};
 };
 
 std::mutex g_mu;
@@ -150,6 +159,7 @@ struct Plan {
   long long s_n, s_z, s_zp, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
       s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_ftag, s_gate,
       s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_ts, s_tc, s_lpart, s_lcnt;
+  long long s_cgain, s_cscore, s_cpool, s_cbat, s_cpart, s_cert, s_dstat;
 };
 
 Plan make_plan(const gmc_config& c) {
@@ -211,6 +221,17 @@ Plan make_plan(const gmc_config& c) {
   pl.s_tu = 2LL * k.N;
   pl.s_ts = 2 * 64 * cdiv(k.ldM, 64);
   pl.s_tc = 2LL * (k.ldM + kMaxPersist);
+  // certificate buffers: rounds of the smallest batch size, at most
+  // kCertMaxRounds
+  k.cert_rounds = static_cast<int>(std::min<long long>(
+      kCertMaxRounds, cdiv(k.K, std::max(1, std::min(c.batch_b, k.bounded_possible ? c.batch_b_bounded : c.batch_b)))));
+  pl.s_cgain = static_cast<long long>(k.cert_rounds) * k.N;
+  pl.s_cscore = static_cast<long long>(k.cert_rounds) * k.pool_cap;
+  pl.s_cpool = pl.s_cscore;
+  pl.s_cbat = static_cast<long long>(k.cert_rounds) * k.bmax;
+  pl.s_cpart = static_cast<long long>(k.cert_rounds) * cdiv(k.ldM, 256);
+  pl.s_cert = static_cast<long long>(k.cert_rounds) * kCertFields + 4;
+  pl.s_dstat = kStats;
   return pl;
 }
 
@@ -259,6 +280,8 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   ws->ts = reinterpret_cast<unsigned long long*>(take(pl.s_ts, 8)); ws->s_ts = pl.s_ts;
   ws->tc = reinterpret_cast<unsigned long long*>(take(pl.s_tc, 8)); ws->s_tc = pl.s_tc;
   F(rstat); F(lstat);
+  ws->cert_rounds = pl.cap.cert_rounds;
+  F(cgain); F(cscore); I(cpool); I(cbat); F(cpart); F(cert); F(dstat);
 #undef F
 #undef I
   return round_up(off, 256);
@@ -267,6 +290,20 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
 }  // namespace
 
 namespace gmc {
+int set_error(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int check_config(const gmc_config* cfg) { return validate_config(cfg); }
+
+Params params_of(const gmc_config& cfg) { return make_params(cfg); }
+
+size_t carve_workspace(const gmc_config& cfg, char* base, Ws* ws) { return carve(make_plan(cfg), base, ws); }
+
 void timer_mark(int stage, bool begin, hipStream_t st) {
   if (!g_timer.on || stage < 0 || stage >= kNumStages) return;
   hipEvent_t e = g_timer.take();
@@ -333,6 +370,7 @@ void gmc_free(void) {
   }
   if (g_ctx->fork) (void)hipEventDestroy(g_ctx->fork);
   if (g_ctx->join) (void)hipEventDestroy(g_ctx->join);
+  if (g_ctx->xfer) (void)hipEventDestroy(g_ctx->xfer);
   if (g_ctx->mem) (void)hipFree(g_ctx->mem);
   delete g_ctx;
   g_ctx = nullptr;
@@ -375,9 +413,11 @@ int gmc_init(const gmc_config* cfg) {
   err = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
   if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->fork, hipEventDisableTiming);
   if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->join, hipEventDisableTiming);
+  if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->xfer, hipEventDisableTiming);
   if (err != hipSuccess) {
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
     if (ctx->fork) (void)hipEventDestroy(ctx->fork);
+    if (ctx->join) (void)hipEventDestroy(ctx->join);
     (void)hipFree(ctx->mem);
     delete ctx;
     return fail(GMC_ERR_HIP, "gmc_init: side stream or events (%s)", hipGetErrorString(err));
@@ -497,15 +537,22 @@ int gmc_timing_read(double* total_ms, int64_t* spans, int32_t n) {
 
 namespace {
 
-// Resolve the call shape; returns GMC_OK or an error code.
 int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req, Shape* out) {
-  const gmc_config& g = c.cfg;
+  return gmc::resolve_shape(c.cfg, Limits{c.cap.B, c.cap.N, c.cap.T, c.cap.K}, B, N, T, K_req, out);
+}
+
+}  // namespace
+
+namespace gmc {
+
+int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, int64_t T, int64_t K_req,
+                  Shape* out) {
   if (B < 1) return fail(GMC_ERR_ARG, "batch=%lld must be >= 1", static_cast<long long>(B));
   if (N < 1) return fail(GMC_ERR_ARG, "N=%lld must be >= 1", static_cast<long long>(N));
   if (T < 0) return fail(GMC_ERR_ARG, "T=%lld must be >= 0", static_cast<long long>(T));
-  if (B > c.cap.B) return fail(GMC_ERR_CAPACITY, "batch=%lld exceeds max_batch=%d", static_cast<long long>(B), c.cap.B);
-  if (N > c.cap.N) return fail(GMC_ERR_CAPACITY, "N=%lld exceeds max_n=%d", static_cast<long long>(N), c.cap.N);
-  if (T > c.cap.T) return fail(GMC_ERR_CAPACITY, "T=%lld exceeds max_t=%d", static_cast<long long>(T), c.cap.T);
+  if (B > cap.B) return fail(GMC_ERR_CAPACITY, "batch=%lld exceeds max_batch=%d", static_cast<long long>(B), cap.B);
+  if (N > cap.N) return fail(GMC_ERR_CAPACITY, "N=%lld exceeds max_n=%d", static_cast<long long>(N), cap.N);
+  if (T > cap.T) return fail(GMC_ERR_CAPACITY, "T=%lld exceeds max_t=%d", static_cast<long long>(T), cap.T);
   const int64_t K = gmc_realized_k(N, K_req);
   Shape s{};
   s.B = static_cast<int>(B);
@@ -521,8 +568,8 @@ int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req,
   s.hr = s.hq * s.r;
   s.dtype = g.dtype;
   s.landmarks = g.landmarks;
-  if (K < N && K > c.cap.K)
-    return fail(GMC_ERR_CAPACITY, "realised K=%lld exceeds max_k=%d", static_cast<long long>(K), c.cap.K);
+  if (K < N && K > cap.K)
+    return fail(GMC_ERR_CAPACITY, "realised K=%lld exceeds max_k=%d", static_cast<long long>(K), cap.K);
   s.bounded = N > g.bounded_threshold_n ? 1 : 0;
   s.app_rank = s.bounded ? g.app_rank : 0;
   s.mg = s.hq * s.T;
@@ -550,18 +597,11 @@ int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req,
   return GMC_OK;
 }
 
-int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
-        int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
-        const float* nonvis_lse, const gmc_trace* trace) {
-  std::lock_guard<std::mutex> lk(g_mu);
-  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_prune: no context (call gmc_init first)");
-  Context& c = *g_ctx;
+int check_tensors(const Shape& s, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+                  const void* out_hidden, const int32_t* out_pos, const int32_t* out_idx) {
   if (!hidden || !vis_k || !pos3d || !out_hidden || !out_pos || !out_idx)
     return fail(GMC_ERR_ARG, "gmc_prune: null tensor pointer");
-  if (T > 0 && !text_q) return fail(GMC_ERR_ARG, "gmc_prune: text_q is NULL with T > 0");
-  Shape s;
-  int rc = make_shape(c, B, N, T, K, &s);
-  if (rc != GMC_OK) return rc;
+  if (s.T > 0 && !text_q) return fail(GMC_ERR_ARG, "gmc_prune: text_q is NULL with T > 0");
   const size_t esz = s.dtype == GMC_F32 ? 4 : 2;
   // outputs must not overlap the inputs
   auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
@@ -584,77 +624,145 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
       if (overlap(outs[o], nouts[o], outs[o2], nouts[o2]))
         return fail(GMC_ERR_ARG, "gmc_prune: outputs %d and %d overlap", o, o2);
   }
-  hipError_t err = hipSetDevice(c.device);
-  if (err != hipSuccess) return fail(GMC_ERR_HIP, "hipSetDevice: %s", hipGetErrorString(err));
-  hipStream_t st = c.stream;
+  return GMC_OK;
+}
+
+int enqueue_prune(const gmc_config& cfg, const Params& pr, const Ws& ws, const Shape& s, const PathStreams& ps,
+                  int diag, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+                  void* out_hidden, int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse,
+                  const gmc_trace& tr, bool* cert_done) {
+  *cert_done = false;
+  hipStream_t st = ps.st;
+  hipError_t err;
   if (s.K == s.N) {
     err = launch_identity(s, hidden, pos3d, out_hidden, out_pos, out_idx, st);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "identity copy: %s", hipGetErrorString(err));
     return GMC_OK;
   }
-  const gmc_trace tr = trace ? *trace : gmc_trace{};
-  // per-call reset and row norms (one kernel), then the bank kernels on the side stream while the message
-  // kernels run on the caller's stream (they write disjoint client rows).
-  // With stage timing on, everything stays on one stream so each stage's
-  // span measures that stage alone.
-  const bool fork = !g_timer.on;
+  // per-call reset and row norms (one kernel), then the bank kernels on the
+  // side stream while the message kernels run on the caller's stream (they
+  // write disjoint client rows).  Without a side stream (stage timing, the
+  // static-scratch entry point) everything stays on one stream.
+  const bool fork = ps.side != nullptr;
   // one image: the fork is a one-block gate on the side stream that waits for
   // this call's row-norm blocks (no event record on the caller's stream, whose
   // next kernel would wait for the command processor to process it).  The
   // gate of the next call may already wait while this call's selection runs,
   // so with several images, whose persistent selection takes every CU, an
   // event is used instead.
-  const bool gate = fork && s.B == 1;
-  int call_tag = 0;
-  if (gate) {
-    c.call_tag = c.call_tag == 0x7fffffff ? 1 : c.call_tag + 1;
-    call_tag = c.call_tag;
-  }
-  err = launch_rownorm(s, c.ws, hidden, call_tag, st);
+  const bool gate = fork && ps.call_tag != 0;
+  err = launch_rownorm(s, ws, hidden, gate ? ps.call_tag : 0, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "row norms: %s", hipGetErrorString(err));
-  hipStream_t bank_st = fork ? c.side : st;
+  hipStream_t bank_st = fork ? ps.side : st;
   if (gate) {
-    err = launch_bank_gate(s, c.ws, call_tag, c.side);
+    err = launch_bank_gate(s, ws, ps.call_tag, ps.side);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
   } else if (fork) {
-    err = hipEventRecord(c.fork, st);
-    if (err == hipSuccess) err = hipStreamWaitEvent(c.side, c.fork, 0);
+    err = hipEventRecord(ps.fork, st);
+    if (err == hipSuccess) err = hipStreamWaitEvent(ps.side, ps.fork, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
   }
-  err = launch_banks(s, c.pr, c.ws, hidden, c.cfg.app_projection, pos3d, bank_st);
+  err = launch_banks(s, pr, ws, hidden, cfg.app_projection, pos3d, bank_st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
   // join: with text queries the last message kernel (one block per problem)
   // waits on a device flag that the side stream raises after its last bank
   // kernel, which costs less than an event wait on the caller's stream;
   // without text queries, an event
-  int* bank_flag = c.ws.cnt + kCntBankFlag;   // cleared by the row-norm kernel
+  int* bank_flag = ws.cnt + kCntBankFlag;   // cleared by the row-norm kernel
   const bool flag_join = fork && s.T > 0;
   if (flag_join) {
-    err = launch_bank_signal(bank_flag, c.side);
+    err = launch_bank_signal(bank_flag, ps.side);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   } else if (fork) {
-    err = hipEventRecord(c.join, c.side);
+    err = hipEventRecord(ps.join, ps.side);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }
-  err = launch_message(s, c.pr, c.ws, hidden, text_q, vis_k, c.cfg.value_probe, nonvis_lse, tr.omega,
+  err = launch_message(s, pr, ws, hidden, text_q, vis_k, cfg.value_probe, nonvis_lse, tr.omega,
                        flag_join ? bank_flag : nullptr, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
   if (fork && !flag_join) {
-    err = hipStreamWaitEvent(st, c.join, 0);
+    err = hipStreamWaitEvent(st, ps.join, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }
+  // per-round outputs of the selection: the trace's buffers, completed with
+  // the workspace's certificate buffers when the certificate is computed
+  const bool want_cert = (diag & GMC_DIAG_CERT) != 0 || (tr.round_gains && tr.round_scores);
+  SelOut so{tr.round_pool, tr.round_batch, tr.round_gains, tr.round_scores};
+  const bool cert = want_cert && s.rounds >= 1 && s.rounds <= ws.cert_rounds;
+  if (cert) {
+    if (!so.pool) so.pool = ws.cpool;
+    if (!so.batch) so.batch = ws.cbat;
+    if (!so.gains) so.gains = ws.cgain;
+    if (!so.scores) so.scores = ws.cscore;
+  }
   bool support_ready = false;
-  err = launch_selection(s, c.pr, c.ws, tr.round_pool, tr.round_batch, st, &support_ready);
+  err = launch_selection(s, pr, ws, so, st, &support_ready);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "selection kernels: %s", hipGetErrorString(err));
-  err = launch_assignment(s, c.pr, c.ws, hidden, support_ready, tr.assign, st);
+  err = launch_assignment(s, pr, ws, hidden, support_ready, tr.assign, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "assignment kernels: %s", hipGetErrorString(err));
-  err = launch_transport(s, c.pr, c.ws, hidden, pos3d, out_hidden, out_pos, out_idx, st);
+  err = launch_transport(s, pr, ws, hidden, pos3d, out_hidden, out_pos, out_idx, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "transport kernels: %s", hipGetErrorString(err));
+  if (cert) {
+    err = launch_certificate(s, ws, so, st);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "certificate kernels: %s", hipGetErrorString(err));
+    *cert_done = true;
+  }
+  if (diag & GMC_DIAG_FINITE) {
+    err = launch_finite_scan(s, ws, out_hidden, st);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "non-finite scan: %s", hipGetErrorString(err));
+  }
   if (tr.client || tr.stats || tr.ebar) {
-    err = launch_trace_exports(s, c.ws, tr.client, tr.stats, tr.ebar, st);
+    err = launch_trace_exports(s, ws, tr.client, tr.stats, tr.ebar, st);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "trace exports: %s", hipGetErrorString(err));
   }
   return GMC_OK;
+}
+
+}  // namespace gmc
+
+namespace {
+
+int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+        int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
+        const float* nonvis_lse, const gmc_trace* trace) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_prune: no context (call gmc_init first)");
+  Context& c = *g_ctx;
+  Shape s;
+  int rc = make_shape(c, B, N, T, K, &s);
+  if (rc != GMC_OK) return rc;
+  rc = check_tensors(s, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx);
+  if (rc != GMC_OK) return rc;
+  const gmc_trace tr = trace ? *trace : gmc_trace{};
+  hipError_t err = hipSetDevice(c.device);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "hipSetDevice: %s", hipGetErrorString(err));
+  hipStream_t st = c.stream;
+  // the workspace is shared by every call: a call on another stream than the
+  // previous one first waits for that stream (its selection may still read
+  // the client matrix that this call's bank kernels rewrite)
+  if (c.has_call && st != c.last_stream) {
+    err = hipEventRecord(c.xfer, c.last_stream);
+    if (err == hipSuccess) err = hipStreamWaitEvent(st, c.xfer, 0);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "ordering after the previous call's stream: %s",
+                                       hipGetErrorString(err));
+  }
+  c.has_call = true;
+  c.last_stream = st;
+  c.last = s;
+  c.last_identity = s.K == s.N;
+  c.last_cert = false;
+  // stage timing keeps every kernel on the caller's stream, so each stage's
+  // span measures that stage alone
+  PathStreams ps{st, g_timer.on ? nullptr : c.side, 0, c.fork, c.join};
+  if (ps.side && s.B == 1 && s.K < s.N) {
+    c.call_tag = c.call_tag == 0x7fffffff ? 1 : c.call_tag + 1;
+    ps.call_tag = c.call_tag;
+  }
+  bool cert = false;
+  rc = enqueue_prune(c.cfg, c.pr, c.ws, s, ps, c.diag, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx,
+                     nonvis_lse, tr, &cert);
+  c.last_cert = cert;
+  return rc;
 }
 
 }  // namespace
@@ -676,6 +784,83 @@ int gmc_prune_ex(int64_t B, const void* hidden, const void* text_q, const void* 
                  int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
                  const float* nonvis_lse, const gmc_trace* trace) {
   return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nonvis_lse, trace);
+}
+
+int gmc_set_diag(int32_t flags) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_set_diag: no context");
+  if (flags & ~(GMC_DIAG_CERT | GMC_DIAG_FINITE)) return fail(GMC_ERR_ARG, "gmc_set_diag: unknown flags 0x%x", flags);
+  g_ctx->diag = flags;
+  return GMC_OK;
+}
+
+int gmc_get_diag(int64_t problem, gmc_diag* out) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_get_diag: no context");
+  Context& c = *g_ctx;
+  if (!c.has_call) return fail(GMC_ERR_STATE, "gmc_get_diag: no pruning call yet");
+  if (!out) return fail(GMC_ERR_ARG, "gmc_get_diag: out is NULL");
+  const Shape& s = c.last;
+  if (problem < 0 || problem >= s.B)
+    return fail(GMC_ERR_ARG, "gmc_get_diag: problem %lld outside [0, %d)", static_cast<long long>(problem), s.B);
+  hipError_t err = hipSetDevice(c.device);
+  if (err == hipSuccess) err = hipStreamSynchronize(c.last_stream);
+  if (err == hipSuccess) err = hipStreamSynchronize(c.side);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "gmc_get_diag: %s", hipGetErrorString(err));
+  const int p = static_cast<int>(problem);
+  std::vector<int> cnt(static_cast<size_t>(c.cap.B) * kCounters);
+  float st[kStats] = {};
+  std::vector<float> cert;
+  if (!c.last_identity) {
+    err = launch_trace_exports(s, c.ws, nullptr, c.ws.dstat, nullptr, c.last_stream);
+    if (err == hipSuccess) err = hipStreamSynchronize(c.last_stream);
+    if (err == hipSuccess)
+      err = hipMemcpy(st, c.ws.dstat + p * c.ws.s_dstat, sizeof(st), hipMemcpyDeviceToHost);
+    if (err == hipSuccess && c.last_cert) {
+      cert.resize(static_cast<size_t>(c.ws.s_cert));
+      err = hipMemcpy(cert.data(), c.ws.cert + p * c.ws.s_cert, cert.size() * sizeof(float), hipMemcpyDeviceToHost);
+    }
+  }
+  if (err == hipSuccess)
+    err = hipMemcpy(cnt.data(), c.ws.cnt, cnt.size() * sizeof(int), hipMemcpyDeviceToHost);
+  if (err == hipSuccess) err = launch_clear_status(c.ws, c.cap.B, c.last_stream);
+  if (err == hipSuccess) err = hipStreamSynchronize(c.last_stream);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "gmc_get_diag: %s", hipGetErrorString(err));
+  uint32_t status = 0;
+  for (int q = 0; q < c.cap.B; ++q) status |= static_cast<uint32_t>(cnt[static_cast<size_t>(q) * kCounters + kCntStatus]);
+  out->status = status;
+  out->identity = c.last_identity ? 1 : 0;
+  out->has_certificate = c.last_cert ? 1 : 0;
+  out->k = s.K;
+  out->rounds = c.last_identity ? 0 : s.rounds;
+  out->m_rows = c.last_identity ? 0 : s.m;
+  out->n_discarded = s.N - s.K;
+  out->s_x = st[0];
+  out->dbar = st[1];
+  out->f_s = st[2];
+  out->f_v = st[3];
+  for (int b = 0; b < 3; ++b) {
+    out->f_bank_s[b] = st[9 + b];
+    out->f_bank_v[b] = st[12 + b];
+  }
+  out->c_b = 0.f;
+  if (c.last_cert) {
+    out->c_b = cert[static_cast<size_t>(c.ws.cert_rounds) * kCertFields];
+    const int nr = std::min(s.rounds, std::max(out->max_rounds, 0));
+    for (int r = 0; r < nr; ++r) {
+      const float* ce = cert.data() + static_cast<size_t>(r) * kCertFields;
+      if (out->u_top) out->u_top[r] = ce[0];
+      if (out->gain) out->gain[r] = ce[1];
+      if (out->q) out->q[r] = ce[2];
+      if (out->pool_margin) out->pool_margin[r] = ce[3];
+      if (out->batch_margin) out->batch_margin[r] = ce[4];
+    }
+  }
+  if (status & (kStatusSelect | kStatusBank))
+    return fail(GMC_ERR_DEVICE, "a bounded device wait timed out (status 0x%x): the results are invalid", status);
+  if (status & kStatusNonfinite)
+    return fail(GMC_ERR_NONFINITE, "a non-finite value was met (status 0x%x)", status);
+  return GMC_OK;
 }
 
 int gmc_trace_dims(int64_t N, int64_t T, int64_t K, int64_t* rounds, int64_t* pool_cap, int64_t* batch_cap,

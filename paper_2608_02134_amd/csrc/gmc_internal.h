@@ -14,8 +14,18 @@ constexpr int kHeadTok = 8;       // tokens per head-Gram block (two per wave)
 constexpr int kStats = 15;
 constexpr int kCounters = 8;      // completion counters per problem
 constexpr int kCntBankFlag = 6;   // slot of problem 0: the bank kernels of the call have finished
-constexpr int kCntStatus = 7;     // device status bits, 1 = a bounded device wait timed out
-constexpr int kBankSpinLimit = 1 << 18;   // polls of the bank flag before the wait gives up
+constexpr int kCntStatus = 7;     // device status bits (sticky; cleared from the host only)
+constexpr unsigned kStatusSelect = 1u;    // a hand-off wait of the persistent selection timed out
+constexpr unsigned kStatusBank = 2u;      // the bank stream's gate or join timed out
+constexpr unsigned kStatusNonfinite = 4u; // debug scan: a non-finite value
+// Bounded waits of the bank stream, in ticks of the 100 MHz constant clock:
+// the start gate may wait behind everything the caller queued before the
+// call, so it gives up only after 10 s; the join waits for bank kernels that
+// run concurrently, 2 s.
+constexpr unsigned long long kGateWaitTicks = 1000000000ull;
+constexpr unsigned long long kJoinWaitTicks = 200000000ull;
+constexpr int kCertMaxRounds = 64;   // GMC_CERT_MAX_ROUNDS
+constexpr int kCertFields = 5;       // U_t, gain, q_t, pool margin, batch margin
 constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection
 constexpr int kMaxGather = 64;    // tensors per row-gather launch (GMC_MAX_GATHER_TENSORS)
 constexpr int kLogitSplit = 8;    // column ranges of the message-logit kernels (at most)
@@ -98,9 +108,36 @@ struct Ws {
   unsigned long long* tu; long long s_tu;  // tagged gains               [2][N]
   unsigned long long* ts; long long s_ts;  // tagged score partials     [2][ceil(M/64)][64]
   unsigned long long* tc; long long s_tc;  // tagged coverage + heartbeats [2][ldM + kMaxPersist]
+  // diagnostics (certificate of the selection rounds, exported statistics);
+  // the per-round buffers are indexed flat as (p * rounds + r) * row, so a
+  // call of at most cert_rounds rounds fits
+  int cert_rounds;                      // round capacity of the buffers below
+  float* cgain;    long long s_cgain;   // each round's gains           [cert_rounds][N]
+  float* cscore;   long long s_cscore;  // each round's pool scores     [cert_rounds][pool_cap]
+  int* cpool;      long long s_cpool;   // each round's pool            [cert_rounds][pool_cap]
+  int* cbat;       long long s_cbat;    // each round's batch           [cert_rounds][bmax]
+  float* cpart;    long long s_cpart;   // coverage-gain block partials [cert_rounds][ceil(ldM/256)]
+  float* cert;     long long s_cert;    // per-round certificate        [cert_rounds][kCertFields] + c_B
+  float* dstat;    long long s_dstat;   // exported statistics          [kStats]
+};
+
+// Per-round outputs of the selection kernels (all optional): pools and
+// batches as the trace lays them out, the gains of every token and the pool
+// scores; entry (p, r) starts at (p * rounds + r) times the row length.
+struct SelOut {
+  int32_t* pool;    // [pool_cap]
+  int32_t* batch;   // [b]
+  float* gains;     // [N]
+  float* scores;    // [pool_cap]
 };
 
 #ifdef __HIPCC__
+// Records device status bits of problem p's counters (sticky OR).
+__device__ __forceinline__ void raise_status(int* cnt, unsigned bits) {
+  __hip_atomic_fetch_or(reinterpret_cast<unsigned*>(&cnt[kCntStatus]), bits, __ATOMIC_RELAXED,
+                        __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Per-call state of problem p, over a grid-stride range (x0, stride): nothing
 // selected, coverage and row-weight padding zero, tagged hand-off buffers and
 // completion counters cleared.  Runs inside the first kernel of a call.
@@ -117,8 +154,10 @@ __device__ __forceinline__ void call_init_range(const Shape& sh, const Ws& ws, i
   for (int j = x0; j < 128 * ((sh.m + 63) / 64); j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
   for (int j = x0; j < 2 * (sh.ldM + kMaxPersist); j += stride) ws.tc[p * ws.s_tc + j] = 0ull;
   for (int j = x0; j < (sh.hg * sh.T + 15) / 16 * sh.hkv; j += stride) ws.lcnt[p * ws.s_lcnt + j] = 0;
-  // written through: the bank stream raises its flag in these words
-  if (x0 < kCounters) __hip_atomic_store(&ws.cnt[p * ws.s_cnt + x0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // written through: the bank stream raises its flag in these words; the
+  // status word is sticky (the host clears it after reading it)
+  if (x0 < kCounters && x0 != kCntStatus)
+    __hip_atomic_store(&ws.cnt[p * ws.s_cnt + x0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 #endif
 

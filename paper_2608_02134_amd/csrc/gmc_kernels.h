@@ -41,8 +41,20 @@ hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const v
 
 // All selection rounds, then the final coverage and objective values.
 // *support_ready reports that the support list and slots were written too.
-hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
-                            int32_t* trace_batch, hipStream_t st, bool* support_ready);
+// `so` receives each round's pool, batch, gains and pool scores (any may be
+// NULL).
+hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, const SelOut& so, hipStream_t st,
+                            bool* support_ready);
+
+// Certificate of the selection rounds from the exported per-round pools,
+// batches, gains and scores (all of `so` set; sh.rounds <= ws.cert_rounds).
+hipError_t launch_certificate(const Shape& sh, const Ws& ws, const SelOut& so, hipStream_t st);
+
+// Debug scan for non-finite client energies, row weights and outputs.
+hipError_t launch_finite_scan(const Shape& sh, const Ws& ws, const void* out_hidden, hipStream_t st);
+
+// Clears the device status words of problems [0, nprob).
+hipError_t launch_clear_status(const Ws& ws, int nprob, hipStream_t st);
 
 // Support list, selected-cosine gaps, separability gate, assignment.
 hipError_t launch_assignment(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,

@@ -58,12 +58,16 @@ __global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* 
 }
 
 // The bank stream's first kernel: one block waits until every row-norm block
-// of the call has tagged itself (bounded), so the bank kernels that follow on
-// that stream see the norms and the per-call reset, and start only after the
-// caller's stream has finished the previous call.
+// of the call has tagged itself, so the bank kernels that follow on that
+// stream see the norms and the per-call reset, and start only after the
+// caller's stream has finished the previous call.  The caller may have queued
+// other work ahead of the call, so the wait is bounded in time (10 s of the
+// constant clock), not in polls; a timeout raises the sticky status bit.
 __global__ void __launch_bounds__(256) bank_gate_kernel(Shape sh, Ws ws, int call_tag) {
   const int nb = (sh.N + 3) / 4, total = nb * sh.B;
-  for (int x0 = 0; x0 < total; x0 += 256 * 8) {
+  const unsigned long long t0 = static_cast<unsigned long long>(wall_clock64());
+  bool expired = false;
+  for (int x0 = 0; x0 < total && !expired; x0 += 256 * 8) {
     int v[8];
     bool need[8];
 #pragma unroll
@@ -78,8 +82,9 @@ __global__ void __launch_bounds__(256) bank_gate_kernel(Shape sh, Ws ws, int cal
 #pragma unroll
       for (int q = 0; q < 8; ++q) pend |= need[q] && v[q] != call_tag;
       if (!pend) break;
-      if (spin == kBankSpinLimit) {
-        __hip_atomic_store(&ws.cnt[kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if ((spin & 255) == 255 && static_cast<unsigned long long>(wall_clock64()) - t0 > kGateWaitTicks) {
+        raise_status(ws.cnt, kStatusBank);
+        expired = true;
         break;
       }
       __builtin_amdgcn_s_sleep(8);   // a light poll: it may wait through a whole selection
@@ -1021,9 +1026,10 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
   // their client rows, so this one ends only once the side stream has raised
   // bank_flag (one thread per block waits; every wait is bounded)
   if (bank_flag && tid == 0) {
+    const unsigned long long t0 = static_cast<unsigned long long>(wall_clock64());
     for (int spin = 0; __hip_atomic_load(bank_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 1; ++spin) {
-      if (spin == kBankSpinLimit) {
-        __hip_atomic_store(&ws.cnt[p * ws.s_cnt + kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if ((spin & 255) == 255 && static_cast<unsigned long long>(wall_clock64()) - t0 > kJoinWaitTicks) {
+        raise_status(ws.cnt + p * ws.s_cnt, kStatusBank);
         break;
       }
       __builtin_amdgcn_s_sleep(2);

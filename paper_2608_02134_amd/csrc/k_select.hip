@@ -301,7 +301,7 @@ __global__ void __launch_bounds__(256) cov_kernel(Shape sh, Ws ws, int nb) {
 // ---------------------------------------------------------------------------
 template <bool kGlobalKeys>
 __global__ void __launch_bounds__(256)
-gains_kernel(Shape sh, Ws ws, int round, int psize, int32_t* trace_pool) {
+gains_kernel(Shape sh, Ws ws, int round, int psize, SelOut so) {
   extern __shared__ uint32_t keys_lds[];
   __shared__ int hist[512], scan[16], bc[2], flag;
   const int p = blockIdx.y;
@@ -357,14 +357,17 @@ gains_kernel(Shape sh, Ws ws, int round, int psize, int32_t* trace_pool) {
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int i = base + q * 256 + tid;
-      if (i < sh.N) keys[i] = (sl[q] >= 0) ? 0u : score_key(g[q]);
+      if (i < sh.N) {
+        keys[i] = (sl[q] >= 0) ? 0u : score_key(g[q]);
+        if (so.gains) so.gains[(static_cast<long long>(p) * sh.rounds + round) * sh.N + i] = (sl[q] >= 0) ? 0.f : g[q];
+      }
     }
   }
   __syncthreads();
   int* pool = ws.pool + p * ws.s_pool;
   block_topk256(keys, sh.N, psize, pool, hist, scan, bc);
-  if (trace_pool) {
-    int32_t* tp = trace_pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
+  if (so.pool) {
+    int32_t* tp = so.pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
     for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool[j] : -1;
   }
 }
@@ -451,7 +454,7 @@ __device__ __forceinline__ float transpose_reduce64(float* v, int lane) {
 // scores summed in block order, top-b by (score desc, index asc).  Leaves
 // the pool in pool_s and the chosen source indices, ascending, in bidx.
 __device__ void small_batch(const Shape& sh, const Ws& ws, int p, int psize, int bsize, int nblk,
-                            int* pool_s, uint32_t* keys, int* chosen, int* bidx) {
+                            int* pool_s, uint32_t* keys, int* chosen, int* bidx, float* scores) {
   const int lane = threadIdx.x & 63;
   pool_s[lane] = (lane < psize) ? ws.pool[p * ws.s_pool + lane] : 0;
   const float* sp = ws.spart + p * ws.s_spart;
@@ -465,6 +468,7 @@ __device__ void small_batch(const Shape& sh, const Ws& ws, int p, int psize, int
     for (int q = 0; q < 8; ++q) s += t[q];
   }
   for (; b < nblk; ++b) s += sp[static_cast<long long>(b) * 64 + lane];
+  if (scores && lane < sh.pool_cap) scores[lane] = lane < psize ? s : 0.f;
   keys[lane] = score_key(s);
   __builtin_amdgcn_wave_barrier();
   wave_topb(keys, psize, bsize, chosen);
@@ -482,7 +486,7 @@ __device__ void small_batch(const Shape& sh, const Ws& ws, int p, int psize, int
 template <bool kGlobalKeys>
 __global__ void __launch_bounds__(256)
 gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int prev_bsize, int prev_base,
-                   int32_t* trace_pool, int32_t* trace_batch) {
+                   SelOut so) {
   extern __shared__ float dyn[];      // refreshed coverage [ldM], then LDS keys [N]
   __shared__ int hist[512], scan[16], bc[2], flag;
   __shared__ int pool_s[64], chosen[64], bidx[64];
@@ -495,9 +499,12 @@ gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int pr
   const float* E = ws.E + p * ws.s_E;
   const int nb = round > 0 ? prev_bsize : 0;
   if (round > 0) {
-    if (wave == 0) small_batch(sh, ws, p, prev_psize, prev_bsize, (sh.m + 255) / 256, pool_s, bkeys, chosen, bidx);
+    float* sc = (so.scores && blockIdx.x == 0)
+                    ? so.scores + (static_cast<long long>(p) * sh.rounds + round - 1) * sh.pool_cap : nullptr;
+    if (wave == 0)
+      small_batch(sh, ws, p, prev_psize, prev_bsize, (sh.m + 255) / 256, pool_s, bkeys, chosen, bidx, sc);
     __syncthreads();
-    if (blockIdx.x == 0) commit_batch(sh, ws, p, round - 1, prev_bsize, prev_base, pool_s, chosen, trace_batch);
+    if (blockIdx.x == 0) commit_batch(sh, ws, p, round - 1, prev_bsize, prev_base, pool_s, chosen, so.batch);
     // two row chunks per trip, all their batch-column loads in flight together
     for (int m0 = tid * 4; m0 < sh.m; m0 += 2048) {
       float4 c[2], a[2], b[2];
@@ -589,27 +596,29 @@ gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int pr
         bool taken = sl[q] >= 0;
         for (int k = 0; k < nb; ++k) taken |= bidx[k] == i;
         keys[i] = taken ? 0u : score_key(g[q]);
+        if (so.gains) so.gains[(static_cast<long long>(p) * sh.rounds + round) * sh.N + i] = taken ? 0.f : g[q];
       }
     }
   }
   __syncthreads();
   int* pool = ws.pool + p * ws.s_pool;
   block_topk256(keys, sh.N, psize, pool, hist, scan, bc);
-  if (trace_pool) {
-    int32_t* tp = trace_pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
+  if (so.pool) {
+    int32_t* tp = so.pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
     for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool[j] : -1;
   }
 }
 
 // Small pools, after the last round: its batch from the responsibility sums.
 __global__ void __launch_bounds__(64) final_batch_kernel(Shape sh, Ws ws, int round, int psize, int bsize,
-                                                         int sel_base, int32_t* trace_batch) {
+                                                         int sel_base, SelOut so) {
   __shared__ int pool_s[64], chosen[64], bidx[64];
   __shared__ __attribute__((aligned(16))) uint32_t keys[64];
   const int p = blockIdx.x;
-  small_batch(sh, ws, p, psize, bsize, (sh.m + 255) / 256, pool_s, keys, chosen, bidx);
+  small_batch(sh, ws, p, psize, bsize, (sh.m + 255) / 256, pool_s, keys, chosen, bidx,
+              so.scores ? so.scores + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap : nullptr);
   __syncthreads();
-  commit_batch(sh, ws, p, round, bsize, sel_base, pool_s, chosen, trace_batch);
+  commit_batch(sh, ws, p, round, bsize, sel_base, pool_s, chosen, so.batch);
 }
 
 // Pool of at most 64: per-block responsibility sums; the batch is picked by
@@ -704,7 +713,7 @@ __global__ void __launch_bounds__(256) rowstat_kernel(Shape sh, Params pr, Ws ws
 // Large pools: one wave per pool position sums rho R over all client rows;
 // the last block picks the batch.
 __global__ void __launch_bounds__(256)
-colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, int32_t* trace_batch) {
+colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, SelOut so) {
   extern __shared__ uint32_t keys[];   // pool_cap words
   __shared__ int hist[512], scan[16], bc[2], flag;
   __shared__ int chosen[1024];
@@ -744,10 +753,16 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 #pragma unroll
     for (int q = 0; q < 8; ++q)
       if (q * 256 + tid < psize) keys[q * 256 + tid] = score_key(g[q]);
+    if (so.scores) {
+      float* sc = so.scores + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (q * 256 + tid < sh.pool_cap) sc[q * 256 + tid] = q * 256 + tid < psize ? g[q] : 0.f;
+    }
   }
   __syncthreads();
   block_topk256(keys, psize, bsize, chosen, hist, scan, bc);
-  commit_batch(sh, ws, p, round, bsize, sel_base, pool, chosen, trace_batch);
+  commit_batch(sh, ws, p, round, bsize, sel_base, pool, chosen, so.batch);
 }
 
 // ---------------------------------------------------------------------------
@@ -785,9 +800,9 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, in
 // every wave always exits.
 constexpr int kSpinLimit = 1 << 18;   // bounded waits (a fraction of a second)
 
-// Marks the call failed (device status word) after a bounded wait.
+// Marks the call failed (sticky device status bit) after a bounded wait.
 __device__ __forceinline__ void mark_timeout(int* cnt, int* failed) {
-  __hip_atomic_store(&cnt[kCntStatus], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  raise_status(cnt, kStatusSelect);
   *failed = 1;
 }
 
@@ -842,7 +857,7 @@ __device__ __forceinline__ void pool_regs(const Shape& sh, const unsigned long l
 constexpr int kResJ = 14;
 template <bool RES>
 __global__ void __launch_bounds__(256)
-select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_pool, int32_t* trace_batch) {
+select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   extern __shared__ float dyn[];
   // LDS: b_m [ldM] | alpha_m [ldM] | selected flags [N, padded to 16 bytes] |
   //      pool keys [N] (only when N exceeds the register top-k)
@@ -925,15 +940,24 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       __syncthreads();
       if (tid < 8) {
         const int t = blk * 8 + tid;
-        if (t < sh.N && !taken[t])
-          st_dev64(&tur[t], tag_value(tag, ((rmu[0][tid] + rmu[1][tid]) + rmu[2][tid]) + rmu[3][tid]));
+        const float g = ((rmu[0][tid] + rmu[1][tid]) + rmu[2][tid]) + rmu[3][tid];
+        if (t < sh.N && !taken[t]) st_dev64(&tur[t], tag_value(tag, g));
+        if (so.gains && t < sh.N)
+          so.gains[(static_cast<long long>(p) * sh.rounds + r) * sh.N + t] = taken[t] ? 0.f : g;
       }
     } else
     for (int i0 = gw; i0 < sh.N; i0 += 2 * nwaves) {
       const int i1 = i0 + nwaves;
       const bool ok0 = taken[i0] == 0;
       const bool ok1 = i1 < sh.N && taken[min(i1, sh.N - 1)] == 0;
-      if (!ok0 && !ok1) continue;
+      float* gout = so.gains ? so.gains + (static_cast<long long>(p) * sh.rounds + r) * sh.N : nullptr;
+      if (!ok0 && !ok1) {
+        if (gout && lane == 0) {
+          gout[i0] = 0.f;
+          if (i1 < sh.N) gout[i1] = 0.f;
+        }
+        continue;
+      }
       // a token that needs no gain re-reads the other one's row (cache hits)
       const float* c0 = E + static_cast<long long>(ok0 ? i0 : i1) * sh.ldM;
       const float* c1 = E + static_cast<long long>(ok1 ? i1 : i0) * sh.ldM;
@@ -954,6 +978,10 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       if (lane == 0) {
         if (ok0) st_dev64(&tur[i0], tag_value(tag, a0));
         if (ok1) st_dev64(&tur[i1], tag_value(tag, a1));
+        if (gout) {
+          gout[i0] = ok0 ? a0 : 0.f;
+          if (i1 < sh.N) gout[i1] = ok1 ? a1 : 0.f;
+        }
       }
     }
 
@@ -1006,8 +1034,8 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
       if (tid < 64) pool_s[tid] = pv;
       __syncthreads();
     }
-    if (blk == nblk - 1 && trace_pool) {
-      int32_t* tp = trace_pool + (static_cast<long long>(p) * sh.rounds + r) * sh.pool_cap;
+    if (blk == nblk - 1 && so.pool) {
+      int32_t* tp = so.pool + (static_cast<long long>(p) * sh.rounds + r) * sh.pool_cap;
       for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool_s[j] : -1;
     }
 
@@ -1093,6 +1121,8 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     __syncthreads();
     if (wave == 0) {
       const float s = ((rmu[0][lane] + rmu[1][lane]) + rmu[2][lane]) + rmu[3][lane];
+      if (blk == nblk - 1 && so.scores && lane < sh.pool_cap)
+        so.scores[(static_cast<long long>(p) * sh.rounds + r) * sh.pool_cap + lane] = lane < psize ? s : 0.f;
       bkeys[lane] = score_key(s);
       __builtin_amdgcn_wave_barrier();
       wave_topb(bkeys, psize, bsize, chosen);
@@ -1102,7 +1132,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, int32_t* trace_po
     __syncthreads();
     const bool last = r + 1 == sh.rounds;
     // the last block records the batch (and alone finishes the last round)
-    if (blk == nblk - 1) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, trace_batch);
+    if (blk == nblk - 1) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, so.batch);
     else if (last) break;
     if (tid < bsize) taken[bidx[tid]] = 1;
     if (!last) {
@@ -1338,8 +1368,8 @@ static int persistent_blocks(const Shape& sh, size_t lds, int res) {
   return nblk >= 1 ? nblk : 0;
 }
 
-hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int32_t* trace_pool,
-                            int32_t* trace_batch, hipStream_t st, bool* support_ready) {
+hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, const SelOut& so, hipStream_t st,
+                            bool* support_ready) {
   *support_ready = false;
   {
     const size_t lds = 2 * static_cast<size_t>(sh.ldM) * sizeof(float) +
@@ -1354,10 +1384,10 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
       timer_mark(kStSelect, true, st);
       if (resident)
         hipLaunchKernelGGL(select_persistent_kernel<true>, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws,
-                           nblk, trace_pool, trace_batch);
+                           nblk, so);
       else
         hipLaunchKernelGGL(select_persistent_kernel<false>, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws, nblk,
-                           trace_pool, trace_batch);
+                           so);
       timer_mark(kStSelect, false, st);
       *support_ready = true;
       return hipGetLastError();
@@ -1383,10 +1413,10 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
       timer_mark(kStGains, true, st);
       if (global_keys)
         hipLaunchKernelGGL(gains_fused_kernel<true>, ggf, dim3(256), fused_lds, st, sh, ws, r, psize,
-                           prev_psize, prev_bsize, prev_base, trace_pool, trace_batch);
+                           prev_psize, prev_bsize, prev_base, so);
       else
         hipLaunchKernelGGL(gains_fused_kernel<false>, ggf, dim3(256), fused_lds, st, sh, ws, r, psize,
-                           prev_psize, prev_bsize, prev_base, trace_pool, trace_batch);
+                           prev_psize, prev_bsize, prev_base, so);
       timer_mark(kStGains, false, st);
       timer_mark(kStResp, true, st);
       hipLaunchKernelGGL(resp_small_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws,
@@ -1400,9 +1430,9 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
       }
       timer_mark(kStGains, true, st);
       if (global_keys)
-        hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, trace_pool);
+        hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, so);
       else
-        hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, trace_pool);
+        hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, so);
       timer_mark(kStGains, false, st);
       timer_mark(kStResp, true, st);
       if (sh.pool_cap <= 64)
@@ -1412,11 +1442,11 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
         hipLaunchKernelGGL(rowstat_kernel, dim3((sh.m + 63) / 64, sh.B), dim3(256), 0, st, sh, pr, ws, psize);
         hipLaunchKernelGGL(colsum_kernel, dim3((psize + 3) / 4, sh.B), dim3(256),
                            static_cast<size_t>(sh.pool_cap) * sizeof(uint32_t), st, sh, ws, r, psize, bsize,
-                           selected, trace_batch);
+                           selected, so);
       }
       if (sh.pool_cap <= 64)
         hipLaunchKernelGGL(final_batch_kernel, dim3(sh.B), dim3(64), 0, st, sh, ws, r, psize, bsize, selected,
-                           trace_batch);
+                           so);
       timer_mark(kStResp, false, st);
     }
     prev_psize = psize;
@@ -1427,7 +1457,7 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, int
   timer_mark(kStObjective, true, st);
   if (fused)
     hipLaunchKernelGGL(final_batch_kernel, dim3(sh.B), dim3(64), 0, st, sh, ws, sh.rounds - 1, prev_psize,
-                       prev_bsize, prev_base, trace_batch);
+                       prev_bsize, prev_base, so);
   launch_cov(sh, ws, prev_bsize, st);
   hipLaunchKernelGGL(objective_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
   timer_mark(kStObjective, false, st);

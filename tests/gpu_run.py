@@ -5,28 +5,7 @@ from __future__ import annotations
 import numpy as np
 
 from paper_2608_02134_amd import binding, synth
-
-
-def to_device(a: np.ndarray, dtype: str, torch):
-    if dtype == "bf16":
-        bits = synth.bf16_bits(a).view(np.int16)
-        return torch.from_numpy(np.ascontiguousarray(bits)).view(torch.bfloat16).cuda()
-    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
-
-
-def from_device(t, torch) -> np.ndarray:
-    return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
-
-
-def make_pruner(prob: synth.Problem, torch, max_k=0, probe_bias=None, **overrides):
-    w = prob.workload
-    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    probe = to_device(prob.probe, w.dtype, torch)
-    proj = None if prob.app_proj is None else to_device(prob.app_proj, w.dtype, torch)
-    bias = None if probe_bias is None else torch.from_numpy(np.ascontiguousarray(probe_bias, np.float32)).cuda()
-    return binding.Pruner(d=w.d, n_q_heads=w.hq, n_kv_heads=w.hkv, head_dim=w.dh, probe=probe,
-                          dtype=tdt, max_batch=w.batch, max_n=w.n, max_t=max(w.t, 1),
-                          max_k=max_k, app_projection=proj, probe_bias=bias, **overrides)
+from paper_2608_02134_amd.binding import from_device, make_pruner, to_device  # noqa: F401
 
 
 def run(prob: synth.Problem, torch, k=None, trace=True, nonvis=None, pruner=None, **overrides):
@@ -48,5 +27,9 @@ def run(prob: synth.Problem, torch, k=None, trace=True, nonvis=None, pruner=None
         if trace:
             for key, v in res[3].items():
                 d[key] = v[b].cpu().numpy()
+            # the call's in-pass certificate and the device status (checked)
+            code, dg = binding.gmc_get_diag(b)
+            assert code == binding.GMC_OK, f"gmc_get_diag({b}): {binding.gmc_last_error()}"
+            d["diag"] = dg if dg["has_certificate"] else None
         outs.append(d)
     return outs, pr

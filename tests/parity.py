@@ -33,6 +33,23 @@ REL_TIE = 1e-3       # candidate-margin tolerance (relative to the top score)
 KAPPA_TOL = 1e-3     # assignment tolerance (kappa is on the cosine scale)
 REL_L2 = {"f32": 1e-4, "bf16": 2e-2}
 CLIENT_TOL = 1e-4    # relative L2 of the pre-weighted client matrix per bank
+# Element bounds.  Client entries: fp32 logits and cosines from bf16 products
+# over d = 3584 carry absolute errors of a few 1e-6 (random-walk sum of
+# 2^-24-sized roundings), which exp(. / tau) with tau = 0.2 turns into relative
+# errors near 1e-5 of an entry; bounded by CLIENT_ELEM x the row's largest
+# entry.  Gains: sums of such entries over M rows, bounded by GAIN_ELEM x the
+# round's largest gain.  Output rows: the fp32 transport is exact to ~1e-6,
+# so each row is within ROW_REL_L2 of the oracle (one bf16 rounding,
+# 2^-9 / sqrt 3 RMS, under 4e-3) and every bf16 element within one ulp of the
+# correctly rounded oracle value, up to ELEM_ABS x the row's largest entry
+# for entries that a centroid's cancellation leaves small.
+CLIENT_ELEM = 1e-4
+GAIN_ELEM = 1e-4
+ROW_REL_L2 = {"f32": 1e-4, "bf16": 4e-3}
+ELEM_ABS = 1e-5
+# Certificate: U_t relative, the round's coverage gain relative to F(S)
+CERT_U_REL = 1e-4
+CERT_GAIN_ABS = 1e-5
 
 
 @dataclasses.dataclass
@@ -44,9 +61,16 @@ class FollowReport:
     min_pool_margin: float = np.inf
     min_batch_margin: float = np.inf
     client_rel_l2: Optional[dict] = None
+    client_elem_max: float = 0.0     # max |delta| / row max over the client matrix
+    gain_elem_max: float = 0.0       # max |delta| / round max over the per-round gains
     out_rel_l2: float = 0.0
+    row_rel_l2_max: float = 0.0
     bf16_ulp_frac: float = 1.0
+    cert_u_rel_max: float = 0.0
+    cert_gain_abs_max: float = 0.0   # relative to F(S)
+    cert_c_b: Optional[tuple] = None  # (gpu, oracle)
     identical_to_free_oracle: bool = True
+    rounds_log: Optional[list] = None
 
 
 def _valid_top(score: np.ndarray, cand: np.ndarray, chosen: np.ndarray, count: int, what: str):
@@ -78,19 +102,30 @@ def _valid_top(score: np.ndarray, cand: np.ndarray, chosen: np.ndarray, count: i
 
 
 def follow_selection(cbar: np.ndarray, k: int, b: int, pools, batches, p: O.GmcParams,
-                     rep: FollowReport):
-    """Walk the oracle along the GPU's per-round pools and batches."""
+                     rep: FollowReport, gains=None, scores=None):
+    """Walk the oracle along the GPU's per-round pools and batches.  With the
+    GPU's per-round gains and pool scores, compare them element by element.
+    Records the oracle's certificate terms of every followed round."""
     m, n = cbar.shape
     cov = np.zeros(m)
     chosen = np.zeros(n, dtype=bool)
     n_sel = 0
     rounds = -(-k // b)
+    rep.rounds_log = []
     for r in range(rounds):
         cand = np.flatnonzero(~chosen)
         u = O.marginal_gains(cbar, cov)
         psize = min(p.pool_mult * b, cand.size)
         gp = np.asarray([x for x in pools[r] if x >= 0], dtype=np.int64)
         srt = np.sort(u[cand])[::-1]
+        if gains is not None:
+            g = np.asarray(gains[r], np.float64)
+            top = float(u[cand].max()) if cand.size else 0.0
+            err = float(np.max(np.abs(g[cand] - u[cand]))) if cand.size else 0.0
+            rel = err / top if top > 0 else err
+            rep.gain_elem_max = max(rep.gain_elem_max, rel)
+            assert rel <= GAIN_ELEM, f"round {r} gains: max |delta| {err:.3e} vs top gain {top:.3e}"
+            assert np.all(g[chosen] == 0.0), f"round {r}: selected tokens must carry gain 0"
         rep.min_pool_margin = min(rep.min_pool_margin, O._cut_margin(srt, psize))
         rep.pool_near_ties += _valid_top(u, cand, gp, psize, f"round {r} pool")
         gp = np.sort(gp)
@@ -99,13 +134,50 @@ def follow_selection(cbar: np.ndarray, k: int, b: int, pools, batches, p: O.GmcP
         s_full[gp] = s
         bsize = min(b, k - n_sel)
         gb = np.asarray([x for x in batches[r] if x >= 0], dtype=np.int64)
-        rep.min_batch_margin = min(rep.min_batch_margin, O._cut_margin(np.sort(s)[::-1], bsize))
+        if scores is not None:
+            sg = np.asarray(scores[r], np.float64)[:gp.size]
+            top = float(s.max()) if s.size else 0.0
+            err = float(np.max(np.abs(sg - s))) if s.size else 0.0
+            assert err <= GAIN_ELEM * max(top, 1e-30), f"round {r} scores: max |delta| {err:.3e} vs top {top:.3e}"
+        bmargin = O._cut_margin(np.sort(s)[::-1], bsize)
+        rep.min_batch_margin = min(rep.min_batch_margin, bmargin)
         rep.batch_near_ties += _valid_top(s_full, gp, gb, bsize, f"round {r} batch")
+        new_cov = np.maximum(cov, cbar[:, gb].max(axis=1))
+        u_top = float(srt[:k].sum())
+        gain = float(new_cov.sum() - cov.sum())
+        rep.rounds_log.append(dict(u_top=u_top, gain=gain, q=gain / u_top if u_top > 0 else 0.0,
+                                   pool_margin=O._cut_margin(srt, psize), batch_margin=bmargin))
         chosen[gb] = True
         n_sel += bsize
-        cov = np.maximum(cov, cbar[:, gb].max(axis=1))
+        cov = new_cov
     rep.rounds = rounds
     return np.flatnonzero(chosen), cov
+
+
+def check_certificate(diag: dict, rep: FollowReport, f_s: float):
+    """The GPU's in-call certificate (gmc_get_diag) against the oracle's terms
+    of the followed rounds: U_t, the coverage gain, q_t, c_B and the margins."""
+    log = rep.rounds_log
+    assert diag["has_certificate"] == 1, "no certificate computed"
+    assert len(diag["q"]) == len(log)
+    for r, o in enumerate(log):
+        u_rel = abs(diag["u_top"][r] - o["u_top"]) / max(o["u_top"], 1e-30)
+        g_abs = abs(diag["gain"][r] - o["gain"]) / max(f_s, 1e-30)
+        rep.cert_u_rel_max = max(rep.cert_u_rel_max, u_rel)
+        rep.cert_gain_abs_max = max(rep.cert_gain_abs_max, g_abs)
+        assert u_rel <= CERT_U_REL, f"round {r}: U_t {diag['u_top'][r]} vs {o['u_top']}"
+        assert g_abs <= CERT_GAIN_ABS, f"round {r}: gain {diag['gain'][r]} vs {o['gain']}"
+        qtol = o["q"] * CERT_U_REL + CERT_GAIN_ABS * f_s / max(o["u_top"], 1e-30) + 1e-7
+        assert abs(diag["q"][r] - o["q"]) <= qtol, f"round {r}: q {diag['q'][r]} vs {o['q']}"
+        for key in ("pool_margin", "batch_margin"):
+            g, w = diag[key][r], o[key]
+            if np.isinf(w):
+                assert np.isinf(g), f"round {r} {key}: {g} vs inf"
+            else:
+                assert abs(g - w) <= 3 * GAIN_ELEM, f"round {r} {key}: {g} vs {w}"
+    c_b = 1.0 - float(np.prod([1.0 - o["q"] for o in log]))
+    rep.cert_c_b = (diag["c_b"], c_b)
+    assert abs(diag["c_b"] - c_b) <= 1e-4 * max(c_b, 1e-6) + 1e-6, f"c_B {diag['c_b']} vs {c_b}"
 
 
 def follow_assignment(x, pc, support, gpu_pi, p: O.GmcParams, rep: FollowReport):
@@ -160,6 +232,13 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
             got = np.asarray(gpu["client"], np.float64)[rows]
             rel[bank] = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
             assert rel[bank] < CLIENT_TOL, f"client bank {bank} rel L2 {rel[bank]:.3e}"
+            rmax = np.max(np.abs(ref), axis=1, keepdims=True)
+            act = rmax[:, 0] > 0
+            elem = np.abs(got - ref)[act] / rmax[act]
+            worst = float(elem.max()) if elem.size else 0.0
+            rep.client_elem_max = max(rep.client_elem_max, worst)
+            assert worst <= CLIENT_ELEM, f"client bank {bank}: an entry off by {worst:.3e} of its row max"
+            assert np.all(got[~act] == 0.0), f"client bank {bank}: an inactive row is not zero"
         rep.client_rel_l2 = rel
     if gpu.get("omega") is not None and q.shape[0] > 0:
         np.testing.assert_allclose(gpu["omega"], cl["omega"], atol=1e-4, err_msg="head weights")
@@ -167,7 +246,8 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
         eb = cl["ebar"]
         assert np.linalg.norm(gpu["ebar"] - eb) / np.linalg.norm(eb) < 1e-4, "normalised energy"
     b = p.batch_b_bounded if cl["bounded"] else p.batch_b
-    support, cov = follow_selection(cbar, kk, b, gpu["round_pool"], gpu["round_batch"], p, rep)
+    support, cov = follow_selection(cbar, kk, b, gpu["round_pool"], gpu["round_batch"], p, rep,
+                                    gpu.get("round_gains"), gpu.get("round_scores"))
     assert np.array_equal(np.asarray(gpu["out_idx"], np.int64), support), "out_idx != followed support"
     assert np.array_equal(gpu["out_pos"], pos[support]), "out_pos != pos3d[out_idx]"
     a = follow_assignment(cl["x"], cl["pc"], support, gpu["assign"], p, rep)
@@ -177,11 +257,22 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
     got = np.asarray(gpu["out_hidden"], np.float64)
     rep.out_rel_l2 = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
     assert rep.out_rel_l2 < REL_L2[dtype], f"out_hidden rel L2 {rep.out_rel_l2:.3e}"
+    # every carrier row on its own
+    row_rel = np.linalg.norm(got - ref, axis=1) / np.maximum(np.linalg.norm(ref, axis=1), 1e-30)
+    rep.row_rel_l2_max = float(row_rel.max())
+    assert rep.row_rel_l2_max < ROW_REL_L2[dtype], (
+        f"carrier row {int(np.argmax(row_rel))} rel L2 {rep.row_rel_l2_max:.3e}")
     if dtype == "bf16":
+        # every element within one bf16 ulp of the correctly rounded oracle value
         want = bf16_round(ref).astype(np.float64)
-        ulp = np.abs(want) * 2.0 ** -8
-        rep.bf16_ulp_frac = float(np.mean(np.abs(got - want) <= ulp + 1e-30))
-        assert rep.bf16_ulp_frac > 0.99, f"only {rep.bf16_ulp_frac:.4f} of bf16 outputs within 1 ulp"
+        mag = np.maximum(np.abs(want), 1e-38)
+        ulp = 2.0 ** (np.floor(np.log2(mag)) - 7)
+        slack = ELEM_ABS * np.max(np.abs(ref), axis=1, keepdims=True)
+        ok = np.abs(got - want) <= ulp + slack
+        rep.bf16_ulp_frac = float(np.mean(np.abs(got - want) <= ulp))
+        bad = np.argwhere(~ok)
+        assert bad.size == 0, (f"{bad.shape[0]} bf16 outputs beyond one ulp, first at {tuple(bad[0])}: "
+                               f"{got[tuple(bad[0])]} vs {want[tuple(bad[0])]}")
     if gpu.get("stats") is not None:
         st = gpu["stats"]
         assert st[8] == 0, f"device status word {st[8]} (grid barrier timeout)"
@@ -198,6 +289,8 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
             fvb = float(cbar[rows].max(axis=1).sum()) if rows.any() else 0.0
             assert abs(st[9 + bank] - fsb) <= 1e-4 * fs, f"F_{bank}(S) {st[9 + bank]} vs {fsb}"
             assert abs(st[12 + bank] - fvb) <= 1e-4 * fv, f"F_{bank}(V) {st[12 + bank]} vs {fvb}"
+    if gpu.get("diag") is not None:
+        check_certificate(gpu["diag"], rep, float(cov.sum()))
     free = O.select_support(cbar, kk, b, p)
     rep.identical_to_free_oracle = bool(np.array_equal(np.sort(free["order"]), support))
     if rep.pool_near_ties == 0 and rep.batch_near_ties == 0:

@@ -137,3 +137,118 @@ def test_header_is_plain_c(tmp_path):
     r = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only",
                         "-I", os.path.dirname(HEADER), str(src)], capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_new_header_constants_match_binding():
+    src = open(HEADER).read()
+    consts = dict((k, int(v)) for k, v in re.findall(r"#define\s+(GMC_[A-Z0-9_]+)\s+\(?(-?\d+)u?\)?", src))
+    assert (consts["GMC_ERR_DEVICE"], consts["GMC_ERR_NONFINITE"]) == (B.GMC_ERR_DEVICE, B.GMC_ERR_NONFINITE)
+    assert (consts["GMC_STATUS_SELECT_TIMEOUT"], consts["GMC_STATUS_BANK_TIMEOUT"],
+            consts["GMC_STATUS_NONFINITE"]) == (B.GMC_STATUS_SELECT_TIMEOUT, B.GMC_STATUS_BANK_TIMEOUT,
+                                                B.GMC_STATUS_NONFINITE)
+    assert (consts["GMC_DIAG_CERT"], consts["GMC_DIAG_FINITE"]) == (B.GMC_DIAG_CERT, B.GMC_DIAG_FINITE)
+    assert consts["GMC_CERT_MAX_ROUNDS"] == B.GMC_CERT_MAX_ROUNDS
+
+
+def test_struct_layouts_match_the_c_compiler(tmp_path):
+    # sizes and field offsets of every struct the binding mirrors, as the C
+    # compiler lays them out
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"gmc_config": B.GmcConfig, "gmc_trace": B.GmcTrace, "gmc_diag": B.GmcDiag}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "gmc.h"', 'int main(void) {']
+    for cname, py in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ['  return 0;', '}']
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    r = subprocess.run([cc, "-std=c99", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {}
+    for ln in out:
+        if ln:
+            a, b, c = ln.split()
+            got[(a, b)] = int(c)
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert got[(cname, fname)] == getattr(py, fname).offset, (cname, fname)
+
+
+def test_diag_entry_points_without_context(lib):
+    B.gmc_free()
+    assert B.gmc_set_diag(B.GMC_DIAG_CERT) == B.GMC_ERR_STATE
+    code, _ = B.gmc_get_diag(0)
+    assert code == B.GMC_ERR_STATE
+
+
+def _cpu_cfg():
+    c = B.gmc_config_default()
+    c.d, c.n_q_heads, c.n_kv_heads, c.head_dim = 64, 4, 2, 32
+    return c
+
+
+def test_wrapper_rejects_mismatched_inputs():
+    torch = pytest.importorskip("torch")
+    cfg = _cpu_cfg()
+    f32 = torch.float32
+    h = torch.zeros((2, 10, 64))
+    q = torch.zeros((2, 3, 4, 32))
+    k = torch.zeros((2, 10, 2, 32))
+    pos = torch.zeros((2, 10, 3), dtype=torch.int32)
+    bad = [
+        (torch.zeros((2, 10, 32)), q, k, pos, None, "hidden"),
+        (h, torch.zeros((2, 3, 4, 16)), k, pos, None, "text_q"),
+        (h, torch.zeros((1, 3, 4, 32)), k, pos, None, "text_q"),
+        (h, q, torch.zeros((2, 10, 4, 32)), pos, None, "vis_k"),
+        (h, q, torch.zeros((2, 9, 2, 32)), pos, None, "vis_k"),
+        (h, q, k, pos.to(torch.int64), None, "pos3d"),
+        (h, q, k, torch.zeros((2, 10, 2), dtype=torch.int32), None, "pos3d"),
+        (h.to(torch.bfloat16), q, k, pos, None, "dtype"),
+        (h, q, k, pos, torch.zeros((2, 4, 2)), "nonvis_lse"),
+        (h, q, k, pos, torch.zeros((2, 4, 3), dtype=torch.float64), "nonvis_lse"),
+        (h.transpose(0, 1).contiguous().transpose(0, 1), q, k, pos, None, "contiguous"),
+        (h, q, k, pos, None, "GPU"),          # valid shapes, but host tensors
+    ]
+    for hh, qq, kk, pp, nv, what in bad:
+        with pytest.raises(ValueError) as ei:
+            B.check_prune_inputs(cfg, f32, hh, qq, kk, pp, nv)
+        assert what in str(ei.value), (what, str(ei.value))
+
+
+def test_gather_and_compact_wrappers_reject_mismatched_inputs():
+    torch = pytest.importorskip("torch")
+    c = torch.zeros((4, 10, 8), dtype=torch.bfloat16)
+    keep = torch.zeros((4, 6), dtype=torch.int32)
+    with pytest.raises(ValueError, match="leading shape"):
+        B.check_gather_inputs([c, torch.zeros((4, 9, 8), dtype=torch.bfloat16)], keep, 1)
+    with pytest.raises(ValueError, match="bytes"):
+        B.check_gather_inputs([c, torch.zeros((4, 10, 8), dtype=torch.float32)], keep, 1)
+    with pytest.raises(ValueError, match="int32"):
+        B.check_gather_inputs([c], keep.to(torch.int64), 1)
+    with pytest.raises(ValueError, match="sequences"):
+        B.check_gather_inputs([c], keep, 2)
+    with pytest.raises(ValueError, match="GPU"):
+        B.check_gather_inputs([c], keep, 1)
+    idx = torch.zeros((2, 3), dtype=torch.int32)
+    rows = torch.zeros((2, 12, 8))
+    vis = torch.zeros((2, 3, 8))
+    pos = torch.zeros((2, 12, 3), dtype=torch.int32)
+    with pytest.raises(ValueError, match="int32"):
+        B.check_compact_inputs(idx.to(torch.int64), 5, rows, vis, pos, 12)
+    with pytest.raises(ValueError, match="K <= N"):
+        B.check_compact_inputs(idx, 2, rows, vis, pos, 12)
+    with pytest.raises(ValueError, match="dtype and row size"):
+        B.check_compact_inputs(idx, 5, rows, vis.to(torch.bfloat16), pos, 12)
+    with pytest.raises(ValueError, match="seq_pos"):
+        B.check_compact_inputs(idx, 5, rows, vis, pos[:, :11], 12)
+    with pytest.raises(ValueError, match="GPU"):
+        B.check_compact_inputs(idx, 5, rows, vis, pos, 12)

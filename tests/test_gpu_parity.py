@@ -11,7 +11,7 @@ from oracle import gmc_oracle as O
 from paper_2608_02134_amd import synth
 
 from .parity import check_problem
-from .gpu_run import run
+from .gpu_run import from_device, run
 
 pytestmark = pytest.mark.gpu
 
@@ -189,3 +189,111 @@ def test_capacity_and_argument_errors():
         run(big, torch, pruner=pr, trace=False)
     assert ei.value.code == binding.GMC_ERR_CAPACITY
     pr.close()
+
+
+@pytest.mark.parametrize("tau_j,pop,label", [(0.0, 0.5, "hard deletion"), (1.0, 0.0, "uniform merge")])
+def test_recovery_variants(tau_j, pop, label):
+    # Table cond-selector-recovery: hard deletion (carriers keep their own
+    # states, tau_j = 0) and uniform centroid merging (population strength 0,
+    # m_i = 1) on the same support path as grounded transport
+    prob = synth.make_problem("qwen", grid=(1, 20, 21), t=24, k=83)
+    _announce(f"recovery: {label}", prob)
+    outs, pr = run(prob, torch, tau_j=tau_j, pop_strength=pop)
+    pr.close()
+    reps = _check_all(prob, outs, params=O.GmcParams(tau_j=tau_j, pop_strength=pop))
+    if tau_j == 0.0:
+        # a carrier keeps its own state up to the restoration's epsilon
+        h = prob.hidden[0][outs[0]["out_idx"]]
+        np.testing.assert_allclose(outs[0]["out_hidden"], h, rtol=2.0 ** -7, atol=1e-6)
+    assert reps[0].rounds > 0
+
+
+def _sleep_cycles_per_second():
+    # calibrate the spin kernel's counter against events on the device
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    torch.cuda._sleep(50_000_000)
+    b.record()
+    torch.cuda.synchronize()
+    return 50_000_000 / (a.elapsed_time(b) / 1e3)
+
+
+def test_call_behind_a_queued_backlog():
+    """One-image call queued behind ~1 s of other work on the caller's stream:
+    the bank stream's gate waits for the call's own row norms, so the outputs
+    equal the unqueued call's bit for bit and the device status stays clear."""
+    from paper_2608_02134_amd import binding
+    from paper_2608_02134_amd.binding import to_device
+    prob = synth.make_problem("qwen", grid=(1, 24, 24), t=16, k=96)
+    _announce("backlog", prob)
+    ref, pr = run(prob, torch)
+    w = prob.workload
+    hid = to_device(prob.hidden, w.dtype, torch)
+    q = to_device(prob.text_q, w.dtype, torch)
+    kk = to_device(prob.vis_k, w.dtype, torch)
+    pos = torch.from_numpy(prob.pos3d).cuda()
+    try:
+        cps = _sleep_cycles_per_second()
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(cps * 1.0))
+        res = pr.prune(hid, q, kk, pos, prob.k)
+        torch.cuda.synchronize()
+        code, dg = binding.gmc_get_diag(0)
+        assert code == binding.GMC_OK and dg["status"] == 0, binding.gmc_last_error()
+        assert np.array_equal(res[2][0].cpu().numpy(), ref[0]["out_idx"])
+        assert np.array_equal(from_device(res[0][0], torch), ref[0]["out_hidden"])
+    finally:
+        pr.close()
+
+
+def test_calls_on_two_streams_are_ordered():
+    """A call on a second stream, queued while the first stream's call waits
+    behind other work, runs after it: both give the reference outputs."""
+    from paper_2608_02134_amd import binding
+    from paper_2608_02134_amd.binding import to_device
+    prob = synth.make_problem("qwen", grid=(1, 24, 24), t=16, k=96)
+    _announce("two streams", prob)
+    ref, pr = run(prob, torch)
+    w = prob.workload
+    hid = to_device(prob.hidden, w.dtype, torch)
+    q = to_device(prob.text_q, w.dtype, torch)
+    kk = to_device(prob.vis_k, w.dtype, torch)
+    pos = torch.from_numpy(prob.pos3d).cuda()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    try:
+        cps = _sleep_cycles_per_second()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s1):
+            torch.cuda._sleep(int(cps * 0.2))
+            r1 = pr.prune(hid, q, kk, pos, prob.k)
+        with torch.cuda.stream(s2):
+            r2 = pr.prune(hid, q, kk, pos, prob.k)
+        torch.cuda.synchronize()
+        code, dg = binding.gmc_get_diag(0)
+        assert code == binding.GMC_OK and dg["status"] == 0, binding.gmc_last_error()
+        for r in (r1, r2):
+            assert np.array_equal(r[2][0].cpu().numpy(), ref[0]["out_idx"])
+            assert np.array_equal(from_device(r[0][0], torch), ref[0]["out_hidden"])
+    finally:
+        pr.close()
+
+
+def test_debug_scan_and_certificate_flags():
+    """With the non-finite scan and the certificate switched on by flag (no
+    trace buffers), a clean call reports status 0 and a certificate whose
+    c_B matches the followed oracle's."""
+    from paper_2608_02134_amd import binding
+    prob = synth.make_problem("qwen", grid=(1, 20, 21), t=24, k=83)
+    _announce("diag flags", prob)
+    outs, pr = run(prob, torch)
+    try:
+        pr.set_diag(binding.GMC_DIAG_CERT | binding.GMC_DIAG_FINITE)
+        outs2, _ = run(prob, torch, pruner=pr, trace=False)
+        code, dg = binding.gmc_get_diag(0)
+        assert code == binding.GMC_OK and dg["status"] == 0, binding.gmc_last_error()
+        assert dg["has_certificate"] == 1
+        assert np.array_equal(outs2[0]["out_hidden"], outs[0]["out_hidden"])
+        assert dg["q"] == outs[0]["diag"]["q"] and dg["c_b"] == outs[0]["diag"]["c_b"]
+    finally:
+        pr.close()
