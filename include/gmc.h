@@ -345,6 +345,33 @@ int gmc_compact_sequence(int64_t B, int64_t L, int64_t vis_start, int64_t N, int
 int gmc_gather_rows(int64_t n_tensors, const void* const* src, void* const* dst, int64_t n_seq,
                     int64_t seqs_per_keep, int64_t L, int64_t L2, int64_t row_bytes, const int32_t* keep);
 
+/*
+ * gmc_prune_static - gmc_prune_ex without a context and without any device
+ * allocation, for callers that cannot allocate device memory at call time:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  The workspace is carved, for this call's own shape, out of a
+ * file-scope device array of GMC_STATIC_SCRATCH_BYTES per device (present
+ * for the process's lifetime on every device the library runs on; its
+ * address is looked up on the first call on a device).  Enough for one
+ * problem at the Qwen2.5-VL-7B shape (N = 1296, T = 64, d = 3584, 28 / 4
+ * heads, K = 256: about 23 MB).
+ *   cfg      shape, settings and the value_probe / app_projection /
+ *            value_probe_bias pointers as for gmc_init; its capacity fields are
+ *            ignored (the call's B, N, T, K are the capacity)
+ *   B, ..., nonvis_lse   as gmc_prune_ex (no trace)
+ *   stream   hipStream_t for all work (NULL: the null stream); one stream,
+ *            no side stream
+ * Every call on a device shares that device's array and clears the region it
+ * uses first: calls that overlap on one device race and give wrong results.
+ * No diagnostics (gmc_get_diag reports on context calls only).  Errors:
+ * GMC_ERR_ARG, GMC_ERR_CAPACITY (the call's workspace exceeds the array;
+ * nothing is enqueued), GMC_ERR_HIP.
+ */
+#define GMC_STATIC_SCRATCH_BYTES (64ull << 20)
+int gmc_prune_static(const gmc_config* cfg, int64_t B, const void* hidden, const void* text_q, const void* vis_k,
+                     const int32_t* pos3d, int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos,
+                     int32_t* out_idx, const float* nonvis_lse, void* stream);
+
 /* Bytes of device workspace the current context holds (0 without one). */
 int64_t gmc_workspace_bytes(void);
 

@@ -20,6 +20,7 @@ GMC_ERR_DEVICE, GMC_ERR_NONFINITE = -5, -6
 GMC_STATUS_SELECT_TIMEOUT, GMC_STATUS_BANK_TIMEOUT, GMC_STATUS_NONFINITE = 1, 2, 4
 GMC_DIAG_CERT, GMC_DIAG_FINITE = 1, 2
 GMC_CERT_MAX_ROUNDS = 64
+GMC_STATIC_SCRATCH_BYTES = 64 << 20
 GMC_F32, GMC_BF16 = 0, 1
 GMC_STATS = 15
 GMC_MAX_GATHER_TENSORS = 64
@@ -90,6 +91,8 @@ SIGNATURES = {
                                        _i64, _vp]),
     "gmc_set_diag": (ctypes.c_int, [_i32]),
     "gmc_get_diag": (ctypes.c_int, [_i64, ctypes.POINTER(GmcDiag)]),
+    "gmc_prune_static": (ctypes.c_int, [ctypes.POINTER(GmcConfig), _i64, _vp, _vp, _vp, _vp, _i64, _i64, _i64,
+                                        _vp, _vp, _vp, _vp, _vp]),
     "gmc_workspace_bytes": (_i64, []),
     "gmc_last_error": (ctypes.c_char_p, []),
     "gmc_free": (None, []),
@@ -340,6 +343,12 @@ def gmc_get_diag(problem: int = 0, max_rounds: int = GMC_CERT_MAX_ROUNDS):
     for k, a in arrs.items():
         out[k] = [a[i] for i in range(nr)]
     return code, out
+
+
+def gmc_prune_static(cfg: GmcConfig, b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden, out_pos, out_idx,
+                     nonvis_lse=None, stream=None) -> int:
+    return lib().gmc_prune_static(ctypes.byref(cfg), b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden,
+                                  out_pos, out_idx, nonvis_lse, stream)
 
 
 def gmc_workspace_bytes() -> int:
