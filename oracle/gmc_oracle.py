@@ -53,7 +53,8 @@ __all__ = [
     "assignment_gaps", "separability_gate", "ambiguity_gate",
     "assign_population", "population_weights", "transport", "compact",
     "gmc_single", "gmc", "prune_rounds", "index_map", "compact_sequence",
-    "gather_cache",
+    "gather_cache", "head_pattern", "head_weights_from_pattern", "view_mass",
+    "message_view",
 ]
 
 
@@ -91,6 +92,7 @@ class GmcParams:
     app_rank: int = 128
     app_max_clients: int = 4096
     batch_b_bounded: int = 512
+    hist_mass: float = 0.5         # reading R14
 
 
 READINGS = {
@@ -116,6 +118,11 @@ READINGS = {
     "R12": "farthest-first picks min(4, active heads) centres; ties to the "
            "earliest centre; empty clusters are dropped",
     "R13": "ties in every ranking go to the lower source index",
+    "R14": "historical views: the message mass beta_msg splits into the current "
+           "view's (1 - hist_mass) beta_msg and hist_mass beta_msg shared equally "
+           "by the historical views (0.5 / 0.5 with two views: 0.5, 0.25, 0.25); "
+           "each view has its own states, queries, keys and folded value probe; "
+           "with no historical view the current view carries beta_msg",
 }
 
 
@@ -211,16 +218,39 @@ def head_pattern_gram(a: np.ndarray, z: np.ndarray, sigma: np.ndarray) -> np.nda
     return np.sum(aa * ww, axis=2)
 
 
+def head_pattern(grams, mean_atom_norms, view_mass) -> np.ndarray:
+    """Gram of the pre-normalisation head patterns concat_v[sqrt(beta_v)
+    vec(U_h^v)] with U_h^v the view's atoms scaled to unit average atom norm
+    (Eq. cond-head-pattern): sum_v beta_v Gamma^v_hg / (abar^v_h abar^v_g); a
+    view in which a head has no energy (abar = 0) adds nothing for it."""
+    hq = grams[0].shape[0]
+    out = np.zeros((hq, hq))
+    for gram, abar, beta in zip(grams, mean_atom_norms, view_mass):
+        inv = np.where(abar > 0, 1.0 / np.where(abar > 0, abar, 1.0), 0.0)
+        out += beta * gram * inv[:, None] * inv[None, :]
+    return out
+
+
 def head_weights(gram: np.ndarray, mean_atom_norm: np.ndarray, p: GmcParams):
     """Farthest-first cosine head clustering and inverse-dispersion weights
-    (Eq. cond-head-pattern, Eq. cond-head-weight; reading R12).
+    (Eq. cond-head-pattern, Eq. cond-head-weight; reading R12) for one
+    message view of mass beta_msg.
 
     gram: Gamma [Hq][Hq]; mean_atom_norm: average atom norm per head, which
     sets the pre-normalisation pattern norm sqrt(beta Gamma_hh)/abar_h.
     Returns (omega [Hq], centres list, cluster id per head (-1 inactive)).
     """
-    hq = gram.shape[0]
-    diag = np.diag(gram).copy()
+    return head_weights_from_pattern(head_pattern([gram], [mean_atom_norm], [p.beta_msg]), p)
+
+
+def head_weights_from_pattern(pattern: np.ndarray, p: GmcParams):
+    """Farthest-first clustering on the Gram of the pre-normalisation head
+    patterns (head_pattern): the first centre has the largest pattern norm,
+    each next one the smallest maximum cosine to the centres chosen; heads
+    join their nearest centre (ties to the earlier one); omega by Eq.
+    cond-head-weight over the non-empty clusters."""
+    hq = pattern.shape[0]
+    diag = np.diag(pattern).copy()
     active = diag > 0
     omega = np.zeros(hq)
     assign = -np.ones(hq, dtype=np.int64)
@@ -228,10 +258,8 @@ def head_weights(gram: np.ndarray, mean_atom_norm: np.ndarray, p: GmcParams):
     if n_active == 0:
         return omega, [], assign
     nrm = np.sqrt(np.where(active, diag, 1.0))
-    cos = gram / nrm[:, None] / nrm[None, :]
-    with np.errstate(divide="ignore", invalid="ignore"):
-        pre = np.where(active, np.sqrt(p.beta_msg * np.where(active, diag, 0.0))
-                       / np.where(mean_atom_norm > 0, mean_atom_norm, 1.0), -np.inf)
+    cos = pattern / nrm[:, None] / nrm[None, :]
+    pre = np.where(active, np.sqrt(np.where(active, diag, 0.0)), -np.inf)
     centres = [int(np.argmax(pre))]
     n_c = min(p.max_head_clusters, n_active)
     while len(centres) < n_c:
@@ -324,10 +352,12 @@ def spatial_bank(pos: np.ndarray, p: GmcParams) -> np.ndarray:
 # Client matrix (Eq. cond-coverage) and coverage objective (Eq. coverage)
 # ----------------------------------------------------------------------------
 def client_matrix(pg: np.ndarray, active: np.ndarray, omega: np.ndarray, nu: np.ndarray,
-                  pv: np.ndarray, ps: np.ndarray, p: GmcParams):
+                  pv: np.ndarray, ps: np.ndarray, p: GmcParams, hist_pg=(), hist_active=(), view_mass=None):
     """Stack the three banks into Cbar [M][N] with preweights.
 
-    Grounded row (h,t): beta_msg omega_h nu_t a_(h,t) P^G (reading R2);
+    Grounded row (h,t) of message view v: beta_v omega_h nu_t a_(h,t) P^G
+    (reading R2; beta_v = beta_msg with one view, reading R14 with historical
+    views, whose rows follow the current view's, view by view);
     appearance row: beta_app / M_V P^V; spatial row: beta_spa / M_S P^S.
     Returns Cbar and the bank id of every row (0 grounded, 1 appearance,
     2 spatial).
@@ -335,9 +365,12 @@ def client_matrix(pg: np.ndarray, active: np.ndarray, omega: np.ndarray, nu: np.
     hq, t, n = pg.shape
     rows, banks = [], []
     if t > 0:
-        wg = p.beta_msg * omega[:, None] * nu[None, :] * active
-        rows.append((wg[:, :, None] * pg).reshape(hq * t, n))
-        banks.append(np.zeros(hq * t, dtype=np.int64))
+        views = [(pg, active)] + list(zip(hist_pg, hist_active))
+        mass = [p.beta_msg] if view_mass is None else view_mass
+        for (pgv, actv), beta in zip(views, mass):
+            wg = beta * omega[:, None] * nu[None, :] * actv
+            rows.append((wg[:, :, None] * pgv).reshape(hq * t, n))
+            banks.append(np.zeros(hq * t, dtype=np.int64))
     rows.append(p.beta_app / pv.shape[0] * pv)
     banks.append(np.ones(pv.shape[0], dtype=np.int64))
     rows.append(p.beta_spa / ps.shape[0] * ps)
@@ -566,34 +599,63 @@ def gather_cache(cache, keep):
 # ----------------------------------------------------------------------------
 # The whole operator for one image (Algorithm 1, steps 2-6)
 # ----------------------------------------------------------------------------
-def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=None, probe_bias=None):
+def view_mass(n_hist: int, p: GmcParams):
+    """Masses of the current and the historical message views (reading R14)."""
+    if n_hist == 0:
+        return [p.beta_msg]
+    return [p.beta_msg * (1.0 - p.hist_mass)] + [p.beta_msg * p.hist_mass / n_hist] * n_hist
+
+
+def message_view(h, q, k, probe, p: GmcParams, nonvis_lse=None, probe_bias=None):
+    """One message view (Eq. cond-native-message, Eq. cond-mass-coordinate,
+    Eq. cond-grounded-client): value coordinates Z from the view's own states
+    and folded probe, the mass coordinate, the native attention slice, atom
+    norms, row sums, P^G rows, the view's head-pattern Gram and mean atom
+    norms."""
+    h = np.asarray(h, np.float64)
+    n = h.shape[0]
+    t = q.shape[0]
+    hq = probe.shape[0]
+    _, _, _, xt = row_features(h, p)
+    z = value_probe(xt, probe, probe_bias)
+    sigma = mass_coordinate(z, p)
+    if t == 0:
+        return dict(z=z, sigma=sigma, a=np.zeros((hq, 0, n)), e=np.zeros((hq, 0, n)), ell=None,
+                    pg=np.zeros((hq, 0, n)), active=np.zeros((hq, 0), dtype=bool), gram=np.zeros((hq, hq)),
+                    abar=np.zeros(hq))
+    a = native_attention(q, k, nonvis_lse)
+    e, ell = grounded_energy_rows(a, z, sigma)
+    zrow = e.sum(axis=2)                                     # [Hq][T]
+    active = zrow > 0
+    pg = np.where(active[:, :, None], e / np.where(active, zrow, 1.0)[:, :, None], 0.0)
+    return dict(z=z, sigma=sigma, a=a, e=e, ell=ell, pg=pg, active=active,
+                gram=head_pattern_gram(a, z, sigma), abar=e.reshape(hq, -1).mean(axis=1))
+
+
+def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=None, probe_bias=None,
+                  hist=()):
     """Steps 2 of Algorithm 1: the three client banks and all message-side
-    quantities.  Returns a dict of intermediates."""
+    quantities.  `hist` lists completed historical message views, each a dict
+    of its own hidden, q, k, probe and optionally nonvis_lse, probe_bias
+    (App. H native message clients).  Returns a dict of intermediates."""
     h = np.asarray(h, np.float64)
     n = h.shape[0]
     t = q.shape[0]
     norm, x, rms, xt = row_features(h, p)
-    z = value_probe(xt, probe, probe_bias)
-    sigma = mass_coordinate(z, p)
     hq = probe.shape[0]
     nu = query_weights(t, p)
+    cur = message_view(h, q, k, probe, p, nonvis_lse, probe_bias)
+    views = [message_view(v["hidden"], v["q"], v["k"], v["probe"], p, v.get("nonvis_lse"), v.get("probe_bias"))
+             for v in hist] if t > 0 else []
+    mass = view_mass(len(views), p)
     if t > 0:
-        a = native_attention(q, k, nonvis_lse)
-        e, ell = grounded_energy_rows(a, z, sigma)
-        zrow = e.sum(axis=2)                                     # [Hq][T]
-        active = zrow > 0
-        pg = np.where(active[:, :, None], e / np.where(active, zrow, 1.0)[:, :, None], 0.0)
-        gram = head_pattern_gram(a, z, sigma)
-        abar = e.reshape(hq, -1).mean(axis=1)
-        omega, centres, clus = head_weights(gram, abar, p)
-        ebar, en = grounded_energy(e, omega, nu)
+        pattern = head_pattern([cur["gram"]] + [v["gram"] for v in views],
+                               [cur["abar"]] + [v["abar"] for v in views], mass)
+        omega, centres, clus = head_weights_from_pattern(pattern, p)
+        # population weights use the current view's energy only
+        ebar, en = grounded_energy(cur["e"], omega, nu)
     else:
-        a = np.zeros((hq, 0, n))
-        e = np.zeros((hq, 0, n))
-        ell = None
-        pg = np.zeros((hq, 0, n))
-        active = np.zeros((hq, 0), dtype=bool)
-        gram = np.zeros((hq, hq))
+        pattern = np.zeros((hq, hq))
         omega, centres, clus = np.zeros(hq), [], -np.ones(hq, dtype=np.int64)
         ebar, en = np.ones(n), np.zeros(n)
     bounded = n > p.bounded_threshold_n
@@ -604,9 +666,11 @@ def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=N
     else:
         pv, app_clients = appearance_bank(x, p), np.arange(n)
     ps = spatial_bank(pos, p)
-    cbar, banks = client_matrix(pg, active, omega, nu, pv, ps, p)
-    return dict(norm=norm, x=x, rms=rms, xt=xt, z=z, sigma=sigma, a=a, e=e, ell=ell,
-                pg=pg, active=active, gram=gram, omega=omega, centres=centres,
+    cbar, banks = client_matrix(cur["pg"], cur["active"], omega, nu, pv, ps, p,
+                                [v["pg"] for v in views], [v["active"] for v in views], mass)
+    return dict(norm=norm, x=x, rms=rms, xt=xt, z=cur["z"], sigma=cur["sigma"], a=cur["a"], e=cur["e"],
+                ell=cur["ell"], pg=cur["pg"], active=cur["active"], gram=cur["gram"], abar=cur["abar"],
+                pattern=pattern, view_mass=mass, hist_views=views, omega=omega, centres=centres,
                 clusters=clus, nu=nu, ebar=ebar, energy=en, pv=pv, ps=ps,
                 app_clients=app_clients, cbar=cbar, banks=banks, bounded=bounded,
                 pc=spatial_coordinates(pos))
@@ -632,7 +696,7 @@ def bank_saturation(cbar: np.ndarray, banks: np.ndarray, support) -> dict:
 
 
 def gmc_single(h, q, k, pos, probe, k_req: int, p: GmcParams = GmcParams(),
-               app_proj=None, nonvis_lse=None, keep_intermediates: bool = False, probe_bias=None):
+               app_proj=None, nonvis_lse=None, keep_intermediates: bool = False, probe_bias=None, hist=()):
     """One problem end to end: budget, clients, selection, assignment,
     transport and compaction.  Returns out_hidden (fp64, before the cast to
     the residual dtype), out_pos, out_idx and diagnostics."""
@@ -642,7 +706,7 @@ def gmc_single(h, q, k, pos, probe, k_req: int, p: GmcParams = GmcParams(),
     if kk == n:
         return dict(out_hidden=h.copy(), out_pos=np.asarray(pos).copy(),
                     out_idx=np.arange(n, dtype=np.int64), identity=True, k=kk)
-    cl = build_clients(h, q, k, pos, probe, p, app_proj, nonvis_lse, probe_bias)
+    cl = build_clients(h, q, k, pos, probe, p, app_proj, nonvis_lse, probe_bias, hist)
     b = p.batch_b_bounded if cl["bounded"] else p.batch_b
     sel = select_support(cl["cbar"], kk, b, p)
     asg = assign_population(cl["x"], cl["pc"], sel["order"], p)
