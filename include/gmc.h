@@ -130,6 +130,18 @@ typedef struct gmc_config {
                                     models whose V projection has a bias; then
                                     Z_h[i] = x~_i G_h + b_h (Eq. cond-mass-
                                     coordinate with V = x~ W^V + b^V)        */
+  /* completed historical message views (App. H "Native message clients";
+     Table cond-config: current/history mass 0.5/0.5, two views); used by
+     gmc_prune_views                                                       */
+  int32_t max_hist_views;       /* 0..GMC_MAX_HIST_VIEWS (default 0)        */
+  float hist_mass;              /* share of beta_msg the historical views
+                                   carry together, split equally (0.5); the
+                                   current view carries the rest           */
+  const void* value_probe_hist; /* [max_hist_views][Hq][r][d] dtype: each
+                                   view's folded probe (W^V O_h P of that
+                                   view's block); required iff
+                                   max_hist_views > 0 (caller-owned, kept)  */
+  const float* value_probe_bias_hist; /* [max_hist_views][Hq][r] fp32 or NULL */
 } gmc_config;
 
 /*
@@ -262,6 +274,37 @@ typedef struct gmc_diag {
  * call, GMC_ERR_ARG for a bad problem index or NULL out, GMC_ERR_HIP.
  */
 int gmc_get_diag(int64_t problem, gmc_diag* out);
+
+/*
+ * gmc_prune_views - gmc_prune_ex with n_hist completed historical message
+ * views (App. H "Native message clients"; Eq. cond-head-pattern; Table
+ * cond-config).  Each view is a separate collection of grounded client rows
+ * built exactly like the current view's, from the view's own states, queries,
+ * keys and folded value probe (config.value_probe_hist[v]); its rows carry
+ * mass hist_mass * beta_msg / n_hist and the current view's
+ * (1 - hist_mass) * beta_msg.  Head weights come from the head patterns
+ * concatenated over the views (each view's atoms scaled to unit average norm
+ * and by sqrt of its mass); the population energy from the current view.
+ *   hist[v].hidden     [B][N][d]        dtype  states entering the view's block
+ *   hist[v].text_q     [B][T][Hq][dh]   dtype  the view's text queries (same T)
+ *   hist[v].vis_k      [B][N][Hkv][dh]  dtype  the view's visual keys
+ *   hist[v].nonvis_lse [B][Hq][T] fp32 or NULL
+ * 0 <= n_hist <= config.max_hist_views; n_hist = 0 is gmc_prune_ex.  With
+ * T = 0 there are no grounded rows and the views are not read.  The trace's
+ * client matrix then holds the current view's grounded rows, then each
+ * historical view's, then the appearance and spatial rows.  Errors: as
+ * gmc_prune_ex, GMC_ERR_CAPACITY for n_hist above the capacity.
+ */
+#define GMC_MAX_HIST_VIEWS 3
+typedef struct gmc_view {
+  const void* hidden;
+  const void* text_q;
+  const void* vis_k;
+  const float* nonvis_lse;
+} gmc_view;
+int gmc_prune_views(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+                    int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
+                    const float* nonvis_lse, int64_t n_hist, const gmc_view* hist, const gmc_trace* trace);
 
 /* Realised budget K = min{N, max{K_r, 1}} (Sec. 3.1); 0 if N < 1. Host-only. */
 int64_t gmc_realized_k(int64_t N, int64_t K_req);

@@ -23,6 +23,7 @@ GMC_CERT_MAX_ROUNDS = 64
 GMC_STATIC_SCRATCH_BYTES = 64 << 20
 GMC_F32, GMC_BF16 = 0, 1
 GMC_STATS = 15
+GMC_MAX_HIST_VIEWS = 3
 GMC_MAX_GATHER_TENSORS = 64
 
 _i32, _f32, _i64, _vp = ctypes.c_int32, ctypes.c_float, ctypes.c_int64, ctypes.c_void_p
@@ -52,6 +53,8 @@ class GmcConfig(ctypes.Structure):
         ("app_rank", _i32), ("app_max_clients", _i32),
         ("batch_b_bounded", _i32),
         ("value_probe_bias", _vp),
+        ("max_hist_views", _i32), ("hist_mass", _f32),
+        ("value_probe_hist", _vp), ("value_probe_bias_hist", _vp),
     ]
 
 
@@ -60,6 +63,11 @@ class GmcTrace(ctypes.Structure):
     _fields_ = [("round_pool", _vp), ("round_batch", _vp), ("assign", _vp), ("omega", _vp),
                 ("ebar", _vp), ("client", _vp), ("stats", _vp), ("round_gains", _vp),
                 ("round_scores", _vp)]
+
+
+class GmcView(ctypes.Structure):
+    """Mirror of ``gmc_view``: one historical message view's device tensors."""
+    _fields_ = [("hidden", _vp), ("text_q", _vp), ("vis_k", _vp), ("nonvis_lse", _vp)]
 
 
 class GmcDiag(ctypes.Structure):
@@ -82,6 +90,8 @@ SIGNATURES = {
     "gmc_prune": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
     "gmc_prune_ex": (ctypes.c_int, [_i64, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _vp,
                                     ctypes.POINTER(GmcTrace)]),
+    "gmc_prune_views": (ctypes.c_int, [_i64, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _i64,
+                                       ctypes.POINTER(GmcView), ctypes.POINTER(GmcTrace)]),
     "gmc_realized_k": (_i64, [_i64, _i64]),
     "gmc_trace_dims": (ctypes.c_int, [_i64, _i64, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
                                       ctypes.POINTER(_i64), ctypes.POINTER(_i64)]),
@@ -153,6 +163,16 @@ def gmc_prune_ex(b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden, out_pos, 
     tr = ctypes.byref(trace) if trace is not None else None
     return lib().gmc_prune_ex(b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden, out_pos,
                               out_idx, nonvis_lse, tr)
+
+
+def gmc_prune_views(b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden, out_pos, out_idx, nonvis_lse,
+                    hist_views, trace: Optional[GmcTrace] = None) -> int:
+    """hist_views: a sequence of GmcView."""
+    nh = len(hist_views)
+    arr = (GmcView * max(nh, 1))(*hist_views)
+    tr = ctypes.byref(trace) if trace is not None else None
+    return lib().gmc_prune_views(b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden, out_pos, out_idx,
+                                 nonvis_lse, nh, arr, tr)
 
 
 def gmc_realized_k(n: int, k_req: int) -> int:
@@ -375,7 +395,7 @@ class Pruner:
     """
 
     def __init__(self, *, d, n_q_heads, n_kv_heads, head_dim, probe, dtype, max_batch, max_n,
-                 max_t, max_k=0, app_projection=None, probe_bias=None, **overrides):
+                 max_t, max_k=0, app_projection=None, probe_bias=None, probe_hist=None, **overrides):
         import torch
         self.torch = torch
         cfg = gmc_config_default()
@@ -394,6 +414,14 @@ class Pruner:
                                             tuple(self.probe_bias.shape) != (n_q_heads, cfg.probe_rank)):
             raise ValueError("probe_bias must be a float32 [n_q_heads][probe_rank] tensor")
         cfg.value_probe_bias = 0 if self.probe_bias is None else self.probe_bias.data_ptr()
+        # probes of the historical message views [n_hist][Hq][r][d]
+        self.probe_hist = None if probe_hist is None else probe_hist.contiguous()
+        if self.probe_hist is not None:
+            if self.probe_hist.dim() != 4 or tuple(self.probe_hist.shape[1:]) != tuple(self.probe.shape) or \
+                    self.probe_hist.dtype != self.probe.dtype:
+                raise ValueError("probe_hist must be [n_hist] x the probe's shape and dtype")
+            cfg.max_hist_views = self.probe_hist.shape[0]
+            cfg.value_probe_hist = self.probe_hist.data_ptr()
         self.cfg = cfg
         self.dtype = dtype
         _check(gmc_init(cfg), "gmc_init")
@@ -401,9 +429,25 @@ class Pruner:
     def trace_dims(self, n, t, k):
         return gmc_trace_dims(n, t, k)
 
-    def prune(self, hidden, text_q, vis_k, pos3d, k, nonvis_lse=None, trace: bool = False):
+    def prune(self, hidden, text_q, vis_k, pos3d, k, nonvis_lse=None, trace: bool = False, hist=None):
+        """hist: optional list of historical views, each (hidden, text_q,
+        vis_k[, nonvis_lse]) shaped like the current view's tensors."""
         torch = self.torch
         b, n, t = check_prune_inputs(self.cfg, self.dtype, hidden, text_q, vis_k, pos3d, nonvis_lse)
+        hist = list(hist or [])
+        views = []
+        for i, hv in enumerate(hist):
+            hv = tuple(hv) + (None,) * (4 - len(hv))
+            try:
+                check_prune_inputs(self.cfg, self.dtype, hv[0], hv[1], hv[2], pos3d, hv[3])
+                if hv[0].shape != hidden.shape or hv[1].shape != text_q.shape:
+                    raise ValueError("shapes differ from the current view's")
+                if hv[0].device != hidden.device:
+                    raise ValueError("not on hidden's device")
+            except ValueError as e:
+                raise ValueError(f"historical view {i}: {e}") from None
+            views.append(GmcView(hv[0].data_ptr(), hv[1].data_ptr(), hv[2].data_ptr(),
+                                 None if hv[3] is None else hv[3].data_ptr()))
         d = hidden.shape[2]
         kk = gmc_realized_k(n, k)
         dev = hidden.device
@@ -414,6 +458,7 @@ class Pruner:
         if trace:
             rounds, pool_cap, bcap, m_rows = gmc_trace_dims(n, t, k)
             hq = self.cfg.n_q_heads
+            m_rows += len(views) * hq * t       # each historical view's grounded rows
             r1 = max(rounds, 1)
             bufs = dict(
                 round_pool=torch.full((b, r1, pool_cap), -1, dtype=torch.int32, device=dev),
@@ -428,10 +473,16 @@ class Pruner:
             tr = GmcTrace(**{key: v.data_ptr() for key, v in bufs.items()})
         _check(gmc_set_stream(torch.cuda.current_stream(dev).cuda_stream), "gmc_set_stream")
         nv = None if nonvis_lse is None else nonvis_lse.data_ptr()
-        code = gmc_prune_ex(b, hidden.data_ptr(), text_q.data_ptr() if t > 0 else None,
-                            vis_k.data_ptr(), pos3d.data_ptr(), n, t, k, out_h.data_ptr(),
-                            out_p.data_ptr(), out_i.data_ptr(), nv, tr)
-        _check(code, "gmc_prune_ex")
+        if views:
+            code = gmc_prune_views(b, hidden.data_ptr(), text_q.data_ptr() if t > 0 else None,
+                                   vis_k.data_ptr(), pos3d.data_ptr(), n, t, k, out_h.data_ptr(),
+                                   out_p.data_ptr(), out_i.data_ptr(), nv, views, tr)
+            _check(code, "gmc_prune_views")
+        else:
+            code = gmc_prune_ex(b, hidden.data_ptr(), text_q.data_ptr() if t > 0 else None,
+                                vis_k.data_ptr(), pos3d.data_ptr(), n, t, k, out_h.data_ptr(),
+                                out_p.data_ptr(), out_i.data_ptr(), nv, tr)
+            _check(code, "gmc_prune_ex")
         if trace:
             return out_h, out_p, out_i, bufs
         return out_h, out_p, out_i
@@ -483,14 +534,16 @@ def from_device(t, torch) -> np.ndarray:
     return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
 
 
-def make_pruner(prob, torch, max_k=0, probe_bias=None, **overrides) -> Pruner:
+def make_pruner(prob, torch, max_k=0, probe_bias=None, hist=None, **overrides) -> Pruner:
     """A Pruner sized for a seeded workload (synth.Problem): its shape, dtype,
-    batch and token capacity, probe and bounded-bank projection."""
+    batch and token capacity, probe and bounded-bank projection, and the
+    probes of its historical views (synth.HistView list) when given."""
     w = prob.workload
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     probe = to_device(prob.probe, w.dtype, torch)
     proj = None if prob.app_proj is None else to_device(prob.app_proj, w.dtype, torch)
     bias = None if probe_bias is None else torch.from_numpy(np.ascontiguousarray(probe_bias, np.float32)).cuda()
+    ph = None if not hist else to_device(np.stack([v.probe for v in hist]), w.dtype, torch)
     return Pruner(d=w.d, n_q_heads=w.hq, n_kv_heads=w.hkv, head_dim=w.dh, probe=probe, dtype=tdt,
                   max_batch=w.batch, max_n=w.n, max_t=max(w.t, 1), max_k=max_k, app_projection=proj,
-                  probe_bias=bias, **overrides)
+                  probe_bias=bias, probe_hist=ph, **overrides)

@@ -111,6 +111,7 @@ Params make_params(const gmc_config& c) {
   p.disp_eps = c.disp_eps; p.terminal_q_weight = c.terminal_q_weight; p.rms_eps = c.rms_eps;
   p.norm_eps = c.norm_eps; p.restore_eps = c.restore_eps; p.pool_mult = c.pool_mult;
   p.probe_bias = c.value_probe_bias;
+  p.beta_view[0] = c.beta_msg;   // one view; calls with historical views set their own masses
   return p;
 }
 
@@ -144,6 +145,12 @@ int validate_config(const gmc_config* c) {
     return fail(GMC_ERR_ARG, "temperatures and gate scales must be positive");
   if (c->g_form != 0 && c->g_form != 1) return fail(GMC_ERR_ARG, "g_form=%d unknown", c->g_form);
   if (c->bounded_threshold_n < 1) return fail(GMC_ERR_ARG, "bounded_threshold_n must be >= 1");
+  if (c->max_hist_views < 0 || c->max_hist_views > GMC_MAX_HIST_VIEWS)
+    return fail(GMC_ERR_ARG, "max_hist_views=%d must be in [0, %d]", c->max_hist_views, GMC_MAX_HIST_VIEWS);
+  if (c->max_hist_views > 0 && !c->value_probe_hist)
+    return fail(GMC_ERR_ARG, "value_probe_hist is NULL but max_hist_views=%d", c->max_hist_views);
+  if (!(c->hist_mass >= 0.f && c->hist_mass <= 1.f))
+    return fail(GMC_ERR_ARG, "hist_mass must be in [0, 1]");
   if (c->max_n > c->bounded_threshold_n) {
     if (!c->app_projection) return fail(GMC_ERR_ARG, "app_projection is NULL but max_n exceeds the bounded threshold");
     if (c->app_rank < 64 || c->app_rank % 64 != 0 || c->app_rank > 1024)
@@ -159,6 +166,7 @@ struct Plan {
   long long s_n, s_z, s_zp, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
       s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_ftag, s_gate,
       s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_ts, s_tc, s_lpart, s_lcnt;
+  long long s_gpart1, s_n2h;
   long long s_cgain, s_cscore, s_cpool, s_cbat, s_cpart, s_cert, s_dstat;
 };
 
@@ -174,7 +182,7 @@ Plan make_plan(const gmc_config& c) {
   k.bounded_possible = c.max_n > c.bounded_threshold_n;
   k.mv = std::max(std::min(c.max_n, c.bounded_threshold_n),
                   k.bounded_possible ? std::min(c.app_max_clients, c.max_n) : 0);
-  k.m = k.hq * k.T + k.mv + c.landmarks * c.landmarks;
+  k.m = (1 + c.max_hist_views) * k.hq * k.T + k.mv + c.landmarks * c.landmarks;
   k.ldM = static_cast<int>(round_up(k.m, 4));
   k.bmax = std::max(c.batch_b, k.bounded_possible ? c.batch_b_bounded : 0);
   k.pool_cap = c.pool_mult * k.bmax;
@@ -191,7 +199,9 @@ Plan make_plan(const gmc_config& c) {
   pl.s_E = static_cast<long long>(k.N) * k.ldM;
   pl.s_m = k.ldM;
   pl.s_apart = cdiv(k.N, 64) * k.mv;
-  pl.s_gpart = cdiv(k.N, kHeadTok) * round_up(npairs, 4);
+  pl.s_gpart1 = std::max(cdiv(k.N, kHeadTok) * round_up(npairs, 4), cdiv(k.N, 64) * k.hq);
+  pl.s_gpart = (1 + c.max_hist_views) * pl.s_gpart1;
+  pl.s_n2h = c.max_hist_views > 0 ? k.N : 1;
   pl.s_e2 = static_cast<long long>(k.hq) * k.N;
   pl.s_om = kMaxHeads;
   pl.s_eb = k.N;
@@ -254,7 +264,8 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   ws->rowsum = reinterpret_cast<float*>(take(pl.s_m, 4));
   ws->apart_sum = reinterpret_cast<float*>(take(pl.s_apart, 4));
   ws->apart_max = reinterpret_cast<float*>(take(pl.s_apart, 4)); ws->s_apart = pl.s_apart;
-  F(gpart); F(e2);
+  F(gpart); F(e2); F(n2h);
+  ws->s_gpart1 = pl.s_gpart1;
   ws->omega = reinterpret_cast<float*>(take(pl.s_om, 4)); ws->s_om = pl.s_om;
   ws->ebar = reinterpret_cast<float*>(take(pl.s_eb, 4)); ws->s_eb = pl.s_eb;
   F(pc);
@@ -356,6 +367,8 @@ void gmc_config_default(gmc_config* c) {
   c->app_rank = 128;
   c->app_max_clients = 4096;
   c->batch_b_bounded = 512;
+  c->max_hist_views = 0;
+  c->hist_mass = 0.5f;
 }
 
 void gmc_free(void) {
@@ -537,8 +550,9 @@ int gmc_timing_read(double* total_ms, int64_t* spans, int32_t n) {
 
 namespace {
 
-int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req, Shape* out) {
-  return gmc::resolve_shape(c.cfg, Limits{c.cap.B, c.cap.N, c.cap.T, c.cap.K}, B, N, T, K_req, out);
+int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req, Shape* out, int64_t n_hist = 0) {
+  return gmc::resolve_shape(c.cfg, Limits{c.cap.B, c.cap.N, c.cap.T, c.cap.K, c.cfg.max_hist_views}, B, N, T,
+                            K_req, out, n_hist);
 }
 
 }  // namespace
@@ -546,13 +560,16 @@ int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req,
 namespace gmc {
 
 int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, int64_t T, int64_t K_req,
-                  Shape* out) {
+                  Shape* out, int64_t n_hist) {
   if (B < 1) return fail(GMC_ERR_ARG, "batch=%lld must be >= 1", static_cast<long long>(B));
   if (N < 1) return fail(GMC_ERR_ARG, "N=%lld must be >= 1", static_cast<long long>(N));
   if (T < 0) return fail(GMC_ERR_ARG, "T=%lld must be >= 0", static_cast<long long>(T));
   if (B > cap.B) return fail(GMC_ERR_CAPACITY, "batch=%lld exceeds max_batch=%d", static_cast<long long>(B), cap.B);
   if (N > cap.N) return fail(GMC_ERR_CAPACITY, "N=%lld exceeds max_n=%d", static_cast<long long>(N), cap.N);
   if (T > cap.T) return fail(GMC_ERR_CAPACITY, "T=%lld exceeds max_t=%d", static_cast<long long>(T), cap.T);
+  if (n_hist < 0) return fail(GMC_ERR_ARG, "n_hist=%lld must be >= 0", static_cast<long long>(n_hist));
+  if (n_hist > cap.H)
+    return fail(GMC_ERR_CAPACITY, "n_hist=%lld exceeds max_hist_views=%d", static_cast<long long>(n_hist), cap.H);
   const int64_t K = gmc_realized_k(N, K_req);
   Shape s{};
   s.B = static_cast<int>(B);
@@ -572,7 +589,10 @@ int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, 
     return fail(GMC_ERR_CAPACITY, "realised K=%lld exceeds max_k=%d", static_cast<long long>(K), cap.K);
   s.bounded = N > g.bounded_threshold_n ? 1 : 0;
   s.app_rank = s.bounded ? g.app_rank : 0;
-  s.mg = s.hq * s.T;
+  // every message view contributes Hq T grounded rows (none without queries)
+  s.nviews = s.T > 0 ? 1 + static_cast<int>(n_hist) : 1;
+  s.mg1 = s.hq * s.T;
+  s.mg = s.nviews * s.mg1;
   s.mv = app_rows(g, s.N);
   s.ms = g.landmarks * g.landmarks;
   s.m = s.mg + s.mv + s.ms;
@@ -598,10 +618,16 @@ int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, 
 }
 
 int check_tensors(const Shape& s, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
-                  const void* out_hidden, const int32_t* out_pos, const int32_t* out_idx) {
+                  const void* out_hidden, const int32_t* out_pos, const int32_t* out_idx, const gmc_view* hist) {
   if (!hidden || !vis_k || !pos3d || !out_hidden || !out_pos || !out_idx)
     return fail(GMC_ERR_ARG, "gmc_prune: null tensor pointer");
   if (s.T > 0 && !text_q) return fail(GMC_ERR_ARG, "gmc_prune: text_q is NULL with T > 0");
+  if (s.nviews > 1) {
+    if (!hist) return fail(GMC_ERR_ARG, "gmc_prune_views: hist is NULL with n_hist > 0");
+    for (int v = 0; v + 1 < s.nviews; ++v)
+      if (!hist[v].hidden || !hist[v].text_q || !hist[v].vis_k)
+        return fail(GMC_ERR_ARG, "gmc_prune_views: historical view %d has a NULL tensor", v);
+  }
   const size_t esz = s.dtype == GMC_F32 ? 4 : 2;
   // outputs must not overlap the inputs
   auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
@@ -627,13 +653,31 @@ int check_tensors(const Shape& s, const void* hidden, const void* text_q, const 
   return GMC_OK;
 }
 
-int enqueue_prune(const gmc_config& cfg, const Params& pr, const Ws& ws, const Shape& s, const PathStreams& ps,
+int enqueue_prune(const gmc_config& cfg, const Params& pr0, const Ws& ws, const Shape& s, const PathStreams& ps,
                   int diag, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
                   void* out_hidden, int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse,
-                  const gmc_trace& tr, bool* cert_done) {
+                  const gmc_trace& tr, bool* cert_done, const gmc_view* hist) {
   *cert_done = false;
   hipStream_t st = ps.st;
   hipError_t err;
+  // message views: the current one, then the historical ones with their own
+  // probes; the message mass beta_msg splits over them (reading R14)
+  Params pr = pr0;
+  MsgView views[kMaxViews] = {};
+  views[0] = MsgView{hidden, text_q, vis_k, cfg.value_probe, cfg.value_probe_bias, nonvis_lse};
+  const int n_hist = s.nviews - 1;
+  if (n_hist > 0) {
+    const size_t esz = s.dtype == GMC_F32 ? 4 : 2;
+    pr.beta_view[0] = cfg.beta_msg * (1.f - cfg.hist_mass);
+    for (int v = 1; v <= n_hist; ++v) {
+      pr.beta_view[v] = cfg.beta_msg * cfg.hist_mass / static_cast<float>(n_hist);
+      const char* probe = static_cast<const char*>(cfg.value_probe_hist) +
+                          static_cast<size_t>(v - 1) * s.hq * s.r * s.d * esz;
+      const float* bias = cfg.value_probe_bias_hist ? cfg.value_probe_bias_hist + (v - 1) * s.hq * s.r : nullptr;
+      views[v] = MsgView{hist[v - 1].hidden, hist[v - 1].text_q, hist[v - 1].vis_k, probe, bias,
+                         hist[v - 1].nonvis_lse};
+    }
+  }
   if (s.K == s.N) {
     err = launch_identity(s, hidden, pos3d, out_hidden, out_pos, out_idx, st);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "identity copy: %s", hipGetErrorString(err));
@@ -677,8 +721,7 @@ int enqueue_prune(const gmc_config& cfg, const Params& pr, const Ws& ws, const S
     err = hipEventRecord(ps.join, ps.side);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }
-  err = launch_message(s, pr, ws, hidden, text_q, vis_k, cfg.value_probe, nonvis_lse, tr.omega,
-                       flag_join ? bank_flag : nullptr, st);
+  err = launch_message(s, pr, ws, views, tr.omega, flag_join ? bank_flag : nullptr, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
   if (fork && !flag_join) {
     err = hipStreamWaitEvent(st, ps.join, 0);
@@ -724,14 +767,14 @@ namespace {
 
 int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
         int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
-        const float* nonvis_lse, const gmc_trace* trace) {
+        const float* nonvis_lse, const gmc_trace* trace, int64_t n_hist = 0, const gmc_view* hist = nullptr) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_prune: no context (call gmc_init first)");
   Context& c = *g_ctx;
   Shape s;
-  int rc = make_shape(c, B, N, T, K, &s);
+  int rc = make_shape(c, B, N, T, K, &s, n_hist);
   if (rc != GMC_OK) return rc;
-  rc = check_tensors(s, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx);
+  rc = check_tensors(s, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx, hist);
   if (rc != GMC_OK) return rc;
   const gmc_trace tr = trace ? *trace : gmc_trace{};
   hipError_t err = hipSetDevice(c.device);
@@ -760,7 +803,7 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   }
   bool cert = false;
   rc = enqueue_prune(c.cfg, c.pr, c.ws, s, ps, c.diag, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx,
-                     nonvis_lse, tr, &cert);
+                     nonvis_lse, tr, &cert, hist);
   c.last_cert = cert;
   return rc;
 }
@@ -784,6 +827,13 @@ int gmc_prune_ex(int64_t B, const void* hidden, const void* text_q, const void* 
                  int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
                  const float* nonvis_lse, const gmc_trace* trace) {
   return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nonvis_lse, trace);
+}
+
+int gmc_prune_views(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+                    int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
+                    const float* nonvis_lse, int64_t n_hist, const gmc_view* hist, const gmc_trace* trace) {
+  return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nonvis_lse, trace, n_hist,
+             hist);
 }
 
 int gmc_set_diag(int32_t flags) {

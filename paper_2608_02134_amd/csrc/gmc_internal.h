@@ -8,6 +8,7 @@
 namespace gmc {
 
 constexpr int kMaxHeads = 32;     // Hq limit (head-pattern Gram kept in registers)
+constexpr int kMaxViews = 4;      // message views: the current one + up to 3 historical
 constexpr int kMaxProbe = 8;      // probe rank limit
 constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 8;       // tokens per head-Gram block (two per wave)
@@ -36,6 +37,7 @@ struct Shape {
   int B, N, T, K, d, hq, hkv, dh, r, hr;  // hr = hq * r
   int hg;                                 // query heads per kv head
   int mg, mv, ms, m;                      // client rows: grounded, appearance, spatial, total
+  int nviews, mg1;                        // message views; grounded rows per view (mg = nviews mg1)
   int ldM;                                // token-major client matrix: floats per token (multiple of 4, >= m)
   int bounded;                            // 1: bounded appearance bank
   int app_rank;
@@ -58,7 +60,8 @@ struct Params {
   int max_head_clusters;
   float disp_eps, terminal_q_weight, rms_eps, norm_eps, restore_eps;
   int pool_mult;
-  const float* probe_bias;   // [hq][r] or null: b_h added to Z_h[i]
+  const float* probe_bias;   // [hq][r] or null: b_h added to Z_h[i] (of the view being built)
+  float beta_view[kMaxViews];   // mass of each message view (current first)
 };
 
 // Workspace: every buffer is [max_batch][per-problem size]; s_* are the
@@ -76,7 +79,9 @@ struct Ws {
   float* peak;                          // max_i Cbar_mi                [ldM]
   float* rowsum;                        // grounded row sums Z_(h,t)    [ldM]
   float* apart_sum; float* apart_max; long long s_apart;  // appearance partials [cblk][mv]
-  float* gpart;    long long s_gpart;   // head-Gram partials           [blk][npairs]
+  float* gpart;    long long s_gpart;   // head-Gram partials, per view [views][blk][npairs]
+  long long s_gpart1;                   // one view's share of gpart
+  float* n2h;      long long s_n2h;     // squared row norms of a historical view's states [N]
   float* e2;       long long s_e2;      // sum_t nu_t e^2               [hq][N]
   float* omega;    long long s_om;      // head weights                 [kMaxHeads]
   float* ebar;     long long s_eb;      // normalised energy            [N]

@@ -24,13 +24,24 @@ hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, int
 // One block that returns once every row-norm block carries call_tag.
 hipError_t launch_bank_gate(const Shape& sh, const Ws& ws, int call_tag, hipStream_t st);
 
-// Value probe, mass coordinate, native slice, head weights, grounded row
-// weights and normalised energy (after launch_rownorm).  With bank_flag set
-// (T > 0), the last kernel also waits until the flag reads 1.
-hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
-                          const void* text_q, const void* vis_k, const void* probe,
-                          const float* nonvis_lse, float* trace_omega, const int* bank_flag,
-                          hipStream_t st);
+// The inputs of one message view: its states, queries, keys, folded value
+// probe (and bias) and optional nonvisual log-sum-exp.
+struct MsgView {
+  const void* hidden;
+  const void* text_q;
+  const void* vis_k;
+  const void* probe;
+  const float* probe_bias;
+  const float* nonvis_lse;
+};
+
+// Value probe, mass coordinate, native slice of every message view (views[0]
+// the current one, sh.nviews in all), head weights over the views' patterns,
+// grounded row weights and the current view's energy (after launch_rownorm).
+// With bank_flag set (T > 0), the last kernel also waits until the flag
+// reads 1.
+hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const MsgView* views,
+                          float* trace_omega, const int* bank_flag, hipStream_t st);
 
 // Sets *flag = 1 once the work before it on st has finished.
 hipError_t launch_bank_signal(int* flag, hipStream_t st);

@@ -17,10 +17,11 @@ namespace gmc {
 // kernel resets the per-call state, being the first of every call.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* hidden, int call_tag) {
+__global__ void __launch_bounds__(256) rownorm_kernel(Shape sh, Ws ws, const T* hidden, int call_tag, int reset) {
   const int p = blockIdx.y;
-  // the call's first kernel also resets the per-call state
-  call_init_range(sh, ws, p, blockIdx.x * 256 + threadIdx.x, gridDim.x * 256);
+  // the call's first kernel also resets the per-call state (a historical
+  // view's states are normed later, into their own buffer, without it)
+  if (reset) call_init_range(sh, ws, p, blockIdx.x * 256 + threadIdx.x, gridDim.x * 256);
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i < sh.N) {
   const T* row = hidden + (static_cast<long long>(p) * sh.N + i) * sh.d;
@@ -674,7 +675,7 @@ constexpr int kGramTok = 2;                 // tokens per wave (kHeadTok per blo
 static_assert(kGramTok * 4 == kHeadTok, "one block covers kHeadTok tokens");
 
 template <int R>
-__global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws ws) {
+__global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws ws, int write_e2) {
   constexpr int U = R + 1;                     // [Z_h[i]; sigma_h] / l_h[i]
   __shared__ __attribute__((aligned(16))) float xs[4][32 * kGramPitch];
   __shared__ float us[4][32 * U];
@@ -782,7 +783,7 @@ __global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws w
 #pragma unroll
         for (int c = 0; c < U; ++c) w += Uv[hh * U + c] * ug[c];
         acc[tl][e] += g[tl][e] * w;
-        if (tl != 1 && hh == gg && hh < H) {
+        if (write_e2 && tl != 1 && hh == gg && hh < H) {
           const float xl = X[hh * kGramPitch + tl_last];
           e2[static_cast<long long>(hh) * sh.N + i] = nu_o * g[tl][e] + (nu_last - nu_o) * xl * xl;
         }
@@ -835,88 +836,106 @@ constexpr int kClusterGB = 36;   // block partial quads in flight per thread
 __global__ void __launch_bounds__(kClusterThreads) __attribute__((amdgpu_waves_per_eu(1, 2)))
 cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_flag) {
   constexpr int NT = kClusterThreads, kRW = 4;
-  __shared__ float gam[kMaxHeads][kMaxHeads + 1];
-  __shared__ float cosm[kMaxHeads][kMaxHeads + 1];
+  __shared__ float gam[kMaxHeads][kMaxHeads + 1];    // pattern Gram over the views
+  __shared__ float cosm[kMaxHeads][kMaxHeads + 1];   // one view's Gamma, then the cosines
   __shared__ float4 gq[NT];
   __shared__ float hs[4 * NT];
-  __shared__ float om[kMaxHeads];
+  __shared__ float om[kMaxHeads], ab[kMaxHeads];
   __shared__ int asg[kMaxHeads];
-  const int p = blockIdx.x, tid = threadIdx.x, H = sh.hq, T = sh.T;
-  const float* gp = ws.gpart + p * ws.s_gpart;
+  const int p = blockIdx.x, tid = threadIdx.x, H = sh.hq, T = sh.T, M1 = sh.mg1;
   const float* rowsum = ws.rowsum + p * ws.s_m;
   const int nb = sh.n_head_blk, npp = (sh.npairs + 3) & ~3, nq = npp / 4;
-  // Gamma: thread (quad qq of pairs, block group bg) adds its groups' quads in
-  // block order; the groups are added in order below.  The first batch of
-  // quads goes out before the row-sum loads, and every load of the first
-  // batch before the first add.
+  // Gamma of a view: thread (quad qq of pairs, block group bg) adds its
+  // groups' quads in block order; the groups are added in order below.  The
+  // first batch of quads goes out before the row-sum loads, and every load
+  // of the first batch before the first add.
   const int ngrp = max(1, NT / nq);
   const int qq = tid % nq, bg = tid / nq;
   const int bper = (nb + ngrp - 1) / ngrp;
   const int b_beg = bg * bper, b_end = min(nb, b_beg + bper);
   const bool gthr = bg < ngrp && b_beg < b_end;
-  float4 v[kClusterGB];
-  if (gthr) {
-#pragma unroll
-    for (int j = 0; j < kClusterGB; ++j)
-      v[j] = *reinterpret_cast<const float4*>(gp + static_cast<long long>(min(b_beg + j, b_end - 1)) * npp + 4 * qq);
-  }
-  // the first pass of the grounded row weights
-  float zv0[kRW], pv0[kRW];
-#pragma unroll
-  for (int k = 0; k < kRW; ++k) {
-    const int m = min(k * NT + tid, sh.mg - 1);
-    zv0[k] = rowsum[m];
-    pv0[k] = ws.peak[p * ws.s_m + m];
-  }
   // grounded row sums in runs of four queries of one head (T a multiple of 4
-  // and at most 4 NT runs; otherwise each head's lane adds its rows below)
-  const bool runs = (T & 3) == 0 && sh.mg <= 16 * NT;
-  float4 rq[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int x = k * NT + tid;
-    rq[k] = (runs && 4 * x < sh.mg) ? *reinterpret_cast<const float4*>(rowsum + 4 * x) : float4{0.f, 0.f, 0.f, 0.f};
-  }
-  __builtin_amdgcn_sched_barrier(0);
-  float4 gs = {0.f, 0.f, 0.f, 0.f};
-  if (gthr) {
-#pragma unroll
-    for (int j = 0; j < kClusterGB; ++j)
-      if (b_beg + j < b_end) { gs.x += v[j].x; gs.y += v[j].y; gs.z += v[j].z; gs.w += v[j].w; }
-    for (int b0 = b_beg + kClusterGB; b0 < b_end; b0 += kClusterGB) {
+  // and at most 4 NT runs per view; otherwise each head's lane adds its rows)
+  const bool runs = (T & 3) == 0 && M1 <= 16 * NT;
+  float zv0[kRW], pv0[kRW];
+  for (int v = 0; v < sh.nviews; ++v) {
+    const float* gp = ws.gpart + p * ws.s_gpart + v * ws.s_gpart1;
+    const float* rs = rowsum + v * M1;
+    float4 vq[kClusterGB];
+    if (gthr) {
 #pragma unroll
       for (int j = 0; j < kClusterGB; ++j)
-        v[j] = *reinterpret_cast<const float4*>(gp + static_cast<long long>(min(b0 + j, b_end - 1)) * npp + 4 * qq);
-      __builtin_amdgcn_sched_barrier(0);
+        vq[j] = *reinterpret_cast<const float4*>(gp + static_cast<long long>(min(b_beg + j, b_end - 1)) * npp + 4 * qq);
+    }
+    if (v == 0) {
+      // the first pass of the grounded row weights
+#pragma unroll
+      for (int k = 0; k < kRW; ++k) {
+        const int m = min(k * NT + tid, sh.mg - 1);
+        zv0[k] = rowsum[m];
+        pv0[k] = ws.peak[p * ws.s_m + m];
+      }
+    }
+    float4 rq[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int x = k * NT + tid;
+      rq[k] = (runs && 4 * x < M1) ? *reinterpret_cast<const float4*>(rs + 4 * x) : float4{0.f, 0.f, 0.f, 0.f};
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    float4 gs = {0.f, 0.f, 0.f, 0.f};
+    if (gthr) {
 #pragma unroll
       for (int j = 0; j < kClusterGB; ++j)
-        if (b0 + j < b_end) { gs.x += v[j].x; gs.y += v[j].y; gs.z += v[j].z; gs.w += v[j].w; }
-    }
-  }
-  gq[tid] = gs;
+        if (b_beg + j < b_end) { gs.x += vq[j].x; gs.y += vq[j].y; gs.z += vq[j].z; gs.w += vq[j].w; }
+      for (int b0 = b_beg + kClusterGB; b0 < b_end; b0 += kClusterGB) {
 #pragma unroll
-  for (int k = 0; k < 4; ++k) hs[k * NT + tid] = (rq[k].x + rq[k].y) + (rq[k].z + rq[k].w);
-  __syncthreads();
-  for (int hg = tid; hg < kMaxHeads * kMaxHeads; hg += NT) {
-    const int h = hg / kMaxHeads, g = hg % kMaxHeads;
-    if (h <= g && g < H) {
-      const int x = h * H - h * (h - 1) / 2 + (g - h);   // pair (h, g) in row-major upper order
-      const int q4 = x >> 2, c = x & 3;
-      const float* gqf = reinterpret_cast<const float*>(gq);
-      float s = 0.f;
-      for (int g2 = 0; g2 < ngrp; ++g2) s += gqf[4 * (g2 * nq + q4) + c];
-      gam[h][g] = s;
-      gam[g][h] = s;
+        for (int j = 0; j < kClusterGB; ++j)
+          vq[j] = *reinterpret_cast<const float4*>(gp + static_cast<long long>(min(b0 + j, b_end - 1)) * npp + 4 * qq);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < kClusterGB; ++j)
+          if (b0 + j < b_end) { gs.x += vq[j].x; gs.y += vq[j].y; gs.z += vq[j].z; gs.w += vq[j].w; }
+      }
     }
-  }
-  float abar = 0.f;
-  if (tid < 64) {
-    // mean atom norm abar_h = sum_t Z_(h,t) / (T N)
-    const int h = min(tid, H - 1);
-    if (runs) {
-      for (int x = h * (T / 4); x < (h + 1) * (T / 4); ++x) abar += hs[x];
-    } else {
-      for (int t = 0; t < T; ++t) abar += rowsum[h * T + t];
+    __syncthreads();   // gq, hs, cosm and ab of the previous view are consumed
+    gq[tid] = gs;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) hs[k * NT + tid] = (rq[k].x + rq[k].y) + (rq[k].z + rq[k].w);
+    __syncthreads();
+    for (int hg = tid; hg < kMaxHeads * kMaxHeads; hg += NT) {
+      const int h = hg / kMaxHeads, g = hg % kMaxHeads;
+      if (h <= g && g < H) {
+        const int x = h * H - h * (h - 1) / 2 + (g - h);   // pair (h, g) in row-major upper order
+        const int q4 = x >> 2, c = x & 3;
+        const float* gqf = reinterpret_cast<const float*>(gq);
+        float sv = 0.f;
+        for (int g2 = 0; g2 < ngrp; ++g2) sv += gqf[4 * (g2 * nq + q4) + c];
+        cosm[h][g] = sv;
+        cosm[g][h] = sv;
+      }
+    }
+    if (tid < 64) {
+      // mean atom norm abar_h = sum_t Z_(h,t) / (T N) of this view
+      const int h = min(tid, H - 1);
+      float abar = 0.f;
+      if (runs) {
+        for (int x = h * (T / 4); x < (h + 1) * (T / 4); ++x) abar += hs[x];
+      } else {
+        for (int t = 0; t < T; ++t) abar += rs[h * T + t];
+      }
+      if (tid < H) ab[tid] = abar / (static_cast<float>(T) * sh.N);
+    }
+    __syncthreads();
+    // the view's share of the pattern Gram: beta_v Gamma_hg / (abar_h abar_g)
+    // (the patterns are its atoms scaled to unit average norm, times
+    // sqrt(beta_v)); a head without energy in the view adds nothing
+    const float beta = pr.beta_view[v];
+    for (int x = tid; x < H * H; x += NT) {
+      const int h = x / H, g = x % H;
+      const float ih = ab[h] > 0.f ? 1.f / ab[h] : 0.f, ig = ab[g] > 0.f ? 1.f / ab[g] : 0.f;
+      const float c = beta * cosm[h][g] * ih * ig;
+      gam[h][g] = v == 0 ? c : gam[h][g] + c;
     }
   }
   __syncthreads();
@@ -930,15 +949,15 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
   if (tid < 64) {
     const int lane = tid, h = lane;
     const bool valid = h < H;
-    abar = valid ? abar / (static_cast<float>(T) * sh.N) : 0.f;
     const float ghh = valid ? gam[h][h] : 0.f;
     const bool active = valid && ghh > 0.f;
     const int n_active = __popcll(__ballot(active));
     float w_h = 0.f;
     int cl = -1;
     if (n_active > 0) {
-      // first centre: largest pre-normalisation pattern sqrt(beta Gamma_hh) / abar_h
-      const float v = active ? sqrtf(pr.beta_msg * ghh) / (abar > 0.f ? abar : 1.f) : -INFINITY;
+      // first centre: the largest pre-normalisation pattern (its squared norm
+      // is the pattern Gram's diagonal)
+      const float v = active ? sqrtf(ghh) : -INFINITY;
       const float vbest = wave_max(v);
       const int idx = __ffsll(static_cast<unsigned long long>(__ballot(active && v == vbest))) - 1;
       int nc = 1;
@@ -995,7 +1014,7 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
     }
   }
   __syncthreads();
-  // grounded row weights beta_msg omega_h nu_t a_(h,t) / Z_(h,t)
+  // grounded row weights beta_v omega_h nu_t a_(h,t) / Z_(h,t) of every view
   const float nu_o = 1.f / (T - 1 + pr.terminal_q_weight);
   for (int m0 = 0; m0 < sh.mg; m0 += NT * kRW) {
     float zv[kRW], pv[kRW];
@@ -1014,9 +1033,9 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
     for (int k = 0; k < kRW; ++k) {
       const int m = m0 + k * NT + tid;
       if (m < sh.mg) {
-        const int h = m / T, t = m % T;
+        const int v = m / M1, mm = m - v * M1, h = mm / T, t = mm % T;
         const float nu = (t == T - 1) ? pr.terminal_q_weight * nu_o : nu_o;
-        const float a = (zv[k] > 0.f) ? pr.beta_msg * om[h] * nu / zv[k] : 0.f;
+        const float a = (zv[k] > 0.f) ? pr.beta_view[v] * om[h] * nu / zv[k] : 0.f;
         ws.alpha[p * ws.s_m + m] = a;
         ws.peak[p * ws.s_m + m] = pv[k] * a;
       }
@@ -1053,49 +1072,58 @@ __global__ void no_grounded_kernel(Shape sh, Ws ws, float* trace_omega) {
 // ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
+// Row norms of a historical view's states into ws.n2h (no per-call reset).
 template <typename T>
-static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden_v,
-                               const void* text_q_v, const void* vis_k_v, const void* probe_v,
-                               const float* nonvis_lse, float* trace_omega, const int* bank_flag,
+static void launch_view_rownorm(const Shape& sh, const Ws& ws, const void* hidden, hipStream_t st) {
+  Ws wv = ws;
+  wv.n2 = ws.n2h;
+  wv.s_n = ws.s_n2h;
+  hipLaunchKernelGGL(rownorm_kernel<T>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, wv,
+                     static_cast<const T*>(hidden), 0, 0);
+}
+
+// One message view: value probe and mass coordinate from the view's states
+// and folded probe, the native slice into the view's grounded rows, and the
+// view's head-pattern Gram partials (the current view also leaves the
+// energy numerators).  `sv` counts one view's grounded rows; `wv` points at
+// the view's rows, norms and Gram partials.
+template <typename T>
+static hipError_t message_view(const Shape& sv, const Params& pr, const Ws& wv, const MsgView& mv, bool current,
                                hipStream_t st) {
-  const T* hidden = static_cast<const T*>(hidden_v);
+  const T* hidden = static_cast<const T*>(mv.hidden);
+  Params pv = pr;
+  pv.probe_bias = mv.probe_bias;
   timer_mark(kStProbe, true, st);
-  RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
-  RowOperand<T> Bp{static_cast<const T*>(probe_v), sh.d, 0, nullptr, 0, sh.hr};
+  RowOperand<T> A{hidden, sv.d, static_cast<long long>(sv.N) * sv.d, nullptr, 0, sv.N};
+  RowOperand<T> Bp{static_cast<const T*>(mv.probe), sv.d, 0, nullptr, 0, sv.hr};
   // split the d-long contraction so four times as many blocks stream hidden
-  const int ksplit = (sh.d % (64 * kProbeSplit) == 0) ? kProbeSplit : 1;
-  ProbeSplitEpi pe{ws, sh.hr, static_cast<long long>(sh.N) * sh.hr};
-  hipError_t err = launch_gemm_nt<T, 64, 64>(A, Bp, sh.d, sh.B, pe, st, ksplit);
+  const int ksplit = (sv.d % (64 * kProbeSplit) == 0) ? kProbeSplit : 1;
+  ProbeSplitEpi pe{wv, sv.hr, static_cast<long long>(sv.N) * sv.hr};
+  hipError_t err = launch_gemm_nt<T, 64, 64>(A, Bp, sv.d, sv.B, pe, st, ksplit);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(sigma_ell_kernel, dim3((sh.N + 63) / 64, (sh.hq + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws,
+  hipLaunchKernelGGL(sigma_ell_kernel, dim3((sv.N + 63) / 64, (sv.hq + 3) / 4, sv.B), dim3(256), 0, st, sv, pv, wv,
                      ksplit);
   timer_mark(kStProbe, false, st);
-  if (sh.T == 0) {
-    timer_mark(kStHeads, true, st);
-    hipLaunchKernelGGL(no_grounded_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws,
-                       trace_omega);
-    timer_mark(kStHeads, false, st);
-    return hipGetLastError();
-  }
-  const dim3 lg((sh.hg * sh.T + 15) / 16 * sh.lsplit, sh.hkv, sh.B);
-  const dim3 lr((sh.hg * sh.T + 15) / 16, sh.hkv, sh.B);
+  const dim3 lg((sv.hg * sv.T + 15) / 16 * sv.lsplit, sv.hkv, sv.B);
+  const dim3 lr((sv.hg * sv.T + 15) / 16, sv.hkv, sv.B);
   // every tile of a block's rows fits the registers of its eight waves
-  const bool reg = (sh.N + 15) / 16 <= 8 * kLogitRegTiles;
-  const T* q = static_cast<const T*>(text_q_v);
-  const T* k = static_cast<const T*>(vis_k_v);
+  const bool reg = (sv.N + 15) / 16 <= 8 * kLogitRegTiles;
+  const T* q = static_cast<const T*>(mv.text_q);
+  const T* k = static_cast<const T*>(mv.vis_k);
+  const float* nonvis_lse = mv.nonvis_lse;
   timer_mark(kStLogits, true, st);
-  switch (sh.dh) {
+  switch (sv.dh) {
 #define GMC_LOGITS(DH)                                                                                         \
     case DH:                                                                                                   \
       if constexpr (logit_reg_ok<T, DH>()) {                                                                  \
         if (reg) {                                                                                             \
-          hipLaunchKernelGGL((logits_reg_kernel<T, DH, kLogitRegTiles>), lr, dim3(512), 0, st, sh, pr, ws, q, k, \
+          hipLaunchKernelGGL((logits_reg_kernel<T, DH, kLogitRegTiles>), lr, dim3(512), 0, st, sv, pv, wv, q, k, \
                              nonvis_lse);                                                                      \
           break;                                                                                               \
         }                                                                                                      \
       }                                                                                                        \
-      hipLaunchKernelGGL((logits_lse_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, pr, ws, q, k); \
-      hipLaunchKernelGGL((logits_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sh, ws, q, k,       \
+      hipLaunchKernelGGL((logits_lse_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sv, pv, wv, q, k); \
+      hipLaunchKernelGGL((logits_kernel<T, DH>), lg, dim3(64 * logit_waves<T, DH>()), 0, st, sv, wv, q, k,       \
                          nonvis_lse);                                                                          \
       break;
     GMC_LOGITS(32) GMC_LOGITS(64) GMC_LOGITS(96) GMC_LOGITS(128)
@@ -1105,14 +1133,47 @@ static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, 
   }
   timer_mark(kStLogits, false, st);
   timer_mark(kStHeads, true, st);
-  switch (sh.r) {
+  const int we2 = current ? 1 : 0;
+  switch (sv.r) {
 #define GMC_HEADGRAM(R) \
-    case R: hipLaunchKernelGGL(headgram_kernel<R>, dim3(sh.n_head_blk, sh.B), dim3(256), 0, st, sh, pr, ws); break;
+    case R: hipLaunchKernelGGL(headgram_kernel<R>, dim3(sv.n_head_blk, sv.B), dim3(256), 0, st, sv, pv, wv, we2); break;
     GMC_HEADGRAM(1) GMC_HEADGRAM(2) GMC_HEADGRAM(3) GMC_HEADGRAM(4)
     GMC_HEADGRAM(5) GMC_HEADGRAM(6) GMC_HEADGRAM(7) GMC_HEADGRAM(8)
 #undef GMC_HEADGRAM
     default: return hipErrorInvalidValue;
   }
+  timer_mark(kStHeads, false, st);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t message_impl(const Shape& sh, const Params& pr, const Ws& ws, const MsgView* views,
+                               float* trace_omega, const int* bank_flag, hipStream_t st) {
+  if (sh.T == 0) {
+    // no grounded rows: the value probe is not needed either
+    timer_mark(kStHeads, true, st);
+    hipLaunchKernelGGL(no_grounded_kernel, dim3((sh.N + 255) / 256, sh.B), dim3(256), 0, st, sh, ws,
+                       trace_omega);
+    timer_mark(kStHeads, false, st);
+    return hipGetLastError();
+  }
+  Shape sv = sh;
+  sv.mg = sh.mg1;
+  for (int v = 0; v < sh.nviews; ++v) {
+    Ws wv = ws;
+    wv.E = ws.E + static_cast<long long>(v) * sh.mg1;
+    wv.rowsum = ws.rowsum + static_cast<long long>(v) * sh.mg1;
+    wv.peak = ws.peak + static_cast<long long>(v) * sh.mg1;
+    wv.gpart = ws.gpart + v * ws.s_gpart1;
+    if (v > 0) {
+      launch_view_rownorm<T>(sh, ws, views[v].hidden, st);
+      wv.n2 = ws.n2h;
+      wv.s_n = ws.s_n2h;
+    }
+    const hipError_t err = message_view<T>(sv, pr, wv, views[v], v == 0, st);
+    if (err != hipSuccess) return err;
+  }
+  timer_mark(kStHeads, true, st);
   hipLaunchKernelGGL(cluster_kernel, dim3(sh.B), dim3(kClusterThreads), 0, st, sh, pr, ws, trace_omega, bank_flag);
   timer_mark(kStHeads, false, st);
   return hipGetLastError();
@@ -1122,10 +1183,10 @@ hipError_t launch_rownorm(const Shape& sh, const Ws& ws, const void* hidden, int
   timer_mark(kStInit, true, st);
   if (sh.dtype == 0)
     hipLaunchKernelGGL(rownorm_kernel<float>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, ws,
-                       static_cast<const float*>(hidden), call_tag);
+                       static_cast<const float*>(hidden), call_tag, 1);
   else
     hipLaunchKernelGGL(rownorm_kernel<bf16_t>, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, ws,
-                       static_cast<const bf16_t*>(hidden), call_tag);
+                       static_cast<const bf16_t*>(hidden), call_tag, 1);
   timer_mark(kStInit, false, st);
   return hipGetLastError();
 }
@@ -1135,13 +1196,10 @@ hipError_t launch_bank_gate(const Shape& sh, const Ws& ws, int call_tag, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
-                          const void* text_q, const void* vis_k, const void* probe,
-                          const float* nonvis_lse, float* trace_omega, const int* bank_flag,
-                          hipStream_t st) {
-  if (sh.dtype == 0)
-    return message_impl<float>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, bank_flag, st);
-  return message_impl<bf16_t>(sh, pr, ws, hidden, text_q, vis_k, probe, nonvis_lse, trace_omega, bank_flag, st);
+hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const MsgView* views,
+                          float* trace_omega, const int* bank_flag, hipStream_t st) {
+  if (sh.dtype == 0) return message_impl<float>(sh, pr, ws, views, trace_omega, bank_flag, st);
+  return message_impl<bf16_t>(sh, pr, ws, views, trace_omega, bank_flag, st);
 }
 
 hipError_t launch_bank_signal(int* flag, hipStream_t st) {

@@ -40,7 +40,7 @@ import numpy as np
 
 __all__ = [
     "Workload", "WORKLOADS", "Problem", "make_problem", "round_bf16",
-    "bf16_bits", "rademacher_projection", "APP_PROJ_SEED",
+    "bf16_bits", "rademacher_projection", "APP_PROJ_SEED", "HistView", "make_history",
 ]
 
 APP_PROJ_SEED = 104729  # seed of the long-prefix appearance projection
@@ -235,3 +235,39 @@ def make_problem(name: str, *, batch: Optional[int] = None, n: Optional[int] = N
     app = rademacher_projection(app_rank, w.d) if with_app_proj else None
     return Problem(w, np.ascontiguousarray(hidden), np.ascontiguousarray(text_q),
                    np.ascontiguousarray(vis_k), pos, np.ascontiguousarray(probe), app, w.k)
+
+
+@dataclasses.dataclass
+class HistView:
+    """One completed historical message view of a problem (the residual
+    states entering an earlier block, that block's queries and keys, and its
+    folded value probe)."""
+    hidden: np.ndarray      # [B][N][d] float32
+    text_q: np.ndarray      # [B][T][Hq][dh] float32
+    vis_k: np.ndarray       # [B][N][Hkv][dh] float32
+    probe: np.ndarray       # [Hq][r][d] float32
+
+
+def make_history(prob: Problem, n_views: int = 2) -> list:
+    """Historical views of a problem, view v drawn from its own stream
+    (SeedSequence(seed).spawn(...) children past the batch's): states one and
+    two blocks earlier differ from the boundary's by a residual update,
+    h_v = h - 0.25 (v + 1) eps; queries keep most of the boundary queries,
+    q_v = 0.8 q + 0.6 eps; keys come from the view's states through the
+    view's own key map W_K,v ~ N(0, 1/d); the folded probe G_v ~ N(0, 1/d).
+    bf16 workloads are rounded like the boundary tensors."""
+    w = prob.workload
+    kids = np.random.SeedSequence(w.seed).spawn(w.batch + n_views)[w.batch:]
+    views = []
+    for v in range(n_views):
+        rng = np.random.Generator(np.random.PCG64(kids[v]))
+        probe = _normal(rng, (w.hq, prob.probe.shape[1], w.d), 1.0 / np.sqrt(w.d))
+        wk = _normal(rng, (w.d, w.hkv * w.dh), 1.0 / np.sqrt(w.d))
+        h = prob.hidden - _normal(rng, prob.hidden.shape, 0.25 * (v + 1))
+        q = np.float32(0.8) * prob.text_q + _normal(rng, prob.text_q.shape, 0.6)
+        k = np.einsum("bnd,de->bne", h, wk).reshape(w.batch, w.n, w.hkv, w.dh).astype(np.float32)
+        if w.dtype == "bf16":
+            h, q, k, probe = round_bf16(h), round_bf16(q), round_bf16(k), round_bf16(probe)
+        views.append(HistView(np.ascontiguousarray(h, np.float32), np.ascontiguousarray(q, np.float32),
+                              np.ascontiguousarray(k, np.float32), np.ascontiguousarray(probe, np.float32)))
+    return views

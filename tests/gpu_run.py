@@ -8,17 +8,20 @@ from paper_2608_02134_amd import binding, synth
 from paper_2608_02134_amd.binding import from_device, make_pruner, to_device  # noqa: F401
 
 
-def run(prob: synth.Problem, torch, k=None, trace=True, nonvis=None, pruner=None, **overrides):
-    """One gmc_prune_ex call; returns (list of per-problem dicts, pruner)."""
+def run(prob: synth.Problem, torch, k=None, trace=True, nonvis=None, pruner=None, hist=None, **overrides):
+    """One gmc_prune_ex call (gmc_prune_views with historical views, a list of
+    synth.HistView); returns (list of per-problem dicts, pruner)."""
     w = prob.workload
-    pr = pruner or make_pruner(prob, torch, **overrides)
+    pr = pruner or make_pruner(prob, torch, hist=hist, **overrides)
     hid = to_device(prob.hidden, w.dtype, torch)
     q = to_device(prob.text_q, w.dtype, torch)
     kk = to_device(prob.vis_k, w.dtype, torch)
     pos = torch.from_numpy(prob.pos3d).cuda()
     nv = None if nonvis is None else torch.from_numpy(np.ascontiguousarray(nonvis, np.float32)).cuda()
     kreq = prob.k if k is None else k
-    res = pr.prune(hid, q, kk, pos, kreq, nonvis_lse=nv, trace=trace)
+    hv = None if not hist else [(to_device(v.hidden, w.dtype, torch), to_device(v.text_q, w.dtype, torch),
+                                 to_device(v.vis_k, w.dtype, torch)) for v in hist]
+    res = pr.prune(hid, q, kk, pos, kreq, nonvis_lse=nv, trace=trace, hist=hv)
     torch.cuda.synchronize()
     outs = []
     for b in range(w.batch):

@@ -206,7 +206,7 @@ def bf16_round(a: np.ndarray) -> np.ndarray:
 
 
 def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcParams = O.GmcParams(),
-                  app_proj=None, nonvis=None, probe_bias=None) -> FollowReport:
+                  app_proj=None, nonvis=None, probe_bias=None, hist=()) -> FollowReport:
     """Full follow-mode check of one problem.  `gpu` holds numpy arrays:
     out_hidden, out_pos, out_idx and, from the trace, round_pool, round_batch,
     assign, and optionally client, omega, ebar, stats."""
@@ -220,7 +220,7 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
         assert np.array_equal(gpu["out_pos"], pos)
         assert np.array_equal(np.asarray(gpu["out_hidden"], np.float64), h)
         return rep
-    cl = O.build_clients(h, q, k, pos, probe, p, app_proj, nonvis, probe_bias)
+    cl = O.build_clients(h, q, k, pos, probe, p, app_proj, nonvis, probe_bias, hist)
     cbar = cl["cbar"]
     if gpu.get("client") is not None:
         rel = {}

@@ -30,9 +30,10 @@ def _check_all(prob, outs, **kw):
     reps = []
     for b, g in enumerate(outs):
         nv = kw.get("nonvis")
+        hist = [dict(hidden=v.hidden[b], q=v.text_q[b], k=v.vis_k[b], probe=v.probe) for v in kw.get("hist", [])]
         rep = check_problem(prob.hidden[b], prob.text_q[b], prob.vis_k[b], prob.pos3d[b], prob.probe,
                             kw.get("k", prob.k), g, w.dtype, kw.get("params", O.GmcParams()),
-                            prob.app_proj, None if nv is None else nv[b])
+                            prob.app_proj, None if nv is None else nv[b], hist=hist)
         reps.append(rep)
         print(f"  problem {b}: {rep}", flush=True)
     return reps
@@ -295,5 +296,57 @@ def test_debug_scan_and_certificate_flags():
         assert dg["has_certificate"] == 1
         assert np.array_equal(outs2[0]["out_hidden"], outs[0]["out_hidden"])
         assert dg["q"] == outs[0]["diag"]["q"] and dg["c_b"] == outs[0]["diag"]["c_b"]
+    finally:
+        pr.close()
+
+
+HIST_CASES = {
+    # the Qwen2.5-VL-7B boundary with two completed views (Table cond-config)
+    "qwen_full_2views": dict(name="qwen"),
+    "qwen_ragged_2views": dict(name="qwen", grid=(1, 20, 21), t=24, k=83),
+    "batch_1view": dict(name="batch16", batch=3, grid=(1, 24, 24), t=16, k=96),
+}
+
+
+@pytest.mark.parametrize("case", list(HIST_CASES))
+def test_historical_views(case):
+    """App. H native message clients with completed historical views: each
+    view's grounded rows, head patterns over the views, current-view energy."""
+    spec = dict(HIST_CASES[case])
+    prob = synth.make_problem(**spec)
+    hist = synth.make_history(prob, 1 if case.endswith("1view") else 2)
+    _announce(f"views {case}", prob)
+    outs, pr = run(prob, torch, hist=hist)
+    pr.close()
+    reps = _check_all(prob, outs, hist=hist)
+    m1 = prob.workload.hq * prob.workload.t
+    assert outs[0]["client"].shape[0] == (1 + len(hist)) * m1 + prob.workload.n + 256
+    assert reps[0].rounds > 0
+
+
+def test_historical_views_without_mass():
+    # history mass 0: the views' rows carry nothing and the operator is the
+    # single-view one (checked through the followed oracle at hist_mass = 0,
+    # which the CPU pins tie to the single-view oracle)
+    prob = synth.make_problem("qwen", grid=(1, 20, 21), t=24, k=83)
+    hist = synth.make_history(prob, 2)
+    _announce("views, history mass 0", prob)
+    outs, pr = run(prob, torch, hist=hist, hist_mass=0.0)
+    pr.close()
+    _check_all(prob, outs, hist=hist, params=O.GmcParams(hist_mass=0.0))
+    m1 = prob.workload.hq * prob.workload.t
+    assert np.all(outs[0]["client"][m1:3 * m1] == 0.0)
+
+
+def test_historical_views_beyond_capacity():
+    from paper_2608_02134_amd import binding
+    prob = synth.make_problem("qwen", grid=(1, 12, 12), t=8, k=20)
+    hist = synth.make_history(prob, 2)
+    _announce("views capacity", prob)
+    outs, pr = run(prob, torch, hist=hist[:1], trace=False)
+    try:
+        with pytest.raises(binding.GmcError) as ei:
+            run(prob, torch, hist=hist, pruner=pr, trace=False)
+        assert ei.value.code == binding.GMC_ERR_CAPACITY
     finally:
         pr.close()
