@@ -54,7 +54,7 @@ __all__ = [
     "assign_population", "population_weights", "transport", "compact",
     "gmc_single", "gmc", "prune_rounds", "index_map", "compact_sequence",
     "gather_cache", "head_pattern", "head_weights_from_pattern", "view_mass",
-    "message_view",
+    "message_view", "image_seeds",
 ]
 
 
@@ -118,6 +118,12 @@ READINGS = {
     "R12": "farthest-first picks min(4, active heads) centres; ties to the "
            "earliest centre; empty clusters are dropped",
     "R13": "ties in every ranking go to the lower source index",
+    "R15": "multi-image prompts: image ids per token; K = min(N, max(K_r, I)); "
+           "S_0 = one largest-singleton-gain token per image (ties to the lower "
+           "index); every image has its own 16 x 16 landmarks on its own grid "
+           "(M_S = 256 I) and its appearance clients cover its own tokens; "
+           "assignment and the gap delta use the image's carriers; the exact "
+           "appearance bank only (N <= 4096)",
     "R14": "historical views: the message mass beta_msg splits into the current "
            "view's (1 - hist_mass) beta_msg and hist_mass beta_msg shared equally "
            "by the historical views (0.5 / 0.5 with two views: 0.5, 0.25, 0.25); "
@@ -312,9 +318,14 @@ def _row_softmax(logits: np.ndarray) -> np.ndarray:
     return ex / ex.sum(axis=1, keepdims=True)
 
 
-def appearance_bank(x: np.ndarray, p: GmcParams) -> np.ndarray:
-    """P^V_m(i) = softmax_i(x_m . x_i / tau_v), one client per token."""
-    return _row_softmax((x @ x.T) / p.tau_v)
+def appearance_bank(x: np.ndarray, p: GmcParams, img: Optional[np.ndarray] = None) -> np.ndarray:
+    """P^V_m(i) = softmax_i(x_m . x_i / tau_v), one client per token; with
+    image ids, each client's distribution covers its own image's tokens
+    (App. H: appearance and spatial rows are restricted to their image)."""
+    logits = (x @ x.T) / p.tau_v
+    if img is not None:
+        logits = np.where(img[:, None] == img[None, :], logits, -np.inf)
+    return _row_softmax(logits)
 
 
 def appearance_bank_bounded(h: np.ndarray, proj: np.ndarray, p: GmcParams):
@@ -328,24 +339,40 @@ def appearance_bank_bounded(h: np.ndarray, proj: np.ndarray, p: GmcParams):
     return _row_softmax((y[clients] @ y.T) / p.tau_v), clients
 
 
-def spatial_coordinates(pos: np.ndarray) -> np.ndarray:
-    """Original-grid (h, w) mapped to cell centres in [0,1]^2 (reading R6)."""
+def spatial_coordinates(pos: np.ndarray, img: Optional[np.ndarray] = None) -> np.ndarray:
+    """Original-grid (h, w) mapped to cell centres in [0,1]^2 (reading R6),
+    over each image's own grid when image ids are given."""
     hh = pos[:, 1].astype(np.float64)
     ww = pos[:, 2].astype(np.float64)
-    h0, w0 = hh.min(), ww.min()
-    gh, gw = hh.max() - h0 + 1.0, ww.max() - w0 + 1.0
-    return np.stack([(hh - h0 + 0.5) / gh, (ww - w0 + 0.5) / gw], axis=1)
+    if img is None:
+        img = np.zeros(pos.shape[0], dtype=np.int64)
+    out = np.empty((pos.shape[0], 2))
+    for g in np.unique(img):
+        sel = img == g
+        h0, w0 = hh[sel].min(), ww[sel].min()
+        gh, gw = hh[sel].max() - h0 + 1.0, ww[sel].max() - w0 + 1.0
+        out[sel, 0] = (hh[sel] - h0 + 0.5) / gh
+        out[sel, 1] = (ww[sel] - w0 + 0.5) / gw
+    return out
 
 
-def spatial_bank(pos: np.ndarray, p: GmcParams) -> np.ndarray:
+def spatial_bank(pos: np.ndarray, p: GmcParams, img: Optional[np.ndarray] = None) -> np.ndarray:
     """P^S_ab(i) = softmax_i(-||p_i - l_ab||^2 / tau_s) around the L x L
-    landmarks l_ab = ((a+.5)/L, (b+.5)/L); row index a*L + b."""
-    pc = spatial_coordinates(pos)
+    landmarks l_ab = ((a+.5)/L, (b+.5)/L); row index a*L + b.  With image ids
+    every image has its own L x L landmarks on its own grid, and each such
+    row covers that image's tokens (Eq. cond-aux-clients: 1[I_i = I_m]);
+    row index g L^2 + a L + b for image g."""
+    pc = spatial_coordinates(pos, img)
     grid = (np.arange(p.landmarks) + 0.5) / p.landmarks
     la, lb = np.meshgrid(grid, grid, indexing="ij")
     land = np.stack([la.ravel(), lb.ravel()], axis=1)
     d2 = np.sum((land[:, None, :] - pc[None, :, :]) ** 2, axis=2)
-    return _row_softmax(-d2 / p.tau_s)
+    if img is None:
+        return _row_softmax(-d2 / p.tau_s)
+    rows = []
+    for g in range(int(img.max()) + 1):
+        rows.append(_row_softmax(np.where((img == g)[None, :], -d2 / p.tau_s, -np.inf)))
+    return np.concatenate(rows, axis=0)
 
 
 # ----------------------------------------------------------------------------
@@ -474,14 +501,18 @@ def select_support(cbar: np.ndarray, k: int, b: int, p: GmcParams, seed_set=()):
 # ----------------------------------------------------------------------------
 # Population assignment (Sec. 3.4; Eq. cond-assignment, cond-population-gate)
 # ----------------------------------------------------------------------------
-def assignment_gaps(x: np.ndarray, support: np.ndarray):
-    """cos_ij = x_i . x_j for j in S and delta_i = best - second best
-    (delta = 0 when S has one member)."""
+def assignment_gaps(x: np.ndarray, support: np.ndarray, img: Optional[np.ndarray] = None):
+    """cos_ij = x_i . x_j for j in S (-inf for j in another image: S_i holds
+    the image-compatible carriers) and delta_i = best - second best
+    compatible cosine (delta = 0 when S_i has one member)."""
     cos = x @ x[support].T                                      # [N][K]
+    if img is not None:
+        cos = np.where(img[:, None] == img[support][None, :], cos, -np.inf)
     if support.size < 2:
         return cos, np.zeros(x.shape[0])
     top2 = -np.sort(-cos, axis=1)[:, :2]
-    return cos, top2[:, 0] - top2[:, 1]
+    delta = np.where(np.isfinite(top2[:, 1]), top2[:, 0] - top2[:, 1], 0.0)
+    return cos, delta
 
 
 def separability_gate(delta: np.ndarray, discarded: np.ndarray, p: GmcParams) -> float:
@@ -497,12 +528,14 @@ def ambiguity_gate(delta: np.ndarray, p: GmcParams) -> np.ndarray:
     return np.exp(-((delta / p.amb_margin) ** p.amb_p))
 
 
-def assign_population(x: np.ndarray, pc: np.ndarray, support: np.ndarray, p: GmcParams):
-    """pi(i) = argmax_(j in S) cos_ij + 0.5 s_x g_i exp(-||p_i - p_j||^2/tau_s);
-    ties to the lower source index; selected tokens represent themselves."""
+def assign_population(x: np.ndarray, pc: np.ndarray, support: np.ndarray, p: GmcParams,
+                      img: Optional[np.ndarray] = None):
+    """pi(i) = argmax_(j in S_i) cos_ij + 0.5 s_x g_i exp(-||p_i - p_j||^2/tau_s)
+    over the image-compatible carriers S_i; ties to the lower source index;
+    selected tokens represent themselves."""
     n = x.shape[0]
     sup = np.sort(np.asarray(support, dtype=np.int64))
-    cos, delta = assignment_gaps(x, sup)
+    cos, delta = assignment_gaps(x, sup, img)
     discarded = np.ones(n, dtype=bool)
     discarded[sup] = False
     sx, dbar = separability_gate(delta, discarded, p)
@@ -512,7 +545,9 @@ def assign_population(x: np.ndarray, pc: np.ndarray, support: np.ndarray, p: Gmc
     pi = sup[np.argmax(kappa, axis=1)]                          # first max = lowest index
     pi[sup] = sup
     srt = -np.sort(-kappa, axis=1)
-    kmargin = srt[:, 0] - srt[:, 1] if sup.size > 1 else np.full(n, np.inf)
+    with np.errstate(invalid="ignore"):
+        kmargin = srt[:, 0] - srt[:, 1] if sup.size > 1 else np.full(n, np.inf)
+    kmargin = np.where(np.isnan(kmargin), np.inf, kmargin)
     kmargin[sup] = np.inf
     return dict(pi=pi, sx=sx, dbar=dbar, delta=delta, g=g, kappa_margin=kmargin,
                 cos=cos, kappa=kappa, support=sup)
@@ -632,12 +667,27 @@ def message_view(h, q, k, probe, p: GmcParams, nonvis_lse=None, probe_bias=None)
                 gram=head_pattern_gram(a, z, sigma), abar=e.reshape(hq, -1).mean(axis=1))
 
 
+def image_seeds(cbar: np.ndarray, img: np.ndarray) -> np.ndarray:
+    """S_0 of a multi-image prompt: in every image the token of largest
+    singleton gain u_i = F({i}) = sum_m Cbar_mi, ties to the lower index
+    (App. H "Batched complementary support")."""
+    u = cbar.sum(axis=0)
+    seeds = []
+    for g in range(int(img.max()) + 1):
+        members = np.flatnonzero(img == g)
+        seeds.append(int(members[np.argmax(u[members])]))
+    return np.asarray(seeds, dtype=np.int64)
+
+
 def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=None, probe_bias=None,
-                  hist=()):
+                  hist=(), img=None):
     """Steps 2 of Algorithm 1: the three client banks and all message-side
     quantities.  `hist` lists completed historical message views, each a dict
     of its own hidden, q, k, probe and optionally nonvis_lse, probe_bias
-    (App. H native message clients).  Returns a dict of intermediates."""
+    (App. H native message clients).  `img` gives each token's image (ids
+    0..I-1, every id present) for a multi-image prompt: appearance and
+    spatial rows then stay within their image (reading R15).  Returns a dict
+    of intermediates."""
     h = np.asarray(h, np.float64)
     n = h.shape[0]
     t = q.shape[0]
@@ -659,13 +709,15 @@ def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=N
         omega, centres, clus = np.zeros(hq), [], -np.ones(hq, dtype=np.int64)
         ebar, en = np.ones(n), np.zeros(n)
     bounded = n > p.bounded_threshold_n
+    if img is not None and (int(img.max()) + 1 > 1) and bounded:
+        raise ValueError("multi-image prompts use the exact appearance bank (reading R15)")
     if bounded:
         if app_proj is None:
             raise ValueError("bounded appearance bank needs the projection matrix")
         pv, app_clients = appearance_bank_bounded(h, app_proj, p)
     else:
-        pv, app_clients = appearance_bank(x, p), np.arange(n)
-    ps = spatial_bank(pos, p)
+        pv, app_clients = appearance_bank(x, p, img), np.arange(n)
+    ps = spatial_bank(pos, p, img)
     cbar, banks = client_matrix(cur["pg"], cur["active"], omega, nu, pv, ps, p,
                                 [v["pg"] for v in views], [v["active"] for v in views], mass)
     return dict(norm=norm, x=x, rms=rms, xt=xt, z=cur["z"], sigma=cur["sigma"], a=cur["a"], e=cur["e"],
@@ -673,7 +725,7 @@ def build_clients(h, q, k, pos, probe, p: GmcParams, app_proj=None, nonvis_lse=N
                 pattern=pattern, view_mass=mass, hist_views=views, omega=omega, centres=centres,
                 clusters=clus, nu=nu, ebar=ebar, energy=en, pv=pv, ps=ps,
                 app_clients=app_clients, cbar=cbar, banks=banks, bounded=bounded,
-                pc=spatial_coordinates(pos))
+                pc=spatial_coordinates(pos, img), img=img)
 
 
 def bank_saturation(cbar: np.ndarray, banks: np.ndarray, support) -> dict:
@@ -696,20 +748,29 @@ def bank_saturation(cbar: np.ndarray, banks: np.ndarray, support) -> dict:
 
 
 def gmc_single(h, q, k, pos, probe, k_req: int, p: GmcParams = GmcParams(),
-               app_proj=None, nonvis_lse=None, keep_intermediates: bool = False, probe_bias=None, hist=()):
+               app_proj=None, nonvis_lse=None, keep_intermediates: bool = False, probe_bias=None, hist=(),
+               img=None):
     """One problem end to end: budget, clients, selection, assignment,
     transport and compaction.  Returns out_hidden (fp64, before the cast to
     the residual dtype), out_pos, out_idx and diagnostics."""
     h = np.asarray(h, np.float64)
     n = h.shape[0]
-    kk = realized_budget(n, k_req)
+    if img is not None:
+        img = np.asarray(img, dtype=np.int64)
+        n_img = int(img.max()) + 1
+        if n_img == 1:
+            img = None
+    else:
+        n_img = 1
+    kk = realized_budget(n, k_req, n_img)
     if kk == n:
         return dict(out_hidden=h.copy(), out_pos=np.asarray(pos).copy(),
                     out_idx=np.arange(n, dtype=np.int64), identity=True, k=kk)
-    cl = build_clients(h, q, k, pos, probe, p, app_proj, nonvis_lse, probe_bias, hist)
+    cl = build_clients(h, q, k, pos, probe, p, app_proj, nonvis_lse, probe_bias, hist, img)
     b = p.batch_b_bounded if cl["bounded"] else p.batch_b
-    sel = select_support(cl["cbar"], kk, b, p)
-    asg = assign_population(cl["x"], cl["pc"], sel["order"], p)
+    seeds = image_seeds(cl["cbar"], img) if img is not None else ()
+    sel = select_support(cl["cbar"], kk, b, p, seeds)
+    asg = assign_population(cl["x"], cl["pc"], sel["order"], p, img)
     m = population_weights(cl["ebar"], asg["sx"], p)
     tr = transport(h, asg["pi"], sel["order"], m, p)
     idx, out_h, out_pos = compact(tr["support"], tr["out"], np.asarray(pos))
