@@ -62,6 +62,7 @@ extern "C" {
 #define GMC_STATUS_BANK_TIMEOUT 2u   /* the bank stream's start gate or its join     */
 #define GMC_STATUS_NONFINITE 4u      /* debug mode: a non-finite client energy, row
                                         weight or output value                      */
+/* GMC_STATUS_INPUT (8): see gmc_prune_full                                           */
 
 #define GMC_F32 0
 #define GMC_BF16 1
@@ -142,6 +143,8 @@ typedef struct gmc_config {
                                    view's block); required iff
                                    max_hist_views > 0 (caller-owned, kept)  */
   const float* value_probe_bias_hist; /* [max_hist_views][Hq][r] fp32 or NULL */
+  /* multi-image prompts (Sec. 3.1; App. H), used by gmc_prune_full          */
+  int32_t max_images;           /* images per problem, 1..GMC_MAX_IMAGES (0 = 1) */
 } gmc_config;
 
 /*
@@ -305,6 +308,46 @@ typedef struct gmc_view {
 int gmc_prune_views(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
                     int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
                     const float* nonvis_lse, int64_t n_hist, const gmc_view* hist, const gmc_trace* trace);
+
+/*
+ * gmc_prune_full - every option at once: gmc_prune_views plus multi-image
+ * prompts.  image_id [B][N] int32 (device) gives each visual token's image,
+ * ids 0..n_images-1 with every id present in every problem; NULL (or
+ * n_images = 1) means one image.  With I = n_images > 1 (Sec. 3.1 totality
+ * rule; App. H "Batched complementary support", "Appearance and spatial
+ * clients"; Eq. cond-aux-clients; Eq. cond-assignment):
+ *   - the realised budget is K = min{N, max{K_r, I}} (gmc_realized_budget);
+ *   - the support starts with one token per image, the one of largest
+ *     singleton gain F({i}) (ties to the lower index), then the batched
+ *     rounds run until |S| = K (ceil((K - I) / b) rounds);
+ *   - appearance clients cover their own image's tokens, and every image has
+ *     its own L x L spatial landmarks on its own grid (M_S = L^2 I rows);
+ *   - each token is assigned among its own image's carriers, and the gap
+ *     delta is 0 for a token whose image has one carrier.
+ * Multi-image calls use the exact appearance bank (N <= bounded_threshold_n,
+ * else GMC_ERR_ARG).  Ids outside [0, I) are clamped and an image without
+ * tokens gets the lowest unselected token as its seed; both are reported by
+ * the GMC_STATUS_INPUT bit.  Other arguments as gmc_prune_views.
+ * Errors: as gmc_prune_views; GMC_ERR_CAPACITY for I above max_images.
+ */
+#define GMC_MAX_IMAGES 64
+#define GMC_STATUS_INPUT 8u   /* image ids out of range or an image without tokens */
+int gmc_prune_full(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+                   const int32_t* image_id, int64_t n_images, int64_t N, int64_t T, int64_t K, void* out_hidden,
+                   int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse, int64_t n_hist,
+                   const gmc_view* hist, const gmc_trace* trace);
+
+/* Realised budget K = min{N, max{K_r, I}} for I images (Sec. 3.1); 0 if N < 1
+ * or I < 1.  Host-only. */
+int64_t gmc_realized_budget(int64_t N, int64_t K_req, int64_t n_images);
+
+/*
+ * Per-problem trace sizes of a gmc_prune_full call shape: selection rounds
+ * (after the image seeds), pool capacity, batch capacity and client rows M
+ * (every view's grounded rows, appearance, L^2 I spatial rows).
+ */
+int gmc_trace_dims_full(int64_t N, int64_t T, int64_t K, int64_t n_hist, int64_t n_images, int64_t* rounds,
+                        int64_t* pool_cap, int64_t* batch_cap, int64_t* m_rows);
 
 /* Realised budget K = min{N, max{K_r, 1}} (Sec. 3.1); 0 if N < 1. Host-only. */
 int64_t gmc_realized_k(int64_t N, int64_t K_req);

@@ -24,6 +24,8 @@ GMC_STATIC_SCRATCH_BYTES = 64 << 20
 GMC_F32, GMC_BF16 = 0, 1
 GMC_STATS = 15
 GMC_MAX_HIST_VIEWS = 3
+GMC_MAX_IMAGES = 64
+GMC_STATUS_INPUT = 8
 GMC_MAX_GATHER_TENSORS = 64
 
 _i32, _f32, _i64, _vp = ctypes.c_int32, ctypes.c_float, ctypes.c_int64, ctypes.c_void_p
@@ -55,6 +57,7 @@ class GmcConfig(ctypes.Structure):
         ("value_probe_bias", _vp),
         ("max_hist_views", _i32), ("hist_mass", _f32),
         ("value_probe_hist", _vp), ("value_probe_bias_hist", _vp),
+        ("max_images", _i32),
     ]
 
 
@@ -92,6 +95,11 @@ SIGNATURES = {
                                     ctypes.POINTER(GmcTrace)]),
     "gmc_prune_views": (ctypes.c_int, [_i64, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _i64,
                                        ctypes.POINTER(GmcView), ctypes.POINTER(GmcTrace)]),
+    "gmc_prune_full": (ctypes.c_int, [_i64, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp, _vp, _vp,
+                                      _i64, ctypes.POINTER(GmcView), ctypes.POINTER(GmcTrace)]),
+    "gmc_realized_budget": (_i64, [_i64, _i64, _i64]),
+    "gmc_trace_dims_full": (ctypes.c_int, [_i64, _i64, _i64, _i64, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
+                                           ctypes.POINTER(_i64), ctypes.POINTER(_i64)]),
     "gmc_realized_k": (_i64, [_i64, _i64]),
     "gmc_trace_dims": (ctypes.c_int, [_i64, _i64, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
                                       ctypes.POINTER(_i64), ctypes.POINTER(_i64)]),
@@ -173,6 +181,26 @@ def gmc_prune_views(b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden, out_po
     tr = ctypes.byref(trace) if trace is not None else None
     return lib().gmc_prune_views(b, hidden, text_q, vis_k, pos3d, n, t, k, out_hidden, out_pos, out_idx,
                                  nonvis_lse, nh, arr, tr)
+
+
+def gmc_prune_full(b, hidden, text_q, vis_k, pos3d, image_id, n_images, n, t, k, out_hidden, out_pos, out_idx,
+                   nonvis_lse=None, hist_views=(), trace: Optional[GmcTrace] = None) -> int:
+    nh = len(hist_views)
+    arr = (GmcView * max(nh, 1))(*hist_views)
+    tr = ctypes.byref(trace) if trace is not None else None
+    return lib().gmc_prune_full(b, hidden, text_q, vis_k, pos3d, image_id, n_images, n, t, k, out_hidden,
+                                out_pos, out_idx, nonvis_lse, nh, arr, tr)
+
+
+def gmc_realized_budget(n: int, k_req: int, n_images: int) -> int:
+    return int(lib().gmc_realized_budget(n, k_req, n_images))
+
+
+def gmc_trace_dims_full(n: int, t: int, k: int, n_hist: int, n_images: int):
+    vals = [_i64() for _ in range(4)]
+    code = lib().gmc_trace_dims_full(n, t, k, n_hist, n_images, *[ctypes.byref(v) for v in vals])
+    _check(code, "gmc_trace_dims_full")
+    return tuple(int(v.value) for v in vals)
 
 
 def gmc_realized_k(n: int, k_req: int) -> int:
@@ -429,9 +457,12 @@ class Pruner:
     def trace_dims(self, n, t, k):
         return gmc_trace_dims(n, t, k)
 
-    def prune(self, hidden, text_q, vis_k, pos3d, k, nonvis_lse=None, trace: bool = False, hist=None):
+    def prune(self, hidden, text_q, vis_k, pos3d, k, nonvis_lse=None, trace: bool = False, hist=None,
+              image_id=None, n_images: int = 1):
         """hist: optional list of historical views, each (hidden, text_q,
-        vis_k[, nonvis_lse]) shaped like the current view's tensors."""
+        vis_k[, nonvis_lse]) shaped like the current view's tensors;
+        image_id: optional int32 [B][N] device tensor of image ids in
+        [0, n_images) for a multi-image prompt."""
         torch = self.torch
         b, n, t = check_prune_inputs(self.cfg, self.dtype, hidden, text_q, vis_k, pos3d, nonvis_lse)
         hist = list(hist or [])
@@ -448,17 +479,22 @@ class Pruner:
                 raise ValueError(f"historical view {i}: {e}") from None
             views.append(GmcView(hv[0].data_ptr(), hv[1].data_ptr(), hv[2].data_ptr(),
                                  None if hv[3] is None else hv[3].data_ptr()))
+        if image_id is not None:
+            if image_id.dtype != torch.int32 or tuple(image_id.shape) != (b, n) or not image_id.is_contiguous() \
+                    or image_id.device != hidden.device:
+                raise ValueError(f"image_id must be a contiguous int32 [B][N] = ({b}, {n}) tensor on hidden's device")
+        multi = image_id is not None and n_images > 1
         d = hidden.shape[2]
-        kk = gmc_realized_k(n, k)
+        kk = gmc_realized_budget(n, k, n_images if image_id is not None else 1)
         dev = hidden.device
         out_h = torch.empty((b, kk, d), dtype=hidden.dtype, device=dev)
         out_p = torch.empty((b, kk, 3), dtype=torch.int32, device=dev)
         out_i = torch.empty((b, kk), dtype=torch.int32, device=dev)
         tr, bufs = None, {}
         if trace:
-            rounds, pool_cap, bcap, m_rows = gmc_trace_dims(n, t, k)
+            rounds, pool_cap, bcap, m_rows = gmc_trace_dims_full(n, t, k, len(views),
+                                                                 n_images if multi else 1)
             hq = self.cfg.n_q_heads
-            m_rows += len(views) * hq * t       # each historical view's grounded rows
             r1 = max(rounds, 1)
             bufs = dict(
                 round_pool=torch.full((b, r1, pool_cap), -1, dtype=torch.int32, device=dev),
@@ -473,7 +509,12 @@ class Pruner:
             tr = GmcTrace(**{key: v.data_ptr() for key, v in bufs.items()})
         _check(gmc_set_stream(torch.cuda.current_stream(dev).cuda_stream), "gmc_set_stream")
         nv = None if nonvis_lse is None else nonvis_lse.data_ptr()
-        if views:
+        if multi:
+            code = gmc_prune_full(b, hidden.data_ptr(), text_q.data_ptr() if t > 0 else None,
+                                  vis_k.data_ptr(), pos3d.data_ptr(), image_id.data_ptr(), n_images, n, t, k,
+                                  out_h.data_ptr(), out_p.data_ptr(), out_i.data_ptr(), nv, views, tr)
+            _check(code, "gmc_prune_full")
+        elif views:
             code = gmc_prune_views(b, hidden.data_ptr(), text_q.data_ptr() if t > 0 else None,
                                    vis_k.data_ptr(), pos3d.data_ptr(), n, t, k, out_h.data_ptr(),
                                    out_p.data_ptr(), out_i.data_ptr(), nv, views, tr)

@@ -23,7 +23,7 @@ using namespace gmc;
 namespace {
 
 struct Capacity {
-  int B, N, T, K, hq, hr, mv, m, ldM, pool_cap, bmax, ldK, rank;
+  int B, N, T, K, I, hq, hr, mv, m, ldM, pool_cap, bmax, ldK, rank;
   int cert_rounds;   // selection rounds the certificate buffers hold
   bool bounded_possible;
 };
@@ -151,6 +151,8 @@ int validate_config(const gmc_config* c) {
     return fail(GMC_ERR_ARG, "value_probe_hist is NULL but max_hist_views=%d", c->max_hist_views);
   if (!(c->hist_mass >= 0.f && c->hist_mass <= 1.f))
     return fail(GMC_ERR_ARG, "hist_mass must be in [0, 1]");
+  if (c->max_images < 0 || c->max_images > GMC_MAX_IMAGES)
+    return fail(GMC_ERR_ARG, "max_images=%d must be in [0, %d]", c->max_images, GMC_MAX_IMAGES);
   if (c->max_n > c->bounded_threshold_n) {
     if (!c->app_projection) return fail(GMC_ERR_ARG, "app_projection is NULL but max_n exceeds the bounded threshold");
     if (c->app_rank < 64 || c->app_rank % 64 != 0 || c->app_rank > 1024)
@@ -166,7 +168,7 @@ struct Plan {
   long long s_n, s_z, s_zp, s_sig, s_ell, s_E, s_m, s_apart, s_gpart, s_e2, s_om, s_eb, s_pc, s_bd, s_y, s_cl,
       s_cov, s_sel, s_ord, s_pool, s_spart, s_bat, s_slot, s_sup, s_cos, s_del, s_ftag, s_gate,
       s_pi, s_st, s_keys, s_u, s_cnt, s_rstat, s_lstat, s_tu, s_ts, s_tc, s_lpart, s_lcnt;
-  long long s_gpart1, s_n2h;
+  long long s_gpart1, s_n2h, s_img, s_imgcnt;
   long long s_cgain, s_cscore, s_cpool, s_cbat, s_cpart, s_cert, s_dstat;
 };
 
@@ -182,7 +184,8 @@ Plan make_plan(const gmc_config& c) {
   k.bounded_possible = c.max_n > c.bounded_threshold_n;
   k.mv = std::max(std::min(c.max_n, c.bounded_threshold_n),
                   k.bounded_possible ? std::min(c.app_max_clients, c.max_n) : 0);
-  k.m = (1 + c.max_hist_views) * k.hq * k.T + k.mv + c.landmarks * c.landmarks;
+  k.I = std::max(1, c.max_images);
+  k.m = (1 + c.max_hist_views) * k.hq * k.T + k.mv + c.landmarks * c.landmarks * k.I;
   k.ldM = static_cast<int>(round_up(k.m, 4));
   k.bmax = std::max(c.batch_b, k.bounded_possible ? c.batch_b_bounded : 0);
   k.pool_cap = c.pool_mult * k.bmax;
@@ -227,7 +230,9 @@ Plan make_plan(const gmc_config& c) {
   pl.s_u = k.N;
   pl.s_cnt = kCounters;
   pl.s_rstat = 3LL * k.ldM;
-  pl.s_lstat = static_cast<long long>(c.landmarks) * c.landmarks;
+  pl.s_lstat = static_cast<long long>(c.landmarks) * c.landmarks * k.I;
+  pl.s_img = k.N;
+  pl.s_imgcnt = kMaxImages;
   pl.s_tu = 2LL * k.N;
   pl.s_ts = 2 * 64 * cdiv(k.ldM, 64);
   pl.s_tc = 2LL * (k.ldM + kMaxPersist);
@@ -264,7 +269,7 @@ size_t carve(const Plan& pl, char* base, Ws* ws) {
   ws->rowsum = reinterpret_cast<float*>(take(pl.s_m, 4));
   ws->apart_sum = reinterpret_cast<float*>(take(pl.s_apart, 4));
   ws->apart_max = reinterpret_cast<float*>(take(pl.s_apart, 4)); ws->s_apart = pl.s_apart;
-  F(gpart); F(e2); F(n2h);
+  F(gpart); F(e2); F(n2h); I(img); I(imgcnt);
   ws->s_gpart1 = pl.s_gpart1;
   ws->omega = reinterpret_cast<float*>(take(pl.s_om, 4)); ws->s_om = pl.s_om;
   ws->ebar = reinterpret_cast<float*>(take(pl.s_eb, 4)); ws->s_eb = pl.s_eb;
@@ -369,6 +374,7 @@ void gmc_config_default(gmc_config* c) {
   c->batch_b_bounded = 512;
   c->max_hist_views = 0;
   c->hist_mass = 0.5f;
+  c->max_images = 1;
 }
 
 void gmc_free(void) {
@@ -397,6 +403,7 @@ int gmc_init(const gmc_config* cfg) {
   Context* ctx = new Context();
   ctx->cfg = *cfg;
   if (ctx->cfg.max_k == 0) ctx->cfg.max_k = ctx->cfg.max_n;
+  if (ctx->cfg.max_images == 0) ctx->cfg.max_images = 1;
   ctx->pr = make_params(ctx->cfg);
   Plan pl = make_plan(ctx->cfg);
   ctx->cap = pl.cap;
@@ -449,6 +456,11 @@ int gmc_set_stream(void* stream) {
 int64_t gmc_realized_k(int64_t N, int64_t K_req) {
   if (N < 1) return 0;
   return std::min<int64_t>(N, std::max<int64_t>(K_req, 1));
+}
+
+int64_t gmc_realized_budget(int64_t N, int64_t K_req, int64_t n_images) {
+  if (N < 1 || n_images < 1) return 0;
+  return std::min<int64_t>(N, std::max<int64_t>(K_req, n_images));
 }
 
 int gmc_compact_sequence(int64_t B, int64_t L, int64_t vis_start, int64_t N, int64_t K, const int32_t* out_idx,
@@ -550,9 +562,10 @@ int gmc_timing_read(double* total_ms, int64_t* spans, int32_t n) {
 
 namespace {
 
-int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req, Shape* out, int64_t n_hist = 0) {
-  return gmc::resolve_shape(c.cfg, Limits{c.cap.B, c.cap.N, c.cap.T, c.cap.K, c.cfg.max_hist_views}, B, N, T,
-                            K_req, out, n_hist);
+int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req, Shape* out, int64_t n_hist = 0,
+               int64_t n_images = 1) {
+  return gmc::resolve_shape(c.cfg, Limits{c.cap.B, c.cap.N, c.cap.T, c.cap.K, c.cfg.max_hist_views, c.cap.I}, B, N,
+                            T, K_req, out, n_hist, n_images);
 }
 
 }  // namespace
@@ -560,7 +573,7 @@ int make_shape(const Context& c, int64_t B, int64_t N, int64_t T, int64_t K_req,
 namespace gmc {
 
 int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, int64_t T, int64_t K_req,
-                  Shape* out, int64_t n_hist) {
+                  Shape* out, int64_t n_hist, int64_t n_images) {
   if (B < 1) return fail(GMC_ERR_ARG, "batch=%lld must be >= 1", static_cast<long long>(B));
   if (N < 1) return fail(GMC_ERR_ARG, "N=%lld must be >= 1", static_cast<long long>(N));
   if (T < 0) return fail(GMC_ERR_ARG, "T=%lld must be >= 0", static_cast<long long>(T));
@@ -570,7 +583,15 @@ int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, 
   if (n_hist < 0) return fail(GMC_ERR_ARG, "n_hist=%lld must be >= 0", static_cast<long long>(n_hist));
   if (n_hist > cap.H)
     return fail(GMC_ERR_CAPACITY, "n_hist=%lld exceeds max_hist_views=%d", static_cast<long long>(n_hist), cap.H);
-  const int64_t K = gmc_realized_k(N, K_req);
+  if (n_images < 1) return fail(GMC_ERR_ARG, "n_images=%lld must be >= 1", static_cast<long long>(n_images));
+  if (n_images > cap.I)
+    return fail(GMC_ERR_CAPACITY, "n_images=%lld exceeds max_images=%d", static_cast<long long>(n_images), cap.I);
+  if (n_images > N) return fail(GMC_ERR_ARG, "n_images=%lld exceeds N=%lld", static_cast<long long>(n_images),
+                                static_cast<long long>(N));
+  if (n_images > 1 && N > g.bounded_threshold_n)
+    return fail(GMC_ERR_ARG, "multi-image prompts use the exact appearance bank: N=%lld exceeds %d",
+                static_cast<long long>(N), g.bounded_threshold_n);
+  const int64_t K = gmc_realized_budget(N, K_req, n_images);
   Shape s{};
   s.B = static_cast<int>(B);
   s.N = static_cast<int>(N);
@@ -594,12 +615,14 @@ int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, 
   s.mg1 = s.hq * s.T;
   s.mg = s.nviews * s.mg1;
   s.mv = app_rows(g, s.N);
-  s.ms = g.landmarks * g.landmarks;
+  s.nimg = static_cast<int>(n_images);
+  s.nseed = s.nimg > 1 ? s.nimg : 0;
+  s.ms = g.landmarks * g.landmarks * s.nimg;
   s.m = s.mg + s.mv + s.ms;
   s.ldM = static_cast<int>(round_up(s.m, 4));
   s.b = s.bounded ? g.batch_b_bounded : g.batch_b;
   s.pool_cap = g.pool_mult * s.b;
-  s.rounds = (K < N) ? static_cast<int>(cdiv(K, s.b)) : 0;
+  s.rounds = (K < N) ? static_cast<int>(cdiv(K - s.nseed, s.b)) : 0;
   s.ldK = static_cast<int>(round_up(K, 4));
   s.n_app_cblk = static_cast<int>(cdiv(N, 64));
   s.n_head_blk = static_cast<int>(cdiv(N, kHeadTok));
@@ -656,7 +679,7 @@ int check_tensors(const Shape& s, const void* hidden, const void* text_q, const 
 int enqueue_prune(const gmc_config& cfg, const Params& pr0, const Ws& ws, const Shape& s, const PathStreams& ps,
                   int diag, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
                   void* out_hidden, int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse,
-                  const gmc_trace& tr, bool* cert_done, const gmc_view* hist) {
+                  const gmc_trace& tr, bool* cert_done, const gmc_view* hist, const int32_t* image_id) {
   *cert_done = false;
   hipStream_t st = ps.st;
   hipError_t err;
@@ -682,6 +705,13 @@ int enqueue_prune(const gmc_config& cfg, const Params& pr0, const Ws& ws, const 
     err = launch_identity(s, hidden, pos3d, out_hidden, out_pos, out_idx, st);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "identity copy: %s", hipGetErrorString(err));
     return GMC_OK;
+  }
+  // a multi-image call first copies the (clamped) image ids and counts each
+  // image's tokens; every later kernel, the bank stream's included, runs
+  // after it
+  if (s.nimg > 1) {
+    err = launch_image_prep(s, ws, image_id, st);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "image ids: %s", hipGetErrorString(err));
   }
   // per-call reset and row norms (one kernel), then the bank kernels on the
   // side stream while the message kernels run on the caller's stream (they
@@ -738,6 +768,11 @@ int enqueue_prune(const gmc_config& cfg, const Params& pr0, const Ws& ws, const 
     if (!so.gains) so.gains = ws.cgain;
     if (!so.scores) so.scores = ws.cscore;
   }
+  if (s.nimg > 1) {
+    // S_0: the largest singleton gain of every image (after the banks joined)
+    err = launch_image_seeds(s, ws, st);
+    if (err != hipSuccess) return fail(GMC_ERR_HIP, "image seeds: %s", hipGetErrorString(err));
+  }
   bool support_ready = false;
   err = launch_selection(s, pr, ws, so, st, &support_ready);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "selection kernels: %s", hipGetErrorString(err));
@@ -767,12 +802,14 @@ namespace {
 
 int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
         int64_t N, int64_t T, int64_t K, void* out_hidden, int32_t* out_pos, int32_t* out_idx,
-        const float* nonvis_lse, const gmc_trace* trace, int64_t n_hist = 0, const gmc_view* hist = nullptr) {
+        const float* nonvis_lse, const gmc_trace* trace, int64_t n_hist = 0, const gmc_view* hist = nullptr,
+        const int32_t* image_id = nullptr, int64_t n_images = 1) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_prune: no context (call gmc_init first)");
   Context& c = *g_ctx;
+  if (!image_id) n_images = 1;
   Shape s;
-  int rc = make_shape(c, B, N, T, K, &s, n_hist);
+  int rc = make_shape(c, B, N, T, K, &s, n_hist, n_images);
   if (rc != GMC_OK) return rc;
   rc = check_tensors(s, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx, hist);
   if (rc != GMC_OK) return rc;
@@ -803,7 +840,7 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   }
   bool cert = false;
   rc = enqueue_prune(c.cfg, c.pr, c.ws, s, ps, c.diag, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx,
-                     nonvis_lse, tr, &cert, hist);
+                     nonvis_lse, tr, &cert, hist, image_id);
   c.last_cert = cert;
   return rc;
 }
@@ -834,6 +871,28 @@ int gmc_prune_views(int64_t B, const void* hidden, const void* text_q, const voi
                     const float* nonvis_lse, int64_t n_hist, const gmc_view* hist, const gmc_trace* trace) {
   return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nonvis_lse, trace, n_hist,
              hist);
+}
+
+int gmc_prune_full(int64_t B, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
+                   const int32_t* image_id, int64_t n_images, int64_t N, int64_t T, int64_t K, void* out_hidden,
+                   int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse, int64_t n_hist,
+                   const gmc_view* hist, const gmc_trace* trace) {
+  return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nonvis_lse, trace, n_hist,
+             hist, image_id, n_images);
+}
+
+int gmc_trace_dims_full(int64_t N, int64_t T, int64_t K, int64_t n_hist, int64_t n_images, int64_t* rounds,
+                        int64_t* pool_cap, int64_t* batch_cap, int64_t* m_rows) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_trace_dims_full: no context");
+  Shape s;
+  const int rc = make_shape(*g_ctx, 1, N, T, K, &s, n_hist, n_images);
+  if (rc != GMC_OK) return rc;
+  if (rounds) *rounds = s.rounds;
+  if (pool_cap) *pool_cap = s.pool_cap;
+  if (batch_cap) *batch_cap = s.b;
+  if (m_rows) *m_rows = s.m;
+  return GMC_OK;
 }
 
 int gmc_set_diag(int32_t flags) {

@@ -19,6 +19,8 @@ constexpr int kCntStatus = 7;     // device status bits (sticky; cleared from th
 constexpr unsigned kStatusSelect = 1u;    // a hand-off wait of the persistent selection timed out
 constexpr unsigned kStatusBank = 2u;      // the bank stream's gate or join timed out
 constexpr unsigned kStatusNonfinite = 4u; // debug scan: a non-finite value
+constexpr unsigned kStatusInput = 8u;     // image ids out of range / an image without tokens
+constexpr int kMaxImages = 64;            // GMC_MAX_IMAGES
 // Bounded waits of the bank stream, in ticks of the 100 MHz constant clock:
 // the start gate may wait behind everything the caller queued before the
 // call, so it gives up only after 10 s; the join waits for bank kernels that
@@ -38,6 +40,7 @@ struct Shape {
   int hg;                                 // query heads per kv head
   int mg, mv, ms, m;                      // client rows: grounded, appearance, spatial, total
   int nviews, mg1;                        // message views; grounded rows per view (mg = nviews mg1)
+  int nimg, nseed;                        // images; seeds before the rounds (nimg when nimg > 1, else 0)
   int ldM;                                // token-major client matrix: floats per token (multiple of 4, >= m)
   int bounded;                            // 1: bounded appearance bank
   int app_rank;
@@ -82,6 +85,8 @@ struct Ws {
   float* gpart;    long long s_gpart;   // head-Gram partials, per view [views][blk][npairs]
   long long s_gpart1;                   // one view's share of gpart
   float* n2h;      long long s_n2h;     // squared row norms of a historical view's states [N]
+  int* img;        long long s_img;     // image of every token (clamped ids)  [N]
+  int* imgcnt;     long long s_imgcnt;  // tokens per image                    [kMaxImages]
   float* e2;       long long s_e2;      // sum_t nu_t e^2               [hq][N]
   float* omega;    long long s_om;      // head weights                 [kMaxHeads]
   float* ebar;     long long s_eb;      // normalised energy            [N]

@@ -64,6 +64,14 @@ hipError_t launch_certificate(const Shape& sh, const Ws& ws, const SelOut& so, h
 // Debug scan for non-finite client energies, row weights and outputs.
 hipError_t launch_finite_scan(const Shape& sh, const Ws& ws, const void* out_hidden, hipStream_t st);
 
+// Multi-image calls: clamped image ids and per-image token counts.
+hipError_t launch_image_prep(const Shape& sh, const Ws& ws, const int32_t* image_id, hipStream_t st);
+
+// Multi-image calls: S_0, the largest singleton gain F({i}) of every image
+// (ties to the lower index), marked selected, recorded first in the support
+// order, and the coverage b_m(S_0).
+hipError_t launch_image_seeds(const Shape& sh, const Ws& ws, hipStream_t st);
+
 // Clears the device status words of problems [0, nprob).
 hipError_t launch_clear_status(const Ws& ws, int nprob, hipStream_t st);
 

@@ -13,7 +13,7 @@ namespace gmc {
 
 // Capacities a call is checked against.
 struct Limits {
-  int B, N, T, K, H;   // H: historical message views
+  int B, N, T, K, H, I;   // H: historical message views, I: images
 };
 
 // Streams of one call: everything runs on `st`; with `side` set the bank
@@ -41,7 +41,7 @@ size_t carve_workspace(const gmc_config& cfg, char* base, Ws* ws);
 
 // Resolves a call's shape against the limits.
 int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, int64_t T, int64_t K_req,
-                  Shape* out, int64_t n_hist = 0);
+                  Shape* out, int64_t n_hist = 0, int64_t n_images = 1);
 
 // Null pointers and overlapping outputs (historical views: hist[0, n_hist)).
 int check_tensors(const Shape& s, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
@@ -53,6 +53,7 @@ int check_tensors(const Shape& s, const void* hidden, const void* text_q, const 
 int enqueue_prune(const gmc_config& cfg, const Params& pr, const Ws& ws, const Shape& s, const PathStreams& ps,
                   int diag, const void* hidden, const void* text_q, const void* vis_k, const int32_t* pos3d,
                   void* out_hidden, int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse,
-                  const gmc_trace& tr, bool* cert_done, const gmc_view* hist = nullptr);
+                  const gmc_trace& tr, bool* cert_done, const gmc_view* hist = nullptr,
+                  const int32_t* image_id = nullptr);
 
 }  // namespace gmc

@@ -51,11 +51,12 @@ extern "C" int gmc_prune_static(const gmc_config* cfg, int64_t B, const void* hi
   c.max_n = static_cast<int32_t>(N);
   c.max_t = static_cast<int32_t>(T);
   c.max_k = static_cast<int32_t>(gmc_realized_k(N, K));
-  c.max_hist_views = 0;   // no historical views on this entry point
+  c.max_hist_views = 0;   // no historical views and one image on this entry point
+  c.max_images = 1;
   int rc = check_config(&c);
   if (rc != GMC_OK) return rc;
   Shape s;
-  rc = resolve_shape(c, Limits{c.max_batch, c.max_n, c.max_t, c.max_k, 0}, B, N, T, K, &s);
+  rc = resolve_shape(c, Limits{c.max_batch, c.max_n, c.max_t, c.max_k, 0, 1}, B, N, T, K, &s);
   if (rc != GMC_OK) return rc;
   rc = check_tensors(s, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx);
   if (rc != GMC_OK) return rc;

@@ -132,7 +132,9 @@ __global__ void __launch_bounds__(256) gap_kernel(Shape sh, Params pr, Ws ws) {
     top2_step<4>(t1, t2);
     top2_step<2>(t1, t2);
     top2_step<1>(t1, t2);
-    const float delta = (sh.K >= 2) ? t1 - t2 : 0.f;
+    // no second compatible carrier (K = 1, or the token's image has one
+    // carrier and the others read -inf): the gap is 0
+    const float delta = (sh.K >= 2 && t2 > -INFINITY) ? t1 - t2 : 0.f;
     if (lane == 0) ws.delta[p * ws.s_del + i] = delta;
     if (sh.T > 0) {
       // lane h holds head h (at most kMaxHeads of them)

@@ -155,6 +155,16 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
       rsc[i][e] = 1.f / fmaxf(sqrtf(n2[min(row0 + wr * WM + i * 16 + orow + e, sh.N - 1)]), norm_eps);
 #pragma unroll
   for (int j = 0; j < TM; ++j) csc[j] = 1.f / fmaxf(sqrtf(n2[min(col0 + wc * WM + j * 16 + oc, sh.N - 1)]), norm_eps);
+  // several images: a client covers its own image's tokens only
+  int rim[TM][4], cim[TM];
+  const int* img = ws.img + p * ws.s_img;
+  const bool multi = sh.nimg > 1;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rim[i][e] = multi ? img[min(row0 + wr * WM + i * 16 + orow + e, sh.N - 1)] : 0;
+#pragma unroll
+  for (int j = 0; j < TM; ++j) cim[j] = multi ? img[min(col0 + wc * WM + j * 16 + oc, sh.N - 1)] : 0;
   float* E = ws.E + p * ws.s_E;
   const bool diag = I == J;
   float rsum[TM][4], rmax[TM][4], csum[TM], cmax[TM];
@@ -173,7 +183,7 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
         const int r = row0 + wr * WM + i * 16 + orow + e;
         const int c = col0 + wc * WM + j * 16 + oc;
         if (r < sh.N && c < sh.N) {
-          const float v = expf((acc[i][j][e] * rsc[i][e] * csc[j] - 1.f) * inv_tau);
+          const float v = rim[i][e] == cim[j] ? expf((acc[i][j][e] * rsc[i][e] * csc[j] - 1.f) * inv_tau) : 0.f;
           E[static_cast<long long>(c) * sh.ldM + sh.mg + r] = v;           // client r, token c
           rsum[i][e] += v;
           rmax[i][e] = fmaxf(rmax[i][e], v);
@@ -278,11 +288,36 @@ __global__ void __launch_bounds__(256) appearance_alpha_kernel(Shape sh, Params 
 }
 
 // Grid origin/extent of (h, w) and the per-token spatial coordinates,
-// cell centres in [0,1]^2 (temporal id excluded).
+// cell centres in [0,1]^2 (temporal id excluded), over each image's own grid
+// when the prompt has several images.
 __global__ void __launch_bounds__(256) spatial_coords_kernel(Shape sh, Ws ws, const int32_t* pos3d) {
   __shared__ float red[16];
+  __shared__ int bh0[kMaxImages], bh1[kMaxImages], bw0[kMaxImages], bw1[kMaxImages];
   const int p = blockIdx.x;
   const int32_t* pos = pos3d + static_cast<long long>(p) * sh.N * 3;
+  float* pc = ws.pc + p * ws.s_pc;
+  if (sh.nimg > 1) {
+    const int* img = ws.img + p * ws.s_img;
+    if (threadIdx.x < kMaxImages) {
+      bh0[threadIdx.x] = 0x7fffffff; bh1[threadIdx.x] = -0x7fffffff;
+      bw0[threadIdx.x] = 0x7fffffff; bw1[threadIdx.x] = -0x7fffffff;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
+      const int g = img[i];
+      atomicMin(&bh0[g], pos[i * 3 + 1]); atomicMax(&bh1[g], pos[i * 3 + 1]);
+      atomicMin(&bw0[g], pos[i * 3 + 2]); atomicMax(&bw1[g], pos[i * 3 + 2]);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
+      const int g = img[i];
+      const float h0 = static_cast<float>(bh0[g]), w0 = static_cast<float>(bw0[g]);
+      const float gh = static_cast<float>(bh1[g]) - h0 + 1.f, gw = static_cast<float>(bw1[g]) - w0 + 1.f;
+      pc[2 * i] = (static_cast<float>(pos[i * 3 + 1]) - h0 + 0.5f) / gh;
+      pc[2 * i + 1] = (static_cast<float>(pos[i * 3 + 2]) - w0 + 0.5f) / gw;
+    }
+    return;
+  }
   float hmin = INFINITY, hmax = -INFINITY, wmin = INFINITY, wmax = -INFINITY;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
     const float hh = static_cast<float>(pos[i * 3 + 1]), ww = static_cast<float>(pos[i * 3 + 2]);
@@ -294,7 +329,6 @@ __global__ void __launch_bounds__(256) spatial_coords_kernel(Shape sh, Ws ws, co
   wmin = block_min(wmin, red);
   wmax = block_max(wmax, red);
   const float gh = hmax - hmin + 1.f, gw = wmax - wmin + 1.f;
-  float* pc = ws.pc + p * ws.s_pc;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
     pc[2 * i] = (static_cast<float>(pos[i * 3 + 1]) - hmin + 0.5f) / gh;
     pc[2 * i + 1] = (static_cast<float>(pos[i * 3 + 2]) - wmin + 0.5f) / gw;
@@ -302,18 +336,23 @@ __global__ void __launch_bounds__(256) spatial_coords_kernel(Shape sh, Ws ws, co
 }
 
 // Spatial bank, landmark side: one block per landmark l_ab = ((a+.5)/L,
-// (b+.5)/L): the minimum squared distance to any token, the row sum of
-// exp(-(d^2 - min d^2)/tau_s), the weight (beta_spa / L^2) / Z and the peak
+// (b+.5)/L) of image g (row g L^2 + a L + b; one image: g = 0): the minimum
+// squared distance to any token of the image, the row sum of
+// exp(-(d^2 - min d^2)/tau_s), the weight (beta_spa / M_S) / Z and the peak
 // (the row maximum is exactly 1).
 __global__ void __launch_bounds__(256) spatial_stats_kernel(Shape sh, Params pr, Ws ws) {
   __shared__ float red[16];
   const int row = blockIdx.x, p = blockIdx.y;
-  const int L = sh.landmarks;
-  const float ly = (static_cast<float>(row / L) + 0.5f) / L;
-  const float lx = (static_cast<float>(row % L) + 0.5f) / L;
+  const int L = sh.landmarks, L2 = L * L;
+  const int g = row / L2, lr = row % L2;
+  const float ly = (static_cast<float>(lr / L) + 0.5f) / L;
+  const float lx = (static_cast<float>(lr % L) + 0.5f) / L;
   const float* pc = ws.pc + p * ws.s_pc;
+  const int* img = ws.img + p * ws.s_img;
+  const bool multi = sh.nimg > 1;
   float dmin = INFINITY;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
+    if (multi && img[i] != g) continue;
     const float dy = pc[2 * i] - ly, dx = pc[2 * i + 1] - lx;
     dmin = fminf(dmin, dy * dy + dx * dx);
   }
@@ -321,35 +360,41 @@ __global__ void __launch_bounds__(256) spatial_stats_kernel(Shape sh, Params pr,
   const float inv_tau = 1.f / pr.tau_s;
   float s = 0.f;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
+    if (multi && img[i] != g) continue;
     const float dy = pc[2 * i] - ly, dx = pc[2 * i + 1] - lx;
     s += expf(-(dy * dy + dx * dx - dmin) * inv_tau);
   }
   s = block_sum(s, red);
   if (threadIdx.x == 0) {
     const int m = sh.mg + sh.mv + row;
-    const float a = pr.beta_spa / static_cast<float>(sh.ms) / s;
+    // an image without tokens (reported by the input status bit) keeps an
+    // inert row
+    const float a = s > 0.f ? pr.beta_spa / static_cast<float>(sh.ms) / s : 0.f;
     ws.alpha[p * ws.s_m + m] = a;
     ws.peak[p * ws.s_m + m] = a;
-    ws.lstat[p * ws.s_lstat + row] = dmin;
+    ws.lstat[p * ws.s_lstat + row] = s > 0.f ? dmin : 0.f;
   }
 }
 
-// Spatial bank, token side: one wave per token writes its L^2 landmark
-// energies, contiguous in the token-major client matrix.
+// Spatial bank, token side: one wave per token writes its landmark energies,
+// contiguous in the token-major client matrix (zero for the landmarks of
+// other images).
 __global__ void __launch_bounds__(256) spatial_write_kernel(Shape sh, Params pr, Ws ws) {
   const int p = blockIdx.y, i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= sh.N) return;
-  const int L = sh.landmarks;
+  const int L = sh.landmarks, L2 = L * L;
   const float* pc = ws.pc + p * ws.s_pc;
   const float py = pc[2 * i], px = pc[2 * i + 1];
+  const int gi = sh.nimg > 1 ? ws.img[p * ws.s_img + i] : 0;
   const float inv_tau = 1.f / pr.tau_s;
   const float* dmin = ws.lstat + p * ws.s_lstat;
   float* E = ws.E + p * ws.s_E + static_cast<long long>(i) * sh.ldM + sh.mg + sh.mv;
   for (int row = lane; row < sh.ms; row += 64) {
-    const float ly = (static_cast<float>(row / L) + 0.5f) / L;
-    const float lx = (static_cast<float>(row % L) + 0.5f) / L;
+    const int lr = row % L2;
+    const float ly = (static_cast<float>(lr / L) + 0.5f) / L;
+    const float lx = (static_cast<float>(lr % L) + 0.5f) / L;
     const float dy = py - ly, dx = px - lx;
-    E[row] = expf(-(dy * dy + dx * dx - dmin[row]) * inv_tau);
+    E[row] = (row / L2 == gi) ? expf(-(dy * dy + dx * dx - dmin[row]) * inv_tau) : 0.f;
   }
 }
 

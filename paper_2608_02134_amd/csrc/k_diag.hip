@@ -64,8 +64,11 @@ __global__ void __launch_bounds__(256) cert_cov_kernel(Shape sh, Ws ws, SelOut s
   const int mc = ok ? m : 0;
   const float a = ok ? ws.alpha[p * ws.s_m + mc] : 0.f;
   const float* E = ws.E + p * ws.s_E + mc;
+  // the rounds start from the image seeds' coverage (none for one image)
   float b = 0.f;
-  int selected = 0;
+  const int* order = ws.order + p * ws.s_ord;
+  for (int g = 0; g < sh.nseed; ++g) b = fmaxf(b, a * E[static_cast<long long>(order[g]) * sh.ldM]);
+  int selected = sh.nseed;
   for (int r = 0; r < sh.rounds; ++r) {
     const int bsize = min(sh.b, sh.K - selected);
     const int32_t* bat = so.batch + (static_cast<long long>(p) * sh.rounds + r) * sh.b;
@@ -86,7 +89,7 @@ __global__ void __launch_bounds__(256) cert_round_kernel(Shape sh, Ws ws, SelOut
   __shared__ float red[16];
   __shared__ int redi[16];
   const int r = blockIdx.x, p = blockIdx.y;
-  const int selected = r * sh.b;
+  const int selected = sh.nseed + r * sh.b;
   const int remaining = sh.N - selected;
   const int psize = min(sh.pool_cap, remaining);
   const int bsize = min(sh.b, sh.K - selected);

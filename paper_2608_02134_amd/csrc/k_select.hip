@@ -544,7 +544,10 @@ gains_fused_kernel(Shape sh, Ws ws, int round, int psize, int prev_psize, int pr
       }
     }
   } else {
-    for (int m = tid * 4; m < sh.m; m += 1024) *reinterpret_cast<float4*>(bnew + m) = make_float4(0.f, 0.f, 0.f, 0.f);
+    // the coverage before the first round: zero, or the image seeds' b_m(S_0)
+    for (int m = tid * 4; m < sh.m; m += 1024)
+      *reinterpret_cast<float4*>(bnew + m) =
+          sh.nseed > 0 ? *reinterpret_cast<const float4*>(cov + m) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   __syncthreads();
   const int col0 = blockIdx.x * kGainColsF + wave * kCpwF;
@@ -881,12 +884,17 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   int* cnt = ws.cnt + p * ws.s_cnt;
   {
     const float* alpha = ws.alpha + p * ws.s_m;
+    const float* cov0 = ws.cov + p * ws.s_cov;
     for (int m = tid; m < sh.ldM; m += 256) {
-      bl[m] = 0.f;   // coverage is zero at call start
+      // coverage at the first round: zero, or the image seeds' b_m(S_0)
+      bl[m] = sh.nseed > 0 ? cov0[m] : 0.f;
       al[m] = alpha[m];
     }
   }
-  for (int i = tid; i < sh.N; i += 256) taken[i] = 0;
+  {
+    const int* sel0 = ws.sel + p * ws.s_sel;
+    for (int i = tid; i < sh.N; i += 256) taken[i] = (sh.nseed > 0 && sel0[i] >= 0) ? 1 : 0;
+  }
   if (tid == 0) failed = 0;
   float er[RES ? 8 : 1][RES ? kResJ : 1];
   if constexpr (RES) {
@@ -905,7 +913,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
     }
   }
   __syncthreads();
-  int selected = 0;
+  int selected = sh.nseed;
   for (int r = 0; r < sh.rounds; ++r) {
     const int psize = min(sh.pool_cap, sh.N - selected);
     const int bsize = min(sh.b, sh.K - selected);
@@ -1371,6 +1379,14 @@ static int persistent_blocks(const Shape& sh, size_t lds, int res) {
 hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, const SelOut& so, hipStream_t st,
                             bool* support_ready) {
   *support_ready = false;
+  if (sh.rounds == 0) {
+    // the image seeds already fill the budget (K = I): only the objective;
+    // the assignment builds the support list from the selection marks
+    timer_mark(kStObjective, true, st);
+    hipLaunchKernelGGL(objective_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
+    timer_mark(kStObjective, false, st);
+    return hipGetLastError();
+  }
   {
     const size_t lds = 2 * static_cast<size_t>(sh.ldM) * sizeof(float) +
                        ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15)) +
@@ -1405,7 +1421,7 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, con
   const bool fused = sh.pool_cap <= 64 && fused_lds <= 56 * 1024 && cbar_bytes <= (48LL << 20);
   const dim3 gg((sh.N + kGainCols - 1) / kGainCols, sh.B);
   const dim3 ggf((sh.N + kGainColsF - 1) / kGainColsF, sh.B);
-  int selected = 0, prev_psize = 0, prev_bsize = 0, prev_base = 0;
+  int selected = sh.nseed, prev_psize = 0, prev_bsize = 0, prev_base = 0;
   for (int r = 0; r < sh.rounds; ++r) {
     const int psize = min(sh.pool_cap, sh.N - selected);
     const int bsize = min(sh.b, sh.K - selected);

@@ -41,6 +41,7 @@ import numpy as np
 __all__ = [
     "Workload", "WORKLOADS", "Problem", "make_problem", "round_bf16",
     "bf16_bits", "rademacher_projection", "APP_PROJ_SEED", "HistView", "make_history",
+    "make_multi_image",
 ]
 
 APP_PROJ_SEED = 104729  # seed of the long-prefix appearance projection
@@ -86,6 +87,8 @@ class Problem:
     probe: np.ndarray       # [Hq][r][d] float32
     app_proj: Optional[np.ndarray]  # [app_rank][d] float32 (+-1) or None
     k: int
+    image_id: Optional[np.ndarray] = None   # [B][N] int32 for a multi-image prompt
+    n_images: int = 1
 
 
 def round_bf16(a: np.ndarray) -> np.ndarray:
@@ -271,3 +274,54 @@ def make_history(prob: Problem, n_views: int = 2) -> list:
         views.append(HistView(np.ascontiguousarray(h, np.float32), np.ascontiguousarray(q, np.float32),
                               np.ascontiguousarray(k, np.float32), np.ascontiguousarray(probe, np.float32)))
     return views
+
+
+def make_multi_image(name: str, grids, *, t: Optional[int] = None, k: Optional[int] = None,
+                     seed: Optional[int] = None, batch: int = 1) -> Problem:
+    """A multi-image prompt: the images' visual tokens one after another,
+    image g on its own (grid_h, grid_w) grid with positions (g, row, col),
+    each image's states an independent draw of the workload's state model
+    (its own mixture centres), keys through the shared key map; queries over
+    all images.  Images are drawn from SeedSequence children of the seed, one
+    per (problem, image)."""
+    w0 = WORKLOADS[name]
+    n = int(sum(gh * gw for gh, gw in grids))
+    repl = dict(batch=batch, n=n, frames=1, grid_h=0, grid_w=0)
+    if t is not None:
+        repl["t"] = t
+    if k is not None:
+        repl["k"] = k
+    if seed is not None:
+        repl["seed"] = seed
+    w = dataclasses.replace(w0, **repl)
+    rng = np.random.Generator(np.random.PCG64(w.seed))
+    probe = _normal(rng, (w.hq, 4, w.d), 1.0 / np.sqrt(w.d))
+    wk = _normal(rng, (w.d, w.hkv * w.dh), 1.0 / np.sqrt(w.d))
+    kids = np.random.SeedSequence(w.seed).spawn(batch * (len(grids) + 1))
+    hs, qs, ks, ps, ids = [], [], [], [], []
+    for b in range(batch):
+        hb, pb, ib = [], [], []
+        for g, (gh, gw) in enumerate(grids):
+            r = np.random.Generator(np.random.PCG64(kids[b * (len(grids) + 1) + g]))
+            wg = dataclasses.replace(w, n=gh * gw, grid_h=gh, grid_w=gw, frames=1)
+            h, _, _ = (_mixture_states(r, wg, gh * gw) if w.kind != "iid" else (_normal(r, (gh * gw, w.d)), 0, 0))
+            hb.append(h)
+            yy, xx = np.divmod(np.arange(gh * gw), gw)
+            pb.append(np.stack([np.full(gh * gw, g), yy, xx], axis=1))
+            ib.append(np.full(gh * gw, g))
+        h = np.concatenate(hb, axis=0)
+        rq = np.random.Generator(np.random.PCG64(kids[b * (len(grids) + 1) + len(grids)]))
+        hs.append(h)
+        qs.append(_normal(rq, (w.t, w.hq, w.dh)))
+        ks.append((h @ wk).reshape(n, w.hkv, w.dh))
+        ps.append(np.concatenate(pb, axis=0))
+        ids.append(np.concatenate(ib))
+    hidden = np.stack(hs).astype(np.float32)
+    text_q = np.stack(qs).astype(np.float32)
+    vis_k = np.stack(ks).astype(np.float32)
+    if w.dtype == "bf16":
+        hidden, text_q, vis_k = round_bf16(hidden), round_bf16(text_q), round_bf16(vis_k)
+        probe = round_bf16(probe)
+    return Problem(w, np.ascontiguousarray(hidden), np.ascontiguousarray(text_q), np.ascontiguousarray(vis_k),
+                   np.stack(ps).astype(np.int32), np.ascontiguousarray(probe), None, w.k,
+                   np.stack(ids).astype(np.int32), len(grids))

@@ -12,6 +12,8 @@ def run(prob: synth.Problem, torch, k=None, trace=True, nonvis=None, pruner=None
     """One gmc_prune_ex call (gmc_prune_views with historical views, a list of
     synth.HistView); returns (list of per-problem dicts, pruner)."""
     w = prob.workload
+    if prob.n_images > 1 and "max_images" not in overrides:
+        overrides["max_images"] = prob.n_images
     pr = pruner or make_pruner(prob, torch, hist=hist, **overrides)
     hid = to_device(prob.hidden, w.dtype, torch)
     q = to_device(prob.text_q, w.dtype, torch)
@@ -21,7 +23,9 @@ def run(prob: synth.Problem, torch, k=None, trace=True, nonvis=None, pruner=None
     kreq = prob.k if k is None else k
     hv = None if not hist else [(to_device(v.hidden, w.dtype, torch), to_device(v.text_q, w.dtype, torch),
                                  to_device(v.vis_k, w.dtype, torch)) for v in hist]
-    res = pr.prune(hid, q, kk, pos, kreq, nonvis_lse=nv, trace=trace, hist=hv)
+    img = None if prob.image_id is None else torch.from_numpy(prob.image_id).cuda()
+    res = pr.prune(hid, q, kk, pos, kreq, nonvis_lse=nv, trace=trace, hist=hv, image_id=img,
+                   n_images=prob.n_images)
     torch.cuda.synchronize()
     outs = []
     for b in range(w.batch):

@@ -102,15 +102,18 @@ def _valid_top(score: np.ndarray, cand: np.ndarray, chosen: np.ndarray, count: i
 
 
 def follow_selection(cbar: np.ndarray, k: int, b: int, pools, batches, p: O.GmcParams,
-                     rep: FollowReport, gains=None, scores=None):
+                     rep: FollowReport, gains=None, scores=None, seeds=()):
     """Walk the oracle along the GPU's per-round pools and batches.  With the
     GPU's per-round gains and pool scores, compare them element by element.
     Records the oracle's certificate terms of every followed round."""
     m, n = cbar.shape
     cov = np.zeros(m)
     chosen = np.zeros(n, dtype=bool)
-    n_sel = 0
-    rounds = -(-k // b)
+    for j in seeds:                      # S_0 of a multi-image prompt
+        chosen[j] = True
+        cov = np.maximum(cov, cbar[:, j])
+    n_sel = len(seeds)
+    rounds = -(-(k - n_sel) // b)
     rep.rounds_log = []
     for r in range(rounds):
         cand = np.flatnonzero(~chosen)
@@ -180,8 +183,8 @@ def check_certificate(diag: dict, rep: FollowReport, f_s: float):
     assert abs(diag["c_b"] - c_b) <= 1e-4 * max(c_b, 1e-6) + 1e-6, f"c_B {diag['c_b']} vs {c_b}"
 
 
-def follow_assignment(x, pc, support, gpu_pi, p: O.GmcParams, rep: FollowReport):
-    a = O.assign_population(x, pc, support, p)
+def follow_assignment(x, pc, support, gpu_pi, p: O.GmcParams, rep: FollowReport, img=None):
+    a = O.assign_population(x, pc, support, p, img)
     kappa = a["kappa"]                       # [N][K], columns in ascending support order
     sup = a["support"]
     slot = {int(j): jj for jj, j in enumerate(sup)}
@@ -205,22 +208,45 @@ def bf16_round(a: np.ndarray) -> np.ndarray:
     return round_bf16(np.asarray(a, dtype=np.float32))
 
 
+def check_seeds(cbar: np.ndarray, img: np.ndarray, gpu_seeds: np.ndarray) -> np.ndarray:
+    """The GPU's image seeds must be valid per-image argmaxes of the oracle's
+    singleton gains F({i}) (near ties within REL_TIE of the largest gain, exact
+    ties to the lower index).  Returns them in image order."""
+    u = cbar.sum(axis=0)
+    tol = REL_TIE * float(u.max())
+    out = []
+    for g in range(int(img.max()) + 1):
+        members = np.flatnonzero(img == g)
+        mine = [int(j) for j in gpu_seeds if img[j] == g]
+        assert len(mine) == 1, f"image {g}: {len(mine)} seeds"
+        j = mine[0]
+        best = float(u[members].max())
+        assert u[j] >= best - tol, f"image {g}: seed {j} gain {u[j]} vs best {best}"
+        ties = members[u[members] == u[j]]
+        assert j == ties.min(), f"image {g}: equal gains not resolved by lower index"
+        out.append(j)
+    return np.asarray(out, dtype=np.int64)
+
+
 def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcParams = O.GmcParams(),
-                  app_proj=None, nonvis=None, probe_bias=None, hist=()) -> FollowReport:
+                  app_proj=None, nonvis=None, probe_bias=None, hist=(), img=None) -> FollowReport:
     """Full follow-mode check of one problem.  `gpu` holds numpy arrays:
     out_hidden, out_pos, out_idx and, from the trace, round_pool, round_batch,
     assign, and optionally client, omega, ebar, stats."""
     rep = FollowReport()
     h = np.asarray(h, np.float64)
     n = h.shape[0]
-    kk = O.realized_budget(n, k_req)
+    n_img = 1 if img is None else int(np.max(img)) + 1
+    if n_img == 1:
+        img = None
+    kk = O.realized_budget(n, k_req, n_img)
     assert gpu["out_idx"].shape == (kk,)
     if kk == n:
         assert np.array_equal(gpu["out_idx"], np.arange(n))
         assert np.array_equal(gpu["out_pos"], pos)
         assert np.array_equal(np.asarray(gpu["out_hidden"], np.float64), h)
         return rep
-    cl = O.build_clients(h, q, k, pos, probe, p, app_proj, nonvis, probe_bias, hist)
+    cl = O.build_clients(h, q, k, pos, probe, p, app_proj, nonvis, probe_bias, hist, img)
     cbar = cl["cbar"]
     if gpu.get("client") is not None:
         rel = {}
@@ -246,11 +272,16 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
         eb = cl["ebar"]
         assert np.linalg.norm(gpu["ebar"] - eb) / np.linalg.norm(eb) < 1e-4, "normalised energy"
     b = p.batch_b_bounded if cl["bounded"] else p.batch_b
+    seeds = ()
+    if img is not None:
+        in_rounds = set(int(x) for x in np.asarray(gpu["round_batch"]).ravel() if x >= 0)
+        gpu_seeds = np.asarray([j for j in gpu["out_idx"] if int(j) not in in_rounds], dtype=np.int64)
+        seeds = check_seeds(cbar, img, gpu_seeds)
     support, cov = follow_selection(cbar, kk, b, gpu["round_pool"], gpu["round_batch"], p, rep,
-                                    gpu.get("round_gains"), gpu.get("round_scores"))
+                                    gpu.get("round_gains"), gpu.get("round_scores"), seeds)
     assert np.array_equal(np.asarray(gpu["out_idx"], np.int64), support), "out_idx != followed support"
     assert np.array_equal(gpu["out_pos"], pos[support]), "out_pos != pos3d[out_idx]"
-    a = follow_assignment(cl["x"], cl["pc"], support, gpu["assign"], p, rep)
+    a = follow_assignment(cl["x"], cl["pc"], support, gpu["assign"], p, rep, img)
     m = O.population_weights(cl["ebar"], a["sx"], p)
     tr = O.transport(h, np.asarray(gpu["assign"], np.int64), support, m, p)
     ref = tr["out"]
@@ -291,7 +322,7 @@ def check_problem(h, q, k, pos, probe, k_req, gpu: dict, dtype: str, p: O.GmcPar
             assert abs(st[12 + bank] - fvb) <= 1e-4 * fv, f"F_{bank}(V) {st[12 + bank]} vs {fvb}"
     if gpu.get("diag") is not None:
         check_certificate(gpu["diag"], rep, float(cov.sum()))
-    free = O.select_support(cbar, kk, b, p)
+    free = O.select_support(cbar, kk, b, p, O.image_seeds(cbar, img) if img is not None else ())
     rep.identical_to_free_oracle = bool(np.array_equal(np.sort(free["order"]), support))
     if rep.pool_near_ties == 0 and rep.batch_near_ties == 0:
         assert rep.identical_to_free_oracle

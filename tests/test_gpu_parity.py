@@ -33,7 +33,8 @@ def _check_all(prob, outs, **kw):
         hist = [dict(hidden=v.hidden[b], q=v.text_q[b], k=v.vis_k[b], probe=v.probe) for v in kw.get("hist", [])]
         rep = check_problem(prob.hidden[b], prob.text_q[b], prob.vis_k[b], prob.pos3d[b], prob.probe,
                             kw.get("k", prob.k), g, w.dtype, kw.get("params", O.GmcParams()),
-                            prob.app_proj, None if nv is None else nv[b], hist=hist)
+                            prob.app_proj, None if nv is None else nv[b], hist=hist,
+                            img=None if prob.image_id is None else prob.image_id[b])
         reps.append(rep)
         print(f"  problem {b}: {rep}", flush=True)
     return reps
@@ -350,3 +351,41 @@ def test_historical_views_beyond_capacity():
         assert ei.value.code == binding.GMC_ERR_CAPACITY
     finally:
         pr.close()
+
+
+IMAGE_CASES = {
+    # three images on their own grids in one prompt (N = 573)
+    "three_images": dict(grids=[(18, 18), (12, 14), (9, 9)], t=16, k=60),
+    # two Qwen2.5-VL-7B images (2 x 36 x 36 = 2592 tokens), K = 512
+    "two_qwen_images": dict(grids=[(36, 36), (36, 36)], t=64, k=512),
+    # K_r below the image count: the budget expands to one carrier per image
+    "budget_below_images": dict(grids=[(6, 7), (5, 5), (4, 6), (3, 3)], t=8, k=2),
+    # a batch of two problems with five small images each
+    "batch_five_images": dict(grids=[(8, 8), (6, 9), (7, 7), (5, 5), (6, 6)], t=8, k=40, batch=2),
+}
+
+
+@pytest.mark.parametrize("case", list(IMAGE_CASES))
+def test_multi_image_prompts(case):
+    """Multi-image prompts (Sec. 3.1, App. H): image seeds, per-image
+    appearance and spatial rows, same-image assignment."""
+    spec = dict(IMAGE_CASES[case])
+    prob = synth.make_multi_image("qwen", spec.pop("grids"), **spec)
+    _announce(f"images {case} (I={prob.n_images})", prob)
+    outs, pr = run(prob, torch)
+    pr.close()
+    _check_all(prob, outs)
+    for b, g in enumerate(outs):
+        img = prob.image_id[b]
+        assert np.all(img[g["assign"]] == img), "an assignment crossed images"
+        assert set(img[g["out_idx"]].tolist()) == set(range(prob.n_images))
+        assert g["out_idx"].size == max(prob.k, prob.n_images)
+
+
+def test_multi_image_with_history_views():
+    prob = synth.make_multi_image("qwen", [(12, 12), (10, 11)], t=16, k=50)
+    hist = synth.make_history(prob, 2)
+    _announce("images + views", prob)
+    outs, pr = run(prob, torch, hist=hist)
+    pr.close()
+    _check_all(prob, outs, hist=hist)
