@@ -24,6 +24,9 @@ VLM Compression") step by step, in its notation, in float64:
   transport       Sec. 3.4 Eq. transport; App. H Eq. cond-transport,
                   Eq. cond-grounded-energy
   compaction      App. H "Index map and physical token accounting"
+  audit           Prop. 2 Eq. message-bound; App. I Eq. cond-message-
+                  decomposition, Eq. cond-softmax-bound, Eq. cond-message-
+                  polar; App. G Eq. cond-message-error
 
 Readings where the paper is silent are listed in ``READINGS`` and in the
 design notes; each is a named constant below.  Pins against the paper's
@@ -54,7 +57,7 @@ __all__ = [
     "assign_population", "population_weights", "transport", "compact",
     "gmc_single", "gmc", "prune_rounds", "index_map", "compact_sequence",
     "gather_cache", "head_pattern", "head_weights_from_pattern", "view_mass",
-    "message_view", "image_seeds",
+    "message_view", "image_seeds", "message_audit",
 ]
 
 
@@ -629,6 +632,73 @@ def gather_cache(cache, keep):
     """Prefix-layer cache rows gathered at the retained original positions
     (axis -2 is the sequence axis)."""
     return np.take(np.asarray(cache), np.asarray(keep, dtype=np.int64), axis=-2)
+
+
+# ----------------------------------------------------------------------------
+# Realisation audit (Prop. 2 Eq. message-bound; App. I Eq.
+# cond-message-decomposition, Eq. cond-softmax-bound, Eq. cond-message-polar;
+# App. G Eq. cond-message-error)
+# ----------------------------------------------------------------------------
+def message_audit(q, k, v, k_c, v_c, carrier_of, weights=None, nonvis_lse=None):
+    """Signed-message realisation audit of one problem.
+
+    q [T][Hq][dh] queries, k / v [N][Hkv][dh] the full visual keys and values,
+    k_c / v_c [K][Hkv][dh] the compact sequence's keys and values at the K
+    carriers, carrier_of [N] the carrier slot (0..K-1) each source token was
+    transported to, weights [Hq][T] the client weights (uniform 1/(Hq T) when
+    None), nonvis_lse [Hq][T] the nonvisual keys' log-sum-exp shared by both
+    softmaxes.  Per client g = (h, t):
+      y_g = sum_i a_gi v_i (Full), y~_g = sum_j abar_gj v~_j (compact),
+      M_gj = sum_(i in C_j) a_gi, term1_g = sum_i a_gi (v_i - v~_pi(i)),
+      term2_g = sum_j (M_gj - abar_gj) v~_j  (y - y~ = term1 + term2),
+      l1_g = ||M_g - abar_g||_1 and its bound ||u^F_g - u^S_g||_inf with
+      u^F_gj = log sum_(i in C_j) exp(s_gi) and u^S_gj the compact logit.
+    Stacked with sqrt(weights): e_M = ||Y - Y~|| / (||Y|| + 1e-8), the
+    amplitude ratio alpha and the cosine kappa of the polar identity."""
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    k_c = np.asarray(k_c, np.float64)
+    v_c = np.asarray(v_c, np.float64)
+    carrier_of = np.asarray(carrier_of, dtype=np.int64)
+    t, hq, dh = q.shape
+    n, hkv, _ = k.shape
+    kc = k_c.shape[0]
+    w = np.full((hq, t), 1.0 / (hq * t)) if weights is None else np.asarray(weights, np.float64)
+    onehot = np.zeros((n, kc))
+    onehot[np.arange(n), carrier_of] = 1.0
+    rows = dict(y=np.zeros((hq, t, dh)), yc=np.zeros((hq, t, dh)), term1=np.zeros((hq, t, dh)),
+                term2=np.zeros((hq, t, dh)), l1=np.zeros((hq, t)), bound=np.zeros((hq, t)),
+                lse_full=np.zeros((hq, t)), lse_comp=np.zeros((hq, t)))
+    for h in range(hq):
+        g = (h * hkv) // hq
+        s_f = q[:, h, :] @ k[:, g, :].T / math.sqrt(dh)          # [T][N]
+        s_c = q[:, h, :] @ k_c[:, g, :].T / math.sqrt(dh)        # [T][K]
+        lse_f = np.log(np.sum(np.exp(s_f - s_f.max(axis=1, keepdims=True)), axis=1)) + s_f.max(axis=1)
+        lse_c = np.log(np.sum(np.exp(s_c - s_c.max(axis=1, keepdims=True)), axis=1)) + s_c.max(axis=1)
+        if nonvis_lse is not None:
+            lse_f = np.logaddexp(lse_f, np.asarray(nonvis_lse, np.float64)[h])
+            lse_c = np.logaddexp(lse_c, np.asarray(nonvis_lse, np.float64)[h])
+        a = np.exp(s_f - lse_f[:, None])                         # Full visual attention
+        ac = np.exp(s_c - lse_c[:, None])                        # compact attention
+        m = a @ onehot                                           # grouped Full mass M_gj
+        rows["y"][h] = a @ v[:, g, :]
+        rows["yc"][h] = ac @ v_c[:, g, :]
+        rows["term1"][h] = a @ (v[:, g, :] - v_c[carrier_of, g, :])
+        rows["term2"][h] = (m - ac) @ v_c[:, g, :]
+        rows["l1"][h] = np.abs(m - ac).sum(axis=1)
+        with np.errstate(divide="ignore"):
+            u_f = np.log(m) + lse_f[:, None]                    # grouped Full logits
+        rows["bound"][h] = np.max(np.abs(u_f - s_c), axis=1)
+        rows["lse_full"][h] = lse_f
+        rows["lse_comp"][h] = lse_c
+    sw = np.sqrt(w)[:, :, None]
+    Y, Yc = sw * rows["y"], sw * rows["yc"]
+    ny, nyc = float(np.linalg.norm(Y)), float(np.linalg.norm(Yc))
+    diff = float(np.linalg.norm(Y - Yc))
+    return dict(rows=rows, e_m=diff / (ny + 1e-8), alpha=nyc / ny if ny > 0 else 0.0,
+                kappa=float(np.sum(Y * Yc)) / (ny * nyc) if ny > 0 and nyc > 0 else 0.0,
+                norm_y=ny, norm_yc=nyc, norm_diff=diff)
 
 
 # ----------------------------------------------------------------------------
