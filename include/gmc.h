@@ -337,6 +337,48 @@ int gmc_prune_full(int64_t B, const void* hidden, const void* text_q, const void
                    int32_t* out_pos, int32_t* out_idx, const float* nonvis_lse, int64_t n_hist,
                    const gmc_view* hist, const gmc_trace* trace);
 
+/*
+ * gmc_audit_message - the signed-message realisation audit of a compact
+ * sequence (App. G Eq. cond-message-error; App. I Eq.
+ * cond-message-decomposition, Eq. cond-softmax-bound, Eq.
+ * cond-message-polar; Prop. 2 Eq. message-bound).  For every query/head
+ * client g = (h, t) it re-runs native attention over the Full visual keys
+ * and values and over the compact ones at the K carriers, both with the same
+ * nonvisual log-sum-exp, and measures the signed messages y_g and y~_g, the
+ * grouped Full mass M_gj over each carrier's cluster, the exact
+ * decomposition y - y~ = term1 + term2 with term1 = sum_i a_gi (v_i -
+ * v~_pi(i)) and term2 = sum_j (M_gj - abar_gj) v~_j, the grouped-mass gap
+ * l1 = ||M_g - abar_g||_1 and its softmax contraction bound
+ * max_j |u^F_gj - u^S_gj|.  Device pointers (dtype as the context's):
+ *   text_q  [B][T][Hq][dh]; vis_k, vis_v [B][N][Hkv][dh] the Full visual
+ *   keys and values of the next block; comp_k, comp_v [B][K][Hkv][dh] the
+ *   keys and values of the compact visual tokens (the transported states at
+ *   the carriers, in slot order); carrier [B][N] int32 each token's carrier
+ *   slot in [0, K) (clamped); weights [B][Hq][T] fp32 client weights or NULL
+ *   (uniform); nonvis_lse [B][Hq][T] fp32 or NULL.
+ *   rows_out [B][Hq][T][GMC_AUDIT_ROW] fp32 or NULL: ||y||^2, ||y~||^2,
+ *            <y, y~>, ||y - y~||^2, ||term1||^2, ||term2||^2, l1, bound
+ *   vec_out  [B][Hq][T][4][dh] fp32 or NULL: y, y~, term1, term2
+ *   out      [B][GMC_AUDIT_OUT] fp32: e_M = ||Y - Y~|| / (||Y|| + 1e-8),
+ *            alpha = ||Y~|| / ||Y||, kappa = cos(Y, Y~), ||Y||, ||Y~||,
+ *            ||Y - Y~||, max_g (l1 - bound) (<= 0 when the bound holds), 0;
+ *            Y stacks sqrt(w_g) y_g.
+ * A carrier slot without members has M_gj = 0 and an infinite bound.  With
+ * gmc_prune's outputs, slot j is the j-th entry of out_idx and a token's
+ * slot is the position of its traced carrier in out_idx.  Scratch comes from
+ * the context's client-matrix buffer (the last call's client matrix is
+ * overwritten; its outputs and diagnostics are kept).  Asynchronous on the
+ * context's stream and ordered with the pruning calls like they are with
+ * each other; nothing is allocated.
+ * Errors: GMC_ERR_STATE, GMC_ERR_ARG, GMC_ERR_CAPACITY (scratch beyond the
+ * client-matrix buffer), GMC_ERR_HIP.
+ */
+#define GMC_AUDIT_ROW 8
+#define GMC_AUDIT_OUT 8
+int gmc_audit_message(int64_t B, int64_t N, int64_t T, int64_t K, const void* text_q, const void* vis_k,
+                      const void* vis_v, const void* comp_k, const void* comp_v, const int32_t* carrier,
+                      const float* weights, const float* nonvis_lse, float* rows_out, float* vec_out, float* out);
+
 /* Realised budget K = min{N, max{K_r, I}} for I images (Sec. 3.1); 0 if N < 1
  * or I < 1.  Host-only. */
 int64_t gmc_realized_budget(int64_t N, int64_t K_req, int64_t n_images);

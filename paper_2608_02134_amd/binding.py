@@ -25,6 +25,7 @@ GMC_F32, GMC_BF16 = 0, 1
 GMC_STATS = 15
 GMC_MAX_HIST_VIEWS = 3
 GMC_MAX_IMAGES = 64
+GMC_AUDIT_ROW, GMC_AUDIT_OUT = 8, 8
 GMC_STATUS_INPUT = 8
 GMC_MAX_GATHER_TENSORS = 64
 
@@ -98,6 +99,8 @@ SIGNATURES = {
     "gmc_prune_full": (ctypes.c_int, [_i64, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp, _vp, _vp,
                                       _i64, ctypes.POINTER(GmcView), ctypes.POINTER(GmcTrace)]),
     "gmc_realized_budget": (_i64, [_i64, _i64, _i64]),
+    "gmc_audit_message": (ctypes.c_int, [_i64, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                         _vp]),
     "gmc_trace_dims_full": (ctypes.c_int, [_i64, _i64, _i64, _i64, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
                                            ctypes.POINTER(_i64), ctypes.POINTER(_i64)]),
     "gmc_realized_k": (_i64, [_i64, _i64]),
@@ -190,6 +193,12 @@ def gmc_prune_full(b, hidden, text_q, vis_k, pos3d, image_id, n_images, n, t, k,
     tr = ctypes.byref(trace) if trace is not None else None
     return lib().gmc_prune_full(b, hidden, text_q, vis_k, pos3d, image_id, n_images, n, t, k, out_hidden,
                                 out_pos, out_idx, nonvis_lse, nh, arr, tr)
+
+
+def gmc_audit_message(b, n, t, k, text_q, vis_k, vis_v, comp_k, comp_v, carrier, weights, nonvis_lse, rows_out,
+                      vec_out, out) -> int:
+    return lib().gmc_audit_message(b, n, t, k, text_q, vis_k, vis_v, comp_k, comp_v, carrier, weights, nonvis_lse,
+                                   rows_out, vec_out, out)
 
 
 def gmc_realized_budget(n: int, k_req: int, n_images: int) -> int:
@@ -527,6 +536,40 @@ class Pruner:
         if trace:
             return out_h, out_p, out_i, bufs
         return out_h, out_p, out_i
+
+    def audit(self, text_q, vis_k, vis_v, comp_k, comp_v, carrier, weights=None, nonvis_lse=None,
+              rows: bool = False, vectors: bool = False):
+        """gmc_audit_message on torch's current stream: text_q [B][T][Hq][dh],
+        vis_k / vis_v [B][N][Hkv][dh], comp_k / comp_v [B][K][Hkv][dh] in the
+        context dtype, carrier [B][N] int32 slots, weights / nonvis_lse
+        [B][Hq][T] fp32 or None.  Returns (out [B][8], rows [B][Hq][T][8] or
+        None, vectors [B][Hq][T][4][dh] or None)."""
+        torch = self.torch
+        cfg = self.cfg
+        b, t = text_q.shape[:2]
+        n, k = vis_k.shape[1], comp_k.shape[1]
+        hd = (cfg.n_kv_heads, cfg.head_dim)
+        for name, x, lead in (("vis_k", vis_k, (b, n)), ("vis_v", vis_v, (b, n)), ("comp_k", comp_k, (b, k)),
+                              ("comp_v", comp_v, (b, k))):
+            if tuple(x.shape) != lead + hd or x.dtype != self.dtype or not x.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous {self.dtype} {lead + hd} tensor")
+        if tuple(text_q.shape) != (b, t, cfg.n_q_heads, cfg.head_dim) or text_q.dtype != self.dtype:
+            raise ValueError("text_q must be [B][T][Hq][dh] in the context dtype")
+        if tuple(carrier.shape) != (b, n) or carrier.dtype != torch.int32 or not carrier.is_contiguous():
+            raise ValueError("carrier must be a contiguous int32 [B][N] tensor")
+        for name, x in (("weights", weights), ("nonvis_lse", nonvis_lse)):
+            if x is not None and (tuple(x.shape) != (b, cfg.n_q_heads, t) or x.dtype != torch.float32):
+                raise ValueError(f"{name} must be float32 [B][Hq][T]")
+        dev = text_q.device
+        out = torch.zeros((b, GMC_AUDIT_OUT), dtype=torch.float32, device=dev)
+        ro = torch.zeros((b, cfg.n_q_heads, t, GMC_AUDIT_ROW), dtype=torch.float32, device=dev) if rows else None
+        vo = torch.zeros((b, cfg.n_q_heads, t, 4, cfg.head_dim), dtype=torch.float32, device=dev) if vectors else None
+        _check(gmc_set_stream(torch.cuda.current_stream(dev).cuda_stream), "gmc_set_stream")
+        ptr = (lambda x: None if x is None else x.contiguous().data_ptr())
+        _check(gmc_audit_message(b, n, t, k, text_q.data_ptr(), vis_k.data_ptr(), vis_v.data_ptr(), comp_k.data_ptr(),
+                                 comp_v.data_ptr(), carrier.data_ptr(), ptr(weights), ptr(nonvis_lse), ptr(ro),
+                                 ptr(vo), out.data_ptr()), "gmc_audit_message")
+        return out, ro, vo
 
     def set_diag(self, flags: int):
         _check(gmc_set_diag(flags), "gmc_set_diag")

@@ -48,6 +48,9 @@ struct Context {
   // the last pruning call: its stream (a call on another stream waits for it
   // through `xfer`), its shape and what it recorded
   hipStream_t last_stream = nullptr;
+  // the stream of the last call of any kind that used the workspace (a
+  // pruning call or an audit, whose scratch lives in the client matrix)
+  hipStream_t order_stream = nullptr;
   hipEvent_t xfer = nullptr;
   bool has_call = false, last_identity = false, last_cert = false;
   Shape last{};
@@ -820,14 +823,15 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   // the workspace is shared by every call: a call on another stream than the
   // previous one first waits for that stream (its selection may still read
   // the client matrix that this call's bank kernels rewrite)
-  if (c.has_call && st != c.last_stream) {
-    err = hipEventRecord(c.xfer, c.last_stream);
+  if (c.order_stream && st != c.order_stream) {
+    err = hipEventRecord(c.xfer, c.order_stream);
     if (err == hipSuccess) err = hipStreamWaitEvent(st, c.xfer, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "ordering after the previous call's stream: %s",
                                        hipGetErrorString(err));
   }
   c.has_call = true;
   c.last_stream = st;
+  c.order_stream = st;
   c.last = s;
   c.last_identity = s.K == s.N;
   c.last_cert = false;
@@ -879,6 +883,56 @@ int gmc_prune_full(int64_t B, const void* hidden, const void* text_q, const void
                    const gmc_view* hist, const gmc_trace* trace) {
   return run(B, hidden, text_q, vis_k, pos3d, N, T, K, out_hidden, out_pos, out_idx, nonvis_lse, trace, n_hist,
              hist, image_id, n_images);
+}
+
+int gmc_audit_message(int64_t B, int64_t N, int64_t T, int64_t K, const void* text_q, const void* vis_k,
+                      const void* vis_v, const void* comp_k, const void* comp_v, const int32_t* carrier,
+                      const float* weights, const float* nonvis_lse, float* rows_out, float* vec_out, float* out) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_ctx) return fail(GMC_ERR_STATE, "gmc_audit_message: no context");
+  Context& c = *g_ctx;
+  if (B < 1 || N < 1 || T < 1 || K < 1 || K > N || N > kMaxN || T > (1 << 20))
+    return fail(GMC_ERR_ARG, "gmc_audit_message: need B, T >= 1 and 1 <= K <= N <= %d", kMaxN);
+  if (!text_q || !vis_k || !vis_v || !comp_k || !comp_v || !carrier || !out)
+    return fail(GMC_ERR_ARG, "gmc_audit_message: null pointer");
+  const gmc_config& g = c.cfg;
+  Shape s{};
+  s.B = static_cast<int>(B);
+  s.N = static_cast<int>(N);
+  s.T = static_cast<int>(T);
+  s.K = static_cast<int>(K);
+  s.d = g.d;
+  s.hq = g.n_q_heads;
+  s.hkv = g.n_kv_heads;
+  s.hg = g.n_q_heads / g.n_kv_heads;
+  s.dh = g.head_dim;
+  s.dtype = g.dtype;
+  s.mg1 = s.hq * s.T;
+  // scratch inside the client-matrix buffer
+  const long long mg1 = s.mg1;
+  long long off = 0;
+  auto take = [&](long long elems) { const long long o = off; off += (elems + 63) / 64 * 64; return o; };
+  const long long oA = take(B * N * mg1), oY = take(B * mg1 * s.dh), oL = take(B * mg1), oM = take(B * K * mg1);
+  const long long oO = take(B * (K + 1)), oMem = take(B * N), oC = take(B * K), oR = take(B * mg1 * kAuditRow);
+  const long long cap = c.ws.s_E * c.cap.B;
+  if (off > cap)
+    return fail(GMC_ERR_CAPACITY, "gmc_audit_message: needs %lld floats of scratch, the client-matrix buffer holds %lld",
+                off, cap);
+  float* base = c.ws.E;
+  AudWs aw{base + oA, base + oY, base + oL, base + oM, reinterpret_cast<int*>(base + oO),
+           reinterpret_cast<int*>(base + oMem), reinterpret_cast<int*>(base + oC), base + oR};
+  hipError_t err = hipSetDevice(c.device);
+  hipStream_t st = c.stream;
+  if (err == hipSuccess && c.order_stream && st != c.order_stream) {
+    err = hipEventRecord(c.xfer, c.order_stream);
+    if (err == hipSuccess) err = hipStreamWaitEvent(st, c.xfer, 0);
+  }
+  if (err == hipSuccess)
+    err = launch_audit(s, aw, text_q, vis_k, vis_v, comp_k, comp_v, carrier, weights, nonvis_lse, rows_out, vec_out,
+                       out, st);
+  if (err != hipSuccess) return fail(GMC_ERR_HIP, "gmc_audit_message: %s", hipGetErrorString(err));
+  c.order_stream = st;
+  return GMC_OK;
 }
 
 int gmc_trace_dims_full(int64_t N, int64_t T, int64_t K, int64_t n_hist, int64_t n_images, int64_t* rounds,

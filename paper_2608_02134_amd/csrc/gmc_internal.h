@@ -28,6 +28,8 @@ constexpr int kMaxImages = 64;            // GMC_MAX_IMAGES
 constexpr unsigned long long kGateWaitTicks = 1000000000ull;
 constexpr unsigned long long kJoinWaitTicks = 200000000ull;
 constexpr int kCertMaxRounds = 64;   // GMC_CERT_MAX_ROUNDS
+constexpr int kAuditRow = 8;         // GMC_AUDIT_ROW: per-client audit statistics
+constexpr int kAuditOut = 8;         // GMC_AUDIT_OUT: per-problem audit results
 constexpr int kCertFields = 5;       // U_t, gain, q_t, pool margin, batch margin
 constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection
 constexpr int kMaxGather = 64;    // tensors per row-gather launch (GMC_MAX_GATHER_TENSORS)

@@ -72,6 +72,25 @@ hipError_t launch_image_prep(const Shape& sh, const Ws& ws, const int32_t* image
 // order, and the coverage b_m(S_0).
 hipError_t launch_image_seeds(const Shape& sh, const Ws& ws, hipStream_t st);
 
+// Scratch of the realisation audit, carved from the context workspace.
+struct AudWs {
+  float* A;      // [B][N][mg1]   Full attention, token-major
+  float* Y;      // [B][mg1][dh]  Full messages
+  float* lse;    // [B][mg1]      Full log-sum-exp (with the nonvisual part)
+  float* Mt;     // [B][K][mg1]   grouped Full mass, carrier-major
+  int* off;      // [B][K + 1]    member list offsets per carrier
+  int* mem;      // [B][N]        members, ascending within a carrier
+  int* cur;      // [B][K]        placement cursors
+  float* rowst;  // [B][mg1][kAuditRow] per-client statistics
+};
+
+// Signed-message realisation audit (Full and compact native attention,
+// grouped mass, decomposition terms, weighted e_M / alpha / kappa).
+hipError_t launch_audit(const Shape& sh, const AudWs& aw, const void* text_q, const void* vis_k,
+                        const void* vis_v, const void* comp_k, const void* comp_v, const int32_t* carrier,
+                        const float* weights, const float* nonvis_lse, float* rows_out, float* vec_out, float* out,
+                        hipStream_t st);
+
 // Clears the device status words of problems [0, nprob).
 hipError_t launch_clear_status(const Ws& ws, int nprob, hipStream_t st);
 

@@ -148,6 +148,8 @@ def test_new_header_constants_match_binding():
                                                 B.GMC_STATUS_NONFINITE)
     assert (consts["GMC_DIAG_CERT"], consts["GMC_DIAG_FINITE"]) == (B.GMC_DIAG_CERT, B.GMC_DIAG_FINITE)
     assert consts["GMC_CERT_MAX_ROUNDS"] == B.GMC_CERT_MAX_ROUNDS
+    for name in ("GMC_STATUS_INPUT", "GMC_MAX_HIST_VIEWS", "GMC_MAX_IMAGES", "GMC_AUDIT_ROW", "GMC_AUDIT_OUT"):
+        assert consts[name] == getattr(B, name), name
 
 
 def test_struct_layouts_match_the_c_compiler(tmp_path):
@@ -188,6 +190,7 @@ def test_diag_entry_points_without_context(lib):
     assert B.gmc_set_diag(B.GMC_DIAG_CERT) == B.GMC_ERR_STATE
     code, _ = B.gmc_get_diag(0)
     assert code == B.GMC_ERR_STATE
+    assert B.gmc_audit_message(1, 8, 2, 4, *([None] * 11)) == B.GMC_ERR_STATE
 
 
 def _cpu_cfg():

@@ -262,3 +262,32 @@ def test_kappa_hand_computed():
     np.testing.assert_allclose(a["kappa"][3], [1.0, 0.0], atol=1e-15)
     np.testing.assert_allclose(a["kappa"][4], [0.0, 1.0], atol=1e-15)
     assert a["pi"].tolist() == [0, 1, 0, 0, 1]
+
+
+def test_recovery_variants_of_the_selector_recovery_table():
+    # Table cond-selector-recovery's three recovery maps on one support:
+    # hard deletion (tau_j = 0) returns each carrier's own state, up to the
+    # restoration's epsilon; uniform merging (population strength 0) gives
+    # every token weight 1, so a carrier's centroid is the plain mean of its
+    # cluster, written out with loops here; grounded transport (the default)
+    # weights tokens by their energy once the separability gate opens
+    h, q, k, g, pos = _problem(21, n=48)
+    base = O.gmc_single(h, q, k, pos, g, 7, P, keep_intermediates=True)
+    hard = O.gmc_single(h, q, k, pos, g, 7, O.GmcParams(tau_j=0.0), keep_intermediates=True)
+    assert np.array_equal(hard["out_idx"], base["out_idx"])
+    hs = h[hard["out_idx"]]
+    rms = np.sqrt(np.mean(hs ** 2, axis=1))
+    np.testing.assert_allclose(hard["out_hidden"], hs * (rms / (rms + P.restore_eps))[:, None], rtol=1e-13)
+    uni = O.gmc_single(h, q, k, pos, g, 7, O.GmcParams(tau_j=1.0, pop_strength=0.0), keep_intermediates=True)
+    assert np.all(uni["m"] == 1.0)
+    pi = uni["assignment"]["pi"]
+    for s, j in enumerate(uni["out_idx"]):
+        members = [i for i in range(h.shape[0]) if pi[i] == j]
+        mean = np.zeros(h.shape[1])
+        for i in members:
+            mean += h[i] / len(members)
+        r_h = math.sqrt(float(np.mean(h[j] ** 2)))
+        r_c = math.sqrt(float(np.mean(mean ** 2)))
+        np.testing.assert_allclose(uni["out_hidden"][s], mean * r_h / (r_c + P.restore_eps), rtol=1e-11)
+    # grounded transport's weights are not all equal here (the gate is open)
+    assert base["assignment"]["sx"] > 0 and np.unique(np.round(base["m"], 12)).size > 1
