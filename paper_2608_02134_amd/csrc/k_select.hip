@@ -128,22 +128,21 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
 // holds the keys of its contiguous index segment [t*seg, t*seg + seg) in
 // k[0..KPT) (0 past the segment; zero keys are excluded).  The radix windows
 // start at the highest bit in which the non-zero keys differ, so the first
-// histogram spreads the keys over up to 256 bins.  Once the bin holding the
-// threshold has at most 64 keys, its keys are gathered into LDS, one per
-// lane, and every wave finds the threshold among them bit by bit with ballots
-// (no further histogram passes or block barriers).  Every wave scans the
-// histograms itself, so a radix pass needs one block barrier (three
-// histogram buffers rotate).  The selected indices are written to out[0,
-// count) in ascending index order and out[count, 64) is filled with index 0.
+// histogram spreads the keys over up to 256 bins.  Passes continue until the
+// bin holding the threshold is taken whole (the selection is then every
+// non-zero key >= the resolved prefix) or every bit is resolved (the
+// threshold is one key value, its first `remaining` copies by index taken).
+// Every wave scans the histograms itself, so a radix pass needs one block
+// barrier (three histogram buffers rotate).  The selected indices are
+// written to out[0, count) in ascending index order and out[count, 64) is
+// filled with index 0.
 // hist: 768 ints of LDS, scan: >= 16 ints.
 template <int KPT>
 __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, int* out, int* hist, int* scan) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const unsigned long long below = (1ull << lane) - 1ull;
   hist[tid] = 0;
   hist[256 + tid] = 0;
   hist[512 + tid] = 0;
-  if (tid == 0) scan[8] = 0;
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
 #pragma unroll
   for (int q = 0; q < KPT; ++q) {
@@ -199,50 +198,10 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
     mask |= wmask;
     remaining = rem;
     hi = lo;
-    if (hi > 0 && inbin <= 64) {
-      // gather the threshold bin's keys into the third buffer (free: last
-      // read before the barrier above), one LDS atomic per wave
-      uint32_t* cand = reinterpret_cast<uint32_t*>(hist + (3 - buf - nxt) * 256);
-      unsigned long long bm[KPT];
-      int tot = 0;
-#pragma unroll
-      for (int q = 0; q < KPT; ++q) {
-        bm[q] = __ballot(k[q] != 0u && (k[q] & mask) == prefix);
-        tot += __popcll(bm[q]);
-      }
-      int base = 0;
-      if (lane == 0 && tot > 0) base = atomicAdd(&scan[8], tot);
-      base = __builtin_amdgcn_readlane(base, 0);
-#pragma unroll
-      for (int q = 0; q < KPT; ++q) {
-        if ((bm[q] >> lane) & 1ull) cand[base + __popcll(bm[q] & below)] = k[q];
-        base += __popcll(bm[q]);
-      }
-      __syncthreads();
-      // the remaining-th largest key of the bin, one bit at a time below hi:
-      // of the keys still matching the prefix, those with the bit set are
-      // all taken when there are fewer than remaining of them.  Once every
-      // key still matching is taken, the selection is exactly the keys >=
-      // prefix (its lower bits zero): kth = prefix, all keys equal to it.
-      const bool has = lane < inbin;
-      const uint32_t c = has ? cand[lane] : 0u;
-      unsigned long long alive = static_cast<unsigned long long>(__ballot(has));
-      for (int b = hi - 1;; --b) {
-        if (__popcll(alive) == remaining) {
-          remaining = __popcll(alive & static_cast<unsigned long long>(__ballot(c == prefix)));
-          break;
-        }
-        if (b < 0) break;
-        const unsigned long long ones = alive & static_cast<unsigned long long>(__ballot((c >> b) & 1u));
-        const int n1 = __popcll(ones);
-        if (n1 >= remaining) {
-          alive = ones;
-          prefix |= 1u << b;
-        } else {
-          remaining -= n1;
-          alive &= ~ones;
-        }
-      }
+    if (inbin == remaining) {
+      // every key of the threshold bin is taken: the selection is exactly
+      // the non-zero keys >= prefix (its unresolved bits zero)
+      remaining = count;
       hi = 0;
     }
     buf = nxt;
@@ -251,8 +210,8 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
   int gt = 0, eq = 0;
 #pragma unroll
   for (int q = 0; q < KPT; ++q) {
-    gt += k[q] > kth;
-    eq += k[q] == kth;
+    gt += k[q] != 0u && k[q] > kth;
+    eq += k[q] != 0u && k[q] == kth;
   }
   // exclusive prefix of (gt, eq) over threads: wave scans, then the wave
   // totals (scan[12..15], untouched earlier in the call) after one barrier
@@ -267,6 +226,7 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
   const int i0 = tid * seg;
 #pragma unroll
   for (int q = 0; q < KPT; ++q) {
+    if (k[q] == 0u) continue;
     if (k[q] > kth) {
       out[gt_b + min(eq_b, remaining)] = i0 + q;
       ++gt_b;
@@ -851,6 +811,13 @@ __device__ __forceinline__ void pool_regs(const Shape& sh, const unsigned long l
   block_topk_regs<KPT>(k, seg, psize, pool_s, hist, scan);
 }
 
+// A wave-uniform value the compiler cannot see through (so it is not
+// hoisted out of a loop): through a VGPR and back.
+__device__ __forceinline__ int opaque_uniform(int v) {
+  asm volatile("" : "+v"(v));
+  return __builtin_amdgcn_readfirstlane(v);
+}
+
 // RES: block b owns tokens [8 b, 8 b + 8) (N <= 8 blocks, M <= 256 kResJ) and
 // keeps their weighted client rows alpha_m E[i][m] (Cbar, the product rounded
 // once) in registers for the whole call, wave w holding the rows
@@ -914,7 +881,22 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   }
   __syncthreads();
   int selected = sh.nseed;
-  for (int r = 0; r < sh.rounds; ++r) {
+  const Shape sh_call = sh;
+  const int tid_call = tid;
+  for (int r = 0; r < sh_call.rounds; ++r) {
+    // Opaque per-round copies of the shape and the thread index: index math
+    // derived from them is redone every round instead of being hoisted out
+    // of the loop and kept live (in spill registers) across all rounds.
+    Shape sh = sh_call;
+    int tid = tid_call;
+    sh.N = opaque_uniform(sh.N);
+    sh.m = opaque_uniform(sh.m);
+    sh.ldM = opaque_uniform(sh.ldM);
+    sh.K = opaque_uniform(sh.K);
+    sh.b = opaque_uniform(sh.b);
+    sh.pool_cap = opaque_uniform(sh.pool_cap);
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, wave = tid >> 6, gw = blk * 4 + wave;
     const int psize = min(sh.pool_cap, sh.N - selected);
     const int bsize = min(sh.b, sh.K - selected);
     const unsigned tag = static_cast<unsigned>(r + 1);
