@@ -831,7 +831,7 @@ __global__ void bank_signal_kernel(int* flag) {
 // sums as float4 runs of queries, the first pass of the row weights; partial
 // sums are combined through LDS in a fixed order.
 constexpr int kClusterThreads = 512;
-constexpr int kClusterGB = 36;   // block partial quads in flight per thread
+constexpr int kClusterGB = 16;   // block partial quads in flight per thread (more spills to scratch)
 
 __global__ void __launch_bounds__(kClusterThreads) __attribute__((amdgpu_waves_per_eu(1, 2)))
 cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_flag) {
