@@ -214,6 +214,147 @@ gemm_nt_kernel(RowOperand<T> A, RowOperand<T> B, int K, int ksplit, Epi epi) {
   }
 }
 
+// Large bf16 contractions: 128 x 128 tiles on 32x32x16 MFMA, each of the
+// four waves a 64 x 64 quarter (2 x 2 MFMA tiles, every LDS fragment feeding
+// two MFMAs), three register stages of 64-wide k slabs ahead, double-buffered
+// LDS (dynamic, 72 KB).  Workgroups are dealt to the eight XCDs round robin,
+// so workgroup b takes entry (b % 8) * per + b / 8 of the (problem, row tile,
+// column tile) sequence and each XCD's L2 serves one contiguous range of it.
+// Epilogues without row statistics only.
+constexpr int kBigTile = 128;
+constexpr int kBigStages = 3;
+constexpr size_t kBigLds = 4ull * kBigTile * (kBK + 8) * sizeof(bf16_t);
+
+template <class Epi>
+__global__ void __launch_bounds__(256, 2)
+gemm_nt_big_kernel(RowOperand<bf16_t> A, RowOperand<bf16_t> B, int K, int batch, Epi epi) {
+  static_assert(!Epi::kRowStats, "row statistics need the 64-tile kernel");
+  typedef float floatx16 __attribute__((ext_vector_type(16)));
+  constexpr int BT = kBigTile, P = kBK + 8, CPR = kBK / 8, CH = BT * CPR / 256, S = kBigStages;
+  extern __shared__ __attribute__((aligned(16))) unsigned char gemm_big_lds[];
+  bf16_t* As = reinterpret_cast<bf16_t*>(gemm_big_lds);   // [2][BT * P]
+  bf16_t* Bs = As + 2 * BT * P;                           // [2][BT * P]
+  const int ntr = (A.rows + BT - 1) / BT, ntc = (B.rows + BT - 1) / BT, ntiles = ntr * ntc;
+  const int per = (ntiles * batch + 7) / 8;
+  const int f = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (f >= ntiles * batch) return;
+  const int p = f / ntiles, t = f % ntiles;
+  const int row0 = (t / ntc) * BT, col0 = (t % ntc) * BT;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  const bf16_t* a_src[CH];
+  const bf16_t* b_src[CH];
+#pragma unroll
+  for (int q = 0; q < CH; ++q) {
+    const int ch = tid + q * 256, r = ch / CPR, kc = (ch % CPR) * 8;
+    a_src[q] = A.row(p, min(row0 + r, A.rows - 1)) + kc;
+    b_src[q] = B.row(p, min(col0 + r, B.rows - 1)) + kc;
+  }
+  uint4 ra[S][CH], rb[S][CH];
+  const int nk = K / kBK;
+  auto load = [&](int kt, uint4* xa, uint4* xb) {
+    const int k0 = min(kt, nk - 1) * kBK;
+#pragma unroll
+    for (int q = 0; q < CH; ++q) { xa[q] = ld16(a_src[q] + k0); xb[q] = ld16(b_src[q] + k0); }
+  };
+  auto store = [&](int buf, const uint4* xa, const uint4* xb) {
+#pragma unroll
+    for (int q = 0; q < CH; ++q) {
+      const int ch = tid + q * 256, r = ch / CPR, kc = (ch % CPR) * 8;
+      st16(&As[buf * BT * P + r * P + kc], xa[q]);
+      st16(&Bs[buf * BT * P + r * P + kc], xb[q]);
+    }
+  };
+  floatx16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  // operand fragment of lane l: row l % 32 of a 32-row tile, k elements
+  // 8 (l / 32) .. + 8 of the 16-wide step
+  const int fr = lane & 31, fk = (lane >> 5) * 8;
+  auto compute = [&](int buf) {
+    const bf16_t* as = As + buf * BT * P;
+    const bf16_t* bs = Bs + buf * BT * P;
+#pragma unroll
+    for (int ks = 0; ks < kBK; ks += 16) {
+      bf16x8 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        fa[i] = __builtin_bit_cast(bf16x8, ld16(&as[(wr * 64 + i * 32 + fr) * P + ks + fk]));
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        fb[j] = __builtin_bit_cast(bf16x8, ld16(&bs[(wc * 64 + j * 32 + fr) * P + ks + fk]));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int s = 0; s < S; ++s) load(s, ra[s], rb[s]);
+  store(0, ra[0], rb[0]);
+  __syncthreads();
+  // whole groups of S steps (static register stages); S is odd, so the LDS
+  // buffer follows the slab's own parity
+  const int nk_main = nk - nk % S;
+  for (int kt = 0; kt < nk_main; kt += S) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      load(kt + s + S, ra[s], rb[s]);
+      compute((kt + s) & 1);
+      store((kt + s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s) {
+    if (nk_main + s >= nk) break;
+    compute((nk_main + s) & 1);
+    store((nk_main + s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
+    __syncthreads();
+  }
+  // epilogue: acc[i][j][4 a + b] is C[32 i + 8 a + 4 (l / 32) + b][32 j + l % 32]
+  // of the wave's quarter
+  const int h = lane >> 5, cl = lane & 31;
+  const int qr0 = row0 + wr * 64, qc0 = col0 + wc * 64;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = qc0 + 32 * j + cl;
+    if (c >= B.rows) continue;
+    const float csc = epi.col_scale(p, c);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int r = qr0 + 32 * i + 8 * a + 4 * h + b;
+          if (r < A.rows) epi.value(p, r, c, acc[i][j][4 * a + b] * epi.row_scale(p, r) * csc);
+        }
+  }
+}
+
+template <class Epi>
+inline hipError_t launch_gemm_nt_big(const RowOperand<bf16_t>& A, const RowOperand<bf16_t>& B, int K, int batch,
+                                     const Epi& epi, hipStream_t stream) {
+  if (K % kBK != 0) return hipErrorInvalidValue;
+  static bool granted = false;
+  if (!granted) {
+    const hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_nt_big_kernel<Epi>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kBigLds));
+    if (err != hipSuccess) return err;
+    granted = true;
+  }
+  const long long tiles = static_cast<long long>((A.rows + kBigTile - 1) / kBigTile) *
+                          ((B.rows + kBigTile - 1) / kBigTile) * batch;
+  hipLaunchKernelGGL((gemm_nt_big_kernel<Epi>), dim3(static_cast<unsigned>((tiles + 7) / 8 * 8)), dim3(256), kBigLds,
+                     stream, A, B, K, batch, epi);
+  return hipGetLastError();
+}
+
 // K must divide into ksplit slices that are multiples of 64; with ksplit > 1
 // the epilogue's problem index is problem * ksplit + split.
 template <typename T, int BM, int BN, class Epi>

@@ -274,7 +274,16 @@ static hipError_t assign_impl(const Shape& sh, const Params& pr, const Ws& ws, c
     RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
     RowOperand<T> S{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, ws.sup, ws.s_sup, sh.K};
     CosEpi epi{ws, sh.ldK, pr.norm_eps};
-    hipError_t err = launch_gemm_nt<T, 64, 64>(A, S, sh.d, sh.B, epi, st);
+    hipError_t err;
+    // 128-row tiles on 32x32 MFMA once they alone fill the chip twice over
+    const long long big_tiles = static_cast<long long>((sh.N + kBigTile - 1) / kBigTile) *
+                                ((sh.K + kBigTile - 1) / kBigTile) * sh.B;
+    if constexpr (sizeof(T) == 2) {
+      if (big_tiles >= 512) err = launch_gemm_nt_big(A, S, sh.d, sh.B, epi, st);
+      else err = launch_gemm_nt<T, 64, 64>(A, S, sh.d, sh.B, epi, st);
+    } else {
+      err = launch_gemm_nt<T, 64, 64>(A, S, sh.d, sh.B, epi, st);
+    }
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(gap_kernel<false>, dim3(nblk, sh.B), dim3(256), 0, st, sh, pr, ws);
   } else {

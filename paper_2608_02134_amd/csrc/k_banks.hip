@@ -235,6 +235,195 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
   }
 }
 
+// The exact bank for many tiles (bf16 states): 128 x 128 upper-triangle
+// tiles of the Gram on 32x32x16 MFMA, each wave a 64 x 64 quarter (2 x 2
+// MFMA tiles, so every LDS operand fragment feeds two MFMAs of 32K flop).
+// Operands: 64-wide k slabs, three register stages ahead, double-buffered
+// LDS.  The quarters are aligned with the 64-column blocks of the row
+// statistics: quarter (a, b) of tile (I, J) is the 64 x 64 block pair
+// (2I + a, 2J + b), written for (client r, token c) and, unless it is a
+// diagonal block, mirrored; on a diagonal tile the lower quarter (1, 0)
+// mirrors (0, 1) and writes nothing.  Row statistics per quarter go through
+// LDS: one lane per client row (or column) of the quarter.
+constexpr int kBigT = 128;
+constexpr int kBigS = 3;
+__global__ void __launch_bounds__(256, 2)
+gram_sym_big_kernel(Shape sh, Ws ws, const bf16_t* hidden, float inv_tau, float norm_eps) {
+  typedef float floatx16 __attribute__((ext_vector_type(16)));
+  constexpr int BT = kBigT, P = kBK + 8, CPR = kBK / 8, CH = BT * CPR / 256, S = kBigS;
+  extern __shared__ __attribute__((aligned(16))) unsigned char big_lds[];
+  bf16_t* As = reinterpret_cast<bf16_t*>(big_lds);          // [2][BT * P]
+  bf16_t* Bs = As + 2 * BT * P;                              // [2][BT * P]
+  const int nt = (sh.N + BT - 1) / BT, ntiles = nt * (nt + 1) / 2;
+  // XCD-contiguous order: workgroups go to the eight XCDs round robin, so
+  // workgroup b takes entry (b % 8) * per + b / 8 of the (problem, tile)
+  // sequence; each XCD then works through one contiguous range, whose tiles
+  // share operand rows in its own L2
+  const int per = (ntiles * sh.B + 7) / 8;
+  const int f = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (f >= ntiles * sh.B) return;
+  const int p = f / ntiles;
+  int I = 0, rem = f % ntiles;
+  while (rem >= nt - I) { rem -= nt - I; ++I; }
+  const int J = I + rem;
+  const int row0 = I * BT, col0 = J * BT;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  const bf16_t* base = hidden + static_cast<long long>(p) * sh.N * sh.d;
+  const bf16_t* a_src[CH];
+  const bf16_t* b_src[CH];
+#pragma unroll
+  for (int q = 0; q < CH; ++q) {
+    const int ch = tid + q * 256, r = ch / CPR, kc = (ch % CPR) * 8;
+    a_src[q] = base + static_cast<long long>(min(row0 + r, sh.N - 1)) * sh.d + kc;
+    b_src[q] = base + static_cast<long long>(min(col0 + r, sh.N - 1)) * sh.d + kc;
+  }
+  uint4 ra[S][CH], rb[S][CH];
+  const int nk = sh.d / kBK;
+  auto load = [&](int kt, uint4* xa, uint4* xb) {
+    const int k0 = min(kt, nk - 1) * kBK;
+#pragma unroll
+    for (int q = 0; q < CH; ++q) { xa[q] = ld16(a_src[q] + k0); xb[q] = ld16(b_src[q] + k0); }
+  };
+  auto store = [&](int buf, const uint4* xa, const uint4* xb) {
+#pragma unroll
+    for (int q = 0; q < CH; ++q) {
+      const int ch = tid + q * 256, r = ch / CPR, kc = (ch % CPR) * 8;
+      st16(&As[buf * BT * P + r * P + kc], xa[q]);
+      st16(&Bs[buf * BT * P + r * P + kc], xb[q]);
+    }
+  };
+  floatx16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  // operand fragment of lane l: row l % 32 of the 32-row tile, k elements
+  // 8 (l / 32) .. + 8 of the 16-wide step
+  const int fr = lane & 31, fk = (lane >> 5) * 8;
+  auto compute = [&](int buf) {
+    const bf16_t* as = As + buf * BT * P;
+    const bf16_t* bs = Bs + buf * BT * P;
+#pragma unroll
+    for (int ks = 0; ks < kBK; ks += 16) {
+      bf16x8 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        fa[i] = __builtin_bit_cast(bf16x8, ld16(&as[(wr * 64 + i * 32 + fr) * P + ks + fk]));
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        fb[j] = __builtin_bit_cast(bf16x8, ld16(&bs[(wc * 64 + j * 32 + fr) * P + ks + fk]));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int s = 0; s < S; ++s) load(s, ra[s], rb[s]);
+  store(0, ra[0], rb[0]);
+  __syncthreads();
+  // whole groups of S steps (static register stages, no exit inside a group)
+  const int nk_main = nk - nk % S;
+  // (S is odd, so the LDS buffer follows the slab's own parity)
+  for (int kt = 0; kt < nk_main; kt += S) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      load(kt + s + S, ra[s], rb[s]);
+      compute((kt + s) & 1);
+      store((kt + s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s) {
+    if (nk_main + s >= nk) break;
+    compute((nk_main + s) & 1);
+    store((nk_main + s + 1) & 1, ra[(s + 1) % S], rb[(s + 1) % S]);
+    __syncthreads();
+  }
+
+  // epilogue.  acc[i][j][4 a + b] is C[32 i + 8 a + 4 (l / 32) + b][32 j + l % 32]
+  // of the quarter; v = exp((cos - 1) / tau_v), zero across images
+  const bool diag_tile = I == J;
+  const bool skip = diag_tile && wr == 1 && wc == 0;   // mirror of quarter (0, 1)
+  const bool mirror = !(diag_tile && wr == wc);
+  const int qr0 = row0 + wr * 64, qc0 = col0 + wc * 64;
+  const float* n2 = ws.n2 + p * ws.s_n;
+  const int* img = ws.img + p * ws.s_img;
+  const bool multi = sh.nimg > 1;
+  float* E = ws.E + p * ws.s_E;
+  float* vt = reinterpret_cast<float*>(big_lds) + wave * 64 * 65;   // the quarter's values, pitch 65
+  const int h = lane >> 5, cl = lane & 31;
+  if (!skip) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int c = qc0 + 32 * j + cl;
+      const bool cok = c < sh.N;
+      const int cc = min(c, sh.N - 1);
+      const float csc = 1.f / fmaxf(sqrtf(n2[cc]), norm_eps);
+      const int cim = multi ? img[cc] : 0;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          float v4[4];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int rl = 32 * i + 8 * a + 4 * h + b, r = qr0 + rl;
+            const int rr = min(r, sh.N - 1);
+            const float rsc = 1.f / fmaxf(sqrtf(n2[rr]), norm_eps);
+            const bool ok = cok && r < sh.N && (!multi || img[rr] == cim);
+            const float v = ok ? expf((acc[i][j][4 * a + b] * rsc * csc - 1.f) * inv_tau) : 0.f;
+            v4[b] = v;
+            vt[rl * 65 + 32 * j + cl] = v;
+            if (mirror && cok && r < sh.N) E[static_cast<long long>(r) * sh.ldM + sh.mg + c] = v;   // client c, token r
+          }
+          const int r0 = qr0 + 32 * i + 8 * a + 4 * h;
+          if (cok) {
+            float* dst = E + static_cast<long long>(c) * sh.ldM + sh.mg + r0;   // client r, token c
+            if (r0 + 3 < sh.N) {
+              *reinterpret_cast<float4*>(dst) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+            } else {
+#pragma unroll
+              for (int b = 0; b < 4; ++b)
+                if (r0 + b < sh.N) dst[b] = v4[b];
+            }
+          }
+        }
+    }
+  }
+  __syncthreads();   // every wave's quarter is in LDS (the operand buffers are done)
+  if (!skip) {
+    float* ps = ws.apart_sum + p * ws.s_apart;
+    float* pm = ws.apart_max + p * ws.s_apart;
+    // client r = qr0 + lane over the quarter's 64 columns (column block 2J + wc)
+    if (qc0 < sh.N) {
+      float sv = 0.f, mv = 0.f;
+#pragma unroll 8
+      for (int x = 0; x < 64; ++x) { const float v = vt[lane * 65 + x]; sv += v; mv = fmaxf(mv, v); }
+      const int r = qr0 + lane;
+      if (r < sh.N) {
+        ps[static_cast<long long>(2 * J + wc) * sh.mv + r] = sv;
+        pm[static_cast<long long>(2 * J + wc) * sh.mv + r] = mv;
+      }
+    }
+    // client c = qc0 + lane over the quarter's 64 rows (row block 2I + wr)
+    if (mirror && qr0 < sh.N) {
+      float sv = 0.f, mv = 0.f;
+#pragma unroll 8
+      for (int x = 0; x < 64; ++x) { const float v = vt[x * 65 + lane]; sv += v; mv = fmaxf(mv, v); }
+      const int c = qc0 + lane;
+      if (c < sh.N) {
+        ps[static_cast<long long>(2 * I + wr) * sh.mv + c] = sv;
+        pm[static_cast<long long>(2 * I + wr) * sh.mv + c] = mv;
+      }
+    }
+  }
+}
+
 // Bounded bank: raw projection y = R h (fp32 out).
 struct ProjEpi {
   Ws ws;
@@ -418,9 +607,28 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
   if (spatial_first) spatial();
   timer_mark(kStAppearance, true, st);
   if (!sh.bounded) {
-    const int nt = (sh.N + 63) / 64;
-    hipLaunchKernelGGL(gram_sym_kernel<T>, dim3(nt * (nt + 1) / 2, sh.B), dim3(kGemmThreads), 0, st, sh, ws,
-                       hidden, 1.f / pr.tau_v, pr.norm_eps);
+    const int nt = (sh.N + 63) / 64, nt2 = (sh.N + kBigT - 1) / kBigT;
+    // 128-row tiles once they alone fill the chip twice over (bf16 states)
+    bool big = false;
+    if constexpr (sizeof(T) == 2) {
+      if (static_cast<long long>(nt2) * (nt2 + 1) / 2 * sh.B >= 512) {
+        constexpr size_t lds = 4ull * kBigT * (kBK + 8) * sizeof(bf16_t);
+        static bool granted = false;
+        if (!granted) {
+          err = hipFuncSetAttribute(reinterpret_cast<const void*>(gram_sym_big_kernel),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+          if (err != hipSuccess) return err;
+          granted = true;
+        }
+        const int per = (nt2 * (nt2 + 1) / 2 * sh.B + 7) / 8;
+        hipLaunchKernelGGL(gram_sym_big_kernel, dim3(8 * per), dim3(256), lds, st, sh, ws, hidden, 1.f / pr.tau_v,
+                           pr.norm_eps);
+        big = true;
+      }
+    }
+    if (!big)
+      hipLaunchKernelGGL(gram_sym_kernel<T>, dim3(nt * (nt + 1) / 2, sh.B), dim3(kGemmThreads), 0, st, sh, ws,
+                         hidden, 1.f / pr.tau_v, pr.norm_eps);
   } else {
     RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
     RowOperand<T> R{static_cast<const T*>(proj_v), sh.d, 0, nullptr, 0, sh.app_rank};

@@ -362,6 +362,9 @@ IMAGE_CASES = {
     "budget_below_images": dict(grids=[(6, 7), (5, 5), (4, 6), (3, 3)], t=8, k=2),
     # a batch of two problems with five small images each
     "batch_five_images": dict(grids=[(8, 8), (6, 9), (7, 7), (5, 5), (6, 6)], t=8, k=40, batch=2),
+    # three problems of two Qwen-size images: enough appearance tiles for the
+    # 128-row Gram kernel, with its image mask and ragged edge tiles
+    "batch_two_qwen_images": dict(grids=[(36, 36), (36, 36)], t=8, k=256, batch=3),
 }
 
 
