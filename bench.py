@@ -122,6 +122,9 @@ def main():
                     help="time budget of the oracle CPU baseline sample (0 disables)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration) and exit")
+    ap.add_argument("--serial", action="store_true",
+                    help="every kernel on the caller's stream for the whole run (stage-timing mode), for "
+                         "profilers whose counter passes serialize dispatches; not a throughput figure")
     ap.add_argument("--op", default="prune", choices=["prune", "compact"],
                     help="prune: the operator (default line); compact: sequence compaction and "
                          "prefix K/V gather after pruning")
@@ -165,6 +168,11 @@ def main():
         if code != 0:
             raise binding.GmcError(code, "gmc_prune")
 
+    if args.serial:
+        # the bank kernels then run on the caller's stream as well: no kernel
+        # waits for another stream's kernel, which a profiler that serializes
+        # dispatches would never start
+        binding._check(binding.gmc_timing_enable(True), "gmc_timing_enable")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -194,7 +202,7 @@ def main():
     for _ in range(args.steps):
         step()
     stage_ms, stage_n = binding.gmc_timing_read()
-    binding._check(binding.gmc_timing_enable(False), "gmc_timing_enable")
+    binding._check(binding.gmc_timing_enable(args.serial), "gmc_timing_enable")
     code, _ = binding.gmc_get_diag(0)
     if code != binding.GMC_OK:
         print(f"stage-timed calls failed on the device: {binding.gmc_last_error()}", file=sys.stderr)
@@ -231,7 +239,7 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "batch": w.batch, "N": w.n, "T": w.t,
                    "K": kr, "d": w.d, "heads": [w.hq, w.hkv], "head_dim": w.dh,
-                   "rounds": rounds, "client_rows": m_rows},
+                   "rounds": rounds, "client_rows": m_rows, **({"serial": True} if args.serial else {})},
         "roofline": roofline, "cpu_baseline": cpu, "stages": stages,
     }
     pr.close()
