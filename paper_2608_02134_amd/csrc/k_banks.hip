@@ -61,10 +61,17 @@ gram_sym_kernel(Shape sh, Ws ws, const T* hidden, float inv_tau, float norm_eps)
   __shared__ __attribute__((aligned(16))) T As[2][BM * P];
   __shared__ __attribute__((aligned(16))) T Bs[2][BM * P];
   __shared__ float rs_sum[2][BM], rs_max[2][BM], cs_sum[2][BM], cs_max[2][BM];
-  const int p = blockIdx.y;
-  // upper-triangle tile (I, J), I <= J, from the linear block index
-  const int nt = (sh.N + BM - 1) / BM;
-  int I = 0, rem = blockIdx.x;
+  // upper-triangle tile (I, J), I <= J, of problem p from the linear block
+  // index, in XCD-contiguous order: workgroups go to the eight XCDs round
+  // robin, so workgroup b takes entry (b % 8) * per + b / 8 of the (problem,
+  // tile) sequence and each XCD works through one contiguous range, whose
+  // tiles share operand rows in its own L2
+  const int nt = (sh.N + BM - 1) / BM, ntiles = nt * (nt + 1) / 2;
+  const int per = (ntiles * sh.B + 7) / 8;
+  const int f = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (f >= ntiles * sh.B) return;
+  const int p = f / ntiles;
+  int I = 0, rem = f % ntiles;
   while (rem >= nt - I) { rem -= nt - I; ++I; }
   const int J = I + rem;
   const int row0 = I * BM, col0 = J * BM;
@@ -476,39 +483,32 @@ __global__ void __launch_bounds__(256) appearance_alpha_kernel(Shape sh, Params 
   ws.peak[p * ws.s_m + sh.mg + r] = a * m;
 }
 
-// Grid origin/extent of (h, w) and the per-token spatial coordinates,
-// cell centres in [0,1]^2 (temporal id excluded), over each image's own grid
-// when the prompt has several images.
-__global__ void __launch_bounds__(256) spatial_coords_kernel(Shape sh, Ws ws, const int32_t* pos3d) {
+// Spatial bank, landmark side: one block per landmark l_ab = ((a+.5)/L,
+// (b+.5)/L) of image g (row g L^2 + a L + b; one image: g = 0).  The block
+// first takes the grid origin and extent of (h, w) over the image's tokens
+// (temporal id excluded) and places each token at its cell centre in
+// [0,1]^2; then the minimum squared distance to any token of the image, the
+// row sum of exp(-(d^2 - min d^2)/tau_s), the weight (beta_spa / M_S) / Z and
+// the peak (the row maximum is exactly 1).  The image's first landmark block
+// also stores the token coordinates for the token-side kernel.
+__device__ __forceinline__ float2 cell_centre(const int32_t* pos, int i, float h0, float w0, float gh, float gw) {
+  return make_float2((static_cast<float>(pos[i * 3 + 1]) - h0 + 0.5f) / gh,
+                     (static_cast<float>(pos[i * 3 + 2]) - w0 + 0.5f) / gw);
+}
+
+__global__ void __launch_bounds__(256) spatial_stats_kernel(Shape sh, Params pr, Ws ws, const int32_t* pos3d) {
   __shared__ float red[16];
-  __shared__ int bh0[kMaxImages], bh1[kMaxImages], bw0[kMaxImages], bw1[kMaxImages];
-  const int p = blockIdx.x;
+  const int row = blockIdx.x, p = blockIdx.y;
+  const int L = sh.landmarks, L2 = L * L;
+  const int g = row / L2, lr = row % L2;
+  const float ly = (static_cast<float>(lr / L) + 0.5f) / L;
+  const float lx = (static_cast<float>(lr % L) + 0.5f) / L;
   const int32_t* pos = pos3d + static_cast<long long>(p) * sh.N * 3;
-  float* pc = ws.pc + p * ws.s_pc;
-  if (sh.nimg > 1) {
-    const int* img = ws.img + p * ws.s_img;
-    if (threadIdx.x < kMaxImages) {
-      bh0[threadIdx.x] = 0x7fffffff; bh1[threadIdx.x] = -0x7fffffff;
-      bw0[threadIdx.x] = 0x7fffffff; bw1[threadIdx.x] = -0x7fffffff;
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
-      const int g = img[i];
-      atomicMin(&bh0[g], pos[i * 3 + 1]); atomicMax(&bh1[g], pos[i * 3 + 1]);
-      atomicMin(&bw0[g], pos[i * 3 + 2]); atomicMax(&bw1[g], pos[i * 3 + 2]);
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
-      const int g = img[i];
-      const float h0 = static_cast<float>(bh0[g]), w0 = static_cast<float>(bw0[g]);
-      const float gh = static_cast<float>(bh1[g]) - h0 + 1.f, gw = static_cast<float>(bw1[g]) - w0 + 1.f;
-      pc[2 * i] = (static_cast<float>(pos[i * 3 + 1]) - h0 + 0.5f) / gh;
-      pc[2 * i + 1] = (static_cast<float>(pos[i * 3 + 2]) - w0 + 0.5f) / gw;
-    }
-    return;
-  }
+  const int* img = ws.img + p * ws.s_img;
+  const bool multi = sh.nimg > 1;
   float hmin = INFINITY, hmax = -INFINITY, wmin = INFINITY, wmax = -INFINITY;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
+    if (multi && img[i] != g) continue;
     const float hh = static_cast<float>(pos[i * 3 + 1]), ww = static_cast<float>(pos[i * 3 + 2]);
     hmin = fminf(hmin, hh); hmax = fmaxf(hmax, hh);
     wmin = fminf(wmin, ww); wmax = fmaxf(wmax, ww);
@@ -518,40 +518,26 @@ __global__ void __launch_bounds__(256) spatial_coords_kernel(Shape sh, Ws ws, co
   wmin = block_min(wmin, red);
   wmax = block_max(wmax, red);
   const float gh = hmax - hmin + 1.f, gw = wmax - wmin + 1.f;
-  for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
-    pc[2 * i] = (static_cast<float>(pos[i * 3 + 1]) - hmin + 0.5f) / gh;
-    pc[2 * i + 1] = (static_cast<float>(pos[i * 3 + 2]) - wmin + 0.5f) / gw;
-  }
-}
-
-// Spatial bank, landmark side: one block per landmark l_ab = ((a+.5)/L,
-// (b+.5)/L) of image g (row g L^2 + a L + b; one image: g = 0): the minimum
-// squared distance to any token of the image, the row sum of
-// exp(-(d^2 - min d^2)/tau_s), the weight (beta_spa / M_S) / Z and the peak
-// (the row maximum is exactly 1).
-__global__ void __launch_bounds__(256) spatial_stats_kernel(Shape sh, Params pr, Ws ws) {
-  __shared__ float red[16];
-  const int row = blockIdx.x, p = blockIdx.y;
-  const int L = sh.landmarks, L2 = L * L;
-  const int g = row / L2, lr = row % L2;
-  const float ly = (static_cast<float>(lr / L) + 0.5f) / L;
-  const float lx = (static_cast<float>(lr % L) + 0.5f) / L;
-  const float* pc = ws.pc + p * ws.s_pc;
-  const int* img = ws.img + p * ws.s_img;
-  const bool multi = sh.nimg > 1;
   float dmin = INFINITY;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
     if (multi && img[i] != g) continue;
-    const float dy = pc[2 * i] - ly, dx = pc[2 * i + 1] - lx;
+    const float2 c = cell_centre(pos, i, hmin, wmin, gh, gw);
+    const float dy = c.x - ly, dx = c.y - lx;
     dmin = fminf(dmin, dy * dy + dx * dx);
   }
   dmin = block_min(dmin, red);
   const float inv_tau = 1.f / pr.tau_s;
   float s = 0.f;
+  float* pc = ws.pc + p * ws.s_pc;
   for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
     if (multi && img[i] != g) continue;
-    const float dy = pc[2 * i] - ly, dx = pc[2 * i + 1] - lx;
+    const float2 c = cell_centre(pos, i, hmin, wmin, gh, gw);
+    const float dy = c.x - ly, dx = c.y - lx;
     s += expf(-(dy * dy + dx * dx - dmin) * inv_tau);
+    if (lr == 0) {
+      pc[2 * i] = c.x;
+      pc[2 * i + 1] = c.y;
+    }
   }
   s = block_sum(s, red);
   if (threadIdx.x == 0) {
@@ -594,8 +580,7 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
   hipError_t err;
   auto spatial = [&]() {
     timer_mark(kStSpatial, true, st);
-    hipLaunchKernelGGL(spatial_coords_kernel, dim3(sh.B), dim3(256), 0, st, sh, ws, pos3d);
-    hipLaunchKernelGGL(spatial_stats_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws);
+    hipLaunchKernelGGL(spatial_stats_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws, pos3d);
     hipLaunchKernelGGL(spatial_write_kernel, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws);
     timer_mark(kStSpatial, false, st);
   };
@@ -626,9 +611,11 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
         big = true;
       }
     }
-    if (!big)
-      hipLaunchKernelGGL(gram_sym_kernel<T>, dim3(nt * (nt + 1) / 2, sh.B), dim3(kGemmThreads), 0, st, sh, ws,
-                         hidden, 1.f / pr.tau_v, pr.norm_eps);
+    if (!big) {
+      const int per = (nt * (nt + 1) / 2 * sh.B + 7) / 8;
+      hipLaunchKernelGGL(gram_sym_kernel<T>, dim3(8 * per), dim3(kGemmThreads), 0, st, sh, ws, hidden,
+                         1.f / pr.tau_v, pr.norm_eps);
+    }
   } else {
     RowOperand<T> A{hidden, sh.d, static_cast<long long>(sh.N) * sh.d, nullptr, 0, sh.N};
     RowOperand<T> R{static_cast<const T*>(proj_v), sh.d, 0, nullptr, 0, sh.app_rank};
