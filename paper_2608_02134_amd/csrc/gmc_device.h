@@ -70,6 +70,10 @@ __device__ __forceinline__ int wave_scan_and(int v) { GMC_WAVE_SCAN(int, dpp_i, 
 __device__ __forceinline__ int wave_scan_or(int v) { GMC_WAVE_SCAN(int, dpp_i, 0, op_or_i) }
 #undef GMC_WAVE_SCAN
 
+// The wave's index in its block as a wave-uniform (scalar) value, so that
+// tile indices derived from it branch and address in scalar registers.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6)); }
+
 __device__ __forceinline__ float lane63(float v) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }

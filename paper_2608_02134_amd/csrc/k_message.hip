@@ -222,7 +222,7 @@ struct LogitBlock {
     split = blockIdx.x % lsplit;
     rows_g = sh.hg * sh.T;
     lane = threadIdx.x & 63;
-    wave = threadIdx.x >> 6;
+    wave = wave_id();
     fr = lane & 15;
     fk = (lane >> 4) * 8;
     orow = (lane >> 4) * 4;
@@ -405,10 +405,12 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
       const int col = ct * 16 + lb.oc;
       if (col >= sh.N) continue;
       float v[4];
+      // atom norm l_h[col]: one per column when the lane's four rows share the head
+      const float nrm0 = vec ? sqrtf(lv[j][0] + sig2[0]) : 0.f;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float a = __expf(acc[e] * lb.scale - D[e]);
-        v[e] = a * sqrtf((vec ? lv[j][0] : lv[j][e]) + sig2[e]);   // atom norm l_h[col]
+        v[e] = a * (vec ? nrm0 : sqrtf(lv[j][e] + sig2[e]));
       }
       if (vec) {
         *reinterpret_cast<float4*>(E + static_cast<long long>(col) * sh.ldM + mrow[0]) =
@@ -487,7 +489,11 @@ constexpr bool logit_reg_ok() {
   return logit_waves<T, DH>() == 8 && (DH / 32) * static_cast<int>(sizeof(Frag<T>) / 4) <= 32;
 }
 
-template <typename T, int DH, int MAXT>
+// VEC (T a multiple of 16): the 16 rows of a block are one head's consecutive
+// queries, so a lane's four rows share the head, its atom norms and sigma
+// (one norm per column instead of four) and are four consecutive client rows
+// (one 16-byte store per tile).
+template <typename T, int DH, int MAXT, bool VEC>
 __global__ void __launch_bounds__(512)
 logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, const float* nonvis_lse) {
   constexpr int W = 8, MT = logit_chunk<T, DH>(), KS = DH / 32;
@@ -514,14 +520,24 @@ logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, c
   int hrow[4];
   long long mrow[4];
   bool rvalid[4];
+  if constexpr (VEC) {
+    // one head per block: its index and the first query are block-uniform
+    const int h = lb.g * sh.hg + lb.rb / sh.T, t0 = lb.rb % sh.T + lb.orow;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int rr = lb.rb + lb.orow + e;
-    rvalid[e] = rr < lb.rows_g;
-    hrow[e] = lb.g * sh.hg + (rvalid[e] ? rr / sh.T : 0);
-    mrow[e] = rvalid[e] ? lb.mrow(sh, lb.orow + e) : 0;
+    for (int e = 0; e < 4; ++e) {
+      rvalid[e] = lb.rb + lb.orow + e < lb.rows_g;
+      hrow[e] = h;
+      mrow[e] = static_cast<long long>(h) * sh.T + t0 + e;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int rr = lb.rb + lb.orow + e;
+      rvalid[e] = rr < lb.rows_g;
+      hrow[e] = lb.g * sh.hg + (rvalid[e] ? rr / sh.T : 0);
+      mrow[e] = rvalid[e] ? lb.mrow(sh, lb.orow + e) : 0;
+    }
   }
-  const bool vec = (sh.T & 15) == 0;
   const float* ell = ws.ell + lb.p * ws.s_ell;
   // logits s = q.k / sqrt(dh) of the wave's tiles wave, wave + W, ...:
   // chunks of MT tiles, every load of a chunk before its MFMAs
@@ -536,7 +552,7 @@ logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, c
       if (t < MAXT && ct < ntile) {
         lb.load_keys(sh, ct, kf[j]);
         const int col = min(ct * 16 + lb.oc, sh.N - 1);
-        if (vec) {
+        if constexpr (VEC) {
           lv[t][0] = ell[static_cast<long long>(hrow[0]) * sh.N + col];
         } else {
 #pragma unroll
@@ -618,9 +634,15 @@ logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, c
     const int ct = lb.wave + t * W, col = ct * 16 + lb.oc;
     if (ct >= ntile || col >= sh.N) continue;
     float v[4];
+    if constexpr (VEC) {
+      const float nrm = sqrtf(lv[t][0] + sig2[0]);   // atom norm l_h[col], shared by the four rows
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = __expf(sv[t][e] - D[e]) * sqrtf((vec ? lv[t][0] : lv[t][e]) + sig2[e]);
-    if (vec) {
+      for (int e = 0; e < 4; ++e) v[e] = __expf(sv[t][e] - D[e]) * nrm;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = __expf(sv[t][e] - D[e]) * sqrtf(lv[t][e] + sig2[e]);
+    }
+    if constexpr (VEC) {
       *reinterpret_cast<float4*>(E + static_cast<long long>(col) * sh.ldM + mrow[0]) = make_float4(v[0], v[1], v[2], v[3]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -1117,8 +1139,12 @@ static hipError_t message_view(const Shape& sv, const Params& pr, const Ws& wv, 
     case DH:                                                                                                   \
       if constexpr (logit_reg_ok<T, DH>()) {                                                                  \
         if (reg) {                                                                                             \
-          hipLaunchKernelGGL((logits_reg_kernel<T, DH, kLogitRegTiles>), lr, dim3(512), 0, st, sv, pv, wv, q, k, \
-                             nonvis_lse);                                                                      \
+          if ((sv.T & 15) == 0)                                                                                \
+            hipLaunchKernelGGL((logits_reg_kernel<T, DH, kLogitRegTiles, true>), lr, dim3(512), 0, st, sv, pv, wv, q, \
+                               k, nonvis_lse);                                                                 \
+          else                                                                                                 \
+            hipLaunchKernelGGL((logits_reg_kernel<T, DH, kLogitRegTiles, false>), lr, dim3(512), 0, st, sv, pv, wv, \
+                               q, k, nonvis_lse);                                                              \
           break;                                                                                               \
         }                                                                                                      \
       }                                                                                                        \
