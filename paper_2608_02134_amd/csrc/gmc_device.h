@@ -316,6 +316,14 @@ __device__ __forceinline__ bool last_arrival(int* counter, int total, int* flag)
   return *flag != 0;
 }
 
+// Four floats from a 16-byte aligned address with a non-temporal (streaming)
+// load: data read once that should not displace cached lines.
+__device__ __forceinline__ float4 ld_stream4(const float* ptr) {
+  typedef float f32x4_t __attribute__((ext_vector_type(4)));
+  const f32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(ptr));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
 // Order-preserving key of a non-negative float score (larger score -> larger
 // key); 0 is reserved for excluded candidates.
 __device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(fmaxf(s, 0.f)) + 1u; }

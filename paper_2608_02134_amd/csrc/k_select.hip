@@ -28,7 +28,7 @@
 
 namespace gmc {
 
-constexpr int kCpw = 2;                 // gains kernel: tokens per wave
+constexpr int kCpw = 4;                 // gains kernel: tokens per wave
 constexpr int kGainCols = 4 * kCpw;     // tokens per block
 constexpr int kCpwF = 4;                // fused gains kernel: tokens per wave
 constexpr int kGainColsF = 4 * kCpwF;
@@ -133,16 +133,19 @@ __device__ void block_topk256(const uint32_t* keys, int n, int count, int* out, 
 // non-zero key >= the resolved prefix) or every bit is resolved (the
 // threshold is one key value, its first `remaining` copies by index taken).
 // Every wave scans the histograms itself, so a radix pass needs one block
-// barrier (three histogram buffers rotate).  The selected indices are
-// written to out[0, count) in ascending index order and out[count, 64) is
-// filled with index 0.
-// hist: 768 ints of LDS, scan: >= 16 ints.
-template <int KPT>
-__device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, int* out, int* hist, int* scan) {
+// barrier (three histogram buffers rotate).  The block has NW >= 4 waves.
+// The selected indices are written to out[0, count) in ascending index order
+// and out[count, fill) is filled with index 0.
+// hist: 768 ints of LDS, scan: >= 3 NW ints.
+template <int KPT, int NW = 4>
+__device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, int* out, int* hist, int* scan,
+                                int fill = 64) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  hist[tid] = 0;
-  hist[256 + tid] = 0;
-  hist[512 + tid] = 0;
+  if (tid < 256) {
+    hist[tid] = 0;
+    hist[256 + tid] = 0;
+    hist[512 + tid] = 0;
+  }
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
 #pragma unroll
   for (int q = 0; q < KPT; ++q) {
@@ -151,12 +154,15 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
   }
   kand = wave_and_u(kand);
   kor = wave_or_u(kor);
-  if (lane == 0) { scan[wave] = static_cast<int>(kand); scan[4 + wave] = static_cast<int>(kor); }
+  if (lane == 0) { scan[wave] = static_cast<int>(kand); scan[NW + wave] = static_cast<int>(kor); }
   __syncthreads();
-  kand = static_cast<uint32_t>(scan[0]) & static_cast<uint32_t>(scan[1]) & static_cast<uint32_t>(scan[2]) &
-         static_cast<uint32_t>(scan[3]);
-  kor = static_cast<uint32_t>(scan[4]) | static_cast<uint32_t>(scan[5]) | static_cast<uint32_t>(scan[6]) |
-        static_cast<uint32_t>(scan[7]);
+  kand = static_cast<uint32_t>(scan[0]);
+  kor = static_cast<uint32_t>(scan[NW]);
+#pragma unroll
+  for (int w = 1; w < NW; ++w) {
+    kand &= static_cast<uint32_t>(scan[w]);
+    kor |= static_cast<uint32_t>(scan[NW + w]);
+  }
   const uint32_t diff = kand ^ kor;
   // bits [hi, 32) are shared by every non-zero key; with no differing bit
   // every non-zero key equals kand
@@ -172,7 +178,7 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
     for (int q = 0; q < KPT; ++q)
       if (k[q] != 0u && (k[q] & mask) == prefix) atomicAdd(&h[(k[q] & wmask) >> lo], 1);
     const int nxt = buf == 2 ? 0 : buf + 1;
-    hist[nxt * 256 + tid] = 0;   // last read two passes ago
+    if (tid < 256) hist[nxt * 256 + tid] = 0;   // last read two passes ago
     __syncthreads();
     int v[4], loc = 0;
 #pragma unroll
@@ -214,13 +220,13 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
     eq += k[q] != 0u && k[q] == kth;
   }
   // exclusive prefix of (gt, eq) over threads: wave scans, then the wave
-  // totals (scan[12..15], untouched earlier in the call) after one barrier
+  // totals (scan[2 NW, 3 NW), untouched earlier in the call) after one barrier
   const int v = gt | (eq << 16);
   const int incl = wave_scan_add(v);
-  if (lane == 63) scan[12 + wave] = incl;
+  if (lane == 63) scan[2 * NW + wave] = incl;
   __syncthreads();
   int pre = incl - v;
-  for (int w = 0; w < wave; ++w) pre += scan[12 + w];
+  for (int w = 0; w < wave; ++w) pre += scan[2 * NW + w];
   int gt_b = static_cast<int>(static_cast<unsigned>(pre) & 0xFFFFu);
   int eq_b = static_cast<int>(static_cast<unsigned>(pre) >> 16);
   const int i0 = tid * seg;
@@ -235,7 +241,7 @@ __device__ void block_topk_regs(const uint32_t (&k)[KPT], int seg, int count, in
       ++eq_b;
     }
   }
-  if (tid >= count && tid < 64) out[tid] = 0;
+  if (tid >= count && tid < fill) out[tid] = 0;
   __syncthreads();
 }
 
@@ -259,7 +265,12 @@ __global__ void __launch_bounds__(256) cov_kernel(Shape sh, Ws ws, int nb) {
 // ---------------------------------------------------------------------------
 // singleton gains and the pool
 // ---------------------------------------------------------------------------
-template <bool kGlobalKeys>
+// Singleton gains u_i = sum_m alpha_m max(E_mi - b_m, 0) of every token, four
+// per wave; the client rows are streamed with non-temporal loads (the matrix
+// is read once per round and is larger than the caches).  With kTail the last block to finish picks the pool itself (keys
+// in LDS, or in global memory for large N); without it pool_topk_kernel
+// follows.
+template <bool kGlobalKeys, bool kTail = true>
 __global__ void __launch_bounds__(256)
 gains_kernel(Shape sh, Ws ws, int round, int psize, SelOut so) {
   extern __shared__ uint32_t keys_lds[];
@@ -284,7 +295,7 @@ gains_kernel(Shape sh, Ws ws, int round, int psize, SelOut so) {
     const float4 b = *reinterpret_cast<const float4*>(cov + m);
 #pragma unroll
     for (int c = 0; c < kCpw; ++c) {
-      const float4 v = *reinterpret_cast<const float4*>(col[c] + m);
+      const float4 v = ld_stream4(col[c] + m);
       acc[c] += fmaxf(a.x * v.x - b.x, 0.f);
       acc[c] += fmaxf(a.y * v.y - b.y, 0.f);
       acc[c] += fmaxf(a.z * v.z - b.z, 0.f);
@@ -296,6 +307,7 @@ gains_kernel(Shape sh, Ws ws, int round, int psize, SelOut so) {
     const float s = wave_sum(acc[c]);
     if (lane == 0 && col0 + c < sh.N) st_dev(&u[col0 + c], s);
   }
+  if constexpr (!kTail) return;
 
   // tail: the pool, the psize largest gains among unselected tokens
   int* cnt = ws.cnt + p * ws.s_cnt;
@@ -329,6 +341,52 @@ gains_kernel(Shape sh, Ws ws, int round, int psize, SelOut so) {
   if (so.pool) {
     int32_t* tp = so.pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
     for (int j = tid; j < sh.pool_cap; j += 256) tp[j] = (j < psize) ? pool[j] : -1;
+  }
+}
+
+// The pool of a per-round call: the psize largest gains among unselected
+// tokens, ascending by index, equal gains resolved to the lower index (the
+// same selection as the gains kernel's tail).  One 1024-thread block per
+// problem: the keys are made from coalesced loads into LDS (dynamic, N
+// words), then thread t takes tokens [t seg, t seg + seg) into registers
+// (seg <= KPT), so every radix pass works on registers and LDS histograms.
+constexpr int kPoolW = 16;   // waves of the pool top-k block
+template <int KPT>
+__global__ void __launch_bounds__(64 * kPoolW) pool_topk_kernel(Shape sh, Ws ws, int round, int psize,
+                                                                 SelOut so) {
+  extern __shared__ uint32_t keys_lds[];
+  __shared__ int hist[768], scan[3 * kPoolW];
+  const int p = blockIdx.x, tid = threadIdx.x;
+  const float* u = ws.u + p * ws.s_u;
+  const int* sel = ws.sel + p * ws.s_sel;
+  constexpr int kT = 64 * kPoolW;
+  float g[KPT];
+  int sl[KPT];
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    const int i = min(q * kT + tid, sh.N - 1);
+    g[q] = u[i];
+    sl[q] = sel[i];
+  }
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    const int i = q * kT + tid;
+    if (i < sh.N) {
+      keys_lds[i] = sl[q] < 0 ? score_key(g[q]) : 0u;
+      if (so.gains) so.gains[(static_cast<long long>(p) * sh.rounds + round) * sh.N + i] = (sl[q] >= 0) ? 0.f : g[q];
+    }
+  }
+  __syncthreads();
+  const int seg = (sh.N + kT - 1) / kT;
+  const int i0 = tid * seg;
+  uint32_t k[KPT];
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) k[q] = (q < seg && i0 + q < sh.N) ? keys_lds[i0 + q] : 0u;
+  int* pool = ws.pool + p * ws.s_pool;
+  block_topk_regs<KPT, kPoolW>(k, seg, psize, pool, hist, scan, 0);
+  if (so.pool) {
+    int32_t* tp = so.pool + (static_cast<long long>(p) * sh.rounds + round) * sh.pool_cap;
+    for (int j = tid; j < sh.pool_cap; j += 64 * kPoolW) tp[j] = (j < psize) ? pool[j] : -1;
   }
 }
 
@@ -634,9 +692,11 @@ __global__ void __launch_bounds__(256) resp_small_kernel(Shape sh, Params pr, Ws
 }
 
 // Large pools: per-row max mu_m and softmax denominator over the pool.
-// Block = 64 rows (lane = row) x 4 waves splitting the pool positions.
-__global__ void __launch_bounds__(256) rowstat_kernel(Shape sh, Params pr, Ws ws, int psize) {
-  __shared__ float part[4][64];
+// Block = 64 rows (lane = row) x 16 waves splitting the pool positions (the
+// grid is only m / 64 blocks, so the waves supply the loads in flight).
+constexpr int kRsW = 16;
+__global__ void __launch_bounds__(64 * kRsW) rowstat_kernel(Shape sh, Params pr, Ws ws, int psize) {
+  __shared__ float part[kRsW][64];
   __shared__ float mu_s[64];
   const int p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m = blockIdx.x * 64 + lane;
@@ -645,13 +705,18 @@ __global__ void __launch_bounds__(256) rowstat_kernel(Shape sh, Params pr, Ws ws
   const float c = row_ok ? ws.cov[p * ws.s_cov + m] : 0.f;
   const float* E = ws.E + p * ws.s_E + (row_ok ? m : 0);
   const int* pool = ws.pool + p * ws.s_pool;
-  const int q = (psize + 3) / 4, j0 = wave * q, j1 = min(psize, j0 + q);
+  const int q = (psize + kRsW - 1) / kRsW, j0 = wave * q, j1 = min(psize, j0 + q);
   float mx = 0.f;
 #pragma unroll 8
   for (int j = j0; j < j1; ++j) mx = fmaxf(mx, fmaxf(a * E[static_cast<long long>(pool[j]) * sh.ldM] - c, 0.f));
   part[wave][lane] = mx;
   __syncthreads();
-  if (wave == 0) mu_s[lane] = fmaxf(fmaxf(part[0][lane], part[1][lane]), fmaxf(part[2][lane], part[3][lane]));
+  if (wave == 0) {
+    float mm = part[0][lane];
+#pragma unroll
+    for (int w = 1; w < kRsW; ++w) mm = fmaxf(mm, part[w][lane]);
+    mu_s[lane] = mm;
+  }
   __syncthreads();
   const float mu = mu_s[lane];
   const float inv = mu > 0.f ? 1.f / (pr.tau_r * mu + pr.resp_eps) : 0.f;
@@ -665,7 +730,9 @@ __global__ void __launch_bounds__(256) rowstat_kernel(Shape sh, Params pr, Ws ws
   part[wave][lane] = den;
   __syncthreads();
   if (wave == 0 && row_ok) {
-    const float d = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+    float d = part[0][lane];
+#pragma unroll
+    for (int w = 1; w < kRsW; ++w) d += part[w][lane];
     float* rs = ws.rstat + p * ws.s_rstat;
     rs[m] = inv;
     rs[sh.ldM + m] = zmax;
@@ -1393,6 +1460,12 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, con
   }
   const bool global_keys = sh.N > kLdsKeys;
   const size_t key_lds = global_keys ? 0 : static_cast<size_t>(sh.N) * sizeof(uint32_t);
+  // unfused rounds pick the pool in a 1024-thread register top-k kernel
+  // (keys per thread: 4, 8 or 16); beyond 16 * 1024 tokens the gains
+  // kernel's last block does it over keys in global memory
+  const int pool_seg = (sh.N + 64 * kPoolW - 1) / (64 * kPoolW);
+  const int pool_kpt = pool_seg <= 4 ? 4 : pool_seg <= 8 ? 8 : pool_seg <= 16 ? 16 : 0;
+  static int pool_lds_granted = 48 * 1024;
   const size_t fused_lds = static_cast<size_t>(sh.ldM) * sizeof(float) + key_lds;
   // small pools fuse the batch pick and the coverage refresh into the gains
   // kernel while the refreshed coverage fits in LDS next to the keys
@@ -1427,17 +1500,35 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, con
         timer_mark(kStCov, false, st);
       }
       timer_mark(kStGains, true, st);
-      if (global_keys)
+      if (pool_kpt > 0) {
+        hipLaunchKernelGGL((gains_kernel<true, false>), gg, dim3(256), 0, st, sh, ws, r, psize, so);
+        const dim3 gp(sh.B), bp(64 * kPoolW);
+        const size_t pl = static_cast<size_t>(sh.N) * sizeof(uint32_t);
+        if (pool_kpt == 16 && static_cast<int>(pl) > pool_lds_granted) {
+          // 64 KB of keys next to the static histograms: grant the dynamic LDS once
+          const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(pool_topk_kernel<16>),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(pl));
+          if (e != hipSuccess) return e;
+          pool_lds_granted = static_cast<int>(pl);
+        }
+        if (pool_kpt == 4)
+          hipLaunchKernelGGL(pool_topk_kernel<4>, gp, bp, pl, st, sh, ws, r, psize, so);
+        else if (pool_kpt == 8)
+          hipLaunchKernelGGL(pool_topk_kernel<8>, gp, bp, pl, st, sh, ws, r, psize, so);
+        else
+          hipLaunchKernelGGL(pool_topk_kernel<16>, gp, bp, pl, st, sh, ws, r, psize, so);
+      } else if (global_keys) {
         hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, so);
-      else
+      } else {
         hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, so);
+      }
       timer_mark(kStGains, false, st);
       timer_mark(kStResp, true, st);
       if (sh.pool_cap <= 64)
         hipLaunchKernelGGL(resp_small_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws,
                            psize);
       else {
-        hipLaunchKernelGGL(rowstat_kernel, dim3((sh.m + 63) / 64, sh.B), dim3(256), 0, st, sh, pr, ws, psize);
+        hipLaunchKernelGGL(rowstat_kernel, dim3((sh.m + 63) / 64, sh.B), dim3(64 * kRsW), 0, st, sh, pr, ws, psize);
         hipLaunchKernelGGL(colsum_kernel, dim3((psize + 3) / 4, sh.B), dim3(256),
                            static_cast<size_t>(sh.pool_cap) * sizeof(uint32_t), st, sh, ws, r, psize, bsize,
                            selected, so);

@@ -25,9 +25,10 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
   constexpr int kPiQ = 8;                 // assignment entries per thread and pass
   __shared__ unsigned long long masks[kPiQ][4];
   __shared__ int members[kPiQ * 256];
+  __shared__ float weights[kPiQ * 256];
   __shared__ float red[16];
   const int jj = blockIdx.x, p = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const unsigned long long below = (1ull << lane) - 1ull;
   const int j = ws.sup[p * ws.s_sup + jj];
   const int* pi = ws.pi + p * ws.s_pi;
@@ -54,41 +55,50 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
   float mass = 0.f;
   for (int base = 0; base < sh.N; base += kPiQ * 256) {
-    // the ordered member list of this pass (ascending source index): every
-    // assignment load in flight, one ballot per 256 tokens
+    // the ordered member list of this pass (ascending source index) with each
+    // member's population weight m_i: the assignment and ebar loads of the
+    // pass are all in flight together, one ballot per 256 tokens
     int pv[kPiQ];
+    float ev[kPiQ];
 #pragma unroll
     for (int q = 0; q < kPiQ; ++q) {
       const int i = base + q * 256 + tid;
       pv[q] = i < sh.N ? pi[i] : -1;
+      ev[q] = i < sh.N ? eb[i] : 0.f;
     }
     unsigned long long bal[kPiQ];
 #pragma unroll
     for (int q = 0; q < kPiQ; ++q) bal[q] = __ballot(pv[q] == j);
-    __syncthreads();   // the previous pass is done with masks and members
+    __syncthreads();   // the previous pass is done with masks, members and weights
     if (lane == 0)
 #pragma unroll
       for (int q = 0; q < kPiQ; ++q) masks[q][wave] = bal[q];
     __syncthreads();
-    int total = 0;
+    // offsets of the 4 * kPiQ ballot words (order q-major, then wave): lane
+    // l < 32 of every wave counts word l, one wave scan gives the prefixes
+    const int cnt = lane < 4 * kPiQ ? __popcll(masks[lane >> 2][lane & 3]) : 0;
+    const int incl = wave_scan_add(cnt);
+    const int total = __builtin_amdgcn_readlane(incl, 4 * kPiQ - 1);
 #pragma unroll
-    for (int q = 0; q < kPiQ; ++q)
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const int c = __popcll(masks[q][w]);
-        if (w == wave && ((bal[q] >> lane) & 1ull)) members[total + __popcll(bal[q] & below)] = base + q * 256 + tid;
-        total += c;
+    for (int q = 0; q < kPiQ; ++q) {
+      const int w = q * 4 + wave;
+      const int off = __builtin_amdgcn_readlane(incl - cnt, w);
+      if ((bal[q] >> lane) & 1ull) {
+        const int slot = off + __popcll(bal[q] & below);
+        members[slot] = base + q * 256 + tid;
+        weights[slot] = m0 + m1 * (inv_mean > 0.f ? ev[q] * inv_mean : 1.f);
       }
+    }
     __syncthreads();
     for (int b0 = 0; b0 < total; b0 += kMB) {
-      // all member rows of the batch are loaded before any accumulation
+      // every member row of the batch is requested before any accumulation;
+      // slots past the list end repeat its last row with weight 0, which
+      // leaves the fp32 sums bit-identical (finite rows) and keeps the
+      // accumulation free of branches, so the loads are not sunk into them
       uint4 raw[kMB][G][CH];
-      float mi[kMB];
 #pragma unroll
       for (int q = 0; q < kMB; ++q) {
-        if (b0 + q >= total) break;
-        const int ii = members[b0 + q];
-        mi[q] = m0 + m1 * (inv_mean > 0.f ? eb[ii] * inv_mean : 1.f);
+        const int ii = members[min(b0 + q, total - 1)];
         const T* row = H + static_cast<long long>(ii) * sh.d;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -99,19 +109,19 @@ transport_kernel(Shape sh, Params pr, Ws ws, const T* hidden, const int32_t* pos
       }
 #pragma unroll
       for (int q = 0; q < kMB; ++q) {
-        if (b0 + q >= total) break;
-        mass += mi[q];
+        const float mi = b0 + q < total ? weights[b0 + q] : 0.f;
+        mass += mi;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           if constexpr (sizeof(T) == 2) {
             const bf16_t* v = reinterpret_cast<const bf16_t*>(&raw[q][g][0]);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[g][e] += mi[q] * bf16_to_f32(v[e]);
+            for (int e = 0; e < 8; ++e) acc[g][e] += mi * bf16_to_f32(v[e]);
           } else {
             const float* v = reinterpret_cast<const float*>(&raw[q][g][0]);
             const float* v2 = reinterpret_cast<const float*>(&raw[q][g][1]);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) { acc[g][e] += mi[q] * v[e]; acc[g][e + 4] += mi[q] * v2[e]; }
+            for (int e = 0; e < 4; ++e) { acc[g][e] += mi * v[e]; acc[g][e + 4] += mi * v2[e]; }
           }
         }
       }
