@@ -478,6 +478,294 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   if (threadIdx.x == 0) st_dev(cnt, 0);
 }
 
+// Wide-row form of the same two kernels (bf16, head_dim <= 128, T a
+// multiple of 16).  A block covers 64 consecutive rows of one kv group (four
+// 16-row fragments, each inside one head) and one column range: every key
+// tile read from L2 feeds four MFMA row fragments, and a token's 64 grounded
+// entries (client rows g * hg * T + rb .. + 63, 256 contiguous bytes of its
+// row of E) are written by one block, so the lines reach HBM whole.
+constexpr int kWideRows = 64;             // rows per wide block
+constexpr int kWideFr = kWideRows / 16;   // MFMA row fragments
+constexpr int kWideW = 4;                 // waves per wide block
+constexpr int kWideMT = 2;                // key tiles per wave and chunk
+
+template <int DH>
+struct WideBlock {
+  static constexpr int KS = DH / 32;
+  int p, g, rb, split, rows_g, nfr, t_beg, t_end;
+  int lane, wave, fr, fk, orow, oc;
+  float scale;
+  const bf16_t* kbase;
+  long long kstride;
+  Frag<bf16_t> qf[kWideFr][KS];
+
+  __device__ WideBlock(const Shape& sh, const bf16_t* text_q, const bf16_t* vis_k, int lsplit) {
+    p = blockIdx.z;
+    g = blockIdx.y;
+    rb = (blockIdx.x / lsplit) * kWideRows;
+    split = blockIdx.x % lsplit;
+    rows_g = sh.hg * sh.T;                       // a multiple of 16
+    nfr = min(kWideFr, (rows_g - rb) / 16);      // fragments holding rows
+    lane = threadIdx.x & 63;
+    wave = wave_id();
+    fr = lane & 15;
+    fk = (lane >> 4) * 8;
+    orow = (lane >> 4) * 4;
+    oc = lane & 15;
+    scale = rsqrtf(static_cast<float>(DH));
+    const int ntile = (sh.N + 15) / 16, tps = (ntile + lsplit - 1) / lsplit;
+    t_beg = min(ntile, split * tps);
+    t_end = min(ntile, t_beg + tps);
+#pragma unroll
+    for (int f = 0; f < kWideFr; ++f) {
+      if (f < nfr) {
+        const int rr = rb + f * 16 + fr;
+        const int h = g * sh.hg + rr / sh.T, t = rr % sh.T;
+        const bf16_t* q = text_q + ((static_cast<long long>(p) * sh.T + t) * sh.hq + h) * DH;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[f][ks] = frag_load<bf16_t>(q + ks * 32 + fk);
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[f][ks] = frag_zero<bf16_t>();
+      }
+    }
+    kbase = vis_k + static_cast<long long>(p) * sh.N * sh.hkv * DH + g * DH;
+    kstride = static_cast<long long>(sh.hkv) * DH;
+  }
+  __device__ void load_keys(const Shape& sh, int ct, Frag<bf16_t>* kf) const {
+    const int col = min(ct * 16 + fr, sh.N - 1);
+    const bf16_t* kr = kbase + col * kstride;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = frag_load<bf16_t>(kr + ks * 32 + fk);
+  }
+  __device__ floatx4 tile_mma(int f, const Frag<bf16_t>* kf) const {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) acc = mma(qf[f][ks], kf[ks], acc);
+    return acc;
+  }
+  // client row of block row 0: rows of a group are consecutive client rows
+  __device__ long long mrow0(const Shape& sh) const { return static_cast<long long>(g) * rows_g + rb; }
+};
+
+template <int DH>
+__global__ void __launch_bounds__(64 * kWideW)
+logits_lse_wide_kernel(Shape sh, Params pr, Ws ws, const bf16_t* text_q, const bf16_t* vis_k) {
+  constexpr int KS = DH / 32;
+  __shared__ float sm_m[kWideW][kWideRows], sm_s[kWideW][kWideRows];
+  const WideBlock<DH> lb(sh, text_q, vis_k, sh.lsplit);
+  // online (max, sum) per row in the base-2 domain (y = s log2 e), one
+  // rescale per chunk: the chunk's tiles are reduced against a common maximum
+  const float c2 = lb.scale * 1.44269504088896341f;
+  float mx[kWideFr][4], sm[kWideFr][4];
+#pragma unroll
+  for (int f = 0; f < kWideFr; ++f)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { mx[f][e] = -INFINITY; sm[f][e] = 0.f; }
+  for (int c0 = lb.t_beg + lb.wave; c0 < lb.t_end; c0 += kWideMT * kWideW) {
+    Frag<bf16_t> kf[kWideMT][KS];
+#pragma unroll
+    for (int j = 0; j < kWideMT; ++j) lb.load_keys(sh, min(c0 + j * kWideW, lb.t_end - 1), kf[j]);
+#pragma unroll
+    for (int f = 0; f < kWideFr; ++f) {
+      if (f >= lb.nfr) continue;
+      float y[kWideMT][4];
+#pragma unroll
+      for (int j = 0; j < kWideMT; ++j) {
+        const int ct = c0 + j * kWideW;
+        if (ct < lb.t_end) {   // wave-uniform: the MFMAs run on full waves
+          const floatx4 acc = lb.tile_mma(f, kf[j]);
+          const bool colok = ct * 16 + lb.oc < sh.N;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[j][e] = colok ? acc[e] * c2 : -INFINITY;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[j][e] = -INFINITY;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float cm = y[0][e];
+#pragma unroll
+        for (int j = 1; j < kWideMT; ++j) cm = fmaxf(cm, y[j][e]);
+        if (cm == -INFINITY) continue;
+        const float nm = fmaxf(mx[f][e], cm);
+        float acc_s = sm[f][e] * __builtin_amdgcn_exp2f(mx[f][e] - nm);
+#pragma unroll
+        for (int j = 0; j < kWideMT; ++j) acc_s += __builtin_amdgcn_exp2f(y[j][e] - nm);
+        sm[f][e] = acc_s;
+        mx[f][e] = nm;
+      }
+    }
+  }
+  // merge across the 16 lanes of a row group and across waves; the maxima
+  // go back to the natural-log domain
+#pragma unroll
+  for (int f = 0; f < kWideFr; ++f)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float m = group16_max(mx[f][e]);
+      const float sc = (mx[f][e] == -INFINITY) ? 0.f : sm[f][e] * __builtin_amdgcn_exp2f(mx[f][e] - m);
+      const float t = group16_sum(sc);
+      if (lb.oc == 0) {
+        sm_m[lb.wave][f * 16 + lb.orow + e] = m * 0.69314718055994531f;
+        sm_s[lb.wave][f * 16 + lb.orow + e] = t;
+      }
+    }
+  __syncthreads();
+  if (threadIdx.x < kWideRows) {
+    const int r = threadIdx.x;
+    if (lb.rb + r < lb.rows_g) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kWideW; ++w) m = fmaxf(m, sm_m[w][r]);
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWideW; ++w) s += (sm_m[w][r] == -INFINITY) ? 0.f : sm_s[w][r] * __expf(sm_m[w][r] - m);
+      float* part = ws.lpart + lb.p * ws.s_lpart;
+      const long long mi = lb.mrow0(sh) + r;
+      part[static_cast<long long>(lb.split) * sh.mg + mi] = m;
+      part[static_cast<long long>(kLogitSplit + lb.split) * sh.mg + mi] = s;
+    }
+  }
+  if (blockIdx.x == 0 && blockIdx.y == 0) sigma_from_partials(sh, pr, ws, lb.p);
+}
+
+template <int DH>
+__global__ void __launch_bounds__(64 * kWideW)
+logits_wide_kernel(Shape sh, Ws ws, const bf16_t* text_q, const bf16_t* vis_k, const float* nonvis_lse) {
+  constexpr int KS = DH / 32;
+  __shared__ float sm_m[kWideW][kWideRows], sm_s[kWideW][kWideRows];
+  __shared__ float sm_D[kWideRows];
+  const WideBlock<DH> lb(sh, text_q, vis_k, sh.lsplit);
+  float* part = ws.lpart + lb.p * ws.s_lpart;
+  const long long m0 = lb.mrow0(sh);
+  if (threadIdx.x < kWideRows) {
+    // the row's log-sum-exp from the per-range partials, in range order
+    const int r = threadIdx.x, rr = lb.rb + r;
+    float D = 0.f;
+    if (rr < lb.rows_g) {
+      const long long mi = m0 + r;
+      float m = -INFINITY;
+      for (int s = 0; s < sh.lsplit; ++s) m = fmaxf(m, part[static_cast<long long>(s) * sh.mg + mi]);
+      float sum = 0.f;
+      for (int s = 0; s < sh.lsplit; ++s) {
+        const float ms = part[static_cast<long long>(s) * sh.mg + mi];
+        sum += (ms == -INFINITY) ? 0.f : part[static_cast<long long>(kLogitSplit + s) * sh.mg + mi] * expf(ms - m);
+      }
+      D = m + logf(sum);
+      if (nonvis_lse) {
+        const int h = lb.g * sh.hg + rr / sh.T, t = rr % sh.T;
+        const float nv = nonvis_lse[(static_cast<long long>(lb.p) * sh.hq + h) * sh.T + t];
+        const float hi = fmaxf(D, nv), lo = fminf(D, nv);
+        D = (hi == -INFINITY) ? hi : hi + log1pf(expf(lo - hi));
+      }
+    }
+    sm_D[r] = D;
+  }
+  __syncthreads();
+  // e = A * l, written to the grounded client rows; row sums / maxima
+  float D[kWideFr][4], rsum[kWideFr][4], rmax[kWideFr][4], sig2[kWideFr];
+  int hf[kWideFr];
+#pragma unroll
+  for (int f = 0; f < kWideFr; ++f) {
+    hf[f] = lb.g * sh.hg + (f < lb.nfr ? (lb.rb + f * 16) / sh.T : 0);   // the fragment's head
+    const float sg = ws.sig[lb.p * ws.s_sig + hf[f]];
+    sig2[f] = sg * sg;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      D[f][e] = sm_D[f * 16 + lb.orow + e] * 1.44269504088896341f;   // base 2
+      rsum[f][e] = 0.f;
+      rmax[f][e] = 0.f;
+    }
+  }
+  float* E = ws.E + lb.p * ws.s_E;
+  const float* ell = ws.ell + lb.p * ws.s_ell;
+  const float c2 = lb.scale * 1.44269504088896341f;
+  for (int c0 = lb.t_beg + lb.wave; c0 < lb.t_end; c0 += kWideMT * kWideW) {
+    Frag<bf16_t> kf[kWideMT][KS];
+    float lv[kWideMT][kWideFr];
+#pragma unroll
+    for (int j = 0; j < kWideMT; ++j) {
+      const int ct = min(c0 + j * kWideW, lb.t_end - 1);
+      lb.load_keys(sh, ct, kf[j]);
+      const int col = min(ct * 16 + lb.oc, sh.N - 1);
+#pragma unroll
+      for (int f = 0; f < kWideFr; ++f) lv[j][f] = ell[static_cast<long long>(hf[f]) * sh.N + col];
+    }
+#pragma unroll
+    for (int j = 0; j < kWideMT; ++j) {
+      const int ct = c0 + j * kWideW;
+      if (ct >= lb.t_end) continue;   // wave-uniform: the MFMAs run on full waves
+      const int col = ct * 16 + lb.oc;
+      const bool colok = col < sh.N;
+      float* ecol = E + static_cast<long long>(colok ? col : 0) * sh.ldM + m0 + lb.orow;
+#pragma unroll
+      for (int f = 0; f < kWideFr; ++f) {
+        if (f >= lb.nfr) continue;
+        const floatx4 acc = lb.tile_mma(f, kf[j]);
+        if (!colok) continue;
+        const float nrm = sqrtf(lv[j][f] + sig2[f]);
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = __builtin_amdgcn_exp2f(acc[e] * c2 - D[f][e]) * nrm;
+          rsum[f][e] += v[e];
+          rmax[f][e] = fmaxf(rmax[f][e], v[e]);
+        }
+        *reinterpret_cast<float4*>(ecol + f * 16) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    }
+  }
+#pragma unroll
+  for (int f = 0; f < kWideFr; ++f)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float s = group16_sum(rsum[f][e]);
+      const float m = group16_max(rmax[f][e]);
+      if (lb.oc == 0) { sm_s[lb.wave][f * 16 + lb.orow + e] = s; sm_m[lb.wave][f * 16 + lb.orow + e] = m; }
+    }
+  __syncthreads();
+  const int r = threadIdx.x;
+  const bool row = r < kWideRows && lb.rb + r < lb.rows_g;
+  const long long mi = m0 + (row ? r : 0);
+  float s = 0.f, m = 0.f;
+  if (row)
+#pragma unroll
+    for (int w = 0; w < kWideW; ++w) { s += sm_s[w][r]; m = fmaxf(m, sm_m[w][r]); }
+  if (sh.lsplit == 1) {
+    if (row) {
+      ws.rowsum[lb.p * ws.s_m + mi] = s;
+      ws.peak[lb.p * ws.s_m + mi] = m;
+    }
+    return;
+  }
+  // the last of the row block's ranges adds the range partials in range order
+  if (row) {
+    st_dev(&part[static_cast<long long>(2 * kLogitSplit + lb.split) * sh.mg + mi], s);
+    st_dev(&part[static_cast<long long>(3 * kLogitSplit + lb.split) * sh.mg + mi], m);
+  }
+  __shared__ int flag;
+  int* cnt = ws.lcnt + lb.p * ws.s_lcnt + (blockIdx.x / sh.lsplit) * sh.hkv + lb.g;
+  if (!last_arrival(cnt, sh.lsplit, &flag)) return;
+  if (row) {
+    float vs[kLogitSplit], vm[kLogitSplit];
+#pragma unroll
+    for (int q = 0; q < kLogitSplit; ++q) {
+      const int qc = min(q, sh.lsplit - 1);
+      vs[q] = ld_dev(&part[static_cast<long long>(2 * kLogitSplit + qc) * sh.mg + mi]);
+      vm[q] = ld_dev(&part[static_cast<long long>(3 * kLogitSplit + qc) * sh.mg + mi]);
+    }
+    float ts = 0.f, tm = 0.f;
+#pragma unroll
+    for (int q = 0; q < kLogitSplit; ++q)
+      if (q < sh.lsplit) { ts += vs[q]; tm = fmaxf(tm, vm[q]); }
+    ws.rowsum[lb.p * ws.s_m + mi] = ts;
+    ws.peak[lb.p * ws.s_m + mi] = tm;
+  }
+  if (threadIdx.x == 0) st_dev(cnt, 0);
+}
+
 // Small N: a block keeps its 16 rows' logits over every column in registers
 // (at most MAXT tiles per wave), so the keys are read once, the log-sum-exp is
 // reduced inside the block, and e is written with 16-byte stores; the mass
@@ -1134,7 +1422,32 @@ static hipError_t message_view(const Shape& sv, const Params& pr, const Ws& wv, 
   const T* k = static_cast<const T*>(mv.vis_k);
   const float* nonvis_lse = mv.nonvis_lse;
   timer_mark(kStLogits, true, st);
-  switch (sv.dh) {
+  bool wide = false;
+  if constexpr (std::is_same<T, bf16_t>::value) {
+    if (!reg && (sv.T & 15) == 0 && sv.dh <= 128) {
+      wide = true;
+      // wide-row blocks: split the columns until about four blocks per CU
+      Shape sw = sv;
+      const int row_blocks = (sv.hg * sv.T + kWideRows - 1) / kWideRows;
+      const long long rbw = static_cast<long long>(row_blocks) * sv.hkv * sv.B;
+      const long long ntile = (sv.N + 15) / 16;
+      long long ls = (1024 + rbw - 1) / rbw;
+      ls = std::min<long long>(ls, ntile / (kWideMT * kWideW));
+      sw.lsplit = static_cast<int>(std::max<long long>(1, std::min<long long>(ls, kLogitSplit)));
+      const dim3 gw(static_cast<unsigned>(row_blocks * sw.lsplit), sv.hkv, sv.B);
+      switch (sv.dh) {
+#define GMC_WIDE(DH)                                                                                        \
+        case DH:                                                                                            \
+          hipLaunchKernelGGL(logits_lse_wide_kernel<DH>, gw, dim3(64 * kWideW), 0, st, sw, pv, wv, q, k);   \
+          hipLaunchKernelGGL(logits_wide_kernel<DH>, gw, dim3(64 * kWideW), 0, st, sw, wv, q, k, nonvis_lse); \
+          break;
+        GMC_WIDE(32) GMC_WIDE(64) GMC_WIDE(96) GMC_WIDE(128)
+#undef GMC_WIDE
+        default: return hipErrorInvalidValue;
+      }
+    }
+  }
+  if (!wide) switch (sv.dh) {
 #define GMC_LOGITS(DH)                                                                                         \
     case DH:                                                                                                   \
       if constexpr (logit_reg_ok<T, DH>()) {                                                                  \

@@ -104,9 +104,14 @@ def test_zero_and_one_text_queries():
             assert np.all(outs[0]["ebar"] == 1.0)
 
 
-def test_nonvisual_denominator():
-    prob = synth.make_problem("tiny", grid=(1, 12, 12), t=6, k=30)
-    nonvis = np.random.default_rng(5).standard_normal((1, prob.workload.hq, 6)).astype(np.float32) * 2
+# the register-held logits (fp32, 144 tokens) and the wide-row column-range
+# kernels (bf16, 1600 tokens, 224 rows per kv group: a partial last row block)
+@pytest.mark.parametrize("spec", [dict(name="tiny", grid=(1, 12, 12), t=6, k=30),
+                                  dict(name="doc", grid=(1, 40, 40), t=32, k=320)])
+def test_nonvisual_denominator(spec):
+    spec = dict(spec)
+    prob = synth.make_problem(spec.pop("name"), **spec)
+    nonvis = np.random.default_rng(5).standard_normal((1, prob.workload.hq, prob.workload.t)).astype(np.float32) * 2
     _announce("nonvis", prob)
     outs, pr = run(prob, torch, nonvis=nonvis)
     pr.close()
