@@ -33,7 +33,7 @@ constexpr int kAuditOut = 8;         // GMC_AUDIT_OUT: per-problem audit results
 constexpr int kCertFields = 5;       // U_t, gain, q_t, pool margin, batch margin
 constexpr int kMaxPersist = 256;  // blocks per problem of the persistent selection
 constexpr int kMaxGather = 64;    // tensors per row-gather launch (GMC_MAX_GATHER_TENSORS)
-constexpr int kLogitSplit = 8;    // column ranges of the message-logit kernels (at most)
+constexpr int kLogitSplit = 16;   // column ranges of the message-logit kernels (at most)
 constexpr int kProbeSplit = 4;    // K splits of the value-probe GEMM (d a multiple of 256)
 
 // Call shape, resolved on the host for one gmc_prune call.

@@ -187,6 +187,9 @@ __global__ void __launch_bounds__(256) sigma_ell_kernel(Shape sh, Params pr, Ws 
 // storing them), writes e = exp(s - D) l_h[i] to the grounded client rows and
 // leaves per-range row sums and row maxima.  Nothing but e reaches HBM.
 // Splitting the columns over blocks puts every CU to work on the key stream.
+// These generic kernels serve fp32, wide heads and query counts that are not
+// a multiple of 16; bf16 calls use the staged pair below (or, while one
+// 16-row block per CU suffices, the register kernel).
 // ---------------------------------------------------------------------------
 // Waves per logits block, each on its own key tiles (fewer where the fp32
 // fragments of a wide head would not fit the registers of eight waves).
@@ -478,174 +481,171 @@ logits_kernel(Shape sh, Ws ws, const T* text_q, const T* vis_k, const float* non
   if (threadIdx.x == 0) st_dev(cnt, 0);
 }
 
-// Wide-row form of the same two kernels (bf16, head_dim <= 128, T a
-// multiple of 16).  A block covers 64 consecutive rows of one kv group (four
-// 16-row fragments, each inside one head) and one column range: every key
-// tile read from L2 feeds four MFMA row fragments, and a token's 64 grounded
-// entries (client rows g * hg * T + rb .. + 63, 256 contiguous bytes of its
-// row of E) are written by one block, so the lines reach HBM whole.
-constexpr int kWideRows = 64;             // rows per wide block
-constexpr int kWideFr = kWideRows / 16;   // MFMA row fragments
-constexpr int kWideW = 4;                 // waves per wide block
-constexpr int kWideMT = 2;                // key tiles per wave and chunk
+// Staged form of the column-range kernels (bf16, T a multiple of 16): a block
+// of kStW waves covers 16 kStW consecutive rows of one kv group, one 16-row
+// MFMA fragment (inside one head) per wave.  The block's key tiles pass
+// through LDS in stages of kStSG tiles, double buffered (the next stage's
+// global loads are in flight while the waves work on this one), so each key
+// byte is read from L2 once per block and feeds every wave's fragment.
+constexpr int kStW = 8;                   // waves per staged block
+constexpr int kStRows = 16 * kStW;        // rows per staged block
+constexpr int kStSG = 4;                  // key tiles per LDS stage
+constexpr int kStPad = 8;                 // bf16 padding per staged key row (bank spread)
 
 template <int DH>
-struct WideBlock {
+struct StageBlock {
   static constexpr int KS = DH / 32;
-  int p, g, rb, split, rows_g, nfr, t_beg, t_end;
+  static constexpr int ROW = DH + kStPad;                                   // staged row, elements
+  static constexpr int CPT = DH / 8;                                        // 16-byte chunks per key row
+  static constexpr int NCH = kStSG * 16 * CPT;                              // chunks per stage
+  static constexpr int CH = (NCH + 64 * kStW - 1) / (64 * kStW);           // chunks per thread
+  static constexpr int BUF = kStSG * 16 * ROW;                              // elements per stage buffer
+  int p, g, rb, split, rows_g, t_beg, t_end, nst;
   int lane, wave, fr, fk, orow, oc;
+  bool active;     // the wave's fragment holds rows
   float scale;
   const bf16_t* kbase;
   long long kstride;
-  Frag<bf16_t> qf[kWideFr][KS];
+  Frag<bf16_t> qf[KS];
 
-  __device__ WideBlock(const Shape& sh, const bf16_t* text_q, const bf16_t* vis_k, int lsplit) {
+  __device__ StageBlock(const Shape& sh, const bf16_t* text_q, const bf16_t* vis_k, int lsplit) {
     p = blockIdx.z;
     g = blockIdx.y;
-    rb = (blockIdx.x / lsplit) * kWideRows;
+    rb = (blockIdx.x / lsplit) * kStRows;
     split = blockIdx.x % lsplit;
-    rows_g = sh.hg * sh.T;                       // a multiple of 16
-    nfr = min(kWideFr, (rows_g - rb) / 16);      // fragments holding rows
+    rows_g = sh.hg * sh.T;                   // a multiple of 16
     lane = threadIdx.x & 63;
     wave = wave_id();
     fr = lane & 15;
     fk = (lane >> 4) * 8;
     orow = (lane >> 4) * 4;
     oc = lane & 15;
+    active = rb + 16 * wave < rows_g;
     scale = rsqrtf(static_cast<float>(DH));
     const int ntile = (sh.N + 15) / 16, tps = (ntile + lsplit - 1) / lsplit;
     t_beg = min(ntile, split * tps);
     t_end = min(ntile, t_beg + tps);
+    nst = (t_end - t_beg + kStSG - 1) / kStSG;
+    if (active) {
+      const int rr = rb + 16 * wave + fr;
+      const int h = g * sh.hg + rr / sh.T, t = rr % sh.T;
+      const bf16_t* q = text_q + ((static_cast<long long>(p) * sh.T + t) * sh.hq + h) * DH;
 #pragma unroll
-    for (int f = 0; f < kWideFr; ++f) {
-      if (f < nfr) {
-        const int rr = rb + f * 16 + fr;
-        const int h = g * sh.hg + rr / sh.T, t = rr % sh.T;
-        const bf16_t* q = text_q + ((static_cast<long long>(p) * sh.T + t) * sh.hq + h) * DH;
+      for (int ks = 0; ks < KS; ++ks) qf[ks] = frag_load<bf16_t>(q + ks * 32 + fk);
+    } else {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[f][ks] = frag_load<bf16_t>(q + ks * 32 + fk);
-      } else {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[f][ks] = frag_zero<bf16_t>();
-      }
+      for (int ks = 0; ks < KS; ++ks) qf[ks] = frag_zero<bf16_t>();
     }
     kbase = vis_k + static_cast<long long>(p) * sh.N * sh.hkv * DH + g * DH;
     kstride = static_cast<long long>(sh.hkv) * DH;
   }
-  __device__ void load_keys(const Shape& sh, int ct, Frag<bf16_t>* kf) const {
-    const int col = min(ct * 16 + fr, sh.N - 1);
-    const bf16_t* kr = kbase + col * kstride;
+  // this thread's 16-byte chunks of stage s (columns clamped to the last token)
+  __device__ void stage_load(const Shape& sh, int s, uint4* r) const {
+    const int c0 = (t_beg + s * kStSG) * 16;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf[ks] = frag_load<bf16_t>(kr + ks * 32 + fk);
+    for (int q = 0; q < CH; ++q) {
+      const int c = min(static_cast<int>(threadIdx.x) + q * 64 * kStW, NCH - 1);
+      const int col = min(c0 + c / CPT, sh.N - 1);
+      r[q] = ld16(kbase + col * kstride + (c % CPT) * 8);
+    }
   }
-  __device__ floatx4 tile_mma(int f, const Frag<bf16_t>* kf) const {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  __device__ void stage_store(bf16_t* buf, const uint4* r) const {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) acc = mma(qf[f][ks], kf[ks], acc);
+    for (int q = 0; q < CH; ++q) {
+      const int c = threadIdx.x + q * 64 * kStW;
+      if (c < NCH) st16(buf + (c / CPT) * ROW + (c % CPT) * 8, r[q]);
+    }
+  }
+  // the wave's 16 x 16 logit tile against key tile j of a staged buffer
+  __device__ floatx4 tile_mma(const bf16_t* buf, int j) const {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    const bf16_t* kr = buf + (j * 16 + fr) * ROW + fk;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      Frag<bf16_t> kf;
+      kf.v = __builtin_bit_cast(bf16x8, ld16(kr + ks * 32));
+      acc = mma(qf[ks], kf, acc);
+    }
     return acc;
   }
-  // client row of block row 0: rows of a group are consecutive client rows
-  __device__ long long mrow0(const Shape& sh) const { return static_cast<long long>(g) * rows_g + rb; }
+  // client row of the wave's fragment row 0 (rows of a group are consecutive client rows)
+  __device__ long long mrow0(const Shape& sh) const { return static_cast<long long>(g) * rows_g + rb + 16 * wave; }
 };
 
 template <int DH>
-__global__ void __launch_bounds__(64 * kWideW)
-logits_lse_wide_kernel(Shape sh, Params pr, Ws ws, const bf16_t* text_q, const bf16_t* vis_k) {
-  constexpr int KS = DH / 32;
-  __shared__ float sm_m[kWideW][kWideRows], sm_s[kWideW][kWideRows];
-  const WideBlock<DH> lb(sh, text_q, vis_k, sh.lsplit);
-  // online (max, sum) per row in the base-2 domain (y = s log2 e), one
-  // rescale per chunk: the chunk's tiles are reduced against a common maximum
+__global__ void __launch_bounds__(64 * kStW)
+logits_lse_stage_kernel(Shape sh, Params pr, Ws ws, const bf16_t* text_q, const bf16_t* vis_k) {
+  using SB = StageBlock<DH>;
+  __shared__ __attribute__((aligned(16))) bf16_t kst[2 * SB::BUF];
+  const SB lb(sh, text_q, vis_k, sh.lsplit);
+  // online (max, sum) per row in the base-2 domain (y = s log2 e): a lane's
+  // sum is rescaled only when its running maximum grows
   const float c2 = lb.scale * 1.44269504088896341f;
-  float mx[kWideFr][4], sm[kWideFr][4];
+  float mx[4], sm[4];
 #pragma unroll
-  for (int f = 0; f < kWideFr; ++f)
+  for (int e = 0; e < 4; ++e) { mx[e] = -INFINITY; sm[e] = 0.f; }
+  uint4 rg[SB::CH];
+  if (lb.nst > 0) lb.stage_load(sh, 0, rg);
+  for (int s = 0; s < lb.nst; ++s) {
+    bf16_t* buf = kst + (s & 1) * SB::BUF;
+    lb.stage_store(buf, rg);
+    __syncthreads();
+    if (s + 1 < lb.nst) lb.stage_load(sh, s + 1, rg);
+    if (lb.active) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) { mx[f][e] = -INFINITY; sm[f][e] = 0.f; }
-  for (int c0 = lb.t_beg + lb.wave; c0 < lb.t_end; c0 += kWideMT * kWideW) {
-    Frag<bf16_t> kf[kWideMT][KS];
+      for (int j = 0; j < kStSG; ++j) {
+        const int ct = lb.t_beg + s * kStSG + j;
+        if (ct >= lb.t_end) break;   // block-uniform
+        const floatx4 acc = lb.tile_mma(buf, j);
+        if (ct * 16 + lb.oc >= sh.N) continue;
 #pragma unroll
-    for (int j = 0; j < kWideMT; ++j) lb.load_keys(sh, min(c0 + j * kWideW, lb.t_end - 1), kf[j]);
-#pragma unroll
-    for (int f = 0; f < kWideFr; ++f) {
-      if (f >= lb.nfr) continue;
-      float y[kWideMT][4];
-#pragma unroll
-      for (int j = 0; j < kWideMT; ++j) {
-        const int ct = c0 + j * kWideW;
-        if (ct < lb.t_end) {   // wave-uniform: the MFMAs run on full waves
-          const floatx4 acc = lb.tile_mma(f, kf[j]);
-          const bool colok = ct * 16 + lb.oc < sh.N;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) y[j][e] = colok ? acc[e] * c2 : -INFINITY;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) y[j][e] = -INFINITY;
+        for (int e = 0; e < 4; ++e) {
+          const float y = acc[e] * c2;
+          if (y > mx[e]) {
+            sm[e] *= __builtin_amdgcn_exp2f(mx[e] - y);
+            mx[e] = y;
+          }
+          sm[e] += __builtin_amdgcn_exp2f(y - mx[e]);
         }
       }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float cm = y[0][e];
-#pragma unroll
-        for (int j = 1; j < kWideMT; ++j) cm = fmaxf(cm, y[j][e]);
-        if (cm == -INFINITY) continue;
-        const float nm = fmaxf(mx[f][e], cm);
-        float acc_s = sm[f][e] * __builtin_amdgcn_exp2f(mx[f][e] - nm);
-#pragma unroll
-        for (int j = 0; j < kWideMT; ++j) acc_s += __builtin_amdgcn_exp2f(y[j][e] - nm);
-        sm[f][e] = acc_s;
-        mx[f][e] = nm;
-      }
     }
   }
-  // merge across the 16 lanes of a row group and across waves; the maxima
-  // go back to the natural-log domain
-#pragma unroll
-  for (int f = 0; f < kWideFr; ++f)
+  // merge across the 16 lanes of a row group; each wave owns its rows
+  if (lb.active) {
+    float* part = ws.lpart + lb.p * ws.s_lpart;
+    const long long m0 = lb.mrow0(sh);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float m = group16_max(mx[f][e]);
-      const float sc = (mx[f][e] == -INFINITY) ? 0.f : sm[f][e] * __builtin_amdgcn_exp2f(mx[f][e] - m);
+      const float m = group16_max(mx[e]);
+      const float sc = (mx[e] == -INFINITY) ? 0.f : sm[e] * __builtin_amdgcn_exp2f(mx[e] - m);
       const float t = group16_sum(sc);
       if (lb.oc == 0) {
-        sm_m[lb.wave][f * 16 + lb.orow + e] = m * 0.69314718055994531f;
-        sm_s[lb.wave][f * 16 + lb.orow + e] = t;
+        const long long mi = m0 + lb.orow + e;
+        part[static_cast<long long>(lb.split) * sh.mg + mi] = m * 0.69314718055994531f;
+        part[static_cast<long long>(kLogitSplit + lb.split) * sh.mg + mi] = t;
       }
     }
-  __syncthreads();
-  if (threadIdx.x < kWideRows) {
-    const int r = threadIdx.x;
-    if (lb.rb + r < lb.rows_g) {
-      float m = -INFINITY;
-#pragma unroll
-      for (int w = 0; w < kWideW; ++w) m = fmaxf(m, sm_m[w][r]);
-      float s = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWideW; ++w) s += (sm_m[w][r] == -INFINITY) ? 0.f : sm_s[w][r] * __expf(sm_m[w][r] - m);
-      float* part = ws.lpart + lb.p * ws.s_lpart;
-      const long long mi = lb.mrow0(sh) + r;
-      part[static_cast<long long>(lb.split) * sh.mg + mi] = m;
-      part[static_cast<long long>(kLogitSplit + lb.split) * sh.mg + mi] = s;
-    }
   }
+  // one spare job for the problem's first block: the mass coordinates, needed
+  // from the next kernel on
   if (blockIdx.x == 0 && blockIdx.y == 0) sigma_from_partials(sh, pr, ws, lb.p);
 }
 
 template <int DH>
-__global__ void __launch_bounds__(64 * kWideW)
-logits_wide_kernel(Shape sh, Ws ws, const bf16_t* text_q, const bf16_t* vis_k, const float* nonvis_lse) {
-  constexpr int KS = DH / 32;
-  __shared__ float sm_m[kWideW][kWideRows], sm_s[kWideW][kWideRows];
-  __shared__ float sm_D[kWideRows];
-  const WideBlock<DH> lb(sh, text_q, vis_k, sh.lsplit);
+__global__ void __launch_bounds__(64 * kStW)
+logits_stage_kernel(Shape sh, Ws ws, const bf16_t* text_q, const bf16_t* vis_k, const float* nonvis_lse) {
+  using SB = StageBlock<DH>;
+  __shared__ __attribute__((aligned(16))) bf16_t kst[2 * SB::BUF];
+  __shared__ float sm_D[kStRows];
+  const SB lb(sh, text_q, vis_k, sh.lsplit);
   float* part = ws.lpart + lb.p * ws.s_lpart;
-  const long long m0 = lb.mrow0(sh);
-  if (threadIdx.x < kWideRows) {
+  const long long mb = static_cast<long long>(lb.g) * lb.rows_g + lb.rb;   // client row of block row 0
+  if (threadIdx.x < kStRows) {
     // the row's log-sum-exp from the per-range partials, in range order
     const int r = threadIdx.x, rr = lb.rb + r;
     float D = 0.f;
     if (rr < lb.rows_g) {
-      const long long mi = m0 + r;
+      const long long mi = mb + r;
       float m = -INFINITY;
       for (int s = 0; s < sh.lsplit; ++s) m = fmaxf(m, part[static_cast<long long>(s) * sh.mg + mi]);
       float sum = 0.f;
@@ -665,90 +665,92 @@ logits_wide_kernel(Shape sh, Ws ws, const bf16_t* text_q, const bf16_t* vis_k, c
   }
   __syncthreads();
   // e = A * l, written to the grounded client rows; row sums / maxima
-  float D[kWideFr][4], rsum[kWideFr][4], rmax[kWideFr][4], sig2[kWideFr];
-  int hf[kWideFr];
-#pragma unroll
-  for (int f = 0; f < kWideFr; ++f) {
-    hf[f] = lb.g * sh.hg + (f < lb.nfr ? (lb.rb + f * 16) / sh.T : 0);   // the fragment's head
-    const float sg = ws.sig[lb.p * ws.s_sig + hf[f]];
-    sig2[f] = sg * sg;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      D[f][e] = sm_D[f * 16 + lb.orow + e] * 1.44269504088896341f;   // base 2
-      rsum[f][e] = 0.f;
-      rmax[f][e] = 0.f;
-    }
-  }
-  float* E = ws.E + lb.p * ws.s_E;
-  const float* ell = ws.ell + lb.p * ws.s_ell;
   const float c2 = lb.scale * 1.44269504088896341f;
-  for (int c0 = lb.t_beg + lb.wave; c0 < lb.t_end; c0 += kWideMT * kWideW) {
-    Frag<bf16_t> kf[kWideMT][KS];
-    float lv[kWideMT][kWideFr];
+  const int h = lb.g * sh.hg + (lb.active ? (lb.rb + 16 * lb.wave) / sh.T : 0);   // the wave's head
+  const float sg = ws.sig[lb.p * ws.s_sig + h];
+  const float sig2 = sg * sg;
+  float D2[4], rsum[4], rmax[4];
 #pragma unroll
-    for (int j = 0; j < kWideMT; ++j) {
-      const int ct = min(c0 + j * kWideW, lb.t_end - 1);
-      lb.load_keys(sh, ct, kf[j]);
-      const int col = min(ct * 16 + lb.oc, sh.N - 1);
+  for (int e = 0; e < 4; ++e) {
+    D2[e] = sm_D[16 * lb.wave + lb.orow + e] * 1.44269504088896341f;
+    rsum[e] = 0.f;
+    rmax[e] = 0.f;
+  }
+  const long long m0 = lb.mrow0(sh);
+  float* E = ws.E + lb.p * ws.s_E + m0 + lb.orow;
+  const float* ellh = ws.ell + lb.p * ws.s_ell + static_cast<long long>(h) * sh.N;
+  // the lane's atom norms l_h[col] of a stage (its column in each tile)
+  auto norms = [&](int s, float* lv) {
 #pragma unroll
-      for (int f = 0; f < kWideFr; ++f) lv[j][f] = ell[static_cast<long long>(hf[f]) * sh.N + col];
+    for (int j = 0; j < kStSG; ++j) lv[j] = ellh[min((lb.t_beg + s * kStSG + j) * 16 + lb.oc, sh.N - 1)];
+  };
+  uint4 rg[SB::CH];
+  float lv[kStSG], lvn[kStSG];
+  if (lb.nst > 0) {
+    lb.stage_load(sh, 0, rg);
+    norms(0, lvn);
+  }
+  for (int s = 0; s < lb.nst; ++s) {
+    bf16_t* buf = kst + (s & 1) * SB::BUF;
+    lb.stage_store(buf, rg);
+#pragma unroll
+    for (int j = 0; j < kStSG; ++j) lv[j] = lvn[j];
+    __syncthreads();
+    if (s + 1 < lb.nst) {
+      lb.stage_load(sh, s + 1, rg);
+      norms(s + 1, lvn);
     }
+    if (lb.active) {
 #pragma unroll
-    for (int j = 0; j < kWideMT; ++j) {
-      const int ct = c0 + j * kWideW;
-      if (ct >= lb.t_end) continue;   // wave-uniform: the MFMAs run on full waves
-      const int col = ct * 16 + lb.oc;
-      const bool colok = col < sh.N;
-      float* ecol = E + static_cast<long long>(colok ? col : 0) * sh.ldM + m0 + lb.orow;
-#pragma unroll
-      for (int f = 0; f < kWideFr; ++f) {
-        if (f >= lb.nfr) continue;
-        const floatx4 acc = lb.tile_mma(f, kf[j]);
-        if (!colok) continue;
-        const float nrm = sqrtf(lv[j][f] + sig2[f]);
+      for (int j = 0; j < kStSG; ++j) {
+        const int ct = lb.t_beg + s * kStSG + j;
+        if (ct >= lb.t_end) break;   // block-uniform
+        const floatx4 acc = lb.tile_mma(buf, j);
+        const int col = ct * 16 + lb.oc;
+        if (col >= sh.N) continue;
+        const float nrm = sqrtf(lv[j] + sig2);
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          v[e] = __builtin_amdgcn_exp2f(acc[e] * c2 - D[f][e]) * nrm;
-          rsum[f][e] += v[e];
-          rmax[f][e] = fmaxf(rmax[f][e], v[e]);
+          v[e] = __builtin_amdgcn_exp2f(acc[e] * c2 - D2[e]) * nrm;
+          rsum[e] += v[e];
+          rmax[e] = fmaxf(rmax[e], v[e]);
         }
-        *reinterpret_cast<float4*>(ecol + f * 16) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(E + static_cast<long long>(col) * sh.ldM) = make_float4(v[0], v[1], v[2], v[3]);
       }
     }
   }
+  // per-row sums and maxima (each wave owns its rows)
+  float rs[4], rm[4];
 #pragma unroll
-  for (int f = 0; f < kWideFr; ++f)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float s = group16_sum(rsum[f][e]);
-      const float m = group16_max(rmax[f][e]);
-      if (lb.oc == 0) { sm_s[lb.wave][f * 16 + lb.orow + e] = s; sm_m[lb.wave][f * 16 + lb.orow + e] = m; }
-    }
-  __syncthreads();
-  const int r = threadIdx.x;
-  const bool row = r < kWideRows && lb.rb + r < lb.rows_g;
-  const long long mi = m0 + (row ? r : 0);
-  float s = 0.f, m = 0.f;
-  if (row)
-#pragma unroll
-    for (int w = 0; w < kWideW; ++w) { s += sm_s[w][r]; m = fmaxf(m, sm_m[w][r]); }
+  for (int e = 0; e < 4; ++e) {
+    rs[e] = group16_sum(rsum[e]);
+    rm[e] = group16_max(rmax[e]);
+  }
+  const bool wrote = lb.active && lb.oc == 0;
   if (sh.lsplit == 1) {
-    if (row) {
-      ws.rowsum[lb.p * ws.s_m + mi] = s;
-      ws.peak[lb.p * ws.s_m + mi] = m;
-    }
+    if (wrote)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ws.rowsum[lb.p * ws.s_m + m0 + lb.orow + e] = rs[e];
+        ws.peak[lb.p * ws.s_m + m0 + lb.orow + e] = rm[e];   // max_i e; scaled by the row weight later
+      }
     return;
   }
   // the last of the row block's ranges adds the range partials in range order
-  if (row) {
-    st_dev(&part[static_cast<long long>(2 * kLogitSplit + lb.split) * sh.mg + mi], s);
-    st_dev(&part[static_cast<long long>(3 * kLogitSplit + lb.split) * sh.mg + mi], m);
-  }
+  if (wrote)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const long long mi = m0 + lb.orow + e;
+      st_dev(&part[static_cast<long long>(2 * kLogitSplit + lb.split) * sh.mg + mi], rs[e]);
+      st_dev(&part[static_cast<long long>(3 * kLogitSplit + lb.split) * sh.mg + mi], rm[e]);
+    }
   __shared__ int flag;
   int* cnt = ws.lcnt + lb.p * ws.s_lcnt + (blockIdx.x / sh.lsplit) * sh.hkv + lb.g;
   if (!last_arrival(cnt, sh.lsplit, &flag)) return;
-  if (row) {
+  const int r = threadIdx.x;
+  if (r < kStRows && lb.rb + r < lb.rows_g) {
+    const long long mi = mb + r;
     float vs[kLogitSplit], vm[kLogitSplit];
 #pragma unroll
     for (int q = 0; q < kLogitSplit; ++q) {
@@ -1417,32 +1419,38 @@ static hipError_t message_view(const Shape& sv, const Params& pr, const Ws& wv, 
   const dim3 lg((sv.hg * sv.T + 15) / 16 * sv.lsplit, sv.hkv, sv.B);
   const dim3 lr((sv.hg * sv.T + 15) / 16, sv.hkv, sv.B);
   // every tile of a block's rows fits the registers of its eight waves
-  const bool reg = (sv.N + 15) / 16 <= 8 * kLogitRegTiles;
+  const bool staged_ok = std::is_same<T, bf16_t>::value && (sv.T & 15) == 0 && sv.dh <= 128;
+  // the register kernel (one pass, keys read once) while its 16-row blocks
+  // number at most one per CU; many images fill the chip better with the
+  // staged column-range kernels
+  const bool reg = (sv.N + 15) / 16 <= 8 * kLogitRegTiles &&
+                   (!staged_ok || static_cast<long long>(lr.x) * lr.y * lr.z <= 256);
   const T* q = static_cast<const T*>(mv.text_q);
   const T* k = static_cast<const T*>(mv.vis_k);
   const float* nonvis_lse = mv.nonvis_lse;
   timer_mark(kStLogits, true, st);
   bool wide = false;
   if constexpr (std::is_same<T, bf16_t>::value) {
-    if (!reg && (sv.T & 15) == 0 && sv.dh <= 128) {
+    if (!reg && staged_ok) {
       wide = true;
-      // wide-row blocks: split the columns until about four blocks per CU
+      // staged blocks of 16 kStW rows: split the columns until about four
+      // blocks per CU, keeping at least two stages per range
       Shape sw = sv;
-      const int row_blocks = (sv.hg * sv.T + kWideRows - 1) / kWideRows;
+      const int row_blocks = (sv.hg * sv.T + kStRows - 1) / kStRows;
       const long long rbw = static_cast<long long>(row_blocks) * sv.hkv * sv.B;
       const long long ntile = (sv.N + 15) / 16;
       long long ls = (1024 + rbw - 1) / rbw;
-      ls = std::min<long long>(ls, ntile / (kWideMT * kWideW));
+      ls = std::min<long long>(ls, ntile / (2 * kStSG));
       sw.lsplit = static_cast<int>(std::max<long long>(1, std::min<long long>(ls, kLogitSplit)));
       const dim3 gw(static_cast<unsigned>(row_blocks * sw.lsplit), sv.hkv, sv.B);
       switch (sv.dh) {
-#define GMC_WIDE(DH)                                                                                        \
-        case DH:                                                                                            \
-          hipLaunchKernelGGL(logits_lse_wide_kernel<DH>, gw, dim3(64 * kWideW), 0, st, sw, pv, wv, q, k);   \
-          hipLaunchKernelGGL(logits_wide_kernel<DH>, gw, dim3(64 * kWideW), 0, st, sw, wv, q, k, nonvis_lse); \
+#define GMC_STAGE(DH)                                                                                        \
+        case DH:                                                                                             \
+          hipLaunchKernelGGL(logits_lse_stage_kernel<DH>, gw, dim3(64 * kStW), 0, st, sw, pv, wv, q, k);     \
+          hipLaunchKernelGGL(logits_stage_kernel<DH>, gw, dim3(64 * kStW), 0, st, sw, wv, q, k, nonvis_lse);  \
           break;
-        GMC_WIDE(32) GMC_WIDE(64) GMC_WIDE(96) GMC_WIDE(128)
-#undef GMC_WIDE
+        GMC_STAGE(32) GMC_STAGE(64) GMC_STAGE(96) GMC_STAGE(128)
+#undef GMC_STAGE
         default: return hipErrorInvalidValue;
       }
     }

@@ -1502,6 +1502,9 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, con
       timer_mark(kStGains, true, st);
       if (pool_kpt > 0) {
         hipLaunchKernelGGL((gains_kernel<true, false>), gg, dim3(256), 0, st, sh, ws, r, psize, so);
+        // the pool's own kernel is timed with the responsibilities
+        timer_mark(kStGains, false, st);
+        timer_mark(kStResp, true, st);
         const dim3 gp(sh.B), bp(64 * kPoolW);
         const size_t pl = static_cast<size_t>(sh.N) * sizeof(uint32_t);
         if (pool_kpt == 16 && static_cast<int>(pl) > pool_lds_granted) {
@@ -1517,13 +1520,14 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, con
           hipLaunchKernelGGL(pool_topk_kernel<8>, gp, bp, pl, st, sh, ws, r, psize, so);
         else
           hipLaunchKernelGGL(pool_topk_kernel<16>, gp, bp, pl, st, sh, ws, r, psize, so);
-      } else if (global_keys) {
-        hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, so);
       } else {
-        hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, so);
+        if (global_keys)
+          hipLaunchKernelGGL(gains_kernel<true>, gg, dim3(256), 0, st, sh, ws, r, psize, so);
+        else
+          hipLaunchKernelGGL(gains_kernel<false>, gg, dim3(256), key_lds, st, sh, ws, r, psize, so);
+        timer_mark(kStGains, false, st);
+        timer_mark(kStResp, true, st);
       }
-      timer_mark(kStGains, false, st);
-      timer_mark(kStResp, true, st);
       if (sh.pool_cap <= 64)
         hipLaunchKernelGGL(resp_small_kernel, dim3((sh.m + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws,
                            psize);
