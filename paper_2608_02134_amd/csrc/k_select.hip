@@ -906,6 +906,9 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   __shared__ int pool_s[64], chosen[64], bidx[64];
   __shared__ __attribute__((aligned(16))) uint32_t bkeys[64];
   __shared__ float rmu[4][64], rden_s[4][64], red[16];
+  // Cbar of the chunk's rows at the pool's tokens (pool position, row lane),
+  // kept from the responsibilities for the coverage refresh
+  __shared__ float cpool[64][64];
   const int p = blockIdx.y, blk = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nwaves = nblk * 4, gw = blk * 4 + wave;
@@ -1112,7 +1115,9 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       float mu = 0.f;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const float rr = (j0 + j < psize) ? fmaxf(a * v[j] - b, 0.f) : 0.f;
+        const float cb = a * v[j];
+        cpool[j0 + j][lane] = cb;
+        const float rr = (j0 + j < psize) ? fmaxf(cb - b, 0.f) : 0.f;
         v[j] = rr;
         mu = fmaxf(mu, rr);
       }
@@ -1203,17 +1208,13 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
         if (blk < nchunk) {
           const int m = blk * 64 + lane;
           const int mc = min(m, sh.m - 1);
-          const float a = al[mc];
           // the pool holds at most 64 = 4 b entries here, so b <= 16: four
-          // batch entries per wave
-          float v[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            v[q] = E[static_cast<long long>(bidx[min(wave + 4 * q, bsize - 1)]) * sh.ldM + mc];
+          // batch entries per wave, their Cbar values kept in LDS by this
+          // block's responsibility pass over the same rows
           float cm = bl[mc];
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            if (wave + 4 * q < bsize) cm = fmaxf(cm, a * v[q]);
+            if (wave + 4 * q < bsize) cm = fmaxf(cm, cpool[chosen[wave + 4 * q]][lane]);
           rmu[wave][lane] = cm;   // free: last read before the barrier after the batch
           __syncthreads();
           if (wave == 0 && m < sh.m)
