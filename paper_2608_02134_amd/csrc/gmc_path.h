@@ -21,9 +21,10 @@ struct Limits {
 // `fork` event, and joined by a device flag (T > 0) or the `join` event.
 struct PathStreams {
   hipStream_t st;
-  hipStream_t side;
+  hipStream_t side;    // appearance bank
+  hipStream_t side2;   // spatial bank
   int call_tag;
-  hipEvent_t fork, join;
+  hipEvent_t fork, join, join2;
 };
 
 // Records the message gmc_last_error() returns; returns code.
