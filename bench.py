@@ -228,6 +228,15 @@ def main():
                 "frac": achieved / peak, "traffic": traffic, "traffic_note": traffic_note,
                 "work_per_launch": work, "launch_avg_us": stages[dom]["launch_avg_us"],
                 "source_hash": source_hash()}
+    if bound == "hbm" and traffic:
+        # `achieved` counts the algorithmic bytes; the counters give what
+        # actually crossed the fabric.  Far fewer measured bytes than
+        # algorithmic ones means the kernel's operands stayed in the caches
+        # and its time is set by latency, not by HBM bandwidth.
+        roofline["traffic_gbs"] = traffic / avg_s / 1e9
+        roofline["traffic_over_work"] = traffic / work
+        roofline["regime"] = ("latency: operands cache-resident, measured traffic well below the algorithmic bytes"
+                              if traffic < 0.5 * work else "bandwidth: operands streamed from HBM")
 
     cpu = None
     if args.cpu_seconds > 0:

@@ -36,13 +36,12 @@ struct Context {
   void* mem = nullptr;
   size_t bytes = 0;
   hipStream_t stream = nullptr;
-  // internal side streams for the bank kernels (default priority), one for
-  // the appearance bank and one for the spatial bank; each starts a call
-  // behind a device gate on the row-norm blocks' call tags (one image) or an
-  // event, and joins the caller's stream through a device flag counting the
-  // finished streams (events without text queries)
-  hipStream_t side = nullptr, side2 = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr, join2 = nullptr;
+  // internal side stream for the bank kernels (default priority); it starts
+  // each call behind a device gate on the row-norm blocks' call tags (one
+  // image) or an event, and joins the caller's stream through a device flag
+  // (an event without text queries)
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   int call_tag = 0;   // last call number handed to the row-norm blocks
   int device = 0;
   int diag = 0;       // GMC_DIAG_* flags for the next calls
@@ -387,14 +386,12 @@ void gmc_free(void) {
   g_timer.release();
   if (!g_ctx) return;
   (void)hipSetDevice(g_ctx->device);
-  for (hipStream_t s : {g_ctx->side, g_ctx->side2}) {
-    if (!s) continue;
-    (void)hipStreamSynchronize(s);
-    (void)hipStreamDestroy(s);
+  if (g_ctx->side) {
+    (void)hipStreamSynchronize(g_ctx->side);
+    (void)hipStreamDestroy(g_ctx->side);
   }
   if (g_ctx->fork) (void)hipEventDestroy(g_ctx->fork);
   if (g_ctx->join) (void)hipEventDestroy(g_ctx->join);
-  if (g_ctx->join2) (void)hipEventDestroy(g_ctx->join2);
   if (g_ctx->xfer) (void)hipEventDestroy(g_ctx->xfer);
   if (g_ctx->mem) (void)hipFree(g_ctx->mem);
   delete g_ctx;
@@ -437,18 +434,13 @@ int gmc_init(const gmc_config* cfg) {
     return fail(GMC_ERR_HIP, "gmc_init: clearing the workspace failed (%s)", hipGetErrorString(err));
   }
   err = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
-  if (err == hipSuccess) err = hipStreamCreateWithFlags(&ctx->side2, hipStreamNonBlocking);
   if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->fork, hipEventDisableTiming);
   if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->join, hipEventDisableTiming);
-  if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->join2, hipEventDisableTiming);
   if (err == hipSuccess) err = hipEventCreateWithFlags(&ctx->xfer, hipEventDisableTiming);
   if (err != hipSuccess) {
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
-    if (ctx->side2) (void)hipStreamDestroy(ctx->side2);
     if (ctx->fork) (void)hipEventDestroy(ctx->fork);
     if (ctx->join) (void)hipEventDestroy(ctx->join);
-    if (ctx->join2) (void)hipEventDestroy(ctx->join2);
-    if (ctx->xfer) (void)hipEventDestroy(ctx->xfer);
     (void)hipFree(ctx->mem);
     delete ctx;
     return fail(GMC_ERR_HIP, "gmc_init: side stream or events (%s)", hipGetErrorString(err));
@@ -724,54 +716,48 @@ int enqueue_prune(const gmc_config& cfg, const Params& pr0, const Ws& ws, const 
     err = launch_image_prep(s, ws, image_id, st);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "image ids: %s", hipGetErrorString(err));
   }
-  // per-call reset and row norms (one kernel), then the appearance bank and
-  // the spatial bank on two side streams while the message kernels run on
-  // the caller's stream (they write disjoint client rows).  Without side
-  // streams (stage timing, the static-scratch entry point) everything stays
-  // on one stream.
-  const bool fork = ps.side != nullptr && ps.side2 != nullptr;
-  // one image: the fork is a one-block gate on each side stream that waits
-  // for this call's row-norm blocks (no event record on the caller's stream,
-  // whose next kernel would wait for the command processor to process it).
-  // The gates of the next call may already wait while this call's selection
-  // runs, so with several images, whose persistent selection takes every CU,
-  // an event is used instead.
+  // per-call reset and row norms (one kernel), then the bank kernels on the
+  // side stream while the message kernels run on the caller's stream (they
+  // write disjoint client rows).  Without a side stream (stage timing, the
+  // static-scratch entry point) everything stays on one stream.
+  const bool fork = ps.side != nullptr;
+  // one image: the fork is a one-block gate on the side stream that waits for
+  // this call's row-norm blocks (no event record on the caller's stream, whose
+  // next kernel would wait for the command processor to process it).  The
+  // gate of the next call may already wait while this call's selection runs,
+  // so with several images, whose persistent selection takes every CU, an
+  // event is used instead.
   const bool gate = fork && ps.call_tag != 0;
   err = launch_rownorm(s, ws, hidden, gate ? ps.call_tag : 0, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "row norms: %s", hipGetErrorString(err));
-  hipStream_t bank_st = fork ? ps.side : st, spatial_st = fork ? ps.side2 : st;
+  hipStream_t bank_st = fork ? ps.side : st;
   if (gate) {
     err = launch_bank_gate(s, ws, ps.call_tag, ps.side);
-    if (err == hipSuccess) err = launch_bank_gate(s, ws, ps.call_tag, ps.side2);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
   } else if (fork) {
     err = hipEventRecord(ps.fork, st);
     if (err == hipSuccess) err = hipStreamWaitEvent(ps.side, ps.fork, 0);
-    if (err == hipSuccess) err = hipStreamWaitEvent(ps.side2, ps.fork, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream fork: %s", hipGetErrorString(err));
   }
-  err = launch_banks(s, pr, ws, hidden, cfg.app_projection, pos3d, bank_st, spatial_st);
+  err = launch_banks(s, pr, ws, hidden, cfg.app_projection, pos3d, bank_st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "bank kernels: %s", hipGetErrorString(err));
   // join: with text queries the last message kernel (one block per problem)
-  // waits on a device flag that each side stream increments after its last
-  // bank kernel, which costs less than an event wait on the caller's stream;
-  // without text queries, events
+  // waits on a device flag that the side stream raises after its last bank
+  // kernel, which costs less than an event wait on the caller's stream;
+  // without text queries, an event
   int* bank_flag = ws.cnt + kCntBankFlag;   // cleared by the row-norm kernel
   const bool flag_join = fork && s.T > 0;
   if (flag_join) {
     err = launch_bank_signal(bank_flag, ps.side);
-    if (err == hipSuccess) err = launch_bank_signal(bank_flag, ps.side2);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   } else if (fork) {
     err = hipEventRecord(ps.join, ps.side);
-    if (err == hipSuccess) err = hipEventRecord(ps.join2, ps.side2);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }
   err = launch_message(s, pr, ws, views, tr.omega, flag_join ? bank_flag : nullptr, st);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "message kernels: %s", hipGetErrorString(err));
   if (fork && !flag_join) {
     err = hipStreamWaitEvent(st, ps.join, 0);
-    if (err == hipSuccess) err = hipStreamWaitEvent(st, ps.join2, 0);
     if (err != hipSuccess) return fail(GMC_ERR_HIP, "stream join: %s", hipGetErrorString(err));
   }
   // per-round outputs of the selection: the trace's buffers, completed with
@@ -851,7 +837,7 @@ int run(int64_t B, const void* hidden, const void* text_q, const void* vis_k, co
   c.last_cert = false;
   // stage timing keeps every kernel on the caller's stream, so each stage's
   // span measures that stage alone
-  PathStreams ps{st, g_timer.on ? nullptr : c.side, g_timer.on ? nullptr : c.side2, 0, c.fork, c.join, c.join2};
+  PathStreams ps{st, g_timer.on ? nullptr : c.side, 0, c.fork, c.join};
   if (ps.side && s.B == 1 && s.K < s.N) {
     c.call_tag = c.call_tag == 0x7fffffff ? 1 : c.call_tag + 1;
     ps.call_tag = c.call_tag;
@@ -983,7 +969,6 @@ int gmc_get_diag(int64_t problem, gmc_diag* out) {
   hipError_t err = hipSetDevice(c.device);
   if (err == hipSuccess) err = hipStreamSynchronize(c.last_stream);
   if (err == hipSuccess) err = hipStreamSynchronize(c.side);
-  if (err == hipSuccess) err = hipStreamSynchronize(c.side2);
   if (err != hipSuccess) return fail(GMC_ERR_HIP, "gmc_get_diag: %s", hipGetErrorString(err));
   const int p = static_cast<int>(problem);
   std::vector<int> cnt(static_cast<size_t>(c.cap.B) * kCounters);

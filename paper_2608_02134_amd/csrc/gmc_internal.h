@@ -14,8 +14,7 @@ constexpr int kMaxN = 32768;      // tokens per problem (top-k keys live in LDS)
 constexpr int kHeadTok = 8;       // tokens per head-Gram block (two per wave)
 constexpr int kStats = 15;
 constexpr int kCounters = 8;      // completion counters per problem
-constexpr int kCntBankFlag = 6;   // slot of problem 0: count of the call's finished bank streams
-constexpr int kBankSignals = 2;   // bank streams that raise it: appearance, spatial
+constexpr int kCntBankFlag = 6;   // slot of problem 0: the bank kernels of the call have finished
 constexpr int kCntStatus = 7;     // device status bits (sticky; cleared from the host only)
 constexpr unsigned kStatusSelect = 1u;    // a hand-off wait of the persistent selection timed out
 constexpr unsigned kStatusBank = 2u;      // the bank stream's gate or join timed out

@@ -47,9 +47,8 @@ hipError_t launch_message(const Shape& sh, const Params& pr, const Ws& ws, const
 hipError_t launch_bank_signal(int* flag, hipStream_t st);
 
 // Appearance (exact or bounded) and spatial banks with their row weights.
-// Appearance bank on st, spatial bank on sp_st (the same stream or another).
 hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
-                        const void* app_proj, const int32_t* pos3d, hipStream_t st, hipStream_t sp_st);
+                        const void* app_proj, const int32_t* pos3d, hipStream_t st);
 
 // All selection rounds, then the final coverage and objective values.
 // *support_ready reports that the support list and slots were written too.

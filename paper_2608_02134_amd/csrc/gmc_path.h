@@ -21,10 +21,9 @@ struct Limits {
 // `fork` event, and joined by a device flag (T > 0) or the `join` event.
 struct PathStreams {
   hipStream_t st;
-  hipStream_t side;    // appearance bank
-  hipStream_t side2;   // spatial bank
+  hipStream_t side;
   int call_tag;
-  hipEvent_t fork, join, join2;
+  hipEvent_t fork, join;
 };
 
 // Records the message gmc_last_error() returns; returns code.

@@ -93,7 +93,7 @@ extern "C" int gmc_prune_static(const gmc_config* cfg, int64_t B, const void* hi
                                             hipGetErrorString(err));
   }
   const Params pr = params_of(c);
-  const PathStreams ps{st, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
+  const PathStreams ps{st, nullptr, 0, nullptr, nullptr};
   bool cert = false;
   return enqueue_prune(c, pr, ws, s, ps, 0, hidden, text_q, vis_k, pos3d, out_hidden, out_pos, out_idx, nonvis_lse,
                        gmc_trace{}, &cert);

@@ -575,21 +575,20 @@ __global__ void __launch_bounds__(256) spatial_write_kernel(Shape sh, Params pr,
 
 template <typename T>
 static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden_v,
-                             const void* proj_v, const int32_t* pos3d, hipStream_t st, hipStream_t sp_st) {
+                             const void* proj_v, const int32_t* pos3d, hipStream_t st) {
   const T* hidden = static_cast<const T*>(hidden_v);
   hipError_t err;
   auto spatial = [&]() {
-    timer_mark(kStSpatial, true, sp_st);
-    hipLaunchKernelGGL(spatial_stats_kernel, dim3(sh.ms, sh.B), dim3(256), 0, sp_st, sh, pr, ws, pos3d);
-    hipLaunchKernelGGL(spatial_write_kernel, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, sp_st, sh, pr, ws);
-    timer_mark(kStSpatial, false, sp_st);
+    timer_mark(kStSpatial, true, st);
+    hipLaunchKernelGGL(spatial_stats_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws, pos3d);
+    hipLaunchKernelGGL(spatial_write_kernel, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws);
+    timer_mark(kStSpatial, false, st);
   };
-  // on a stream of their own the spatial kernels run beside the appearance
-  // bank; on one stream, up to 2048 tokens the light spatial kernels go
-  // first, so that the Gram, the heaviest bank kernel, overlaps the
-  // head-pattern kernels rather than the message logits; a larger Gram
-  // starts at once
-  const bool spatial_first = sp_st != st || sh.N <= 2048;
+  // up to 2048 tokens the light spatial kernels go first, so that the Gram,
+  // the heaviest bank kernel, overlaps the head-pattern kernels rather than
+  // the message logits (measured: the Gram then still ends before the head
+  // clustering); a larger Gram starts at once
+  const bool spatial_first = sh.N <= 2048;
   if (spatial_first) spatial();
   timer_mark(kStAppearance, true, st);
   if (!sh.bounded) {
@@ -638,9 +637,9 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
 }
 
 hipError_t launch_banks(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden,
-                        const void* app_proj, const int32_t* pos3d, hipStream_t st, hipStream_t sp_st) {
-  if (sh.dtype == 0) return banks_impl<float>(sh, pr, ws, hidden, app_proj, pos3d, st, sp_st);
-  return banks_impl<bf16_t>(sh, pr, ws, hidden, app_proj, pos3d, st, sp_st);
+                        const void* app_proj, const int32_t* pos3d, hipStream_t st) {
+  if (sh.dtype == 0) return banks_impl<float>(sh, pr, ws, hidden, app_proj, pos3d, st);
+  return banks_impl<bf16_t>(sh, pr, ws, hidden, app_proj, pos3d, st);
 }
 
 }  // namespace gmc

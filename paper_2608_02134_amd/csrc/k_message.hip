@@ -984,15 +984,13 @@ logits_reg_kernel(Shape sh, Params pr, Ws ws, const T* text_q, const T* vis_k, c
 constexpr int kGramTC = 64;                 // t columns per LDS chunk
 constexpr int kGramPitch = kGramTC + 4;     // floats per staged head row
 constexpr int kGramTok = 2;                 // tokens per wave (kHeadTok per block)
-constexpr int kGramWaves = 4;               // waves per block
-static_assert(kGramTok * kGramWaves == kHeadTok, "one block covers kHeadTok tokens");
+static_assert(kGramTok * 4 == kHeadTok, "one block covers kHeadTok tokens");
 
 template <int R>
-__global__ void __launch_bounds__(64 * kGramWaves) headgram_kernel(Shape sh, Params pr, Ws ws, int write_e2) {
+__global__ void __launch_bounds__(256) headgram_kernel(Shape sh, Params pr, Ws ws, int write_e2) {
   constexpr int U = R + 1;                     // [Z_h[i]; sigma_h] / l_h[i]
-  constexpr int NT = 64 * kGramWaves;
-  __shared__ __attribute__((aligned(16))) float xs[kGramWaves][32 * kGramPitch];
-  __shared__ float us[kGramWaves][32 * U];
+  __shared__ __attribute__((aligned(16))) float xs[4][32 * kGramPitch];
+  __shared__ float us[4][32 * U];
   const int p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int H = sh.hq, T = sh.T;
   const int fr = lane & 15, fk = lane >> 4;
@@ -1106,7 +1104,7 @@ __global__ void __launch_bounds__(64 * kGramWaves) headgram_kernel(Shape sh, Par
   }
   // the block's partial: waves summed in order, one value per pair h <= g
   __syncthreads();
-  float* red = &xs[0][0];   // kGramWaves waves x 768 floats, staging buffers are free now
+  float* red = &xs[0][0];   // 4 waves x 768 floats, staging buffers are free now
 #pragma unroll
   for (int tl = 0; tl < 3; ++tl)
 #pragma unroll
@@ -1115,14 +1113,12 @@ __global__ void __launch_bounds__(64 * kGramWaves) headgram_kernel(Shape sh, Par
   // block-major partials, pairs padded to a multiple of four
   const long long npp = (sh.npairs + 3) & ~3;
   float* gp = ws.gpart + p * ws.s_gpart + blockIdx.x * npp;
-  for (int x = tid; x < 768; x += NT) {
+  for (int x = tid; x < 768; x += 256) {
     const int tl = x / 256, e = (x / 64) % 4, l = x % 64;
     const int hb = tl == 2 ? 1 : 0, gb = tl == 0 ? 0 : 1;
     const int hh = 16 * hb + 4 * (l >> 4) + e, gg = 16 * gb + (l & 15);
     if (hh <= gg && gg < H) {
-      float v = red[x];
-#pragma unroll
-      for (int w = 1; w < kGramWaves; ++w) v += red[w * 768 + x];
+      const float v = ((red[x] + red[768 + x]) + red[2 * 768 + x]) + red[3 * 768 + x];
       gp[hh * H - hh * (hh - 1) / 2 + (gg - hh)] = v;
     }
   }
@@ -1136,10 +1132,9 @@ __global__ void __launch_bounds__(64 * kGramWaves) headgram_kernel(Shape sh, Par
 // holding the best value by ballot.
 // ---------------------------------------------------------------------------
 
-// Each bank side stream adds one once its bank kernels of the call have
-// finished.
+// Raised by the side stream once every bank kernel of the call has finished.
 __global__ void bank_signal_kernel(int* flag) {
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // One block per problem (occupancy is irrelevant, so the register budget goes
@@ -1148,15 +1143,15 @@ __global__ void bank_signal_kernel(int* flag) {
 // sums as float4 runs of queries, the first pass of the row weights; partial
 // sums are combined through LDS in a fixed order.
 constexpr int kClusterThreads = 512;
-constexpr int kClusterGB = 16;   // block partial quads in flight per thread (more spill to scratch)
+constexpr int kClusterGB = 16;   // block partial quads in flight per thread (more spills to scratch)
 
 __global__ void __launch_bounds__(kClusterThreads) __attribute__((amdgpu_waves_per_eu(1, 2)))
 cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_flag) {
-  constexpr int NT = kClusterThreads, kRW = 4, kRQ = 4;
+  constexpr int NT = kClusterThreads, kRW = 4;
   __shared__ float gam[kMaxHeads][kMaxHeads + 1];    // pattern Gram over the views
   __shared__ float cosm[kMaxHeads][kMaxHeads + 1];   // one view's Gamma, then the cosines
   __shared__ float4 gq[NT];
-  __shared__ float hs[kRQ * NT];
+  __shared__ float hs[4 * NT];
   __shared__ float om[kMaxHeads], ab[kMaxHeads];
   __shared__ int asg[kMaxHeads];
   const int p = blockIdx.x, tid = threadIdx.x, H = sh.hq, T = sh.T, M1 = sh.mg1;
@@ -1172,8 +1167,8 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
   const int b_beg = bg * bper, b_end = min(nb, b_beg + bper);
   const bool gthr = bg < ngrp && b_beg < b_end;
   // grounded row sums in runs of four queries of one head (T a multiple of 4
-  // and at most kRQ NT runs per view; otherwise each head's lane adds its rows)
-  const bool runs = (T & 3) == 0 && M1 <= 4 * kRQ * NT;
+  // and at most 4 NT runs per view; otherwise each head's lane adds its rows)
+  const bool runs = (T & 3) == 0 && M1 <= 16 * NT;
   float zv0[kRW], pv0[kRW];
   for (int v = 0; v < sh.nviews; ++v) {
     const float* gp = ws.gpart + p * ws.s_gpart + v * ws.s_gpart1;
@@ -1193,9 +1188,9 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
         pv0[k] = ws.peak[p * ws.s_m + m];
       }
     }
-    float4 rq[kRQ];
+    float4 rq[4];
 #pragma unroll
-    for (int k = 0; k < kRQ; ++k) {
+    for (int k = 0; k < 4; ++k) {
       const int x = k * NT + tid;
       rq[k] = (runs && 4 * x < M1) ? *reinterpret_cast<const float4*>(rs + 4 * x) : float4{0.f, 0.f, 0.f, 0.f};
     }
@@ -1218,7 +1213,7 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
     __syncthreads();   // gq, hs, cosm and ab of the previous view are consumed
     gq[tid] = gs;
 #pragma unroll
-    for (int k = 0; k < kRQ; ++k) hs[k * NT + tid] = (rq[k].x + rq[k].y) + (rq[k].z + rq[k].w);
+    for (int k = 0; k < 4; ++k) hs[k * NT + tid] = (rq[k].x + rq[k].y) + (rq[k].z + rq[k].w);
     __syncthreads();
     for (int hg = tid; hg < kMaxHeads * kMaxHeads; hg += NT) {
       const int h = hg / kMaxHeads, g = hg % kMaxHeads;
@@ -1306,30 +1301,22 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
       int n_clusters = 0;
       for (int c = 0; c < nc; ++c) n_clusters += __ballot(cl == c) != 0ull;
       // members of the head's cluster (adding zeros for the others leaves
-      // the sum unchanged), four interleaved partial sums over the heads
-      float s4[4] = {0.f, 0.f, 0.f, 0.f};
+      // the sum unchanged)
+      float s_h = 0.f;
 #pragma unroll
-      for (int g = 0; g < kMaxHeads; ++g) s4[g & 3] += (g < H && asg[g] == cl) ? cosm[h][g] : 0.f;
-      float s_h = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+      for (int g = 0; g < kMaxHeads; ++g) s_h += (g < H && asg[g] == cl) ? cosm[h][g] : 0.f;
       if (cl < 0) s_h = 0.f;
-      // the per-cluster wave sums four clusters at a time (independent
-      // reductions in flight together)
       float inv = 0.f;
-      for (int c0 = 0; c0 < nc; c0 += 4) {
-        float tot[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) tot[q] = wave_sum(cl == c0 + q ? s_h : 0.f);
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (cl == c0 + q) inv = 1.f / ((1.f - s_h / sqrtf(fmaxf(tot[q], 0.f))) + pr.disp_eps);
+      for (int c = 0; c < nc; ++c) {
+        const float tot = wave_sum(cl == c ? s_h : 0.f);
+        if (cl == c) {
+          const float disp = 1.f - s_h / sqrtf(fmaxf(tot, 0.f));
+          inv = 1.f / (disp + pr.disp_eps);
+        }
       }
-      for (int c0 = 0; c0 < nc; c0 += 4) {
-        float isum[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) isum[q] = wave_sum(cl == c0 + q ? inv : 0.f);
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (cl == c0 + q) w_h = inv / isum[q] / static_cast<float>(n_clusters);
+      for (int c = 0; c < nc; ++c) {
+        const float isum = wave_sum(cl == c ? inv : 0.f);
+        if (cl == c) w_h = inv / isum / static_cast<float>(n_clusters);
       }
     }
     if (valid) {
@@ -1366,14 +1353,12 @@ cluster_kernel(Shape sh, Params pr, Ws ws, float* trace_omega, const int* bank_f
       }
     }
   }
-  // the bank kernels run on other streams; the kernel after this one reads
-  // their client rows, so this one ends only once every bank stream has
-  // counted itself in bank_flag (one thread per block waits; every wait is
-  // bounded)
+  // the bank kernels run on another stream; the kernel after this one reads
+  // their client rows, so this one ends only once the side stream has raised
+  // bank_flag (one thread per block waits; every wait is bounded)
   if (bank_flag && tid == 0) {
     const unsigned long long t0 = static_cast<unsigned long long>(wall_clock64());
-    for (int spin = 0; __hip_atomic_load(bank_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < kBankSignals;
-         ++spin) {
+    for (int spin = 0; __hip_atomic_load(bank_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 1; ++spin) {
       if ((spin & 255) == 255 && static_cast<unsigned long long>(wall_clock64()) - t0 > kJoinWaitTicks) {
         raise_status(ws.cnt + p * ws.s_cnt, kStatusBank);
         break;
@@ -1498,7 +1483,7 @@ static hipError_t message_view(const Shape& sv, const Params& pr, const Ws& wv, 
   const int we2 = current ? 1 : 0;
   switch (sv.r) {
 #define GMC_HEADGRAM(R) \
-    case R: hipLaunchKernelGGL(headgram_kernel<R>, dim3(sv.n_head_blk, sv.B), dim3(64 * kGramWaves), 0, st, sv, pv, wv, we2); break;
+    case R: hipLaunchKernelGGL(headgram_kernel<R>, dim3(sv.n_head_blk, sv.B), dim3(256), 0, st, sv, pv, wv, we2); break;
     GMC_HEADGRAM(1) GMC_HEADGRAM(2) GMC_HEADGRAM(3) GMC_HEADGRAM(4)
     GMC_HEADGRAM(5) GMC_HEADGRAM(6) GMC_HEADGRAM(7) GMC_HEADGRAM(8)
 #undef GMC_HEADGRAM
