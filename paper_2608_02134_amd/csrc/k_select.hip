@@ -1419,8 +1419,10 @@ static int persistent_blocks(const Shape& sh, size_t lds, int res) {
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(res), 256, lds) != hipSuccess || per_cu < 1)
     return 0;
-  // one CU per block; about two gain tokens per wave
-  const int cap = n_cu / sh.B;
+  // about two gain tokens per wave; one block per CU, or two when the
+  // streamed (non-resident) kernel fits twice, which doubles the waves that
+  // stream the client rows
+  const int cap = (res ? 1 : std::min(per_cu, 2)) * n_cu / sh.B;
   const int want = max((sh.N + 7) / 8, ((sh.m + 63) / 64 + 3) / 4);
   const int nblk = min(min(cap, want), kMaxPersist);
   return nblk >= 1 ? nblk : 0;
