@@ -707,7 +707,7 @@ __global__ void __launch_bounds__(64 * kRsW) rowstat_kernel(Shape sh, Params pr,
   const int* pool = ws.pool + p * ws.s_pool;
   const int q = (psize + kRsW - 1) / kRsW, j0 = wave * q, j1 = min(psize, j0 + q);
   float mx = 0.f;
-#pragma unroll 8
+#pragma unroll 32
   for (int j = j0; j < j1; ++j) mx = fmaxf(mx, fmaxf(a * E[static_cast<long long>(pool[j]) * sh.ldM] - c, 0.f));
   part[wave][lane] = mx;
   __syncthreads();
@@ -723,7 +723,7 @@ __global__ void __launch_bounds__(64 * kRsW) rowstat_kernel(Shape sh, Params pr,
   const float zmax = mu * inv;
   float den = 0.f;
   if (mu > 0.f)
-#pragma unroll 8
+#pragma unroll 32
     for (int j = j0; j < j1; ++j)
       den += __expf(fmaxf(a * E[static_cast<long long>(pool[j]) * sh.ldM] - c, 0.f) * inv - zmax);
   __syncthreads();
@@ -896,11 +896,12 @@ template <bool RES>
 __global__ void __launch_bounds__(256)
 select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   extern __shared__ float dyn[];
-  // LDS: b_m [ldM] | alpha_m [ldM] | selected flags [N, padded to 16 bytes] |
-  //      pool keys [N] (only when N exceeds the register top-k)
+  // LDS: b_m [ldM] | selected flags [N, padded to 16 bytes] | pool keys [N]
+  //      (only when N exceeds the register top-k); the row weights are read
+  //      from L2 beside the client values they scale, which keeps a block
+  //      small enough for two per CU on the document page
   float* bl = dyn;
-  float* al = dyn + sh.ldM;
-  unsigned char* taken = reinterpret_cast<unsigned char*>(dyn + 2 * sh.ldM);
+  unsigned char* taken = reinterpret_cast<unsigned char*>(dyn + sh.ldM);
   uint32_t* keys = reinterpret_cast<uint32_t*>(taken + ((sh.N + 15) & ~15));
   __shared__ int hist[768], scan[16], bc[2], failed;
   __shared__ int pool_s[64], chosen[64], bidx[64];
@@ -920,12 +921,10 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   const float* alpha_g = ws.alpha + p * ws.s_m;
   int* cnt = ws.cnt + p * ws.s_cnt;
   {
-    const float* alpha = ws.alpha + p * ws.s_m;
     const float* cov0 = ws.cov + p * ws.s_cov;
     for (int m = tid; m < sh.ldM; m += 256) {
       // coverage at the first round: zero, or the image seeds' b_m(S_0)
       bl[m] = sh.nseed > 0 ? cov0[m] : 0.f;
-      al[m] = alpha[m];
     }
   }
   {
@@ -1106,7 +1105,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       const int m = c * 64 + lane;
       const bool row_ok = m < sh.m;
       const int mc = row_ok ? m : 0;
-      const float a = row_ok ? al[mc] : 0.f;
+      const float a = row_ok ? alpha_g[mc] : 0.f;
       const float b = bl[mc];
       const int j0 = wave * 16;
       float v[16];
@@ -1224,7 +1223,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       for (int c = gw; c < nchunk; c += nwaves) {
         const int m = c * 64 + lane;
         const int mc = min(m, sh.m - 1);
-        const float a = al[mc];
+        const float a = alpha_g[mc];
         float cm = bl[mc];
         for (int k0 = 0; k0 < bsize; k0 += 16) {
           float v[16];
@@ -1291,7 +1290,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       for (int h = 0; h < 2; ++h) {
         const int m = m0 + h * 1024;
         if (m < sh.m) {
-          const float4 a = *reinterpret_cast<const float4*>(al + m);
+          const float4 a = *reinterpret_cast<const float4*>(alpha_g + m);
           float4 b = *reinterpret_cast<const float4*>(bl + m);
           b.x = fmaxf(b.x, a.x * c[h].x); b.y = fmaxf(b.y, a.y * c[h].y);
           b.z = fmaxf(b.z, a.z * c[h].z); b.w = fmaxf(b.w, a.w * c[h].w);
@@ -1440,7 +1439,7 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, con
     return hipGetLastError();
   }
   {
-    const size_t lds = 2 * static_cast<size_t>(sh.ldM) * sizeof(float) +
+    const size_t lds = static_cast<size_t>(sh.ldM) * sizeof(float) +
                        ((static_cast<size_t>(sh.N) + 15) & ~static_cast<size_t>(15)) +
                        (sh.N > 256 * 16 ? static_cast<size_t>(sh.N) * sizeof(uint32_t) : 0);
     int nblk = persistent_blocks(sh, lds, 0);
