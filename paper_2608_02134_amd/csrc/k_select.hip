@@ -797,8 +797,9 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, Se
 
 // ---------------------------------------------------------------------------
 // Persistent selection: every round of a small-pool call in one launch.  The
-// grid is nblk blocks per problem, sized to be co-resident; every block keeps
-// its own copy of the coverage b_m and of the row weights in LDS.  A round:
+// grid is nblk blocks per problem, sized to be co-resident (one block per CU,
+// two for the streamed kernel when it fits twice); every block keeps its own
+// copy of the coverage b_m in LDS and reads the row weights from L2.  A round:
 //   gains  - waves stream the client rows of unselected tokens (round robin
 //            over all waves of the problem) and publish u_i tagged with the
 //            round number
