@@ -51,8 +51,8 @@ CASES = {
     # logits kernels, with a query count that is not a multiple of 16
     "tiny_ranges": dict(name="tiny", grid=(1, 40, 40), t=7, k=200),
     # the benchmarked shapes at full size, in the launch configuration the
-    # benchmark times (document: 16 pool keys per thread; 16 images: 16 blocks
-    # per problem)
+    # benchmark times (document: 16 pool keys per thread; 16 images: 32
+    # blocks per problem, two per CU)
     "doc_full": dict(name="doc"),
     "batch16_full": dict(name="batch16"),
     "frames_full": dict(name="frames"),
