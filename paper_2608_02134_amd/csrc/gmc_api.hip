@@ -237,7 +237,7 @@ Plan make_plan(const gmc_config& c) {
   pl.s_img = k.N;
   pl.s_imgcnt = kMaxImages;
   pl.s_tu = 2LL * k.N;
-  pl.s_ts = 2 * 64 * cdiv(k.ldM, 64);
+  pl.s_ts = 2 * 64 * cdiv(k.ldM, 64) + 2 * 64;   // chunk partials, then the published pool
   pl.s_tc = 2LL * (k.ldM + kMaxPersist);
   // certificate buffers: rounds of the smallest batch size, at most
   // kCertMaxRounds

@@ -118,7 +118,7 @@ struct Ws {
   // persistent selection: values tagged with (round + 1) in the high word,
   // double-buffered by round parity; zeroed at the start of every call
   unsigned long long* tu; long long s_tu;  // tagged gains               [2][N]
-  unsigned long long* ts; long long s_ts;  // tagged score partials     [2][ceil(M/64)][64]
+  unsigned long long* ts; long long s_ts;  // tagged score partials [2][ceil(M/64)][64], then the pool [2][64]
   unsigned long long* tc; long long s_tc;  // tagged coverage + heartbeats [2][ldM + kMaxPersist]
   // diagnostics (certificate of the selection rounds, exported statistics);
   // the per-round buffers are indexed flat as (p * rounds + r) * row, so a
@@ -163,7 +163,7 @@ __device__ __forceinline__ void call_init_range(const Shape& sh, const Ws& ws, i
     ws.cov[p * ws.s_cov + m] = 0.f;
     if (m >= sh.m) ws.alpha[p * ws.s_m + m] = 0.f;
   }
-  for (int j = x0; j < 128 * ((sh.m + 63) / 64); j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
+  for (int j = x0; j < 128 * ((sh.m + 63) / 64) + 128; j += stride) ws.ts[p * ws.s_ts + j] = 0ull;
   for (int j = x0; j < 2 * (sh.ldM + kMaxPersist); j += stride) ws.tc[p * ws.s_tc + j] = 0ull;
   for (int j = x0; j < (sh.hg * sh.T + 15) / 16 * sh.hkv; j += stride) ws.lcnt[p * ws.s_lcnt + j] = 0;
   // written through: the bank stream raises its flag in these words; the

@@ -915,6 +915,12 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nwaves = nblk * 4, gw = blk * 4 + wave;
   const int nchunk = (sh.m + 63) / 64;
+  // the pool is needed by the blocks that own a row chunk (responsibilities)
+  // and by the last block (it records the batch); with one chunk per block
+  // the others skip it and take the pool's tokens, published by block 0,
+  // along with the chunk sums
+  const bool pool_here = nchunk > nblk || blk < nchunk || blk == nblk - 1;
+  const bool pool_pub = nchunk + 1 < nblk;
   const float* E = ws.E + p * ws.s_E;
   unsigned long long* tu = ws.tu + p * ws.s_tu;
   unsigned long long* ts = ws.ts + p * ws.s_ts;
@@ -1045,7 +1051,10 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       }
     }
 
-    // ---- the pool, identical in every block (waits for this round's gains)
+    // ---- the pool, identical in every block that needs it (waits for this
+    //      round's gains)
+    unsigned long long* tpr = ts + 128LL * nchunk + (r & 1) * 64;
+    if (pool_here) {
     if constexpr (RES) {
       if (sh.N <= 256 * 6)
         pool_regs<6>(sh, tur, tag, taken, psize, pool_s, hist, scan, cnt, &failed);
@@ -1093,6 +1102,9 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       __syncthreads();
       if (tid < 64) pool_s[tid] = pv;
       __syncthreads();
+    }
+    if (pool_pub && blk == 0 && tid < 64)
+      st_dev64(&tpr[tid], tag_value(tag, __int_as_float(pool_s[tid])));
     }
     if (blk == nblk - 1 && so.pool) {
       int32_t* tp = so.pool + (static_cast<long long>(p) * sh.rounds + r) * sh.pool_cap;
@@ -1159,6 +1171,9 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       const int per = (nchunk + 3) / 4;
       const int c_end = min(nchunk, (wave + 1) * per);
       float s = 0.f;
+      // blocks without the pool: its published tokens, loaded with the sums
+      unsigned long long pw = 0ull;
+      if (!pool_here && wave == 0) pw = ld_dev64(&tpr[lane]);
       for (int c0 = wave * per; c0 < c_end; c0 += 16) {
         unsigned long long w[16];
 #pragma unroll
@@ -1179,6 +1194,16 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
           if (c0 + q < c_end) s += value_of(w[q]);
       }
       rmu[wave][lane] = s;   // free: the responsibility loop ended with a barrier
+      if (!pool_here && wave == 0) {
+        // block 0 published the pool before its responsibilities, so the
+        // tokens are normally there once the sums are
+        for (int spin = 0; tag_of(pw) != tag && !failed; ++spin) {
+          if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
+          __builtin_amdgcn_s_sleep(1);
+          pw = ld_dev64(&tpr[lane]);
+        }
+        pool_s[lane] = __float_as_int(value_of(pw));
+      }
     }
     __syncthreads();
     if (wave == 0) {
