@@ -915,10 +915,10 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nwaves = nblk * 4, gw = blk * 4 + wave;
   const int nchunk = (sh.m + 63) / 64;
-  // the pool is needed by the blocks that own a row chunk (responsibilities)
-  // and by the last block (it records the batch); with one chunk per block
-  // the others skip it and take the pool's tokens, published by block 0,
-  // along with the chunk sums
+  // the pool and the chunk sums are needed by the blocks that own a row
+  // chunk (responsibilities, coverage) and by the last block (it records the
+  // batch); with one chunk per block the others skip both and wait only for
+  // the batch's tokens, which block 0 publishes after its pick
   const bool pool_here = nchunk > nblk || blk < nchunk || blk == nblk - 1;
   const bool pool_pub = nchunk + 1 < nblk;
   const float* E = ws.E + p * ws.s_E;
@@ -1053,6 +1053,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
 
     // ---- the pool, identical in every block that needs it (waits for this
     //      round's gains)
+    // the batch's tokens, published by block 0 for the blocks without the pool
     unsigned long long* tpr = ts + 128LL * nchunk + (r & 1) * 64;
     if (pool_here) {
     if constexpr (RES) {
@@ -1103,8 +1104,6 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       if (tid < 64) pool_s[tid] = pv;
       __syncthreads();
     }
-    if (pool_pub && blk == 0 && tid < 64)
-      st_dev64(&tpr[tid], tag_value(tag, __int_as_float(pool_s[tid])));
     }
     if (blk == nblk - 1 && so.pool) {
       int32_t* tp = so.pool + (static_cast<long long>(p) * sh.rounds + r) * sh.pool_cap;
@@ -1164,16 +1163,32 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       __syncthreads();   // rmu / rden_s are reused by the next chunk
     }
 
-    // ---- the batch, identical in every block: each wave waits for the
-    //      tagged sums of a quarter of the chunks (16 loads in flight) and
-    //      adds them in chunk order; the quarters are added in wave order
+    // ---- the batch, identical in every block with the pool: each wave waits
+    //      for the tagged sums of a quarter of the chunks (16 loads in
+    //      flight) and adds them in chunk order; the quarters are added in
+    //      wave order.  The other blocks wait for the batch's tokens alone.
+    if (!pool_here) {
+      // nothing left for these blocks in the last round
+      if (r + 1 == sh.rounds) break;
+      // they read nothing else of this round (the batch's slots are
+      // rewritten two rounds on, after every block's gains of that round),
+      // so their heartbeat goes out before the wait
+      if (tid == 0) st_dev64(&tc[(r & 1) * (sh.ldM + kMaxPersist) + sh.ldM + blk], tag_value(tag, 0.f));
+      if (tid < 16) {
+        unsigned long long bw = ld_dev64(&tpr[tid]);
+        for (int spin = 0; tag_of(bw) != tag && !failed; ++spin) {
+          if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
+          __builtin_amdgcn_s_sleep(1);
+          bw = ld_dev64(&tpr[tid]);
+        }
+        bidx[tid] = min(max(__float_as_int(value_of(bw)), 0), sh.N - 1);
+      }
+      __syncthreads();
+    } else {
     {
       const int per = (nchunk + 3) / 4;
       const int c_end = min(nchunk, (wave + 1) * per);
       float s = 0.f;
-      // blocks without the pool: its published tokens, loaded with the sums
-      unsigned long long pw = 0ull;
-      if (!pool_here && wave == 0) pw = ld_dev64(&tpr[lane]);
       for (int c0 = wave * per; c0 < c_end; c0 += 16) {
         unsigned long long w[16];
 #pragma unroll
@@ -1194,16 +1209,6 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
           if (c0 + q < c_end) s += value_of(w[q]);
       }
       rmu[wave][lane] = s;   // free: the responsibility loop ended with a barrier
-      if (!pool_here && wave == 0) {
-        // block 0 published the pool before its responsibilities, so the
-        // tokens are normally there once the sums are
-        for (int spin = 0; tag_of(pw) != tag && !failed; ++spin) {
-          if (spin == kSpinLimit) { mark_timeout(cnt, &failed); break; }
-          __builtin_amdgcn_s_sleep(1);
-          pw = ld_dev64(&tpr[lane]);
-        }
-        pool_s[lane] = __float_as_int(value_of(pw));
-      }
     }
     __syncthreads();
     if (wave == 0) {
@@ -1215,8 +1220,12 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
       wave_topb(bkeys, psize, bsize, chosen);
       __builtin_amdgcn_wave_barrier();
       if (lane < bsize) bidx[lane] = pool_s[chosen[lane]];
+      __builtin_amdgcn_wave_barrier();
+      if (pool_pub && blk == 0 && lane < 16)
+        st_dev64(&tpr[lane], tag_value(tag, __int_as_float(lane < bsize ? bidx[lane] : 0)));
     }
     __syncthreads();
+    }
     const bool last = r + 1 == sh.rounds;
     // the last block records the batch (and alone finishes the last round)
     if (blk == nblk - 1) commit_batch(sh, ws, p, r, bsize, selected, pool_s, chosen, so.batch);
@@ -1261,7 +1270,7 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
         if (m < sh.m) st_dev64(&tcr[m], tag_value(tag, cm));
       }
       // this block's heartbeat: it has read everything of earlier rounds
-      if (tid == 0) st_dev64(&tcr[sh.ldM + blk], tag_value(tag, 0.f));
+      if (pool_here && tid == 0) st_dev64(&tcr[sh.ldM + blk], tag_value(tag, 0.f));
       // ---- every block copies the refreshed coverage into LDS, waiting for
       //      the tags and for every block's heartbeat
       const int nst = sh.ldM + nblk;
