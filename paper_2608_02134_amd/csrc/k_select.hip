@@ -803,13 +803,16 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, Se
 //   gains  - waves stream the client rows of unselected tokens (round robin
 //            over all waves of the problem) and publish u_i tagged with the
 //            round number
-//   pool   - every block waits for the tagged gains and picks the same pool
-//            (identical inputs, deterministic top-k)
+//   pool   - every block that owns a row chunk (and the last block) waits
+//            for the tagged gains and picks the same pool (identical inputs,
+//            deterministic top-k)
 //   resp   - one block per 64-row chunk, its waves splitting the pool:
 //            responsibility softmax over the pool, per-chunk sums per pool
 //            token, published tagged
-//   batch  - every block waits for the tagged chunk sums, adds them in chunk
-//            order and picks the same batch; the last block records it
+//   batch  - those blocks wait for the tagged chunk sums, add them in chunk
+//            order and pick the same batch; the last block records it and
+//            block 0 publishes its tokens, which are all the other blocks
+//            wait for (with one chunk per block)
 //   cov    - one wave per 64-row chunk: b_m <- max(b_m, max_{j in batch}
 //            Cbar_mj), published tagged; every block waits for the tags and
 //            copies b into LDS
@@ -820,8 +823,10 @@ colsum_kernel(Shape sh, Ws ws, int round, int psize, int bsize, int sel_base, Se
 // Tagged values are double-buffered by round parity, so a buffer is rewritten
 // two rounds after the round that read it.  Along with its coverage rows each
 // block publishes a tagged heartbeat (after it has read everything of the
-// round except the coverage), and the coverage hand-off waits for every
-// block's heartbeat as well as for the rows.  A block therefore starts round
+// round except the coverage; a block without the pool reads only the batch's
+// tokens, whose slots are rewritten only after every block's gains two
+// rounds on, so it publishes first), and the coverage hand-off waits for
+// every block's heartbeat as well as for the rows.  A block therefore starts round
 // r + 1 only after every block has finished its reads of round r - 1 and
 // earlier, so no value is overwritten before all its readers are done; the
 // ordering rides on a poll that happens anyway, with no barrier and no
