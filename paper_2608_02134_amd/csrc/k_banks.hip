@@ -573,6 +573,86 @@ __global__ void __launch_bounds__(256) spatial_write_kernel(Shape sh, Params pr,
   }
 }
 
+// Spatial bank in one launch (up to kSpatialFusedN tokens per call, all
+// problems together): one block per landmark row, as in the landmark-side
+// kernel above, except that the extents of (h, w) are one four-value block
+// reduction, and that the block then writes its row's energies itself: one
+// 4-byte value per token row of the client matrix (zero for the tokens of
+// other images).  Beyond kSpatialFusedN tokens those scattered stores cost
+// more than the token-side kernel's contiguous rows and the second launch
+// it needs (measured: one 1296-token image 14.5 against 16.0 us, sixteen
+// of them 65 against 46 us).
+constexpr int kSpatialFusedN = 2048;
+
+__device__ __forceinline__ float sq_dist(float2 c, float ly, float lx) {
+  const float dy = c.x - ly, dx = c.y - lx;
+  return dy * dy + dx * dx;
+}
+
+__global__ void __launch_bounds__(256) spatial_bank_kernel(Shape sh, Params pr, Ws ws, const int32_t* pos3d) {
+  __shared__ float red[16];
+  __shared__ float4 ext4[4];
+  const int row = blockIdx.x, p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int L = sh.landmarks, L2 = L * L;
+  const int g = row / L2, lr = row % L2;
+  const float ly = (static_cast<float>(lr / L) + 0.5f) / L;
+  const float lx = (static_cast<float>(lr % L) + 0.5f) / L;
+  const int32_t* pos = pos3d + static_cast<long long>(p) * sh.N * 3;
+  const int* img = ws.img + p * ws.s_img;
+  const bool multi = sh.nimg > 1;
+  float hmin = INFINITY, hmax = -INFINITY, wmin = INFINITY, wmax = -INFINITY;
+  for (int i = tid; i < sh.N; i += 256) {
+    if (multi && img[i] != g) continue;
+    const float hh = static_cast<float>(pos[i * 3 + 1]), ww = static_cast<float>(pos[i * 3 + 2]);
+    hmin = fminf(hmin, hh); hmax = fmaxf(hmax, hh);
+    wmin = fminf(wmin, ww); wmax = fmaxf(wmax, ww);
+  }
+  hmin = wave_min(hmin); hmax = wave_max(hmax);
+  wmin = wave_min(wmin); wmax = wave_max(wmax);
+  if (lane == 0) ext4[wave] = make_float4(hmin, hmax, wmin, wmax);
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float4 e = ext4[w];
+    hmin = fminf(hmin, e.x); hmax = fmaxf(hmax, e.y);
+    wmin = fminf(wmin, e.z); wmax = fmaxf(wmax, e.w);
+  }
+  const float gh = hmax - hmin + 1.f, gw = wmax - wmin + 1.f;
+  float* pc = ws.pc + p * ws.s_pc;
+  float dmin = INFINITY;
+  for (int i = tid; i < sh.N; i += 256) {
+    if (multi && img[i] != g) continue;
+    const float2 c = cell_centre(pos, i, hmin, wmin, gh, gw);
+    dmin = fminf(dmin, sq_dist(c, ly, lx));
+    if (lr == 0) {
+      pc[2 * i] = c.x;
+      pc[2 * i + 1] = c.y;
+    }
+  }
+  dmin = block_min(dmin, red);
+  const float inv_tau = 1.f / pr.tau_s;
+  float s = 0.f;
+  for (int i = tid; i < sh.N; i += 256) {
+    if (multi && img[i] != g) continue;
+    s += expf(-(sq_dist(cell_centre(pos, i, hmin, wmin, gh, gw), ly, lx) - dmin) * inv_tau);
+  }
+  s = block_sum(s, red);
+  if (tid == 0) {
+    const int m = sh.mg + sh.mv + row;
+    // an image without tokens (reported by the input status bit) keeps an
+    // inert row
+    const float a = s > 0.f ? pr.beta_spa / static_cast<float>(sh.ms) / s : 0.f;
+    ws.alpha[p * ws.s_m + m] = a;
+    ws.peak[p * ws.s_m + m] = a;
+  }
+  float* E = ws.E + p * ws.s_E + sh.mg + sh.mv + row;
+  for (int i = tid; i < sh.N; i += 256) {
+    const bool own = !multi || img[i] == g;
+    const float d2 = own ? sq_dist(cell_centre(pos, i, hmin, wmin, gh, gw), ly, lx) : 0.f;
+    E[static_cast<long long>(i) * sh.ldM] = own ? expf(-(d2 - dmin) * inv_tau) : 0.f;
+  }
+}
+
 template <typename T>
 static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, const void* hidden_v,
                              const void* proj_v, const int32_t* pos3d, hipStream_t st) {
@@ -580,8 +660,12 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
   hipError_t err;
   auto spatial = [&]() {
     timer_mark(kStSpatial, true, st);
-    hipLaunchKernelGGL(spatial_stats_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws, pos3d);
-    hipLaunchKernelGGL(spatial_write_kernel, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws);
+    if (static_cast<long long>(sh.N) * sh.B <= kSpatialFusedN) {
+      hipLaunchKernelGGL(spatial_bank_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws, pos3d);
+    } else {
+      hipLaunchKernelGGL(spatial_stats_kernel, dim3(sh.ms, sh.B), dim3(256), 0, st, sh, pr, ws, pos3d);
+      hipLaunchKernelGGL(spatial_write_kernel, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws);
+    }
     timer_mark(kStSpatial, false, st);
   };
   // up to 2048 tokens the light spatial kernels go first, so that the Gram,
