@@ -466,21 +466,32 @@ __global__ void clients_kernel(Shape sh, Ws ws) {
 }
 
 // Appearance row weights alpha = (beta_app / M_V) / Z_m and peaks.
+// 64 client rows per block (lane = row); wave w adds the column blocks
+// [w nb/4, (w+1) nb/4) in order, then the four partial sums are added in
+// wave order.
 __global__ void __launch_bounds__(256) appearance_alpha_kernel(Shape sh, Params pr, Ws ws) {
-  const int p = blockIdx.y;
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= sh.mv) return;
+  __shared__ float ps4[4][64], pm4[4][64];
+  const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = blockIdx.x * 64 + lane, rc = min(r, sh.mv - 1);
   const float* ps = ws.apart_sum + p * ws.s_apart;
   const float* pm = ws.apart_max + p * ws.s_apart;
+  const int per = (sh.n_app_cblk + 3) / 4, b0 = wave * per, b1 = min(sh.n_app_cblk, b0 + per);
   float s = 0.f, m = 0.f;
 #pragma unroll 8
-  for (int b = 0; b < sh.n_app_cblk; ++b) {
-    s += ps[static_cast<long long>(b) * sh.mv + r];
-    m = fmaxf(m, pm[static_cast<long long>(b) * sh.mv + r]);
+  for (int b = b0; b < b1; ++b) {
+    s += ps[static_cast<long long>(b) * sh.mv + rc];
+    m = fmaxf(m, pm[static_cast<long long>(b) * sh.mv + rc]);
   }
-  const float a = pr.beta_app / static_cast<float>(sh.mv) / s;
-  ws.alpha[p * ws.s_m + sh.mg + r] = a;
-  ws.peak[p * ws.s_m + sh.mg + r] = a * m;
+  ps4[wave][lane] = s;
+  pm4[wave][lane] = m;
+  __syncthreads();
+  if (wave == 0 && r < sh.mv) {
+    s = ((ps4[0][lane] + ps4[1][lane]) + ps4[2][lane]) + ps4[3][lane];
+    m = fmaxf(fmaxf(pm4[0][lane], pm4[1][lane]), fmaxf(pm4[2][lane], pm4[3][lane]));
+    const float a = pr.beta_app / static_cast<float>(sh.mv) / s;
+    ws.alpha[p * ws.s_m + sh.mg + r] = a;
+    ws.peak[p * ws.s_m + sh.mg + r] = a * m;
+  }
 }
 
 // Spatial bank, landmark side: one block per landmark l_ab = ((a+.5)/L,
@@ -498,7 +509,8 @@ __device__ __forceinline__ float2 cell_centre(const int32_t* pos, int i, float h
 
 __global__ void __launch_bounds__(256) spatial_stats_kernel(Shape sh, Params pr, Ws ws, const int32_t* pos3d) {
   __shared__ float red[16];
-  const int row = blockIdx.x, p = blockIdx.y;
+  __shared__ float4 ext4[4];
+  const int row = blockIdx.x, p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = sh.landmarks, L2 = L * L;
   const int g = row / L2, lr = row % L2;
   const float ly = (static_cast<float>(lr / L) + 0.5f) / L;
@@ -506,41 +518,50 @@ __global__ void __launch_bounds__(256) spatial_stats_kernel(Shape sh, Params pr,
   const int32_t* pos = pos3d + static_cast<long long>(p) * sh.N * 3;
   const int* img = ws.img + p * ws.s_img;
   const bool multi = sh.nimg > 1;
+  // the image's extents: one four-value block reduction
   float hmin = INFINITY, hmax = -INFINITY, wmin = INFINITY, wmax = -INFINITY;
-  for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
+  for (int i = tid; i < sh.N; i += blockDim.x) {
     if (multi && img[i] != g) continue;
     const float hh = static_cast<float>(pos[i * 3 + 1]), ww = static_cast<float>(pos[i * 3 + 2]);
     hmin = fminf(hmin, hh); hmax = fmaxf(hmax, hh);
     wmin = fminf(wmin, ww); wmax = fmaxf(wmax, ww);
   }
-  hmin = block_min(hmin, red);
-  hmax = block_max(hmax, red);
-  wmin = block_min(wmin, red);
-  wmax = block_max(wmax, red);
-  const float gh = hmax - hmin + 1.f, gw = wmax - wmin + 1.f;
-  float dmin = INFINITY;
-  for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
-    if (multi && img[i] != g) continue;
-    const float2 c = cell_centre(pos, i, hmin, wmin, gh, gw);
-    const float dy = c.x - ly, dx = c.y - lx;
-    dmin = fminf(dmin, dy * dy + dx * dx);
+  hmin = wave_min(hmin); hmax = wave_max(hmax);
+  wmin = wave_min(wmin); wmax = wave_max(wmax);
+  if (lane == 0) ext4[wave] = make_float4(hmin, hmax, wmin, wmax);
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float4 e = ext4[w];
+    hmin = fminf(hmin, e.x); hmax = fmaxf(hmax, e.y);
+    wmin = fminf(wmin, e.z); wmax = fmaxf(wmax, e.w);
   }
-  dmin = block_min(dmin, red);
+  const float gh = hmax - hmin + 1.f, gw = wmax - wmin + 1.f;
+  // one pass for the minimum and the row sum: each thread keeps its own
+  // running minimum m and the sum of exp(-(d^2 - m)/tau_s) relative to it
+  // (rescaled when m drops); the sums are then brought to the block minimum
   const float inv_tau = 1.f / pr.tau_s;
-  float s = 0.f;
   float* pc = ws.pc + p * ws.s_pc;
-  for (int i = threadIdx.x; i < sh.N; i += blockDim.x) {
+  float mt = INFINITY, st = 0.f;
+  for (int i = tid; i < sh.N; i += blockDim.x) {
     if (multi && img[i] != g) continue;
     const float2 c = cell_centre(pos, i, hmin, wmin, gh, gw);
     const float dy = c.x - ly, dx = c.y - lx;
-    s += expf(-(dy * dy + dx * dx - dmin) * inv_tau);
+    const float d2 = dy * dy + dx * dx;
+    if (d2 < mt) {
+      st = (mt == INFINITY ? 0.f : st * expf(-(mt - d2) * inv_tau)) + 1.f;
+      mt = d2;
+    } else {
+      st += expf(-(d2 - mt) * inv_tau);
+    }
     if (lr == 0) {
       pc[2 * i] = c.x;
       pc[2 * i + 1] = c.y;
     }
   }
-  s = block_sum(s, red);
-  if (threadIdx.x == 0) {
+  const float dmin = block_min(mt, red);
+  const float s = block_sum(mt == INFINITY ? 0.f : st * expf(-(mt - dmin) * inv_tau), red);
+  if (tid == 0) {
     const int m = sh.mg + sh.mv + row;
     // an image without tokens (reported by the input status bit) keeps an
     // inert row
@@ -574,11 +595,10 @@ __global__ void __launch_bounds__(256) spatial_write_kernel(Shape sh, Params pr,
 }
 
 // Spatial bank in one launch (up to kSpatialFusedN tokens per call, all
-// problems together): one block per landmark row, as in the landmark-side
-// kernel above, except that the extents of (h, w) are one four-value block
-// reduction, and that the block then writes its row's energies itself: one
-// 4-byte value per token row of the client matrix (zero for the tokens of
-// other images).  Beyond kSpatialFusedN tokens those scattered stores cost
+// problems together): one block per landmark row with the landmark-side
+// kernel's statistics (the minimum and the row sum in two passes here), and
+// the block then writes its row's energies itself: one 4-byte value per
+// token row of the client matrix (zero for the tokens of other images).  Beyond kSpatialFusedN tokens those scattered stores cost
 // more than the token-side kernel's contiguous rows and the second launch
 // it needs (measured: one 1296-token image 14.5 against 16.0 us, sixteen
 // of them 65 against 46 us).
@@ -716,7 +736,7 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
     err = launch_gemm_nt<float, 64, 64>(Yc, Y, sh.app_rank, sh.B, epi, st);
     if (err != hipSuccess) return err;
   }
-  hipLaunchKernelGGL(appearance_alpha_kernel, dim3((sh.mv + 255) / 256, sh.B), dim3(256), 0, st, sh, pr, ws);
+  hipLaunchKernelGGL(appearance_alpha_kernel, dim3((sh.mv + 63) / 64, sh.B), dim3(256), 0, st, sh, pr, ws);
   timer_mark(kStAppearance, false, st);
   if (!spatial_first) spatial();
   return hipGetLastError();
