@@ -204,7 +204,7 @@ Plan make_plan(const gmc_config& c) {
   pl.s_ell = static_cast<long long>(k.hq) * k.N;
   pl.s_E = static_cast<long long>(k.N) * k.ldM;
   pl.s_m = k.ldM;
-  pl.s_apart = cdiv(k.N, 64) * k.mv;
+  pl.s_apart = cdiv(k.N, k.bounded_possible ? kAppBoundedTile : 64) * k.mv;
   pl.s_gpart1 = std::max(cdiv(k.N, kHeadTok) * round_up(npairs, 4), cdiv(k.N, 64) * k.hq);
   pl.s_gpart = (1 + c.max_hist_views) * pl.s_gpart1;
   pl.s_n2h = c.max_hist_views > 0 ? k.N : 1;
@@ -627,7 +627,9 @@ int resolve_shape(const gmc_config& g, const Limits& cap, int64_t B, int64_t N, 
   s.pool_cap = g.pool_mult * s.b;
   s.rounds = (K < N) ? static_cast<int>(cdiv(K - s.nseed, s.b)) : 0;
   s.ldK = static_cast<int>(round_up(K, 4));
-  s.n_app_cblk = static_cast<int>(cdiv(N, 64));
+  // column blocks of the appearance row statistics: 64-token tiles of the
+  // exact Gram, smaller tiles of the bounded bank's GEMM
+  s.n_app_cblk = static_cast<int>(cdiv(N, s.bounded ? kAppBoundedTile : 64));
   s.n_head_blk = static_cast<int>(cdiv(N, kHeadTok));
   {
     // split the logit columns until about two blocks per CU of a 256-CU part

@@ -35,6 +35,7 @@ constexpr int kMaxPersist = 256;  // blocks per problem of the persistent select
 constexpr int kMaxGather = 64;    // tensors per row-gather launch (GMC_MAX_GATHER_TENSORS)
 constexpr int kLogitSplit = 16;   // column ranges of the message-logit kernels (at most)
 constexpr int kProbeSplit = 4;    // K splits of the value-probe GEMM (d a multiple of 256)
+constexpr int kAppBoundedTile = 32;   // tile of the bounded appearance GEMM (fp32 operands, rank-long)
 
 // Call shape, resolved on the host for one gmc_prune call.
 struct Shape {

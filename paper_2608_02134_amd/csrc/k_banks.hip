@@ -733,7 +733,9 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
     RowOperand<float> Yc{ws.y, sh.app_rank, ws.s_y, ws.clients, ws.s_cl, sh.mv};
     RowOperand<float> Y{ws.y, sh.app_rank, ws.s_y, nullptr, 0, sh.N};
     AppearanceEpi epi{ws, sh.ldM, sh.mg, 0, 1.f / pr.tau_v, pr.norm_eps, sh.n_app_cblk, sh.mv};
-    err = launch_gemm_nt<float, 64, 64>(Yc, Y, sh.app_rank, sh.B, epi, st);
+    // small tiles: a rank-long contraction per tile, so four blocks per CU
+    // (LDS) overlap their loads, MFMAs and exponential epilogues
+    err = launch_gemm_nt<float, kAppBoundedTile, kAppBoundedTile>(Yc, Y, sh.app_rank, sh.B, epi, st);
     if (err != hipSuccess) return err;
   }
   hipLaunchKernelGGL(appearance_alpha_kernel, dim3((sh.mv + 63) / 64, sh.B), dim3(256), 0, st, sh, pr, ws);
