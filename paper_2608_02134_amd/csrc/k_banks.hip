@@ -445,9 +445,13 @@ struct ProjEpi {
   __device__ void row_stats(int, int, int, float, float) const {}
 };
 
-// Normalise projected rows: one wave per token.
+// Normalise projected rows: one wave per token.  The same grid (N / 4
+// blocks of 256 threads, N >= M_V) also lists the bounded bank's client
+// tokens m_k = floor(k N / M_V).
 __global__ void __launch_bounds__(256) normalize_rows_kernel(Shape sh, Params pr, Ws ws) {
   const int p = blockIdx.y, i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k < sh.mv) ws.clients[p * ws.s_cl + k] = static_cast<int>((static_cast<long long>(k) * sh.N) / sh.mv);
   if (i >= sh.N) return;
   float* y = ws.y + p * ws.s_y + static_cast<long long>(i) * sh.app_rank;
   float s = 0.f;
@@ -455,14 +459,6 @@ __global__ void __launch_bounds__(256) normalize_rows_kernel(Shape sh, Params pr
   s = wave_sum(s);
   const float inv = 1.f / fmaxf(sqrtf(s), pr.norm_eps);
   for (int c = lane; c < sh.app_rank; c += 64) y[c] *= inv;
-}
-
-// Client tokens m_k = floor(k N / M_V) of the bounded bank.
-__global__ void clients_kernel(Shape sh, Ws ws) {
-  const int p = blockIdx.y;
-  for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < sh.mv; k += gridDim.x * blockDim.x)
-    ws.clients[p * ws.s_cl + k] =
-        static_cast<int>((static_cast<long long>(k) * sh.N) / sh.mv);
 }
 
 // Appearance row weights alpha = (beta_app / M_V) / Z_m and peaks.
@@ -729,7 +725,6 @@ static hipError_t banks_impl(const Shape& sh, const Params& pr, const Ws& ws, co
     err = launch_gemm_nt<T, 64, 64>(A, R, sh.d, sh.B, pe, st);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(normalize_rows_kernel, dim3((sh.N + 3) / 4, sh.B), dim3(256), 0, st, sh, pr, ws);
-    hipLaunchKernelGGL(clients_kernel, dim3((sh.mv + 255) / 256, sh.B), dim3(256), 0, st, sh, ws);
     RowOperand<float> Yc{ws.y, sh.app_rank, ws.s_y, ws.clients, ws.s_cl, sh.mv};
     RowOperand<float> Y{ws.y, sh.app_rank, ws.s_y, nullptr, 0, sh.N};
     AppearanceEpi epi{ws, sh.ldM, sh.mg, 0, 1.f / pr.tau_v, pr.norm_eps, sh.n_app_cblk, sh.mv};
