@@ -900,7 +900,7 @@ __device__ __forceinline__ int opaque_uniform(int v) {
 constexpr int kResJ = 14;
 template <bool RES>
 __global__ void __launch_bounds__(256)
-select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
+select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so, int quad) {
   extern __shared__ float dyn[];
   // LDS: b_m [ldM] | selected flags [N, padded to 16 bytes] | pool keys [N]
   //      (only when N exceeds the register top-k); the row weights are read
@@ -1015,6 +1015,57 @@ select_persistent_kernel(Shape sh, Params pr, Ws ws, int nblk, SelOut so) {
         if (t < sh.N && !taken[t]) st_dev64(&tur[t], tag_value(tag, g));
         if (so.gains && t < sh.N)
           so.gains[(static_cast<long long>(p) * sh.rounds + r) * sh.N + t] = taken[t] ? 0.f : g;
+      }
+    } else if (quad) {
+      // one block per CU: four tokens per wave pass, all their row loads in
+      // flight together (each token's sum is formed exactly as in the
+      // two-token loop below)
+      for (int i0 = gw; i0 < sh.N; i0 += 4 * nwaves) {
+        int it[4];
+        bool ok[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          it[k] = i0 + k * nwaves;
+          ok[k] = it[k] < sh.N && taken[min(it[k], sh.N - 1)] == 0;
+        }
+        float* gout = so.gains ? so.gains + (static_cast<long long>(p) * sh.rounds + r) * sh.N : nullptr;
+        if (!(ok[0] || ok[1] || ok[2] || ok[3])) {
+          if (gout && lane == 0)
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+              if (it[k] < sh.N) gout[it[k]] = 0.f;
+          continue;
+        }
+        // a token that needs no gain re-reads a needed one's row (cache hits)
+        const int any = ok[0] ? it[0] : ok[1] ? it[1] : ok[2] ? it[2] : it[3];
+        const float* c[4];
+        float acc[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          c[k] = E + static_cast<long long>(ok[k] ? it[k] : any) * sh.ldM;
+          acc[k] = 0.f;
+        }
+#pragma unroll 4
+        for (int m = lane * 4; m < sh.m; m += 256) {
+          const float4 a = *reinterpret_cast<const float4*>(alpha_g + m);
+          const float4 b = *reinterpret_cast<const float4*>(bl + m);
+          float4 v[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = *reinterpret_cast<const float4*>(c[k] + m);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            acc[k] += fmaxf(a.x * v[k].x - b.x, 0.f); acc[k] += fmaxf(a.y * v[k].y - b.y, 0.f);
+            acc[k] += fmaxf(a.z * v[k].z - b.z, 0.f); acc[k] += fmaxf(a.w * v[k].w - b.w, 0.f);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[k] = wave_sum(acc[k]);
+        if (lane == 0)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (ok[k]) st_dev64(&tur[it[k]], tag_value(tag, acc[k]));
+            if (gout && it[k] < sh.N) gout[it[k]] = ok[k] ? acc[k] : 0.f;
+          }
       }
     } else
     for (int i0 = gw; i0 < sh.N; i0 += 2 * nwaves) {
@@ -1437,8 +1488,11 @@ static const void* persistent_fn(int res) {
              : reinterpret_cast<const void*>(select_persistent_kernel<false>);
 }
 
+static int g_n_cu = -1;   // compute units of the current device (0: unknown)
+
 static int persistent_blocks(const Shape& sh, size_t lds, int res) {
-  static int n_cu = -1, lds_max = 0, lds_set[2] = {64 * 1024, 64 * 1024};
+  static int lds_max = 0, lds_set[2] = {64 * 1024, 64 * 1024};
+  int& n_cu = g_n_cu;
   if (n_cu < 0) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -1489,12 +1543,16 @@ hipError_t launch_selection(const Shape& sh, const Params& pr, const Ws& ws, con
                           persistent_blocks(sh, lds, 1) == nblk;
     if (nblk > 0) {
       timer_mark(kStSelect, true, st);
+      // the streamed gains take four tokens per wave pass when the grid has
+      // one block per CU (registers to spare); with two per CU the two-token
+      // loop measured faster
+      const int quad = !resident && g_n_cu > 0 && nblk * sh.B <= g_n_cu;
       if (resident)
         hipLaunchKernelGGL(select_persistent_kernel<true>, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws,
-                           nblk, so);
+                           nblk, so, 0);
       else
         hipLaunchKernelGGL(select_persistent_kernel<false>, dim3(nblk, sh.B), dim3(256), lds, st, sh, pr, ws, nblk,
-                           so);
+                           so, quad);
       timer_mark(kStSelect, false, st);
       *support_ready = true;
       return hipGetLastError();
