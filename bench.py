@@ -236,7 +236,7 @@ def main():
         roofline["traffic_gbs"] = traffic / avg_s / 1e9
         roofline["traffic_over_work"] = traffic / work
         roofline["regime"] = ("latency: operands cache-resident, measured traffic well below the algorithmic bytes"
-                              if traffic < 0.5 * work else "bandwidth: operands streamed from HBM")
+                              if traffic < 0.5 * work else "bandwidth: operands streamed past the L2 caches every round")
 
     cpu = None
     if args.cpu_seconds > 0:
